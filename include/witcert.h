@@ -1,0 +1,204 @@
+/*
+ * witcert.h -- C-ABI of the WitCert hot path on MI355X (gfx950).
+ *
+ * WitCert meters, per (layer, head, decode step), a sound upper bound on the
+ * total variation between exact and compressed softmax attention (paper:
+ * "WitCert: Sound Runtime Risk Observability and Gating for KV-Cache
+ * Quantization").  This library implements the meter loop of Sec. 6:
+ *
+ *   write path  wc_quantize_write   dithered INT8 (Sec. 4.2) or raw fp8 cast,
+ *                                   plus the residual witness (Sec. 4.1, Eq. witness)
+ *               wc_witness          witness of any cache-preserving scheme (Sec. 4.1)
+ *   read path   wc_metered_decode_attention
+ *                                   GQA decode attention over the compressed cache
+ *                                   fused with the Tier-A meter (Theorem black-box
+ *                                   logit bound + Theorem sound replacement), split
+ *                                   over the KV axis and merged under the softmax
+ *                                   LSE weights (Sec. 6.2, SGLang decode kernel)
+ *   gate        wc_gate             meter (raw score when tau >= 1) > tau, routed per
+ *                                   KV head by any-of-G (Sec. 4.3, Sec. 5)
+ *               wc_exact_decode_attention
+ *                                   exact attention from an uncompressed bf16 cache for
+ *                                   the routed heads (the fallback of the meter loop)
+ *
+ * Conventions shared by every entry point
+ *   - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *     never allocates, frees, synchronizes or reads results back.  Scratch
+ *     memory is a caller-provided workspace sized by wc_decode_workspace_size.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *     returns immediately; results are valid once the stream reaches them.
+ *     Every call is safe to capture in a HIP graph (no host synchronization,
+ *     no memset nodes).
+ *   - Return value: WC_OK (0) or a negative WC_E* code; nothing is enqueued
+ *     when an argument check fails.  wc_strerror names the codes.  No C++
+ *     exception crosses this boundary.  The library keeps no state and is
+ *     thread-safe.
+ *   - Pointers must be 16-byte aligned; shapes are row-major, innermost last.
+ *   - Preconditions not checked on the device: finite inputs, |x| <= 8.28e6
+ *     (keeps fp16 scales finite), |x| <= 448 for the fp8 cache, |q| < 65504,
+ *     block-table entries < num_blocks, slots < num_blocks * 16, every
+ *     seq_lens[b] <= max_seq_len and <= max_blocks_per_seq * 16.
+ */
+#ifndef WITCERT_H
+#define WITCERT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------- */
+#define WC_OK              0
+#define WC_EINVAL         -1   /* null/misaligned pointer, bad shape or enum    */
+#define WC_EUNSUPPORTED   -2   /* valid but not built (e.g. head_dim 96)        */
+#define WC_EHIP           -3   /* the HIP runtime rejected a launch             */
+#define WC_EWORKSPACE     -4   /* workspace smaller than wc_decode_workspace_size */
+
+/* ---- element types ---------------------------------------------------- */
+#define WC_F32   0
+#define WC_BF16  1
+#define WC_F16   2
+
+/* ---- cache kinds ------------------------------------------------------ */
+#define WC_KIND_INT8_DITHER  0   /* int8 codes + fp16 per-token scales + fp16 key witness */
+#define WC_KIND_FP8_RAW      1   /* fp8 E4M3 raw cast (no scale) + fp16 key witness       */
+#define WC_KIND_BF16         2   /* uncompressed bf16 (the exact fallback cache)          */
+
+/* ---- RoPE pair layouts (they decide the band map) ---------------------- */
+#define WC_ROPE_HALF         0   /* pair j = channels (j, j + d/2)  (rotate-half)  */
+#define WC_ROPE_INTERLEAVED  1   /* pair j = channels (2j, 2j + 1)                 */
+
+#define WC_BLOCK_TOKENS 16       /* tokens per paged block */
+
+/*
+ * One layer's paged cache.  Slot s lives in block s/16 at offset s%16.
+ * Memory layout (elements; sizes from wc_cache_bytes):
+ *   k_data     [num_blocks][n_kv_heads][16][head_dim]         token-major
+ *   v_data     [num_blocks][n_kv_heads][4][head_dim][4]       token quads, channel-major
+ *              (token o of a block, channel c -> ((o/4)*head_dim + c)*4 + o%4)
+ *   k_scale,
+ *   v_scale    [num_blocks][n_kv_heads][16] fp16              INT8_DITHER only, else NULL
+ *   k_witness  [num_blocks][n_kv_heads][16][n_bands] fp16     NULL for BF16
+ * Element type of k_data/v_data: int8 (INT8_DITHER), E4M3 byte (FP8_RAW), bf16 (BF16).
+ * Band b holds the channels of RoPE pairs b*P .. b*P+P-1, P = head_dim/(2*n_bands)
+ * (Sec. 4.1; Lemma RoPE band unitarity).  `seed` keys the Philox dither; `layer`
+ * enters its counter (Sec. 6.2: counter (layer, kv_head, slot, channel)).
+ */
+typedef struct wc_cache {
+    int32_t  kind;          /* WC_KIND_*                                       */
+    int32_t  head_dim;      /* 64 or 128                                       */
+    int32_t  n_kv_heads;    /* 1 .. 65535                                      */
+    int32_t  n_bands;       /* B, head_dim % (2*B) == 0, 1 <= B <= 16           */
+    int32_t  rope_layout;   /* WC_ROPE_*                                       */
+    int32_t  layer;         /* 0 .. 65535, Philox counter field                */
+    int64_t  num_blocks;    /* pages of 16 slots                               */
+    uint64_t seed;          /* Philox4x32-10 key (low word = key[0])           */
+    void *k_data, *v_data, *k_scale, *v_scale, *k_witness;
+} wc_cache;
+
+const char* wc_strerror(int status);
+int         wc_version(void);   /* 100*major + minor */
+
+/*
+ * Bytes of each array of a cache (k_data, v_data, k_scale, v_scale, k_witness)
+ * written to sizes[0..4]; returns their sum, 0 on bad arguments.  The "exact
+ * byte account" of the cache (Sec. 5 memory saving; Sec. 6.2 acceptance).
+ */
+size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim,
+                      int n_bands, size_t sizes[5]);
+
+/*
+ * Write path (Sec. 4.2 subtractive dither; Sec. 6.2 research kernels and storage
+ * side; Sec. 4.1 Eq. witness).  For every token i < n_tok and KV head h:
+ *   INT8_DITHER: s = fp16_round_up(fl32(amax/126.5)) per (token, head, tensor);
+ *                xi_c = (u_c - 127.5)/256 with u_c the Philox4x32-10 byte of channel c
+ *                (key = seed, counter = (c/16, slot lo, slot hi, layer<<16 | h)),
+ *                shared by K and V; code = rint_even(fl32(fl32(x*fl32(1/s)) + xi));
+ *   FP8_RAW:     code = E4M3(x), nearest-even, saturating at +-448;
+ *   BF16:        x rounded to bf16 (nearest-even);
+ * and, except for BF16, the key witness w_b = ||(khat - k)_b|| rounded up to fp16
+ * (computed in fp32, enlarged by 2^-18 relative before rounding, so it never falls
+ * below the exact norm).
+ *   k, v          [n_tok][n_kv_heads][head_dim], in_dtype WC_F32 or WC_BF16 (post-RoPE keys)
+ *   slot_mapping  [n_tok] int64 device; slot < 0 skips the token
+ */
+int wc_quantize_write(const wc_cache* cache, const void* k, const void* v, int in_dtype,
+                      const int64_t* slot_mapping, int64_t n_tok, void* stream);
+
+/*
+ * Black-box witness (Sec. 4.1, Tier A scope: any scheme that writes back a
+ * per-token reconstruction): w[i][b] = fp16_round_up(||(xhat_i - x_i)_b||).
+ *   x, xhat  [n_vec][head_dim] in x_dtype / xhat_dtype (WC_F32, WC_BF16 or WC_F16)
+ *   w_out    [n_vec][n_bands] fp16 bits
+ */
+int wc_witness(const void* x, int x_dtype, const void* xhat, int xhat_dtype, int64_t n_vec,
+               int head_dim, int n_bands, int rope_layout, uint16_t* w_out, void* stream);
+
+/*
+ * Workspace bytes needed by wc_metered_decode_attention / wc_exact_decode_attention
+ * for these sizes.  split_tokens as passed to the decode call (0 = library choice).
+ */
+size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
+                                int64_t max_seq_len, int split_tokens);
+
+/*
+ * Metered decode attention (the read path of the meter loop, Sec. 6).  For each
+ * sequence b and query head h (KV head h / (n_q_heads / n_kv_heads)), over the
+ * seq_lens[b] tokens whose slots are block_table[b][t/16]*16 + t%16:
+ *   khat_t, vhat_t  reconstructions (INT8: s*(code - xi), xi regenerated from the slot)
+ *   ptilde         = softmax(sm_scale * q . khat_t)
+ *   out[b][h]      = sum_t ptilde_t vhat_t
+ *   c_t            = sm_scale * sum_b ||q_b|| w_{t,b}      (Theorem black-box logit bound)
+ *   A - 1          = sum_t ptilde_t (e^{c_t} - 1)            (Theorem sound replacement)
+ *   raw[b][h]      = (A - 1)(A + 1)/2, +inf on overflow
+ *   meter[b][h]    = min(1, raw)                             (Sec. 4.3)
+ * The KV axis is split into chunks whose partial (max, sum, A-1 numerator, output)
+ * are merged under the LSE weights; A merges exactly like the output (Sec. 6.2).
+ *   q            [batch][n_q_heads][head_dim], q_dtype WC_F32 or WC_BF16
+ *   block_table  [batch][max_blocks_per_seq] int32;  seq_lens [batch] int32 (>= 0)
+ *   max_seq_len  host-side upper bound of seq_lens (sizes the split grid)
+ *   out          [batch][n_q_heads][head_dim], out_dtype WC_F32 or WC_BF16
+ *   meter, raw   [batch][n_q_heads] fp32 (raw may be NULL)
+ *   split_tokens tokens per KV split, multiple of 64 (0 = library choice)
+ *   ws           workspace of ws_bytes >= wc_decode_workspace_size(...)
+ * A sequence with seq_lens[b] == 0 gets out = 0, meter = raw = 0.
+ * cache->kind must be INT8_DITHER or FP8_RAW.
+ */
+int wc_metered_decode_attention(const wc_cache* cache, const void* q, int q_dtype, int batch,
+                                int n_q_heads, const int32_t* block_table,
+                                int max_blocks_per_seq, const int32_t* seq_lens,
+                                int64_t max_seq_len, float sm_scale, void* out, int out_dtype,
+                                float* meter, float* raw, int split_tokens, void* ws,
+                                size_t ws_bytes, void* stream);
+
+/*
+ * Gate (the meter loop's gate, Sec. 6; certified vs risk-ranked, Sec. 4.3):
+ *   mask_q[b][h]   = (tau < 1 ? meter : raw)[b][h] > tau      (strict)
+ *   mask_kv[b][g]  = OR over the `group` query heads of KV head g (any-of-G, Sec. 5)
+ *   n_gated[0] += number of set mask_q, n_gated[1] += number of set mask_kv
+ *                  (device int32[2], may be NULL; the caller zeroes it)
+ * raw may be NULL when tau < 1.
+ */
+int wc_gate(const float* meter, const float* raw, int batch, int n_q_heads, int group,
+            float tau, uint8_t* mask_q, uint8_t* mask_kv, int32_t* n_gated, void* stream);
+
+/*
+ * Exact fallback (the meter loop: a gated head is served from the exact store).
+ * For every (b, g) with mask_kv[b][g] != 0, overwrites out[b][h] for the G query
+ * heads h of KV head g with softmax(sm_scale * q . k_t) v over the bf16 cache
+ * `exact` (kind WC_KIND_BF16); other rows of `out` are not touched.
+ * Arguments as in wc_metered_decode_attention.
+ */
+int wc_exact_decode_attention(const wc_cache* exact, const void* q, int q_dtype, int batch,
+                              int n_q_heads, const int32_t* block_table,
+                              int max_blocks_per_seq, const int32_t* seq_lens,
+                              int64_t max_seq_len, float sm_scale, const uint8_t* mask_kv,
+                              void* out, int out_dtype, int split_tokens, void* ws,
+                              size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WITCERT_H */

@@ -1,0 +1,20 @@
+"""WitCert hot path on MI355X: dithered INT8 KV write with residual witness,
+metered GQA decode attention, threshold gate and exact fallback.
+
+The compute lives in libwitcert.so (HIP, gfx950; C-ABI in include/witcert.h);
+this package is its Python binding.  Importing it does not load the library;
+the first call does, and fails loudly if the library is not built.
+"""
+from .api import (  # noqa: F401
+    KINDS,
+    LAYOUTS,
+    PagedCache,
+    cache_bytes,
+    decode_workspace,
+    exact_decode_attention,
+    gate,
+    metered_decode_attention,
+    quantize_write,
+    witness,
+)
+from ._lib import LIB_PATH, WitCertError, lib  # noqa: F401

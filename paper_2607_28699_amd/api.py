@@ -1,0 +1,173 @@
+"""Thin Python binding of libwitcert: argument marshalling only.
+
+PyTorch is used for device memory and the current HIP stream; every step of the
+hot path runs in the library's kernels.  Function names follow the C-ABI
+(``wc_quantize_write`` -> ``quantize_write`` and so on).
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass, field
+
+import torch
+
+from . import _lib
+from ._lib import (WC_BF16, WC_BLOCK_TOKENS, WC_F16, WC_F32, WC_KIND_BF16, WC_KIND_FP8_RAW,
+                   WC_KIND_INT8_DITHER, WC_ROPE_HALF, WC_ROPE_INTERLEAVED, WcCache, check, lib)
+
+KINDS = {"int8_dither": WC_KIND_INT8_DITHER, "fp8_raw": WC_KIND_FP8_RAW, "bf16": WC_KIND_BF16}
+LAYOUTS = {"half": WC_ROPE_HALF, "interleaved": WC_ROPE_INTERLEAVED}
+_DT = {torch.float32: WC_F32, torch.bfloat16: WC_BF16, torch.float16: WC_F16}
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _dt(t: torch.Tensor) -> int:
+    try:
+        return _DT[t.dtype]
+    except KeyError:
+        raise _lib.WitCertError(f"unsupported dtype {t.dtype}") from None
+
+
+def _dev_check(*ts):
+    for t in ts:
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise _lib.WitCertError("tensors must be contiguous device tensors")
+
+
+def cache_bytes(kind: str, num_blocks: int, n_kv: int, head_dim: int, n_bands: int):
+    sizes = (ctypes.c_size_t * 5)()
+    total = lib().wc_cache_bytes(KINDS[kind], num_blocks, n_kv, head_dim, n_bands, sizes)
+    if total == 0:
+        raise _lib.WitCertError("bad cache geometry")
+    return total, list(sizes)
+
+
+@dataclass
+class PagedCache:
+    """One layer's paged cache in device memory (layout: include/witcert.h)."""
+    kind: str
+    num_blocks: int
+    n_kv: int
+    head_dim: int
+    n_bands: int
+    layer: int = 0
+    seed: int = 0
+    rope_layout: str = "half"
+    device: str = "cuda"
+    tensors: dict = field(default_factory=dict)
+
+    def __post_init__(self):
+        total, sizes = cache_bytes(self.kind, self.num_blocks, self.n_kv, self.head_dim, self.n_bands)
+        names = ("k_data", "v_data", "k_scale", "v_scale", "k_witness")
+        slots = self.num_blocks * WC_BLOCK_TOKENS * self.n_kv
+        shapes = {
+            "k_data": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.head_dim),
+            "v_data": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS // 4, self.head_dim, 4),
+            "k_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
+            "v_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
+            "k_witness": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.n_bands),
+        }
+        el = {"int8_dither": torch.int8, "fp8_raw": torch.uint8, "bf16": torch.bfloat16}[self.kind]
+        for n, s in zip(names, sizes):
+            if s == 0:
+                self.tensors[n] = None
+                continue
+            dt = el if n in ("k_data", "v_data") else torch.uint16
+            t = torch.zeros(shapes[n], dtype=dt, device=self.device)
+            assert t.numel() * t.element_size() == s, (n, s, slots)
+            self.tensors[n] = t
+        self.total_bytes = total
+
+    def struct(self) -> WcCache:
+        t = self.tensors
+        return WcCache(KINDS[self.kind], self.head_dim, self.n_kv, self.n_bands,
+                       LAYOUTS[self.rope_layout], self.layer, self.num_blocks, self.seed,
+                       _ptr(t["k_data"]), _ptr(t["v_data"]), _ptr(t["k_scale"]),
+                       _ptr(t["v_scale"]), _ptr(t["k_witness"]))
+
+
+def quantize_write(cache: PagedCache, k: torch.Tensor, v: torch.Tensor, slots: torch.Tensor) -> None:
+    """k, v [n_tok, n_kv, d] (fp32/bf16, post-RoPE keys); slots [n_tok] int64."""
+    _dev_check(k, v, slots)
+    assert slots.dtype == torch.int64 and k.shape == v.shape and k.dtype == v.dtype
+    c = cache.struct()
+    check(lib().wc_quantize_write(ctypes.byref(c), _ptr(k), _ptr(v), _dt(k), _ptr(slots),
+                                  k.shape[0], _stream()), "wc_quantize_write")
+
+
+def witness(x: torch.Tensor, xhat: torch.Tensor, n_bands: int, rope_layout: str = "half",
+            out: torch.Tensor | None = None) -> torch.Tensor:
+    """Band norms of xhat - x rounded up to fp16: [n_vec, n_bands] float16."""
+    _dev_check(x, xhat)
+    d = x.shape[-1]
+    n = x.numel() // d
+    if out is None:
+        out = torch.empty((n, n_bands), dtype=torch.float16, device=x.device)
+    check(lib().wc_witness(_ptr(x), _dt(x), _ptr(xhat), _dt(xhat), n, d, n_bands,
+                           LAYOUTS[rope_layout], _ptr(out), _stream()), "wc_witness")
+    return out
+
+
+def decode_workspace(batch: int, n_q: int, n_kv: int, head_dim: int, max_seq_len: int,
+                     split_tokens: int = 0, device="cuda") -> torch.Tensor:
+    n = lib().wc_decode_workspace_size(batch, n_q, n_kv, head_dim, max_seq_len, split_tokens)
+    if n == 0:
+        raise _lib.WitCertError("bad workspace geometry")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def metered_decode_attention(cache: PagedCache, q: torch.Tensor, block_table: torch.Tensor,
+                             seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float,
+                             out_dtype=torch.float32, split_tokens: int = 0,
+                             ws: torch.Tensor | None = None, out=None, meter=None, raw=None):
+    """q [batch, n_q, d] -> (out [batch, n_q, d], meter [batch, n_q], raw [batch, n_q])."""
+    _dev_check(q, block_table, seq_lens)
+    batch, n_q, d = q.shape
+    if ws is None:
+        ws = decode_workspace(batch, n_q, cache.n_kv, d, max_seq_len, split_tokens, q.device)
+    out = torch.empty((batch, n_q, d), dtype=out_dtype, device=q.device) if out is None else out
+    meter = torch.empty((batch, n_q), dtype=torch.float32, device=q.device) if meter is None else meter
+    raw = torch.empty((batch, n_q), dtype=torch.float32, device=q.device) if raw is None else raw
+    c = cache.struct()
+    check(lib().wc_metered_decode_attention(
+        ctypes.byref(c), _ptr(q), _dt(q), batch, n_q, _ptr(block_table), block_table.shape[1],
+        _ptr(seq_lens), max_seq_len, float(sm_scale), _ptr(out), _dt(out), _ptr(meter), _ptr(raw),
+        split_tokens, _ptr(ws), ws.numel(), _stream()), "wc_metered_decode_attention")
+    return out, meter, raw
+
+
+def gate(meter: torch.Tensor, raw: torch.Tensor, group: int, tau: float,
+         n_gated: torch.Tensor | None = None, mask_q=None, mask_kv=None):
+    """-> (mask_q [batch, n_q] uint8, mask_kv [batch, n_kv] uint8)."""
+    _dev_check(meter, raw)
+    batch, n_q = meter.shape
+    mask_q = torch.empty((batch, n_q), dtype=torch.uint8, device=meter.device) if mask_q is None else mask_q
+    mask_kv = (torch.empty((batch, n_q // group), dtype=torch.uint8, device=meter.device)
+               if mask_kv is None else mask_kv)
+    check(lib().wc_gate(_ptr(meter), _ptr(raw), batch, n_q, group, float(tau), _ptr(mask_q),
+                        _ptr(mask_kv), _ptr(n_gated), _stream()), "wc_gate")
+    return mask_q, mask_kv
+
+
+def exact_decode_attention(cache: PagedCache, q: torch.Tensor, block_table: torch.Tensor,
+                           seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float,
+                           mask_kv: torch.Tensor, out: torch.Tensor, split_tokens: int = 0,
+                           ws: torch.Tensor | None = None) -> torch.Tensor:
+    """Overwrite out[b, heads of routed KV heads] with exact attention over a bf16 cache."""
+    _dev_check(q, block_table, seq_lens, mask_kv, out)
+    batch, n_q, d = q.shape
+    if ws is None:
+        ws = decode_workspace(batch, n_q, cache.n_kv, d, max_seq_len, split_tokens, q.device)
+    c = cache.struct()
+    check(lib().wc_exact_decode_attention(
+        ctypes.byref(c), _ptr(q), _dt(q), batch, n_q, _ptr(block_table), block_table.shape[1],
+        _ptr(seq_lens), max_seq_len, float(sm_scale), _ptr(mask_kv), _ptr(out), _dt(out),
+        split_tokens, _ptr(ws), ws.numel(), _stream()), "wc_exact_decode_attention")
+    return out

@@ -1,0 +1,221 @@
+// extern "C" entry points of libwitcert: argument checks, launch shapes.
+// Every entry point validates on the host, enqueues on the caller's stream and
+// returns; nothing allocates, synchronizes or reads device memory back.
+#include <stdint.h>
+#include <string.h>
+
+#include "wc_launch.h"
+
+namespace {
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int elem_bytes(int kind) { return kind == WC_KIND_BF16 ? 2 : 1; }
+
+int check_cache(const wc_cache* c, bool need_witness) {
+  if (c == nullptr) return WC_EINVAL;
+  if (c->kind < WC_KIND_INT8_DITHER || c->kind > WC_KIND_BF16) return WC_EINVAL;
+  if (c->head_dim != 64 && c->head_dim != 128) return WC_EUNSUPPORTED;
+  if (c->n_kv_heads < 1 || c->n_kv_heads > 65535 || c->layer < 0 || c->layer > 65535) return WC_EINVAL;
+  if (c->rope_layout != WC_ROPE_HALF && c->rope_layout != WC_ROPE_INTERLEAVED) return WC_EINVAL;
+  if (c->num_blocks < 1 || !c->k_data || !c->v_data) return WC_EINVAL;
+  if (!aligned16(c->k_data) || !aligned16(c->v_data)) return WC_EINVAL;
+  if (c->kind != WC_KIND_BF16 || need_witness) {
+    if (c->n_bands < 1 || c->n_bands > 16 || c->head_dim % (2 * c->n_bands)) return WC_EINVAL;
+    if (!c->k_witness || !aligned16(c->k_witness)) return WC_EINVAL;
+  }
+  if (c->kind == WC_KIND_INT8_DITHER &&
+      (!c->k_scale || !c->v_scale || !aligned16(c->k_scale) || !aligned16(c->v_scale)))
+    return WC_EINVAL;
+  return WC_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? WC_OK : WC_EHIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* wc_strerror(int status) {
+  switch (status) {
+    case WC_OK: return "ok";
+    case WC_EINVAL: return "invalid argument";
+    case WC_EUNSUPPORTED: return "unsupported configuration";
+    case WC_EHIP: return "HIP launch error";
+    case WC_EWORKSPACE: return "workspace too small";
+    default: return "unknown status";
+  }
+}
+
+int wc_version(void) { return 100; }
+
+size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim, int n_bands,
+                      size_t sizes[5]) {
+  if (kind < WC_KIND_INT8_DITHER || kind > WC_KIND_BF16 || num_blocks < 0 || n_kv_heads < 1 ||
+      head_dim < 1 || (kind != WC_KIND_BF16 && n_bands < 1))
+    return 0;
+  const size_t slots = (size_t)num_blocks * WC_BLOCK_TOKENS * (size_t)n_kv_heads;
+  size_t s[5];
+  s[0] = s[1] = slots * head_dim * elem_bytes(kind);
+  s[2] = s[3] = kind == WC_KIND_INT8_DITHER ? slots * 2 : 0;
+  s[4] = kind == WC_KIND_BF16 ? 0 : slots * n_bands * 2;
+  if (sizes) memcpy(sizes, s, sizeof(s));
+  return s[0] + s[1] + s[2] + s[3] + s[4];
+}
+
+int wc_quantize_write(const wc_cache* cache, const void* k, const void* v, int in_dtype,
+                      const int64_t* slot_mapping, int64_t n_tok, void* stream) {
+  int st = check_cache(cache, false);
+  if (st != WC_OK) return st;
+  if (n_tok < 0 || (in_dtype != WC_F32 && in_dtype != WC_BF16)) return WC_EINVAL;
+  if (n_tok == 0) return WC_OK;
+  if (!k || !v || !slot_mapping || !aligned16(k) || !aligned16(v)) return WC_EINVAL;
+  wc::WriteArgs a{};
+  a.kind = cache->kind;
+  a.head_dim = cache->head_dim;
+  a.n_kv = cache->n_kv_heads;
+  a.n_bands = cache->n_bands;
+  a.interleaved = cache->rope_layout == WC_ROPE_INTERLEAVED;
+  a.layer = cache->layer;
+  a.in_dtype = in_dtype;
+  a.key0 = (uint32_t)cache->seed;
+  a.key1 = (uint32_t)(cache->seed >> 32);
+  a.n_tok = n_tok;
+  a.k = k;
+  a.v = v;
+  a.slots = slot_mapping;
+  a.k_data = cache->k_data;
+  a.v_data = cache->v_data;
+  a.k_scale = static_cast<uint16_t*>(cache->k_scale);
+  a.v_scale = static_cast<uint16_t*>(cache->v_scale);
+  a.k_witness = static_cast<uint16_t*>(cache->k_witness);
+  return hip_status(wc::launch_quantize_write(a, static_cast<hipStream_t>(stream)));
+}
+
+int wc_witness(const void* x, int x_dtype, const void* xhat, int xhat_dtype, int64_t n_vec,
+               int head_dim, int n_bands, int rope_layout, uint16_t* w_out, void* stream) {
+  if (n_vec < 0 || head_dim < 2 || n_bands < 1 || n_bands > 64 || head_dim % (2 * n_bands))
+    return WC_EINVAL;
+  if (x_dtype < WC_F32 || x_dtype > WC_F16 || xhat_dtype < WC_F32 || xhat_dtype > WC_F16)
+    return WC_EINVAL;
+  if (rope_layout != WC_ROPE_HALF && rope_layout != WC_ROPE_INTERLEAVED) return WC_EINVAL;
+  if (n_vec == 0) return WC_OK;
+  if (!x || !xhat || !w_out) return WC_EINVAL;
+  wc::WitnessArgs a{x, xhat, x_dtype, xhat_dtype, head_dim, n_bands,
+                    rope_layout == WC_ROPE_INTERLEAVED, n_vec, w_out};
+  return hip_status(wc::launch_witness(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
+                                int64_t max_seq_len, int split_tokens) {
+  if (batch < 0 || n_q_heads < 1 || n_kv_heads < 1 || head_dim < 1 || max_seq_len < 0 ||
+      split_tokens < 0)
+    return 0;
+  const int st = wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens);
+  const int64_t ns = wc::n_splits_for(max_seq_len, st);
+  size_t bytes = (size_t)batch * n_q_heads * ns * wc::partial_record_floats(head_dim) * sizeof(float);
+  return bytes < 256 ? 256 : bytes;
+}
+
+static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int batch,
+                         int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                         const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out,
+                         int out_dtype, int split_tokens, void* ws, size_t ws_bytes,
+                         wc::DecodeArgs& a) {
+  if (batch < 0 || n_q_heads < 1 || max_blocks_per_seq < 1 || max_seq_len < 0 || split_tokens < 0)
+    return WC_EINVAL;
+  if (n_q_heads % cache->n_kv_heads) return WC_EINVAL;
+  const int group = n_q_heads / cache->n_kv_heads;
+  if (group > 16) return WC_EUNSUPPORTED;
+  if (q_dtype != WC_F32 && q_dtype != WC_BF16) return WC_EINVAL;
+  if (out_dtype != WC_F32 && out_dtype != WC_BF16) return WC_EINVAL;
+  if (max_seq_len > (int64_t)max_blocks_per_seq * WC_BLOCK_TOKENS || max_seq_len > INT32_MAX / 2)
+    return WC_EINVAL;
+  if (!(sm_scale > 0.0f)) return WC_EINVAL;
+  if (batch > 0 && (!q || !block_table || !seq_lens || !out || !ws)) return WC_EINVAL;
+  const int st = wc::choose_split_tokens(batch, cache->n_kv_heads, max_seq_len, split_tokens);
+  const int64_t ns = wc::n_splits_for(max_seq_len, st);
+  if (ns > 65535) return WC_EUNSUPPORTED;
+  if (ws_bytes < wc_decode_workspace_size(batch, n_q_heads, cache->n_kv_heads, cache->head_dim,
+                                          max_seq_len, split_tokens))
+    return WC_EWORKSPACE;
+  a.k_data = cache->k_data;
+  a.v_data = cache->v_data;
+  a.k_scale = static_cast<const uint16_t*>(cache->k_scale);
+  a.v_scale = static_cast<const uint16_t*>(cache->v_scale);
+  a.k_witness = static_cast<const uint16_t*>(cache->k_witness);
+  a.q = q;
+  a.table = block_table;
+  a.seq_lens = seq_lens;
+  a.part = static_cast<float*>(ws);
+  a.out = out;
+  a.kind = cache->kind;
+  a.head_dim = cache->head_dim;
+  a.n_bands = cache->n_bands;
+  a.interleaved = cache->rope_layout == WC_ROPE_INTERLEAVED;
+  a.q_dtype = q_dtype;
+  a.out_dtype = out_dtype;
+  a.batch = batch;
+  a.n_q = n_q_heads;
+  a.n_kv = cache->n_kv_heads;
+  a.group = group;
+  a.max_blocks = max_blocks_per_seq;
+  a.n_splits = (int)ns;
+  a.split_tokens = st;
+  a.layer = cache->layer;
+  a.key0 = (uint32_t)cache->seed;
+  a.key1 = (uint32_t)(cache->seed >> 32);
+  a.sm_scale = sm_scale;
+  return WC_OK;
+}
+
+int wc_metered_decode_attention(const wc_cache* cache, const void* q, int q_dtype, int batch,
+                                int n_q_heads, const int32_t* block_table,
+                                int max_blocks_per_seq, const int32_t* seq_lens,
+                                int64_t max_seq_len, float sm_scale, void* out, int out_dtype,
+                                float* meter, float* raw, int split_tokens, void* ws,
+                                size_t ws_bytes, void* stream) {
+  int s = check_cache(cache, true);
+  if (s != WC_OK) return s;
+  if (cache->kind == WC_KIND_BF16) return WC_EINVAL;
+  if (batch > 0 && !meter) return WC_EINVAL;
+  wc::DecodeArgs a{};
+  s = decode_common(cache, q, q_dtype, batch, n_q_heads, block_table, max_blocks_per_seq,
+                    seq_lens, max_seq_len, sm_scale, out, out_dtype, split_tokens, ws, ws_bytes, a);
+  if (s != WC_OK) return s;
+  a.meter = meter;
+  a.raw = raw;
+  a.mask_kv = nullptr;
+  return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
+}
+
+int wc_gate(const float* meter, const float* raw, int batch, int n_q_heads, int group, float tau,
+            uint8_t* mask_q, uint8_t* mask_kv, int32_t* n_gated, void* stream) {
+  if (batch < 0 || n_q_heads < 1 || group < 1 || n_q_heads % group || !(tau >= 0.0f)) return WC_EINVAL;
+  if (batch == 0) return WC_OK;
+  if (!mask_q || !mask_kv || (tau < 1.0f ? !meter : !raw)) return WC_EINVAL;
+  wc::GateArgs a{meter, raw, mask_q, mask_kv, n_gated, batch, n_q_heads, group, tau};
+  return hip_status(wc::launch_gate(a, static_cast<hipStream_t>(stream)));
+}
+
+int wc_exact_decode_attention(const wc_cache* exact, const void* q, int q_dtype, int batch,
+                              int n_q_heads, const int32_t* block_table,
+                              int max_blocks_per_seq, const int32_t* seq_lens,
+                              int64_t max_seq_len, float sm_scale, const uint8_t* mask_kv,
+                              void* out, int out_dtype, int split_tokens, void* ws,
+                              size_t ws_bytes, void* stream) {
+  int s = check_cache(exact, false);
+  if (s != WC_OK) return s;
+  if (exact->kind != WC_KIND_BF16) return WC_EINVAL;
+  if (batch > 0 && !mask_kv) return WC_EINVAL;
+  wc::DecodeArgs a{};
+  s = decode_common(exact, q, q_dtype, batch, n_q_heads, block_table, max_blocks_per_seq,
+                    seq_lens, max_seq_len, sm_scale, out, out_dtype, split_tokens, ws, ws_bytes, a);
+  if (s != WC_OK) return s;
+  a.mask_kv = mask_kv;
+  a.meter = nullptr;
+  a.raw = nullptr;
+  return hip_status(wc::launch_decode(a, false, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

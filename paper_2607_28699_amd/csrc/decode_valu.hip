@@ -1,0 +1,395 @@
+// Metered decode attention, vector-ALU path (fp32 arithmetic throughout).
+//
+// Read path of the meter loop (Sec. 6): over a split of the KV axis one
+// workgroup regenerates the Philox dither of every cached token, dequantizes,
+// forms the compressed logits of the G query heads of one KV head, keeps an
+// online softmax, accumulates the meter numerator sum_t e^{l_t - m} (e^{c_t} - 1)
+// with c_t = sm_scale * sum_b ||q_b|| w_{t,b} (Theorem black-box logit bound),
+// and the unnormalized output.  A second kernel merges the split partials under
+// the LSE weights; A merges exactly like the output because it is a softmax-
+// weighted average (Sec. 6.2, SGLang decode kernel).  The same kernels, without
+// the meter and restricted to routed KV heads, serve the exact bf16 fallback.
+//
+// Tile of 64 tokens, 256 threads, three phases separated by barriers:
+//   1  thread (token i, quarter of the channels): dither + dequant + partial
+//      dot products with all G queries, reduced over the 4 quarter-lanes;
+//      per-token bound c_t from the stored witness.
+//   2  wave w, heads w, w+4, ...: lane = token; running max / sum / meter
+//      numerator, weights p_t * s^v_t to LDS.
+//   3  thread (channel, head subset): rescale and accumulate p_t * (code - xi).
+#include <float.h>
+
+#include "wc_device.h"
+#include "wc_launch.h"
+
+namespace wc {
+
+namespace {
+
+constexpr int kT = 64;        // tokens per tile
+constexpr int kGMax = 16;     // query heads per KV head
+constexpr int kThreads = 256;
+
+template <int D, int KIND, int QT, bool METER>
+__global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
+  constexpr int CH = D / 4;            // phase-1 channels per thread
+  constexpr int NG = CH / 16;          // Philox groups per thread
+  constexpr int NHS = kThreads / D;    // phase-3 head subsets
+  constexpr int HPT = kGMax / NHS;     // phase-3 heads per thread (max)
+
+  __shared__ float q_s[kGMax][D];
+  __shared__ float qbn_s[kGMax][16];
+  __shared__ float logit_s[kGMax][kT];
+  __shared__ float cb_s[kGMax][kT];
+  __shared__ float pw_s[kGMax][kT];
+  __shared__ uint32_t xi_s[kT][D / 4];
+  __shared__ float vs_s[kT];
+  __shared__ float alpha_s[kGMax];
+  __shared__ int64_t slot_s[kT];
+
+  const int split = blockIdx.x;
+  const int unit = blockIdx.y;
+  const int b = unit / a.n_kv, kv = unit % a.n_kv;
+  if (a.mask_kv != nullptr && a.mask_kv[unit] == 0) return;
+  const int L = a.seq_lens[b];
+  const int t_begin = split * a.split_tokens;
+  if (t_begin >= L) return;
+  // clamp to what the block table can address (guards a seq_lens above max_seq_len)
+  const int t_end = min(min(L, t_begin + a.split_tokens), a.max_blocks * kBlockTokens);
+  const int G = a.group;
+  const int B = a.n_bands;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+
+  for (int i = tid; i < G * D; i += kThreads) {
+    const int h = i / D, c = i % D;
+    const int64_t qi = ((int64_t)b * a.n_q + (int64_t)kv * G + h) * D + c;
+    q_s[h][c] = QT == WC_F32 ? reinterpret_cast<const float*>(a.q)[qi]
+                             : bf16_to_f32(reinterpret_cast<const uint16_t*>(a.q)[qi]);
+  }
+  __syncthreads();
+  if constexpr (METER) {
+    for (int i = tid; i < G * B; i += kThreads) {
+      const int h = i / B, bb = i % B;
+      float acc = 0.0f;
+      for (int k = 0; k < D / B; ++k) {
+        const float x = q_s[h][band_channel(bb, k, D, B, a.interleaved)];
+        acc = fmaf(x, x, acc);
+      }
+      qbn_s[h][bb] = sqrtf(acc) * a.sm_scale;
+    }
+  }
+
+  float m_run[4], l_run[4], n_run[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    m_run[k] = -INFINITY;
+    l_run[k] = 0.0f;
+    n_run[k] = 0.0f;
+  }
+  const int c3 = tid % D, hs = tid / D;
+  float acc[HPT];
+#pragma unroll
+  for (int k = 0; k < HPT; ++k) acc[k] = 0.0f;
+  const uint32_t layer_head = ((uint32_t)a.layer << 16) | (uint32_t)kv;
+
+  for (int t0 = t_begin; t0 < t_end; t0 += kT) {
+    __syncthreads();
+    // ---------------- phase 1: logits and per-token bounds ----------------
+    {
+      const int i = tid >> 2, part = tid & 3;
+      const int t = t0 + i;
+      const bool valid = t < t_end;
+      int64_t slot = -1;
+      if (valid) slot = (int64_t)a.table[(int64_t)b * a.max_blocks + t / kBlockTokens] * kBlockTokens +
+                        t % kBlockTokens;
+      if (part == 0) slot_s[i] = slot;
+      const int c0 = part * CH;
+      const int64_t page = valid ? (slot / kBlockTokens) * a.n_kv + kv : 0;
+      const int off = valid ? (int)(slot % kBlockTokens) : 0;
+      float kval[CH];
+#pragma unroll
+      for (int c = 0; c < CH; ++c) kval[c] = 0.0f;
+      if (valid) {
+        if constexpr (KIND == WC_KIND_INT8_DITHER) {
+          const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const int8_t*>(a.k_data) +
+                                                           (page * kBlockTokens + off) * D + c0);
+          const float s = f16_to_f32(a.k_scale[page * kBlockTokens + off]);
+#pragma unroll
+          for (int gi = 0; gi < NG; ++gi) {
+            const uint4 cw = kp[gi];
+            const U4 r = dither_block(c0 / 16 + gi, slot, layer_head, a.key0, a.key1);
+            const uint32_t codes[4] = {cw.x, cw.y, cw.z, cw.w};
+            const uint32_t rw[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+            for (int w4 = 0; w4 < 4; ++w4) {
+              xi_s[i][(c0 + 16 * gi) / 4 + w4] = rw[w4];
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const float code = (float)(int8_t)((codes[w4] >> (8 * j)) & 0xFFu);
+                const float xi = dither_value((rw[w4] >> (8 * j)) & 0xFFu);
+                kval[16 * gi + 4 * w4 + j] = s * (code - xi);
+              }
+            }
+          }
+          if (part == 0) vs_s[i] = f16_to_f32(a.v_scale[page * kBlockTokens + off]);
+        } else if constexpr (KIND == WC_KIND_FP8_RAW) {
+          const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.k_data) +
+                                                           (page * kBlockTokens + off) * D + c0);
+#pragma unroll
+          for (int gi = 0; gi < NG; ++gi) {
+            const uint4 cw = kp[gi];
+            const uint32_t codes[4] = {cw.x, cw.y, cw.z, cw.w};
+#pragma unroll
+            for (int w4 = 0; w4 < 4; ++w4)
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                kval[16 * gi + 4 * w4 + j] = e4m3_to_f32((codes[w4] >> (8 * j)) & 0xFFu);
+          }
+          if (part == 0) vs_s[i] = 1.0f;
+        } else {
+          const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a.k_data) +
+                                                           (page * kBlockTokens + off) * D + c0);
+#pragma unroll
+          for (int v4 = 0; v4 < CH / 8; ++v4) {
+            const uint4 cw = kp[v4];
+            const uint32_t wds[4] = {cw.x, cw.y, cw.z, cw.w};
+#pragma unroll
+            for (int w4 = 0; w4 < 4; ++w4) {
+              kval[8 * v4 + 2 * w4] = bf16_to_f32((uint16_t)(wds[w4] & 0xFFFFu));
+              kval[8 * v4 + 2 * w4 + 1] = bf16_to_f32((uint16_t)(wds[w4] >> 16));
+            }
+          }
+          if (part == 0) vs_s[i] = 1.0f;
+        }
+      } else if (part == 0) {
+        vs_s[i] = 0.0f;
+      }
+      for (int h = 0; h < G; ++h) {
+        float d = 0.0f;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) d = fmaf(q_s[h][c0 + c], kval[c], d);
+        d += __shfl_xor(d, 1, 4);
+        d += __shfl_xor(d, 2, 4);
+        if (part == 0) logit_s[h][i] = valid ? d * a.sm_scale : -INFINITY;
+      }
+      if constexpr (METER) {
+        float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (valid) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int bb = part + 4 * k;
+            if (bb < B) wv[k] = f16_to_f32(a.k_witness[(page * kBlockTokens + off) * B + bb]);
+          }
+        }
+        for (int h = 0; h < G; ++h) {
+          float cp = 0.0f;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int bb = part + 4 * k;
+            if (bb < B) cp = fmaf(qbn_s[h][bb], wv[k], cp);
+          }
+          cp += __shfl_xor(cp, 1, 4);
+          cp += __shfl_xor(cp, 2, 4);
+          if (part == 0) cb_s[h][i] = cp;
+        }
+      }
+    }
+    __syncthreads();
+    // ---------------- phase 2: online softmax and meter numerator ----------------
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int h = wave + 4 * k;
+      if (h < G) {
+        const float l = logit_s[h][lane];
+        const float m_new = fmaxf(m_run[k], wave_max(l));
+        const float alpha = expf(m_run[k] - m_new);
+        const float p = expf(l - m_new);
+        float term = 0.0f;
+        if constexpr (METER) {
+          const float c = cb_s[h][lane];
+          // p (e^c - 1); for large c in the log domain so that a token whose
+          // weight underflows still counts with its bound (never truncate c)
+          term = c > 1.0f ? expf(l - m_new + c) - p : p * expm1f(c);
+        }
+        const float lsum = wave_sum(p);
+        l_run[k] = fmaf(alpha, l_run[k], lsum);
+        if constexpr (METER) {
+          const float nn = fmaf(alpha, n_run[k], wave_sum(term));
+          n_run[k] = isnan(nn) ? INFINITY : nn;
+        }
+        m_run[k] = m_new;
+        pw_s[h][lane] = p * vs_s[lane];
+        if (lane == 0) alpha_s[h] = alpha;
+      }
+    }
+    __syncthreads();
+    // ---------------- phase 3: P V ----------------
+    {
+#pragma unroll
+      for (int k = 0; k < HPT; ++k) {
+        const int h = hs + k * NHS;
+        if (h < G) acc[k] *= alpha_s[h];
+      }
+      for (int qd = 0; qd < kT / 4; ++qd) {
+        const int i0 = 4 * qd;
+        const int64_t slot = slot_s[i0];
+        if (slot < 0) break;
+        const int64_t page = (slot / kBlockTokens) * a.n_kv + kv;
+        const int off = (int)(slot % kBlockTokens);   // multiple of 4
+        float vv[4];
+        if constexpr (KIND == WC_KIND_BF16) {
+          const uint2 w = *reinterpret_cast<const uint2*>(
+              reinterpret_cast<const uint16_t*>(a.v_data) + page * (kBlockTokens * D) +
+              ((off >> 2) * D + c3) * 4);
+          vv[0] = bf16_to_f32((uint16_t)(w.x & 0xFFFFu));
+          vv[1] = bf16_to_f32((uint16_t)(w.x >> 16));
+          vv[2] = bf16_to_f32((uint16_t)(w.y & 0xFFFFu));
+          vv[3] = bf16_to_f32((uint16_t)(w.y >> 16));
+        } else {
+          const uint32_t w = *reinterpret_cast<const uint32_t*>(
+              reinterpret_cast<const uint8_t*>(a.v_data) + page * (kBlockTokens * D) +
+              ((off >> 2) * D + c3) * 4);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t byte = (w >> (8 * j)) & 0xFFu;
+            if constexpr (KIND == WC_KIND_INT8_DITHER) {
+              const uint32_t u = (xi_s[i0 + j][c3 >> 2] >> (8 * (c3 & 3))) & 0xFFu;
+              vv[j] = (float)(int8_t)byte - dither_value(u);
+            } else {
+              vv[j] = e4m3_to_f32(byte);
+            }
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (t0 + i0 + j >= t_end) vv[j] = 0.0f;
+#pragma unroll
+        for (int k = 0; k < HPT; ++k) {
+          const int h = hs + k * NHS;
+          if (h < G) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[k] = fmaf(pw_s[h][i0 + j], vv[j], acc[k]);
+          }
+        }
+      }
+    }
+  }
+
+  const int64_t R = (int64_t)partial_record_floats(D);
+  const int64_t rec_base = ((int64_t)b * a.n_q + (int64_t)kv * G) * a.n_splits + split;
+#pragma unroll
+  for (int k = 0; k < HPT; ++k) {
+    const int h = hs + k * NHS;
+    if (h < G) a.part[(rec_base + (int64_t)h * a.n_splits) * R + c3] = acc[k];
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int h = wave + 4 * k;
+      if (h < G) {
+        float* rec = a.part + (rec_base + (int64_t)h * a.n_splits) * R;
+        rec[D] = m_run[k];
+        rec[D + 1] = l_run[k];
+        rec[D + 2] = n_run[k];
+      }
+    }
+  }
+}
+
+// Merge of the split partials of one (sequence, query head) under the LSE
+// weights: out = sum_j e^{m_j - M} acc_j / L, A - 1 = sum_j e^{m_j - M} N_j / L.
+template <int D, bool METER>
+__global__ __launch_bounds__(64) void merge_kernel(DecodeArgs a) {
+  constexpr int CPT = D / 64;
+  const int bh = blockIdx.x;
+  const int b = bh / a.n_q, h = bh % a.n_q;
+  if (a.mask_kv != nullptr && a.mask_kv[b * a.n_kv + h / a.group] == 0) return;
+  const int L = a.seq_lens[b];
+  const int ns = min((L + a.split_tokens - 1) / a.split_tokens, a.n_splits);
+  const int64_t R = (int64_t)partial_record_floats(D);
+  const float* rec0 = a.part + (int64_t)bh * a.n_splits * R;
+  const int tid = threadIdx.x;
+  float M = -INFINITY;
+  for (int j = 0; j < ns; ++j) M = fmaxf(M, rec0[j * R + D]);
+  float lsum = 0.0f, nsum = 0.0f, acc[CPT];
+#pragma unroll
+  for (int k = 0; k < CPT; ++k) acc[k] = 0.0f;
+  for (int j = 0; j < ns; ++j) {
+    const float* rec = rec0 + j * R;
+    const float e = expf(rec[D] - M);
+    lsum = fmaf(e, rec[D + 1], lsum);
+    if constexpr (METER) {
+      const float nn = fmaf(e, rec[D + 2], nsum);
+      nsum = isnan(nn) ? INFINITY : nn;
+    }
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) acc[k] = fmaf(e, rec[tid + 64 * k], acc[k]);
+  }
+  const float inv = ns > 0 ? 1.0f / lsum : 0.0f;
+#pragma unroll
+  for (int k = 0; k < CPT; ++k) {
+    const float o = acc[k] * inv;
+    const int64_t oi = (int64_t)bh * D + tid + 64 * k;
+    if (a.out_dtype == WC_F32)
+      reinterpret_cast<float*>(a.out)[oi] = o;
+    else
+      reinterpret_cast<uint16_t*>(a.out)[oi] = f32_to_bf16_rne(o);
+  }
+  if constexpr (METER) {
+    if (tid == 0) {
+      float raw = 0.0f;
+      if (ns > 0) {
+        const float am1 = nsum * inv;
+        raw = 0.5f * am1 * (2.0f + am1);
+        if (!(raw <= FLT_MAX)) raw = INFINITY;
+      }
+      a.meter[bh] = fminf(1.0f, raw);
+      if (a.raw != nullptr) a.raw[bh] = raw;
+    }
+  }
+}
+
+template <int D, int KIND, int QT, bool METER>
+hipError_t launch_dq(const DecodeArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((decode_split_kernel<D, KIND, QT, METER>), dim3(a.n_splits, a.batch * a.n_kv),
+                     dim3(kThreads), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((merge_kernel<D, METER>), dim3(a.batch * a.n_q), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int D, int KIND, bool METER>
+hipError_t launch_dk(const DecodeArgs& a, hipStream_t st) {
+  return a.q_dtype == WC_F32 ? launch_dq<D, KIND, WC_F32, METER>(a, st)
+                             : launch_dq<D, KIND, WC_BF16, METER>(a, st);
+}
+
+template <int D>
+hipError_t launch_d(const DecodeArgs& a, bool metered, hipStream_t st) {
+  if (!metered) return launch_dk<D, WC_KIND_BF16, false>(a, st);
+  return a.kind == WC_KIND_INT8_DITHER ? launch_dk<D, WC_KIND_INT8_DITHER, true>(a, st)
+                                       : launch_dk<D, WC_KIND_FP8_RAW, true>(a, st);
+}
+
+}  // namespace
+
+int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested) {
+  if (requested > 0) return (requested + 63) / 64 * 64;
+  const int64_t units = (int64_t)batch * n_kv;
+  const int64_t target = 1024;   // workgroups: 4 per compute unit
+  int64_t splits = target / (units > 0 ? units : 1);
+  if (splits < 1) splits = 1;
+  int64_t st = (max_seq_len + splits - 1) / splits;
+  st = (st + 63) / 64 * 64;
+  if (st < 256) st = 256;
+  return (int)st;
+}
+
+hipError_t launch_decode(const DecodeArgs& a, bool metered, hipStream_t st) {
+  if (a.batch == 0 || a.n_q == 0) return hipSuccess;
+  return a.head_dim == 64 ? launch_d<64>(a, metered, st) : launch_d<128>(a, metered, st);
+}
+
+}  // namespace wc

@@ -1,0 +1,77 @@
+// Kernel argument blocks and launchers behind the C-ABI (host + device visible).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/witcert.h"
+
+namespace wc {
+
+struct WriteArgs {
+  int kind, head_dim, n_kv, n_bands, interleaved, layer, in_dtype;
+  uint32_t key0, key1;
+  int64_t n_tok;
+  const void* k;
+  const void* v;
+  const int64_t* slots;
+  void* k_data;
+  void* v_data;
+  uint16_t* k_scale;
+  uint16_t* v_scale;
+  uint16_t* k_witness;
+};
+
+struct WitnessArgs {
+  const void* x;
+  const void* xhat;
+  int x_dtype, xhat_dtype, head_dim, n_bands, interleaved;
+  int64_t n_vec;
+  uint16_t* w_out;
+};
+
+// Decode: one split (a contiguous chunk of split_tokens tokens) of one
+// (sequence, KV head) per workgroup; partial records merged by a second kernel.
+struct DecodeArgs {
+  const void* k_data;
+  const void* v_data;
+  const uint16_t* k_scale;
+  const uint16_t* v_scale;
+  const uint16_t* k_witness;
+  const void* q;
+  const int32_t* table;
+  const int32_t* seq_lens;
+  const uint8_t* mask_kv;   // exact fallback: only routed (b, kv) units run
+  float* part;              // partial records [batch][n_q][n_splits][D + 4]
+  void* out;
+  float* meter;
+  float* raw;
+  int kind, head_dim, n_bands, interleaved, q_dtype, out_dtype;
+  int batch, n_q, n_kv, group, max_blocks, n_splits, split_tokens, layer;
+  uint32_t key0, key1;
+  float sm_scale;
+};
+
+struct GateArgs {
+  const float* meter;
+  const float* raw;
+  uint8_t* mask_q;
+  uint8_t* mask_kv;
+  int32_t* n_gated;
+  int batch, n_q, group;
+  float tau;
+};
+
+// Tokens per KV split chosen by the library (multiple of 64).
+int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested);
+inline int64_t n_splits_for(int64_t max_seq_len, int split_tokens) {
+  return max_seq_len <= 0 ? 1 : (max_seq_len + split_tokens - 1) / split_tokens;
+}
+__host__ __device__ inline size_t partial_record_floats(int head_dim) { return (size_t)head_dim + 4; }
+
+hipError_t launch_quantize_write(const WriteArgs& a, hipStream_t st);
+hipError_t launch_witness(const WitnessArgs& a, hipStream_t st);
+hipError_t launch_decode(const DecodeArgs& a, bool metered, hipStream_t st);
+hipError_t launch_gate(const GateArgs& a, hipStream_t st);
+
+}  // namespace wc

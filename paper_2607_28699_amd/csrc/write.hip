@@ -1,0 +1,241 @@
+// Write path of the certified cache: dithered INT8 quantizer, raw fp8 cast, bf16
+// copy, and the residual witness (Sec. 4.2 subtractive dither; Sec. 6.2 research
+// kernels and storage side; Sec. 4.1 Eq. witness).
+//
+// One token-head (one token of one KV head, K and V together) is handled by
+// D/16 lanes, lane g owning channels 16g .. 16g+15 -- exactly one Philox call
+// of dither, shared by K and V.  Key residuals go through LDS so that any band
+// map can be summed; each band norm is then rounded up to fp16.
+#include "wc_device.h"
+#include "wc_launch.h"
+
+namespace wc {
+
+namespace {
+
+constexpr int kWriteThreads = 256;
+
+template <int D, typename TIn>
+__device__ __forceinline__ void load16(const TIn* src, float (&x)[16]) {
+  if constexpr (sizeof(TIn) == 4) {
+    const float4* p = reinterpret_cast<const float4*>(src);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float4 v = p[i];
+      x[4 * i] = v.x; x[4 * i + 1] = v.y; x[4 * i + 2] = v.z; x[4 * i + 3] = v.w;
+    }
+  } else {
+    const uint4* p = reinterpret_cast<const uint4*>(src);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      uint4 v = p[i];
+      uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[8 * i + 2 * j] = bf16_to_f32((uint16_t)(w[j] & 0xFFFFu));
+        x[8 * i + 2 * j + 1] = bf16_to_f32((uint16_t)(w[j] >> 16));
+      }
+    }
+  }
+}
+
+// Per-token, per-head fp16 scale s = round_up(fl32(amax / 126.5)) and fl32(1/s).
+__device__ __forceinline__ void int8_scale(float amax, uint16_t& s_bits, float& s, float& inv) {
+  s_bits = f16_round_up(__fdiv_rn(amax, 126.5f));
+  s = f16_to_f32(s_bits);
+  inv = s > 0.0f ? __fdiv_rn(1.0f, s) : 0.0f;
+}
+
+template <int D, int KIND, typename TIn>
+__global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs a) {
+  constexpr int LPT = D / 16;                 // lanes per token-head
+  constexpr int TH = kWriteThreads / LPT;     // token-heads per block
+  __shared__ float r2[TH][D];                 // squared key residuals
+  __shared__ int64_t slot_s[TH];
+
+  const int tid = threadIdx.x;
+  const int lth = tid / LPT;
+  const int g = tid % LPT;
+  const int64_t th = (int64_t)blockIdx.x * TH + lth;
+  const int64_t total = a.n_tok * (int64_t)a.n_kv;
+  const bool in_range = th < total;
+  const int64_t tok = in_range ? th / a.n_kv : 0;
+  const int h = in_range ? (int)(th % a.n_kv) : 0;
+  const int64_t slot = in_range ? a.slots[tok] : -1;
+  const bool active = in_range && slot >= 0;
+
+  float k[16], v[16];
+  if (active) {
+    const TIn* kp = reinterpret_cast<const TIn*>(a.k) + (tok * a.n_kv + h) * D + 16 * g;
+    const TIn* vp = reinterpret_cast<const TIn*>(a.v) + (tok * a.n_kv + h) * D + 16 * g;
+    load16<D>(kp, k);
+    load16<D>(vp, v);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) k[i] = v[i] = 0.0f;
+  }
+  const int64_t blk = active ? slot / kBlockTokens : 0;
+  const int off = active ? (int)(slot % kBlockTokens) : 0;
+  const int64_t bh = blk * a.n_kv + h;        // (block, head) page index
+  if (g == 0) slot_s[lth] = slot;
+
+  if constexpr (KIND == WC_KIND_INT8_DITHER) {
+    float ak = 0.0f, av = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      ak = fmaxf(ak, fabsf(k[i]));
+      av = fmaxf(av, fabsf(v[i]));
+    }
+#pragma unroll
+    for (int o = 1; o < LPT; o <<= 1) {
+      ak = fmaxf(ak, __shfl_xor(ak, o, LPT));
+      av = fmaxf(av, __shfl_xor(av, o, LPT));
+    }
+    uint16_t skb, svb;
+    float sk, ikk, sv, ivv;
+    int8_scale(ak, skb, sk, ikk);
+    int8_scale(av, svb, sv, ivv);
+
+    const U4 rnd = dither_block(g, slot, ((uint32_t)a.layer << 16) | (uint32_t)h, a.key0, a.key1);
+    const uint32_t words[4] = {rnd.x, rnd.y, rnd.z, rnd.w};
+    uint32_t kc[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float xi = dither_value((words[i >> 2] >> (8 * (i & 3))) & 0xFFu);
+      const float ck = rintf(__fadd_rn(__fmul_rn(k[i], ikk), xi));
+      const float cv = rintf(__fadd_rn(__fmul_rn(v[i], ivv), xi));
+      const float rk = fmaf(sk, ck - xi, -k[i]);   // khat - k, one rounding
+      r2[lth][16 * g + i] = rk * rk;
+      kc[i >> 2] |= ((uint32_t)(int32_t)ck & 0xFFu) << (8 * (i & 3));
+      if (active) {
+        int8_t* vd = reinterpret_cast<int8_t*>(a.v_data) + bh * (kBlockTokens * D) +
+                     ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
+        *vd = (int8_t)(int32_t)cv;
+      }
+    }
+    if (active) {
+      uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<int8_t*>(a.k_data) +
+                                           (bh * kBlockTokens + off) * D + 16 * g);
+      *kd = make_uint4(kc[0], kc[1], kc[2], kc[3]);
+      if (g == 0) {
+        a.k_scale[bh * kBlockTokens + off] = skb;
+        a.v_scale[bh * kBlockTokens + off] = svb;
+      }
+    }
+  } else if constexpr (KIND == WC_KIND_FP8_RAW) {
+    uint32_t kc[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const uint32_t bk = f32_to_e4m3_sat(k[i]);
+      const uint32_t bv = f32_to_e4m3_sat(v[i]);
+      const float rk = e4m3_to_f32(bk) - k[i];    // exact (operands within a factor 2)
+      r2[lth][16 * g + i] = rk * rk;
+      kc[i >> 2] |= bk << (8 * (i & 3));
+      if (active) {
+        uint8_t* vd = reinterpret_cast<uint8_t*>(a.v_data) + bh * (kBlockTokens * D) +
+                      ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
+        *vd = (uint8_t)bv;
+      }
+    }
+    if (active) {
+      uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(a.k_data) +
+                                           (bh * kBlockTokens + off) * D + 16 * g);
+      *kd = make_uint4(kc[0], kc[1], kc[2], kc[3]);
+    }
+  } else {  // WC_KIND_BF16: exact cache, no witness
+    if (active) {
+      uint32_t kw[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        kw[i] = (uint32_t)f32_to_bf16_rne(k[2 * i]) | ((uint32_t)f32_to_bf16_rne(k[2 * i + 1]) << 16);
+      uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.k_data) +
+                                           (bh * kBlockTokens + off) * D + 16 * g);
+      kd[0] = make_uint4(kw[0], kw[1], kw[2], kw[3]);
+      kd[1] = make_uint4(kw[4], kw[5], kw[6], kw[7]);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        uint16_t* vd = reinterpret_cast<uint16_t*>(a.v_data) + bh * (kBlockTokens * D) +
+                       ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
+        *vd = f32_to_bf16_rne(v[i]);
+      }
+    }
+    return;
+  }
+
+  // ---- witness: band norms of the key residual, rounded up to fp16 ----
+  __syncthreads();
+  const int B = a.n_bands;
+  const int per_band = D / B;
+  for (int item = tid; item < TH * B; item += kWriteThreads) {
+    const int t = item / B, b = item % B;
+    const int64_t th2 = (int64_t)blockIdx.x * TH + t;
+    const int64_t s2 = slot_s[t];
+    if (th2 >= total || s2 < 0) continue;
+    const int h2 = (int)(th2 % a.n_kv);
+    float acc = 0.0f;
+    for (int kk = 0; kk < per_band; ++kk) acc += r2[t][band_channel(b, kk, D, B, a.interleaved)];
+    const float w = sqrtf(acc) * (1.0f + 0x1p-18f);   // never below the exact norm
+    const int64_t bh2 = (s2 / kBlockTokens) * a.n_kv + h2;
+    a.k_witness[(bh2 * kBlockTokens + s2 % kBlockTokens) * B + b] = f16_round_up(w);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ float load_any(const void* p, int64_t i, int dt) {
+  if (dt == WC_F32) return reinterpret_cast<const float*>(p)[i];
+  if (dt == WC_BF16) return bf16_to_f32(reinterpret_cast<const uint16_t*>(p)[i]);
+  return f16_to_f32(reinterpret_cast<const uint16_t*>(p)[i]);
+}
+
+__global__ __launch_bounds__(256) void witness_kernel(WitnessArgs a) {
+  const int64_t item = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (item >= a.n_vec * a.n_bands) return;
+  const int64_t vec = item / a.n_bands;
+  const int b = (int)(item % a.n_bands);
+  const int per_band = a.head_dim / a.n_bands;
+  float acc = 0.0f;
+  for (int kk = 0; kk < per_band; ++kk) {
+    const int c = band_channel(b, kk, a.head_dim, a.n_bands, a.interleaved);
+    const float r = load_any<float>(a.xhat, vec * a.head_dim + c, a.xhat_dtype) -
+                    load_any<float>(a.x, vec * a.head_dim + c, a.x_dtype);
+    acc = fmaf(r, r, acc);
+  }
+  a.w_out[item] = f16_round_up(sqrtf(acc) * (1.0f + 0x1p-18f));
+}
+
+template <int D, int KIND>
+hipError_t launch_write_dt(const WriteArgs& a, hipStream_t st) {
+  constexpr int TH = kWriteThreads / (D / 16);
+  const int64_t total = a.n_tok * (int64_t)a.n_kv;
+  const unsigned grid = (unsigned)((total + TH - 1) / TH);
+  if (a.in_dtype == WC_F32)
+    hipLaunchKernelGGL((quantize_write_kernel<D, KIND, float>), dim3(grid), dim3(kWriteThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((quantize_write_kernel<D, KIND, uint16_t>), dim3(grid), dim3(kWriteThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_write_d(const WriteArgs& a, hipStream_t st) {
+  switch (a.kind) {
+    case WC_KIND_INT8_DITHER: return launch_write_dt<D, WC_KIND_INT8_DITHER>(a, st);
+    case WC_KIND_FP8_RAW: return launch_write_dt<D, WC_KIND_FP8_RAW>(a, st);
+    default: return launch_write_dt<D, WC_KIND_BF16>(a, st);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_quantize_write(const WriteArgs& a, hipStream_t st) {
+  if (a.n_tok == 0) return hipSuccess;
+  return a.head_dim == 64 ? launch_write_d<64>(a, st) : launch_write_d<128>(a, st);
+}
+
+hipError_t launch_witness(const WitnessArgs& a, hipStream_t st) {
+  const int64_t items = a.n_vec * a.n_bands;
+  if (items == 0) return hipSuccess;
+  hipLaunchKernelGGL(witness_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace wc

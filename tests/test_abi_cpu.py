@@ -1,0 +1,70 @@
+"""The C-ABI library loads and exports every entry point of include/witcert.h;
+host-side argument checks and size queries work without a GPU (no compute call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_28699_amd import _lib
+
+HDR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "witcert.h")
+
+
+def declared_functions():
+    text = open(HDR).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(wc_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.fail("libwitcert.so is not built (run __graft_entry__.build())")
+    return _lib.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert set(names) == set(_lib.EXPORTS)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings_and_version(L):
+    assert L.wc_strerror(0) == b"ok"
+    assert L.wc_strerror(_lib.WC_EINVAL) == b"invalid argument"
+    assert L.wc_strerror(_lib.WC_EWORKSPACE) == b"workspace too small"
+    assert L.wc_version() >= 100
+
+
+def test_cache_byte_account(L):
+    sizes = (ctypes.c_size_t * 5)()
+    # one KV head, 32768 tokens, d = 128, B = 8: 128 + 128 + 2 + 2 + 16 = 276 B per token
+    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, sizes)
+    assert tot == 32768 * 276
+    assert list(sizes) == [32768 * 128, 32768 * 128, 65536, 65536, 32768 * 16]
+    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, sizes) == 32768 * 272
+    assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, sizes) == 32768 * 512
+    assert L.wc_cache_bytes(7, 1, 1, 128, 8, sizes) == 0
+
+
+def test_workspace_size_and_argument_checks(L):
+    n = L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 0)
+    assert n > 0 and n % 4 == 0
+    assert L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 512) == 4 * 28 * 64 * 132 * 4
+    assert L.wc_decode_workspace_size(-1, 28, 4, 128, 100, 0) == 0
+    # null cache / pointers are rejected before anything is launched
+    assert L.wc_quantize_write(None, None, None, 0, None, 1, None) == _lib.WC_EINVAL
+    c = _lib.WcCache(0, 96, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16)
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EUNSUPPORTED
+    c.head_dim = 128
+    c.k_data = 8                              # misaligned
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
+    assert L.wc_gate(None, None, 1, 28, 7, 0.2, None, None, None, None) == _lib.WC_EINVAL
+    assert L.wc_witness(None, 0, None, 0, 4, 128, 7, 0, None, None) == _lib.WC_EINVAL
+    c.k_data = 16
+    # workspace too small
+    st = L.wc_metered_decode_attention(ctypes.byref(c), 16, 1, 1, 7, 16, 4, 16, 64, 0.1, 16, 0,
+                                       16, 16, 0, 16, 8, None)
+    assert st == _lib.WC_EWORKSPACE

@@ -1,0 +1,123 @@
+"""GPU parity of the write path against the oracle (codes and scales bit-exact,
+witness within one fp16 step above the oracle's and never below it)."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import decode as odec
+from oracle import fpformats as ofp
+from oracle import quantizer as oq
+
+from . import support as S
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    ("tiny-d64-s256", [37]),
+    ("tiny-d64-s256", [256, 1, 17]),
+    ("gqa-28x4-d128-s4k-b8", [300, 45]),
+]
+
+
+@pytest.mark.parametrize("name,lens", CASES)
+@pytest.mark.parametrize("layout", ["half", "interleaved"])
+def test_int8_write_bitexact(name, lens, layout):
+    wl = synth.WORKLOADS[name].replace(rope_layout=layout)
+    S.say(f"[write-int8] {name} lens={lens} layout={layout}")
+    case = S.make_case(wl, lens, permute=True, layer=3)
+    cache = S.gpu_cache(case, "int8_dither")
+    ref = S.oracle_write(case, "int8_dither")
+    for b, r in enumerate(ref):
+        got = S.read_cache(cache, case["slots"][b])
+        assert np.array_equal(got["k"].astype(np.int64), r["kcode"])
+        assert np.array_equal(got["v"].astype(np.int64), r["vcode"])
+        assert np.array_equal(got["ks"], r["ks"])
+        assert np.array_equal(got["vs"], r["vs"])
+        assert np.all(got["kw"] >= r["kw"])
+        assert np.all(got["kw"] <= S.next_f16_up(r["kw"]))
+        # the stored witness bounds the residual of the stored reconstruction
+        assert np.all(got["kw"] >= oq.band_norms(r["khat"] - case["k"][b], wl.bands, layout) * (1 - 1e-12))
+
+
+@pytest.mark.parametrize("name,lens", CASES[1:])
+def test_fp8_write_bitexact(name, lens):
+    wl = synth.WORKLOADS[name]
+    S.say(f"[write-fp8] {name} lens={lens}")
+    case = S.make_case(wl, lens, permute=True, layer=1)
+    cache = S.gpu_cache(case, "fp8_raw")
+    ref = S.oracle_write(case, "fp8_raw")
+    for b, r in enumerate(ref):
+        got = S.read_cache(cache, case["slots"][b])
+        assert np.array_equal(got["k"], ofp.e4m3_encode(case["k"][b]))
+        assert np.array_equal(got["v"], ofp.e4m3_encode(case["v"][b]))
+        assert np.all(got["kw"] >= r["kw"]) and np.all(got["kw"] <= S.next_f16_up(r["kw"]))
+
+
+def test_fp8_cast_saturates_and_keeps_sign():
+    import torch
+
+    import paper_2607_28699_amd as wc
+    wl = synth.WORKLOADS["gqa-28x4-d128-s4k-b8"].replace(n_kv=1, n_q=7, dtype="f32")
+    S.say("[write-fp8] extremes")
+    x = np.zeros((4, 1, 128), np.float32)
+    x[0, 0, :4] = [448.0, -448.0, 447.9, -1e-12]
+    x[1, 0, :4] = [600.0, -2000.0, 2.0 ** -9, 2.0 ** -10]    # beyond 448: saturating reading
+    x[2, 0] = np.linspace(-300, 300, 128)
+    x[3, 0] = np.linspace(-1e-3, 1e-3, 128)
+    c = wc.PagedCache("fp8_raw", 1, 1, 128, 8)
+    wc.quantize_write(c, torch.from_numpy(x).cuda(), torch.from_numpy(x).cuda(),
+                      torch.arange(4, dtype=torch.int64).cuda())
+    torch.cuda.synchronize()
+    got = S.read_cache(c, np.arange(4))
+    assert np.array_equal(got["k"][:, 0], ofp.e4m3_encode(x[:, 0]))
+    _ = wl
+
+
+def test_bf16_write_is_exact_copy():
+    import torch
+    wl = synth.WORKLOADS["gqa-28x4-d128-s4k-b8"]
+    S.say("[write-bf16]")
+    case = S.make_case(wl, [50, 7], permute=True)
+    cache = S.gpu_cache(case, "bf16")
+    for b in range(2):
+        got = S.read_cache(cache, case["slots"][b])
+        want_k = synth.to_bf16_bits(case["k"][b]).view(np.int16)
+        want_v = synth.to_bf16_bits(case["v"][b]).view(np.int16)
+        assert np.array_equal(got["k"], want_k) and np.array_equal(got["v"], want_v)
+    _ = torch
+
+
+def test_zero_token_has_zero_scale_codes_and_witness():
+    import torch
+
+    import paper_2607_28699_amd as wc
+    S.say("[write-int8] zero rows")
+    x = np.zeros((3, 2, 128), np.float32)
+    x[1, 1, 5] = 1.0
+    c = wc.PagedCache("int8_dither", 1, 2, 128, 8, seed=5)
+    wc.quantize_write(c, torch.from_numpy(x).cuda(), torch.from_numpy(x).cuda(),
+                      torch.tensor([3, 9, 15], dtype=torch.int64).cuda())
+    torch.cuda.synchronize()
+    got = S.read_cache(c, np.array([3, 9, 15]))
+    assert np.all(got["ks"][0] == 0) and np.all(got["k"][0] == 0) and np.all(got["kw"][0] == 0)
+    ref = odec.write_cache("int8_dither", x[1:2], x[1:2], np.array([9]), 0, 5, 8)
+    assert np.array_equal(got["k"][1:2].astype(np.int64), ref["kcode"])
+    assert np.array_equal(got["kw"][1:2], np.maximum(got["kw"][1:2], ref["kw"]))
+
+
+@pytest.mark.parametrize("dts", [("f32", "f32"), ("bf16", "f32"), ("f32", "f16"), ("bf16", "bf16")])
+@pytest.mark.parametrize("layout", ["half", "interleaved"])
+def test_blackbox_witness(dts, layout):
+    import torch
+
+    import paper_2607_28699_amd as wc
+    S.say(f"[witness] {dts} {layout}")
+    rng = np.random.default_rng(3)
+    tmap = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+    x = torch.from_numpy(rng.standard_normal((333, 128)).astype(np.float32) * 3).to(tmap[dts[0]])
+    xh = (x.float() + torch.from_numpy(rng.standard_normal((333, 128)).astype(np.float32)) * 0.05).to(tmap[dts[1]])
+    w = wc.witness(x.cuda(), xh.cuda(), 16, layout)
+    torch.cuda.synchronize()
+    ref = oq.witness(x.double().numpy(), xh.double().numpy(), 16, layout)
+    got = w.cpu().double().numpy()
+    assert np.all(got >= ref) and np.all(got <= S.next_f16_up(ref))
