@@ -1,0 +1,320 @@
+"""Throughput of the WitCert hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--tau T]
+
+One step = one decode step of every layer of the workload, each layer running the
+whole hot path on the GPU: the new token of every sequence written through the
+dithered INT8 quantizer with its witness (and into the exact bf16 cache), the
+metered decode attention over the INT8 cache, the gate at tau, and the exact
+fallback for the routed KV heads.  The serving mix also writes one prefill
+chunk per layer and step.  Caches are filled (prefill write, timed separately
+as the quant+witness figure) and every decode-step input is generated on the
+GPU before the timed region.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0       # MI355X HBM3E
+INT8_BYTES = 276             # per token-head at d=128, B=8: 128+128 codes, 2+2 scales, 16 witness
+FP8_BYTES = 272
+BF16_BYTES = 512
+WRITE_BYTES_BF16_IN = 512 + 276
+DECODE_KERNEL_SRC = os.path.join(ROOT, "paper_2607_28699_amd", "csrc")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(DECODE_KERNEL_SRC)):
+        with open(os.path.join(DECODE_KERNEL_SRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=8)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="gqa-28x4-d128-s32k-b4")
+    ap.add_argument("--tau", type=float, default=0.2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of known size (HBM counter calibration)")
+    return ap.parse_args()
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 28                     # 256 MiB each way
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_each_way": n, "launches": 3}), flush=True)
+
+
+class Layout:
+    """Slots of the decode sequences (and of the serving mix's prefill chunks)."""
+
+    def __init__(self, wl, lens, extra_steps, np):
+        self.lens = np.asarray(lens, dtype=np.int64)
+        cap = self.lens + extra_steps
+        chunk_cap = wl.chunk * extra_steps if wl.chunk else 0
+        caps = np.concatenate([cap, [chunk_cap]]) if wl.chunk else cap
+        import synth
+        self.table, self.nblocks = synth.block_table(caps, permute=wl.ragged, seed_key=wl.wid)
+        self.batch = len(lens)
+
+    def slots(self, seq, positions, np):
+        return self.table[seq, positions // 16].astype(np.int64) * 16 + positions % 16
+
+
+def cpu_baseline(wl, lens, tau, seconds, np, torch):
+    """The oracle, as it stands, on a bounded sample of the same workload: per
+    sampled (sequence, layer), write the new token, metered decode over the
+    sequence, gate, exact fallback.  Prefill quantization of the sample is not timed."""
+    import threadpoolctl
+
+    from oracle import decode as odec
+    from oracle import gate as ogate
+    from synth import torch_gen
+    sm = 1.0 / np.sqrt(wl.d)
+    timed, tokens, samples = 0.0, 0, 0
+    layer_ids = list(range(wl.n_layers))
+    for i in range(64):
+        seq = i % len(lens)
+        layer = layer_ids[(i * 7) % len(layer_ids)]
+        L = int(lens[seq])
+        pos = torch.arange(L, device="cuda")
+        k, v = torch_gen.gen_kv_layer(wl, layer, seq, pos)
+        kn, vn = torch_gen.gen_kv_layer(wl, layer, seq, torch.tensor([L], device="cuda"), step=0)
+        q = torch_gen.gen_q_batch(wl, layer, 0, torch.tensor([L], device="cuda"))[0]
+        k, v, kn, vn, q = (x.float().cpu().numpy().astype(np.float64) for x in (k, v, kn, vn, q))
+        slots = np.arange(L + 1, dtype=np.int64)
+        cache = odec.write_cache("int8_dither", k, v, slots[:L], layer, wl.philox_seed(), wl.bands,
+                                 wl.rope_layout)
+        t0 = time.perf_counter()
+        new = odec.write_cache("int8_dither", kn, vn, slots[L:], layer, wl.philox_seed(), wl.bands,
+                               wl.rope_layout)
+        kh = np.concatenate([cache["khat"], new["khat"]])
+        vh = np.concatenate([cache["vhat"], new["vhat"]])
+        kw = np.concatenate([cache["kw"], new["kw"]])
+        res = odec.metered_decode(q, kh, vh, kw, sm, wl.bands, wl.rope_layout)
+        mq = ogate.gate_q(res["meter"], res["raw"], tau)
+        mkv = ogate.gate_kv(mq[None], wl.group)[0]
+        ex = odec.exact_decode(q, np.concatenate([k, kn]), np.concatenate([v, vn]), sm)
+        _ = ogate.apply_fallback(res["out"], ex["out"], mkv, wl.group)
+        timed += time.perf_counter() - t0
+        tokens += L + 1
+        samples += 1
+        if timed >= seconds:
+            break
+    info = threadpoolctl.threadpool_info()
+    blas = max([p.get("num_threads", 1) for p in info if p.get("user_api") == "blas"] or [1])
+    return {"value": tokens / timed, "unit": "KV tokens/s", "cores": int(blas), "kind": "oracle",
+            "sample": (f"{samples} (sequence, layer) cells at context {int(lens[0])}: new-token write, "
+                       f"metered decode of all {wl.n_q} query heads, gate at tau={tau}, exact fallback; "
+                       f"{timed:.1f} s of oracle time (float64 numpy; BLAS threads={blas}, "
+                       f"elementwise single-threaded)")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the hot path shards by sequence and KV head, see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    import paper_2607_28699_amd as wc
+    import synth
+    from synth import torch_gen
+
+    wl = synth.WORKLOADS[args.workload]
+    dev = "cuda"
+    K, W = args.steps, args.warmup
+    lens0 = (synth.serving_lengths(wl.batch, wl.len_lo, wl.ctx) if wl.ragged
+             else np.full(wl.batch, wl.ctx, dtype=np.int64))
+    lay = Layout(wl, lens0, K + W, np)
+    sm = 1.0 / np.sqrt(wl.d)
+    seed = wl.philox_seed()
+
+    # ---- caches and prefill write (timed separately: quant+witness throughput) ----
+    caches, exact = [], []
+    write_ms, write_tokens = 0.0, 0
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for layer in range(wl.n_layers):
+        c = wc.PagedCache("int8_dither", lay.nblocks, wl.n_kv, wl.d, wl.bands, layer=layer, seed=seed,
+                          rope_layout=wl.rope_layout)
+        e = wc.PagedCache("bf16", lay.nblocks, wl.n_kv, wl.d, 0, layer=layer)
+        for b in range(lay.batch):
+            L = int(lens0[b])
+            pos = torch.arange(L, device=dev)
+            k, v = torch_gen.gen_kv_layer(wl, layer, b, pos)
+            sl = torch.from_numpy(lay.slots(b, np.arange(L), np)).to(dev)
+            ev0.record()
+            wc.quantize_write(c, k, v, sl)
+            ev1.record()
+            wc.quantize_write(e, k, v, sl)
+            torch.cuda.synchronize()
+            write_ms += ev0.elapsed_time(ev1)
+            write_tokens += L * wl.n_kv
+        caches.append(c)
+        exact.append(e)
+    torch.cuda.synchronize()
+
+    # ---- decode-step inputs, resident before timing ----
+    steps_in = []
+    table = torch.from_numpy(lay.table).to(dev)
+    for s in range(K + W):
+        pos = torch.from_numpy(lens0 + s).to(dev)
+        lens = torch.from_numpy((lens0 + s + 1).astype(np.int32)).to(dev)
+        slots = torch.from_numpy(np.array([lay.slots(b, np.array([lens0[b] + s]), np)[0]
+                                           for b in range(lay.batch)], dtype=np.int64)).to(dev)
+        per_layer = []
+        for layer in range(wl.n_layers):
+            q = torch_gen.gen_q_batch(wl, layer, s, pos)
+            kv = [torch_gen.gen_kv_layer(wl, layer, b, pos[b:b + 1], step=s) for b in range(lay.batch)]
+            kn = torch.cat([x[0] for x in kv])
+            vn = torch.cat([x[1] for x in kv])
+            item = {"q": q, "k": kn, "v": vn}
+            if wl.chunk:
+                cpos = torch.arange(s * wl.chunk, (s + 1) * wl.chunk, device=dev)
+                ck, cv = torch_gen.gen_kv_layer(wl, layer, lay.batch, cpos, step=s)
+                item["ck"], item["cv"] = ck, cv
+                item["cslots"] = torch.from_numpy(lay.slots(lay.batch, cpos.cpu().numpy(), np)).to(dev)
+            per_layer.append(item)
+        steps_in.append({"lens": lens, "slots": slots, "max_len": int(lens0.max() + s + 1),
+                         "tokens": int((lens0 + s + 1).sum()), "layers": per_layer})
+    max_len_all = int(lens0.max() + K + W)
+    ws = wc.decode_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all)
+    out = torch.empty((lay.batch, wl.n_q, wl.d), dtype=torch.bfloat16, device=dev)
+    meter = torch.empty((lay.batch, wl.n_q), dtype=torch.float32, device=dev)
+    raw = torch.empty_like(meter)
+    mask_q = torch.empty((lay.batch, wl.n_q), dtype=torch.uint8, device=dev)
+    mask_kv = torch.empty((lay.batch, wl.n_kv), dtype=torch.uint8, device=dev)
+    counts = torch.zeros(2, dtype=torch.int32, device=dev)
+    n_ev = K * wl.n_layers
+    dec_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(n_ev)]
+    fb_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(n_ev)]
+
+    def run_step(si, timed_idx):
+        st = steps_in[si]
+        for layer in range(wl.n_layers):
+            it = st["layers"][layer]
+            if wl.chunk:
+                wc.quantize_write(caches[layer], it["ck"], it["cv"], it["cslots"])
+                wc.quantize_write(exact[layer], it["ck"], it["cv"], it["cslots"])
+            wc.quantize_write(caches[layer], it["k"], it["v"], st["slots"])
+            wc.quantize_write(exact[layer], it["k"], it["v"], st["slots"])
+            if timed_idx is not None:
+                dec_ev[timed_idx * wl.n_layers + layer][0].record()
+            wc.metered_decode_attention(caches[layer], it["q"], table, st["lens"], max_len_all, sm,
+                                        ws=ws, out=out, meter=meter, raw=raw)
+            if timed_idx is not None:
+                dec_ev[timed_idx * wl.n_layers + layer][1].record()
+            wc.gate(meter, raw, wl.group, args.tau, n_gated=counts, mask_q=mask_q, mask_kv=mask_kv)
+            if timed_idx is not None:
+                fb_ev[timed_idx * wl.n_layers + layer][0].record()
+            wc.exact_decode_attention(exact[layer], it["q"], table, st["lens"], max_len_all, sm,
+                                      mask_kv, out, ws=ws)
+            if timed_idx is not None:
+                fb_ev[timed_idx * wl.n_layers + layer][1].record()
+
+    for s in range(W):
+        run_step(s, None)
+    torch.cuda.synchronize()
+    counts.zero_()
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for s in range(K):
+        run_step(W + s, s)
+    t_end.record()
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / K
+    kv_tokens = sum(steps_in[W + s]["tokens"] for s in range(K)) * wl.n_layers
+    value = kv_tokens / (total_ms / 1e3)
+
+    dec_ms = np.array([a.elapsed_time(b) for a, b in dec_ev])
+    fb_ms = np.array([a.elapsed_time(b) for a, b in fb_ev])
+    th_per_launch = np.array([steps_in[W + s]["tokens"] * wl.n_kv for s in range(K)
+                              for _ in range(wl.n_layers)], dtype=np.float64)
+    dec_gbps = float(np.mean(th_per_launch * INT8_BYTES) / (dec_ms.mean() * 1e-3) / 1e9)
+    gq, gkv = counts.cpu().tolist()
+    frac_kv = gkv / (K * wl.n_layers * lay.batch * wl.n_kv)
+    frac_q = gq / (K * wl.n_layers * lay.batch * wl.n_q)
+    fb_bytes = float(np.mean(th_per_launch) * frac_kv * BF16_BYTES)
+    fb_gbps = fb_bytes / (fb_ms.mean() * 1e-3) / 1e9 if fb_ms.mean() > 0 else 0.0
+    write_gbps = write_tokens * WRITE_BYTES_BF16_IN / (write_ms * 1e-3) / 1e9
+
+    dominant = "metered_decode" if dec_ms.sum() >= fb_ms.sum() else "exact_fallback"
+    traffic = None
+    prof = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
+    if os.path.exists(prof):
+        with open(prof) as fh:
+            pj = json.load(fh)
+        if pj.get("kernel_source_hash") == kernel_source_hash():
+            traffic = pj.get("bytes_per_launch", {}).get(dominant)
+    if dominant == "metered_decode":
+        roof = {"kernel": "metered decode (split + merge kernels)", "bound": "hbm",
+                "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                "algorithmic_bytes_per_launch": float(np.mean(th_per_launch * INT8_BYTES)),
+                "avg_launch_ms": round(float(dec_ms.mean()), 4)}
+    else:
+        roof = {"kernel": "exact bf16 fallback (split + merge kernels)", "bound": "hbm",
+                "achieved": round(fb_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(fb_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                "algorithmic_bytes_per_launch": fb_bytes,
+                "avg_launch_ms": round(float(fb_ms.mean()), 4)}
+
+    line = {
+        "metric": "metered INT8 decode-attn KV tokens/s & HBM GB/s (% peak); quant+witness GB/s",
+        "value": round(value, 1), "unit": "KV tokens/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "layers": wl.n_layers, "n_q": wl.n_q, "n_kv": wl.n_kv,
+                   "head_dim": wl.d, "bands": wl.bands, "batch": lay.batch,
+                   "context": int(lens0.max()), "mean_context": float(lens0.mean()),
+                   "tau": args.tau, "cache": "int8 dither + fp16 scales + fp16 key witness",
+                   "fallback": "bf16 exact cache in HBM"},
+        "roofline": roof,
+        "metered_decode": {"avg_launch_ms": round(float(dec_ms.mean()), 4), "GBps": round(dec_gbps, 1),
+                           "frac_hbm": round(dec_gbps / HBM_PEAK_GBPS, 4),
+                           "bytes_per_token_head": INT8_BYTES},
+        "exact_fallback": {"avg_launch_ms": round(float(fb_ms.mean()), 4), "GBps": round(fb_gbps, 1),
+                           "frac_hbm": round(fb_gbps / HBM_PEAK_GBPS, 4)},
+        "gate": {"tau": args.tau, "fraction_q_heads": round(frac_q, 4),
+                 "fraction_kv_heads": round(frac_kv, 4)},
+        "quant_witness": {"GBps": round(write_gbps, 1), "frac_hbm": round(write_gbps / HBM_PEAK_GBPS, 4),
+                          "bytes_per_token_head": WRITE_BYTES_BF16_IN,
+                          "token_heads": write_tokens},
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, lens0, args.tau, args.cpu_seconds, np, torch)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

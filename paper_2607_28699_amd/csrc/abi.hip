@@ -2,6 +2,7 @@
 // Every entry point validates on the host, enqueues on the caller's stream and
 // returns; nothing allocates, synchronizes or reads device memory back.
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include "wc_launch.h"
@@ -166,6 +167,10 @@ static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int 
   a.key0 = (uint32_t)cache->seed;
   a.key1 = (uint32_t)(cache->seed >> 32);
   a.sm_scale = sm_scale;
+  // WITCERT_FORCE_VALU=1 selects the vector-ALU kernels even where the
+  // matrix-core ones apply (used to cross-check the two paths)
+  const char* force = getenv("WITCERT_FORCE_VALU");
+  a.use_mfma = !(force && force[0] == '1');
   return WC_OK;
 }
 

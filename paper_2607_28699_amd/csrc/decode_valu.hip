@@ -387,8 +387,23 @@ int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested)
   return (int)st;
 }
 
+hipError_t launch_merge(const DecodeArgs& a, bool metered, hipStream_t st) {
+  if (a.head_dim == 64) {
+    if (metered) hipLaunchKernelGGL((merge_kernel<64, true>), dim3(a.batch * a.n_q), dim3(64), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<64, false>), dim3(a.batch * a.n_q), dim3(64), 0, st, a);
+  } else {
+    if (metered) hipLaunchKernelGGL((merge_kernel<128, true>), dim3(a.batch * a.n_q), dim3(64), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<128, false>), dim3(a.batch * a.n_q), dim3(64), 0, st, a);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_decode(const DecodeArgs& a, bool metered, hipStream_t st) {
   if (a.batch == 0 || a.n_q == 0) return hipSuccess;
+  if (a.use_mfma && mfma_decode_supported(a)) {
+    hipError_t e = launch_decode_mfma(a, metered, st);
+    return e != hipSuccess ? e : launch_merge(a, metered, st);
+  }
   return a.head_dim == 64 ? launch_d<64>(a, metered, st) : launch_d<128>(a, metered, st);
 }
 

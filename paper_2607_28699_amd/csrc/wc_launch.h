@@ -50,6 +50,7 @@ struct DecodeArgs {
   int batch, n_q, n_kv, group, max_blocks, n_splits, split_tokens, layer;
   uint32_t key0, key1;
   float sm_scale;
+  int use_mfma;             // matrix-core kernels where supported (else the vector path)
 };
 
 struct GateArgs {
@@ -72,6 +73,9 @@ __host__ __device__ inline size_t partial_record_floats(int head_dim) { return (
 hipError_t launch_quantize_write(const WriteArgs& a, hipStream_t st);
 hipError_t launch_witness(const WitnessArgs& a, hipStream_t st);
 hipError_t launch_decode(const DecodeArgs& a, bool metered, hipStream_t st);
+bool mfma_decode_supported(const DecodeArgs& a);
+hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st);
+hipError_t launch_merge(const DecodeArgs& a, bool metered, hipStream_t st);
 hipError_t launch_gate(const GateArgs& a, hipStream_t st);
 
 }  // namespace wc

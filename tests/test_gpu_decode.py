@@ -66,9 +66,12 @@ def test_split_count_invariance():
     o1, m1, r1 = S.gpu_decode(case, cache, split_tokens=64)
     o2, m2, r2 = S.gpu_decode(case, cache, split_tokens=2048)
     o3, m3, r3 = S.gpu_decode(case, cache, split_tokens=0)
+    # the merge is exact in exact arithmetic; numerically the splits differ by the
+    # rounding of the fp16 softmax weights relative to each split's running max
+    tol = S.out_tol(W_GQA)
     for o, r in ((o2, r2), (o3, r3)):
-        assert S.rel_err(o, o1) < 1e-5
-        assert np.all(np.abs(r - r1) <= 1e-5 * np.abs(r1))
+        assert S.rel_err(o, o1) < tol
+        assert np.all(np.abs(r - r1) <= tol * np.abs(r1))
 
 
 def test_bf16_output_is_rounded_fp32_output():

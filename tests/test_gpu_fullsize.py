@@ -1,0 +1,121 @@
+"""Parity at the full workload sizes, in the launch configuration bench.py times.
+
+One layer of each long-context workload is written through wc_quantize_write and
+decoded with the same split choice as the benchmark (max_seq_len = prefill +
+steps + warmup); sampled (sequence, query head) cells are recomputed by the
+oracle one by one from the stored inputs of that cell, and sampled tokens'
+codes are compared bit-exactly.  Also: the matrix-core and vector-ALU decode
+paths agree on the same cache.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import decode as odec
+from oracle import quantizer as oq
+
+from . import support as S
+
+pytestmark = pytest.mark.gpu
+
+BENCH_STEPS, BENCH_WARMUP = 8, 2
+
+
+def _setup(name, n_lens=None):
+    import torch
+
+    import paper_2607_28699_amd as wc
+    from synth import torch_gen
+    wl = synth.WORKLOADS[name]
+    lens0 = (synth.serving_lengths(wl.batch, wl.len_lo, wl.ctx) if wl.ragged
+             else np.full(wl.batch, wl.ctx, dtype=np.int64))
+    if n_lens is not None:
+        lens0 = lens0[:n_lens]
+    extra = BENCH_STEPS + BENCH_WARMUP
+    table, nblocks = synth.block_table(lens0 + extra, permute=wl.ragged, seed_key=wl.wid)
+    layer = 5
+    cache = wc.PagedCache("int8_dither", nblocks, wl.n_kv, wl.d, wl.bands, layer=layer,
+                          seed=wl.philox_seed(), rope_layout=wl.rope_layout)
+    kv = []
+    for b, L in enumerate(lens0):
+        pos = torch.arange(int(L) + 1, device="cuda")
+        k, v = torch_gen.gen_kv_layer(wl, layer, b, pos)
+        sl = synth.slots_of(table, b, np.arange(int(L) + 1))
+        wc.quantize_write(cache, k, v, torch.from_numpy(sl).cuda())
+        kv.append((k, v, sl))
+    pos = torch.from_numpy(lens0).cuda()
+    q = torch_gen.gen_q_batch(wl, layer, 0, pos)
+    lens = torch.from_numpy((lens0 + 1).astype(np.int32)).cuda()
+    tab = torch.from_numpy(table).cuda()
+    max_len = int(lens0.max() + extra)
+    return wl, lens0, cache, kv, q, tab, lens, max_len, layer
+
+
+def _cell_check(wl, kv, q, b, h, layer):
+    """Oracle result for query head h of sequence b from that cell's stored inputs."""
+    k, v, sl = kv[b]
+    g = h // wl.group
+    kb = k[:, g].float().cpu().numpy().astype(np.float64)
+    vb = v[:, g].float().cpu().numpy().astype(np.float64)
+    qb = q[b, h:h + 1].float().cpu().numpy().astype(np.float64)
+    kc, ks, _, kh = oq.int8_quantize_slots(kb, sl, layer, g, wl.philox_seed())
+    vc, vs, _, vh = oq.int8_quantize_slots(vb, sl, layer, g, wl.philox_seed())
+    kw = oq.witness(kb, kh, wl.bands, wl.rope_layout)
+    sm = 1 / np.sqrt(wl.d)
+    res = odec.metered_decode(qb, kh[:, None], vh[:, None], kw[:, None], sm, wl.bands, wl.rope_layout)
+    tv = odec.true_tv(qb, kb[:, None], kh[:, None], sm)
+    return res, tv, kc, vc, ks
+
+
+@pytest.mark.parametrize("name,n_lens", [("gqa-28x4-d128-s32k-b4", None),
+                                         ("gqa-28x4-d128-s131k-b1", None),
+                                         ("serving-64seq-paged", 16)])
+def test_fullsize_sampled_cells(name, n_lens):
+    import torch
+
+    import paper_2607_28699_amd as wc
+    S.say(f"[fullsize] {name}")
+    wl, lens0, cache, kv, q, tab, lens, max_len, layer = _setup(name, n_lens)
+    out, meter, raw = wc.metered_decode_attention(cache, q, tab, lens, max_len, 1 / np.sqrt(wl.d))
+    torch.cuda.synchronize()
+    out, meter, raw = out.cpu().numpy(), meter.cpu().numpy(), raw.cpu().numpy()
+    rng = np.random.default_rng(17)
+    cells = [(int(rng.integers(len(lens0))), int(rng.integers(wl.n_q))) for _ in range(3)]
+    for b, h in cells:
+        S.say(f"  cell b={b} h={h} L={int(lens0[b]) + 1}")
+        res, tv, kc, vc, ks = _cell_check(wl, kv, q, b, h, layer)
+        assert S.rel_err(out[b, h], res["out"][0]) <= 2e-3
+        assert abs(raw[b, h] - res["raw"][0]) <= 2e-3 * res["raw"][0]
+        assert meter[b, h] >= tv[0]
+        # codes of sampled tokens of this cell, bit-exact
+        sl = kv[b][2]
+        pick = rng.choice(len(sl), 512, replace=False)
+        got = S.read_cache(cache, sl[pick])
+        g = h // wl.group
+        assert np.array_equal(got["k"][:, g].astype(np.int64), kc[pick])
+        assert np.array_equal(got["v"][:, g].astype(np.int64), vc[pick])
+        assert np.array_equal(got["ks"][:, g], ks[pick])
+
+
+def test_matrix_core_and_vector_paths_agree():
+    import torch
+
+    import paper_2607_28699_amd as wc
+    S.say("[fullsize] mfma vs valu")
+    wl = synth.WORKLOADS["gqa-28x4-d128-s4k-b8"]
+    case = S.make_case(wl, [4097, 1000, 33, 1], permute=True)
+    out = {}
+    for kind in ("int8_dither", "fp8_raw"):
+        cache = S.gpu_cache(case, kind)
+        a = S.gpu_decode(case, cache)
+        os.environ["WITCERT_FORCE_VALU"] = "1"
+        try:
+            bv = S.gpu_decode(case, cache)
+        finally:
+            del os.environ["WITCERT_FORCE_VALU"]
+        assert S.rel_err(a[0], bv[0]) <= 2e-3
+        assert np.all(np.abs(a[2] - bv[2]) <= 2e-3 * np.abs(bv[2]))
+        out[kind] = a
+    _ = torch
