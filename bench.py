@@ -158,25 +158,30 @@ def main():
     # ---- caches and prefill write (timed separately: quant+witness throughput) ----
     caches, exact = [], []
     write_ms, write_tokens = 0.0, 0
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     for layer in range(wl.n_layers):
         c = wc.PagedCache("int8_dither", lay.nblocks, wl.n_kv, wl.d, wl.bands, layer=layer, seed=seed,
                           rope_layout=wl.rope_layout)
         e = wc.PagedCache("bf16", lay.nblocks, wl.n_kv, wl.d, 0, layer=layer)
+        gen = []
         for b in range(lay.batch):
             L = int(lens0[b])
-            pos = torch.arange(L, device=dev)
-            k, v = torch_gen.gen_kv_layer(wl, layer, b, pos)
-            sl = torch.from_numpy(lay.slots(b, np.arange(L), np)).to(dev)
+            k, v = torch_gen.gen_kv_layer(wl, layer, b, torch.arange(L, device=dev))
+            gen.append((k, v, torch.from_numpy(lay.slots(b, np.arange(L), np)).to(dev)))
+        evs = []
+        for k, v, sl in gen:       # back to back, so the GPU never waits between the events
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             ev0.record()
             wc.quantize_write(c, k, v, sl)
             ev1.record()
+            evs.append((ev0, ev1))
+            write_tokens += k.shape[0] * wl.n_kv
+        for k, v, sl in gen:
             wc.quantize_write(e, k, v, sl)
-            torch.cuda.synchronize()
-            write_ms += ev0.elapsed_time(ev1)
-            write_tokens += L * wl.n_kv
+        torch.cuda.synchronize()
+        write_ms += sum(a.elapsed_time(b) for a, b in evs)
         caches.append(c)
         exact.append(e)
+        del gen
     torch.cuda.synchronize()
 
     # ---- decode-step inputs, resident before timing ----
@@ -200,8 +205,8 @@ def main():
                 item["ck"], item["cv"] = ck, cv
                 item["cslots"] = torch.from_numpy(lay.slots(lay.batch, cpos.cpu().numpy(), np)).to(dev)
             per_layer.append(item)
-        steps_in.append({"lens": lens, "slots": slots, "max_len": int(lens0.max() + s + 1),
-                         "tokens": int((lens0 + s + 1).sum()), "layers": per_layer})
+        steps_in.append({"lens": lens, "slots": slots, "tokens": int((lens0 + s + 1).sum()),
+                         "layers": per_layer})
     max_len_all = int(lens0.max() + K + W)
     ws = wc.decode_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all)
     out = torch.empty((lay.batch, wl.n_q, wl.d), dtype=torch.bfloat16, device=dev)
@@ -210,13 +215,8 @@ def main():
     mask_q = torch.empty((lay.batch, wl.n_q), dtype=torch.uint8, device=dev)
     mask_kv = torch.empty((lay.batch, wl.n_kv), dtype=torch.uint8, device=dev)
     counts = torch.zeros(2, dtype=torch.int32, device=dev)
-    n_ev = K * wl.n_layers
-    dec_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(n_ev)]
-    fb_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(n_ev)]
 
-    def run_step(si, timed_idx):
+    def run_step(si):
         st = steps_in[si]
         for layer in range(wl.n_layers):
             it = st["layers"][layer]
@@ -225,49 +225,70 @@ def main():
                 wc.quantize_write(exact[layer], it["ck"], it["cv"], it["cslots"])
             wc.quantize_write(caches[layer], it["k"], it["v"], st["slots"])
             wc.quantize_write(exact[layer], it["k"], it["v"], st["slots"])
-            if timed_idx is not None:
-                dec_ev[timed_idx * wl.n_layers + layer][0].record()
             wc.metered_decode_attention(caches[layer], it["q"], table, st["lens"], max_len_all, sm,
                                         ws=ws, out=out, meter=meter, raw=raw)
-            if timed_idx is not None:
-                dec_ev[timed_idx * wl.n_layers + layer][1].record()
             wc.gate(meter, raw, wl.group, args.tau, n_gated=counts, mask_q=mask_q, mask_kv=mask_kv)
-            if timed_idx is not None:
-                fb_ev[timed_idx * wl.n_layers + layer][0].record()
             wc.exact_decode_attention(exact[layer], it["q"], table, st["lens"], max_len_all, sm,
                                       mask_kv, out, ws=ws)
-            if timed_idx is not None:
-                fb_ev[timed_idx * wl.n_layers + layer][1].record()
 
+    # one decode step per HIP graph (all layers), replayed back to back: the timed
+    # region is GPU work only, as in a graph-captured serving loop
+    run_step(0)
+    torch.cuda.synchronize()
+    graphs = []
+    for s in range(K + W):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            run_step(s)
+        graphs.append(g)
     for s in range(W):
-        run_step(s, None)
+        graphs[s].replay()
     torch.cuda.synchronize()
     counts.zero_()
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start.record()
     for s in range(K):
-        run_step(W + s, s)
+        graphs[W + s].replay()
     t_end.record()
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / K
     kv_tokens = sum(steps_in[W + s]["tokens"] for s in range(K)) * wl.n_layers
     value = kv_tokens / (total_ms / 1e3)
-
-    dec_ms = np.array([a.elapsed_time(b) for a, b in dec_ev])
-    fb_ms = np.array([a.elapsed_time(b) for a, b in fb_ev])
-    th_per_launch = np.array([steps_in[W + s]["tokens"] * wl.n_kv for s in range(K)
-                              for _ in range(wl.n_layers)], dtype=np.float64)
-    dec_gbps = float(np.mean(th_per_launch * INT8_BYTES) / (dec_ms.mean() * 1e-3) / 1e9)
     gq, gkv = counts.cpu().tolist()
     frac_kv = gkv / (K * wl.n_layers * lay.batch * wl.n_kv)
     frac_q = gq / (K * wl.n_layers * lay.batch * wl.n_q)
-    fb_bytes = float(np.mean(th_per_launch) * frac_kv * BF16_BYTES)
-    fb_gbps = fb_bytes / (fb_ms.mean() * 1e-3) / 1e9 if fb_ms.mean() > 0 else 0.0
+
+    # ---- per-kernel timing (eager, launches back to back, events on the launch stream) ----
+    def timed(fn, reps):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        torch.cuda.synchronize()
+        for i in range(reps):
+            evs[i][0].record()
+            fn(i)
+            evs[i][1].record()
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) for a, b in evs])
+
+    last = steps_in[W + K - 1]
+    reps = 2 * wl.n_layers
+    dec_ms = timed(lambda i: wc.metered_decode_attention(
+        caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
+        max_len_all, sm, ws=ws, out=out, meter=meter, raw=raw), reps)
+    wc.gate(meter, raw, wl.group, args.tau, mask_q=mask_q, mask_kv=mask_kv)
+    fb_ms = timed(lambda i: wc.exact_decode_attention(
+        exact[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
+        max_len_all, sm, mask_kv, out, ws=ws), reps)
+    th_per_launch = float(last["tokens"] * wl.n_kv)
+    dec_gbps = th_per_launch * INT8_BYTES / (float(np.median(dec_ms)) * 1e-3) / 1e9
+    routed = float(mask_kv.float().mean().item())
+    fb_bytes = th_per_launch * routed * BF16_BYTES
+    fb_gbps = fb_bytes / (float(np.median(fb_ms)) * 1e-3) / 1e9 if routed > 0 else 0.0
     write_gbps = write_tokens * WRITE_BYTES_BF16_IN / (write_ms * 1e-3) / 1e9
 
-    dominant = "metered_decode" if dec_ms.sum() >= fb_ms.sum() else "exact_fallback"
+    dominant = "metered_decode" if float(np.median(dec_ms)) >= float(np.median(fb_ms)) else "exact_fallback"
     traffic = None
     prof = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
     if os.path.exists(prof):
@@ -276,17 +297,17 @@ def main():
         if pj.get("kernel_source_hash") == kernel_source_hash():
             traffic = pj.get("bytes_per_launch", {}).get(dominant)
     if dominant == "metered_decode":
-        roof = {"kernel": "metered decode (split + merge kernels)", "bound": "hbm",
+        roof = {"kernel": "metered decode (decode_mfma_kernel + merge_kernel)", "bound": "hbm",
                 "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                "algorithmic_bytes_per_launch": float(np.mean(th_per_launch * INT8_BYTES)),
-                "avg_launch_ms": round(float(dec_ms.mean()), 4)}
+                "algorithmic_bytes_per_launch": th_per_launch * INT8_BYTES,
+                "median_launch_ms": round(float(np.median(dec_ms)), 4)}
     else:
-        roof = {"kernel": "exact bf16 fallback (split + merge kernels)", "bound": "hbm",
+        roof = {"kernel": "exact bf16 fallback (decode_mfma_kernel + merge_kernel)", "bound": "hbm",
                 "achieved": round(fb_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(fb_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                 "algorithmic_bytes_per_launch": fb_bytes,
-                "avg_launch_ms": round(float(fb_ms.mean()), 4)}
+                "median_launch_ms": round(float(np.median(fb_ms)), 4)}
 
     line = {
         "metric": "metered INT8 decode-attn KV tokens/s & HBM GB/s (% peak); quant+witness GB/s",
@@ -299,11 +320,11 @@ def main():
                    "tau": args.tau, "cache": "int8 dither + fp16 scales + fp16 key witness",
                    "fallback": "bf16 exact cache in HBM"},
         "roofline": roof,
-        "metered_decode": {"avg_launch_ms": round(float(dec_ms.mean()), 4), "GBps": round(dec_gbps, 1),
+        "metered_decode": {"median_launch_ms": round(float(np.median(dec_ms)), 4), "GBps": round(dec_gbps, 1),
                            "frac_hbm": round(dec_gbps / HBM_PEAK_GBPS, 4),
                            "bytes_per_token_head": INT8_BYTES},
-        "exact_fallback": {"avg_launch_ms": round(float(fb_ms.mean()), 4), "GBps": round(fb_gbps, 1),
-                           "frac_hbm": round(fb_gbps / HBM_PEAK_GBPS, 4)},
+        "exact_fallback": {"median_launch_ms": round(float(np.median(fb_ms)), 4), "GBps": round(fb_gbps, 1),
+                           "frac_hbm": round(fb_gbps / HBM_PEAK_GBPS, 4), "routed_kv_fraction": routed},
         "gate": {"tau": args.tau, "fraction_q_heads": round(frac_q, 4),
                  "fraction_kv_heads": round(frac_kv, 4)},
         "quant_witness": {"GBps": round(write_gbps, 1), "frac_hbm": round(write_gbps / HBM_PEAK_GBPS, 4),

@@ -139,6 +139,8 @@ int wc_witness(const void* x, int x_dtype, const void* xhat, int xhat_dtype, int
 /*
  * Workspace bytes needed by wc_metered_decode_attention / wc_exact_decode_attention
  * for these sizes.  split_tokens as passed to the decode call (0 = library choice).
+ * The workspace holds the per-split partial records (no initialization needed);
+ * calls that share a workspace must not run concurrently.
  */
 size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
                                 int64_t max_seq_len, int split_tokens);

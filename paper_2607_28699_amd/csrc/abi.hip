@@ -114,8 +114,7 @@ size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int he
     return 0;
   const int st = wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens);
   const int64_t ns = wc::n_splits_for(max_seq_len, st);
-  size_t bytes = (size_t)batch * n_q_heads * ns * wc::partial_record_floats(head_dim) * sizeof(float);
-  return bytes < 256 ? 256 : bytes;
+  return wc::records_bytes(batch, n_q_heads, ns, head_dim);
 }
 
 static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int batch,

@@ -297,11 +297,19 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   }
 }
 
-// Merge of the split partials of one (sequence, query head) under the LSE
-// weights: out = sum_j e^{m_j - M} acc_j / L, A - 1 = sum_j e^{m_j - M} N_j / L.
+// Merge of the split records of one (sequence, query head) under the LSE
+// weights: out = sum_j e^{m_j - M} acc_j / L, A - 1 = sum_j e^{m_j - M} N_j / L with
+// L = sum_j e^{m_j - M} l_j; raw = (A-1)(A+1)/2 (+inf on overflow), meter = min(1, raw)
+// (Sec. 6.2: A merges exactly like the output).  256 threads: the split maxima and
+// weights are reduced in LDS, then thread (channel, half) sums every other split
+// with all its loads independent.
+constexpr int kMergeThreads = 256;
+
 template <int D, bool METER>
-__global__ __launch_bounds__(64) void merge_kernel(DecodeArgs a) {
-  constexpr int CPT = D / 64;
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
+  __shared__ float red[kMergeThreads];
+  __shared__ float red2[kMergeThreads];
+  __shared__ float acc_s[kMergeThreads / D][D];
   const int bh = blockIdx.x;
   const int b = bh / a.n_q, h = bh % a.n_q;
   if (a.mask_kv != nullptr && a.mask_kv[b * a.n_kv + h / a.group] == 0) return;
@@ -310,27 +318,51 @@ __global__ __launch_bounds__(64) void merge_kernel(DecodeArgs a) {
   const int64_t R = (int64_t)partial_record_floats(D);
   const float* rec0 = a.part + (int64_t)bh * a.n_splits * R;
   const int tid = threadIdx.x;
-  float M = -INFINITY;
-  for (int j = 0; j < ns; ++j) M = fmaxf(M, rec0[j * R + D]);
-  float lsum = 0.0f, nsum = 0.0f, acc[CPT];
-#pragma unroll
-  for (int k = 0; k < CPT; ++k) acc[k] = 0.0f;
-  for (int j = 0; j < ns; ++j) {
-    const float* rec = rec0 + j * R;
-    const float e = expf(rec[D] - M);
-    lsum = fmaf(e, rec[D + 1], lsum);
-    if constexpr (METER) {
-      const float nn = fmaf(e, rec[D + 2], nsum);
-      nsum = isnan(nn) ? INFINITY : nn;
-    }
-#pragma unroll
-    for (int k = 0; k < CPT; ++k) acc[k] = fmaf(e, rec[tid + 64 * k], acc[k]);
+
+  // M = max_j m_j
+  float m = -INFINITY;
+  for (int j = tid; j < ns; j += kMergeThreads) m = fmaxf(m, rec0[j * R + D]);
+  red[tid] = m;
+  __syncthreads();
+  for (int o = kMergeThreads / 2; o > 0; o >>= 1) {
+    if (tid < o) red[tid] = fmaxf(red[tid], red[tid + o]);
+    __syncthreads();
   }
-  const float inv = ns > 0 ? 1.0f / lsum : 0.0f;
+  const float M = red[0];
+  __syncthreads();
+  // L and the meter numerator
+  float ls = 0.0f, nsum = 0.0f;
+  for (int j = tid; j < ns; j += kMergeThreads) {
+    const float e = __expf(rec0[j * R + D] - M);
+    ls = fmaf(e, rec0[j * R + D + 1], ls);
+    if constexpr (METER) nsum = fmaf(e, rec0[j * R + D + 2], nsum);
+  }
+  red[tid] = ls;
+  red2[tid] = nsum;
+  __syncthreads();
+  for (int o = kMergeThreads / 2; o > 0; o >>= 1) {
+    if (tid < o) {
+      red[tid] += red[tid + o];
+      red2[tid] += red2[tid + o];
+    }
+    __syncthreads();
+  }
+  const float lsum = red[0];
+  float nt = red2[0];
+  // output: thread (channel c, part p) sums splits j = p, p + P, ...
+  constexpr int P = kMergeThreads / D;
+  const int c = tid % D, part = tid / D;
+  float acc = 0.0f;
+#pragma unroll 8
+  for (int j = part; j < ns; j += P) acc = fmaf(__expf(rec0[j * R + D] - M), rec0[j * R + c], acc);
+  acc_s[part][c] = acc;
+  __syncthreads();
+  if (tid < D) {
+    float o = 0.0f;
 #pragma unroll
-  for (int k = 0; k < CPT; ++k) {
-    const float o = acc[k] * inv;
-    const int64_t oi = (int64_t)bh * D + tid + 64 * k;
+    for (int p = 0; p < P; ++p) o += acc_s[p][tid];
+    o = ns > 0 ? o / lsum : 0.0f;
+    const int64_t oi = (int64_t)bh * D + tid;
     if (a.out_dtype == WC_F32)
       reinterpret_cast<float*>(a.out)[oi] = o;
     else
@@ -340,7 +372,8 @@ __global__ __launch_bounds__(64) void merge_kernel(DecodeArgs a) {
     if (tid == 0) {
       float raw = 0.0f;
       if (ns > 0) {
-        const float am1 = nsum * inv;
+        if (isnan(nt)) nt = INFINITY;
+        const float am1 = nt / lsum;
         raw = 0.5f * am1 * (2.0f + am1);
         if (!(raw <= FLT_MAX)) raw = INFINITY;
       }
@@ -356,8 +389,7 @@ hipError_t launch_dq(const DecodeArgs& a, hipStream_t st) {
                      dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((merge_kernel<D, METER>), dim3(a.batch * a.n_q), dim3(64), 0, st, a);
-  return hipGetLastError();
+  return launch_merge(a, METER, st);
 }
 
 template <int D, int KIND, bool METER>
@@ -377,8 +409,9 @@ hipError_t launch_d(const DecodeArgs& a, bool metered, hipStream_t st) {
 
 int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested) {
   if (requested > 0) return (requested + 63) / 64 * 64;
+  // about two 256-thread workgroups per compute unit over the longest sequence
   const int64_t units = (int64_t)batch * n_kv;
-  const int64_t target = 1024;   // workgroups: 4 per compute unit
+  const int64_t target = 512;
   int64_t splits = target / (units > 0 ? units : 1);
   if (splits < 1) splits = 1;
   int64_t st = (max_seq_len + splits - 1) / splits;
@@ -389,11 +422,11 @@ int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested)
 
 hipError_t launch_merge(const DecodeArgs& a, bool metered, hipStream_t st) {
   if (a.head_dim == 64) {
-    if (metered) hipLaunchKernelGGL((merge_kernel<64, true>), dim3(a.batch * a.n_q), dim3(64), 0, st, a);
-    else hipLaunchKernelGGL((merge_kernel<64, false>), dim3(a.batch * a.n_q), dim3(64), 0, st, a);
+    if (metered) hipLaunchKernelGGL((merge_kernel<64, true>), dim3(a.batch * a.n_q), dim3(kMergeThreads), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<64, false>), dim3(a.batch * a.n_q), dim3(kMergeThreads), 0, st, a);
   } else {
-    if (metered) hipLaunchKernelGGL((merge_kernel<128, true>), dim3(a.batch * a.n_q), dim3(64), 0, st, a);
-    else hipLaunchKernelGGL((merge_kernel<128, false>), dim3(a.batch * a.n_q), dim3(64), 0, st, a);
+    if (metered) hipLaunchKernelGGL((merge_kernel<128, true>), dim3(a.batch * a.n_q), dim3(kMergeThreads), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<128, false>), dim3(a.batch * a.n_q), dim3(kMergeThreads), 0, st, a);
   }
   return hipGetLastError();
 }

@@ -69,6 +69,11 @@ inline int64_t n_splits_for(int64_t max_seq_len, int split_tokens) {
   return max_seq_len <= 0 ? 1 : (max_seq_len + split_tokens - 1) / split_tokens;
 }
 __host__ __device__ inline size_t partial_record_floats(int head_dim) { return (size_t)head_dim + 4; }
+// Workspace: the partial records, rounded up to 256 bytes.
+inline size_t records_bytes(int batch, int n_q, int64_t n_splits, int head_dim) {
+  const size_t b = (size_t)batch * n_q * n_splits * partial_record_floats(head_dim) * sizeof(float);
+  return (b + 255) / 256 * 256;
+}
 
 hipError_t launch_quantize_write(const WriteArgs& a, hipStream_t st);
 hipError_t launch_witness(const WitnessArgs& a, hipStream_t st);

@@ -52,6 +52,7 @@ def test_cache_byte_account(L):
 def test_workspace_size_and_argument_checks(L):
     n = L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 0)
     assert n > 0 and n % 4 == 0
+    # 64 splits of partial records (132 floats each), rounded up to 256 B
     assert L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 512) == 4 * 28 * 64 * 132 * 4
     assert L.wc_decode_workspace_size(-1, 28, 4, 128, 100, 0) == 0
     # null cache / pointers are rejected before anything is launched
