@@ -81,7 +81,8 @@ extern "C" {
  *   k_scale,
  *   v_scale    [num_blocks][n_kv_heads][16] fp16              INT8_DITHER only, else NULL
  *   k_witness  [num_blocks][n_kv_heads][16][n_bands] fp16     NULL for BF16
- * Element type of k_data/v_data: int8 (INT8_DITHER), E4M3 byte (FP8_RAW), bf16 (BF16).
+ * Element type of k_data/v_data: int8 code stored excess-128, i.e. the byte code + 128
+ * (INT8_DITHER; codes lie in [-127, 127]), E4M3 byte (FP8_RAW), bf16 (BF16).
  * Band b holds the channels of RoPE pairs b*P .. b*P+P-1, P = head_dim/(2*n_bands)
  * (Sec. 4.1; Lemma RoPE band unitarity).  `seed` keys the Philox dither; `layer`
  * enters its counter (Sec. 6.2: counter (layer, kv_head, slot, channel)).

@@ -74,7 +74,8 @@ class PagedCache:
             "v_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
             "k_witness": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.n_bands),
         }
-        el = {"int8_dither": torch.int8, "fp8_raw": torch.uint8, "bf16": torch.bfloat16}[self.kind]
+        # int8 codes are stored excess-128 (byte = code + 128)
+        el = {"int8_dither": torch.uint8, "fp8_raw": torch.uint8, "bf16": torch.bfloat16}[self.kind]
         for n, s in zip(names, sizes):
             if s == 0:
                 self.tensors[n] = None

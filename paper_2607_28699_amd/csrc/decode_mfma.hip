@@ -49,10 +49,10 @@ constexpr int kWaves = 4;
 constexpr int kRow = 272;  // LDS bytes per token row of the dither transpose (256 + pad)
 // The running max is raised only when a page exceeds it by more than kSlack, so
 // softmax weights stay below e^2.  Weights enter the fp16 PV operand multiplied
-// by kWScale = 2^8 (undone at the end), which keeps small weights out of the fp16
-// subnormal range; the product stays below 65504 for value scales up to 34.
+// by 2^8 (cancelled by the same factor in the weight sum), which keeps small
+// weights out of the fp16 subnormal range; the product stays below 65504 for
+// value scales up to 34.
 constexpr float kSlack = 2.0f;
-constexpr float kWScale = 256.0f;
 constexpr float kDOff = 2303.0f;   // 2048 + 255: D = 2u + 2048 = 512 xi + 2303
 
 __device__ __forceinline__ uint32_t as_u32(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
@@ -67,7 +67,7 @@ constexpr uint32_t kSelHi = 0x04030402u;   // bytes 2, 3 of lo
 constexpr uint32_t kSelH0 = 0x05040100u;   // low halves of lo and hi
 constexpr uint32_t kSelH1 = 0x07060302u;   // high halves of lo and hi
 
-// Two int8 codes (already xor 0x80: u = code + 128) -> fp16 (1024 + u) - 1152, exact.
+// Two codes stored excess-128 (byte u = code + 128) -> fp16 (1024 + u) - 1152 = code, exact.
 __device__ __forceinline__ uint32_t codes2(uint32_t xb, uint32_t sel) {
   return as_u32(as_h2(perm(0x64646464u, xb, sel)) - h2_t{(_Float16)1152.0f, (_Float16)1152.0f});
 }
@@ -98,21 +98,6 @@ __device__ __forceinline__ h4_t pack4(uint32_t a, uint32_t b) {
 
 __device__ __forceinline__ float xor_max(float v, int m) { return fmaxf(v, __shfl_xor(v, m, 64)); }
 
-// e^c - 1 for 0 <= c <= 1 by its Taylor series to c^10/10! (relative error < 3e-7).
-__device__ __forceinline__ float expm1_small(float c) {
-  float s = 1.0f / 3628800.0f;
-  s = fmaf(s, c, 1.0f / 362880.0f);
-  s = fmaf(s, c, 1.0f / 40320.0f);
-  s = fmaf(s, c, 1.0f / 5040.0f);
-  s = fmaf(s, c, 1.0f / 720.0f);
-  s = fmaf(s, c, 1.0f / 120.0f);
-  s = fmaf(s, c, 1.0f / 24.0f);
-  s = fmaf(s, c, 1.0f / 6.0f);
-  s = fmaf(s, c, 0.5f);
-  s = fmaf(s, c, 1.0f);
-  return s * c;
-}
-
 // Loaded bytes of one 16-token page for one lane.
 template <int KIND>
 struct PageRegs {
@@ -120,73 +105,105 @@ struct PageRegs {
   uint32_t kw[NW];   // keys of token r, channels 32g..32g+31
   uint32_t vw[NW];   // values of channels 8r..8r+7 for token quad g
   uint2 ks, vs;      // fp16 scales of tokens 4g..4g+3
-  uint4 wit;         // witness bands 8(g%2).. of token r
-  int64_t blk;
+  uint4 wit;         // witness bands 8(g%2).. of token r (garbage where 8(g%2) >= n_bands)
+  int blk;           // cache block of the page (wave-uniform)
 };
 
+// Buffer resource over one page of one tensor.  A page past the end of the
+// wave's range gets an empty resource: its loads return zeros without touching
+// memory, so every load is issued unconditionally and the in-order load counter
+// stays exact (a conditional load makes the compiler wait for all of them).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t page_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ uint2 bload8(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+
 template <int KIND, bool METER>
-__device__ __forceinline__ void load_page(const DecodeArgs& a, const int32_t* trow, int t0, int kv,
-                                          int r, int g, PageRegs<KIND>& p) {
+__device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool valid, int kv, int r,
+                                          int g, int wit_off, PageRegs<KIND>& p) {
   constexpr int KB = KIND == WC_KIND_BF16 ? 64 : 32;   // bytes per lane and tensor
-  p.blk = trow[t0 / kBlockTokens];
-  const int64_t page = p.blk * a.n_kv + kv;
-  const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.k_data) +
-                                                   (page * kBlockTokens + r) * (kD * (KB / 32)) + KB * g);
-  const uint4* vp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.v_data) +
-                                                   page * (kBlockTokens * kD * (KB / 32)) +
-                                                   (g * kD + 8 * r) * 4 * (KB / 32));
+  constexpr int PB = kBlockTokens * kD * (KB / 32);    // bytes per page and tensor
+  p.blk = blk;
+  const int64_t page = (int64_t)blk * a.n_kv + kv;
+  const auto kr = page_rsrc(reinterpret_cast<const uint8_t*>(a.k_data) + page * PB, valid ? PB : 0);
+  const auto vr = page_rsrc(reinterpret_cast<const uint8_t*>(a.v_data) + page * PB, valid ? PB : 0);
+  const int koff = r * (kD * (KB / 32)) + KB * g;
+  const int voff = (g * kD + 8 * r) * 4 * (KB / 32);
 #pragma unroll
   for (int i = 0; i < KB / 16; ++i) {
-    const uint4 k4 = kp[i], v4 = vp[i];
+    const uint4 k4 = bload16(kr, koff + 16 * i), v4 = bload16(vr, voff + 16 * i);
     p.kw[4 * i] = k4.x; p.kw[4 * i + 1] = k4.y; p.kw[4 * i + 2] = k4.z; p.kw[4 * i + 3] = k4.w;
     p.vw[4 * i] = v4.x; p.vw[4 * i + 1] = v4.y; p.vw[4 * i + 2] = v4.z; p.vw[4 * i + 3] = v4.w;
   }
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
-    p.ks = *reinterpret_cast<const uint2*>(a.k_scale + page * kBlockTokens + 4 * g);
-    p.vs = *reinterpret_cast<const uint2*>(a.v_scale + page * kBlockTokens + 4 * g);
+    const int sb = valid ? 2 * kBlockTokens : 0;
+    p.ks = bload8(page_rsrc(a.k_scale + page * kBlockTokens, sb), 8 * g);
+    p.vs = bload8(page_rsrc(a.v_scale + page * kBlockTokens, sb), 8 * g);
   }
   if constexpr (METER) {
-    p.wit = make_uint4(0, 0, 0, 0);
-    if (8 * (g & 1) < a.n_bands)
-      p.wit = *reinterpret_cast<const uint4*>(a.k_witness + (page * kBlockTokens + r) * a.n_bands + 8 * (g & 1));
+    const int wb = valid ? 2 * kBlockTokens * a.n_bands : 0;
+    p.wit = bload16(page_rsrc(a.k_witness + page * kBlockTokens * a.n_bands, wb), wit_off);
   }
 }
 
-// Running state of one wave.
+// Running state of one wave.  Logits are kept in log2 units; every weight carries
+// an extra factor 2^8 (the exponent is raised by 8), which keeps the fp16 PV
+// operand out of the subnormal range and cancels in out / l and n / l.
 struct WaveState {
   f4_t o1[8], o2[8];
-  float m, l, n, wsum;
+  float m, l, n, wsum;   // running max (log2 units), sum of weights, meter numerator, sum of fp16 weights
 };
 
-template <int KIND, bool METER>
-__device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs<KIND>& cur, int t0,
-                                             int t_end, int r, int g, uint32_t layer_head,
-                                             const h8_t (&qop)[4], const s8_t (&qbf)[4],
-                                             const h8_t& qnop, float qsum, uint8_t* my_dsh,
-                                             WaveState& st) {
-  float sk[4], sv[4];
-  if constexpr (KIND == WC_KIND_INT8_DITHER) {
-    sk[0] = f16_to_f32((uint16_t)(cur.ks.x & 0xFFFFu)); sk[1] = f16_to_f32((uint16_t)(cur.ks.x >> 16));
-    sk[2] = f16_to_f32((uint16_t)(cur.ks.y & 0xFFFFu)); sk[3] = f16_to_f32((uint16_t)(cur.ks.y >> 16));
-    sv[0] = f16_to_f32((uint16_t)(cur.vs.x & 0xFFFFu)); sv[1] = f16_to_f32((uint16_t)(cur.vs.x >> 16));
-    sv[2] = f16_to_f32((uint16_t)(cur.vs.y & 0xFFFFu)); sv[3] = f16_to_f32((uint16_t)(cur.vs.y >> 16));
-#pragma unroll
-    for (int e = 0; e < 4; ++e) sv[e] *= kWScale;
-  } else {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      sk[e] = KIND == WC_KIND_FP8_RAW ? 256.0f : 1.0f;
-      sv[e] = kWScale;
-    }
-  }
+// Per-wave constants of the page loop.
+struct WaveConst {
+  h8_t qop[4];     // fp16 queries, B operands of QK (channels 32g + 8kt ..)
+  s8_t qbf[4];     // bf16 queries (bf16 cache)
+  h8_t qnop;       // band norms * sm_scale * log2(e), hi (g < 2) / lo (g >= 2) parts
+  float s1_init;   // 2303 sum(q) / 512: the dither offset, preloaded into the code accumulator
+  float lmul;      // logit multiplier: sm_scale * log2(e) (times 256 for fp8 operands)
+  uint32_t layer_head;
+  bool wit_ok;
+};
 
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kWExp = 8.0f;                 // weights carry 2^kWExp
+constexpr float kSlack2 = kSlack * kLog2e;    // kSlack in log2 units
+constexpr float kTaylorMax = 0.5f * kLog2e;   // c <= 0.5 in log2 units
+
+// 2^x - 1 for 0 <= x <= log2(e)/2 (that is e^c - 1, c = x ln 2 <= 1/2) by the
+// Taylor series of e^c to c^7/7! (relative error below 2e-7).
+__device__ __forceinline__ float exp2m1_small(float x) {
+  float s = 1.5252733804059840e-05f;
+  s = fmaf(s, x, 1.5403530393381609e-04f);
+  s = fmaf(s, x, 1.3333558146428443e-03f);
+  s = fmaf(s, x, 9.6181291076284772e-03f);
+  s = fmaf(s, x, 5.5504108664821580e-02f);
+  s = fmaf(s, x, 2.4022650695910071e-01f);
+  s = fmaf(s, x, 6.9314718055994531e-01f);
+  return s * x;
+}
+
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// One 16-token page.  FULL: every token of the page is below t_end (no masking).
+template <int KIND, bool METER, bool FULL>
+__device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs<KIND>& cur, int t0,
+                                             int t_end, int r, int g, const WaveConst& wc,
+                                             uint8_t* my_dsh, WaveState& st) {
   // ---------------- QK^T and the bound ----------------
   const f4_t z4 = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
   f4_t s1 = z4, s2 = z4;   // code products, dither products
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
-    const int64_t slot = cur.blk * kBlockTokens + r;
-    const U4 r0 = dither_block(2 * g, slot, layer_head, a.key0, a.key1);
-    const U4 r1 = dither_block(2 * g + 1, slot, layer_head, a.key0, a.key1);
+    s1 = f4_t{wc.s1_init, wc.s1_init, wc.s1_init, wc.s1_init};
+    const int64_t slot = (int64_t)cur.blk * kBlockTokens + r;
+    const U4 r0 = dither_block(2 * g, slot, wc.layer_head, a.key0, a.key1);
+    const U4 r1 = dither_block(2 * g + 1, slot, wc.layer_head, a.key0, a.key1);
     const uint32_t u[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
     uint32_t dq[16];   // 2048 + 2u of token r, channels 32g + 2i, 32g + 2i + 1
 #pragma unroll
@@ -196,11 +213,11 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     }
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
-      const uint32_t x0 = cur.kw[2 * kt] ^ 0x80808080u, x1 = cur.kw[2 * kt + 1] ^ 0x80808080u;
+      const uint32_t x0 = cur.kw[2 * kt], x1 = cur.kw[2 * kt + 1];   // excess-128 codes
       const h8_t ka = pack8(codes2(x0, kSelLo), codes2(x0, kSelHi), codes2(x1, kSelLo), codes2(x1, kSelHi));
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qop[kt], s1, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, wc.qop[kt], s1, 0, 0, 0);
       s2 = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-          pack8(dq[4 * kt], dq[4 * kt + 1], dq[4 * kt + 2], dq[4 * kt + 3]), qop[kt], s2, 0, 0, 0);
+          pack8(dq[4 * kt], dq[4 * kt + 1], dq[4 * kt + 2], dq[4 * kt + 3]), wc.qop[kt], s2, 0, 0, 0);
     }
     // dither of this page to LDS (row = token r, channels 32g..32g+31)
     uint4* dst = reinterpret_cast<uint4*>(my_dsh + r * kRow + 64 * g);
@@ -216,36 +233,46 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
         c[2 * j] = e4m3pair(x & 0xFFu, (x >> 8) & 0xFFu);
         c[2 * j + 1] = e4m3pair((x >> 16) & 0xFFu, x >> 24);
       }
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(pack8(c[0], c[1], c[2], c[3]), qop[kt], s1, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(pack8(c[0], c[1], c[2], c[3]), wc.qop[kt], s1, 0, 0, 0);
     }
   } else {
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
       const uint4 v = make_uint4(cur.kw[4 * kt], cur.kw[4 * kt + 1], cur.kw[4 * kt + 2], cur.kw[4 * kt + 3]);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(s8_t, v), qbf[kt], s1, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(s8_t, v), wc.qbf[kt], s1, 0, 0, 0);
     }
   }
   f4_t cb = z4;
   if constexpr (METER) {
-    cb = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, cur.wit), qnop, cb, 0, 0, 0);
+    const uint4 w = wc.wit_ok ? cur.wit : make_uint4(0, 0, 0, 0);
+    cb = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, w), wc.qnop, cb, 0, 0, 0);
   }
 
   // ---------------- online softmax and meter numerator ----------------
-  // this lane: head r, tokens t0 + 4g + e
+  // this lane: head r, tokens t0 + 4g + e; logits in log2 units
+  const h2_t ksh[2] = {as_h2(cur.ks.x), as_h2(cur.ks.y)};
+  const h2_t vsh[2] = {as_h2(cur.vs.x), as_h2(cur.vs.y)};
+  bool valid[4];
   float lg[4];
   float loc = -INFINITY;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const bool valid = t0 + 4 * g + e < t_end;
+    valid[e] = FULL || t0 + 4 * g + e < t_end;
     float sc = s1[e];
-    if constexpr (KIND == WC_KIND_INT8_DITHER) sc = fmaf(s2[e] - kDOff * qsum, -0.001953125f, sc);
-    lg[e] = valid ? sc * (sk[e] * a.sm_scale) : -INFINITY;
+    if constexpr (KIND == WC_KIND_INT8_DITHER) {
+      sc = fmaf(s2[e], -0.001953125f, sc);          // q . (code + xi)
+      // (fma with a +0 addend keeps the fp16 operand inside one mixed-precision fma)
+      sc = fmaf((float)ksh[e >> 1][e & 1], sc, 0.0f) * wc.lmul;
+    } else {
+      sc = sc * wc.lmul;
+    }
+    lg[e] = valid[e] ? sc : -INFINITY;
     loc = fmaxf(loc, lg[e]);
   }
-  if (__ballot(loc > st.m + kSlack) != 0) {
+  if (__ballot(loc > st.m + kSlack2) != 0) {
     const float full = xor_max(xor_max(loc, 16), 32);
     const float m_new = fmaxf(st.m, full);
-    const float alpha = __expf(st.m - m_new);
+    const float alpha = exp2_fast(st.m - m_new);
     st.m = m_new;
     st.l *= alpha;
     st.n *= alpha;
@@ -256,26 +283,32 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       st.o2[j] *= alpha;
     }
   }
-  float wgt[4];
+  const float mo = st.m - kWExp;
+  _Float16 wh[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const bool valid = t0 + 4 * g + e < t_end;
-    const float x = lg[e] - st.m;
-    const float p = valid ? __expf(x) : 0.0f;
+    const float x = lg[e] - mo;
+    const float p = exp2_fast(x);                    // 2^8 softmax weight; 0 for masked tokens
     st.l += p;
     if constexpr (METER) {
-      // p (e^c - 1): Taylor series below 1; above, e^(x + c) - p in the log domain
-      // so that a token whose weight underflows still counts with its bound
+      // p (e^c - 1): Taylor series for c <= 1/2; above, 2^(x + c) - p, which
+      // also counts a token whose weight underflows with its bound
       const float c = cb[e];
-      const float small = p * expm1_small(fminf(c, 1.0f));
-      const float big = __expf(x + c) - p;
-      st.n += valid ? (c > 1.0f ? big : small) : 0.0f;
+      const float small = p * exp2m1_small(__builtin_amdgcn_fmed3f(c, 0.0f, kTaylorMax));
+      const float big = exp2_fast(x + c) - p;
+      const float term = c > kTaylorMax ? big : small;
+      st.n += valid[e] ? term : 0.0f;
     }
-    wgt[e] = valid ? p * sv[e] : 0.0f;
+    float w = p;
+    if constexpr (KIND == WC_KIND_INT8_DITHER) w = fmaf((float)vsh[e >> 1][e & 1], p, 0.0f);
+    wh[e] = valid[e] ? (_Float16)w : (_Float16)0.0f;
   }
-  const h4_t wop = h4_t{(_Float16)wgt[0], (_Float16)wgt[1], (_Float16)wgt[2], (_Float16)wgt[3]};
-  if constexpr (KIND == WC_KIND_INT8_DITHER)
-    st.wsum += ((float)wop[0] + (float)wop[1]) + ((float)wop[2] + (float)wop[3]);
+  const h2_t w01 = h2_t{wh[0], wh[1]}, w23 = h2_t{wh[2], wh[3]};
+  const h4_t wop = h4_t{wh[0], wh[1], wh[2], wh[3]};
+  if constexpr (KIND == WC_KIND_INT8_DITHER) {
+    const h2_t one = h2_t{(_Float16)1.0f, (_Float16)1.0f};
+    st.wsum = __builtin_amdgcn_fdot2(w23, one, __builtin_amdgcn_fdot2(w01, one, st.wsum, false), false);
+  }
 
   // ---------------- P V ----------------
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
@@ -291,7 +324,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     const uint32_t* r3 = reinterpret_cast<const uint32_t*>(&rows[3]);
 #pragma unroll
     for (int jt = 0; jt < 8; ++jt) {
-      const uint32_t x = cur.vw[jt] ^ 0x80808080u;     // codes of channel 8r+jt, tokens 4g..4g+3
+      const uint32_t x = cur.vw[jt];     // codes (excess-128) of channel 8r+jt, tokens 4g..4g+3
       st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(codes2(x, kSelLo), codes2(x, kSelHi)), wop,
                                                         st.o1[jt], 0, 0, 0);
       const uint32_t sel = (jt & 1) ? kSelH1 : kSelH0;
@@ -307,11 +340,13 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       const uint32_t x = cur.vw[jt];
       uint32_t lo = e4m3pair(x & 0xFFu, (x >> 8) & 0xFFu);
       uint32_t hi = e4m3pair((x >> 16) & 0xFFu, x >> 24);
-      // tokens past the end may hold any byte pattern (the 0x7F NaN code): zero them
-      if (t0 + 4 * g + 0 >= t_end) lo &= 0xFFFF0000u;
-      if (t0 + 4 * g + 1 >= t_end) lo &= 0x0000FFFFu;
-      if (t0 + 4 * g + 2 >= t_end) hi &= 0xFFFF0000u;
-      if (t0 + 4 * g + 3 >= t_end) hi &= 0x0000FFFFu;
+      if constexpr (!FULL) {
+        // tokens past the end may hold any byte pattern (the 0x7F NaN code): zero them
+        if (!valid[0]) lo &= 0xFFFF0000u;
+        if (!valid[1]) lo &= 0x0000FFFFu;
+        if (!valid[2]) hi &= 0xFFFF0000u;
+        if (!valid[3]) hi &= 0x0000FFFFu;
+      }
       st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(lo, hi), wop, st.o1[jt], 0, 0, 0);
     }
   } else {
@@ -320,10 +355,12 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       // bf16 values of channel 8r+jt, tokens 4g..4g+3: 8 bytes at offset 8*jt
       uint32_t lo = bf16pair_to_f16(cur.vw[2 * jt]);
       uint32_t hi = bf16pair_to_f16(cur.vw[2 * jt + 1]);
-      if (t0 + 4 * g + 0 >= t_end) lo &= 0xFFFF0000u;
-      if (t0 + 4 * g + 1 >= t_end) lo &= 0x0000FFFFu;
-      if (t0 + 4 * g + 2 >= t_end) hi &= 0xFFFF0000u;
-      if (t0 + 4 * g + 3 >= t_end) hi &= 0x0000FFFFu;
+      if constexpr (!FULL) {
+        if (!valid[0]) lo &= 0xFFFF0000u;
+        if (!valid[1]) lo &= 0x0000FFFFu;
+        if (!valid[2]) hi &= 0xFFFF0000u;
+        if (!valid[3]) hi &= 0x0000FFFFu;
+      }
       st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(lo, hi), wop, st.o1[jt], 0, 0, 0);
     }
   }
@@ -336,7 +373,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) float acc_s[kWaves][16][kD];
   __shared__ float ml_s[kWaves][16][3];
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // the wave index is uniform: page addresses then live in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
   const int unit = blockIdx.y;
   const int b = unit / a.n_kv, kv = unit % a.n_kv;
@@ -366,15 +404,42 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       qraw[4 * i] = v.x; qraw[4 * i + 1] = v.y; qraw[4 * i + 2] = v.z; qraw[4 * i + 3] = v.w;
     }
   }
+
+  // Pages stream through a ring of three register buffers, so two pages are in
+  // flight while one is computed.  Block numbers come 64 pages at a time from one
+  // vector load of the table and are read out with readlane (wave-uniform).  The
+  // first two pages are requested before the queries are prepared.
+  const int32_t* trow = a.table + (int64_t)b * a.max_blocks;
+  // full pages go through the ring; a last page that reaches past t_end is done after it
+  const int np = t_end > t_begin ? (t_end - t_begin) / kBlockTokens : 0;
+  const int pg0 = t_begin / kBlockTokens;
+  const int wit_off = 8 * (g & 1) < B ? 2 * (r * B + 8 * (g & 1)) : 0;
+  PageRegs<KIND> p0, p1, p2;
+  int nc = 0, tv = 0;
+  auto blk_at = [&](int j) { return __builtin_amdgcn_readlane(tv, min(j, nc - 1)); };
+  // (scheduling barriers keep each page's loads together, so that waiting for
+  // one page never waits for a later one)
+  auto start_chunk = [&](int c0) {
+    nc = min(64, np - c0);
+    tv = lane < nc ? trow[pg0 + c0 + lane] : 0;
+    load_page<KIND, METER>(a, blk_at(0), true, kv, r, g, wit_off, p0);
+    __builtin_amdgcn_sched_barrier(0);
+    load_page<KIND, METER>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  if (np > 0) start_chunk(0);
+
+  WaveConst wc;
+  wc.layer_head = ((uint32_t)a.layer << 16) | (uint32_t)kv;
+  wc.wit_ok = 8 * (g & 1) < B;
+  wc.lmul = a.sm_scale * kLog2e * (KIND == WC_KIND_FP8_RAW ? 256.0f : 1.0f);
   // B operands of QK: the kt-th MFMA uses channels 32g + 8kt .. 32g + 8kt + 7.
-  h8_t qop[4];
-  s8_t qbf[4];
   float qsum = 0.0f;   // sum of the fp16 queries of head r over all channels
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) {
     if constexpr (KIND == WC_KIND_BF16) {
-      qbf[kt] = __builtin_bit_cast(s8_t, make_uint4(qraw[4 * kt], qraw[4 * kt + 1], qraw[4 * kt + 2],
-                                                    qraw[4 * kt + 3]));
+      wc.qbf[kt] = __builtin_bit_cast(s8_t, make_uint4(qraw[4 * kt], qraw[4 * kt + 1], qraw[4 * kt + 2],
+                                                       qraw[4 * kt + 3]));
     } else {
       uint32_t w[4];
 #pragma unroll
@@ -383,24 +448,53 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
         const h2_t h = as_h2(w[j]);
         qsum += (float)h[0] + (float)h[1];
       }
-      qop[kt] = pack8(w[0], w[1], w[2], w[3]);
+      wc.qop[kt] = pack8(w[0], w[1], w[2], w[3]);
     }
   }
   qsum += __shfl_xor(qsum, 16, 64);
   qsum += __shfl_xor(qsum, 32, 64);
-  // band norms ||q_b|| * sm_scale -> witness-MFMA B operand (hi parts for g < 2, lo for g >= 2)
-  h8_t qnop = pack8(0, 0, 0, 0);
+  wc.s1_init = kDOff * qsum * 0.001953125f;
+  // band norms ||q_b|| * sm_scale * log2(e) -> witness-MFMA B operand (hi parts
+  // for g < 2, lo for g >= 2); the bound then comes out in log2 units
+  wc.qnop = pack8(0, 0, 0, 0);
   if constexpr (METER) {
-    for (int i = lane; i < 256; i += 64) (&qn_s[wave][0][0])[i] = 0.0f;
-    __builtin_amdgcn_s_waitcnt(0xc07f);
-    __builtin_amdgcn_wave_barrier();
+    // Squares of this lane's 32 channels summed in runs of 4.  The band of
+    // channel 32g + i is base + i / S with S = 64 / B (rotate-half pairs (j, j + 64))
+    // or 128 / B (adjacent pairs), so runs of 4 coarsen exactly into the lane's bands.
+    float p4[8];
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const float x = bf16_to_f32((uint16_t)((qraw[i >> 1] >> (16 * (i & 1))) & 0xFFFFu));
-      atomicAdd(&qn_s[wave][r][band_of(32 * g + i, kD, B, a.interleaved)], x * x);
+    for (int k = 0; k < 8; ++k) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int i = 4 * k; i < 4 * k + 4; ++i) {
+        const float x = bf16_to_f32((uint16_t)((qraw[i >> 1] >> (16 * (i & 1))) & 0xFFFFu));
+        acc = fmaf(x, x, acc);
+      }
+      p4[k] = acc;
+    }
+    const int S = (a.interleaved ? 2 * kD : kD) / (2 * B);   // 4, 8 or 16
+    const int nl = 32 / S;                                     // bands touched by this lane
+    const int base = 32 * (a.interleaved ? g : (g & 1)) / S;
+    float pb[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      if (S == 4) pb[k] = p4[k];
+      else if (S == 8) pb[k] = k < 4 ? p4[2 * k] + p4[2 * k + 1] : 0.0f;
+      else pb[k] = k < 2 ? (p4[4 * k] + p4[4 * k + 1]) + (p4[4 * k + 2] + p4[4 * k + 3]) : 0.0f;
+    }
+    // rotate-half: lanes g and g ^ 2 hold the two halves of the same pairs
+    if (!a.interleaved) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) pb[k] += __shfl_xor(pb[k], 32, 64);
+    }
+    if (a.interleaved || g < 2) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (k < nl) qn_s[wave][r][base + k] = pb[k];
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_wave_barrier();
+    const float nmul = a.sm_scale * kLog2e;
     uint32_t hw[4];
 #pragma unroll
     for (int e2 = 0; e2 < 4; ++e2) {
@@ -408,13 +502,13 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int band = 8 * (g & 1) + 2 * e2 + j;
-        const float x = band < B ? sqrtf(qn_s[wave][r][band]) * a.sm_scale : 0.0f;
+        const float x = band < B ? sqrtf(qn_s[wave][r][band]) * nmul : 0.0f;
         const _Float16 hi = (_Float16)x;
         hv2[j] = (g < 2) ? hi : (_Float16)(x - (float)hi);
       }
       hw[e2] = as_u32(h2_t{hv2[0], hv2[1]});
     }
-    qnop = pack8(hw[0], hw[1], hw[2], hw[3]);
+    wc.qnop = pack8(hw[0], hw[1], hw[2], hw[3]);
   }
 
   WaveState st;
@@ -425,20 +519,45 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   }
   st.m = -INFINITY;
   st.l = st.n = st.wsum = 0.0f;
-  const uint32_t layer_head = ((uint32_t)a.layer << 16) | (uint32_t)kv;
   uint8_t* my_dsh = dsh[KIND == WC_KIND_INT8_DITHER ? wave : 0];
-  const int32_t* trow = a.table + (int64_t)b * a.max_blocks;
 
-  // two page buffers used alternately: loads of one are in flight while the other is computed
-  PageRegs<KIND> pa, pb;
-  if (t_begin < t_end) load_page<KIND, METER>(a, trow, t_begin, kv, r, g, pa);
-  for (int t0 = t_begin; t0 < t_end; t0 += 2 * kBlockTokens) {
-    const int t1 = t0 + kBlockTokens;
-    if (t1 < t_end) load_page<KIND, METER>(a, trow, t1, kv, r, g, pb);
-    process_page<KIND, METER>(a, pa, t0, t_end, r, g, layer_head, qop, qbf, qnop, qsum, my_dsh, st);
-    if (t1 >= t_end) break;
-    if (t1 + kBlockTokens < t_end) load_page<KIND, METER>(a, trow, t1 + kBlockTokens, kv, r, g, pa);
-    process_page<KIND, METER>(a, pb, t1, t_end, r, g, layer_head, qop, qbf, qnop, qsum, my_dsh, st);
+  // Two workgroups share each SIMD, and instruction issue favours the older
+  // wave, so the later workgroup would finish long after the earlier one, alone
+  // on its SIMD.  A wave's issue priority therefore falls with its progress: the
+  // wave that is behind gets the issue slots, and the pair finishes together.
+  auto set_priority = [&](int done) {
+    const int left4 = 4 * (np - done);
+    if (left4 > 3 * np) __builtin_amdgcn_s_setprio(3);
+    else if (left4 > 2 * np) __builtin_amdgcn_s_setprio(2);
+    else if (left4 > np) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(0);
+  };
+  for (int c0 = 0; c0 < np;) {
+    const int tb = t_begin + c0 * kBlockTokens;
+    // No early exit from this loop: a break lets the compiler's load counting
+    // assume the ring order may differ on the back edge and wait for every page.
+    for (int j = 0; j < nc; j += 3) {
+      set_priority(c0 + j);
+      load_page<KIND, METER>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
+      __builtin_amdgcn_sched_barrier(0);
+      process_page<KIND, METER, true>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      load_page<KIND, METER>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (j + 1 < nc)
+        process_page<KIND, METER, true>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      load_page<KIND, METER>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (j + 2 < nc)
+        process_page<KIND, METER, true>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+    }
+    c0 += 64;
+    if (c0 < np) start_chunk(c0);
+  }
+  __builtin_amdgcn_s_setprio(0);
+  const int t_last = t_begin + np * kBlockTokens;
+  if (t_last < t_end) {   // a partial last page: tokens from t_end on are masked
+    load_page<KIND, METER>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
+    process_page<KIND, METER, false>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
   }
 
   // ---- merge the four waves of the workgroup, write one partial record ----
@@ -452,8 +571,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     st.wsum += __shfl_xor(st.wsum, 16, 64);
     st.wsum += __shfl_xor(st.wsum, 32, 64);
   }
-  // fp8 operands hold value/256, so the weight scale already cancels there
-  constexpr float unscale = KIND == WC_KIND_FP8_RAW ? 1.0f : 1.0f / kWScale;
+  // fp8 value operands hold value / 256
+  constexpr float unscale = KIND == WC_KIND_FP8_RAW ? 256.0f : 1.0f;
   // rows 4g+e of tile jt hold channel 8(4g+e)+jt = 32g + 8e + jt
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -463,7 +582,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       v[jt] = st.o1[jt][e];
       if constexpr (KIND == WC_KIND_INT8_DITHER)
         v[jt] = fmaf(st.o2[jt][e] - kDOff * st.wsum, -0.001953125f, v[jt]);
-      v[jt] *= unscale;
+      if constexpr (unscale != 1.0f) v[jt] *= unscale;
     }
     float4* dst = reinterpret_cast<float4*>(&acc_s[wave][r][32 * g + 8 * e]);
     dst[0] = make_float4(v[0], v[1], v[2], v[3]);
@@ -484,7 +603,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
       const float mw = ml_s[w][r][0];
-      f[w] = mw == -INFINITY ? 0.0f : __expf(mw - M);
+      f[w] = mw == -INFINITY ? 0.0f : exp2_fast(mw - M);
       lsum = fmaf(f[w], ml_s[w][r][1], lsum);
       if constexpr (METER) nsum = fmaf(f[w], ml_s[w][r][2], nsum);
     }
@@ -504,7 +623,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       *reinterpret_cast<float4*>(rec + 32 * g + i) = sum;
     }
     if (g == 0) {
-      rec[kD] = M;
+      rec[kD] = M * kLn2;   // records hold the max in natural-log units
       rec[kD + 1] = lsum;
       rec[kD + 2] = nsum;
     }

@@ -112,7 +112,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
       for (int c = 0; c < CH; ++c) kval[c] = 0.0f;
       if (valid) {
         if constexpr (KIND == WC_KIND_INT8_DITHER) {
-          const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const int8_t*>(a.k_data) +
+          const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.k_data) +
                                                            (page * kBlockTokens + off) * D + c0);
           const float s = f16_to_f32(a.k_scale[page * kBlockTokens + off]);
 #pragma unroll
@@ -126,7 +126,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
               xi_s[i][(c0 + 16 * gi) / 4 + w4] = rw[w4];
 #pragma unroll
               for (int j = 0; j < 4; ++j) {
-                const float code = (float)(int8_t)((codes[w4] >> (8 * j)) & 0xFFu);
+                const float code = (float)((int32_t)((codes[w4] >> (8 * j)) & 0xFFu) - 128);   // excess-128
                 const float xi = dither_value((rw[w4] >> (8 * j)) & 0xFFu);
                 kval[16 * gi + 4 * w4 + j] = s * (code - xi);
               }
@@ -255,7 +255,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
             const uint32_t byte = (w >> (8 * j)) & 0xFFu;
             if constexpr (KIND == WC_KIND_INT8_DITHER) {
               const uint32_t u = (xi_s[i0 + j][c3 >> 2] >> (8 * (c3 & 3))) & 0xFFu;
-              vv[j] = (float)(int8_t)byte - dither_value(u);
+              vv[j] = (float)((int32_t)byte - 128) - dither_value(u);   // excess-128 code
             } else {
               vv[j] = e4m3_to_f32(byte);
             }

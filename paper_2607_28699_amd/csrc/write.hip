@@ -106,15 +106,16 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
       const float cv = rintf(__fadd_rn(__fmul_rn(v[i], ivv), xi));
       const float rk = fmaf(sk, ck - xi, -k[i]);   // khat - k, one rounding
       r2[lth][16 * g + i] = rk * rk;
-      kc[i >> 2] |= ((uint32_t)(int32_t)ck & 0xFFu) << (8 * (i & 3));
+      // codes are stored excess-128: byte = code + 128
+      kc[i >> 2] |= ((uint32_t)((int32_t)ck + 128) & 0xFFu) << (8 * (i & 3));
       if (active) {
-        int8_t* vd = reinterpret_cast<int8_t*>(a.v_data) + bh * (kBlockTokens * D) +
-                     ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
-        *vd = (int8_t)(int32_t)cv;
+        uint8_t* vd = reinterpret_cast<uint8_t*>(a.v_data) + bh * (kBlockTokens * D) +
+                      ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
+        *vd = (uint8_t)((int32_t)cv + 128);
       }
     }
     if (active) {
-      uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<int8_t*>(a.k_data) +
+      uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(a.k_data) +
                                            (bh * kBlockTokens + off) * D + 16 * g);
       *kd = make_uint4(kc[0], kc[1], kc[2], kc[3]);
       if (g == 0) {

@@ -105,6 +105,9 @@ def read_cache(cache, slots):
     vd = t["v_data"].numpy() if cache.kind != "bf16" else t["v_data"].view(__import__("torch").int16).numpy()
     out["k"] = kd[blk, :, off, :]
     out["v"] = vd[blk, :, off // 4, :, off % 4]
+    if cache.kind == "int8_dither":   # stored excess-128
+        out["k"] = out["k"].astype(np.int16) - 128
+        out["v"] = out["v"].astype(np.int16) - 128
     if t["k_scale"] is not None:
         out["ks"] = ofp_f16(t["k_scale"].numpy()[blk, :, off])
         out["vs"] = ofp_f16(t["v_scale"].numpy()[blk, :, off])
