@@ -303,77 +303,124 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
 // (Sec. 6.2: A merges exactly like the output).  256 threads: the split maxima and
 // weights are reduced in LDS, then thread (channel, half) sums every other split
 // with all its loads independent.
-constexpr int kMergeThreads = 256;
+constexpr int kMergeWaves = 4;
+constexpr int kMergeThreads = 64 * kMergeWaves;
 
+// Split-KV merge (Sec. 6.2): one workgroup per (sequence, query head).  Splits
+// go 32 at a time to the four waves in turn.  In a chunk, lane j % 32 holds the
+// (max, weight sum, meter numerator) of split j and every lane holds its channels
+// of all 32 partial outputs; all of a chunk's loads are issued together, and the
+// split weights reach the channel lanes through readlane.  The waves' running
+// states are combined in LDS at the end.
 template <int D, bool METER>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
-  __shared__ float red[kMergeThreads];
-  __shared__ float red2[kMergeThreads];
-  __shared__ float acc_s[kMergeThreads / D][D];
+  constexpr int C = D / 64;   // channels per lane
+  __shared__ float st_s[kMergeWaves][3];
+  __shared__ float acc_s[kMergeWaves][D];
   const int bh = blockIdx.x;
   const int b = bh / a.n_q, h = bh % a.n_q;
   if (a.mask_kv != nullptr && a.mask_kv[b * a.n_kv + h / a.group] == 0) return;
-  const int L = a.seq_lens[b];
-  const int ns = min((L + a.split_tokens - 1) / a.split_tokens, a.n_splits);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t R = (int64_t)partial_record_floats(D);
   const float* rec0 = a.part + (int64_t)bh * a.n_splits * R;
-  const int tid = threadIdx.x;
+  const int jl = lane & 31;
 
-  // M = max_j m_j
-  float m = -INFINITY;
-  for (int j = tid; j < ns; j += kMergeThreads) m = fmaxf(m, rec0[j * R + D]);
-  red[tid] = m;
-  __syncthreads();
-  for (int o = kMergeThreads / 2; o > 0; o >>= 1) {
-    if (tid < o) red[tid] = fmaxf(red[tid], red[tid + o]);
-    __syncthreads();
-  }
-  const float M = red[0];
-  __syncthreads();
-  // L and the meter numerator
-  float ls = 0.0f, nsum = 0.0f;
-  for (int j = tid; j < ns; j += kMergeThreads) {
-    const float e = __expf(rec0[j * R + D] - M);
-    ls = fmaf(e, rec0[j * R + D + 1], ls);
-    if constexpr (METER) nsum = fmaf(e, rec0[j * R + D + 2], nsum);
-  }
-  red[tid] = ls;
-  red2[tid] = nsum;
-  __syncthreads();
-  for (int o = kMergeThreads / 2; o > 0; o >>= 1) {
-    if (tid < o) {
-      red[tid] += red[tid + o];
-      red2[tid] += red2[tid + o];
+  float M = -INFINITY, lsum = 0.0f, nsum = 0.0f, acc[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) acc[c] = 0.0f;
+  // The records of a chunk are requested before the sequence length is known;
+  // records past the last active split are read but not used.
+  int ns = -1;
+  for (int j0 = 32 * wave; j0 < a.n_splits; j0 += 32 * kMergeWaves) {
+    const int nr = min(32, a.n_splits - j0);    // records that exist in the workspace
+    const float4 t = *reinterpret_cast<const float4*>(rec0 + (int64_t)(j0 + min(jl, nr - 1)) * R + D);
+    float ov[32][C];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      const float* src = rec0 + (int64_t)(j0 + min(j, nr - 1)) * R + C * lane;
+      if constexpr (C == 2) {
+        const float2 v = *reinterpret_cast<const float2*>(src);
+        ov[j][0] = v.x;
+        ov[j][1] = v.y;
+      } else {
+        ov[j][0] = src[0];
+      }
     }
-    __syncthreads();
+    if (ns < 0) {
+      const int L = a.seq_lens[b];
+      ns = min((L + a.split_tokens - 1) / a.split_tokens, a.n_splits);
+    }
+    if (j0 >= ns) break;
+    const int nj = min(32, ns - j0);
+    const float mj = jl < nj ? t.x : -INFINITY;
+    float mc = mj;
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) mc = fmaxf(mc, __shfl_xor(mc, o, 64));
+    const float Mn = fmaxf(M, mc);
+    const float alpha = M == -INFINITY ? 0.0f : __expf(M - Mn);
+    const float ej = mj == -INFINITY ? 0.0f : __expf(mj - Mn);
+    float dl = jl < nj ? ej * t.y : 0.0f, dn = METER && jl < nj ? ej * t.z : 0.0f;
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) {
+      dl += __shfl_xor(dl, o, 64);
+      if constexpr (METER) dn += __shfl_xor(dn, o, 64);
+    }
+    M = Mn;
+    lsum = fmaf(lsum, alpha, dl);
+    if constexpr (METER) nsum = fmaf(nsum, alpha, dn);
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[c] *= alpha;
+    // (records past the last active split may hold anything, NaN included: skip them)
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      if (j < nj) {
+        const float e = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ej), j));
+#pragma unroll
+        for (int c = 0; c < C; ++c) acc[c] = fmaf(e, ov[j][c], acc[c]);
+      }
+    }
   }
-  const float lsum = red[0];
-  float nt = red2[0];
-  // output: thread (channel c, part p) sums splits j = p, p + P, ...
-  constexpr int P = kMergeThreads / D;
-  const int c = tid % D, part = tid / D;
-  float acc = 0.0f;
-#pragma unroll 8
-  for (int j = part; j < ns; j += P) acc = fmaf(__expf(rec0[j * R + D] - M), rec0[j * R + c], acc);
-  acc_s[part][c] = acc;
+  if (ns < 0) {
+    const int L = a.seq_lens[b];
+    ns = min((L + a.split_tokens - 1) / a.split_tokens, a.n_splits);
+  }
+  if (lane == 0) {
+    st_s[wave][0] = M;
+    st_s[wave][1] = lsum;
+    st_s[wave][2] = nsum;
+  }
+#pragma unroll
+  for (int c = 0; c < C; ++c) acc_s[wave][C * lane + c] = acc[c];
   __syncthreads();
-  if (tid < D) {
+  if (wave != 0) return;
+  float Mt = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < kMergeWaves; ++w) Mt = fmaxf(Mt, st_s[w][0]);
+  float f[kMergeWaves], lt = 0.0f, nt = 0.0f;
+#pragma unroll
+  for (int w = 0; w < kMergeWaves; ++w) {
+    f[w] = st_s[w][0] == -INFINITY ? 0.0f : __expf(st_s[w][0] - Mt);
+    lt = fmaf(f[w], st_s[w][1], lt);
+    if constexpr (METER) nt = fmaf(f[w], st_s[w][2], nt);
+  }
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
     float o = 0.0f;
 #pragma unroll
-    for (int p = 0; p < P; ++p) o += acc_s[p][tid];
-    o = ns > 0 ? o / lsum : 0.0f;
-    const int64_t oi = (int64_t)bh * D + tid;
+    for (int w = 0; w < kMergeWaves; ++w) o = fmaf(f[w], acc_s[w][C * lane + c], o);
+    o = ns > 0 ? o / lt : 0.0f;
+    const int64_t oi = (int64_t)bh * D + C * lane + c;
     if (a.out_dtype == WC_F32)
       reinterpret_cast<float*>(a.out)[oi] = o;
     else
       reinterpret_cast<uint16_t*>(a.out)[oi] = f32_to_bf16_rne(o);
   }
   if constexpr (METER) {
-    if (tid == 0) {
+    if (lane == 0) {
       float raw = 0.0f;
       if (ns > 0) {
         if (isnan(nt)) nt = INFINITY;
-        const float am1 = nt / lsum;
+        const float am1 = nt / lt;
         raw = 0.5f * am1 * (2.0f + am1);
         if (!(raw <= FLT_MAX)) raw = INFINITY;
       }
