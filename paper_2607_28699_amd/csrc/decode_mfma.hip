@@ -191,8 +191,19 @@ __device__ __forceinline__ float exp2m1_small(float x) {
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// DPP row shifts within each 16-lane row: lanes 8..15 take `from` of lane - 8
+// (lanes 0..7 keep `keep`); lanes 0..7 take `v` of lane + 8 (lanes 8..15 get 0).
+__device__ __forceinline__ float dpp_from_lower8(float keep, float from) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, keep),
+                                                               __builtin_bit_cast(int, from),
+                                                               0x118 /* row_shr:8 */, 0xF, 0xC, false));
+}
+__device__ __forceinline__ uint32_t dpp_from_upper8(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x108 /* row_shl:8 */, 0xF, 0x3, false);
+}
+
 // One 16-token page.  FULL: every token of the page is below t_end (no masking).
-template <int KIND, bool METER, bool FULL>
+template <int KIND, bool METER, bool FULL, bool HALF>
 __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs<KIND>& cur, int t0,
                                              int t_end, int r, int g, const WaveConst& wc,
                                              uint8_t* my_dsh, WaveState& st) {
@@ -249,18 +260,43 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   }
 
   // ---------------- online softmax and meter numerator ----------------
-  // this lane: head r, tokens t0 + 4g + e; logits in log2 units
-  const h2_t ksh[2] = {as_h2(cur.ks.x), as_h2(cur.ks.y)};
-  const h2_t vsh[2] = {as_h2(cur.vs.x), as_h2(cur.vs.y)};
-  bool valid[4];
-  float lg[4];
-  float loc = -INFINITY;
+  // Lane (r, g) holds head r, tokens t0 + 4g + e.  HALF (at most 8 heads per KV
+  // head): the lanes of heads 8..15 are padding, so tokens 4g+2, 4g+3 of head r
+  // move to lane r + 8 (one DPP row shift per value) and every lane does the
+  // softmax and meter work of two tokens.  Logits are in log2 units.
+  constexpr int NT = HALF ? 2 : 4;
+  const bool upper = HALF && r >= 8;
+  const int tok0 = 4 * g + (upper ? 2 : 0);            // first token of this lane
+  float scv[4], cbv[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    valid[e] = FULL || t0 + 4 * g + e < t_end;
-    float sc = s1[e];
+    scv[e] = s1[e];
+    if constexpr (KIND == WC_KIND_INT8_DITHER) scv[e] = fmaf(s2[e], -0.001953125f, scv[e]);   // q . (code + xi)
+    cbv[e] = cb[e];
+  }
+  uint32_t ksw0 = cur.ks.x, ksw1 = cur.ks.y, vsw0 = cur.vs.x, vsw1 = cur.vs.y;
+  if constexpr (HALF) {
+    scv[0] = dpp_from_lower8(scv[0], scv[2]);
+    scv[1] = dpp_from_lower8(scv[1], scv[3]);
+    if constexpr (METER) {
+      cbv[0] = dpp_from_lower8(cbv[0], cbv[2]);
+      cbv[1] = dpp_from_lower8(cbv[1], cbv[3]);
+    }
     if constexpr (KIND == WC_KIND_INT8_DITHER) {
-      sc = fmaf(s2[e], -0.001953125f, sc);          // q . (code + xi)
+      ksw0 = upper ? cur.ks.y : cur.ks.x;
+      vsw0 = upper ? cur.vs.y : cur.vs.x;
+    }
+  }
+  const h2_t ksh[2] = {as_h2(ksw0), as_h2(ksw1)};
+  const h2_t vsh[2] = {as_h2(vsw0), as_h2(vsw1)};
+  bool valid[NT];
+  float lg[NT];
+  float loc = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < NT; ++e) {
+    valid[e] = FULL || t0 + tok0 + e < t_end;
+    float sc = scv[e];
+    if constexpr (KIND == WC_KIND_INT8_DITHER) {
       // (fma with a +0 addend keeps the fp16 operand inside one mixed-precision fma)
       sc = fmaf((float)ksh[e >> 1][e & 1], sc, 0.0f) * wc.lmul;
     } else {
@@ -270,7 +306,8 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     loc = fmaxf(loc, lg[e]);
   }
   if (__ballot(loc > st.m + kSlack2) != 0) {
-    const float full = xor_max(xor_max(loc, 16), 32);
+    float full = HALF ? xor_max(loc, 8) : loc;     // lanes r and r + 8 share head r's max
+    full = xor_max(xor_max(full, 16), 32);
     const float m_new = fmaxf(st.m, full);
     const float alpha = exp2_fast(st.m - m_new);
     st.m = m_new;
@@ -284,16 +321,16 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     }
   }
   const float mo = st.m - kWExp;
-  _Float16 wh[4];
+  _Float16 wh[NT];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
+  for (int e = 0; e < NT; ++e) {
     const float x = lg[e] - mo;
     const float p = exp2_fast(x);                    // 2^8 softmax weight; 0 for masked tokens
     st.l += p;
     if constexpr (METER) {
       // p (e^c - 1): Taylor series for c <= 1/2; above, 2^(x + c) - p, which
       // also counts a token whose weight underflows with its bound
-      const float c = cb[e];
+      const float c = cbv[e];
       const float small = p * exp2m1_small(__builtin_amdgcn_fmed3f(c, 0.0f, kTaylorMax));
       const float big = exp2_fast(x + c) - p;
       const float term = c > kTaylorMax ? big : small;
@@ -303,12 +340,24 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     if constexpr (KIND == WC_KIND_INT8_DITHER) w = fmaf((float)vsh[e >> 1][e & 1], p, 0.0f);
     wh[e] = valid[e] ? (_Float16)w : (_Float16)0.0f;
   }
-  const h2_t w01 = h2_t{wh[0], wh[1]}, w23 = h2_t{wh[2], wh[3]};
-  const h4_t wop = h4_t{wh[0], wh[1], wh[2], wh[3]};
-  if constexpr (KIND == WC_KIND_INT8_DITHER) {
-    const h2_t one = h2_t{(_Float16)1.0f, (_Float16)1.0f};
-    st.wsum = __builtin_amdgcn_fdot2(w23, one, __builtin_amdgcn_fdot2(w01, one, st.wsum, false), false);
+  const h2_t one = h2_t{(_Float16)1.0f, (_Float16)1.0f};
+  h4_t wop;
+  if constexpr (HALF) {
+    // the PV operand of head r takes tokens 4g+2, 4g+3 back from lane r + 8
+    const uint32_t w01 = as_u32(h2_t{wh[0], wh[1]});
+    wop = pack4(w01, dpp_from_upper8(w01));
+    if constexpr (KIND == WC_KIND_INT8_DITHER)
+      st.wsum = __builtin_amdgcn_fdot2(as_h2(w01), one, st.wsum, false);
+  } else {
+    const h2_t w01 = h2_t{wh[0], wh[1]}, w23 = h2_t{wh[NT - 2], wh[NT - 1]};
+    wop = h4_t{wh[0], wh[1], wh[NT - 2], wh[NT - 1]};
+    if constexpr (KIND == WC_KIND_INT8_DITHER)
+      st.wsum = __builtin_amdgcn_fdot2(w23, one, __builtin_amdgcn_fdot2(w01, one, st.wsum, false), false);
   }
+  // validity of tokens 4g .. 4g+3 (the k index of the PV operands)
+  bool vtok[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) vtok[e] = FULL || t0 + 4 * g + e < t_end;
 
   // ---------------- P V ----------------
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
@@ -342,10 +391,10 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       uint32_t hi = e4m3pair((x >> 16) & 0xFFu, x >> 24);
       if constexpr (!FULL) {
         // tokens past the end may hold any byte pattern (the 0x7F NaN code): zero them
-        if (!valid[0]) lo &= 0xFFFF0000u;
-        if (!valid[1]) lo &= 0x0000FFFFu;
-        if (!valid[2]) hi &= 0xFFFF0000u;
-        if (!valid[3]) hi &= 0x0000FFFFu;
+        if (!vtok[0]) lo &= 0xFFFF0000u;
+        if (!vtok[1]) lo &= 0x0000FFFFu;
+        if (!vtok[2]) hi &= 0xFFFF0000u;
+        if (!vtok[3]) hi &= 0x0000FFFFu;
       }
       st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(lo, hi), wop, st.o1[jt], 0, 0, 0);
     }
@@ -356,17 +405,17 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       uint32_t lo = bf16pair_to_f16(cur.vw[2 * jt]);
       uint32_t hi = bf16pair_to_f16(cur.vw[2 * jt + 1]);
       if constexpr (!FULL) {
-        if (!valid[0]) lo &= 0xFFFF0000u;
-        if (!valid[1]) lo &= 0x0000FFFFu;
-        if (!valid[2]) hi &= 0xFFFF0000u;
-        if (!valid[3]) hi &= 0x0000FFFFu;
+        if (!vtok[0]) lo &= 0xFFFF0000u;
+        if (!vtok[1]) lo &= 0x0000FFFFu;
+        if (!vtok[2]) hi &= 0xFFFF0000u;
+        if (!vtok[3]) hi &= 0x0000FFFFu;
       }
       st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(lo, hi), wop, st.o1[jt], 0, 0, 0);
     }
   }
 }
 
-template <int KIND, bool METER>
+template <int KIND, bool METER, bool HALF>
 __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
   __shared__ float qn_s[kWaves][16][16];
@@ -540,15 +589,15 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       set_priority(c0 + j);
       load_page<KIND, METER>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
       __builtin_amdgcn_sched_barrier(0);
-      process_page<KIND, METER, true>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      process_page<KIND, METER, true, HALF>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
       load_page<KIND, METER>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 1 < nc)
-        process_page<KIND, METER, true>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+        process_page<KIND, METER, true, HALF>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
       load_page<KIND, METER>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 2 < nc)
-        process_page<KIND, METER, true>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+        process_page<KIND, METER, true, HALF>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
     }
     c0 += 64;
     if (c0 < np) start_chunk(c0);
@@ -557,10 +606,15 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   const int t_last = t_begin + np * kBlockTokens;
   if (t_last < t_end) {   // a partial last page: tokens from t_end on are masked
     load_page<KIND, METER>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
-    process_page<KIND, METER, false>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
+    process_page<KIND, METER, false, HALF>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
   }
 
   // ---- merge the four waves of the workgroup, write one partial record ----
+  if constexpr (HALF) {   // lanes r and r + 8 hold different tokens of head r
+    st.l += __shfl_xor(st.l, 8, 64);
+    if constexpr (METER) st.n += __shfl_xor(st.n, 8, 64);
+    if constexpr (KIND == WC_KIND_INT8_DITHER) st.wsum += __shfl_xor(st.wsum, 8, 64);
+  }
   st.l += __shfl_xor(st.l, 16, 64);
   st.l += __shfl_xor(st.l, 32, 64);
   if constexpr (METER) {
@@ -640,12 +694,21 @@ bool mfma_decode_supported(const DecodeArgs& a) {
 
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st) {
   const dim3 grid(a.n_splits, a.batch * a.n_kv);
-  if (!metered)
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false>), grid, dim3(64 * kWaves), 0, st, a);
-  else if (a.kind == WC_KIND_INT8_DITHER)
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true>), grid, dim3(64 * kWaves), 0, st, a);
-  else
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true>), grid, dim3(64 * kWaves), 0, st, a);
+  if (a.group <= 8) {
+    if (!metered)
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, true>), grid, dim3(64 * kWaves), 0, st, a);
+    else if (a.kind == WC_KIND_INT8_DITHER)
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, true>), grid, dim3(64 * kWaves), 0, st, a);
+    else
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, true>), grid, dim3(64 * kWaves), 0, st, a);
+  } else {
+    if (!metered)
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, false>), grid, dim3(64 * kWaves), 0, st, a);
+    else if (a.kind == WC_KIND_INT8_DITHER)
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, false>), grid, dim3(64 * kWaves), 0, st, a);
+    else
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, false>), grid, dim3(64 * kWaves), 0, st, a);
+  }
   return hipGetLastError();
 }
 

@@ -5,7 +5,10 @@
 // One token-head (one token of one KV head, K and V together) is handled by
 // D/16 lanes, lane g owning channels 16g .. 16g+15 -- exactly one Philox call
 // of dither, shared by K and V.  Key residuals go through LDS so that any band
-// map can be summed; each band norm is then rounded up to fp16.
+// map can be summed; each band norm is then rounded up to fp16.  The residuals
+// are exact in float64 (a dequantized value needs 28 bits), and squares, sums and
+// square roots are taken in float64 too, so the stored witness is the fp16
+// round-up of the float64 band norm.
 #include "wc_device.h"
 #include "wc_launch.h"
 
@@ -50,7 +53,7 @@ template <int D, int KIND, typename TIn>
 __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs a) {
   constexpr int LPT = D / 16;                 // lanes per token-head
   constexpr int TH = kWriteThreads / LPT;     // token-heads per block
-  __shared__ float r2[TH][D];                 // squared key residuals
+  __shared__ double r2[TH][D];                // squared key residuals
   __shared__ int64_t slot_s[TH];
 
   const int tid = threadIdx.x;
@@ -104,7 +107,7 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
       const float xi = dither_value((words[i >> 2] >> (8 * (i & 3))) & 0xFFu);
       const float ck = rintf(__fadd_rn(__fmul_rn(k[i], ikk), xi));
       const float cv = rintf(__fadd_rn(__fmul_rn(v[i], ivv), xi));
-      const float rk = fmaf(sk, ck - xi, -k[i]);   // khat - k, one rounding
+      const double rk = (double)sk * (double)(ck - xi) - (double)k[i];   // khat - k
       r2[lth][16 * g + i] = rk * rk;
       // codes are stored excess-128: byte = code + 128
       kc[i >> 2] |= ((uint32_t)((int32_t)ck + 128) & 0xFFu) << (8 * (i & 3));
@@ -129,7 +132,7 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
     for (int i = 0; i < 16; ++i) {
       const uint32_t bk = f32_to_e4m3_sat(k[i]);
       const uint32_t bv = f32_to_e4m3_sat(v[i]);
-      const float rk = e4m3_to_f32(bk) - k[i];    // exact (operands within a factor 2)
+      const double rk = (double)e4m3_to_f32(bk) - (double)k[i];
       r2[lth][16 * g + i] = rk * rk;
       kc[i >> 2] |= bk << (8 * (i & 3));
       if (active) {
@@ -173,11 +176,10 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
     const int64_t s2 = slot_s[t];
     if (th2 >= total || s2 < 0) continue;
     const int h2 = (int)(th2 % a.n_kv);
-    float acc = 0.0f;
+    double acc = 0.0;
     for (int kk = 0; kk < per_band; ++kk) acc += r2[t][band_channel(b, kk, D, B, a.interleaved)];
-    const float w = sqrtf(acc) * (1.0f + 0x1p-18f);   // never below the exact norm
     const int64_t bh2 = (s2 / kBlockTokens) * a.n_kv + h2;
-    a.k_witness[(bh2 * kBlockTokens + s2 % kBlockTokens) * B + b] = f16_round_up(w);
+    a.k_witness[(bh2 * kBlockTokens + s2 % kBlockTokens) * B + b] = f16_round_up_f64(sqrt(acc));
   }
 }
 
@@ -194,14 +196,14 @@ __global__ __launch_bounds__(256) void witness_kernel(WitnessArgs a) {
   const int64_t vec = item / a.n_bands;
   const int b = (int)(item % a.n_bands);
   const int per_band = a.head_dim / a.n_bands;
-  float acc = 0.0f;
+  double acc = 0.0;   // float64: the inputs' difference is exact, the round-up is taken once
   for (int kk = 0; kk < per_band; ++kk) {
     const int c = band_channel(b, kk, a.head_dim, a.n_bands, a.interleaved);
-    const float r = load_any<float>(a.xhat, vec * a.head_dim + c, a.xhat_dtype) -
-                    load_any<float>(a.x, vec * a.head_dim + c, a.x_dtype);
-    acc = fmaf(r, r, acc);
+    const double r = (double)load_any<float>(a.xhat, vec * a.head_dim + c, a.xhat_dtype) -
+                     (double)load_any<float>(a.x, vec * a.head_dim + c, a.x_dtype);
+    acc += r * r;
   }
-  a.w_out[item] = f16_round_up(sqrtf(acc) * (1.0f + 0x1p-18f));
+  a.w_out[item] = f16_round_up_f64(sqrt(acc));
 }
 
 template <int D, int KIND>

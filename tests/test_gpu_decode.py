@@ -27,6 +27,10 @@ DECODE_CASES = [
     ("gqa-split64", W_GQA, [300, 1000 + 13, 64], 64),
     ("gqa-informative", INFORMATIVE, [777, 129], 128),
     ("gqa-interleaved", W_GQA.replace(rope_layout="interleaved"), [513], 0),
+    # 16 query heads per KV head (every head lane real), exactly 8, and 16 bands
+    ("gqa-group16", W_GQA.replace(n_q=32, n_kv=2), [700, 129], 0),
+    ("gqa-group8", W_GQA.replace(n_q=32, n_kv=4), [333, 18], 64),
+    ("gqa-bands16", W_GQA.replace(bands=16), [450], 0),
 ]
 
 
