@@ -157,7 +157,7 @@ def main():
 
     # ---- caches and prefill write (timed separately: quant+witness throughput) ----
     caches, exact = [], []
-    write_ms, write_tokens = 0.0, 0
+    gen0 = None
     for layer in range(wl.n_layers):
         c = wc.PagedCache("int8_dither", lay.nblocks, wl.n_kv, wl.d, wl.bands, layer=layer, seed=seed,
                           rope_layout=wl.rope_layout)
@@ -167,20 +167,14 @@ def main():
             L = int(lens0[b])
             k, v = torch_gen.gen_kv_layer(wl, layer, b, torch.arange(L, device=dev))
             gen.append((k, v, torch.from_numpy(lay.slots(b, np.arange(L), np)).to(dev)))
-        evs = []
-        for k, v, sl in gen:       # back to back, so the GPU never waits between the events
-            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            ev0.record()
-            wc.quantize_write(c, k, v, sl)
-            ev1.record()
-            evs.append((ev0, ev1))
-            write_tokens += k.shape[0] * wl.n_kv
         for k, v, sl in gen:
+            wc.quantize_write(c, k, v, sl)
             wc.quantize_write(e, k, v, sl)
         torch.cuda.synchronize()
-        write_ms += sum(a.elapsed_time(b) for a, b in evs)
         caches.append(c)
         exact.append(e)
+        if layer == 0:
+            gen0 = gen            # kept for timing the quantizing write below
         del gen
     torch.cuda.synchronize()
 
@@ -260,17 +254,34 @@ def main():
     frac_kv = gkv / (K * wl.n_layers * lay.batch * wl.n_kv)
     frac_q = gq / (K * wl.n_layers * lay.batch * wl.n_q)
 
-    # ---- per-kernel timing (eager, launches back to back, events on the launch stream) ----
-    def timed(fn, reps):
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(reps)]
+    # ---- per-call timing: reps calls captured back to back in one HIP graph, the
+    # replays timed with events on the launch stream (no host gaps between calls) ----
+    def timed(fn, reps, replays=5):
+        fn(0)
         torch.cuda.synchronize()
-        for i in range(reps):
-            evs[i][0].record()
-            fn(i)
-            evs[i][1].record()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(reps):
+                fn(i)
+        g.replay()
         torch.cuda.synchronize()
-        return np.array([a.elapsed_time(b) for a, b in evs])
+        per_call = []
+        for _ in range(replays):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            per_call.append(e0.elapsed_time(e1) / reps)
+        del g
+        return np.array(per_call)
+
+    # quantize+witness write of the prefill: layer 0's sequences, each call
+    # rewriting the same slots with the same values
+    write_tokens = sum(k.shape[0] for k, _, _ in gen0) * wl.n_kv
+    wr_ms = timed(lambda i: [wc.quantize_write(caches[0], k, v, sl) for k, v, sl in gen0], 4)
+    write_ms = float(np.median(wr_ms))
+    del gen0
 
     last = steps_in[W + K - 1]
     reps = 2 * wl.n_layers
@@ -286,7 +297,7 @@ def main():
     routed = float(mask_kv.float().mean().item())
     fb_bytes = th_per_launch * routed * BF16_BYTES
     fb_gbps = fb_bytes / (float(np.median(fb_ms)) * 1e-3) / 1e9 if routed > 0 else 0.0
-    write_gbps = write_tokens * WRITE_BYTES_BF16_IN / (write_ms * 1e-3) / 1e9
+    write_gbps = write_tokens * WRITE_BYTES_BF16_IN / (write_ms * 1e-3) / 1e9   # per prefill of one layer
 
     dominant = "metered_decode" if float(np.median(dec_ms)) >= float(np.median(fb_ms)) else "exact_fallback"
     traffic = None

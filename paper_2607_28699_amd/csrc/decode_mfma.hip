@@ -427,20 +427,22 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   const int r = lane & 15, g = lane >> 4;
   const int unit = blockIdx.y;
   const int b = unit / a.n_kv, kv = unit % a.n_kv;
-  if (a.mask_kv != nullptr && a.mask_kv[unit] == 0) return;   // whole workgroup
   const int G = a.group;
   const int B = a.n_bands;
-  const int L = a.seq_lens[b];
   const int wg_begin = blockIdx.x * a.split_tokens;
-  if (blockIdx.x >= a.n_splits || wg_begin >= L) return;      // whole workgroup
-  const int wg_end = min(min(L, wg_begin + a.split_tokens), a.max_blocks * kBlockTokens);
-  // this wave's share: a contiguous run of pages of the workgroup's split
-  const int n_pages = (wg_end - wg_begin + kBlockTokens - 1) / kBlockTokens;
-  const int ppw = (n_pages + kWaves - 1) / kWaves;
-  const int t_begin = wg_begin + wave * ppw * kBlockTokens;
-  const int t_end = min(wg_end, t_begin + ppw * kBlockTokens);
+  const int32_t* trow = a.table + (int64_t)b * a.max_blocks;
+  const int L = a.seq_lens[b];
 
-  // ---- queries of head r (zero for padding heads), channels 32g .. 32g+31 ----
+  // Requests that need no sequence length go out with it: this wave's block
+  // numbers as if its split were full (it is, except for a sequence's last
+  // split) and the queries, so that their latency overlaps that of the length.
+  const int ppw_full = a.split_tokens / (kBlockTokens * kWaves);
+  const int pg_spec = wg_begin / kBlockTokens + wave * ppw_full;
+  const int nc_spec = max(0, min(min(64, ppw_full), a.max_blocks - pg_spec));
+  const int tv_spec = lane < nc_spec ? trow[pg_spec + lane] : 0;
+  // ---- queries of head r, channels 32g .. 32g+31 ----
+  // Lanes of padding heads (r >= G) repeat head 0: their scores and weights land
+  // in result columns that are never written out.
   const bool hv = r < G;
   const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q) +
                        ((int64_t)b * a.n_q + (int64_t)kv * G + (hv ? r : 0)) * kD + 32 * g;
@@ -449,16 +451,26 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     const uint4* q4 = reinterpret_cast<const uint4*>(qp);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const uint4 v = hv ? q4[i] : make_uint4(0, 0, 0, 0);
+      const uint4 v = q4[i];
       qraw[4 * i] = v.x; qraw[4 * i + 1] = v.y; qraw[4 * i + 2] = v.z; qraw[4 * i + 3] = v.w;
     }
   }
+
+  // whole workgroup: a KV head not routed here, or a split past the sequence end
+  // (evaluated together, so that the length load is not held back behind the mask)
+  const bool unrouted = a.mask_kv != nullptr && a.mask_kv[unit] == 0;
+  if (unrouted | (blockIdx.x >= a.n_splits) | (wg_begin >= L)) return;
+  const int wg_end = min(min(L, wg_begin + a.split_tokens), a.max_blocks * kBlockTokens);
+  // this wave's share: a contiguous run of pages of the workgroup's split
+  const int n_pages = (wg_end - wg_begin + kBlockTokens - 1) / kBlockTokens;
+  const int ppw = (n_pages + kWaves - 1) / kWaves;
+  const int t_begin = wg_begin + wave * ppw * kBlockTokens;
+  const int t_end = min(wg_end, t_begin + ppw * kBlockTokens);
 
   // Pages stream through a ring of three register buffers, so two pages are in
   // flight while one is computed.  Block numbers come 64 pages at a time from one
   // vector load of the table and are read out with readlane (wave-uniform).  The
   // first two pages are requested before the queries are prepared.
-  const int32_t* trow = a.table + (int64_t)b * a.max_blocks;
   // full pages go through the ring; a last page that reaches past t_end is done after it
   const int np = t_end > t_begin ? (t_end - t_begin) / kBlockTokens : 0;
   const int pg0 = t_begin / kBlockTokens;
@@ -470,7 +482,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   // one page never waits for a later one)
   auto start_chunk = [&](int c0) {
     nc = min(64, np - c0);
-    tv = lane < nc ? trow[pg0 + c0 + lane] : 0;
+    if (c0 == 0 && pg0 == pg_spec && nc <= nc_spec) tv = tv_spec;   // the early request holds them
+    else tv = lane < nc ? trow[pg0 + c0 + lane] : 0;
     load_page<KIND, METER>(a, blk_at(0), true, kv, r, g, wit_off, p0);
     __builtin_amdgcn_sched_barrier(0);
     load_page<KIND, METER>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
