@@ -214,14 +214,14 @@ def main():
         st = steps_in[si]
         for layer in range(wl.n_layers):
             it = st["layers"][layer]
+            # new tokens into the quantized cache and the exact bf16 copy in one pass
             if wl.chunk:
-                wc.quantize_write(caches[layer], it["ck"], it["cv"], it["cslots"])
-                wc.quantize_write(exact[layer], it["ck"], it["cv"], it["cslots"])
-            wc.quantize_write(caches[layer], it["k"], it["v"], st["slots"])
-            wc.quantize_write(exact[layer], it["k"], it["v"], st["slots"])
-            wc.metered_decode_attention(caches[layer], it["q"], table, st["lens"], max_len_all, sm,
-                                        ws=ws, out=out, meter=meter, raw=raw)
-            wc.gate(meter, raw, wl.group, args.tau, n_gated=counts, mask_q=mask_q, mask_kv=mask_kv)
+                wc.quantize_write_pair(caches[layer], exact[layer], it["ck"], it["cv"], it["cslots"])
+            wc.quantize_write_pair(caches[layer], exact[layer], it["k"], it["v"], st["slots"])
+            # metered decode with the gate in its split merge, then the exact fallback
+            wc.metered_decode_gate(caches[layer], it["q"], table, st["lens"], max_len_all, sm, args.tau,
+                                   ws=ws, out=out, meter=meter, raw=raw, mask_q=mask_q,
+                                   mask_kv=mask_kv, n_gated=counts)
             wc.exact_decode_attention(exact[layer], it["q"], table, st["lens"], max_len_all, sm,
                                       mask_kv, out, ws=ws)
 
@@ -285,10 +285,10 @@ def main():
 
     last = steps_in[W + K - 1]
     reps = 2 * wl.n_layers
-    dec_ms = timed(lambda i: wc.metered_decode_attention(
+    dec_ms = timed(lambda i: wc.metered_decode_gate(
         caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
-        max_len_all, sm, ws=ws, out=out, meter=meter, raw=raw), reps)
-    wc.gate(meter, raw, wl.group, args.tau, mask_q=mask_q, mask_kv=mask_kv)
+        max_len_all, sm, args.tau, ws=ws, out=out, meter=meter, raw=raw, mask_q=mask_q,
+        mask_kv=mask_kv), reps)
     fb_ms = timed(lambda i: wc.exact_decode_attention(
         exact[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
         max_len_all, sm, mask_kv, out, ws=ws), reps)
@@ -308,7 +308,7 @@ def main():
         if pj.get("kernel_source_hash") == kernel_source_hash():
             traffic = pj.get("bytes_per_launch", {}).get(dominant)
     if dominant == "metered_decode":
-        roof = {"kernel": "metered decode (decode_mfma_kernel + merge_kernel)", "bound": "hbm",
+        roof = {"kernel": "metered decode with gate (decode_mfma_kernel + merge_kernel)", "bound": "hbm",
                 "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                 "algorithmic_bytes_per_launch": th_per_launch * INT8_BYTES,

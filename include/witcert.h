@@ -120,13 +120,23 @@ size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim
  *   FP8_RAW:     code = E4M3(x), nearest-even, saturating at +-448;
  *   BF16:        x rounded to bf16 (nearest-even);
  * and, except for BF16, the key witness w_b = ||(khat - k)_b|| rounded up to fp16
- * (computed in fp32, enlarged by 2^-18 relative before rounding, so it never falls
- * below the exact norm).
+ * (the residual, its squares, sums and square root in float64; one round-up).
  *   k, v          [n_tok][n_kv_heads][head_dim], in_dtype WC_F32 or WC_BF16 (post-RoPE keys)
  *   slot_mapping  [n_tok] int64 device; slot < 0 skips the token
  */
 int wc_quantize_write(const wc_cache* cache, const void* k, const void* v, int in_dtype,
                       const int64_t* slot_mapping, int64_t n_tok, void* stream);
+
+/*
+ * wc_quantize_write into `cache` (INT8_DITHER or FP8_RAW) and into the bf16 exact
+ * cache `exact` that the fallback reads (Sec. 6: the gated heads are recomputed
+ * from an exact copy), in one pass over k and v.  The result equals
+ * wc_quantize_write(cache, ...) followed by wc_quantize_write(exact, ...).
+ * exact must be a BF16 cache with the same head_dim and n_kv_heads and at least
+ * cache->num_blocks blocks; both are addressed by the same slot_mapping.
+ */
+int wc_quantize_write_pair(const wc_cache* cache, const wc_cache* exact, const void* k, const void* v,
+                           int in_dtype, const int64_t* slot_mapping, int64_t n_tok, void* stream);
 
 /*
  * Black-box witness (Sec. 4.1, Tier A scope: any scheme that writes back a
@@ -140,8 +150,9 @@ int wc_witness(const void* x, int x_dtype, const void* xhat, int xhat_dtype, int
 /*
  * Workspace bytes needed by wc_metered_decode_attention / wc_exact_decode_attention
  * for these sizes.  split_tokens as passed to the decode call (0 = library choice).
- * The workspace holds the per-split partial records (no initialization needed);
- * calls that share a workspace must not run concurrently.
+ * The workspace holds the per-split partial records and, for the fused gate,
+ * one int32 per (sequence, KV head); it needs no initialization.  Calls that
+ * share a workspace must not run concurrently.
  */
 size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
                                 int64_t max_seq_len, int split_tokens);
@@ -175,6 +186,20 @@ int wc_metered_decode_attention(const wc_cache* cache, const void* q, int q_dtyp
                                 int64_t max_seq_len, float sm_scale, void* out, int out_dtype,
                                 float* meter, float* raw, int split_tokens, void* ws,
                                 size_t ws_bytes, void* stream);
+
+/*
+ * wc_metered_decode_attention with the gate applied in its split merge (one
+ * launch fewer): same arguments, then tau, mask_q, mask_kv and n_gated as in
+ * wc_gate below.  Results equal wc_metered_decode_attention followed by
+ * wc_gate(meter, raw, batch, n_q_heads, n_q_heads / n_kv_heads, tau, mask_q,
+ * mask_kv, n_gated).  raw may be NULL also when tau >= 1.
+ */
+int wc_metered_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int batch,
+                           int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                           const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out,
+                           int out_dtype, float* meter, float* raw, int split_tokens, float tau,
+                           uint8_t* mask_q, uint8_t* mask_kv, int32_t* n_gated, void* ws,
+                           size_t ws_bytes, void* stream);
 
 /*
  * Gate (the meter loop's gate, Sec. 6; certified vs risk-ranked, Sec. 4.3):

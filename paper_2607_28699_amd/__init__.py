@@ -14,7 +14,9 @@ from .api import (  # noqa: F401
     exact_decode_attention,
     gate,
     metered_decode_attention,
+    metered_decode_gate,
     quantize_write,
+    quantize_write_pair,
     witness,
 )
 from ._lib import LIB_PATH, WitCertError, lib  # noqa: F401

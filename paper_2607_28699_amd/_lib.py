@@ -17,9 +17,9 @@ WC_ROPE_HALF, WC_ROPE_INTERLEAVED = 0, 1
 WC_BLOCK_TOKENS = 16
 
 EXPORTS = (
-    "wc_strerror", "wc_version", "wc_cache_bytes", "wc_quantize_write", "wc_witness",
-    "wc_decode_workspace_size", "wc_metered_decode_attention", "wc_gate",
-    "wc_exact_decode_attention",
+    "wc_strerror", "wc_version", "wc_cache_bytes", "wc_quantize_write", "wc_quantize_write_pair",
+    "wc_witness", "wc_decode_workspace_size", "wc_metered_decode_attention",
+    "wc_metered_decode_gate", "wc_gate", "wc_exact_decode_attention",
 )
 
 
@@ -58,6 +58,7 @@ def lib() -> ctypes.CDLL:
         "wc_cache_bytes": (sz, [ctypes.c_int, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                 ctypes.POINTER(sz)]),
         "wc_quantize_write": (ctypes.c_int, [cp, vp, vp, ctypes.c_int, vp, i64, vp]),
+        "wc_quantize_write_pair": (ctypes.c_int, [cp, cp, vp, vp, ctypes.c_int, vp, i64, vp]),
         "wc_witness": (ctypes.c_int, [vp, ctypes.c_int, vp, ctypes.c_int, i64, ctypes.c_int,
                                       ctypes.c_int, ctypes.c_int, vp, vp]),
         "wc_decode_workspace_size": (sz, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -66,6 +67,10 @@ def lib() -> ctypes.CDLL:
                                                        ctypes.c_int, vp, ctypes.c_int, vp, i64, f32,
                                                        vp, ctypes.c_int, vp, vp, ctypes.c_int, vp,
                                                        sz, vp]),
+        "wc_metered_decode_gate": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                  vp, ctypes.c_int, vp, i64, f32, vp, ctypes.c_int,
+                                                  vp, vp, ctypes.c_int, f32, vp, vp, vp, vp, sz,
+                                                  vp]),
         "wc_gate": (ctypes.c_int, [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, f32, vp, vp,
                                    vp, vp]),
         "wc_exact_decode_attention": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int,

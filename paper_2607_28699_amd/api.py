@@ -103,6 +103,16 @@ def quantize_write(cache: PagedCache, k: torch.Tensor, v: torch.Tensor, slots: t
                                   k.shape[0], _stream()), "wc_quantize_write")
 
 
+def quantize_write_pair(cache: PagedCache, exact: PagedCache, k: torch.Tensor, v: torch.Tensor,
+                        slots: torch.Tensor) -> None:
+    """quantize_write into `cache` and a bf16 copy into `exact`, in one pass."""
+    _dev_check(k, v, slots)
+    assert slots.dtype == torch.int64 and k.shape == v.shape and k.dtype == v.dtype
+    c, e = cache.struct(), exact.struct()
+    check(lib().wc_quantize_write_pair(ctypes.byref(c), ctypes.byref(e), _ptr(k), _ptr(v), _dt(k),
+                                       _ptr(slots), k.shape[0], _stream()), "wc_quantize_write_pair")
+
+
 def witness(x: torch.Tensor, xhat: torch.Tensor, n_bands: int, rope_layout: str = "half",
             out: torch.Tensor | None = None) -> torch.Tensor:
     """Band norms of xhat - x rounded up to fp16: [n_vec, n_bands] float16."""
@@ -142,6 +152,30 @@ def metered_decode_attention(cache: PagedCache, q: torch.Tensor, block_table: to
         _ptr(seq_lens), max_seq_len, float(sm_scale), _ptr(out), _dt(out), _ptr(meter), _ptr(raw),
         split_tokens, _ptr(ws), ws.numel(), _stream()), "wc_metered_decode_attention")
     return out, meter, raw
+
+
+def metered_decode_gate(cache: PagedCache, q: torch.Tensor, block_table: torch.Tensor,
+                        seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float, tau: float,
+                        out_dtype=torch.float32, split_tokens: int = 0, ws=None, out=None, meter=None,
+                        raw=None, mask_q=None, mask_kv=None, n_gated=None):
+    """metered_decode_attention then gate, fused: -> (out, meter, raw, mask_q, mask_kv)."""
+    _dev_check(q, block_table, seq_lens)
+    batch, n_q, d = q.shape
+    if ws is None:
+        ws = decode_workspace(batch, n_q, cache.n_kv, d, max_seq_len, split_tokens, q.device)
+    out = torch.empty((batch, n_q, d), dtype=out_dtype, device=q.device) if out is None else out
+    meter = torch.empty((batch, n_q), dtype=torch.float32, device=q.device) if meter is None else meter
+    raw = torch.empty((batch, n_q), dtype=torch.float32, device=q.device) if raw is None else raw
+    mask_q = torch.empty((batch, n_q), dtype=torch.uint8, device=q.device) if mask_q is None else mask_q
+    mask_kv = (torch.empty((batch, cache.n_kv), dtype=torch.uint8, device=q.device)
+               if mask_kv is None else mask_kv)
+    c = cache.struct()
+    check(lib().wc_metered_decode_gate(
+        ctypes.byref(c), _ptr(q), _dt(q), batch, n_q, _ptr(block_table), block_table.shape[1],
+        _ptr(seq_lens), max_seq_len, float(sm_scale), _ptr(out), _dt(out), _ptr(meter), _ptr(raw),
+        split_tokens, float(tau), _ptr(mask_q), _ptr(mask_kv), _ptr(n_gated), _ptr(ws), ws.numel(),
+        _stream()), "wc_metered_decode_gate")
+    return out, meter, raw, mask_q, mask_kv
 
 
 def gate(meter: torch.Tensor, raw: torch.Tensor, group: int, tau: float,

@@ -64,10 +64,18 @@ size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim
   return s[0] + s[1] + s[2] + s[3] + s[4];
 }
 
-int wc_quantize_write(const wc_cache* cache, const void* k, const void* v, int in_dtype,
-                      const int64_t* slot_mapping, int64_t n_tok, void* stream) {
+static int write_common(const wc_cache* cache, const wc_cache* exact, const void* k, const void* v,
+                        int in_dtype, const int64_t* slot_mapping, int64_t n_tok, void* stream) {
   int st = check_cache(cache, false);
   if (st != WC_OK) return st;
+  if (exact != nullptr) {
+    st = check_cache(exact, false);
+    if (st != WC_OK) return st;
+    if (cache->kind == WC_KIND_BF16 || exact->kind != WC_KIND_BF16 ||
+        exact->head_dim != cache->head_dim || exact->n_kv_heads != cache->n_kv_heads ||
+        exact->num_blocks < cache->num_blocks)
+      return WC_EINVAL;
+  }
   if (n_tok < 0 || (in_dtype != WC_F32 && in_dtype != WC_BF16)) return WC_EINVAL;
   if (n_tok == 0) return WC_OK;
   if (!k || !v || !slot_mapping || !aligned16(k) || !aligned16(v)) return WC_EINVAL;
@@ -90,7 +98,20 @@ int wc_quantize_write(const wc_cache* cache, const void* k, const void* v, int i
   a.k_scale = static_cast<uint16_t*>(cache->k_scale);
   a.v_scale = static_cast<uint16_t*>(cache->v_scale);
   a.k_witness = static_cast<uint16_t*>(cache->k_witness);
+  a.x_k_data = exact ? exact->k_data : nullptr;
+  a.x_v_data = exact ? exact->v_data : nullptr;
   return hip_status(wc::launch_quantize_write(a, static_cast<hipStream_t>(stream)));
+}
+
+int wc_quantize_write(const wc_cache* cache, const void* k, const void* v, int in_dtype,
+                      const int64_t* slot_mapping, int64_t n_tok, void* stream) {
+  return write_common(cache, nullptr, k, v, in_dtype, slot_mapping, n_tok, stream);
+}
+
+int wc_quantize_write_pair(const wc_cache* cache, const wc_cache* exact, const void* k, const void* v,
+                           int in_dtype, const int64_t* slot_mapping, int64_t n_tok, void* stream) {
+  if (exact == nullptr) return WC_EINVAL;
+  return write_common(cache, exact, k, v, in_dtype, slot_mapping, n_tok, stream);
 }
 
 int wc_witness(const void* x, int x_dtype, const void* xhat, int xhat_dtype, int64_t n_vec,
@@ -114,7 +135,7 @@ size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int he
     return 0;
   const int st = wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens);
   const int64_t ns = wc::n_splits_for(max_seq_len, st);
-  return wc::records_bytes(batch, n_q_heads, ns, head_dim);
+  return wc::records_bytes(batch, n_q_heads, ns, head_dim) + wc::gate_unit_bytes(batch, n_kv_heads);
 }
 
 static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int batch,
@@ -148,6 +169,8 @@ static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int 
   a.table = block_table;
   a.seq_lens = seq_lens;
   a.part = static_cast<float*>(ws);
+  a.gate_unit = reinterpret_cast<int32_t*>(static_cast<char*>(ws) +
+                                           wc::records_bytes(batch, n_q_heads, ns, cache->head_dim));
   a.out = out;
   a.kind = cache->kind;
   a.head_dim = cache->head_dim;
@@ -190,6 +213,30 @@ int wc_metered_decode_attention(const wc_cache* cache, const void* q, int q_dtyp
   a.meter = meter;
   a.raw = raw;
   a.mask_kv = nullptr;
+  return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
+}
+
+int wc_metered_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int batch,
+                           int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                           const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out,
+                           int out_dtype, float* meter, float* raw, int split_tokens, float tau,
+                           uint8_t* mask_q, uint8_t* mask_kv, int32_t* n_gated, void* ws,
+                           size_t ws_bytes, void* stream) {
+  int s = check_cache(cache, true);
+  if (s != WC_OK) return s;
+  if (cache->kind == WC_KIND_BF16) return WC_EINVAL;
+  if (!(tau >= 0.0f)) return WC_EINVAL;
+  if (batch > 0 && (!meter || !mask_q || !mask_kv)) return WC_EINVAL;
+  wc::DecodeArgs a{};
+  s = decode_common(cache, q, q_dtype, batch, n_q_heads, block_table, max_blocks_per_seq,
+                    seq_lens, max_seq_len, sm_scale, out, out_dtype, split_tokens, ws, ws_bytes, a);
+  if (s != WC_OK) return s;
+  a.meter = meter;
+  a.raw = raw;
+  a.gate_mask_q = mask_q;
+  a.gate_mask_kv = mask_kv;
+  a.gate_count = n_gated;
+  a.gate_tau = tau;
   return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
 }
 

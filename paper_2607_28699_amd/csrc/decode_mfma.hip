@@ -427,6 +427,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   const int r = lane & 15, g = lane >> 4;
   const int unit = blockIdx.y;
   const int b = unit / a.n_kv, kv = unit % a.n_kv;
+  gate_clear(a, unit);
   const int G = a.group;
   const int B = a.n_bands;
   const int wg_begin = blockIdx.x * a.split_tokens;

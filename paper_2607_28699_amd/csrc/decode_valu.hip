@@ -50,6 +50,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   const int split = blockIdx.x;
   const int unit = blockIdx.y;
   const int b = unit / a.n_kv, kv = unit % a.n_kv;
+  gate_clear(a, unit);
   if (a.mask_kv != nullptr && a.mask_kv[unit] == 0) return;
   const int L = a.seq_lens[b];
   const int t_begin = split * a.split_tokens;
@@ -424,8 +425,23 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
         raw = 0.5f * am1 * (2.0f + am1);
         if (!(raw <= FLT_MAX)) raw = INFINITY;
       }
-      a.meter[bh] = fminf(1.0f, raw);
+      const float meter = fminf(1.0f, raw);
+      a.meter[bh] = meter;
       if (a.raw != nullptr) a.raw[bh] = raw;
+      if (a.gate_mask_q != nullptr) {
+        // the gate of this query head; its KV head is counted by the first gated head
+        const bool gated = (a.gate_tau >= 1.0f ? raw : meter) > a.gate_tau;
+        a.gate_mask_q[bh] = gated ? 1 : 0;
+        if (gated) {
+          const int unit = b * a.n_kv + h / a.group;
+          a.gate_mask_kv[unit] = 1;
+          const int first = atomicAdd(a.gate_unit + unit, 1) == 0;
+          if (a.gate_count != nullptr) {
+            atomicAdd(a.gate_count, 1);
+            if (first) atomicAdd(a.gate_count + 1, 1);
+          }
+        }
+      }
     }
   }
 }

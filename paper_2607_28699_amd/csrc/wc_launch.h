@@ -20,6 +20,8 @@ struct WriteArgs {
   uint16_t* k_scale;
   uint16_t* v_scale;
   uint16_t* k_witness;
+  void* x_k_data;           // bf16 exact cache written in the same pass (or null)
+  void* x_v_data;
 };
 
 struct WitnessArgs {
@@ -51,7 +53,21 @@ struct DecodeArgs {
   uint32_t key0, key1;
   float sm_scale;
   int use_mfma;             // matrix-core kernels where supported (else the vector path)
+  // gate applied in the split merge (null gate_mask_q: no gate)
+  uint8_t* gate_mask_q;     // [batch][n_q]
+  uint8_t* gate_mask_kv;    // [batch][n_kv], cleared by the decode kernel
+  int32_t* gate_unit;       // [batch][n_kv] gated-head counts (workspace), cleared likewise
+  int32_t* gate_count;      // device int32[2] or null
+  float gate_tau;
 };
+
+// Clears the gate outputs of one (sequence, KV head) ahead of the merge.
+__device__ __forceinline__ void gate_clear(const DecodeArgs& a, int unit) {
+  if (a.gate_mask_q != nullptr && blockIdx.x == 0 && threadIdx.x == 0) {
+    a.gate_mask_kv[unit] = 0;
+    a.gate_unit[unit] = 0;
+  }
+}
 
 struct GateArgs {
   const float* meter;
@@ -69,10 +85,14 @@ inline int64_t n_splits_for(int64_t max_seq_len, int split_tokens) {
   return max_seq_len <= 0 ? 1 : (max_seq_len + split_tokens - 1) / split_tokens;
 }
 __host__ __device__ inline size_t partial_record_floats(int head_dim) { return (size_t)head_dim + 4; }
-// Workspace: the partial records, rounded up to 256 bytes.
+// Workspace: the partial records, then one int32 per (sequence, KV head) for the
+// fused gate; each part rounded up to 256 bytes.
 inline size_t records_bytes(int batch, int n_q, int64_t n_splits, int head_dim) {
   const size_t b = (size_t)batch * n_q * n_splits * partial_record_floats(head_dim) * sizeof(float);
   return (b + 255) / 256 * 256;
+}
+inline size_t gate_unit_bytes(int batch, int n_kv) {
+  return ((size_t)batch * n_kv * sizeof(int32_t) + 255) / 256 * 256;
 }
 
 hipError_t launch_quantize_write(const WriteArgs& a, hipStream_t st);

@@ -49,6 +49,26 @@ __device__ __forceinline__ void int8_scale(float amax, uint16_t& s_bits, float& 
   inv = s > 0.0f ? __fdiv_rn(1.0f, s) : 0.0f;
 }
 
+// bf16 copy of one token-head's 16 channels (this lane's share) into an exact cache.
+template <int D>
+__device__ __forceinline__ void store_exact(void* k_data, void* v_data, int64_t bh, int off, int g,
+                                            const float (&k)[16], const float (&v)[16]) {
+  uint32_t kw[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    kw[i] = (uint32_t)f32_to_bf16_rne(k[2 * i]) | ((uint32_t)f32_to_bf16_rne(k[2 * i + 1]) << 16);
+  uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(k_data) + (bh * kBlockTokens + off) * D +
+                                       16 * g);
+  kd[0] = make_uint4(kw[0], kw[1], kw[2], kw[3]);
+  kd[1] = make_uint4(kw[4], kw[5], kw[6], kw[7]);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    uint16_t* vd = reinterpret_cast<uint16_t*>(v_data) + bh * (kBlockTokens * D) +
+                   ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
+    *vd = f32_to_bf16_rne(v[i]);
+  }
+}
+
 template <int D, int KIND, typename TIn>
 __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs a) {
   constexpr int LPT = D / 16;                 // lanes per token-head
@@ -147,24 +167,10 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
       *kd = make_uint4(kc[0], kc[1], kc[2], kc[3]);
     }
   } else {  // WC_KIND_BF16: exact cache, no witness
-    if (active) {
-      uint32_t kw[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        kw[i] = (uint32_t)f32_to_bf16_rne(k[2 * i]) | ((uint32_t)f32_to_bf16_rne(k[2 * i + 1]) << 16);
-      uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.k_data) +
-                                           (bh * kBlockTokens + off) * D + 16 * g);
-      kd[0] = make_uint4(kw[0], kw[1], kw[2], kw[3]);
-      kd[1] = make_uint4(kw[4], kw[5], kw[6], kw[7]);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        uint16_t* vd = reinterpret_cast<uint16_t*>(a.v_data) + bh * (kBlockTokens * D) +
-                       ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
-        *vd = f32_to_bf16_rne(v[i]);
-      }
-    }
+    if (active) store_exact<D>(a.k_data, a.v_data, bh, off, g, k, v);
     return;
   }
+  if (active && a.x_k_data != nullptr) store_exact<D>(a.x_k_data, a.x_v_data, bh, off, g, k, v);
 
   // ---- witness: band norms of the key residual, rounded up to fp16 ----
   __syncthreads();
