@@ -188,6 +188,28 @@ int wc_metered_decode_attention(const wc_cache* cache, const void* q, int q_dtyp
                                 size_t ws_bytes, void* stream);
 
 /*
+ * Tier-B certified decode (Sec. 4.2, Tier B: Lemma uniform sub-Gaussian proxy and
+ * the request-level budget) over an INT8_DITHER cache: as
+ * wc_metered_decode_attention, with the witness bound c_t replaced by the
+ * sub-Gaussian radius of the subtractive-dither residual,
+ *   u_t = (alpha_h + beta_h) * s_t,
+ *   alpha_h = sm_scale * ||q_h|| * sqrt(2 log(2 S_b / delta_loc) / 12),
+ *   beta_h  = sm_scale * ||q_h||_1 / 256 (bound on the residual mean of the 8-bit
+ *             dither lattice),
+ * s_t the token's stored key scale and S_b = seq_lens[b]; A = sum_t ptilde_t e^{u_t},
+ * raw = (A^2 - 1)/2, meter = min(1, raw).  No witness is read (k_witness may be
+ * NULL).  With probability at least 1 - delta_loc (over the dither, for a query
+ * that does not depend on it) raw bounds the TV of every query head of the call;
+ * delta_loc in (0, 1) is the per-(layer, head, step) budget, e.g. delta_req /
+ * (layers * query heads * steps).
+ */
+int wc_tierb_decode_attention(const wc_cache* cache, const void* q, int q_dtype, int batch,
+                              int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                              const int32_t* seq_lens, int64_t max_seq_len, float sm_scale,
+                              void* out, int out_dtype, float* meter, float* raw, int split_tokens,
+                              float delta_loc, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * wc_metered_decode_attention with the gate applied in its split merge (one
  * launch fewer): same arguments, then tau, mask_q, mask_kv and n_gated as in
  * wc_gate below.  Results equal wc_metered_decode_attention followed by

@@ -20,6 +20,8 @@ theorem or table) and is written for reading against it, not for speed:
                  TV bound (Theorem sound replacement), saturation reporting
                  (Sec. 4.3), the flawed certificate (Eq. flawed) and the
                  two-sided form (Proposition two-sided) for regression tests.
+* ``tierb``      Tier-B sub-Gaussian certificate of the dithered cache (Sec. 4.2:
+                 Lemma uniform sub-Gaussian proxy, radius, request-level budget).
 * ``gate``       threshold gate and exact fallback (the meter loop, Sec. 6).
 * ``decode``     one metered decode of a batch over per-token caches, composed
                  from the above.
@@ -27,4 +29,4 @@ theorem or table) and is written for reading against it, not for speed:
 Parity status of each function is listed in its docstring; every function is
 pinned by a CPU test in ``tests/test_oracle_*.py``.
 """
-from . import attention, decode, fpformats, gate, meter, philox, quantizer  # noqa: F401
+from . import attention, decode, fpformats, gate, meter, philox, quantizer, tierb  # noqa: F401

@@ -17,6 +17,8 @@ from .api import (  # noqa: F401
     metered_decode_gate,
     quantize_write,
     quantize_write_pair,
+    tierb_decode_attention,
+    tierb_delta_loc,
     witness,
 )
 from ._lib import LIB_PATH, WitCertError, lib  # noqa: F401

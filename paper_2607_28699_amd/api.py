@@ -154,6 +154,31 @@ def metered_decode_attention(cache: PagedCache, q: torch.Tensor, block_table: to
     return out, meter, raw
 
 
+def tierb_delta_loc(delta_req: float, n_layers: int, n_q_heads: int, n_steps: int) -> float:
+    """Per-(layer, head, step) failure budget delta_req / (L * H * T) (Sec. 4.2)."""
+    return float(delta_req) / (n_layers * n_q_heads * n_steps)
+
+
+def tierb_decode_attention(cache: PagedCache, q: torch.Tensor, block_table: torch.Tensor,
+                           seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float, delta_loc: float,
+                           out_dtype=torch.float32, split_tokens: int = 0, ws=None, out=None, meter=None,
+                           raw=None):
+    """Tier-B certified decode over an int8_dither cache -> (out, meter, raw)."""
+    _dev_check(q, block_table, seq_lens)
+    batch, n_q, d = q.shape
+    if ws is None:
+        ws = decode_workspace(batch, n_q, cache.n_kv, d, max_seq_len, split_tokens, q.device)
+    out = torch.empty((batch, n_q, d), dtype=out_dtype, device=q.device) if out is None else out
+    meter = torch.empty((batch, n_q), dtype=torch.float32, device=q.device) if meter is None else meter
+    raw = torch.empty((batch, n_q), dtype=torch.float32, device=q.device) if raw is None else raw
+    c = cache.struct()
+    check(lib().wc_tierb_decode_attention(
+        ctypes.byref(c), _ptr(q), _dt(q), batch, n_q, _ptr(block_table), block_table.shape[1],
+        _ptr(seq_lens), max_seq_len, float(sm_scale), _ptr(out), _dt(out), _ptr(meter), _ptr(raw),
+        split_tokens, float(delta_loc), _ptr(ws), ws.numel(), _stream()), "wc_tierb_decode_attention")
+    return out, meter, raw
+
+
 def metered_decode_gate(cache: PagedCache, q: torch.Tensor, block_table: torch.Tensor,
                         seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float, tau: float,
                         out_dtype=torch.float32, split_tokens: int = 0, ws=None, out=None, meter=None,

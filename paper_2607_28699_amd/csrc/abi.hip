@@ -13,7 +13,9 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 int elem_bytes(int kind) { return kind == WC_KIND_BF16 ? 2 : 1; }
 
-int check_cache(const wc_cache* c, bool need_witness) {
+// need_witness: also a BF16 cache must carry one; witness_optional: a quantized
+// cache may come without one (the Tier-B decode reads none).
+int check_cache(const wc_cache* c, bool need_witness, bool witness_optional = false) {
   if (c == nullptr) return WC_EINVAL;
   if (c->kind < WC_KIND_INT8_DITHER || c->kind > WC_KIND_BF16) return WC_EINVAL;
   if (c->head_dim != 64 && c->head_dim != 128) return WC_EUNSUPPORTED;
@@ -23,7 +25,7 @@ int check_cache(const wc_cache* c, bool need_witness) {
   if (!aligned16(c->k_data) || !aligned16(c->v_data)) return WC_EINVAL;
   if (c->kind != WC_KIND_BF16 || need_witness) {
     if (c->n_bands < 1 || c->n_bands > 16 || c->head_dim % (2 * c->n_bands)) return WC_EINVAL;
-    if (!c->k_witness || !aligned16(c->k_witness)) return WC_EINVAL;
+    if (c->k_witness ? !aligned16(c->k_witness) : !witness_optional) return WC_EINVAL;
   }
   if (c->kind == WC_KIND_INT8_DITHER &&
       (!c->k_scale || !c->v_scale || !aligned16(c->k_scale) || !aligned16(c->v_scale)))
@@ -213,6 +215,26 @@ int wc_metered_decode_attention(const wc_cache* cache, const void* q, int q_dtyp
   a.meter = meter;
   a.raw = raw;
   a.mask_kv = nullptr;
+  return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
+}
+
+int wc_tierb_decode_attention(const wc_cache* cache, const void* q, int q_dtype, int batch,
+                              int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                              const int32_t* seq_lens, int64_t max_seq_len, float sm_scale,
+                              void* out, int out_dtype, float* meter, float* raw, int split_tokens,
+                              float delta_loc, void* ws, size_t ws_bytes, void* stream) {
+  int s = check_cache(cache, false, true);   // no witness is read
+  if (s != WC_OK) return s;
+  if (cache->kind != WC_KIND_INT8_DITHER) return WC_EINVAL;
+  if (!(delta_loc > 0.0f && delta_loc < 1.0f)) return WC_EINVAL;
+  if (batch > 0 && !meter) return WC_EINVAL;
+  wc::DecodeArgs a{};
+  s = decode_common(cache, q, q_dtype, batch, n_q_heads, block_table, max_blocks_per_seq,
+                    seq_lens, max_seq_len, sm_scale, out, out_dtype, split_tokens, ws, ws_bytes, a);
+  if (s != WC_OK) return s;
+  a.meter = meter;
+  a.raw = raw;
+  a.tierb_delta = delta_loc;
   return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
 }
 

@@ -123,7 +123,7 @@ __device__ __forceinline__ uint2 bload8(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
 
-template <int KIND, bool METER>
+template <int KIND, bool METER, bool TB>
 __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool valid, int kv, int r,
                                           int g, int wit_off, PageRegs<KIND>& p) {
   constexpr int KB = KIND == WC_KIND_BF16 ? 64 : 32;   // bytes per lane and tensor
@@ -145,7 +145,7 @@ __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool val
     p.ks = bload8(page_rsrc(a.k_scale + page * kBlockTokens, sb), 8 * g);
     p.vs = bload8(page_rsrc(a.v_scale + page * kBlockTokens, sb), 8 * g);
   }
-  if constexpr (METER) {
+  if constexpr (METER && !TB) {   // Tier B reads no witness
     const int wb = valid ? 2 * kBlockTokens * a.n_bands : 0;
     p.wit = bload16(page_rsrc(a.k_witness + page * kBlockTokens * a.n_bands, wb), wit_off);
   }
@@ -166,6 +166,7 @@ struct WaveConst {
   h8_t qnop;       // band norms * sm_scale * log2(e), hi (g < 2) / lo (g >= 2) parts
   float s1_init;   // 2303 sum(q) / 512: the dither offset, preloaded into the code accumulator
   float lmul;      // logit multiplier: sm_scale * log2(e) (times 256 for fp8 operands)
+  float ab2;       // Tier B: (alpha_h + beta_h) * log2(e)
   uint32_t layer_head;
   bool wit_ok;
 };
@@ -203,7 +204,7 @@ __device__ __forceinline__ uint32_t dpp_from_upper8(uint32_t v) {
 }
 
 // One 16-token page.  FULL: every token of the page is below t_end (no masking).
-template <int KIND, bool METER, bool FULL, bool HALF>
+template <int KIND, bool METER, bool FULL, bool HALF, bool TB>
 __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs<KIND>& cur, int t0,
                                              int t_end, int r, int g, const WaveConst& wc,
                                              uint8_t* my_dsh, WaveState& st) {
@@ -254,7 +255,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     }
   }
   f4_t cb = z4;
-  if constexpr (METER) {
+  if constexpr (METER && !TB) {
     const uint4 w = wc.wit_ok ? cur.wit : make_uint4(0, 0, 0, 0);
     cb = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, w), wc.qnop, cb, 0, 0, 0);
   }
@@ -278,7 +279,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   if constexpr (HALF) {
     scv[0] = dpp_from_lower8(scv[0], scv[2]);
     scv[1] = dpp_from_lower8(scv[1], scv[3]);
-    if constexpr (METER) {
+    if constexpr (METER && !TB) {
       cbv[0] = dpp_from_lower8(cbv[0], cbv[2]);
       cbv[1] = dpp_from_lower8(cbv[1], cbv[3]);
     }
@@ -289,6 +290,12 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   }
   const h2_t ksh[2] = {as_h2(ksw0), as_h2(ksw1)};
   const h2_t vsh[2] = {as_h2(vsw0), as_h2(vsw1)};
+  if constexpr (TB) {
+    // Tier B (Sec. 4.2): the radius u_t = (alpha_h + beta_h) s_t from the stored
+    // key scale of each of this lane's tokens, in log2 units
+#pragma unroll
+    for (int e = 0; e < NT; ++e) cbv[e] = fmaf((float)ksh[e >> 1][e & 1], wc.ab2, 0.0f);
+  }
   bool valid[NT];
   float lg[NT];
   float loc = -INFINITY;
@@ -415,7 +422,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   }
 }
 
-template <int KIND, bool METER, bool HALF>
+template <int KIND, bool METER, bool HALF, bool TB>
 __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
   __shared__ float qn_s[kWaves][16][16];
@@ -485,9 +492,9 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     nc = min(64, np - c0);
     if (c0 == 0 && pg0 == pg_spec && nc <= nc_spec) tv = tv_spec;   // the early request holds them
     else tv = lane < nc ? trow[pg0 + c0 + lane] : 0;
-    load_page<KIND, METER>(a, blk_at(0), true, kv, r, g, wit_off, p0);
+    load_page<KIND, METER, TB>(a, blk_at(0), true, kv, r, g, wit_off, p0);
     __builtin_amdgcn_sched_barrier(0);
-    load_page<KIND, METER>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
+    load_page<KIND, METER, TB>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
     __builtin_amdgcn_sched_barrier(0);
   };
   if (np > 0) start_chunk(0);
@@ -520,7 +527,23 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   // band norms ||q_b|| * sm_scale * log2(e) -> witness-MFMA B operand (hi parts
   // for g < 2, lo for g >= 2); the bound then comes out in log2 units
   wc.qnop = pack8(0, 0, 0, 0);
-  if constexpr (METER) {
+  wc.ab2 = 0.0f;
+  if constexpr (TB) {
+    float sq = 0.0f, l1 = 0.0f;   // ||q||^2 and ||q||_1 of head r
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const float x = bf16_to_f32((uint16_t)((qraw[i >> 1] >> (16 * (i & 1))) & 0xFFFFu));
+      sq = fmaf(x, x, sq);
+      l1 += fabsf(x);
+    }
+    sq += __shfl_xor(sq, 16, 64);
+    sq += __shfl_xor(sq, 32, 64);
+    l1 += __shfl_xor(l1, 16, 64);
+    l1 += __shfl_xor(l1, 32, 64);
+    wc.ab2 = tierb_factor(sq, l1, L, a.tierb_delta, a.sm_scale) * kLog2e;
+    // with two tokens per lane, lanes r + 8 hold tokens of head r
+    if constexpr (HALF) wc.ab2 = dpp_from_lower8(wc.ab2, wc.ab2);
+  } else if constexpr (METER) {
     // Squares of this lane's 32 channels summed in runs of 4.  The band of
     // channel 32g + i is base + i / S with S = 64 / B (rotate-half pairs (j, j + 64))
     // or 128 / B (adjacent pairs), so runs of 4 coarsen exactly into the lane's bands.
@@ -601,17 +624,17 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     // assume the ring order may differ on the back edge and wait for every page.
     for (int j = 0; j < nc; j += 3) {
       set_priority(c0 + j);
-      load_page<KIND, METER>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
+      load_page<KIND, METER, TB>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
       __builtin_amdgcn_sched_barrier(0);
-      process_page<KIND, METER, true, HALF>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
-      load_page<KIND, METER>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
+      process_page<KIND, METER, true, HALF, TB>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      load_page<KIND, METER, TB>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 1 < nc)
-        process_page<KIND, METER, true, HALF>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
-      load_page<KIND, METER>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
+        process_page<KIND, METER, true, HALF, TB>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      load_page<KIND, METER, TB>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 2 < nc)
-        process_page<KIND, METER, true, HALF>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+        process_page<KIND, METER, true, HALF, TB>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
     }
     c0 += 64;
     if (c0 < np) start_chunk(c0);
@@ -619,8 +642,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __builtin_amdgcn_s_setprio(0);
   const int t_last = t_begin + np * kBlockTokens;
   if (t_last < t_end) {   // a partial last page: tokens from t_end on are masked
-    load_page<KIND, METER>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
-    process_page<KIND, METER, false, HALF>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
+    load_page<KIND, METER, TB>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
+    process_page<KIND, METER, false, HALF, TB>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
   }
 
   // ---- merge the four waves of the workgroup, write one partial record ----
@@ -708,20 +731,26 @@ bool mfma_decode_supported(const DecodeArgs& a) {
 
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st) {
   const dim3 grid(a.n_splits, a.batch * a.n_kv);
+  const dim3 block(64 * kWaves);
+  const bool tb = metered && a.tierb_delta > 0.0f;   // Tier B: INT8 dithered cache only
   if (a.group <= 8) {
     if (!metered)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, true>), grid, dim3(64 * kWaves), 0, st, a);
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, true, false>), grid, block, 0, st, a);
+    else if (tb)
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, true, true>), grid, block, 0, st, a);
     else if (a.kind == WC_KIND_INT8_DITHER)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, true>), grid, dim3(64 * kWaves), 0, st, a);
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, true, false>), grid, block, 0, st, a);
     else
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, true>), grid, dim3(64 * kWaves), 0, st, a);
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, true, false>), grid, block, 0, st, a);
   } else {
     if (!metered)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, false>), grid, dim3(64 * kWaves), 0, st, a);
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, false, false>), grid, block, 0, st, a);
+    else if (tb)
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, false, true>), grid, block, 0, st, a);
     else if (a.kind == WC_KIND_INT8_DITHER)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, false>), grid, dim3(64 * kWaves), 0, st, a);
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, false, false>), grid, block, 0, st, a);
     else
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, false>), grid, dim3(64 * kWaves), 0, st, a);
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, false, false>), grid, block, 0, st, a);
   }
   return hipGetLastError();
 }

@@ -39,6 +39,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
 
   __shared__ float q_s[kGMax][D];
   __shared__ float qbn_s[kGMax][16];
+  __shared__ float ab_s[kGMax];       // Tier-B factor per head
   __shared__ float logit_s[kGMax][kT];
   __shared__ float cb_s[kGMax][kT];
   __shared__ float pw_s[kGMax][kT];
@@ -78,6 +79,16 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         acc = fmaf(x, x, acc);
       }
       qbn_s[h][bb] = sqrtf(acc) * a.sm_scale;
+    }
+    if (a.tierb_delta > 0.0f) {
+      for (int h = tid; h < G; h += kThreads) {
+        float sq = 0.0f, l1 = 0.0f;
+        for (int c = 0; c < D; ++c) {
+          sq = fmaf(q_s[h][c], q_s[h][c], sq);
+          l1 += fabsf(q_s[h][c]);
+        }
+        ab_s[h] = tierb_factor(sq, l1, L, a.tierb_delta, a.sm_scale);
+      }
     }
   }
 
@@ -174,7 +185,11 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         d += __shfl_xor(d, 2, 4);
         if (part == 0) logit_s[h][i] = valid ? d * a.sm_scale : -INFINITY;
       }
-      if constexpr (METER) {
+      if (METER && a.tierb_delta > 0.0f) {   // Tier B: u_t = (alpha_h + beta_h) s_t, no witness
+        const float s = valid ? f16_to_f32(a.k_scale[page * kBlockTokens + off]) : 0.0f;
+        if (part == 0)
+          for (int h = 0; h < G; ++h) cb_s[h][i] = ab_s[h] * s;
+      } else if constexpr (METER) {
         float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
         if (valid) {
 #pragma unroll

@@ -53,6 +53,7 @@ struct DecodeArgs {
   uint32_t key0, key1;
   float sm_scale;
   int use_mfma;             // matrix-core kernels where supported (else the vector path)
+  float tierb_delta;        // > 0: Tier-B radius (u_t = (alpha_h + beta_h) s_t) instead of the witness
   // gate applied in the split merge (null gate_mask_q: no gate)
   uint8_t* gate_mask_q;     // [batch][n_q]
   uint8_t* gate_mask_kv;    // [batch][n_kv], cleared by the decode kernel
@@ -60,6 +61,16 @@ struct DecodeArgs {
   int32_t* gate_count;      // device int32[2] or null
   float gate_tau;
 };
+
+// Tier-B factor (alpha + beta) of one query head: u_t = (alpha + beta) * s_t with
+// alpha = sm ||q|| sqrt(2 log(2S / delta) / 12) (Sec. 4.2, Tier B; the square root
+// hoisted out of the token loop, Sec. 6.2 serving integration) and beta =
+// sm ||q||_1 / 256, the mean of the 8-bit dither lattice's residual.
+__device__ __forceinline__ float tierb_factor(float q_sq, float q_l1, int n_tokens, float delta,
+                                             float sm_scale) {
+  const float lg = logf(2.0f * (float)n_tokens / delta);
+  return sm_scale * (sqrtf(q_sq) * sqrtf(2.0f * lg / 12.0f) + q_l1 * (1.0f / 256.0f));
+}
 
 // Clears the gate outputs of one (sequence, KV head) ahead of the merge.
 __device__ __forceinline__ void gate_clear(const DecodeArgs& a, int unit) {
