@@ -27,6 +27,7 @@ HBM_PEAK_GBPS = 8000.0       # MI355X HBM3E
 INT8_BYTES = 276             # per token-head at d=128, B=8: 128+128 codes, 2+2 scales, 16 witness
 FP8_BYTES = 272
 BF16_BYTES = 512
+TIERB_BYTES = 276 - 16       # the Tier-B certificate reads no witness
 WRITE_BYTES_BF16_IN = 512 + 276
 DECODE_KERNEL_SRC = os.path.join(ROOT, "paper_2607_28699_amd", "csrc")
 
@@ -292,7 +293,22 @@ def main():
     fb_ms = timed(lambda i: wc.exact_decode_attention(
         exact[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
         max_len_all, sm, mask_kv, out, ws=ws), reps)
+    # Tier-B certificate (Sec. 4.2) over the same caches: per-call time and, over
+    # every layer of the last step, its gate fractions (delta_req 1e-2 over
+    # layers x query heads x 256 steps)
+    dloc = wc.tierb_delta_loc(1e-2, wl.n_layers, wl.n_q, 256)
+    tb_ms = timed(lambda i: wc.tierb_decode_attention(
+        caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
+        max_len_all, sm, dloc, ws=ws, out=out, meter=meter, raw=raw), reps)
+    counts_b = torch.zeros(2, dtype=torch.int32, device=dev)
+    mq_b, mkv_b = torch.empty_like(mask_q), torch.empty_like(mask_kv)
+    for layer in range(wl.n_layers):
+        wc.tierb_decode_attention(caches[layer], last["layers"][layer]["q"], table, last["lens"],
+                                  max_len_all, sm, dloc, ws=ws, out=out, meter=meter, raw=raw)
+        wc.gate(meter, raw, wl.group, args.tau, n_gated=counts_b, mask_q=mq_b, mask_kv=mkv_b)
+    gqb, gkvb = counts_b.cpu().tolist()
     th_per_launch = float(last["tokens"] * wl.n_kv)
+    tb_gbps = th_per_launch * TIERB_BYTES / (float(np.median(tb_ms)) * 1e-3) / 1e9
     dec_gbps = th_per_launch * INT8_BYTES / (float(np.median(dec_ms)) * 1e-3) / 1e9
     routed = float(mask_kv.float().mean().item())
     fb_bytes = th_per_launch * routed * BF16_BYTES
@@ -338,6 +354,11 @@ def main():
                            "frac_hbm": round(fb_gbps / HBM_PEAK_GBPS, 4), "routed_kv_fraction": routed},
         "gate": {"tau": args.tau, "fraction_q_heads": round(frac_q, 4),
                  "fraction_kv_heads": round(frac_kv, 4)},
+        "tierb": {"median_launch_ms": round(float(np.median(tb_ms)), 4), "GBps": round(tb_gbps, 1),
+                  "frac_hbm": round(tb_gbps / HBM_PEAK_GBPS, 4), "bytes_per_token_head": TIERB_BYTES,
+                  "delta_req": 1e-2, "delta_loc": dloc,
+                  "gate_fraction_q_heads": round(gqb / (wl.n_layers * lay.batch * wl.n_q), 4),
+                  "gate_fraction_kv_heads": round(gkvb / (wl.n_layers * lay.batch * wl.n_kv), 4)},
         "quant_witness": {"GBps": round(write_gbps, 1), "frac_hbm": round(write_gbps / HBM_PEAK_GBPS, 4),
                           "bytes_per_token_head": WRITE_BYTES_BF16_IN,
                           "token_heads": write_tokens},

@@ -15,6 +15,7 @@ import pytest
 import synth
 from oracle import decode as odec
 from oracle import quantizer as oq
+from oracle import tierb
 
 from . import support as S
 
@@ -66,6 +67,7 @@ def _cell_check(wl, kv, q, b, h, layer):
     sm = 1 / np.sqrt(wl.d)
     res = odec.metered_decode(qb, kh[:, None], vh[:, None], kw[:, None], sm, wl.bands, wl.rope_layout)
     tv = odec.true_tv(qb, kb[:, None], kh[:, None], sm)
+    res["khat"], res["vhat"] = kh, vh
     return res, tv, kc, vc, ks
 
 
@@ -79,8 +81,11 @@ def test_fullsize_sampled_cells(name, n_lens):
     S.say(f"[fullsize] {name}")
     wl, lens0, cache, kv, q, tab, lens, max_len, layer = _setup(name, n_lens)
     out, meter, raw = wc.metered_decode_attention(cache, q, tab, lens, max_len, 1 / np.sqrt(wl.d))
+    dloc = wc.tierb_delta_loc(1e-2, wl.n_layers, wl.n_q, 256)
+    _, meter_b, raw_b = wc.tierb_decode_attention(cache, q, tab, lens, max_len, 1 / np.sqrt(wl.d), dloc)
     torch.cuda.synchronize()
     out, meter, raw = out.cpu().numpy(), meter.cpu().numpy(), raw.cpu().numpy()
+    meter_b, raw_b = meter_b.cpu().numpy(), raw_b.cpu().numpy()
     rng = np.random.default_rng(17)
     cells = [(int(rng.integers(len(lens0))), int(rng.integers(wl.n_q))) for _ in range(3)]
     for b, h in cells:
@@ -89,6 +94,11 @@ def test_fullsize_sampled_cells(name, n_lens):
         assert S.rel_err(out[b, h], res["out"][0]) <= 2e-3
         assert abs(raw[b, h] - res["raw"][0]) <= 2e-3 * res["raw"][0]
         assert meter[b, h] >= tv[0]
+        # the Tier-B certificate of the same cell (Sec. 4.2)
+        rb = tierb.tierb_decode(q[b, h:h + 1].float().cpu().numpy().astype(np.float64), res["khat"][:, None],
+                                res["vhat"][:, None], ks[:, None], 1 / np.sqrt(wl.d), dloc)
+        assert abs(raw_b[b, h] - rb["raw"][0]) <= 2e-3 * rb["raw"][0]
+        assert meter_b[b, h] >= tv[0]
         # codes of sampled tokens of this cell, bit-exact
         sl = kv[b][2]
         pick = rng.choice(len(sl), 512, replace=False)
