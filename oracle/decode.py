@@ -11,18 +11,21 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import attention, meter as mt, quantizer
+from . import attention, bypass, meter as mt, quantizer
+from .philox import dither_values
 
 KINDS = ("int8_dither", "fp8_raw", "bf16")
 
 
 def write_cache(kind: str, k: np.ndarray, v: np.ndarray, slots: np.ndarray, layer: int,
-                seed: int, n_bands: int, layout: str = "half") -> dict:
+                seed: int, n_bands: int, layout: str = "half", pairs=None) -> dict:
     """Quantize one sequence's tokens for every KV head.
 
     k, v: stored inputs [S, n_kv, d] (float); slots: int [S] physical slots.
+    pairs: int [n_kv, m] bypassed RoPE pairs of the keys (int8 only; ``bypass``).
     Returns reconstructions khat/vhat [S, n_kv, d], key witness kw [S, n_kv, B]
-    and, for int8, codes and scales.
+    and, for int8, codes and scales; with pairs also the stored fp16 values
+    ko [S, n_kv, 2m] and their channels chans [n_kv, 2m].
     """
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
@@ -34,8 +37,20 @@ def write_cache(kind: str, k: np.ndarray, v: np.ndarray, slots: np.ndarray, laye
             out[key] = np.empty((S, n_kv, d), dtype=np.int64)
         for key in ("ks", "vs"):
             out[key] = np.empty((S, n_kv))
+    if pairs is not None:
+        if kind != "int8_dither":
+            raise ValueError("the outlier bypass is defined for the int8 cache")
+        pairs = np.asarray(pairs, dtype=np.int64)
+        out["chans"] = np.stack([bypass.bypass_channels(pairs[h], d, layout) for h in range(n_kv)])
+        out["ko"] = np.empty((S, n_kv, out["chans"].shape[1]))
     for h in range(n_kv):
-        if kind == "int8_dither":
+        if kind == "int8_dither" and pairs is not None:
+            xi = dither_values(slots, d, layer, h, seed)
+            kc, ks, ko, kh = bypass.quantize_bypass(k[:, h], xi, out["chans"][h])
+            vc, vs, _, vh = quantizer.int8_quantize_slots(v[:, h], slots, layer, h, seed)
+            out["kcode"][:, h], out["ks"][:, h], out["ko"][:, h] = kc, ks, ko
+            out["vcode"][:, h], out["vs"][:, h] = vc, vs
+        elif kind == "int8_dither":
             kc, ks, _, kh = quantizer.int8_quantize_slots(k[:, h], slots, layer, h, seed)
             vc, vs, _, vh = quantizer.int8_quantize_slots(v[:, h], slots, layer, h, seed)
             out["kcode"][:, h], out["ks"][:, h] = kc, ks
