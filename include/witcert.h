@@ -9,6 +9,9 @@
  *   write path  wc_quantize_write   dithered INT8 (Sec. 4.2) or raw fp8 cast,
  *                                   plus the residual witness (Sec. 4.1, Eq. witness)
  *               wc_witness          witness of any cache-preserving scheme (Sec. 4.1)
+ *               wc_select_outlier_pairs
+ *                                   the fixed outlier RoPE pairs of each KV head that the
+ *                                   INT8 key cache keeps in fp16 (Sec. 4.2, Sec. 6.2)
  *   read path   wc_metered_decode_attention
  *                                   GQA decode attention over the compressed cache
  *                                   fused with the Tier-A meter (Theorem black-box
@@ -37,7 +40,10 @@
  *   - Preconditions not checked on the device: finite inputs, |x| <= 8.28e6
  *     (keeps fp16 scales finite), |x| <= 448 for the fp8 cache, |q| < 65504,
  *     block-table entries < num_blocks, slots < num_blocks * 16, every
- *     seq_lens[b] <= max_seq_len and <= max_blocks_per_seq * 16.
+ *     seq_lens[b] <= max_seq_len and <= max_blocks_per_seq * 16, outlier pair
+ *     lists ascending and distinct (out-of-range pair indices are clamped, so a
+ *     bad list gives wrong values, never a fault), |x| <= 65504 on bypassed
+ *     channels.
  */
 #ifndef WITCERT_H
 #define WITCERT_H
@@ -81,11 +87,23 @@ extern "C" {
  *   k_scale,
  *   v_scale    [num_blocks][n_kv_heads][16] fp16              INT8_DITHER only, else NULL
  *   k_witness  [num_blocks][n_kv_heads][16][n_bands] fp16     NULL for BF16
+ *   k_outlier  [num_blocks][n_kv_heads][16][2m] fp16          keys of the bypassed pairs
+ *              (m = n_outlier_pairs > 0 only, else NULL)
  * Element type of k_data/v_data: int8 code stored excess-128, i.e. the byte code + 128
  * (INT8_DITHER; codes lie in [-127, 127]), E4M3 byte (FP8_RAW), bf16 (BF16).
  * Band b holds the channels of RoPE pairs b*P .. b*P+P-1, P = head_dim/(2*n_bands)
  * (Sec. 4.1; Lemma RoPE band unitarity).  `seed` keys the Philox dither; `layer`
  * enters its counter (Sec. 6.2: counter (layer, kv_head, slot, channel)).
+ *
+ * Outlier-pair bypass (INT8_DITHER; Sec. 4.2 outlier RoPE pairs, Sec. 6.2
+ * fixed-channel bypass): a fixed set of m RoPE pairs per KV head,
+ * outlier_pairs[h][0..m-1] (ascending, distinct, < head_dim/2; see
+ * wc_select_outlier_pairs), is kept in fp16 instead of INT8: both channels of
+ * each pair leave the key's amax, their codes are 0, and their values, rounded to
+ * nearest fp16, are stored in k_outlier in the order (pair 0 first channel, pair 0
+ * second channel, pair 1 first, ...); the pair channels are (j, j + head_dim/2)
+ * for WC_ROPE_HALF and (2j, 2j + 1) for WC_ROPE_INTERLEAVED.  Values stay within
+ * +-65504.  Values are not bypassed.  m is even, 0 <= m <= 16.
  */
 typedef struct wc_cache {
     int32_t  kind;          /* WC_KIND_*                                       */
@@ -97,18 +115,38 @@ typedef struct wc_cache {
     int64_t  num_blocks;    /* pages of 16 slots                               */
     uint64_t seed;          /* Philox4x32-10 key (low word = key[0])           */
     void *k_data, *v_data, *k_scale, *v_scale, *k_witness;
+    int32_t  n_outlier_pairs;          /* m: bypassed RoPE pairs per KV head (0: none) */
+    int32_t  reserved;                 /* 0                                            */
+    const int32_t* outlier_pairs;      /* [n_kv_heads][m] device, or NULL when m == 0  */
+    void*    k_outlier;                /* see above, or NULL when m == 0               */
 } wc_cache;
 
 const char* wc_strerror(int status);
 int         wc_version(void);   /* 100*major + minor */
 
 /*
- * Bytes of each array of a cache (k_data, v_data, k_scale, v_scale, k_witness)
- * written to sizes[0..4]; returns their sum, 0 on bad arguments.  The "exact
- * byte account" of the cache (Sec. 5 memory saving; Sec. 6.2 acceptance).
+ * Bytes of each array of a cache (k_data, v_data, k_scale, v_scale, k_witness,
+ * k_outlier) written to sizes[0..5]; returns their sum, 0 on bad arguments.  The
+ * "exact byte account" of the cache (Sec. 5 memory saving; Sec. 6.2 acceptance;
+ * Table 6: 4m bytes per token and KV head for the bypassed pairs).
  */
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim,
-                      int n_bands, size_t sizes[5]);
+                      int n_bands, int n_outlier_pairs, size_t sizes[6]);
+
+/*
+ * Fixed outlier-pair set of each KV head (Sec. 6.2 fixed-channel bypass; Sec. 4.2
+ * pairs selected by energy): the m RoPE pairs j of largest energy
+ * E_j = sum_i ||(k_i)_pair j||^2 over the n_tok rows given (e.g. a prefill),
+ * ties to the lower j, written in ascending order to pairs_out[h][0..m-1].
+ * The energies are summed in float64.  RoPE does not change E_j, so the set is
+ * the same before and after the rotation.
+ *   k          [n_tok][n_kv_heads][head_dim], in_dtype WC_F32 or WC_BF16, n_tok >= 1
+ *   m          0 <= m <= head_dim/2 (m = 0 writes nothing)
+ *   pairs_out  [n_kv_heads][m] int32 device
+ */
+int wc_select_outlier_pairs(const void* k, int in_dtype, int64_t n_tok, int n_kv_heads,
+                            int head_dim, int rope_layout, int m, int32_t* pairs_out,
+                            void* stream);
 
 /*
  * Write path (Sec. 4.2 subtractive dither; Sec. 6.2 research kernels and storage
@@ -117,6 +155,8 @@ size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim
  *                xi_c = (u_c - 127.5)/256 with u_c the Philox4x32-10 byte of channel c
  *                (key = seed, counter = (c/16, slot lo, slot hi, layer<<16 | h)),
  *                shared by K and V; code = rint_even(fl32(fl32(x*fl32(1/s)) + xi));
+ *                with bypassed pairs (n_outlier_pairs > 0) the amax and the codes
+ *                skip their channels and k_outlier receives fp16(x) of them;
  *   FP8_RAW:     code = E4M3(x), nearest-even, saturating at +-448;
  *   BF16:        x rounded to bf16 (nearest-even);
  * and, except for BF16, the key witness w_b = ||(khat - k)_b|| rounded up to fp16
@@ -161,7 +201,8 @@ size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int he
  * Metered decode attention (the read path of the meter loop, Sec. 6).  For each
  * sequence b and query head h (KV head h / (n_q_heads / n_kv_heads)), over the
  * seq_lens[b] tokens whose slots are block_table[b][t/16]*16 + t%16:
- *   khat_t, vhat_t  reconstructions (INT8: s*(code - xi), xi regenerated from the slot)
+ *   khat_t, vhat_t  reconstructions (INT8: s*(code - xi), xi regenerated from the slot;
+ *                   the stored fp16 value on the channels of bypassed pairs)
  *   ptilde         = softmax(sm_scale * q . khat_t)
  *   out[b][h]      = sum_t ptilde_t vhat_t
  *   c_t            = sm_scale * sum_b ||q_b|| w_{t,b}      (Theorem black-box logit bound)
@@ -196,9 +237,12 @@ int wc_metered_decode_attention(const wc_cache* cache, const void* q, int q_dtyp
  *   alpha_h = sm_scale * ||q_h|| * sqrt(2 log(2 S_b / delta_loc) / 12),
  *   beta_h  = sm_scale * ||q_h||_1 / 256 (bound on the residual mean of the 8-bit
  *             dither lattice),
- * s_t the token's stored key scale and S_b = seq_lens[b]; A = sum_t ptilde_t e^{u_t},
- * raw = (A^2 - 1)/2, meter = min(1, raw).  No witness is read (k_witness may be
- * NULL).  With probability at least 1 - delta_loc (over the dither, for a query
+ * s_t the token's stored key scale and S_b = seq_lens[b].  With bypassed pairs,
+ * ||q_h|| and ||q_h||_1 are taken over the other channels and u_t gains the fp16
+ * rounding bound of the bypassed ones,
+ *   sm_scale * sum_{c bypassed} |q_c| (2^-11 |khat_{t,c}| + 2^-25).
+ * A = sum_t ptilde_t e^{u_t}, raw = (A^2 - 1)/2, meter = min(1, raw).  No witness
+ * is read (k_witness may be NULL).  With probability at least 1 - delta_loc (over the dither, for a query
  * that does not depend on it) raw bounds the TV of every query head of the call;
  * delta_loc in (0, 1) is the per-(layer, head, step) budget, e.g. delta_req /
  * (layers * query heads * steps).

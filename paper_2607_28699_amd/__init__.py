@@ -17,6 +17,7 @@ from .api import (  # noqa: F401
     metered_decode_gate,
     quantize_write,
     quantize_write_pair,
+    select_outlier_pairs,
     tierb_decode_attention,
     tierb_delta_loc,
     witness,

@@ -18,7 +18,7 @@ WC_BLOCK_TOKENS = 16
 
 EXPORTS = (
     "wc_strerror", "wc_version", "wc_cache_bytes", "wc_quantize_write", "wc_quantize_write_pair",
-    "wc_witness", "wc_decode_workspace_size", "wc_metered_decode_attention",
+    "wc_witness", "wc_select_outlier_pairs", "wc_decode_workspace_size", "wc_metered_decode_attention",
     "wc_metered_decode_gate", "wc_tierb_decode_attention", "wc_gate", "wc_exact_decode_attention",
 )
 
@@ -30,6 +30,8 @@ class WcCache(ctypes.Structure):
         ("num_blocks", ctypes.c_int64), ("seed", ctypes.c_uint64),
         ("k_data", ctypes.c_void_p), ("v_data", ctypes.c_void_p), ("k_scale", ctypes.c_void_p),
         ("v_scale", ctypes.c_void_p), ("k_witness", ctypes.c_void_p),
+        ("n_outlier_pairs", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("outlier_pairs", ctypes.c_void_p), ("k_outlier", ctypes.c_void_p),
     ]
 
 
@@ -56,7 +58,9 @@ def lib() -> ctypes.CDLL:
         "wc_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         "wc_version": (ctypes.c_int, []),
         "wc_cache_bytes": (sz, [ctypes.c_int, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-                                ctypes.POINTER(sz)]),
+                                ctypes.c_int, ctypes.POINTER(sz)]),
+        "wc_select_outlier_pairs": (ctypes.c_int, [vp, ctypes.c_int, i64, ctypes.c_int, ctypes.c_int,
+                                                   ctypes.c_int, ctypes.c_int, vp, vp]),
         "wc_quantize_write": (ctypes.c_int, [cp, vp, vp, ctypes.c_int, vp, i64, vp]),
         "wc_quantize_write_pair": (ctypes.c_int, [cp, cp, vp, vp, ctypes.c_int, vp, i64, vp]),
         "wc_witness": (ctypes.c_int, [vp, ctypes.c_int, vp, ctypes.c_int, i64, ctypes.c_int,

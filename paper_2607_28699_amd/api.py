@@ -41,9 +41,11 @@ def _dev_check(*ts):
             raise _lib.WitCertError("tensors must be contiguous device tensors")
 
 
-def cache_bytes(kind: str, num_blocks: int, n_kv: int, head_dim: int, n_bands: int):
-    sizes = (ctypes.c_size_t * 5)()
-    total = lib().wc_cache_bytes(KINDS[kind], num_blocks, n_kv, head_dim, n_bands, sizes)
+def cache_bytes(kind: str, num_blocks: int, n_kv: int, head_dim: int, n_bands: int,
+                n_outlier_pairs: int = 0):
+    sizes = (ctypes.c_size_t * 6)()
+    total = lib().wc_cache_bytes(KINDS[kind], num_blocks, n_kv, head_dim, n_bands, n_outlier_pairs,
+                                 sizes)
     if total == 0:
         raise _lib.WitCertError("bad cache geometry")
     return total, list(sizes)
@@ -61,11 +63,13 @@ class PagedCache:
     seed: int = 0
     rope_layout: str = "half"
     device: str = "cuda"
+    n_outlier_pairs: int = 0
     tensors: dict = field(default_factory=dict)
 
     def __post_init__(self):
-        total, sizes = cache_bytes(self.kind, self.num_blocks, self.n_kv, self.head_dim, self.n_bands)
-        names = ("k_data", "v_data", "k_scale", "v_scale", "k_witness")
+        m = self.n_outlier_pairs
+        total, sizes = cache_bytes(self.kind, self.num_blocks, self.n_kv, self.head_dim, self.n_bands, m)
+        names = ("k_data", "v_data", "k_scale", "v_scale", "k_witness", "k_outlier")
         slots = self.num_blocks * WC_BLOCK_TOKENS * self.n_kv
         shapes = {
             "k_data": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.head_dim),
@@ -73,6 +77,7 @@ class PagedCache:
             "k_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
             "v_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
             "k_witness": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.n_bands),
+            "k_outlier": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, 2 * m),
         }
         # int8 codes are stored excess-128 (byte = code + 128)
         el = {"int8_dither": torch.uint8, "fp8_raw": torch.uint8, "bf16": torch.bfloat16}[self.kind]
@@ -85,13 +90,24 @@ class PagedCache:
             assert t.numel() * t.element_size() == s, (n, s, slots)
             self.tensors[n] = t
         self.total_bytes = total
+        # bypassed RoPE pairs per KV head (set with set_outlier_pairs before writing)
+        self.tensors["outlier_pairs"] = (
+            torch.arange(m, dtype=torch.int32, device=self.device).repeat(self.n_kv, 1) if m else None)
+
+    def set_outlier_pairs(self, pairs: torch.Tensor) -> None:
+        """pairs [n_kv, m] int32, ascending per row (e.g. from select_outlier_pairs)."""
+        t = self.tensors["outlier_pairs"]
+        if t is None or tuple(pairs.shape) != tuple(t.shape):
+            raise _lib.WitCertError("outlier pairs do not match the cache")
+        t.copy_(pairs.to(device=t.device, dtype=torch.int32))
 
     def struct(self) -> WcCache:
         t = self.tensors
         return WcCache(KINDS[self.kind], self.head_dim, self.n_kv, self.n_bands,
                        LAYOUTS[self.rope_layout], self.layer, self.num_blocks, self.seed,
                        _ptr(t["k_data"]), _ptr(t["v_data"]), _ptr(t["k_scale"]),
-                       _ptr(t["v_scale"]), _ptr(t["k_witness"]))
+                       _ptr(t["v_scale"]), _ptr(t["k_witness"]), self.n_outlier_pairs, 0,
+                       _ptr(t["outlier_pairs"]), _ptr(t["k_outlier"]))
 
 
 def quantize_write(cache: PagedCache, k: torch.Tensor, v: torch.Tensor, slots: torch.Tensor) -> None:
@@ -111,6 +127,19 @@ def quantize_write_pair(cache: PagedCache, exact: PagedCache, k: torch.Tensor, v
     c, e = cache.struct(), exact.struct()
     check(lib().wc_quantize_write_pair(ctypes.byref(c), ctypes.byref(e), _ptr(k), _ptr(v), _dt(k),
                                        _ptr(slots), k.shape[0], _stream()), "wc_quantize_write_pair")
+
+
+def select_outlier_pairs(k: torch.Tensor, m: int, rope_layout: str = "half",
+                         out: torch.Tensor | None = None) -> torch.Tensor:
+    """The m RoPE pairs of largest energy of each KV head over the rows of
+    k [n_tok, n_kv, d] -> int32 [n_kv, m], ascending."""
+    _dev_check(k)
+    n_tok, n_kv, d = k.shape
+    if out is None:
+        out = torch.empty((n_kv, m), dtype=torch.int32, device=k.device)
+    check(lib().wc_select_outlier_pairs(_ptr(k), _dt(k), n_tok, n_kv, d, LAYOUTS[rope_layout], m,
+                                        _ptr(out), _stream()), "wc_select_outlier_pairs")
+    return out
 
 
 def witness(x: torch.Tensor, xhat: torch.Tensor, n_bands: int, rope_layout: str = "half",

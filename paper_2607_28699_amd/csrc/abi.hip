@@ -30,6 +30,12 @@ int check_cache(const wc_cache* c, bool need_witness, bool witness_optional = fa
   if (c->kind == WC_KIND_INT8_DITHER &&
       (!c->k_scale || !c->v_scale || !aligned16(c->k_scale) || !aligned16(c->v_scale)))
     return WC_EINVAL;
+  if (c->n_outlier_pairs != 0) {   // bypassed pairs: INT8 keys only, m even, <= 16
+    const int m = c->n_outlier_pairs;
+    if (c->kind != WC_KIND_INT8_DITHER || m < 0 || m > 16 || (m & 1) || m > c->head_dim / 2)
+      return WC_EINVAL;
+    if (!c->outlier_pairs || !c->k_outlier || !aligned16(c->k_outlier)) return WC_EINVAL;
+  }
   return WC_OK;
 }
 
@@ -53,17 +59,21 @@ const char* wc_strerror(int status) {
 int wc_version(void) { return 100; }
 
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim, int n_bands,
-                      size_t sizes[5]) {
+                      int n_outlier_pairs, size_t sizes[6]) {
   if (kind < WC_KIND_INT8_DITHER || kind > WC_KIND_BF16 || num_blocks < 0 || n_kv_heads < 1 ||
       head_dim < 1 || (kind != WC_KIND_BF16 && n_bands < 1))
     return 0;
+  if (n_outlier_pairs < 0 || n_outlier_pairs > 16 || (n_outlier_pairs & 1) ||
+      2 * n_outlier_pairs > head_dim || (n_outlier_pairs && kind != WC_KIND_INT8_DITHER))
+    return 0;
   const size_t slots = (size_t)num_blocks * WC_BLOCK_TOKENS * (size_t)n_kv_heads;
-  size_t s[5];
+  size_t s[6];
   s[0] = s[1] = slots * head_dim * elem_bytes(kind);
   s[2] = s[3] = kind == WC_KIND_INT8_DITHER ? slots * 2 : 0;
   s[4] = kind == WC_KIND_BF16 ? 0 : slots * n_bands * 2;
+  s[5] = slots * (size_t)n_outlier_pairs * 4;   // 2m fp16 values per token-head
   if (sizes) memcpy(sizes, s, sizeof(s));
-  return s[0] + s[1] + s[2] + s[3] + s[4];
+  return s[0] + s[1] + s[2] + s[3] + s[4] + s[5];
 }
 
 static int write_common(const wc_cache* cache, const wc_cache* exact, const void* k, const void* v,
@@ -102,6 +112,9 @@ static int write_common(const wc_cache* cache, const wc_cache* exact, const void
   a.k_witness = static_cast<uint16_t*>(cache->k_witness);
   a.x_k_data = exact ? exact->k_data : nullptr;
   a.x_v_data = exact ? exact->v_data : nullptr;
+  a.n_pairs = cache->n_outlier_pairs;
+  a.pairs = cache->outlier_pairs;
+  a.k_outlier = static_cast<uint16_t*>(cache->k_outlier);
   return hip_status(wc::launch_quantize_write(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -128,6 +141,21 @@ int wc_witness(const void* x, int x_dtype, const void* xhat, int xhat_dtype, int
   wc::WitnessArgs a{x, xhat, x_dtype, xhat_dtype, head_dim, n_bands,
                     rope_layout == WC_ROPE_INTERLEAVED, n_vec, w_out};
   return hip_status(wc::launch_witness(a, static_cast<hipStream_t>(stream)));
+}
+
+int wc_select_outlier_pairs(const void* k, int in_dtype, int64_t n_tok, int n_kv_heads,
+                            int head_dim, int rope_layout, int m, int32_t* pairs_out,
+                            void* stream) {
+  if (n_tok < 1 || n_kv_heads < 1 || n_kv_heads > 65535 || (in_dtype != WC_F32 && in_dtype != WC_BF16))
+    return WC_EINVAL;
+  if (head_dim != 64 && head_dim != 128) return WC_EUNSUPPORTED;
+  if (rope_layout != WC_ROPE_HALF && rope_layout != WC_ROPE_INTERLEAVED) return WC_EINVAL;
+  if (m < 0 || m > head_dim / 2) return WC_EINVAL;
+  if (m == 0) return WC_OK;
+  if (!k || !pairs_out || !aligned16(k)) return WC_EINVAL;
+  wc::SelectArgs a{k, in_dtype, n_kv_heads, head_dim, rope_layout == WC_ROPE_INTERLEAVED, m, n_tok,
+                   pairs_out};
+  return hip_status(wc::launch_select_pairs(a, static_cast<hipStream_t>(stream)));
 }
 
 size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
@@ -191,6 +219,9 @@ static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int 
   a.key0 = (uint32_t)cache->seed;
   a.key1 = (uint32_t)(cache->seed >> 32);
   a.sm_scale = sm_scale;
+  a.n_pairs = cache->n_outlier_pairs;
+  a.pairs = cache->outlier_pairs;
+  a.k_outlier = static_cast<const uint16_t*>(cache->k_outlier);
   // WITCERT_FORCE_VALU=1 selects the vector-ALU kernels even where the
   // matrix-core ones apply (used to cross-check the two paths)
   const char* force = getenv("WITCERT_FORCE_VALU");

@@ -106,6 +106,7 @@ struct PageRegs {
   uint32_t vw[NW];   // values of channels 8r..8r+7 for token quad g
   uint2 ks, vs;      // fp16 scales of tokens 4g..4g+3
   uint4 wit;         // witness bands 8(g%2).. of token r (garbage where 8(g%2) >= n_bands)
+  uint4 ov;          // fp16 keys of bypassed pairs: values 8g .. 8g+7 of token r (when 8g < 2m)
   int blk;           // cache block of the page (wave-uniform)
 };
 
@@ -123,7 +124,7 @@ __device__ __forceinline__ uint2 bload8(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
 
-template <int KIND, bool METER, bool TB>
+template <int KIND, bool METER, bool TB, bool BYP>
 __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool valid, int kv, int r,
                                           int g, int wit_off, PageRegs<KIND>& p) {
   constexpr int KB = KIND == WC_KIND_BF16 ? 64 : 32;   // bytes per lane and tensor
@@ -149,6 +150,13 @@ __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool val
     const int wb = valid ? 2 * kBlockTokens * a.n_bands : 0;
     p.wit = bload16(page_rsrc(a.k_witness + page * kBlockTokens * a.n_bands, wb), wit_off);
   }
+  if constexpr (BYP) {
+    // rows of 4m bytes; a lane past its row's values reads the next row (or, at the
+    // page end, zeros from the resource bound) and masks them in process_page
+    const int ob = 4 * a.n_pairs * kBlockTokens;
+    p.ov = bload16(page_rsrc(a.k_outlier + page * (2 * a.n_pairs * kBlockTokens), valid ? ob : 0),
+                   r * 4 * a.n_pairs + 16 * g);
+  }
 }
 
 // Running state of one wave.  Logits are kept in log2 units; every weight carries
@@ -167,8 +175,13 @@ struct WaveConst {
   float s1_init;   // 2303 sum(q) / 512: the dither offset, preloaded into the code accumulator
   float lmul;      // logit multiplier: sm_scale * log2(e) (times 256 for fp8 operands)
   float ab2;       // Tier B: (alpha_h + beta_h) * log2(e)
+  h8_t qo;         // bypassed pairs: fp16 queries at the stored values 8g .. 8g+7
+  h8_t qa;         // their magnitudes (Tier B rounding term)
+  float gmul;      // Tier B: sm_scale * 2^-11 * log2(e)
+  float gc;        // Tier B: sm_scale * 2^-25 * log2(e) * sum |q_c| over the bypassed channels
   uint32_t layer_head;
   bool wit_ok;
+  bool ov_lo, ov_hi;   // this lane's stored values 8g..8g+3, 8g+4..8g+7 exist (< 2m)
 };
 
 constexpr float kLog2e = 1.4426950408889634f;
@@ -204,7 +217,7 @@ __device__ __forceinline__ uint32_t dpp_from_upper8(uint32_t v) {
 }
 
 // One 16-token page.  FULL: every token of the page is below t_end (no masking).
-template <int KIND, bool METER, bool FULL, bool HALF, bool TB>
+template <int KIND, bool METER, bool FULL, bool HALF, bool TB, bool BYP>
 __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs<KIND>& cur, int t0,
                                              int t_end, int r, int g, const WaveConst& wc,
                                              uint8_t* my_dsh, WaveState& st) {
@@ -259,6 +272,20 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     const uint4 w = wc.wit_ok ? cur.wit : make_uint4(0, 0, 0, 0);
     cb = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, w), wc.qnop, cb, 0, 0, 0);
   }
+  // bypassed pairs (Sec. 6.2): q . khat over their channels from the stored fp16
+  // values (the query operand of the code products is zero there), and for Tier B
+  // sum |q_c| |khat_c| for the fp16 rounding bound
+  f4_t so = z4, go = z4;
+  if constexpr (BYP) {
+    const uint32_t o0 = wc.ov_lo ? cur.ov.x : 0u, o1 = wc.ov_lo ? cur.ov.y : 0u;
+    const uint32_t o2 = wc.ov_hi ? cur.ov.z : 0u, o3 = wc.ov_hi ? cur.ov.w : 0u;
+    so = __builtin_amdgcn_mfma_f32_16x16x32_f16(pack8(o0, o1, o2, o3), wc.qo, so, 0, 0, 0);
+    if constexpr (TB) {
+      constexpr uint32_t kAbs = 0x7FFF7FFFu;
+      go = __builtin_amdgcn_mfma_f32_16x16x32_f16(pack8(o0 & kAbs, o1 & kAbs, o2 & kAbs, o3 & kAbs),
+                                                  wc.qa, go, 0, 0, 0);
+    }
+  }
 
   // ---------------- online softmax and meter numerator ----------------
   // Lane (r, g) holds head r, tokens t0 + 4g + e.  HALF (at most 8 heads per KV
@@ -268,12 +295,14 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   constexpr int NT = HALF ? 2 : 4;
   const bool upper = HALF && r >= 8;
   const int tok0 = 4 * g + (upper ? 2 : 0);            // first token of this lane
-  float scv[4], cbv[4];
+  float scv[4], cbv[4], sov[4], gov[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     scv[e] = s1[e];
     if constexpr (KIND == WC_KIND_INT8_DITHER) scv[e] = fmaf(s2[e], -0.001953125f, scv[e]);   // q . (code + xi)
     cbv[e] = cb[e];
+    sov[e] = so[e];
+    gov[e] = go[e];
   }
   uint32_t ksw0 = cur.ks.x, ksw1 = cur.ks.y, vsw0 = cur.vs.x, vsw1 = cur.vs.y;
   if constexpr (HALF) {
@@ -282,6 +311,14 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     if constexpr (METER && !TB) {
       cbv[0] = dpp_from_lower8(cbv[0], cbv[2]);
       cbv[1] = dpp_from_lower8(cbv[1], cbv[3]);
+    }
+    if constexpr (BYP) {
+      sov[0] = dpp_from_lower8(sov[0], sov[2]);
+      sov[1] = dpp_from_lower8(sov[1], sov[3]);
+      if constexpr (TB) {
+        gov[0] = dpp_from_lower8(gov[0], gov[2]);
+        gov[1] = dpp_from_lower8(gov[1], gov[3]);
+      }
     }
     if constexpr (KIND == WC_KIND_INT8_DITHER) {
       ksw0 = upper ? cur.ks.y : cur.ks.x;
@@ -294,7 +331,8 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     // Tier B (Sec. 4.2): the radius u_t = (alpha_h + beta_h) s_t from the stored
     // key scale of each of this lane's tokens, in log2 units
 #pragma unroll
-    for (int e = 0; e < NT; ++e) cbv[e] = fmaf((float)ksh[e >> 1][e & 1], wc.ab2, 0.0f);
+    for (int e = 0; e < NT; ++e)
+      cbv[e] = fmaf((float)ksh[e >> 1][e & 1], wc.ab2, BYP ? fmaf(gov[e], wc.gmul, wc.gc) : 0.0f);
   }
   bool valid[NT];
   float lg[NT];
@@ -305,7 +343,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     float sc = scv[e];
     if constexpr (KIND == WC_KIND_INT8_DITHER) {
       // (fma with a +0 addend keeps the fp16 operand inside one mixed-precision fma)
-      sc = fmaf((float)ksh[e >> 1][e & 1], sc, 0.0f) * wc.lmul;
+      sc = fmaf((float)ksh[e >> 1][e & 1], sc, BYP ? sov[e] : 0.0f) * wc.lmul;
     } else {
       sc = sc * wc.lmul;
     }
@@ -422,7 +460,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   }
 }
 
-template <int KIND, bool METER, bool HALF, bool TB>
+template <int KIND, bool METER, bool HALF, bool TB, bool BYP>
 __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
   __shared__ float qn_s[kWaves][16][16];
@@ -492,14 +530,68 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     nc = min(64, np - c0);
     if (c0 == 0 && pg0 == pg_spec && nc <= nc_spec) tv = tv_spec;   // the early request holds them
     else tv = lane < nc ? trow[pg0 + c0 + lane] : 0;
-    load_page<KIND, METER, TB>(a, blk_at(0), true, kv, r, g, wit_off, p0);
+    load_page<KIND, METER, TB, BYP>(a, blk_at(0), true, kv, r, g, wit_off, p0);
     __builtin_amdgcn_sched_barrier(0);
-    load_page<KIND, METER, TB>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
+    load_page<KIND, METER, TB, BYP>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
     __builtin_amdgcn_sched_barrier(0);
   };
   if (np > 0) start_chunk(0);
 
   WaveConst wc;
+  // Bypassed pairs (Sec. 6.2 fixed-channel bypass): the query channels of this
+  // lane that are bypassed leave the code products (qk); their keys come from the
+  // stored fp16 values through wc.qo.  Tier A's band norms keep the whole query.
+  uint32_t qk[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) qk[i] = qraw[i];
+  wc.gmul = wc.gc = 0.0f;
+  wc.ov_lo = wc.ov_hi = false;
+  if constexpr (BYP) {
+    const int m = a.n_pairs;
+    const int32_t* pl = a.pairs + (int64_t)kv * m;
+    uint32_t mw = 0;   // bypassed channels among 32g .. 32g+31
+    for (int i = 0; i < m; ++i) {
+      const int j = pl[i];
+#pragma unroll
+      for (int sec = 0; sec < 2; ++sec) {
+        const int c = pair_channel(j, sec, kD, a.interleaved) - 32 * g;
+        if ((unsigned)c < 32u) mw |= 1u << c;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      qk[i] &= (((mw >> (2 * i)) & 1u) ? 0u : 0xFFFFu) | (((mw >> (2 * i + 1)) & 1u) ? 0u : 0xFFFF0000u);
+    const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.q) +
+                           ((int64_t)b * a.n_q + (int64_t)kv * G + (hv ? r : 0)) * kD;
+    uint32_t qw[4], qaw[4];
+    float asum = 0.0f;
+#pragma unroll
+    for (int e2 = 0; e2 < 4; ++e2) {
+      uint32_t w = 0;
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int pos = 8 * g + 2 * e2 + h2;   // stored value pos: pair pos/2, channel pos%2
+        if (pos < 2 * m) {
+          const _Float16 hx = (_Float16)bf16_to_f32(qrow[pair_channel(pl[pos >> 1], pos & 1, kD, a.interleaved)]);
+          w |= (uint32_t)f16_bits(hx) << (16 * h2);
+          asum += fabsf((float)hx);
+        }
+      }
+      qw[e2] = w;
+      qaw[e2] = w & 0x7FFF7FFFu;
+    }
+    wc.qo = pack8(qw[0], qw[1], qw[2], qw[3]);
+    wc.qa = pack8(qaw[0], qaw[1], qaw[2], qaw[3]);
+    wc.ov_lo = 8 * g < 2 * m;
+    wc.ov_hi = 8 * g + 4 < 2 * m;
+    if constexpr (TB) {
+      asum += __shfl_xor(asum, 16, 64);
+      asum += __shfl_xor(asum, 32, 64);
+      wc.gmul = a.sm_scale * 0x1p-11f * kLog2e;
+      wc.gc = a.sm_scale * 0x1p-25f * kLog2e * asum;
+      if constexpr (HALF) wc.gc = dpp_from_lower8(wc.gc, wc.gc);
+    }
+  }
   wc.layer_head = ((uint32_t)a.layer << 16) | (uint32_t)kv;
   wc.wit_ok = 8 * (g & 1) < B;
   wc.lmul = a.sm_scale * kLog2e * (KIND == WC_KIND_FP8_RAW ? 256.0f : 1.0f);
@@ -514,7 +606,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       uint32_t w[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        w[j] = bf16pair_to_f16(qraw[4 * kt + j]);
+        w[j] = bf16pair_to_f16(qk[4 * kt + j]);
         const h2_t h = as_h2(w[j]);
         qsum += (float)h[0] + (float)h[1];
       }
@@ -529,10 +621,10 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   wc.qnop = pack8(0, 0, 0, 0);
   wc.ab2 = 0.0f;
   if constexpr (TB) {
-    float sq = 0.0f, l1 = 0.0f;   // ||q||^2 and ||q||_1 of head r
+    float sq = 0.0f, l1 = 0.0f;   // ||q||^2 and ||q||_1 of head r (channels not bypassed)
 #pragma unroll
     for (int i = 0; i < 32; ++i) {
-      const float x = bf16_to_f32((uint16_t)((qraw[i >> 1] >> (16 * (i & 1))) & 0xFFFFu));
+      const float x = bf16_to_f32((uint16_t)((qk[i >> 1] >> (16 * (i & 1))) & 0xFFFFu));
       sq = fmaf(x, x, sq);
       l1 += fabsf(x);
     }
@@ -624,17 +716,17 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     // assume the ring order may differ on the back edge and wait for every page.
     for (int j = 0; j < nc; j += 3) {
       set_priority(c0 + j);
-      load_page<KIND, METER, TB>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
+      load_page<KIND, METER, TB, BYP>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
       __builtin_amdgcn_sched_barrier(0);
-      process_page<KIND, METER, true, HALF, TB>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
-      load_page<KIND, METER, TB>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
+      process_page<KIND, METER, true, HALF, TB, BYP>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      load_page<KIND, METER, TB, BYP>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 1 < nc)
-        process_page<KIND, METER, true, HALF, TB>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
-      load_page<KIND, METER, TB>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
+        process_page<KIND, METER, true, HALF, TB, BYP>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      load_page<KIND, METER, TB, BYP>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 2 < nc)
-        process_page<KIND, METER, true, HALF, TB>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+        process_page<KIND, METER, true, HALF, TB, BYP>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
     }
     c0 += 64;
     if (c0 < np) start_chunk(c0);
@@ -642,8 +734,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __builtin_amdgcn_s_setprio(0);
   const int t_last = t_begin + np * kBlockTokens;
   if (t_last < t_end) {   // a partial last page: tokens from t_end on are masked
-    load_page<KIND, METER, TB>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
-    process_page<KIND, METER, false, HALF, TB>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
+    load_page<KIND, METER, TB, BYP>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
+    process_page<KIND, METER, false, HALF, TB, BYP>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
   }
 
   // ---- merge the four waves of the workgroup, write one partial record ----
@@ -729,29 +821,30 @@ bool mfma_decode_supported(const DecodeArgs& a) {
          (a.kind == WC_KIND_BF16 || a.n_bands == 8 || a.n_bands == 16);
 }
 
+template <bool HALF>
+void launch_decode_mfma_g(const DecodeArgs& a, bool metered, bool tb, bool byp, const dim3& grid,
+                          const dim3& block, hipStream_t st) {
+  if (!metered)
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, HALF, false, false>), grid, block, 0, st, a);
+  else if (a.kind == WC_KIND_FP8_RAW)
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, HALF, false, false>), grid, block, 0, st, a);
+  else if (tb && byp)
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, true>), grid, block, 0, st, a);
+  else if (tb)
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, false>), grid, block, 0, st, a);
+  else if (byp)
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, true>), grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, false>), grid, block, 0, st, a);
+}
+
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st) {
   const dim3 grid(a.n_splits, a.batch * a.n_kv);
   const dim3 block(64 * kWaves);
   const bool tb = metered && a.tierb_delta > 0.0f;   // Tier B: INT8 dithered cache only
-  if (a.group <= 8) {
-    if (!metered)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, true, false>), grid, block, 0, st, a);
-    else if (tb)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, true, true>), grid, block, 0, st, a);
-    else if (a.kind == WC_KIND_INT8_DITHER)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, true, false>), grid, block, 0, st, a);
-    else
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, true, false>), grid, block, 0, st, a);
-  } else {
-    if (!metered)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, false, false>), grid, block, 0, st, a);
-    else if (tb)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, false, true>), grid, block, 0, st, a);
-    else if (a.kind == WC_KIND_INT8_DITHER)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, false, false>), grid, block, 0, st, a);
-    else
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, false, false>), grid, block, 0, st, a);
-  }
+  const bool byp = metered && a.n_pairs > 0;        // bypassed pairs: INT8 keys only
+  if (a.group <= 8) launch_decode_mfma_g<true>(a, metered, tb, byp, grid, block, st);
+  else launch_decode_mfma_g<false>(a, metered, tb, byp, grid, block, st);
   return hipGetLastError();
 }
 

@@ -40,6 +40,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   __shared__ float q_s[kGMax][D];
   __shared__ float qbn_s[kGMax][16];
   __shared__ float ab_s[kGMax];       // Tier-B factor per head
+  __shared__ float qo_s[kGMax][32];   // bypassed pairs: q at the stored values' channels
   __shared__ float logit_s[kGMax][kT];
   __shared__ float cb_s[kGMax][kT];
   __shared__ float pw_s[kGMax][kT];
@@ -70,6 +71,11 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
                              : bf16_to_f32(reinterpret_cast<const uint16_t*>(a.q)[qi]);
   }
   __syncthreads();
+  // Bypassed pairs (Sec. 6.2 fixed-channel bypass): q at the channels of the
+  // stored fp16 values goes to qo_s and leaves q_s, so the code products skip
+  // those channels; Tier A's band norms are taken from the whole query first.
+  const int m2 = 2 * a.n_pairs;
+  const int32_t* plist = a.pairs + (int64_t)kv * a.n_pairs;
   if constexpr (METER) {
     for (int i = tid; i < G * B; i += kThreads) {
       const int h = i / B, bb = i % B;
@@ -80,6 +86,20 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
       }
       qbn_s[h][bb] = sqrtf(acc) * a.sm_scale;
     }
+  }
+  if (m2 > 0) {
+    for (int i = tid; i < G * m2; i += kThreads) {
+      const int h = i / m2, pos = i % m2;
+      qo_s[h][pos] = q_s[h][pair_channel(plist[pos >> 1], pos & 1, D, a.interleaved)];
+    }
+    __syncthreads();
+    for (int i = tid; i < G * m2; i += kThreads) {
+      const int h = i / m2, pos = i % m2;
+      q_s[h][pair_channel(plist[pos >> 1], pos & 1, D, a.interleaved)] = 0.0f;
+    }
+    __syncthreads();
+  }
+  if constexpr (METER) {
     if (a.tierb_delta > 0.0f) {
       for (int h = tid; h < G; h += kThreads) {
         float sq = 0.0f, l1 = 0.0f;
@@ -177,18 +197,37 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
       } else if (part == 0) {
         vs_s[i] = 0.0f;
       }
+      // stored fp16 values of the bypassed pairs: positions part, part + 4, ...
+      float kov[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int pos = part + 4 * k;
+        kov[k] = (valid && pos < m2) ? f16_to_f32(a.k_outlier[(page * kBlockTokens + off) * m2 + pos]) : 0.0f;
+      }
       for (int h = 0; h < G; ++h) {
         float d = 0.0f;
 #pragma unroll
         for (int c = 0; c < CH; ++c) d = fmaf(q_s[h][c0 + c], kval[c], d);
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (part + 4 * k < m2) d = fmaf(qo_s[h][part + 4 * k], kov[k], d);
         d += __shfl_xor(d, 1, 4);
         d += __shfl_xor(d, 2, 4);
         if (part == 0) logit_s[h][i] = valid ? d * a.sm_scale : -INFINITY;
       }
       if (METER && a.tierb_delta > 0.0f) {   // Tier B: u_t = (alpha_h + beta_h) s_t, no witness
         const float s = valid ? f16_to_f32(a.k_scale[page * kBlockTokens + off]) : 0.0f;
-        if (part == 0)
-          for (int h = 0; h < G; ++h) cb_s[h][i] = ab_s[h] * s;
+        for (int h = 0; h < G; ++h) {
+          // fp16 rounding bound of the bypassed channels: sm sum |q_c| (2^-11 |khat_c| + 2^-25)
+          float gb = 0.0f;
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            if (part + 4 * k < m2)
+              gb = fmaf(fabsf(qo_s[h][part + 4 * k]), fmaf(fabsf(kov[k]), 0x1p-11f, 0x1p-25f), gb);
+          gb += __shfl_xor(gb, 1, 4);
+          gb += __shfl_xor(gb, 2, 4);
+          if (part == 0) cb_s[h][i] = fmaf(ab_s[h], s, gb * a.sm_scale);
+        }
       } else if constexpr (METER) {
         float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
         if (valid) {

@@ -22,6 +22,16 @@ struct WriteArgs {
   uint16_t* k_witness;
   void* x_k_data;           // bf16 exact cache written in the same pass (or null)
   void* x_v_data;
+  int n_pairs;              // bypassed RoPE pairs per KV head (0: none)
+  const int32_t* pairs;     // [n_kv][n_pairs]
+  uint16_t* k_outlier;      // [blocks][n_kv][16][2 n_pairs] fp16
+};
+
+struct SelectArgs {
+  const void* k;
+  int in_dtype, n_kv, head_dim, interleaved, m;
+  int64_t n_tok;
+  int32_t* pairs_out;
 };
 
 struct WitnessArgs {
@@ -60,7 +70,16 @@ struct DecodeArgs {
   int32_t* gate_unit;       // [batch][n_kv] gated-head counts (workspace), cleared likewise
   int32_t* gate_count;      // device int32[2] or null
   float gate_tau;
+  int n_pairs;              // bypassed RoPE pairs per KV head (0: none)
+  const int32_t* pairs;     // [n_kv][n_pairs]
+  const uint16_t* k_outlier;  // [blocks][n_kv][16][2 n_pairs] fp16
 };
+
+// Channel of member `second` of RoPE pair j (pair index clamped into range).
+__host__ __device__ inline int pair_channel(int j, int second, int d, bool interleaved) {
+  j = j < 0 ? 0 : (j >= d / 2 ? d / 2 - 1 : j);
+  return interleaved ? 2 * j + second : j + second * (d / 2);
+}
 
 // Tier-B factor (alpha + beta) of one query head: u_t = (alpha + beta) * s_t with
 // alpha = sm ||q|| sqrt(2 log(2S / delta) / 12) (Sec. 4.2, Tier B; the square root
@@ -108,6 +127,7 @@ inline size_t gate_unit_bytes(int batch, int n_kv) {
 
 hipError_t launch_quantize_write(const WriteArgs& a, hipStream_t st);
 hipError_t launch_witness(const WitnessArgs& a, hipStream_t st);
+hipError_t launch_select_pairs(const SelectArgs& a, hipStream_t st);
 hipError_t launch_decode(const DecodeArgs& a, bool metered, hipStream_t st);
 bool mfma_decode_supported(const DecodeArgs& a);
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st);

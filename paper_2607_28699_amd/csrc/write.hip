@@ -103,10 +103,22 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
   if (g == 0) slot_s[lth] = slot;
 
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
+    // Bypassed key channels of this lane (outlier RoPE pairs, Sec. 6.2): out of the
+    // amax, code 0, value kept in fp16 (bit i: channel 16g + i).
+    uint32_t bmask = 0;
+    const int32_t* plist = a.pairs + (int64_t)h * a.n_pairs;
+    for (int i = 0; i < a.n_pairs; ++i) {
+      const int j = plist[i];
+#pragma unroll
+      for (int sec = 0; sec < 2; ++sec) {
+        const int c = pair_channel(j, sec, D, a.interleaved) - 16 * g;
+        if (c >= 0 && c < 16) bmask |= 1u << c;
+      }
+    }
     float ak = 0.0f, av = 0.0f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      ak = fmaxf(ak, fabsf(k[i]));
+      if (((bmask >> i) & 1u) == 0) ak = fmaxf(ak, fabsf(k[i]));
       av = fmaxf(av, fabsf(v[i]));
     }
 #pragma unroll
@@ -124,10 +136,13 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
     uint32_t kc[4] = {0, 0, 0, 0};
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
+      const bool byp = (bmask >> i) & 1u;
       const float xi = dither_value((words[i >> 2] >> (8 * (i & 3))) & 0xFFu);
-      const float ck = rintf(__fadd_rn(__fmul_rn(k[i], ikk), xi));
+      // a bypassed channel quantizes 0 (|xi| < 1/2, so its code is 0)
+      const float ck = rintf(__fadd_rn(__fmul_rn(byp ? 0.0f : k[i], ikk), xi));
       const float cv = rintf(__fadd_rn(__fmul_rn(v[i], ivv), xi));
-      const double rk = (double)sk * (double)(ck - xi) - (double)k[i];   // khat - k
+      const double rk = byp ? (double)(float)(_Float16)k[i] - (double)k[i]     // fp16(k) - k
+                            : (double)sk * (double)(ck - xi) - (double)k[i];   // khat - k
       r2[lth][16 * g + i] = rk * rk;
       // codes are stored excess-128: byte = code + 128
       kc[i >> 2] |= ((uint32_t)((int32_t)ck + 128) & 0xFFu) << (8 * (i & 3));
@@ -144,6 +159,23 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
       if (g == 0) {
         a.k_scale[bh * kBlockTokens + off] = skb;
         a.v_scale[bh * kBlockTokens + off] = svb;
+      }
+      if (bmask != 0) {
+        // fp16 (nearest-even) values of the bypassed channels, in pair order
+        const TIn* kp = reinterpret_cast<const TIn*>(a.k) + (tok * a.n_kv + h) * D;
+        uint16_t* orow = a.k_outlier + (bh * kBlockTokens + off) * (int64_t)(2 * a.n_pairs);
+        for (int i = 0; i < a.n_pairs; ++i) {
+          const int j = plist[i];
+#pragma unroll
+          for (int sec = 0; sec < 2; ++sec) {
+            const int c = pair_channel(j, sec, D, a.interleaved);
+            if (c >= 16 * g && c < 16 * g + 16) {
+              const float x = sizeof(TIn) == 4 ? (float)reinterpret_cast<const float*>(kp)[c]
+                                               : bf16_to_f32(reinterpret_cast<const uint16_t*>(kp)[c]);
+              orow[2 * i + sec] = f16_bits((_Float16)x);
+            }
+          }
+        }
       }
     }
   } else if constexpr (KIND == WC_KIND_FP8_RAW) {
@@ -238,6 +270,85 @@ hipError_t launch_write_d(const WriteArgs& a, hipStream_t st) {
 hipError_t launch_quantize_write(const WriteArgs& a, hipStream_t st) {
   if (a.n_tok == 0) return hipSuccess;
   return a.head_dim == 64 ? launch_write_d<64>(a, st) : launch_write_d<128>(a, st);
+}
+
+// Fixed outlier pairs of one KV head (Sec. 6.2 fixed-channel bypass): the
+// float64 energy sum_t ||(k_t)_pair j||^2 of each of the D/2 RoPE pairs over all
+// rows, then the m largest (ties to the lower index), written in ascending order.
+// 1024 threads: thread (pair j, row stream s) sums rows s, s + TS, ...; the
+// streams are added in a fixed order, and wave 0 (lane = pair) selects.
+constexpr int kSelThreads = 1024;
+
+template <int D, typename TIn>
+__global__ __launch_bounds__(kSelThreads) void select_pairs_kernel(SelectArgs a) {
+  constexpr int NP = D / 2;
+  constexpr int TS = kSelThreads / NP;
+  __shared__ double e_s[TS][NP];
+  const int h = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int j = tid % NP, ts = tid / NP;
+  const int c0 = pair_channel(j, 0, D, a.interleaved), c1 = pair_channel(j, 1, D, a.interleaved);
+  const TIn* base = reinterpret_cast<const TIn*>(a.k) + (int64_t)h * D;
+  const int64_t stride = (int64_t)a.n_kv * D;
+  auto val = [&](int64_t t, int c) -> double {
+    const TIn* row = base + t * stride;
+    if constexpr (sizeof(TIn) == 4) return (double)reinterpret_cast<const float*>(row)[c];
+    else return (double)bf16_to_f32(reinterpret_cast<const uint16_t*>(row)[c]);
+  };
+  double acc = 0.0;
+  int64_t t = ts;
+  for (; t + 3 * TS < a.n_tok; t += 4 * TS) {   // four rows in flight
+    double x[8];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      x[2 * u] = val(t + u * TS, c0);
+      x[2 * u + 1] = val(t + u * TS, c1);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc = fma(x[u], x[u], acc);
+  }
+  for (; t < a.n_tok; t += TS) {
+    const double x0 = val(t, c0), x1 = val(t, c1);
+    acc = fma(x1, x1, fma(x0, x0, acc));
+  }
+  e_s[ts][j] = acc;
+  __syncthreads();
+  if (tid >= 64) return;
+  double e = -1.0;   // lanes past the last pair never win (energies are >= 0)
+  if (tid < NP) {
+    e = 0.0;
+    for (int s2 = 0; s2 < TS; ++s2) e += e_s[s2][tid];
+  }
+  uint64_t chosen = 0;
+  for (int i = 0; i < a.m; ++i) {
+    double be = e;
+    int bj = tid;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const double oe = __shfl_xor(be, o, 64);
+      const int oj = __shfl_xor(bj, o, 64);
+      if (oe > be || (oe == be && oj < bj)) {
+        be = oe;
+        bj = oj;
+      }
+    }
+    chosen |= 1ull << bj;
+    if (tid == bj) e = -2.0;
+  }
+  if ((chosen >> tid) & 1ull)
+    a.pairs_out[(int64_t)h * a.m + __popcll(chosen & ((1ull << tid) - 1ull))] = tid;
+}
+
+hipError_t launch_select_pairs(const SelectArgs& a, hipStream_t st) {
+  const dim3 grid(a.n_kv), block(kSelThreads);
+  if (a.head_dim == 128) {
+    if (a.in_dtype == WC_F32) hipLaunchKernelGGL((select_pairs_kernel<128, float>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((select_pairs_kernel<128, uint16_t>), grid, block, 0, st, a);
+  } else {
+    if (a.in_dtype == WC_F32) hipLaunchKernelGGL((select_pairs_kernel<64, float>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((select_pairs_kernel<64, uint16_t>), grid, block, 0, st, a);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_witness(const WitnessArgs& a, hipStream_t st) {

@@ -41,14 +41,27 @@ def torch_dtype(wl):
     return torch.float32 if wl.dtype == "f32" else torch.bfloat16
 
 
-def gpu_cache(case, kind, seed=None):
-    """Write every sequence of the case into a fresh GPU cache through wc_quantize_write."""
+def case_pairs(case, m):
+    """Bypassed pairs [n_kv, m] chosen by the oracle from all keys of the case."""
+    from oracle import bypass as obp
+    wl = case["wl"]
+    k = np.concatenate(case["k"])
+    return np.stack([obp.select_pairs(k[:, h], m, wl.rope_layout) for h in range(wl.n_kv)])
+
+
+def gpu_cache(case, kind, seed=None, pairs=None):
+    """Write every sequence of the case into a fresh GPU cache through wc_quantize_write
+    (pairs [n_kv, m]: bypassed RoPE pairs of the keys)."""
     import torch
 
     import paper_2607_28699_amd as wc
     wl = case["wl"]
+    m = 0 if pairs is None else int(np.asarray(pairs).shape[1])
     c = wc.PagedCache(kind, case["nblocks"], wl.n_kv, wl.d, wl.bands, layer=case["layer"],
-                      seed=wl.philox_seed() if seed is None else seed, rope_layout=wl.rope_layout)
+                      seed=wl.philox_seed() if seed is None else seed, rope_layout=wl.rope_layout,
+                      n_outlier_pairs=m)
+    if m:
+        c.set_outlier_pairs(torch.from_numpy(np.asarray(pairs, dtype=np.int32)))
     dt = torch_dtype(wl)
     k = np.concatenate(case["k"]) if len(case["k"]) else np.zeros((0, wl.n_kv, wl.d), np.float32)
     v = np.concatenate(case["v"])
@@ -74,9 +87,10 @@ def gpu_decode(case, cache, split_tokens=0, out_dtype=None):
     return out.float().cpu().numpy().astype(np.float64), meter.cpu().numpy(), raw.cpu().numpy()
 
 
-def oracle_write(case, kind):
+def oracle_write(case, kind, pairs=None):
     wl = case["wl"]
-    return [odec.write_cache(kind, k, v, s, case["layer"], wl.philox_seed(), wl.bands, wl.rope_layout)
+    return [odec.write_cache(kind, k, v, s, case["layer"], wl.philox_seed(), wl.bands, wl.rope_layout,
+                             pairs=pairs)
             for k, v, s in zip(case["k"], case["v"], case["slots"])]
 
 
@@ -113,6 +127,8 @@ def read_cache(cache, slots):
         out["vs"] = ofp_f16(t["v_scale"].numpy()[blk, :, off])
     if t["k_witness"] is not None:
         out["kw"] = ofp_f16(t["k_witness"].numpy()[blk, :, off, :])
+    if t.get("k_outlier") is not None:
+        out["ko"] = ofp_f16(t["k_outlier"].numpy()[blk, :, off, :])
     return out
 
 

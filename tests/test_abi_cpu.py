@@ -39,14 +39,21 @@ def test_status_strings_and_version(L):
 
 
 def test_cache_byte_account(L):
-    sizes = (ctypes.c_size_t * 5)()
+    sizes = (ctypes.c_size_t * 6)()
     # one KV head, 32768 tokens, d = 128, B = 8: 128 + 128 + 2 + 2 + 16 = 276 B per token
-    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, sizes)
+    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, sizes)
     assert tot == 32768 * 276
-    assert list(sizes) == [32768 * 128, 32768 * 128, 65536, 65536, 32768 * 16]
-    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, sizes) == 32768 * 272
-    assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, sizes) == 32768 * 512
-    assert L.wc_cache_bytes(7, 1, 1, 128, 8, sizes) == 0
+    assert list(sizes) == [32768 * 128, 32768 * 128, 65536, 65536, 32768 * 16, 0]
+    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, sizes) == 32768 * 272
+    assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, 0, sizes) == 32768 * 512
+    assert L.wc_cache_bytes(7, 1, 1, 128, 8, 0, sizes) == 0
+    # bypassed pairs: 2m fp16 values per token and KV head (Table 6: 16 B at m = 4)
+    for m in (2, 4, 8, 16):
+        tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, m, sizes)
+        assert sizes[5] == 32768 * 4 * m and tot == 32768 * (276 + 4 * m)
+    for bad in (-2, 3, 18):
+        assert L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, bad, sizes) == 0
+    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 4, sizes) == 0
 
 
 def test_workspace_size_and_argument_checks(L):
@@ -59,7 +66,7 @@ def test_workspace_size_and_argument_checks(L):
     assert L.wc_decode_workspace_size(-1, 28, 4, 128, 100, 0) == 0
     # null cache / pointers are rejected before anything is launched
     assert L.wc_quantize_write(None, None, None, 0, None, 1, None) == _lib.WC_EINVAL
-    c = _lib.WcCache(0, 96, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16)
+    c = _lib.WcCache(0, 96, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16, 0, 0, None, None)
     assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EUNSUPPORTED
     c.head_dim = 128
     c.k_data = 8                              # misaligned
@@ -71,3 +78,20 @@ def test_workspace_size_and_argument_checks(L):
     st = L.wc_metered_decode_attention(ctypes.byref(c), 16, 1, 1, 7, 16, 4, 16, 64, 0.1, 16, 0,
                                        16, 16, 0, 16, 8, None)
     assert st == _lib.WC_EWORKSPACE
+    # bypassed pairs: INT8 only, m even and <= 16, pair list and value array required
+    c.n_outlier_pairs = 4
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
+    c.outlier_pairs, c.k_outlier = 16, 16
+    c.n_outlier_pairs = 3
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
+    c.n_outlier_pairs, c.kind = 4, _lib.WC_KIND_FP8_RAW
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
+    c.kind = _lib.WC_KIND_INT8_DITHER
+    c.k_outlier = 24                          # misaligned
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
+    # pair selection: m within the pairs, head_dim 64 / 128, n_tok >= 1
+    assert L.wc_select_outlier_pairs(16, 1, 10, 4, 128, 0, 65, 16, None) == _lib.WC_EINVAL
+    assert L.wc_select_outlier_pairs(16, 1, 0, 4, 128, 0, 4, 16, None) == _lib.WC_EINVAL
+    assert L.wc_select_outlier_pairs(16, 1, 10, 4, 96, 0, 4, 16, None) == _lib.WC_EUNSUPPORTED
+    assert L.wc_select_outlier_pairs(None, 1, 10, 4, 128, 0, 4, 16, None) == _lib.WC_EINVAL
+    assert L.wc_select_outlier_pairs(16, 1, 10, 4, 128, 0, 0, None, None) == _lib.WC_OK
