@@ -17,11 +17,12 @@
 //   softmax online over the page; the running max is only raised when a page
 //         exceeds it by more than kSlack (then the accumulators are rescaled),
 //         so the common case needs no cross-lane exchange.
-//   PV    O^T = V^T W with v_mfma_f32_16x16x16_f16: A = value codes of 16 channels
-//         x 4 tokens per lane group (the value pages are stored token-quad
-//         interleaved, so this is one 32-byte load), B = p_t s^v_t in fp16, and a
-//         second product with D, transposed through LDS; the 2303 offset is
-//         removed with the running sum of the fp16 weights.
+//   PV    O^T = V^T W with v_mfma_f32_16x16x16_f16: A = value codes + 1152 (the
+//         stored byte as fp16 1024 + u, one permute) of 16 channels x 4 tokens per
+//         lane group (the value pages are stored token-quad interleaved, so this is
+//         one 32-byte load), B = p_t s^v_t in fp16, and a second product with D,
+//         transposed through LDS; the 1152 and 2303 offsets are removed at the end
+//         with the running sum of the fp16 weights.
 //
 // Lane l: r = l % 16 (token in the QK operands, head in B and in the results,
 // channel row in the PV operands), g = l / 16 (k-group).  The channel order of
@@ -54,6 +55,7 @@ constexpr int kRow = 272;  // LDS bytes per token row of the dither transpose (2
 // value scales up to 34.
 constexpr float kSlack = 2.0f;
 constexpr float kDOff = 2303.0f;   // 2048 + 255: D = 2u + 2048 = 512 xi + 2303
+constexpr float kCOff = 1152.0f;   // 1024 + 128: value operand 1024 + u = code + 1152
 
 __device__ __forceinline__ uint32_t as_u32(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
 __device__ __forceinline__ h2_t as_h2(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
@@ -70,6 +72,11 @@ constexpr uint32_t kSelH1 = 0x07060302u;   // high halves of lo and hi
 // Two codes stored excess-128 (byte u = code + 128) -> fp16 (1024 + u) - 1152 = code, exact.
 __device__ __forceinline__ uint32_t codes2(uint32_t xb, uint32_t sel) {
   return as_u32(as_h2(perm(0x64646464u, xb, sel)) - h2_t{(_Float16)1152.0f, (_Float16)1152.0f});
+}
+// Two stored bytes u -> fp16 1024 + u = code + 1152 (exact): the value operand of
+// PV, whose 1152 offset is removed once at the end with the weight sum.
+__device__ __forceinline__ uint32_t ucodes2(uint32_t xb, uint32_t sel) {
+  return perm(0x64646464u, xb, sel);
 }
 // Two dither bytes u -> fp16 2048 + 2u (bits 0x6800 | u), exact, one permute.
 __device__ __forceinline__ uint32_t dith2(uint32_t u, uint32_t sel) {
@@ -419,7 +426,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
 #pragma unroll
     for (int jt = 0; jt < 8; ++jt) {
       const uint32_t x = cur.vw[jt];     // codes (excess-128) of channel 8r+jt, tokens 4g..4g+3
-      st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(codes2(x, kSelLo), codes2(x, kSelHi)), wop,
+      st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(ucodes2(x, kSelLo), ucodes2(x, kSelHi)), wop,
                                                         st.o1[jt], 0, 0, 0);
       const uint32_t sel = (jt & 1) ? kSelH1 : kSelH0;
       const uint32_t d01 = perm(r1[jt >> 1], r0[jt >> 1], sel);
@@ -466,6 +473,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ float qn_s[kWaves][16][16];
   __shared__ __attribute__((aligned(16))) float acc_s[kWaves][16][kD];
   __shared__ float ml_s[kWaves][16][3];
+  __shared__ uint4 q_lds[16][17];   // the workgroup's queries, bf16 rows of 256 bytes (+16 pad)
 
   // the wave index is uniform: page addresses then live in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -477,6 +485,15 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   const int B = a.n_bands;
   const int wg_begin = blockIdx.x * a.split_tokens;
   const int32_t* trow = a.table + (int64_t)b * a.max_blocks;
+  // The workgroup's queries (G x 256 bytes) are requested first, once per
+  // workgroup (thread = 16 bytes of one head), and shared through LDS below: every
+  // workgroup of a (sequence, KV head) reads the same bytes, and loading them per
+  // wave made one L2 channel a hot spot at kernel start that held back the first
+  // page requests.
+  uint4 qv = make_uint4(0, 0, 0, 0);
+  if (threadIdx.x < a.group * 16)
+    qv = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a.q) +
+                                        ((int64_t)b * a.n_q + (int64_t)kv * a.group) * kD)[threadIdx.x];
   const int L = a.seq_lens[b];
 
   // Requests that need no sequence length go out with it: this wave's block
@@ -486,21 +503,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   const int pg_spec = wg_begin / kBlockTokens + wave * ppw_full;
   const int nc_spec = max(0, min(min(64, ppw_full), a.max_blocks - pg_spec));
   const int tv_spec = lane < nc_spec ? trow[pg_spec + lane] : 0;
-  // ---- queries of head r, channels 32g .. 32g+31 ----
-  // Lanes of padding heads (r >= G) repeat head 0: their scores and weights land
-  // in result columns that are never written out.
   const bool hv = r < G;
-  const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q) +
-                       ((int64_t)b * a.n_q + (int64_t)kv * G + (hv ? r : 0)) * kD + 32 * g;
-  uint32_t qraw[16];
-  {
-    const uint4* q4 = reinterpret_cast<const uint4*>(qp);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint4 v = q4[i];
-      qraw[4 * i] = v.x; qraw[4 * i + 1] = v.y; qraw[4 * i + 2] = v.z; qraw[4 * i + 3] = v.w;
-    }
-  }
 
   // whole workgroup: a KV head not routed here, or a split past the sequence end
   // (evaluated together, so that the length load is not held back behind the mask)
@@ -536,6 +539,24 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     __builtin_amdgcn_sched_barrier(0);
   };
   if (np > 0) start_chunk(0);
+
+  // ---- queries of head r, channels 32g .. 32g+31, from LDS ----
+  // Padding heads (r >= G) get zeros: their scores and weights land in result
+  // columns that are never written out.
+  uint32_t qraw[16];
+  {
+    if (threadIdx.x < G * 16) q_lds[threadIdx.x >> 4][threadIdx.x & 15] = qv;
+    // a barrier fenced for LDS only: a full workgroup fence would also wait for
+    // the page loads just issued
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint4 v = hv ? q_lds[r][4 * g + i] : make_uint4(0, 0, 0, 0);
+      qraw[4 * i] = v.x; qraw[4 * i + 1] = v.y; qraw[4 * i + 2] = v.z; qraw[4 * i + 3] = v.w;
+    }
+  }
 
   WaveConst wc;
   // Bypassed pairs (Sec. 6.2 fixed-channel bypass): the query channels of this
@@ -607,8 +628,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         w[j] = bf16pair_to_f16(qk[4 * kt + j]);
-        const h2_t h = as_h2(w[j]);
-        qsum += (float)h[0] + (float)h[1];
+        qsum = __builtin_amdgcn_fdot2(as_h2(w[j]), h2_t{(_Float16)1.0f, (_Float16)1.0f}, qsum, false);
       }
       wc.qop[kt] = pack8(w[0], w[1], w[2], w[3]);
     }
@@ -680,7 +700,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int band = 8 * (g & 1) + 2 * e2 + j;
-        const float x = band < B ? sqrtf(qn_s[wave][r][band]) * nmul : 0.0f;
+        const float x = band < B ? __builtin_amdgcn_sqrtf(qn_s[wave][r][band]) * nmul : 0.0f;
         const _Float16 hi = (_Float16)x;
         hv2[j] = (g < 2) ? hi : (_Float16)(x - (float)hi);
       }
@@ -764,7 +784,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     for (int jt = 0; jt < 8; ++jt) {
       v[jt] = st.o1[jt][e];
       if constexpr (KIND == WC_KIND_INT8_DITHER)
-        v[jt] = fmaf(st.o2[jt][e] - kDOff * st.wsum, -0.001953125f, v[jt]);
+        v[jt] = fmaf(st.o2[jt][e] - kDOff * st.wsum, -0.001953125f, v[jt] - kCOff * st.wsum);
       if constexpr (unscale != 1.0f) v[jt] *= unscale;
     }
     float4* dst = reinterpret_cast<float4*>(&acc_s[wave][r][32 * g + 8 * e]);
