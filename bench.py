@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="gqa-28x4-d128-s32k-b4")
     ap.add_argument("--tau", type=float, default=0.2)
+    ap.add_argument("--outlier-pairs", type=int, default=4,
+                    help="bypassed RoPE pairs per KV head for the bypass measurement (0: skip it)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -157,8 +159,12 @@ def main():
     seed = wl.philox_seed()
 
     # ---- caches and prefill write (timed separately: quant+witness throughput) ----
-    caches, exact = [], []
+    # With --outlier-pairs m > 0 every layer also gets an INT8 cache whose keys
+    # bypass the m RoPE pairs of largest energy over the layer's prefill keys (the
+    # fixed per-(layer, KV head) set of the outlier-pair bypass), chosen on the GPU.
+    caches, exact, byp_caches = [], [], []
     gen0 = None
+    m_byp = args.outlier_pairs
     for layer in range(wl.n_layers):
         c = wc.PagedCache("int8_dither", lay.nblocks, wl.n_kv, wl.d, wl.bands, layer=layer, seed=seed,
                           rope_layout=wl.rope_layout)
@@ -171,6 +177,14 @@ def main():
         for k, v, sl in gen:
             wc.quantize_write(c, k, v, sl)
             wc.quantize_write(e, k, v, sl)
+        if m_byp:
+            cb = wc.PagedCache("int8_dither", lay.nblocks, wl.n_kv, wl.d, wl.bands, layer=layer, seed=seed,
+                               rope_layout=wl.rope_layout, n_outlier_pairs=m_byp)
+            cb.set_outlier_pairs(wc.select_outlier_pairs(torch.cat([k for k, _, _ in gen]), m_byp,
+                                                         wl.rope_layout))
+            for k, v, sl in gen:
+                wc.quantize_write(cb, k, v, sl)
+            byp_caches.append(cb)
         torch.cuda.synchronize()
         caches.append(c)
         exact.append(e)
@@ -307,6 +321,59 @@ def main():
                                   max_len_all, sm, dloc, ws=ws, out=out, meter=meter, raw=raw)
         wc.gate(meter, raw, wl.group, args.tau, n_gated=counts_b, mask_q=mq_b, mask_kv=mkv_b)
     gqb, gkvb = counts_b.cpu().tolist()
+
+    # ---- outlier-pair bypass (Sec. 6.2): both certificates over caches whose keys
+    # keep the m most energetic RoPE pairs in fp16, out of the amax ----
+    byp = None
+    if m_byp:
+        for s in range(K + W):      # the decode-step tokens, as the timed steps wrote them
+            st = steps_in[s]
+            for layer in range(wl.n_layers):
+                it = st["layers"][layer]
+                if wl.chunk:
+                    wc.quantize_write(byp_caches[layer], it["ck"], it["cv"], it["cslots"])
+                wc.quantize_write(byp_caches[layer], it["k"], it["v"], st["slots"])
+        ba_ms = timed(lambda i: wc.metered_decode_gate(
+            byp_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
+            max_len_all, sm, args.tau, ws=ws, out=out, meter=meter, raw=raw, mask_q=mask_q,
+            mask_kv=mask_kv), reps)
+        bb_ms = timed(lambda i: wc.tierb_decode_attention(
+            byp_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
+            max_len_all, sm, dloc, ws=ws, out=out, meter=meter, raw=raw), reps)
+        cnt = {"A": torch.zeros(2, dtype=torch.int32, device=dev), "B": torch.zeros(2, dtype=torch.int32, device=dev)}
+        raws = {"A": [], "B": []}
+        for layer in range(wl.n_layers):
+            q_l = last["layers"][layer]["q"]
+            wc.metered_decode_attention(byp_caches[layer], q_l, table, last["lens"], max_len_all, sm, ws=ws,
+                                        out=out, meter=meter, raw=raw)
+            wc.gate(meter, raw, wl.group, args.tau, n_gated=cnt["A"], mask_q=mq_b, mask_kv=mkv_b)
+            raws["A"].append(raw.clone())
+            wc.tierb_decode_attention(byp_caches[layer], q_l, table, last["lens"], max_len_all, sm, dloc,
+                                      ws=ws, out=out, meter=meter, raw=raw)
+            wc.gate(meter, raw, wl.group, args.tau, n_gated=cnt["B"], mask_q=mq_b, mask_kv=mkv_b)
+            raws["B"].append(raw.clone())
+        # the fixed pair set itself: one layer's prefill keys, every KV head
+        kcat = torch.cat([torch_gen.gen_kv_layer(wl, 0, b, torch.arange(int(lens0[b]), device=dev))[0]
+                          for b in range(lay.batch)])
+        pairs_out = torch.empty((wl.n_kv, m_byp), dtype=torch.int32, device=dev)
+        sel_ws = torch.empty(wc.lib().wc_select_workspace_size(kcat.shape[0], wl.n_kv, wl.d),
+                             dtype=torch.uint8, device=dev)
+        sel_ms = float(np.median(timed(lambda i: wc.select_outlier_pairs(kcat, m_byp, wl.rope_layout,
+                                                                         out=pairs_out, ws=sel_ws), 4)))
+        n_cells = wl.n_layers * lay.batch
+        byp = {"outlier_pairs": m_byp, "select_pairs": {
+                   "median_launch_ms": round(sel_ms, 4), "rows": int(kcat.shape[0]),
+                   "GBps": round(kcat.numel() * kcat.element_size() / (sel_ms * 1e-3) / 1e9, 1)}}
+        for tier, ms, nbytes in (("tier_a", ba_ms, INT8_BYTES + 4 * m_byp), ("tier_b", bb_ms, TIERB_BYTES + 4 * m_byp)):
+            key = "A" if tier == "tier_a" else "B"
+            gq_, gkv_ = cnt[key].cpu().tolist()
+            gbps = float(last["tokens"] * wl.n_kv) * nbytes / (float(np.median(ms)) * 1e-3) / 1e9
+            byp[tier] = {"median_launch_ms": round(float(np.median(ms)), 4), "GBps": round(gbps, 1),
+                         "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4), "bytes_per_token_head": nbytes,
+                         "raw_median": round(float(torch.cat(raws[key]).median().item()), 4),
+                         "gate_fraction_q_heads": round(gq_ / (n_cells * wl.n_q), 4),
+                         "gate_fraction_kv_heads": round(gkv_ / (n_cells * wl.n_kv), 4)}
+        del kcat
     th_per_launch = float(last["tokens"] * wl.n_kv)
     tb_gbps = th_per_launch * TIERB_BYTES / (float(np.median(tb_ms)) * 1e-3) / 1e9
     dec_gbps = th_per_launch * INT8_BYTES / (float(np.median(dec_ms)) * 1e-3) / 1e9
@@ -359,6 +426,7 @@ def main():
                   "delta_req": 1e-2, "delta_loc": dloc,
                   "gate_fraction_q_heads": round(gqb / (wl.n_layers * lay.batch * wl.n_q), 4),
                   "gate_fraction_kv_heads": round(gkvb / (wl.n_layers * lay.batch * wl.n_kv), 4)},
+        "bypass": byp,
         "quant_witness": {"GBps": round(write_gbps, 1), "frac_hbm": round(write_gbps / HBM_PEAK_GBPS, 4),
                           "bytes_per_token_head": WRITE_BYTES_BF16_IN,
                           "token_heads": write_tokens},

@@ -138,15 +138,19 @@ size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim
  * pairs selected by energy): the m RoPE pairs j of largest energy
  * E_j = sum_i ||(k_i)_pair j||^2 over the n_tok rows given (e.g. a prefill),
  * ties to the lower j, written in ascending order to pairs_out[h][0..m-1].
- * The energies are summed in float64.  RoPE does not change E_j, so the set is
- * the same before and after the rotation.
+ * The energies are summed in float64, over fixed row chunks in a fixed order, so
+ * the result does not depend on scheduling.  RoPE does not change E_j, so the set
+ * is the same before and after the rotation.
  *   k          [n_tok][n_kv_heads][head_dim], in_dtype WC_F32 or WC_BF16, n_tok >= 1
  *   m          0 <= m <= head_dim/2 (m = 0 writes nothing)
  *   pairs_out  [n_kv_heads][m] int32 device
+ *   ws         device workspace of ws_bytes >= wc_select_workspace_size(n_tok,
+ *              n_kv_heads, head_dim) bytes, 8-byte aligned, no initialization needed
  */
+size_t wc_select_workspace_size(int64_t n_tok, int n_kv_heads, int head_dim);
 int wc_select_outlier_pairs(const void* k, int in_dtype, int64_t n_tok, int n_kv_heads,
-                            int head_dim, int rope_layout, int m, int32_t* pairs_out,
-                            void* stream);
+                            int head_dim, int rope_layout, int m, int32_t* pairs_out, void* ws,
+                            size_t ws_bytes, void* stream);
 
 /*
  * Write path (Sec. 4.2 subtractive dither; Sec. 6.2 research kernels and storage

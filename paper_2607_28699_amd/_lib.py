@@ -18,7 +18,7 @@ WC_BLOCK_TOKENS = 16
 
 EXPORTS = (
     "wc_strerror", "wc_version", "wc_cache_bytes", "wc_quantize_write", "wc_quantize_write_pair",
-    "wc_witness", "wc_select_outlier_pairs", "wc_decode_workspace_size", "wc_metered_decode_attention",
+    "wc_witness", "wc_select_workspace_size", "wc_select_outlier_pairs", "wc_decode_workspace_size", "wc_metered_decode_attention",
     "wc_metered_decode_gate", "wc_tierb_decode_attention", "wc_gate", "wc_exact_decode_attention",
 )
 
@@ -59,8 +59,9 @@ def lib() -> ctypes.CDLL:
         "wc_version": (ctypes.c_int, []),
         "wc_cache_bytes": (sz, [ctypes.c_int, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                 ctypes.c_int, ctypes.POINTER(sz)]),
+        "wc_select_workspace_size": (sz, [i64, ctypes.c_int, ctypes.c_int]),
         "wc_select_outlier_pairs": (ctypes.c_int, [vp, ctypes.c_int, i64, ctypes.c_int, ctypes.c_int,
-                                                   ctypes.c_int, ctypes.c_int, vp, vp]),
+                                                   ctypes.c_int, ctypes.c_int, vp, vp, sz, vp]),
         "wc_quantize_write": (ctypes.c_int, [cp, vp, vp, ctypes.c_int, vp, i64, vp]),
         "wc_quantize_write_pair": (ctypes.c_int, [cp, cp, vp, vp, ctypes.c_int, vp, i64, vp]),
         "wc_witness": (ctypes.c_int, [vp, ctypes.c_int, vp, ctypes.c_int, i64, ctypes.c_int,

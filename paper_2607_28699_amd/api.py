@@ -130,15 +130,19 @@ def quantize_write_pair(cache: PagedCache, exact: PagedCache, k: torch.Tensor, v
 
 
 def select_outlier_pairs(k: torch.Tensor, m: int, rope_layout: str = "half",
-                         out: torch.Tensor | None = None) -> torch.Tensor:
+                         out: torch.Tensor | None = None, ws: torch.Tensor | None = None) -> torch.Tensor:
     """The m RoPE pairs of largest energy of each KV head over the rows of
     k [n_tok, n_kv, d] -> int32 [n_kv, m], ascending."""
     _dev_check(k)
     n_tok, n_kv, d = k.shape
     if out is None:
         out = torch.empty((n_kv, m), dtype=torch.int32, device=k.device)
+    if ws is None:
+        n = lib().wc_select_workspace_size(n_tok, n_kv, d)
+        ws = torch.empty(max(n, 8), dtype=torch.uint8, device=k.device)
     check(lib().wc_select_outlier_pairs(_ptr(k), _dt(k), n_tok, n_kv, d, LAYOUTS[rope_layout], m,
-                                        _ptr(out), _stream()), "wc_select_outlier_pairs")
+                                        _ptr(out), _ptr(ws), ws.numel(), _stream()),
+          "wc_select_outlier_pairs")
     return out
 
 

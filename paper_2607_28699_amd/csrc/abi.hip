@@ -143,18 +143,33 @@ int wc_witness(const void* x, int x_dtype, const void* xhat, int xhat_dtype, int
   return hip_status(wc::launch_witness(a, static_cast<hipStream_t>(stream)));
 }
 
+size_t wc_select_workspace_size(int64_t n_tok, int n_kv_heads, int head_dim) {
+  if (n_tok < 1 || n_kv_heads < 1 || head_dim < 2) return 0;
+  return (size_t)n_kv_heads * wc::select_chunks(n_tok) * (head_dim / 2) * sizeof(double);
+}
+
 int wc_select_outlier_pairs(const void* k, int in_dtype, int64_t n_tok, int n_kv_heads,
-                            int head_dim, int rope_layout, int m, int32_t* pairs_out,
-                            void* stream) {
+                            int head_dim, int rope_layout, int m, int32_t* pairs_out, void* ws,
+                            size_t ws_bytes, void* stream) {
   if (n_tok < 1 || n_kv_heads < 1 || n_kv_heads > 65535 || (in_dtype != WC_F32 && in_dtype != WC_BF16))
     return WC_EINVAL;
   if (head_dim != 64 && head_dim != 128) return WC_EUNSUPPORTED;
   if (rope_layout != WC_ROPE_HALF && rope_layout != WC_ROPE_INTERLEAVED) return WC_EINVAL;
   if (m < 0 || m > head_dim / 2) return WC_EINVAL;
   if (m == 0) return WC_OK;
-  if (!k || !pairs_out || !aligned16(k)) return WC_EINVAL;
-  wc::SelectArgs a{k, in_dtype, n_kv_heads, head_dim, rope_layout == WC_ROPE_INTERLEAVED, m, n_tok,
-                   pairs_out};
+  if (!k || !pairs_out || !ws || !aligned16(k) || ((uintptr_t)ws & 7u)) return WC_EINVAL;
+  if (ws_bytes < wc_select_workspace_size(n_tok, n_kv_heads, head_dim)) return WC_EWORKSPACE;
+  wc::SelectArgs a{};
+  a.k = k;
+  a.in_dtype = in_dtype;
+  a.n_kv = n_kv_heads;
+  a.head_dim = head_dim;
+  a.interleaved = rope_layout == WC_ROPE_INTERLEAVED;
+  a.m = m;
+  a.n_chunks = wc::select_chunks(n_tok);
+  a.n_tok = n_tok;
+  a.pairs_out = pairs_out;
+  a.part = static_cast<double*>(ws);
   return hip_status(wc::launch_select_pairs(a, static_cast<hipStream_t>(stream)));
 }
 

@@ -29,9 +29,10 @@ struct WriteArgs {
 
 struct SelectArgs {
   const void* k;
-  int in_dtype, n_kv, head_dim, interleaved, m;
+  int in_dtype, n_kv, head_dim, interleaved, m, n_chunks;
   int64_t n_tok;
   int32_t* pairs_out;
+  double* part;             // [n_kv][n_chunks][head_dim / 2] partial pair energies (workspace)
 };
 
 struct WitnessArgs {
@@ -128,6 +129,7 @@ inline size_t gate_unit_bytes(int batch, int n_kv) {
 hipError_t launch_quantize_write(const WriteArgs& a, hipStream_t st);
 hipError_t launch_witness(const WitnessArgs& a, hipStream_t st);
 hipError_t launch_select_pairs(const SelectArgs& a, hipStream_t st);
+int select_chunks(int64_t n_tok);   // row chunks of the pair-energy pass
 hipError_t launch_decode(const DecodeArgs& a, bool metered, hipStream_t st);
 bool mfma_decode_supported(const DecodeArgs& a);
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st);

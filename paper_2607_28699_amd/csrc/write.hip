@@ -272,32 +272,36 @@ hipError_t launch_quantize_write(const WriteArgs& a, hipStream_t st) {
   return a.head_dim == 64 ? launch_write_d<64>(a, st) : launch_write_d<128>(a, st);
 }
 
-// Fixed outlier pairs of one KV head (Sec. 6.2 fixed-channel bypass): the
-// float64 energy sum_t ||(k_t)_pair j||^2 of each of the D/2 RoPE pairs over all
-// rows, then the m largest (ties to the lower index), written in ascending order.
-// 1024 threads: thread (pair j, row stream s) sums rows s, s + TS, ...; the
-// streams are added in a fixed order, and wave 0 (lane = pair) selects.
-constexpr int kSelThreads = 1024;
+// Fixed outlier pairs of each KV head (Sec. 6.2 fixed-channel bypass), in two
+// passes so that the sum over many rows uses the whole GPU and stays
+// deterministic: (1) workgroup (chunk c, head h) sums the float64 energies
+// ||(k_t)_pair j||^2 of all D/2 pairs over its rows into part[h][c][j] (thread =
+// pair x row stream, streams added in a fixed order); (2) one wave per head adds
+// the chunks in order and takes the m largest (ties to the lower index), written
+// in ascending order.
+constexpr int kEnThreads = 256;
 
 template <int D, typename TIn>
-__global__ __launch_bounds__(kSelThreads) void select_pairs_kernel(SelectArgs a) {
+__global__ __launch_bounds__(kEnThreads) void pair_energy_kernel(SelectArgs a) {
   constexpr int NP = D / 2;
-  constexpr int TS = kSelThreads / NP;
+  constexpr int TS = kEnThreads / NP;
   __shared__ double e_s[TS][NP];
-  const int h = blockIdx.x;
+  const int c = blockIdx.x, h = blockIdx.y;
   const int tid = threadIdx.x;
   const int j = tid % NP, ts = tid / NP;
   const int c0 = pair_channel(j, 0, D, a.interleaved), c1 = pair_channel(j, 1, D, a.interleaved);
+  const int64_t rows = (a.n_tok + a.n_chunks - 1) / a.n_chunks;
+  const int64_t r0 = (int64_t)c * rows, r1 = min(a.n_tok, r0 + rows);
   const TIn* base = reinterpret_cast<const TIn*>(a.k) + (int64_t)h * D;
   const int64_t stride = (int64_t)a.n_kv * D;
-  auto val = [&](int64_t t, int c) -> double {
+  auto val = [&](int64_t t, int ch) -> double {
     const TIn* row = base + t * stride;
-    if constexpr (sizeof(TIn) == 4) return (double)reinterpret_cast<const float*>(row)[c];
-    else return (double)bf16_to_f32(reinterpret_cast<const uint16_t*>(row)[c]);
+    if constexpr (sizeof(TIn) == 4) return (double)reinterpret_cast<const float*>(row)[ch];
+    else return (double)bf16_to_f32(reinterpret_cast<const uint16_t*>(row)[ch]);
   };
   double acc = 0.0;
-  int64_t t = ts;
-  for (; t + 3 * TS < a.n_tok; t += 4 * TS) {   // four rows in flight
+  int64_t t = r0 + ts;
+  for (; t + 3 * TS < r1; t += 4 * TS) {   // four rows in flight
     double x[8];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -307,22 +311,31 @@ __global__ __launch_bounds__(kSelThreads) void select_pairs_kernel(SelectArgs a)
 #pragma unroll
     for (int u = 0; u < 8; ++u) acc = fma(x[u], x[u], acc);
   }
-  for (; t < a.n_tok; t += TS) {
+  for (; t < r1; t += TS) {
     const double x0 = val(t, c0), x1 = val(t, c1);
     acc = fma(x1, x1, fma(x0, x0, acc));
   }
   e_s[ts][j] = acc;
   __syncthreads();
-  if (tid >= 64) return;
-  double e = -1.0;   // lanes past the last pair never win (energies are >= 0)
   if (tid < NP) {
-    e = 0.0;
+    double e = 0.0;
     for (int s2 = 0; s2 < TS; ++s2) e += e_s[s2][tid];
+    a.part[((int64_t)h * a.n_chunks + c) * NP + tid] = e;
+  }
+}
+
+__global__ __launch_bounds__(64) void select_pairs_kernel(SelectArgs a) {
+  const int NP = a.head_dim / 2;
+  const int h = blockIdx.x, lane = threadIdx.x;
+  double e = -1.0;   // lanes past the last pair never win (energies are >= 0)
+  if (lane < NP) {
+    e = 0.0;
+    for (int c = 0; c < a.n_chunks; ++c) e += a.part[((int64_t)h * a.n_chunks + c) * NP + lane];
   }
   uint64_t chosen = 0;
   for (int i = 0; i < a.m; ++i) {
     double be = e;
-    int bj = tid;
+    int bj = lane;
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
       const double oe = __shfl_xor(be, o, 64);
@@ -333,21 +346,27 @@ __global__ __launch_bounds__(kSelThreads) void select_pairs_kernel(SelectArgs a)
       }
     }
     chosen |= 1ull << bj;
-    if (tid == bj) e = -2.0;
+    if (lane == bj) e = -2.0;
   }
-  if ((chosen >> tid) & 1ull)
-    a.pairs_out[(int64_t)h * a.m + __popcll(chosen & ((1ull << tid) - 1ull))] = tid;
+  if ((chosen >> lane) & 1ull)
+    a.pairs_out[(int64_t)h * a.m + __popcll(chosen & ((1ull << lane) - 1ull))] = lane;
+}
+
+int select_chunks(int64_t n_tok) {
+  const int64_t c = (n_tok + 2047) / 2048;
+  return (int)(c < 1 ? 1 : (c > 64 ? 64 : c));
 }
 
 hipError_t launch_select_pairs(const SelectArgs& a, hipStream_t st) {
-  const dim3 grid(a.n_kv), block(kSelThreads);
+  const dim3 grid(a.n_chunks, a.n_kv), block(kEnThreads);
   if (a.head_dim == 128) {
-    if (a.in_dtype == WC_F32) hipLaunchKernelGGL((select_pairs_kernel<128, float>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((select_pairs_kernel<128, uint16_t>), grid, block, 0, st, a);
+    if (a.in_dtype == WC_F32) hipLaunchKernelGGL((pair_energy_kernel<128, float>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((pair_energy_kernel<128, uint16_t>), grid, block, 0, st, a);
   } else {
-    if (a.in_dtype == WC_F32) hipLaunchKernelGGL((select_pairs_kernel<64, float>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((select_pairs_kernel<64, uint16_t>), grid, block, 0, st, a);
+    if (a.in_dtype == WC_F32) hipLaunchKernelGGL((pair_energy_kernel<64, float>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((pair_energy_kernel<64, uint16_t>), grid, block, 0, st, a);
   }
+  hipLaunchKernelGGL(select_pairs_kernel, dim3(a.n_kv), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 

@@ -89,9 +89,15 @@ def test_workspace_size_and_argument_checks(L):
     c.kind = _lib.WC_KIND_INT8_DITHER
     c.k_outlier = 24                          # misaligned
     assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
-    # pair selection: m within the pairs, head_dim 64 / 128, n_tok >= 1
-    assert L.wc_select_outlier_pairs(16, 1, 10, 4, 128, 0, 65, 16, None) == _lib.WC_EINVAL
-    assert L.wc_select_outlier_pairs(16, 1, 0, 4, 128, 0, 4, 16, None) == _lib.WC_EINVAL
-    assert L.wc_select_outlier_pairs(16, 1, 10, 4, 96, 0, 4, 16, None) == _lib.WC_EUNSUPPORTED
-    assert L.wc_select_outlier_pairs(None, 1, 10, 4, 128, 0, 4, 16, None) == _lib.WC_EINVAL
-    assert L.wc_select_outlier_pairs(16, 1, 10, 4, 128, 0, 0, None, None) == _lib.WC_OK
+    # pair selection: m within the pairs, head_dim 64 / 128, n_tok >= 1, a workspace of
+    # float64 partial energies per (KV head, chunk of 2048 rows, pair), up to 64 chunks
+    assert L.wc_select_workspace_size(131072, 4, 128) == 4 * 64 * 64 * 8
+    assert L.wc_select_workspace_size(1000, 2, 64) == 2 * 1 * 32 * 8
+    assert L.wc_select_workspace_size(10 ** 7, 1, 128) == 64 * 64 * 8
+    assert L.wc_select_workspace_size(0, 4, 128) == 0
+    assert L.wc_select_outlier_pairs(16, 1, 10, 4, 128, 0, 65, 16, 16, 4096, None) == _lib.WC_EINVAL
+    assert L.wc_select_outlier_pairs(16, 1, 0, 4, 128, 0, 4, 16, 16, 4096, None) == _lib.WC_EINVAL
+    assert L.wc_select_outlier_pairs(16, 1, 10, 4, 96, 0, 4, 16, 16, 4096, None) == _lib.WC_EUNSUPPORTED
+    assert L.wc_select_outlier_pairs(None, 1, 10, 4, 128, 0, 4, 16, 16, 4096, None) == _lib.WC_EINVAL
+    assert L.wc_select_outlier_pairs(16, 1, 10, 4, 128, 0, 4, 16, 16, 8, None) == _lib.WC_EWORKSPACE
+    assert L.wc_select_outlier_pairs(16, 1, 10, 4, 128, 0, 0, None, None, 0, None) == _lib.WC_OK
