@@ -11,7 +11,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import attention, bypass, meter as mt, quantizer
+from . import attention, bypass, meter as mt, quantizer, value
 from .philox import dither_values
 
 KINDS = ("int8_dither", "fp8_raw", "bf16")
@@ -23,8 +23,9 @@ def write_cache(kind: str, k: np.ndarray, v: np.ndarray, slots: np.ndarray, laye
 
     k, v: stored inputs [S, n_kv, d] (float); slots: int [S] physical slots.
     pairs: int [n_kv, m] bypassed RoPE pairs of the keys (int8 only; ``bypass``).
-    Returns reconstructions khat/vhat [S, n_kv, d], key witness kw [S, n_kv, B]
-    and, for int8, codes and scales; with pairs also the stored fp16 values
+    Returns reconstructions khat/vhat [S, n_kv, d], key witness kw [S, n_kv, B],
+    for the quantized kinds the value residual and value norms vr, vn [S, n_kv]
+    (``value``) and, for int8, codes and scales; with pairs also the stored fp16 values
     ko [S, n_kv, 2m] and their channels chans [n_kv, 2m].
     """
     k = np.asarray(k, dtype=np.float64)
@@ -64,6 +65,9 @@ def write_cache(kind: str, k: np.ndarray, v: np.ndarray, slots: np.ndarray, laye
         out["khat"][:, h], out["vhat"][:, h] = kh, vh
         if kind != "bf16":
             out["kw"][:, h] = quantizer.witness(k[:, h], kh, n_bands, layout)
+    if kind != "bf16":   # value side: stored residual norm (up) and value norm (down)
+        out["vr"] = value.value_residual(v, out["vhat"])
+        out["vn"] = value.value_norm(v)
     return out
 
 

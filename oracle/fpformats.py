@@ -9,6 +9,9 @@
                    "amax/s <= 126.5" (no clipping, Sec. 4.2) and keeps the stored
                    witness an upper bound of the residual norm (Theorem black-box
                    logit bound needs w >= ||r_b||).
+* ``f16_round_down`` round toward 0 to fp16, for the stored value norm, which the
+                   value meter divides by (a lower bound keeps the meter an upper
+                   bound).
 * ``e4m3_*``       OCP fp8 E4M3 ("fn": no infinities, one NaN pattern), round to
                    nearest even, saturating at +-448 (the raw fp8 cast, a
                    black-box scheme of Sec. 4.1; saturation is our reading).
@@ -31,6 +34,17 @@ def f16_round_up(x) -> np.ndarray:
     with np.errstate(over="ignore"):
         up = np.nextafter(h, np.float16(np.inf))
     h = np.where(low, up, h)
+    return h.astype(np.float64)
+
+
+def f16_round_down(x) -> np.ndarray:
+    """Largest fp16 value <= x (as float64); x must be finite and >= 0 (values
+    above 65504 give 65504)."""
+    x = np.asarray(x, dtype=np.float64)
+    h = np.minimum(x, 65504.0).astype(np.float16)   # nearest even
+    high = h.astype(np.float64) > x
+    down = np.nextafter(h, np.float16(0.0))
+    h = np.where(high, down, h)
     return h.astype(np.float64)
 
 
