@@ -89,6 +89,10 @@ extern "C" {
  *   k_witness  [num_blocks][n_kv_heads][16][n_bands] fp16     NULL for BF16
  *   k_outlier  [num_blocks][n_kv_heads][16][2m] fp16          keys of the bypassed pairs
  *              (m = n_outlier_pairs > 0 only, else NULL)
+ *   v_resid,
+ *   v_norm     [num_blocks][n_kv_heads][16] fp16              value side (optional, both or
+ *              neither, quantized kinds only): ||vhat_t - v_t|| rounded up and ||v_t||
+ *              rounded down, from float64 norms (Sec. 3 output bound; Sec. 4.2 value side)
  * Element type of k_data/v_data: int8 code stored excess-128, i.e. the byte code + 128
  * (INT8_DITHER; codes lie in [-127, 127]), E4M3 byte (FP8_RAW), bf16 (BF16).
  * Band b holds the channels of RoPE pairs b*P .. b*P+P-1, P = head_dim/(2*n_bands)
@@ -119,6 +123,7 @@ typedef struct wc_cache {
     int32_t  reserved;                 /* 0                                            */
     const int32_t* outlier_pairs;      /* [n_kv_heads][m] device, or NULL when m == 0  */
     void*    k_outlier;                /* see above, or NULL when m == 0               */
+    void    *v_resid, *v_norm;          /* value side, or both NULL                     */
 } wc_cache;
 
 const char* wc_strerror(int status);
@@ -126,12 +131,13 @@ int         wc_version(void);   /* 100*major + minor */
 
 /*
  * Bytes of each array of a cache (k_data, v_data, k_scale, v_scale, k_witness,
- * k_outlier) written to sizes[0..5]; returns their sum, 0 on bad arguments.  The
- * "exact byte account" of the cache (Sec. 5 memory saving; Sec. 6.2 acceptance;
- * Table 6: 4m bytes per token and KV head for the bypassed pairs).
+ * k_outlier, v_resid, v_norm) written to sizes[0..7]; returns their sum, 0 on bad
+ * arguments.  The "exact byte account" of the cache (Sec. 5 memory saving;
+ * Sec. 6.2 acceptance; Table 6: 4m bytes per token and KV head for the bypassed
+ * pairs; 2 + 2 bytes for the value side when value_side != 0).
  */
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim,
-                      int n_bands, int n_outlier_pairs, size_t sizes[6]);
+                      int n_bands, int n_outlier_pairs, int value_side, size_t sizes[8]);
 
 /*
  * Fixed outlier-pair set of each KV head (Sec. 6.2 fixed-channel bypass; Sec. 4.2
@@ -164,7 +170,9 @@ int wc_select_outlier_pairs(const void* k, int in_dtype, int64_t n_tok, int n_kv
  *   FP8_RAW:     code = E4M3(x), nearest-even, saturating at +-448;
  *   BF16:        x rounded to bf16 (nearest-even);
  * and, except for BF16, the key witness w_b = ||(khat - k)_b|| rounded up to fp16
- * (the residual, its squares, sums and square root in float64; one round-up).
+ * (the residual, its squares, sums and square root in float64; one round-up), and,
+ * when the cache has a value side, ||vhat - v|| rounded up and ||v|| rounded down to
+ * fp16 (float64 norms).
  *   k, v          [n_tok][n_kv_heads][head_dim], in_dtype WC_F32 or WC_BF16 (post-RoPE keys)
  *   slot_mapping  [n_tok] int64 device; slot < 0 skips the token
  */
@@ -270,6 +278,28 @@ int wc_metered_decode_gate(const wc_cache* cache, const void* q, int q_dtype, in
                            int out_dtype, float* meter, float* raw, int split_tokens, float tau,
                            uint8_t* mask_q, uint8_t* mask_kv, int32_t* n_gated, void* ws,
                            size_t ws_bytes, void* stream);
+
+/*
+ * Joint key + value certificate with its gate (Sec. 3 output bound; Sec. 4.2 value
+ * side and joint event): wc_metered_decode_gate (delta_loc == 0: Tier A, the
+ * witness bound) or Tier B (0 < delta_loc < 1, as wc_tierb_decode_attention), plus
+ * the value meter of each query head over its KV head's cache,
+ *   meter_v[b][h] = (sum_t ptilde_t rho_t) / max_t nu_t,
+ * rho_t, nu_t the stored value residual (up) and value norm (down), so that
+ *   ||y - yhat|| <= (2 meter + meter_v) * max_t ||v_t||
+ * (the key-side TV bound times 2 plus the value term, in units of the largest value
+ * norm; 0/0 = 0, x/0 = +inf), and the joint gate
+ *   mask_q[b][h] = !(pass_K && pass_V),  pass_K = (tau_k < 1 ? meter : raw) <= tau_k,
+ *                                        pass_V = meter_v <= tau_v,
+ * routed per KV head (any-of-G), n_gated counted as in wc_gate.  The cache must
+ * carry the value side (v_resid and v_norm) and, for Tier A, the key witness.
+ */
+int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int batch,
+                         int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                         const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out,
+                         int out_dtype, float* meter, float* raw, float* meter_v, int split_tokens,
+                         float delta_loc, float tau, float tau_v, uint8_t* mask_q, uint8_t* mask_kv,
+                         int32_t* n_gated, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Gate (the meter loop's gate, Sec. 6; certified vs risk-ranked, Sec. 4.3):

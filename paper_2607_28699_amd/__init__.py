@@ -13,6 +13,7 @@ from .api import (  # noqa: F401
     decode_workspace,
     exact_decode_attention,
     gate,
+    joint_decode_gate,
     metered_decode_attention,
     metered_decode_gate,
     quantize_write,

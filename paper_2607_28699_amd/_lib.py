@@ -19,7 +19,8 @@ WC_BLOCK_TOKENS = 16
 EXPORTS = (
     "wc_strerror", "wc_version", "wc_cache_bytes", "wc_quantize_write", "wc_quantize_write_pair",
     "wc_witness", "wc_select_workspace_size", "wc_select_outlier_pairs", "wc_decode_workspace_size", "wc_metered_decode_attention",
-    "wc_metered_decode_gate", "wc_tierb_decode_attention", "wc_gate", "wc_exact_decode_attention",
+    "wc_metered_decode_gate", "wc_tierb_decode_attention", "wc_joint_decode_gate", "wc_gate",
+    "wc_exact_decode_attention",
 )
 
 
@@ -32,6 +33,7 @@ class WcCache(ctypes.Structure):
         ("v_scale", ctypes.c_void_p), ("k_witness", ctypes.c_void_p),
         ("n_outlier_pairs", ctypes.c_int32), ("reserved", ctypes.c_int32),
         ("outlier_pairs", ctypes.c_void_p), ("k_outlier", ctypes.c_void_p),
+        ("v_resid", ctypes.c_void_p), ("v_norm", ctypes.c_void_p),
     ]
 
 
@@ -58,7 +60,7 @@ def lib() -> ctypes.CDLL:
         "wc_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         "wc_version": (ctypes.c_int, []),
         "wc_cache_bytes": (sz, [ctypes.c_int, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-                                ctypes.c_int, ctypes.POINTER(sz)]),
+                                ctypes.c_int, ctypes.c_int, ctypes.POINTER(sz)]),
         "wc_select_workspace_size": (sz, [i64, ctypes.c_int, ctypes.c_int]),
         "wc_select_outlier_pairs": (ctypes.c_int, [vp, ctypes.c_int, i64, ctypes.c_int, ctypes.c_int,
                                                    ctypes.c_int, ctypes.c_int, vp, vp, sz, vp]),
@@ -80,6 +82,10 @@ def lib() -> ctypes.CDLL:
                                                      ctypes.c_int, vp, ctypes.c_int, vp, i64, f32,
                                                      vp, ctypes.c_int, vp, vp, ctypes.c_int, f32,
                                                      vp, sz, vp]),
+        "wc_joint_decode_gate": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                vp, ctypes.c_int, vp, i64, f32, vp, ctypes.c_int,
+                                                vp, vp, vp, ctypes.c_int, f32, f32, f32, vp, vp, vp,
+                                                vp, sz, vp]),
         "wc_gate": (ctypes.c_int, [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, f32, vp, vp,
                                    vp, vp]),
         "wc_exact_decode_attention": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int,

@@ -42,10 +42,10 @@ def _dev_check(*ts):
 
 
 def cache_bytes(kind: str, num_blocks: int, n_kv: int, head_dim: int, n_bands: int,
-                n_outlier_pairs: int = 0):
-    sizes = (ctypes.c_size_t * 6)()
+                n_outlier_pairs: int = 0, value_side: bool = False):
+    sizes = (ctypes.c_size_t * 8)()
     total = lib().wc_cache_bytes(KINDS[kind], num_blocks, n_kv, head_dim, n_bands, n_outlier_pairs,
-                                 sizes)
+                                 int(value_side), sizes)
     if total == 0:
         raise _lib.WitCertError("bad cache geometry")
     return total, list(sizes)
@@ -64,12 +64,14 @@ class PagedCache:
     rope_layout: str = "half"
     device: str = "cuda"
     n_outlier_pairs: int = 0
+    value_side: bool = False
     tensors: dict = field(default_factory=dict)
 
     def __post_init__(self):
         m = self.n_outlier_pairs
-        total, sizes = cache_bytes(self.kind, self.num_blocks, self.n_kv, self.head_dim, self.n_bands, m)
-        names = ("k_data", "v_data", "k_scale", "v_scale", "k_witness", "k_outlier")
+        total, sizes = cache_bytes(self.kind, self.num_blocks, self.n_kv, self.head_dim, self.n_bands, m,
+                                   self.value_side)
+        names = ("k_data", "v_data", "k_scale", "v_scale", "k_witness", "k_outlier", "v_resid", "v_norm")
         slots = self.num_blocks * WC_BLOCK_TOKENS * self.n_kv
         shapes = {
             "k_data": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.head_dim),
@@ -78,6 +80,8 @@ class PagedCache:
             "v_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
             "k_witness": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.n_bands),
             "k_outlier": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, 2 * m),
+            "v_resid": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
+            "v_norm": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
         }
         # int8 codes are stored excess-128 (byte = code + 128)
         el = {"int8_dither": torch.uint8, "fp8_raw": torch.uint8, "bf16": torch.bfloat16}[self.kind]
@@ -107,7 +111,8 @@ class PagedCache:
                        LAYOUTS[self.rope_layout], self.layer, self.num_blocks, self.seed,
                        _ptr(t["k_data"]), _ptr(t["v_data"]), _ptr(t["k_scale"]),
                        _ptr(t["v_scale"]), _ptr(t["k_witness"]), self.n_outlier_pairs, 0,
-                       _ptr(t["outlier_pairs"]), _ptr(t["k_outlier"]))
+                       _ptr(t["outlier_pairs"]), _ptr(t["k_outlier"]), _ptr(t["v_resid"]),
+                       _ptr(t["v_norm"]))
 
 
 def quantize_write(cache: PagedCache, k: torch.Tensor, v: torch.Tensor, slots: torch.Tensor) -> None:
@@ -234,6 +239,33 @@ def metered_decode_gate(cache: PagedCache, q: torch.Tensor, block_table: torch.T
         split_tokens, float(tau), _ptr(mask_q), _ptr(mask_kv), _ptr(n_gated), _ptr(ws), ws.numel(),
         _stream()), "wc_metered_decode_gate")
     return out, meter, raw, mask_q, mask_kv
+
+
+def joint_decode_gate(cache: PagedCache, q: torch.Tensor, block_table: torch.Tensor,
+                      seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float, tau: float = 0.2,
+                      tau_v: float = 0.05, delta_loc: float = 0.0, out_dtype=torch.float32,
+                      split_tokens: int = 0, ws=None, out=None, meter=None, raw=None, meter_v=None,
+                      mask_q=None, mask_kv=None, n_gated=None):
+    """Key meter (Tier A, or Tier B when delta_loc > 0), value meter and the joint
+    gate -> (out, meter, raw, meter_v, mask_q, mask_kv)."""
+    _dev_check(q, block_table, seq_lens)
+    batch, n_q, d = q.shape
+    dev = q.device
+    if ws is None:
+        ws = decode_workspace(batch, n_q, cache.n_kv, d, max_seq_len, split_tokens, dev)
+    out = torch.empty((batch, n_q, d), dtype=out_dtype, device=dev) if out is None else out
+    meter = torch.empty((batch, n_q), dtype=torch.float32, device=dev) if meter is None else meter
+    raw = torch.empty((batch, n_q), dtype=torch.float32, device=dev) if raw is None else raw
+    meter_v = torch.empty((batch, n_q), dtype=torch.float32, device=dev) if meter_v is None else meter_v
+    mask_q = torch.empty((batch, n_q), dtype=torch.uint8, device=dev) if mask_q is None else mask_q
+    mask_kv = torch.empty((batch, cache.n_kv), dtype=torch.uint8, device=dev) if mask_kv is None else mask_kv
+    c = cache.struct()
+    check(lib().wc_joint_decode_gate(
+        ctypes.byref(c), _ptr(q), _dt(q), batch, n_q, _ptr(block_table), block_table.shape[1],
+        _ptr(seq_lens), max_seq_len, float(sm_scale), _ptr(out), _dt(out), _ptr(meter), _ptr(raw),
+        _ptr(meter_v), split_tokens, float(delta_loc), float(tau), float(tau_v), _ptr(mask_q),
+        _ptr(mask_kv), _ptr(n_gated), _ptr(ws), ws.numel(), _stream()), "wc_joint_decode_gate")
+    return out, meter, raw, meter_v, mask_q, mask_kv
 
 
 def gate(meter: torch.Tensor, raw: torch.Tensor, group: int, tau: float,

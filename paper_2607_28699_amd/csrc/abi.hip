@@ -36,6 +36,10 @@ int check_cache(const wc_cache* c, bool need_witness, bool witness_optional = fa
       return WC_EINVAL;
     if (!c->outlier_pairs || !c->k_outlier || !aligned16(c->k_outlier)) return WC_EINVAL;
   }
+  if ((c->v_resid != nullptr) != (c->v_norm != nullptr)) return WC_EINVAL;   // value side: both or neither
+  if (c->v_resid != nullptr &&
+      (c->kind == WC_KIND_BF16 || !aligned16(c->v_resid) || !aligned16(c->v_norm)))
+    return WC_EINVAL;
   return WC_OK;
 }
 
@@ -59,21 +63,23 @@ const char* wc_strerror(int status) {
 int wc_version(void) { return 100; }
 
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim, int n_bands,
-                      int n_outlier_pairs, size_t sizes[6]) {
+                      int n_outlier_pairs, int value_side, size_t sizes[8]) {
   if (kind < WC_KIND_INT8_DITHER || kind > WC_KIND_BF16 || num_blocks < 0 || n_kv_heads < 1 ||
       head_dim < 1 || (kind != WC_KIND_BF16 && n_bands < 1))
     return 0;
   if (n_outlier_pairs < 0 || n_outlier_pairs > 16 || (n_outlier_pairs & 1) ||
       2 * n_outlier_pairs > head_dim || (n_outlier_pairs && kind != WC_KIND_INT8_DITHER))
     return 0;
+  if (value_side && kind == WC_KIND_BF16) return 0;
   const size_t slots = (size_t)num_blocks * WC_BLOCK_TOKENS * (size_t)n_kv_heads;
-  size_t s[6];
+  size_t s[8];
   s[0] = s[1] = slots * head_dim * elem_bytes(kind);
   s[2] = s[3] = kind == WC_KIND_INT8_DITHER ? slots * 2 : 0;
   s[4] = kind == WC_KIND_BF16 ? 0 : slots * n_bands * 2;
   s[5] = slots * (size_t)n_outlier_pairs * 4;   // 2m fp16 values per token-head
+  s[6] = s[7] = value_side ? slots * 2 : 0;     // value residual, value norm
   if (sizes) memcpy(sizes, s, sizeof(s));
-  return s[0] + s[1] + s[2] + s[3] + s[4] + s[5];
+  return s[0] + s[1] + s[2] + s[3] + s[4] + s[5] + s[6] + s[7];
 }
 
 static int write_common(const wc_cache* cache, const wc_cache* exact, const void* k, const void* v,
@@ -115,6 +121,8 @@ static int write_common(const wc_cache* cache, const wc_cache* exact, const void
   a.n_pairs = cache->n_outlier_pairs;
   a.pairs = cache->outlier_pairs;
   a.k_outlier = static_cast<uint16_t*>(cache->k_outlier);
+  a.v_resid = static_cast<uint16_t*>(cache->v_resid);
+  a.v_norm = static_cast<uint16_t*>(cache->v_norm);
   return hip_status(wc::launch_quantize_write(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -237,6 +245,8 @@ static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int 
   a.n_pairs = cache->n_outlier_pairs;
   a.pairs = cache->outlier_pairs;
   a.k_outlier = static_cast<const uint16_t*>(cache->k_outlier);
+  a.v_resid = static_cast<const uint16_t*>(cache->v_resid);
+  a.v_norm = static_cast<const uint16_t*>(cache->v_norm);
   // WITCERT_FORCE_VALU=1 selects the vector-ALU kernels even where the
   // matrix-core ones apply (used to cross-check the two paths)
   const char* force = getenv("WITCERT_FORCE_VALU");
@@ -305,6 +315,36 @@ int wc_metered_decode_gate(const wc_cache* cache, const void* q, int q_dtype, in
   a.gate_mask_kv = mask_kv;
   a.gate_count = n_gated;
   a.gate_tau = tau;
+  return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
+}
+
+int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int batch,
+                         int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                         const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out,
+                         int out_dtype, float* meter, float* raw, float* meter_v, int split_tokens,
+                         float delta_loc, float tau, float tau_v, uint8_t* mask_q, uint8_t* mask_kv,
+                         int32_t* n_gated, void* ws, size_t ws_bytes, void* stream) {
+  const bool tierb = delta_loc != 0.0f;
+  int s = check_cache(cache, !tierb, tierb);   // Tier B reads no witness
+  if (s != WC_OK) return s;
+  if (cache->kind == WC_KIND_BF16 || !cache->v_resid) return WC_EINVAL;
+  if (tierb && (cache->kind != WC_KIND_INT8_DITHER || !(delta_loc > 0.0f && delta_loc < 1.0f)))
+    return WC_EINVAL;
+  if (!(tau >= 0.0f) || !(tau_v >= 0.0f)) return WC_EINVAL;
+  if (batch > 0 && (!meter || !meter_v || !mask_q || !mask_kv)) return WC_EINVAL;
+  wc::DecodeArgs a{};
+  s = decode_common(cache, q, q_dtype, batch, n_q_heads, block_table, max_blocks_per_seq,
+                    seq_lens, max_seq_len, sm_scale, out, out_dtype, split_tokens, ws, ws_bytes, a);
+  if (s != WC_OK) return s;
+  a.meter = meter;
+  a.raw = raw;
+  a.meter_v = meter_v;
+  a.tierb_delta = tierb ? delta_loc : 0.0f;
+  a.gate_mask_q = mask_q;
+  a.gate_mask_kv = mask_kv;
+  a.gate_count = n_gated;
+  a.gate_tau = tau;
+  a.gate_tau_v = tau_v;
   return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
 }
 

@@ -114,6 +114,7 @@ struct PageRegs {
   uint2 ks, vs;      // fp16 scales of tokens 4g..4g+3
   uint4 wit;         // witness bands 8(g%2).. of token r (garbage where 8(g%2) >= n_bands)
   uint4 ov;          // fp16 keys of bypassed pairs: values 8g .. 8g+7 of token r (when 8g < 2m)
+  uint2 vr, vn;      // value side: stored ||vhat - v|| and ||v|| of tokens 4g..4g+3
   int blk;           // cache block of the page (wave-uniform)
 };
 
@@ -131,7 +132,7 @@ __device__ __forceinline__ uint2 bload8(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
 
-template <int KIND, bool METER, bool TB, bool BYP>
+template <int KIND, bool METER, bool TB, bool BYP, bool VM>
 __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool valid, int kv, int r,
                                           int g, int wit_off, PageRegs<KIND>& p) {
   constexpr int KB = KIND == WC_KIND_BF16 ? 64 : 32;   // bytes per lane and tensor
@@ -164,6 +165,11 @@ __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool val
     p.ov = bload16(page_rsrc(a.k_outlier + page * (2 * a.n_pairs * kBlockTokens), valid ? ob : 0),
                    r * 4 * a.n_pairs + 16 * g);
   }
+  if constexpr (VM) {
+    const int sb = valid ? 2 * kBlockTokens : 0;
+    p.vr = bload8(page_rsrc(a.v_resid + page * kBlockTokens, sb), 8 * g);
+    p.vn = bload8(page_rsrc(a.v_norm + page * kBlockTokens, sb), 8 * g);
+  }
 }
 
 // Running state of one wave.  Logits are kept in log2 units; every weight carries
@@ -172,6 +178,7 @@ __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool val
 struct WaveState {
   f4_t o1[8], o2[8];
   float m, l, n, wsum;   // running max (log2 units), sum of weights, meter numerator, sum of fp16 weights
+  float ev, vmax;        // value side: sum of weights x stored ||vhat - v||, largest stored ||v||
 };
 
 // Per-wave constants of the page loop.
@@ -224,7 +231,7 @@ __device__ __forceinline__ uint32_t dpp_from_upper8(uint32_t v) {
 }
 
 // One 16-token page.  FULL: every token of the page is below t_end (no masking).
-template <int KIND, bool METER, bool FULL, bool HALF, bool TB, bool BYP>
+template <int KIND, bool METER, bool FULL, bool HALF, bool TB, bool BYP, bool VM>
 __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs<KIND>& cur, int t0,
                                              int t_end, int r, int g, const WaveConst& wc,
                                              uint8_t* my_dsh, WaveState& st) {
@@ -334,6 +341,9 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   }
   const h2_t ksh[2] = {as_h2(ksw0), as_h2(ksw1)};
   const h2_t vsh[2] = {as_h2(vsw0), as_h2(vsw1)};
+  // value side: this lane's tokens' stored residual and value norms
+  const h2_t vrh[2] = {as_h2(HALF && upper ? cur.vr.y : cur.vr.x), as_h2(cur.vr.y)};
+  const h2_t vnh[2] = {as_h2(HALF && upper ? cur.vn.y : cur.vn.x), as_h2(cur.vn.y)};
   if constexpr (TB) {
     // Tier B (Sec. 4.2): the radius u_t = (alpha_h + beta_h) s_t from the stored
     // key scale of each of this lane's tokens, in log2 units
@@ -366,6 +376,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     st.l *= alpha;
     st.n *= alpha;
     st.wsum *= alpha;
+    if constexpr (VM) st.ev *= alpha;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       st.o1[j] *= alpha;
@@ -379,6 +390,11 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     const float x = lg[e] - mo;
     const float p = exp2_fast(x);                    // 2^8 softmax weight; 0 for masked tokens
     st.l += p;
+    if constexpr (VM) {
+      // (a masked token's stored bytes may be anything: leave them out)
+      st.ev += valid[e] ? p * (float)vrh[e >> 1][e & 1] : 0.0f;
+      st.vmax = fmaxf(st.vmax, valid[e] ? (float)vnh[e >> 1][e & 1] : 0.0f);
+    }
     if constexpr (METER) {
       // p (e^c - 1): Taylor series for c <= 1/2; above, 2^(x + c) - p, which
       // also counts a token whose weight underflows with its bound
@@ -467,12 +483,12 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   }
 }
 
-template <int KIND, bool METER, bool HALF, bool TB, bool BYP>
+template <int KIND, bool METER, bool HALF, bool TB, bool BYP, bool VM>
 __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
   __shared__ float qn_s[kWaves][16][16];
   __shared__ __attribute__((aligned(16))) float acc_s[kWaves][16][kD];
-  __shared__ float ml_s[kWaves][16][3];
+  __shared__ float ml_s[kWaves][16][5];
   __shared__ uint4 q_lds[16][17];   // the workgroup's queries, bf16 rows of 256 bytes (+16 pad)
 
   // the wave index is uniform: page addresses then live in scalar registers
@@ -533,9 +549,9 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     nc = min(64, np - c0);
     if (c0 == 0 && pg0 == pg_spec && nc <= nc_spec) tv = tv_spec;   // the early request holds them
     else tv = lane < nc ? trow[pg0 + c0 + lane] : 0;
-    load_page<KIND, METER, TB, BYP>(a, blk_at(0), true, kv, r, g, wit_off, p0);
+    load_page<KIND, METER, TB, BYP, VM>(a, blk_at(0), true, kv, r, g, wit_off, p0);
     __builtin_amdgcn_sched_barrier(0);
-    load_page<KIND, METER, TB, BYP>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
+    load_page<KIND, METER, TB, BYP, VM>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
     __builtin_amdgcn_sched_barrier(0);
   };
   if (np > 0) start_chunk(0);
@@ -717,6 +733,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   }
   st.m = -INFINITY;
   st.l = st.n = st.wsum = 0.0f;
+  st.ev = st.vmax = 0.0f;
   uint8_t* my_dsh = dsh[KIND == WC_KIND_INT8_DITHER ? wave : 0];
 
   // Two workgroups share each SIMD, and instruction issue favours the older
@@ -736,17 +753,17 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     // assume the ring order may differ on the back edge and wait for every page.
     for (int j = 0; j < nc; j += 3) {
       set_priority(c0 + j);
-      load_page<KIND, METER, TB, BYP>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
+      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
       __builtin_amdgcn_sched_barrier(0);
-      process_page<KIND, METER, true, HALF, TB, BYP>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
-      load_page<KIND, METER, TB, BYP>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
+      process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 1 < nc)
-        process_page<KIND, METER, true, HALF, TB, BYP>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
-      load_page<KIND, METER, TB, BYP>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
+        process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 2 < nc)
-        process_page<KIND, METER, true, HALF, TB, BYP>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+        process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
     }
     c0 += 64;
     if (c0 < np) start_chunk(c0);
@@ -754,8 +771,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __builtin_amdgcn_s_setprio(0);
   const int t_last = t_begin + np * kBlockTokens;
   if (t_last < t_end) {   // a partial last page: tokens from t_end on are masked
-    load_page<KIND, METER, TB, BYP>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
-    process_page<KIND, METER, false, HALF, TB, BYP>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
+    load_page<KIND, METER, TB, BYP, VM>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
+    process_page<KIND, METER, false, HALF, TB, BYP, VM>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
   }
 
   // ---- merge the four waves of the workgroup, write one partial record ----
@@ -763,6 +780,16 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     st.l += __shfl_xor(st.l, 8, 64);
     if constexpr (METER) st.n += __shfl_xor(st.n, 8, 64);
     if constexpr (KIND == WC_KIND_INT8_DITHER) st.wsum += __shfl_xor(st.wsum, 8, 64);
+    if constexpr (VM) {
+      st.ev += __shfl_xor(st.ev, 8, 64);
+      st.vmax = fmaxf(st.vmax, __shfl_xor(st.vmax, 8, 64));
+    }
+  }
+  if constexpr (VM) {
+    st.ev += __shfl_xor(st.ev, 16, 64);
+    st.ev += __shfl_xor(st.ev, 32, 64);
+    st.vmax = fmaxf(st.vmax, __shfl_xor(st.vmax, 16, 64));
+    st.vmax = fmaxf(st.vmax, __shfl_xor(st.vmax, 32, 64));
   }
   st.l += __shfl_xor(st.l, 16, 64);
   st.l += __shfl_xor(st.l, 32, 64);
@@ -795,6 +822,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     ml_s[wave][r][0] = st.m;     // -inf for a wave without tokens
     ml_s[wave][r][1] = st.l;
     ml_s[wave][r][2] = st.n;
+    ml_s[wave][r][3] = st.ev;
+    ml_s[wave][r][4] = st.vmax;
   }
   __syncthreads();
   const int64_t R = (int64_t)partial_record_floats(kD);
@@ -802,13 +831,17 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) M = fmaxf(M, ml_s[w][r][0]);
-    float f[kWaves], lsum = 0.0f, nsum = 0.0f;
+    float f[kWaves], lsum = 0.0f, nsum = 0.0f, esum = 0.0f, vmax = 0.0f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
       const float mw = ml_s[w][r][0];
       f[w] = mw == -INFINITY ? 0.0f : exp2_fast(mw - M);
       lsum = fmaf(f[w], ml_s[w][r][1], lsum);
       if constexpr (METER) nsum = fmaf(f[w], ml_s[w][r][2], nsum);
+      if constexpr (VM) {
+        esum = fmaf(f[w], ml_s[w][r][3], esum);
+        vmax = fmaxf(vmax, ml_s[w][r][4]);
+      }
     }
     if (isnan(nsum)) nsum = INFINITY;
     float* rec = a.part + (((int64_t)b * a.n_q + (int64_t)kv * G + r) * a.n_splits + blockIdx.x) * R;
@@ -829,6 +862,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       rec[kD] = M * kLn2;   // records hold the max in natural-log units
       rec[kD + 1] = lsum;
       rec[kD + 2] = nsum;
+      rec[kD + 3] = esum;
+      rec[kD + 4] = vmax;
     }
   }
 
@@ -841,21 +876,23 @@ bool mfma_decode_supported(const DecodeArgs& a) {
          (a.kind == WC_KIND_BF16 || a.n_bands == 8 || a.n_bands == 16);
 }
 
-template <bool HALF>
+template <bool HALF, bool VM>
 void launch_decode_mfma_g(const DecodeArgs& a, bool metered, bool tb, bool byp, const dim3& grid,
                           const dim3& block, hipStream_t st) {
-  if (!metered)
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, HALF, false, false>), grid, block, 0, st, a);
-  else if (a.kind == WC_KIND_FP8_RAW)
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, HALF, false, false>), grid, block, 0, st, a);
-  else if (tb && byp)
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, true>), grid, block, 0, st, a);
-  else if (tb)
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, false>), grid, block, 0, st, a);
-  else if (byp)
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, true>), grid, block, 0, st, a);
-  else
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, false>), grid, block, 0, st, a);
+  if (!metered) {
+    if constexpr (!VM)
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, HALF, false, false, false>), grid, block, 0, st, a);
+  } else if (a.kind == WC_KIND_FP8_RAW) {
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, HALF, false, false, VM>), grid, block, 0, st, a);
+  } else if (tb && byp) {
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, true, VM>), grid, block, 0, st, a);
+  } else if (tb) {
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, false, VM>), grid, block, 0, st, a);
+  } else if (byp) {
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, true, VM>), grid, block, 0, st, a);
+  } else {
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, false, VM>), grid, block, 0, st, a);
+  }
 }
 
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st) {
@@ -863,8 +900,14 @@ hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st)
   const dim3 block(64 * kWaves);
   const bool tb = metered && a.tierb_delta > 0.0f;   // Tier B: INT8 dithered cache only
   const bool byp = metered && a.n_pairs > 0;        // bypassed pairs: INT8 keys only
-  if (a.group <= 8) launch_decode_mfma_g<true>(a, metered, tb, byp, grid, block, st);
-  else launch_decode_mfma_g<false>(a, metered, tb, byp, grid, block, st);
+  const bool vm = metered && a.meter_v != nullptr;    // value side
+  if (a.group <= 8) {
+    if (vm) launch_decode_mfma_g<true, true>(a, metered, tb, byp, grid, block, st);
+    else launch_decode_mfma_g<true, false>(a, metered, tb, byp, grid, block, st);
+  } else {
+    if (vm) launch_decode_mfma_g<false, true>(a, metered, tb, byp, grid, block, st);
+    else launch_decode_mfma_g<false, false>(a, metered, tb, byp, grid, block, st);
+  }
   return hipGetLastError();
 }
 

@@ -46,6 +46,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   __shared__ float pw_s[kGMax][kT];
   __shared__ uint32_t xi_s[kT][D / 4];
   __shared__ float vs_s[kT];
+  __shared__ float vr_s[kT], vn_s[kT];   // value side: stored ||vhat - v|| and ||v|| of the tile
   __shared__ float alpha_s[kGMax];
   __shared__ int64_t slot_s[kT];
 
@@ -112,12 +113,14 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
     }
   }
 
-  float m_run[4], l_run[4], n_run[4];
+  const bool vm = METER && a.meter_v != nullptr;   // value side
+  float m_run[4], l_run[4], n_run[4], e_run[4], vmax_run = 0.0f;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     m_run[k] = -INFINITY;
     l_run[k] = 0.0f;
     n_run[k] = 0.0f;
+    e_run[k] = 0.0f;
   }
   const int c3 = tid % D, hs = tid / D;
   float acc[HPT];
@@ -197,6 +200,10 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
       } else if (part == 0) {
         vs_s[i] = 0.0f;
       }
+      if (vm && part == 0) {
+        vr_s[i] = valid ? f16_to_f32(a.v_resid[page * kBlockTokens + off]) : 0.0f;
+        vn_s[i] = valid ? f16_to_f32(a.v_norm[page * kBlockTokens + off]) : 0.0f;
+      }
       // stored fp16 values of the bypassed pairs: positions part, part + 4, ...
       float kov[8];
 #pragma unroll
@@ -273,6 +280,10 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
           const float nn = fmaf(alpha, n_run[k], wave_sum(term));
           n_run[k] = isnan(nn) ? INFINITY : nn;
         }
+        if (vm) {
+          e_run[k] = fmaf(alpha, e_run[k], wave_sum(p * vr_s[lane]));
+          vmax_run = fmaxf(vmax_run, wave_max(vn_s[lane]));
+        }
         m_run[k] = m_new;
         pw_s[h][lane] = p * vs_s[lane];
         if (lane == 0) alpha_s[h] = alpha;
@@ -347,6 +358,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         rec[D] = m_run[k];
         rec[D + 1] = l_run[k];
         rec[D + 2] = n_run[k];
+        rec[D + 3] = e_run[k];
+        rec[D + 4] = vmax_run;
       }
     }
   }
@@ -367,10 +380,10 @@ constexpr int kMergeThreads = 64 * kMergeWaves;
 // of all 32 partial outputs; all of a chunk's loads are issued together, and the
 // split weights reach the channel lanes through readlane.  The waves' running
 // states are combined in LDS at the end.
-template <int D, bool METER>
+template <int D, bool METER, bool VM>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
   constexpr int C = D / 64;   // channels per lane
-  __shared__ float st_s[kMergeWaves][3];
+  __shared__ float st_s[kMergeWaves][5];
   __shared__ float acc_s[kMergeWaves][D];
   const int bh = blockIdx.x;
   const int b = bh / a.n_q, h = bh % a.n_q;
@@ -380,7 +393,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
   const float* rec0 = a.part + (int64_t)bh * a.n_splits * R;
   const int jl = lane & 31;
 
-  float M = -INFINITY, lsum = 0.0f, nsum = 0.0f, acc[C];
+  float M = -INFINITY, lsum = 0.0f, nsum = 0.0f, esum = 0.0f, vmax = 0.0f, acc[C];
 #pragma unroll
   for (int c = 0; c < C; ++c) acc[c] = 0.0f;
   // The records of a chunk are requested before the sequence length is known;
@@ -389,6 +402,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
   for (int j0 = 32 * wave; j0 < a.n_splits; j0 += 32 * kMergeWaves) {
     const int nr = min(32, a.n_splits - j0);    // records that exist in the workspace
     const float4 t = *reinterpret_cast<const float4*>(rec0 + (int64_t)(j0 + min(jl, nr - 1)) * R + D);
+    const float tv = VM ? rec0[(int64_t)(j0 + min(jl, nr - 1)) * R + D + 4] : 0.0f;
     float ov[32][C];
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
@@ -415,14 +429,23 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
     const float alpha = M == -INFINITY ? 0.0f : __expf(M - Mn);
     const float ej = mj == -INFINITY ? 0.0f : __expf(mj - Mn);
     float dl = jl < nj ? ej * t.y : 0.0f, dn = METER && jl < nj ? ej * t.z : 0.0f;
+    float de = VM && jl < nj ? ej * t.w : 0.0f, dv = VM && jl < nj ? tv : 0.0f;
 #pragma unroll
     for (int o = 1; o < 32; o <<= 1) {
       dl += __shfl_xor(dl, o, 64);
       if constexpr (METER) dn += __shfl_xor(dn, o, 64);
+      if constexpr (VM) {
+        de += __shfl_xor(de, o, 64);
+        dv = fmaxf(dv, __shfl_xor(dv, o, 64));
+      }
     }
     M = Mn;
     lsum = fmaf(lsum, alpha, dl);
     if constexpr (METER) nsum = fmaf(nsum, alpha, dn);
+    if constexpr (VM) {
+      esum = fmaf(esum, alpha, de);
+      vmax = fmaxf(vmax, dv);
+    }
 #pragma unroll
     for (int c = 0; c < C; ++c) acc[c] *= alpha;
     // (records past the last active split may hold anything, NaN included: skip them)
@@ -443,6 +466,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
     st_s[wave][0] = M;
     st_s[wave][1] = lsum;
     st_s[wave][2] = nsum;
+    st_s[wave][3] = esum;
+    st_s[wave][4] = vmax;
   }
 #pragma unroll
   for (int c = 0; c < C; ++c) acc_s[wave][C * lane + c] = acc[c];
@@ -451,12 +476,16 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
   float Mt = -INFINITY;
 #pragma unroll
   for (int w = 0; w < kMergeWaves; ++w) Mt = fmaxf(Mt, st_s[w][0]);
-  float f[kMergeWaves], lt = 0.0f, nt = 0.0f;
+  float f[kMergeWaves], lt = 0.0f, nt = 0.0f, et = 0.0f, vt = 0.0f;
 #pragma unroll
   for (int w = 0; w < kMergeWaves; ++w) {
     f[w] = st_s[w][0] == -INFINITY ? 0.0f : __expf(st_s[w][0] - Mt);
     lt = fmaf(f[w], st_s[w][1], lt);
     if constexpr (METER) nt = fmaf(f[w], st_s[w][2], nt);
+    if constexpr (VM) {
+      et = fmaf(f[w], st_s[w][3], et);
+      vt = fmaxf(vt, st_s[w][4]);
+    }
   }
 #pragma unroll
   for (int c = 0; c < C; ++c) {
@@ -482,9 +511,18 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
       const float meter = fminf(1.0f, raw);
       a.meter[bh] = meter;
       if (a.raw != nullptr) a.raw[bh] = raw;
+      // value meter: sum_t ptilde_t rho_t over the largest stored value norm (0/0 = 0)
+      float mv = 0.0f;
+      if constexpr (VM) {
+        const float ev = ns > 0 ? et / lt : 0.0f;
+        mv = vt > 0.0f ? ev / vt : (ev > 0.0f ? INFINITY : 0.0f);
+        if (isnan(mv)) mv = INFINITY;
+        a.meter_v[bh] = mv;
+      }
       if (a.gate_mask_q != nullptr) {
-        // the gate of this query head; its KV head is counted by the first gated head
-        const bool gated = (a.gate_tau >= 1.0f ? raw : meter) > a.gate_tau;
+        // the gate of this query head (the joint one: pass_K and pass_V); its KV
+        // head is counted by the first gated head
+        const bool gated = (a.gate_tau >= 1.0f ? raw : meter) > a.gate_tau || (VM && mv > a.gate_tau_v);
         a.gate_mask_q[bh] = gated ? 1 : 0;
         if (gated) {
           const int unit = b * a.n_kv + h / a.group;
@@ -537,14 +575,17 @@ int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested)
   return (int)st;
 }
 
+template <int D>
+void launch_merge_d(const DecodeArgs& a, bool metered, hipStream_t st) {
+  const dim3 grid(a.batch * a.n_q), block(kMergeThreads);
+  if (!metered) hipLaunchKernelGGL((merge_kernel<D, false, false>), grid, block, 0, st, a);
+  else if (a.meter_v != nullptr) hipLaunchKernelGGL((merge_kernel<D, true, true>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((merge_kernel<D, true, false>), grid, block, 0, st, a);
+}
+
 hipError_t launch_merge(const DecodeArgs& a, bool metered, hipStream_t st) {
-  if (a.head_dim == 64) {
-    if (metered) hipLaunchKernelGGL((merge_kernel<64, true>), dim3(a.batch * a.n_q), dim3(kMergeThreads), 0, st, a);
-    else hipLaunchKernelGGL((merge_kernel<64, false>), dim3(a.batch * a.n_q), dim3(kMergeThreads), 0, st, a);
-  } else {
-    if (metered) hipLaunchKernelGGL((merge_kernel<128, true>), dim3(a.batch * a.n_q), dim3(kMergeThreads), 0, st, a);
-    else hipLaunchKernelGGL((merge_kernel<128, false>), dim3(a.batch * a.n_q), dim3(kMergeThreads), 0, st, a);
-  }
+  if (a.head_dim == 64) launch_merge_d<64>(a, metered, st);
+  else launch_merge_d<128>(a, metered, st);
   return hipGetLastError();
 }
 

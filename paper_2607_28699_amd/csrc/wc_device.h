@@ -81,6 +81,15 @@ __device__ __forceinline__ uint16_t f16_round_up_f64(double d) {
   return b;
 }
 
+// Largest fp16 value <= d (d finite, >= 0; 65504 above the range): nearest-even
+// conversion, then one step down if that landed above d.
+__device__ __forceinline__ uint16_t f16_round_down_f64(double d) {
+  const _Float16 h = (_Float16)d;
+  uint16_t b = f16_bits(h);
+  if ((double)h > d) b -= 1;
+  return b;
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __builtin_bit_cast(float, (uint32_t)b << 16);
 }

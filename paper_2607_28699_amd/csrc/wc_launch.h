@@ -25,6 +25,8 @@ struct WriteArgs {
   int n_pairs;              // bypassed RoPE pairs per KV head (0: none)
   const int32_t* pairs;     // [n_kv][n_pairs]
   uint16_t* k_outlier;      // [blocks][n_kv][16][2 n_pairs] fp16
+  uint16_t* v_resid;        // value side (or null): ||vhat - v|| fp16 up, [blocks][n_kv][16]
+  uint16_t* v_norm;         // ||v|| fp16 down, same layout
 };
 
 struct SelectArgs {
@@ -55,7 +57,7 @@ struct DecodeArgs {
   const int32_t* table;
   const int32_t* seq_lens;
   const uint8_t* mask_kv;   // exact fallback: only routed (b, kv) units run
-  float* part;              // partial records [batch][n_q][n_splits][D + 4]
+  float* part;              // partial records [batch][n_q][n_splits][D + 8]
   void* out;
   float* meter;
   float* raw;
@@ -74,6 +76,12 @@ struct DecodeArgs {
   int n_pairs;              // bypassed RoPE pairs per KV head (0: none)
   const int32_t* pairs;     // [n_kv][n_pairs]
   const uint16_t* k_outlier;  // [blocks][n_kv][16][2 n_pairs] fp16
+  // value side (null meter_v: off): stored ||vhat - v|| (up) and ||v|| (down), the
+  // value meter out, and its threshold in the joint gate
+  const uint16_t* v_resid;
+  const uint16_t* v_norm;
+  float* meter_v;           // [batch][n_q]
+  float gate_tau_v;
 };
 
 // Channel of member `second` of RoPE pair j (pair index clamped into range).
@@ -115,7 +123,11 @@ int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested)
 inline int64_t n_splits_for(int64_t max_seq_len, int split_tokens) {
   return max_seq_len <= 0 ? 1 : (max_seq_len + split_tokens - 1) / split_tokens;
 }
-__host__ __device__ inline size_t partial_record_floats(int head_dim) { return (size_t)head_dim + 4; }
+// Partial record of one (query head, split): head_dim output floats, then the
+// running max (natural log units), weight sum, meter numerator, value-side
+// numerator sum p rho, the largest stored value norm, and three spare floats (the
+// record stays a multiple of 16 bytes).
+__host__ __device__ inline size_t partial_record_floats(int head_dim) { return (size_t)head_dim + 8; }
 // Workspace: the partial records, then one int32 per (sequence, KV head) for the
 // fused gate; each part rounded up to 256 bytes.
 inline size_t records_bytes(int batch, int n_q, int64_t n_splits, int head_dim) {

@@ -102,6 +102,7 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
   const int64_t bh = blk * a.n_kv + h;        // (block, head) page index
   if (g == 0) slot_s[lth] = slot;
 
+  double vr2 = 0.0, vn2 = 0.0;   // value side: ||vhat - v||^2 and ||v||^2 of this lane's channels
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
     // Bypassed key channels of this lane (outlier RoPE pairs, Sec. 6.2): out of the
     // amax, code 0, value kept in fp16 (bit i: channel 16g + i).
@@ -144,6 +145,9 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
       const double rk = byp ? (double)(float)(_Float16)k[i] - (double)k[i]     // fp16(k) - k
                             : (double)sk * (double)(ck - xi) - (double)k[i];   // khat - k
       r2[lth][16 * g + i] = rk * rk;
+      const double rv = (double)sv * (double)(cv - xi) - (double)v[i];         // vhat - v
+      vr2 = fma(rv, rv, vr2);
+      vn2 = fma((double)v[i], (double)v[i], vn2);
       // codes are stored excess-128: byte = code + 128
       kc[i >> 2] |= ((uint32_t)((int32_t)ck + 128) & 0xFFu) << (8 * (i & 3));
       if (active) {
@@ -186,6 +190,9 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
       const uint32_t bv = f32_to_e4m3_sat(v[i]);
       const double rk = (double)e4m3_to_f32(bk) - (double)k[i];
       r2[lth][16 * g + i] = rk * rk;
+      const double rv = (double)e4m3_to_f32(bv) - (double)v[i];
+      vr2 = fma(rv, rv, vr2);
+      vn2 = fma((double)v[i], (double)v[i], vn2);
       kc[i >> 2] |= bk << (8 * (i & 3));
       if (active) {
         uint8_t* vd = reinterpret_cast<uint8_t*>(a.v_data) + bh * (kBlockTokens * D) +
@@ -203,6 +210,17 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
     return;
   }
   if (active && a.x_k_data != nullptr) store_exact<D>(a.x_k_data, a.x_v_data, bh, off, g, k, v);
+  if (a.v_resid != nullptr) {   // value side (Sec. 3 output bound): residual norm up, value norm down
+#pragma unroll
+    for (int o = 1; o < LPT; o <<= 1) {
+      vr2 += __shfl_xor(vr2, o, LPT);
+      vn2 += __shfl_xor(vn2, o, LPT);
+    }
+    if (active && g == 0) {
+      a.v_resid[bh * kBlockTokens + off] = f16_round_up_f64(sqrt(vr2));
+      a.v_norm[bh * kBlockTokens + off] = f16_round_down_f64(sqrt(vn2));
+    }
+  }
 
   // ---- witness: band norms of the key residual, rounded up to fp16 ----
   __syncthreads();

@@ -49,9 +49,10 @@ def case_pairs(case, m):
     return np.stack([obp.select_pairs(k[:, h], m, wl.rope_layout) for h in range(wl.n_kv)])
 
 
-def gpu_cache(case, kind, seed=None, pairs=None):
+def gpu_cache(case, kind, seed=None, pairs=None, value_side=False):
     """Write every sequence of the case into a fresh GPU cache through wc_quantize_write
-    (pairs [n_kv, m]: bypassed RoPE pairs of the keys)."""
+    (pairs [n_kv, m]: bypassed RoPE pairs of the keys; value_side: store the value
+    residual and value norms)."""
     import torch
 
     import paper_2607_28699_amd as wc
@@ -59,7 +60,7 @@ def gpu_cache(case, kind, seed=None, pairs=None):
     m = 0 if pairs is None else int(np.asarray(pairs).shape[1])
     c = wc.PagedCache(kind, case["nblocks"], wl.n_kv, wl.d, wl.bands, layer=case["layer"],
                       seed=wl.philox_seed() if seed is None else seed, rope_layout=wl.rope_layout,
-                      n_outlier_pairs=m)
+                      n_outlier_pairs=m, value_side=value_side)
     if m:
         c.set_outlier_pairs(torch.from_numpy(np.asarray(pairs, dtype=np.int32)))
     dt = torch_dtype(wl)
@@ -129,6 +130,9 @@ def read_cache(cache, slots):
         out["kw"] = ofp_f16(t["k_witness"].numpy()[blk, :, off, :])
     if t.get("k_outlier") is not None:
         out["ko"] = ofp_f16(t["k_outlier"].numpy()[blk, :, off, :])
+    if t.get("v_resid") is not None:
+        out["vr"] = ofp_f16(t["v_resid"].numpy()[blk, :, off])
+        out["vn"] = ofp_f16(t["v_norm"].numpy()[blk, :, off])
     return out
 
 

@@ -39,34 +39,38 @@ def test_status_strings_and_version(L):
 
 
 def test_cache_byte_account(L):
-    sizes = (ctypes.c_size_t * 6)()
+    sizes = (ctypes.c_size_t * 8)()
     # one KV head, 32768 tokens, d = 128, B = 8: 128 + 128 + 2 + 2 + 16 = 276 B per token
-    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, sizes)
+    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, 0, sizes)
     assert tot == 32768 * 276
-    assert list(sizes) == [32768 * 128, 32768 * 128, 65536, 65536, 32768 * 16, 0]
-    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, sizes) == 32768 * 272
-    assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, 0, sizes) == 32768 * 512
-    assert L.wc_cache_bytes(7, 1, 1, 128, 8, 0, sizes) == 0
+    assert list(sizes) == [32768 * 128, 32768 * 128, 65536, 65536, 32768 * 16, 0, 0, 0]
+    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, 0, sizes) == 32768 * 272
+    assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, 0, 0, sizes) == 32768 * 512
+    assert L.wc_cache_bytes(7, 1, 1, 128, 8, 0, 0, sizes) == 0
     # bypassed pairs: 2m fp16 values per token and KV head (Table 6: 16 B at m = 4)
     for m in (2, 4, 8, 16):
-        tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, m, sizes)
+        tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, m, 0, sizes)
         assert sizes[5] == 32768 * 4 * m and tot == 32768 * (276 + 4 * m)
     for bad in (-2, 3, 18):
-        assert L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, bad, sizes) == 0
-    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 4, sizes) == 0
+        assert L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, bad, 0, sizes) == 0
+    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 4, 0, sizes) == 0
+    # value side: 2 + 2 bytes per token-head (residual and value norms), quantized kinds only
+    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, 1, sizes)
+    assert tot == 32768 * 280 and sizes[6] == sizes[7] == 65536
+    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, 1, sizes) == 32768 * 276
+    assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, 0, 1, sizes) == 0
 
 
 def test_workspace_size_and_argument_checks(L):
     n = L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 0)
     assert n > 0 and n % 4 == 0
-    # 64 splits of partial records (132 floats each), rounded up to 256 B
-    # partial records (batch, q heads, splits, head_dim + 4 floats), then one int32
+    # partial records (batch, q heads, 64 splits, head_dim + 8 floats), then one int32
     # per (sequence, KV head) for the fused gate; each part rounded up to 256 bytes
-    assert L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 512) == 4 * 28 * 64 * 132 * 4 + 256
+    assert L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 512) == 4 * 28 * 64 * 136 * 4 + 256
     assert L.wc_decode_workspace_size(-1, 28, 4, 128, 100, 0) == 0
     # null cache / pointers are rejected before anything is launched
     assert L.wc_quantize_write(None, None, None, 0, None, 1, None) == _lib.WC_EINVAL
-    c = _lib.WcCache(0, 96, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16, 0, 0, None, None)
+    c = _lib.WcCache(0, 96, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16, 0, 0, None, None, None, None)
     assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EUNSUPPORTED
     c.head_dim = 128
     c.k_data = 8                              # misaligned
@@ -89,6 +93,14 @@ def test_workspace_size_and_argument_checks(L):
     c.kind = _lib.WC_KIND_INT8_DITHER
     c.k_outlier = 24                          # misaligned
     assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
+    c.k_outlier, c.n_outlier_pairs, c.outlier_pairs = None, 0, None
+    # value side: both arrays or neither; the joint decode needs it
+    c.v_resid = 16
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
+    c.v_resid = None
+    st = L.wc_joint_decode_gate(ctypes.byref(c), 16, 1, 1, 7, 16, 4, 16, 64, 0.1, 16, 0, 16, 16, 16,
+                                0, 0.0, 0.2, 0.05, 16, 16, None, 16, 1 << 20, None)
+    assert st == _lib.WC_EINVAL
     # pair selection: m within the pairs, head_dim 64 / 128, n_tok >= 1, a workspace of
     # float64 partial energies per (KV head, chunk of 2048 rows, pair), up to 64 chunks
     assert L.wc_select_workspace_size(131072, 4, 128) == 4 * 64 * 64 * 8
