@@ -49,6 +49,7 @@ def parse():
     ap.add_argument("--tau", type=float, default=0.2)
     ap.add_argument("--outlier-pairs", type=int, default=4,
                     help="bypassed RoPE pairs per KV head for the bypass measurement (0: skip it)")
+    ap.add_argument("--tau-v", type=float, default=0.05, help="value-side threshold of the joint gate")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -179,7 +180,7 @@ def main():
             wc.quantize_write(e, k, v, sl)
         if m_byp:
             cb = wc.PagedCache("int8_dither", lay.nblocks, wl.n_kv, wl.d, wl.bands, layer=layer, seed=seed,
-                               rope_layout=wl.rope_layout, n_outlier_pairs=m_byp)
+                               rope_layout=wl.rope_layout, n_outlier_pairs=m_byp, value_side=True)
             cb.set_outlier_pairs(wc.select_outlier_pairs(torch.cat([k for k, _, _ in gen]), m_byp,
                                                          wl.rope_layout))
             for k, v, sl in gen:
@@ -374,6 +375,35 @@ def main():
                          "gate_fraction_q_heads": round(gq_ / (n_cells * wl.n_q), 4),
                          "gate_fraction_kv_heads": round(gkv_ / (n_cells * wl.n_kv), 4)}
         del kcat
+
+        # joint key + value certificate with its gate (Sec. 4.2 joint event) over the
+        # same caches, Tier B keys at the same budget: the paper's deployment form
+        mv = torch.empty_like(meter)
+        jt_ms = timed(lambda i: wc.joint_decode_gate(
+            byp_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
+            max_len_all, sm, args.tau, args.tau_v, dloc, ws=ws, out=out, meter=meter, raw=raw, meter_v=mv,
+            mask_q=mask_q, mask_kv=mask_kv), reps)
+        cj = torch.zeros(2, dtype=torch.int32, device=dev)
+        pass_k = pass_v = 0
+        mvs = []
+        for layer in range(wl.n_layers):
+            wc.joint_decode_gate(byp_caches[layer], last["layers"][layer]["q"], table, last["lens"], max_len_all,
+                                 sm, args.tau, args.tau_v, dloc, ws=ws, out=out, meter=meter, raw=raw,
+                                 meter_v=mv, mask_q=mq_b, mask_kv=mkv_b, n_gated=cj)
+            pass_k += int((meter <= args.tau).sum().item())
+            pass_v += int((mv <= args.tau_v).sum().item())
+            mvs.append(mv.clone())
+        gqj, gkvj = cj.cpu().tolist()
+        nbytes = TIERB_BYTES + 4 * m_byp + 4
+        gbps = float(last["tokens"] * wl.n_kv) * nbytes / (float(np.median(jt_ms)) * 1e-3) / 1e9
+        byp["joint"] = {"tier": "B", "tau_k": args.tau, "tau_v": args.tau_v,
+                        "median_launch_ms": round(float(np.median(jt_ms)), 4), "GBps": round(gbps, 1),
+                        "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4), "bytes_per_token_head": nbytes,
+                        "meter_v_median": round(float(torch.cat(mvs).median().item()), 5),
+                        "pass_k_fraction": round(pass_k / (n_cells * wl.n_q), 4),
+                        "pass_v_fraction": round(pass_v / (n_cells * wl.n_q), 4),
+                        "gate_fraction_q_heads": round(gqj / (n_cells * wl.n_q), 4),
+                        "gate_fraction_kv_heads": round(gkvj / (n_cells * wl.n_kv), 4)}
     th_per_launch = float(last["tokens"] * wl.n_kv)
     tb_gbps = th_per_launch * TIERB_BYTES / (float(np.median(tb_ms)) * 1e-3) / 1e9
     dec_gbps = th_per_launch * INT8_BYTES / (float(np.median(dec_ms)) * 1e-3) / 1e9
