@@ -27,6 +27,9 @@ theorem or table) and is written for reading against it, not for speed:
                  Sec. 6.2 fixed-channel bypass, Tables 5 and 6).
 * ``value``      value side: the output bound of Sec. 3, the value meter and the
                  joint K+V gate (Sec. 4.2 value side and joint event).
+* ``repair``     block-granular repair of gated heads (Sec. 6.3, block-level
+                 paging): block shares of A - 1, the repair order, the repaired
+                 state and the stop rule.
 * ``gate``       threshold gate and exact fallback (the meter loop, Sec. 6).
 * ``decode``     one metered decode of a batch over per-token caches, composed
                  from the above.
@@ -34,4 +37,4 @@ theorem or table) and is written for reading against it, not for speed:
 Parity status of each function is listed in its docstring; every function is
 pinned by a CPU test in ``tests/test_oracle_*.py``.
 """
-from . import attention, bypass, decode, fpformats, gate, meter, philox, quantizer, tierb, value  # noqa: F401
+from . import attention, bypass, decode, fpformats, gate, meter, philox, quantizer, repair, tierb, value  # noqa: F401
