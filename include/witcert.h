@@ -23,6 +23,8 @@
  *               wc_exact_decode_attention
  *                                   exact attention from an uncompressed bf16 cache for
  *                                   the routed heads (the fallback of the meter loop)
+ *               wc_block_repair     repair of routed heads from the exact cache at block
+ *                                   granularity (Sec. 6.3)
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are DEVICE pointers owned by the caller; the library
@@ -300,6 +302,35 @@ int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int 
                          int out_dtype, float* meter, float* raw, float* meter_v, int split_tokens,
                          float delta_loc, float tau, float tau_v, uint8_t* mask_q, uint8_t* mask_kv,
                          int32_t* n_gated, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Block-granular repair of routed KV heads (Sec. 6.3, block-level paging; the
+ * meter loop's gate pages in the top-contributing blocks).  Run after a metered
+ * decode call (Tier A, or Tier B with delta_loc > 0) over the same cache, queries,
+ * table, lengths and split_tokens, whose workspace `ws` still holds its partial
+ * records, and whose gate set mask_kv.  For every KV head with mask_kv != 0:
+ *   blocks are the quarters of the decode's KV splits, block i covering tokens
+ *   [i*bs, (i+1)*bs), bs = split_tokens/4 (split_tokens as chosen for the decode:
+ *   0 selects the library's choice for the same sizes);
+ *   share_{h,i} = sum_{t in i} ptilde_{h,t} (e^{c_{h,t}} - 1) (they add up to A_h - 1),
+ *   taken in decreasing order of sum_h share_{h,i} (ties to the lower i), at most
+ *   max_repair_blocks (1 .. 64) of them;
+ *   a taken block contributes exact logits and values (from the bf16 cache `exact`)
+ *   with bound 0; after each block A_h is recomputed, and the repair stops as soon
+ *   as every query head h of the KV head passes: (tau < 1 ? meter : raw) <= tau.
+ * A repaired KV head gets its G outputs, meter and raw rewritten for the repaired
+ * state and its mask_kv cleared (no whole-head fallback needed); otherwise nothing
+ * of it changes.  repaired[b][g][0..max_repair_blocks-1] receives the block order
+ * (-1 padded; may be NULL) and n_repaired[b][g] the number of blocks taken (0: not
+ * routed, -1: the budget did not suffice; may be NULL).  At most 4096 blocks per
+ * sequence.  out must be the decode's output array (out_dtype as there).
+ */
+int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q, int q_dtype,
+                    int batch, int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                    const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, int split_tokens,
+                    float delta_loc, float tau, int max_repair_blocks, const void* ws,
+                    size_t ws_bytes, void* out, int out_dtype, float* meter, float* raw,
+                    uint8_t* mask_kv, int32_t* repaired, int32_t* n_repaired, void* stream);
 
 /*
  * Gate (the meter loop's gate, Sec. 6; certified vs risk-ranked, Sec. 4.3):

@@ -7,6 +7,7 @@ the first call does, and fails loudly if the library is not built.
 """
 from .api import (  # noqa: F401
     KINDS,
+    block_repair,
     LAYOUTS,
     PagedCache,
     cache_bytes,

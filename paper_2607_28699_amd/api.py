@@ -268,6 +268,30 @@ def joint_decode_gate(cache: PagedCache, q: torch.Tensor, block_table: torch.Ten
     return out, meter, raw, meter_v, mask_q, mask_kv
 
 
+def block_repair(cache: PagedCache, exact: PagedCache, q: torch.Tensor, block_table: torch.Tensor,
+                 seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float, tau: float, ws: torch.Tensor,
+                 out: torch.Tensor, meter: torch.Tensor, raw: torch.Tensor, mask_kv: torch.Tensor,
+                 delta_loc: float = 0.0, max_blocks: int = 16, split_tokens: int = 0,
+                 repaired: torch.Tensor | None = None, n_repaired: torch.Tensor | None = None):
+    """Block repair of the KV heads a metered decode (same ws, split_tokens) routed:
+    updates out, meter, raw and mask_kv in place -> (n_repaired [batch, n_kv],
+    repaired [batch, n_kv, max_blocks])."""
+    _dev_check(q, block_table, seq_lens, ws, out, meter, raw, mask_kv)
+    batch, n_q, d = q.shape
+    if n_repaired is None:
+        n_repaired = torch.empty((batch, cache.n_kv), dtype=torch.int32, device=q.device)
+    if repaired is None:
+        repaired = torch.empty((batch, cache.n_kv, max_blocks), dtype=torch.int32, device=q.device)
+    c, e = cache.struct(), exact.struct()
+    check(lib().wc_block_repair(
+        ctypes.byref(c), ctypes.byref(e), _ptr(q), _dt(q), batch, n_q, _ptr(block_table),
+        block_table.shape[1], _ptr(seq_lens), max_seq_len, float(sm_scale), split_tokens,
+        float(delta_loc), float(tau), max_blocks, _ptr(ws), ws.numel(), _ptr(out), _dt(out),
+        _ptr(meter), _ptr(raw), _ptr(mask_kv), _ptr(repaired), _ptr(n_repaired), _stream()),
+        "wc_block_repair")
+    return n_repaired, repaired
+
+
 def gate(meter: torch.Tensor, raw: torch.Tensor, group: int, tau: float,
          n_gated: torch.Tensor | None = None, mask_q=None, mask_kv=None):
     """-> (mask_q [batch, n_q] uint8, mask_kv [batch, n_kv] uint8)."""

@@ -348,6 +348,48 @@ int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int 
   return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
 }
 
+int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q, int q_dtype,
+                    int batch, int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                    const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, int split_tokens,
+                    float delta_loc, float tau, int max_repair_blocks, const void* ws,
+                    size_t ws_bytes, void* out, int out_dtype, float* meter, float* raw,
+                    uint8_t* mask_kv, int32_t* repaired, int32_t* n_repaired, void* stream) {
+  const bool tierb = delta_loc != 0.0f;
+  int s = check_cache(cache, !tierb, tierb);
+  if (s != WC_OK) return s;
+  s = check_cache(exact, false);
+  if (s != WC_OK) return s;
+  if (cache->kind == WC_KIND_BF16 || exact->kind != WC_KIND_BF16 || exact->head_dim != cache->head_dim ||
+      exact->n_kv_heads != cache->n_kv_heads || exact->num_blocks < cache->num_blocks)
+    return WC_EINVAL;
+  if (tierb && (cache->kind != WC_KIND_INT8_DITHER || !(delta_loc > 0.0f && delta_loc < 1.0f)))
+    return WC_EINVAL;
+  if (!(tau >= 0.0f) || max_repair_blocks < 1 || max_repair_blocks > 64) return WC_EINVAL;
+  if (batch > 0 && (!meter || !mask_kv)) return WC_EINVAL;
+  wc::DecodeArgs a{};
+  s = decode_common(cache, q, q_dtype, batch, n_q_heads, block_table, max_blocks_per_seq,
+                    seq_lens, max_seq_len, sm_scale, out, out_dtype, split_tokens,
+                    const_cast<void*>(ws), ws_bytes, a);   // the records are only read
+  if (s != WC_OK) return s;
+  if ((max_seq_len + a.split_tokens / 4 - 1) / (a.split_tokens / 4) > wc::repair_max_blocks())
+    return WC_EUNSUPPORTED;
+  if (batch == 0) return WC_OK;
+  a.meter = meter;
+  a.raw = raw;
+  a.mask_kv = mask_kv;
+  a.tierb_delta = tierb ? delta_loc : 0.0f;
+  wc::RepairArgs r{};
+  r.d = a;
+  r.x_k_data = exact->k_data;
+  r.x_v_data = exact->v_data;
+  r.tau = tau;
+  r.max_rep = max_repair_blocks;
+  r.mask_kv_out = mask_kv;
+  r.rep_list = repaired;
+  r.n_rep = n_repaired;
+  return hip_status(wc::launch_repair(r, static_cast<hipStream_t>(stream)));
+}
+
 int wc_gate(const float* meter, const float* raw, int batch, int n_q_heads, int group, float tau,
             uint8_t* mask_q, uint8_t* mask_kv, int32_t* n_gated, void* stream) {
   if (batch < 0 || n_q_heads < 1 || group < 1 || n_q_heads % group || !(tau >= 0.0f)) return WC_EINVAL;

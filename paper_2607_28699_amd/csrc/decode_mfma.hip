@@ -526,10 +526,11 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   const bool unrouted = a.mask_kv != nullptr && a.mask_kv[unit] == 0;
   if (unrouted | (blockIdx.x >= a.n_splits) | (wg_begin >= L)) return;
   const int wg_end = min(min(L, wg_begin + a.split_tokens), a.max_blocks * kBlockTokens);
-  // this wave's share: a contiguous run of pages of the workgroup's split
-  const int n_pages = (wg_end - wg_begin + kBlockTokens - 1) / kBlockTokens;
-  const int ppw = (n_pages + kWaves - 1) / kWaves;
-  const int t_begin = wg_begin + wave * ppw * kBlockTokens;
+  // this wave's share: a quarter of the split (split_tokens / 4 tokens, a whole
+  // number of pages), also in a sequence's last split, so that the wave ranges are
+  // the fixed blocks whose meter shares the record carries (block repair)
+  const int ppw = ppw_full;
+  const int t_begin = min(wg_begin + wave * ppw * kBlockTokens, wg_end);
   const int t_end = min(wg_end, t_begin + ppw * kBlockTokens);
 
   // Pages stream through a ring of three register buffers, so two pages are in
@@ -831,11 +832,13 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) M = fmaxf(M, ml_s[w][r][0]);
+    // (weights carry 2^kWExp: the record is written without it, in the same units
+    // as the vector path's records)
     float f[kWaves], lsum = 0.0f, nsum = 0.0f, esum = 0.0f, vmax = 0.0f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
       const float mw = ml_s[w][r][0];
-      f[w] = mw == -INFINITY ? 0.0f : exp2_fast(mw - M);
+      f[w] = mw == -INFINITY ? 0.0f : exp2_fast(mw - M - kWExp);
       lsum = fmaf(f[w], ml_s[w][r][1], lsum);
       if constexpr (METER) nsum = fmaf(f[w], ml_s[w][r][2], nsum);
       if constexpr (VM) {
@@ -864,6 +867,9 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       rec[kD + 2] = nsum;
       rec[kD + 3] = esum;
       rec[kD + 4] = vmax;
+      // meter shares of the four blocks (one per wave), same units as nsum
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) rec[kD + 8 + w] = f[w] * ml_s[w][r][2];
     }
   }
 

@@ -115,13 +115,17 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
 
   const bool vm = METER && a.meter_v != nullptr;   // value side
   float m_run[4], l_run[4], n_run[4], e_run[4], vmax_run = 0.0f;
+  float nb_run[4][4];   // meter numerators of the split's four blocks (quarters), per head slot
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     m_run[k] = -INFINITY;
     l_run[k] = 0.0f;
     n_run[k] = 0.0f;
     e_run[k] = 0.0f;
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) nb_run[k][q4] = 0.0f;
   }
+  const int blk_tokens = a.split_tokens / 4;
   const int c3 = tid % D, hs = tid / D;
   float acc[HPT];
 #pragma unroll
@@ -279,6 +283,12 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         if constexpr (METER) {
           const float nn = fmaf(alpha, n_run[k], wave_sum(term));
           n_run[k] = isnan(nn) ? INFINITY : nn;
+          const int qb = (t0 + lane - t_begin) / blk_tokens;   // this token's block in the split
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const float nbq = fmaf(alpha, nb_run[k][q4], wave_sum(qb == q4 ? term : 0.0f));
+            nb_run[k][q4] = isnan(nbq) ? INFINITY : nbq;
+          }
         }
         if (vm) {
           e_run[k] = fmaf(alpha, e_run[k], wave_sum(p * vr_s[lane]));
@@ -360,6 +370,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         rec[D + 2] = n_run[k];
         rec[D + 3] = e_run[k];
         rec[D + 4] = vmax_run;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) rec[D + 8 + q4] = nb_run[k][q4];
       }
     }
   }

@@ -57,7 +57,7 @@ struct DecodeArgs {
   const int32_t* table;
   const int32_t* seq_lens;
   const uint8_t* mask_kv;   // exact fallback: only routed (b, kv) units run
-  float* part;              // partial records [batch][n_q][n_splits][D + 8]
+  float* part;              // partial records [batch][n_q][n_splits][D + 12]
   void* out;
   float* meter;
   float* raw;
@@ -108,6 +108,20 @@ __device__ __forceinline__ void gate_clear(const DecodeArgs& a, int unit) {
   }
 }
 
+// Block repair (Sec. 6.3): the decode arguments of the call that routed the KV
+// heads (its records in d.part, d.mask_kv the routed units), the exact cache, the
+// threshold and the repair budget.
+struct RepairArgs {
+  DecodeArgs d;
+  const void* x_k_data;     // exact bf16 cache
+  const void* x_v_data;
+  float tau;
+  int max_rep;              // blocks per KV head, <= 64
+  uint8_t* mask_kv_out;     // cleared for repaired KV heads (the same array as d.mask_kv)
+  int32_t* rep_list;        // [batch][n_kv][max_rep] block order (-1 padded), or null
+  int32_t* n_rep;           // [batch][n_kv] blocks taken, 0 not routed, -1 not repaired; or null
+};
+
 struct GateArgs {
   const float* meter;
   const float* raw;
@@ -125,9 +139,10 @@ inline int64_t n_splits_for(int64_t max_seq_len, int split_tokens) {
 }
 // Partial record of one (query head, split): head_dim output floats, then the
 // running max (natural log units), weight sum, meter numerator, value-side
-// numerator sum p rho, the largest stored value norm, and three spare floats (the
-// record stays a multiple of 16 bytes).
-__host__ __device__ inline size_t partial_record_floats(int head_dim) { return (size_t)head_dim + 8; }
+// numerator sum p rho, the largest stored value norm, three spare floats, and the
+// meter numerators of the split's four blocks (quarters of split_tokens tokens).
+// Weights are e^{logit - max}; the record is a multiple of 16 bytes.
+__host__ __device__ inline size_t partial_record_floats(int head_dim) { return (size_t)head_dim + 12; }
 // Workspace: the partial records, then one int32 per (sequence, KV head) for the
 // fused gate; each part rounded up to 256 bytes.
 inline size_t records_bytes(int batch, int n_q, int64_t n_splits, int head_dim) {
@@ -147,5 +162,7 @@ bool mfma_decode_supported(const DecodeArgs& a);
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st);
 hipError_t launch_merge(const DecodeArgs& a, bool metered, hipStream_t st);
 hipError_t launch_gate(const GateArgs& a, hipStream_t st);
+hipError_t launch_repair(const RepairArgs& a, hipStream_t st);
+int repair_max_blocks();
 
 }  // namespace wc

@@ -64,9 +64,9 @@ def test_cache_byte_account(L):
 def test_workspace_size_and_argument_checks(L):
     n = L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 0)
     assert n > 0 and n % 4 == 0
-    # partial records (batch, q heads, 64 splits, head_dim + 8 floats), then one int32
+    # partial records (batch, q heads, 64 splits, head_dim + 12 floats), then one int32
     # per (sequence, KV head) for the fused gate; each part rounded up to 256 bytes
-    assert L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 512) == 4 * 28 * 64 * 136 * 4 + 256
+    assert L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 512) == 4 * 28 * 64 * 140 * 4 + 256
     assert L.wc_decode_workspace_size(-1, 28, 4, 128, 100, 0) == 0
     # null cache / pointers are rejected before anything is launched
     assert L.wc_quantize_write(None, None, None, 0, None, 1, None) == _lib.WC_EINVAL

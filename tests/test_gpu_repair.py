@@ -1,0 +1,165 @@
+"""GPU parity of block-granular repair (Sec. 6.3, block-level paging) against the oracle.
+
+After a metered decode with its gate, wc_block_repair takes the routed KV heads'
+blocks (quarters of the decode's splits) in decreasing order of their meter shares
+until every query head passes tau:
+* the number of blocks taken matches the oracle's minimal count (a count whose
+  stopping state lies within 1e-3 relative of tau is accepted either way), and the
+  block order matches (blocks whose totals are within 1e-5 relative may swap);
+* repaired KV heads: outputs within 1e-5 (fp32) / 2e-3 (bf16) of the oracle's
+  repaired state, raw and meter relative, mask cleared; heads the budget cannot
+  repair and heads that were not routed are left untouched;
+* both decode paths produced the records; Tier A and Tier B keys; bypassed pairs.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import attention
+from oracle import bypass as obp
+from oracle import meter as mt
+from oracle import decode as odec
+from oracle import repair as orep
+from oracle import tierb
+
+from . import support as S
+
+pytestmark = pytest.mark.gpu
+
+W_TINY = synth.WORKLOADS["tiny-d64-s256"]
+W_GQA = synth.WORKLOADS["gqa-28x4-d128-s4k-b8"]
+INFORMATIVE = W_GQA.replace(q_scale=1 / 16, n_outliers=0)
+DLOC = 1e-6
+SPLIT = 256           # blocks of 64 tokens
+
+CASES = [
+    ("tiny", W_TINY.replace(q_scale=1 / 8), [256, 0, 100], "A", 0, 8),
+    ("gqa-informative", INFORMATIVE, [1500, 700, 0, 300], "A", 0, 16),
+    ("gqa-informative-tierb", INFORMATIVE, [1500, 700], "B", 0, 16),
+    ("gqa-bypass-tierb", W_GQA.replace(q_scale=1 / 4), [900, 333], "B", 4, 16),
+    ("gqa-small-budget", INFORMATIVE, [1500, 700], "A", 0, 2),
+]
+
+
+def _run(case, cache, exact, tier, tau, max_blocks, force_valu):
+    import torch
+
+    import paper_2607_28699_amd as wc
+    wl = case["wl"]
+    q = torch.from_numpy(case["q"]).to("cuda", S.torch_dtype(wl))
+    table = torch.from_numpy(case["table"]).cuda()
+    lens = torch.from_numpy(case["seq_lens"].astype(np.int32)).cuda()
+    L = max(int(case["seq_lens"].max()), 1)
+    sm = 1 / np.sqrt(wl.d)
+    delta = 0.0 if tier == "A" else DLOC
+    if force_valu:
+        os.environ["WITCERT_FORCE_VALU"] = "1"
+    try:
+        ws = wc.decode_workspace(q.shape[0], wl.n_q, wl.n_kv, wl.d, L, SPLIT)
+        if tier == "A":
+            out, meter, raw, mq, mk = wc.metered_decode_gate(cache, q, table, lens, L, sm, tau, ws=ws,
+                                                             split_tokens=SPLIT)
+        else:
+            out, meter, raw = wc.tierb_decode_attention(cache, q, table, lens, L, sm, delta, ws=ws,
+                                                        split_tokens=SPLIT)
+            mq, mk = wc.gate(meter, raw, wl.group, tau)
+        before = (out.clone(), meter.clone(), raw.clone(), mk.clone())
+        n_rep, rep = wc.block_repair(cache, exact, q, table, lens, L, sm, tau, ws, out, meter, raw, mk,
+                                     delta_loc=delta, max_blocks=max_blocks, split_tokens=SPLIT)
+    finally:
+        os.environ.pop("WITCERT_FORCE_VALU", None)
+    torch.cuda.synchronize()
+    cpu = lambda t: t.cpu().numpy()
+    return ([cpu(x) for x in before], cpu(out).astype(np.float64), cpu(meter), cpu(raw), cpu(mk),
+            cpu(n_rep), cpu(rep))
+
+
+@pytest.mark.parametrize("name,wl,lens,tier,m,max_blocks", CASES)
+@pytest.mark.parametrize("path", ["default", "vector"])
+def test_block_repair_parity(name, wl, lens, tier, m, max_blocks, path):
+    if path == "vector" and wl.d != 128:
+        pytest.skip("head_dim 64 always takes the vector path")
+    case = S.make_case(wl, lens, permute=True, layer=1)
+    pairs = S.case_pairs(case, m) if m else None
+    refs = S.oracle_write(case, "int8_dither", pairs)
+    sm = 1 / np.sqrt(wl.d)
+    g = wl.n_q // wl.n_kv
+    # per (sequence, KV head): the bounds c of its query heads, from the oracle
+    bounds = []
+    for b, c in enumerate(refs):
+        if case["seq_lens"][b] == 0:
+            bounds.append(None)
+            continue
+        q = case["q"][b]
+        if tier == "A":
+            cb = odec.metered_decode(q, c["khat"], c["vhat"], c["kw"], sm, wl.bands, wl.rope_layout)["c"]
+        elif pairs is None:
+            cb = tierb.tierb_decode(q, c["khat"], c["vhat"], c["ks"], sm, DLOC)["u"]
+        else:
+            cb = obp.tierb_decode(q, c["khat"], c["vhat"], c["ks"], c["ko"], c["chans"], sm, DLOC)["u"]
+        bounds.append(cb)
+    # a threshold that routes most heads but that a few blocks can meet
+    raws = []
+    for b in range(len(refs)):
+        if case["seq_lens"][b] == 0:
+            continue
+        for h in range(wl.n_q):
+            z = attention.logits(case["q"][b][h], refs[b]["khat"][:, h // g], sm)
+            raws.append(mt.raw_from_am1(mt.a_minus_one_logits(z, bounds[b][h])))
+    tau = float(np.quantile(raws, 0.2))
+    S.say(f"[repair] {name} path={path} tier={tier} tau={tau:.4g} max_blocks={max_blocks}")
+    cache = S.gpu_cache(case, "int8_dither", pairs=pairs)
+    exact = S.gpu_cache(case, "bf16")
+    before, out, meter, raw, mk, n_rep, rep = _run(case, cache, exact, tier, tau, max_blocks, path == "vector")
+    out0, meter0, raw0, mk0 = before
+    tol = S.out_tol(wl)
+    bs = SPLIT // 4
+    n_fixed = 0
+    for b in range(len(lens)):
+        for kv in range(wl.n_kv):
+            hs = slice(kv * g, (kv + 1) * g)
+            if case["seq_lens"][b] == 0 or mk0[b, kv] == 0:
+                assert n_rep[b, kv] == 0
+                assert np.array_equal(out[b, hs], out0[b, hs].astype(np.float64))
+                continue
+            c = refs[b]
+            S_ = case["seq_lens"][b]
+            # the exact store holds bf16 (the fallback cache): repaired blocks take those values
+            kx = synth.bf16_round(case["k"][b][:, kv]).astype(np.float64)
+            vx = synth.bf16_round(case["v"][b][:, kv]).astype(np.float64)
+            ranges = orep.block_ranges(S_, bs)
+            res = orep.block_repair(case["q"][b][hs], c["khat"][:, kv], c["vhat"][:, kv], kx, vx,
+                                    bounds[b][hs], ranges, sm, tau, max_blocks)
+            # the order: same blocks up to swaps of near-equal totals
+            tot = res["shares"].sum(axis=0)
+            K = min(max_blocks, len(ranges))
+            got_order = rep[b, kv, :K]
+            for i in range(K):
+                if got_order[i] != res["order"][i]:
+                    assert abs(tot[got_order[i]] - tot[res["order"][i]]) <= 1e-5 * tot.max(), (b, kv, i)
+            n_o, n_g = res["n_blocks"], n_rep[b, kv]
+            if n_g != n_o:
+                # accepted only at a stopping state within 1e-3 of tau
+                n_lo = min(x for x in (n_o, n_g) if x > 0) if max(n_o, n_g) > 0 else K
+                st = orep.repaired_state(case["q"][b][hs], c["khat"][:, kv], c["vhat"][:, kv], kx, vx,
+                                         bounds[b][hs], got_order[:n_lo], ranges, sm)
+                val = st["raw"] if tau >= 1 else st["meter"]
+                assert np.max(np.abs(val - tau)) <= 1e-3 * tau, (b, kv, n_o, n_g)
+                continue
+            if n_g == -1:
+                assert mk[b, kv] == 1
+                assert np.array_equal(out[b, hs], out0[b, hs].astype(np.float64))
+                continue
+            n_fixed += 1
+            assert mk[b, kv] == 0
+            st = orep.repaired_state(case["q"][b][hs], c["khat"][:, kv], c["vhat"][:, kv], kx, vx,
+                                     bounds[b][hs], got_order[:n_g], ranges, sm)
+            S.say(f"  ({b},{kv}) blocks {n_g}, output error {S.rel_err(out[b, hs], st['out']):.2e}")
+            assert S.rel_err(out[b, hs], st["out"]) <= tol, (b, kv, S.rel_err(out[b, hs], st["out"]))
+            assert np.all(np.abs(raw[b, hs] - st["raw"]) <= tol * np.maximum(st["raw"], 1e-30) + 1e-7)
+            assert np.all(meter[b, hs] <= tau + 1e-6 if tau < 1 else raw[b, hs] <= tau * (1 + 1e-6))
+    S.say(f"  repaired KV heads: {n_fixed}, left to the fallback: {int((n_rep == -1).sum())}")
+    if name != "gqa-small-budget":
+        assert n_fixed > 0
