@@ -29,6 +29,7 @@ FP8_BYTES = 272
 BF16_BYTES = 512
 TIERB_BYTES = 276 - 16       # the Tier-B certificate reads no witness
 WRITE_BYTES_BF16_IN = 512 + 276
+REPAIR_BUDGET = 64           # blocks per KV head that block repair may page in
 DECODE_KERNEL_SRC = os.path.join(ROOT, "paper_2607_28699_amd", "csrc")
 
 
@@ -308,6 +309,7 @@ def main():
     fb_ms = timed(lambda i: wc.exact_decode_attention(
         exact[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
         max_len_all, sm, mask_kv, out, ws=ws), reps)
+    routed = float(mask_kv.float().mean().item())    # the route mask the fallback timing used
     # Tier-B certificate (Sec. 4.2) over the same caches: per-call time and, over
     # every layer of the last step, its gate fractions (delta_req 1e-2 over
     # layers x query heads x 256 steps)
@@ -404,10 +406,48 @@ def main():
                         "pass_v_fraction": round(pass_v / (n_cells * wl.n_q), 4),
                         "gate_fraction_q_heads": round(gqj / (n_cells * wl.n_q), 4),
                         "gate_fraction_kv_heads": round(gkvj / (n_cells * wl.n_kv), 4)}
+
+        # block-granular repair (Sec. 6.3) of the KV heads the Tier-A gate routes over
+        # the same caches: blocks are quarters of the decode's splits, paged in from
+        # the exact bf16 cache in decreasing order of their meter shares until every
+        # query head passes tau, at most REPAIR_BUDGET blocks per KV head.  Timed as
+        # (metered decode + gate + repair) minus the metered decode + gate alone.
+        nrep = torch.empty((lay.batch, wl.n_kv), dtype=torch.int32, device=dev)
+        rlist = torch.empty((lay.batch, wl.n_kv, REPAIR_BUDGET), dtype=torch.int32, device=dev)
+        rws = wc.repair_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all, REPAIR_BUDGET)
+
+        def dec_rep(i):
+            layer = i % wl.n_layers
+            q_l = last["layers"][layer]["q"]
+            wc.metered_decode_gate(byp_caches[layer], q_l, table, last["lens"], max_len_all, sm, args.tau,
+                                   ws=ws, out=out, meter=meter, raw=raw, mask_q=mq_b, mask_kv=mkv_b)
+            wc.block_repair(byp_caches[layer], exact[layer], q_l, table, last["lens"], max_len_all, sm,
+                            args.tau, ws, out, meter, raw, mkv_b, max_blocks=REPAIR_BUDGET,
+                            repaired=rlist, n_repaired=nrep, repair_ws=rws)
+        dr_ms = timed(dec_rep, reps)
+        nreps = []
+        for layer in range(wl.n_layers):
+            dec_rep(layer)
+            nreps.append(nrep.clone())
+        nr = torch.cat(nreps).flatten().cpu().numpy()
+        routed_r = nr != 0
+        fixed = nr > 0
+        bs = wc.split_tokens_for(lay.batch, wl.n_kv, max_len_all) // 4
+        rep_ms = max(float(np.median(dr_ms)) - float(np.median(ba_ms)), 0.0)
+        del rws
+        whole = float(np.mean(last["lens"].cpu().numpy())) * BF16_BYTES
+        byp["repair"] = {
+            "tau": args.tau, "budget_blocks": REPAIR_BUDGET, "block_tokens": bs,
+            "median_launch_ms": round(rep_ms, 4),
+            "routed_kv_fraction": round(float(routed_r.mean()), 4),
+            "repaired_fraction_of_routed": round(float(fixed.sum() / max(routed_r.sum(), 1)), 4),
+            "median_blocks_repaired": float(np.median(nr[fixed])) if fixed.any() else None,
+            "paged_bytes_per_repaired_kv_head": (round(float(np.median(nr[fixed])) * bs * BF16_BYTES)
+                                                 if fixed.any() else None),
+            "whole_head_bytes": round(whole)}
     th_per_launch = float(last["tokens"] * wl.n_kv)
     tb_gbps = th_per_launch * TIERB_BYTES / (float(np.median(tb_ms)) * 1e-3) / 1e9
     dec_gbps = th_per_launch * INT8_BYTES / (float(np.median(dec_ms)) * 1e-3) / 1e9
-    routed = float(mask_kv.float().mean().item())
     fb_bytes = th_per_launch * routed * BF16_BYTES
     fb_gbps = fb_bytes / (float(np.median(fb_ms)) * 1e-3) / 1e9 if routed > 0 else 0.0
     write_gbps = write_tokens * WRITE_BYTES_BF16_IN / (write_ms * 1e-3) / 1e9   # per prefill of one layer

@@ -212,6 +212,14 @@ size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int he
                                 int64_t max_seq_len, int split_tokens);
 
 /*
+ * Tokens per KV split that the decode calls use for these sizes: split_tokens
+ * rounded up to a multiple of 64, or, for 0, the library's choice (about 512
+ * workgroups over the batch's KV heads, at least 256 tokens).  wc_block_repair's
+ * blocks are quarters of it.  Returns 0 for invalid sizes.
+ */
+int wc_decode_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int split_tokens);
+
+/*
  * Metered decode attention (the read path of the meter loop, Sec. 6).  For each
  * sequence b and query head h (KV head h / (n_q_heads / n_kv_heads)), over the
  * seq_lens[b] tokens whose slots are block_table[b][t/16]*16 + t%16:
@@ -324,13 +332,26 @@ int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int 
  * (-1 padded; may be NULL) and n_repaired[b][g] the number of blocks taken (0: not
  * routed, -1: the budget did not suffice; may be NULL).  At most 4096 blocks per
  * sequence.  out must be the decode's output array (out_dtype as there).
+ * repair_ws (repair_ws_bytes >= wc_block_repair_workspace_size for the same sizes,
+ * caller-owned device memory, no initialization needed) holds the per-KV-head
+ * state and the block corrections; the blocks' corrections are computed in
+ * parallel and added in the repair order, so the result does not depend on how
+ * they are scheduled.  Calls that share a repair workspace must not overlap.
  */
 int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q, int q_dtype,
                     int batch, int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
                     const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, int split_tokens,
                     float delta_loc, float tau, int max_repair_blocks, const void* ws,
                     size_t ws_bytes, void* out, int out_dtype, float* meter, float* raw,
-                    uint8_t* mask_kv, int32_t* repaired, int32_t* n_repaired, void* stream);
+                    uint8_t* mask_kv, int32_t* repaired, int32_t* n_repaired, void* repair_ws,
+                    size_t repair_ws_bytes, void* stream);
+
+/*
+ * Bytes of the repair workspace of wc_block_repair for these sizes (split_tokens
+ * as passed to the decode call, 0 = library choice); 0 for invalid sizes.
+ */
+size_t wc_block_repair_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
+                                      int64_t max_seq_len, int split_tokens, int max_repair_blocks);
 
 /*
  * Gate (the meter loop's gate, Sec. 6; certified vs risk-ranked, Sec. 4.3):

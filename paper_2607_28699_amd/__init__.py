@@ -19,7 +19,9 @@ from .api import (  # noqa: F401
     metered_decode_gate,
     quantize_write,
     quantize_write_pair,
+    repair_workspace,
     select_outlier_pairs,
+    split_tokens_for,
     tierb_decode_attention,
     tierb_delta_loc,
     witness,

@@ -18,9 +18,10 @@ WC_BLOCK_TOKENS = 16
 
 EXPORTS = (
     "wc_strerror", "wc_version", "wc_cache_bytes", "wc_quantize_write", "wc_quantize_write_pair",
-    "wc_witness", "wc_select_workspace_size", "wc_select_outlier_pairs", "wc_decode_workspace_size", "wc_metered_decode_attention",
+    "wc_witness", "wc_select_workspace_size", "wc_select_outlier_pairs", "wc_decode_workspace_size",
+    "wc_decode_split_tokens", "wc_metered_decode_attention",
     "wc_metered_decode_gate", "wc_tierb_decode_attention", "wc_joint_decode_gate", "wc_gate",
-    "wc_exact_decode_attention", "wc_block_repair",
+    "wc_exact_decode_attention", "wc_block_repair", "wc_block_repair_workspace_size",
 )
 
 
@@ -70,6 +71,7 @@ def lib() -> ctypes.CDLL:
                                       ctypes.c_int, ctypes.c_int, vp, vp]),
         "wc_decode_workspace_size": (sz, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                           i64, ctypes.c_int]),
+        "wc_decode_split_tokens": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, i64, ctypes.c_int]),
         "wc_metered_decode_attention": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int,
                                                        ctypes.c_int, vp, ctypes.c_int, vp, i64, f32,
                                                        vp, ctypes.c_int, vp, vp, ctypes.c_int, vp,
@@ -89,7 +91,9 @@ def lib() -> ctypes.CDLL:
         "wc_block_repair": (ctypes.c_int, [cp, cp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp,
                                            ctypes.c_int, vp, i64, f32, ctypes.c_int, f32, f32,
                                            ctypes.c_int, vp, sz, vp, ctypes.c_int, vp, vp, vp, vp, vp,
-                                           vp]),
+                                           vp, sz, vp]),
+        "wc_block_repair_workspace_size": (sz, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                i64, ctypes.c_int, ctypes.c_int]),
         "wc_gate": (ctypes.c_int, [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, f32, vp, vp,
                                    vp, vp]),
         "wc_exact_decode_attention": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int,

@@ -172,6 +172,14 @@ def decode_workspace(batch: int, n_q: int, n_kv: int, head_dim: int, max_seq_len
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
+def split_tokens_for(batch: int, n_kv: int, max_seq_len: int, split_tokens: int = 0) -> int:
+    """Tokens per KV split of the decode calls (block repair's blocks are quarters)."""
+    n = lib().wc_decode_split_tokens(batch, n_kv, max_seq_len, split_tokens)
+    if n <= 0:
+        raise _lib.WitCertError("bad split geometry")
+    return n
+
+
 def metered_decode_attention(cache: PagedCache, q: torch.Tensor, block_table: torch.Tensor,
                              seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float,
                              out_dtype=torch.float32, split_tokens: int = 0,
@@ -272,12 +280,16 @@ def block_repair(cache: PagedCache, exact: PagedCache, q: torch.Tensor, block_ta
                  seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float, tau: float, ws: torch.Tensor,
                  out: torch.Tensor, meter: torch.Tensor, raw: torch.Tensor, mask_kv: torch.Tensor,
                  delta_loc: float = 0.0, max_blocks: int = 16, split_tokens: int = 0,
-                 repaired: torch.Tensor | None = None, n_repaired: torch.Tensor | None = None):
+                 repaired: torch.Tensor | None = None, n_repaired: torch.Tensor | None = None,
+                 repair_ws: torch.Tensor | None = None):
     """Block repair of the KV heads a metered decode (same ws, split_tokens) routed:
     updates out, meter, raw and mask_kv in place -> (n_repaired [batch, n_kv],
     repaired [batch, n_kv, max_blocks])."""
     _dev_check(q, block_table, seq_lens, ws, out, meter, raw, mask_kv)
     batch, n_q, d = q.shape
+    if repair_ws is None:
+        repair_ws = repair_workspace(batch, n_q, cache.n_kv, d, max_seq_len, max_blocks, split_tokens,
+                                     device=q.device)
     if n_repaired is None:
         n_repaired = torch.empty((batch, cache.n_kv), dtype=torch.int32, device=q.device)
     if repaired is None:
@@ -287,9 +299,20 @@ def block_repair(cache: PagedCache, exact: PagedCache, q: torch.Tensor, block_ta
         ctypes.byref(c), ctypes.byref(e), _ptr(q), _dt(q), batch, n_q, _ptr(block_table),
         block_table.shape[1], _ptr(seq_lens), max_seq_len, float(sm_scale), split_tokens,
         float(delta_loc), float(tau), max_blocks, _ptr(ws), ws.numel(), _ptr(out), _dt(out),
-        _ptr(meter), _ptr(raw), _ptr(mask_kv), _ptr(repaired), _ptr(n_repaired), _stream()),
+        _ptr(meter), _ptr(raw), _ptr(mask_kv), _ptr(repaired), _ptr(n_repaired), _ptr(repair_ws),
+        repair_ws.numel(), _stream()),
         "wc_block_repair")
     return n_repaired, repaired
+
+
+def repair_workspace(batch: int, n_q: int, n_kv: int, head_dim: int, max_seq_len: int,
+                     max_blocks: int = 16, split_tokens: int = 0, device="cuda") -> torch.Tensor:
+    """Device workspace of block_repair for these sizes."""
+    n = lib().wc_block_repair_workspace_size(batch, n_q, n_kv, head_dim, max_seq_len, split_tokens,
+                                             max_blocks)
+    if n == 0:
+        raise _lib.WitCertError("bad repair workspace geometry")
+    return torch.empty(n, dtype=torch.uint8, device=device)
 
 
 def gate(meter: torch.Tensor, raw: torch.Tensor, group: int, tau: float,

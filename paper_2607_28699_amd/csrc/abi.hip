@@ -191,6 +191,11 @@ size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int he
   return wc::records_bytes(batch, n_q_heads, ns, head_dim) + wc::gate_unit_bytes(batch, n_kv_heads);
 }
 
+int wc_decode_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int split_tokens) {
+  if (batch < 0 || n_kv_heads < 1 || max_seq_len < 0 || split_tokens < 0) return 0;
+  return wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens);
+}
+
 static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int batch,
                          int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
                          const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out,
@@ -353,7 +358,8 @@ int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q,
                     const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, int split_tokens,
                     float delta_loc, float tau, int max_repair_blocks, const void* ws,
                     size_t ws_bytes, void* out, int out_dtype, float* meter, float* raw,
-                    uint8_t* mask_kv, int32_t* repaired, int32_t* n_repaired, void* stream) {
+                    uint8_t* mask_kv, int32_t* repaired, int32_t* n_repaired, void* repair_ws,
+                    size_t repair_ws_bytes, void* stream) {
   const bool tierb = delta_loc != 0.0f;
   int s = check_cache(cache, !tierb, tierb);
   if (s != WC_OK) return s;
@@ -374,6 +380,11 @@ int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q,
   if ((max_seq_len + a.split_tokens / 4 - 1) / (a.split_tokens / 4) > wc::repair_max_blocks())
     return WC_EUNSUPPORTED;
   if (batch == 0) return WC_OK;
+  if (!repair_ws || reinterpret_cast<uintptr_t>(repair_ws) % 256) return WC_EINVAL;
+  if (repair_ws_bytes < wc_block_repair_workspace_size(batch, n_q_heads, cache->n_kv_heads,
+                                                       cache->head_dim, max_seq_len, split_tokens,
+                                                       max_repair_blocks))
+    return WC_EWORKSPACE;
   a.meter = meter;
   a.raw = raw;
   a.mask_kv = mask_kv;
@@ -387,7 +398,26 @@ int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q,
   r.mask_kv_out = mask_kv;
   r.rep_list = repaired;
   r.n_rep = n_repaired;
+  r.rws = repair_ws;
+  // WITCERT_REPAIR_ROUND0=n caps the first round of block corrections at n blocks
+  // (default: the predicted count plus one); the result does not depend on it
+  const char* r0 = getenv("WITCERT_REPAIR_ROUND0");
+  r.round0_cap = r0 != nullptr ? atoi(r0) : 0;
+  r.tiles = wc::repair_tiles(a.split_tokens);
+  r.unit_bytes = wc::repair_unit_bytes(a.group, a.head_dim, max_repair_blocks, r.tiles);
   return hip_status(wc::launch_repair(r, static_cast<hipStream_t>(stream)));
+}
+
+size_t wc_block_repair_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
+                                      int64_t max_seq_len, int split_tokens, int max_repair_blocks) {
+  if (batch < 0 || n_kv_heads < 1 || n_q_heads < 1 || n_q_heads % n_kv_heads || head_dim < 1 ||
+      max_seq_len < 0 || split_tokens < 0 || max_repair_blocks < 1 || max_repair_blocks > 64)
+    return 0;
+  const int st = wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens);
+  const size_t unit = wc::repair_unit_bytes(n_q_heads / n_kv_heads, head_dim, max_repair_blocks,
+                                            wc::repair_tiles(st));
+  const size_t total = (size_t)batch * n_kv_heads * unit;
+  return total > 0 ? total : 256;
 }
 
 int wc_gate(const float* meter, const float* raw, int batch, int n_q_heads, int group, float tau,

@@ -2,23 +2,34 @@
 //
 // The certificate is block decomposable: A - 1 = sum_t ptilde_t (e^{c_t} - 1) splits
 // into per-block shares, and a block taken from the exact store contributes exact
-// logits and values with bound 0.  One workgroup per routed (sequence, KV head):
-//   1  rebuild each query head's merged state (max M, weight sum L, meter
-//      numerator N, unnormalized output O) in float64 from the split records of
-//      the metered decode that routed it, and the share of every block (a quarter
-//      of a split: the records carry the four blocks' numerators);
-//   2  order the blocks by the sum of their shares over the G query heads (ties
-//      to the lower block), up to the repair budget;
-//   3  take the blocks in that order; for each, recompute its tokens' compressed
-//      logits, bounds and values and their exact logits and values (the exact
-//      bf16 cache), and move L, N and O from the compressed to the exact terms:
-//        L += sum (e^{l_t - M} - e^{lt_t - M}),  N -= sum e^{lt_t - M} (e^{c_t} - 1),
-//        O += sum (e^{l_t - M} v_t - e^{lt_t - M} vhat_t);
-//      after each block A = 1 + N / L per head; stop when every head passes tau.
-// A repaired KV head gets its new outputs, meter and raw, and leaves the route
-// mask; a KV head the budget cannot repair keeps its mask (whole-head fallback).
-// Arithmetic of the state and the corrections is float64; logits and bounds are
-// formed in fp32 as in the vector decode path.
+// logits and values with bound 0.  Blocks are taken in decreasing order of their
+// shares until every query head of the KV head passes tau.  The walk is
+// sequential only in its stop rule; the block corrections are independent, so
+// the work runs in three kinds of launches:
+//   rank   one workgroup per (sequence, KV head): the merged state of each query
+//          head (max M, weight sum L, meter numerator N) in float64 from the split
+//          records of the metered decode that routed it; the block totals (sum over
+//          the G heads of the block's share; a block is a quarter of a split, whose
+//          numerator the records carry); the repair order (largest first, ties to
+//          the lower block) up to the budget; and a predicted block count, the
+//          first prefix after which every head passes when only N moves (the
+//          exact logits usually move L very little);
+//   block  one workgroup per (candidate, 64-token tile, routed KV head) of a round:
+//          compressed and exact logits, bounds and values of the tile, and the
+//          corrections that move L, N and the unnormalized output O from the
+//          compressed to the exact terms,
+//            dL = sum (e^{l_t - M} - e^{lt_t - M}),  dN = -sum e^{lt_t - M} (e^{c_t} - 1),
+//            dO = sum (e^{l_t - M} v_t - e^{lt_t - M} vhat_t)   (float64);
+//   scan   one workgroup per KV head: adds the round's corrections in order, stops
+//          at the first block after which every head passes, and for a repaired
+//          head writes its meter and raw and clears its route mask;
+//   final  one workgroup per (repaired KV head, query head): the output, the
+//          records' merged output plus the taken blocks' corrections (fixed
+//          summation order) over the repaired weight sum.
+// Round 0 covers the predicted count plus one block, round 1 the rest of the
+// budget (its launches exit at once where round 0 finished).  A KV head the
+// budget cannot repair keeps its mask (whole-head fallback).  Logits and bounds
+// are formed in fp32 as in the vector decode path.
 #include <float.h>
 
 #include "wc_device.h"
@@ -29,71 +40,264 @@ namespace wc {
 namespace {
 
 constexpr int kRThreads = 256;
-constexpr int kRTile = 64;       // tokens per tile (4 threads per token in phase 1)
+constexpr int kRTile = 64;        // tokens per block-kernel workgroup
 constexpr int kRGMax = 16;
 constexpr int kRMaxBlocks = 4096;
+constexpr int kRMaxRep = 64;
 
-template <int D, int QT>
-__global__ __launch_bounds__(kRThreads) void repair_kernel(RepairArgs ra) {
+enum : int32_t { kIdle = 0, kActive = 1, kRepaired = 2, kExhausted = 3 };
+
+// Per-(sequence, KV head) header at the start of its workspace slice.
+struct RepHeader {
+  int32_t status, K, round0_end, n_taken;
+  int32_t order[kRMaxRep];
+  double M[kRGMax], L[kRGMax], N[kRGMax];
+};
+static_assert(sizeof(RepHeader) <= kRepHeaderBytes, "repair header");
+
+__device__ __forceinline__ RepHeader* header_of(const RepairArgs& ra, int unit) {
+  return reinterpret_cast<RepHeader*>(static_cast<char*>(ra.rws) + (size_t)unit * ra.unit_bytes);
+}
+// Corrections of candidate j, tile k: G records of D + 2 doubles (dO[D], dL, dN).
+__device__ __forceinline__ double* corr_of(const RepairArgs& ra, int unit, int j, int k) {
+  const size_t rec = (size_t)ra.d.group * (ra.d.head_dim + 2);
+  return reinterpret_cast<double*>(static_cast<char*>(ra.rws) + (size_t)unit * ra.unit_bytes +
+                                   kRepHeaderBytes) + ((size_t)j * ra.tiles + k) * rec;
+}
+
+__device__ __forceinline__ bool head_passes(double L, double N, float tau) {
+  if (!(L > 0.0)) return false;
+  const double am1 = N / L;
+  const double raw = 0.5 * am1 * (2.0 + am1);
+  return (tau >= 1.0f ? raw : fmin(1.0, raw)) <= (double)tau;
+}
+
+struct UnitGeom {
+  int b, kv, L, Lc, ns, nb, bs;
+};
+__device__ __forceinline__ UnitGeom unit_geom(const DecodeArgs& a, int unit) {
+  UnitGeom u;
+  u.b = unit / a.n_kv;
+  u.kv = unit % a.n_kv;
+  u.L = a.seq_lens[u.b];
+  u.bs = a.split_tokens / 4;
+  u.Lc = min(u.L, a.max_blocks * kBlockTokens);
+  u.ns = min((u.Lc + a.split_tokens - 1) / a.split_tokens, a.n_splits);
+  u.nb = min((u.Lc + u.bs - 1) / u.bs, 4 * u.ns);
+  return u;
+}
+
+// ---------------------------------------------------------------------------
+// rank: merged state, block order, predicted count
+template <int D>
+__global__ __launch_bounds__(kRThreads) void repair_rank_kernel(RepairArgs ra) {
+  const DecodeArgs& a = ra.d;
+  __shared__ double T_s[kRMaxBlocks];
+  __shared__ float sh_s[kRGMax][kRMaxRep];
+  __shared__ uint64_t pass_s[kRGMax];
+  __shared__ int order_s[kRMaxRep];
+  __shared__ double M_s[kRGMax], L_s[kRGMax];
+
+  const int unit = blockIdx.x;
+  const int tid = threadIdx.x;
+  RepHeader* hd = header_of(ra, unit);
+  if (tid == 0) {
+    hd->status = kIdle;
+    if (ra.n_rep != nullptr) ra.n_rep[unit] = 0;
+  }
+  if (a.mask_kv[unit] == 0) return;   // nothing routed here
+  const UnitGeom u = unit_geom(a, unit);
+  if (u.nb <= 0) return;
+  const int G = a.group;
+  const int64_t R = (int64_t)partial_record_floats(D);
+  const float* recs = a.part + ((int64_t)u.b * a.n_q + (int64_t)u.kv * G) * a.n_splits * R;
+
+  // merged state of each query head: one wave per head, lanes over the splits
+  const int wave = tid >> 6, lane = tid & 63;
+  for (int h = wave; h < G; h += kRThreads / 64) {
+    const float* rh = recs + (int64_t)h * a.n_splits * R;
+    double M = -INFINITY;
+    for (int j = lane; j < u.ns; j += 64) M = fmax(M, (double)rh[j * R + D]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) M = fmax(M, __shfl_xor(M, o, 64));
+    double Ls = 0.0, Ns = 0.0;
+    for (int j = lane; j < u.ns; j += 64) {
+      const double w = exp((double)rh[j * R + D] - M);
+      Ls += w * rh[j * R + D + 1];
+      Ns += w * rh[j * R + D + 2];
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      Ls += __shfl_xor(Ls, o, 64);
+      Ns += __shfl_xor(Ns, o, 64);
+    }
+    if (lane == 0) {
+      M_s[h] = M;
+      L_s[h] = Ls;
+      hd->M[h] = M;
+      hd->L[h] = Ls;
+      hd->N[h] = Ns;
+    }
+  }
+  __syncthreads();
+  // block totals: sum over the heads of e^{m_j - M} n_{j,w} / L (the heads' loads
+  // issued together)
+  for (int i = tid; i < u.nb; i += kRThreads) {
+    const int j = i >> 2, w = i & 3;
+    float mv[kRGMax], nv[kRGMax];
+#pragma unroll
+    for (int h = 0; h < kRGMax; ++h) {
+      const float* rc = recs + ((int64_t)(h < G ? h : 0) * a.n_splits + j) * R;
+      mv[h] = rc[D];
+      nv[h] = rc[D + 8 + w];
+    }
+    double t = 0.0;
+#pragma unroll
+    for (int h = 0; h < kRGMax; ++h)
+      if (h < G) t += exp((double)mv[h] - M_s[h]) * nv[h] / L_s[h];
+    T_s[i] = t;
+  }
+  __syncthreads();
+  // repair order: the budget's largest blocks, ties to the lower index.  Up to
+  // 1024 blocks every block counts the blocks ahead of it; beyond, one wave takes
+  // an arg-max per step.
+  const int K = min(ra.max_rep, u.nb);
+  if (u.nb <= 1024) {
+    for (int i = tid; i < u.nb; i += kRThreads) {
+      const double ti = T_s[i];
+      int rank = 0;
+      for (int j = 0; j < u.nb; ++j) {
+        const double tj = T_s[j];
+        rank += (tj > ti || (tj == ti && j < i)) ? 1 : 0;
+      }
+      if (rank < K) order_s[rank] = i;
+    }
+  } else if (tid < 64) {
+    for (int k = 0; k < K; ++k) {
+      double bv = -2.0;
+      int bi = 0x7fffffff;
+      for (int i = tid; i < u.nb; i += 64)
+        if (T_s[i] > bv) {
+          bv = T_s[i];
+          bi = i;
+        }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const double ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (ov > bv || (ov == bv && oi < bi)) {
+          bv = ov;
+          bi = oi;
+        }
+      }
+      if (tid == 0) {
+        order_s[k] = bi;
+        T_s[bi] = -1.0;
+      }
+      __builtin_amdgcn_wave_barrier();   // (one wave: LDS accesses stay in program order)
+    }
+  }
+  __syncthreads();
+  // predicted count: per head, N minus the taken shares (L held fixed)
+  for (int i = tid; i < G * K; i += kRThreads) {
+    const int h = i / K, k = i % K;
+    const int blk = order_s[k];
+    const float* rc = recs + ((int64_t)h * a.n_splits + (blk >> 2)) * R;
+    sh_s[h][k] = (float)(exp((double)rc[D] - M_s[h]) * rc[D + 8 + (blk & 3)]);
+  }
+  __syncthreads();
+  if (tid < G) {
+    double N = hd->N[tid];
+    uint64_t bits = 0;
+    for (int k = 0; k < K; ++k) {
+      N -= sh_s[tid][k];
+      if (head_passes(L_s[tid], N, ra.tau)) bits |= 1ull << k;
+    }
+    pass_s[tid] = bits;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t all = K == 64 ? ~0ull : ((1ull << K) - 1);
+    for (int h = 0; h < G; ++h) all &= pass_s[h];
+    const int pred = all ? __builtin_ctzll(all) + 1 : K;
+    hd->K = K;
+    hd->n_taken = 0;
+    hd->round0_end = min(K, ra.round0_cap > 0 ? ra.round0_cap : pred + 1);
+    hd->status = kActive;
+  }
+  for (int k = tid; k < kRMaxRep; k += kRThreads) hd->order[k] = k < K ? order_s[k] : -1;
+  if (ra.rep_list != nullptr)
+    for (int k = tid; k < ra.max_rep; k += kRThreads)
+      ra.rep_list[(int64_t)unit * ra.max_rep + k] = k < K ? order_s[k] : -1;
+}
+
+// ---------------------------------------------------------------------------
+// block: corrections of one 64-token tile of one candidate block
+template <int D, int QT, int GM>
+__global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs ra, int round) {
   const DecodeArgs& a = ra.d;
   constexpr int CH = D / 4;
   constexpr int NG = CH / 16;
-  constexpr int NHS = kRThreads / D;
+  constexpr int NSUB = kRThreads / D;   // channel-thread subsets in the output pass
 
-  __shared__ float q_s[kRGMax][D];
-  __shared__ float qk_s[kRGMax][D];      // q with bypassed channels zeroed (Tier B terms)
-  __shared__ float qbn_s[kRGMax][16];
-  __shared__ float ab_s[kRGMax];
+  __shared__ float q_s[GM][D];
+  __shared__ float qbn_s[GM][16];
+  __shared__ float ab_s[GM];
   __shared__ int8_t opos_s[D];           // stored-value position of a bypassed channel, else -1
-  __shared__ double M_s[kRGMax], L_s[kRGMax], N_s[kRGMax];
-  __shared__ double O_s[kRGMax][D];
-  __shared__ float T_s[kRMaxBlocks];     // block totals over the heads (-1: taken)
-  __shared__ int order_s[64];
-  __shared__ float lq_s[kRGMax][kRTile], lx_s[kRGMax][kRTile], cb_s[kRGMax][kRTile];
-  __shared__ double wq_s[kRGMax][kRTile], wx_s[kRGMax][kRTile];
-  __shared__ uint32_t xi_s[kRTile][D / 4];
+  __shared__ double wq_s[GM][kRTile], wx_s[GM][kRTile];
+  __shared__ uint32_t xi_s[kRTile][D / 16 * 4];
   __shared__ float vs_s[kRTile];
   __shared__ int64_t slot_s[kRTile];
-  __shared__ float red_v[kRThreads];
-  __shared__ int red_i[kRThreads];
-  __shared__ int stop_s;
+  __shared__ double dl_s[GM], dn_s[GM];
+  __shared__ uint16_t ko_s[kRTile][32];  // stored fp16 values of the bypassed pairs (2m <= 32)
+  // logits and bounds of phases 1-2, then the output reduction of phase 3
+  constexpr int kLogitBytes = 3 * GM * kRTile * 4;
+  constexpr int kRedBytes = (NSUB > 1 ? NSUB - 1 : 1) * GM * D * 8;
+  __shared__ __align__(16) char un_s[kLogitBytes > kRedBytes ? kLogitBytes : kRedBytes];
+  float (*lq_s)[kRTile] = reinterpret_cast<float (*)[kRTile]>(un_s);
+  float (*lx_s)[kRTile] = reinterpret_cast<float (*)[kRTile]>(un_s + GM * kRTile * 4);
+  float (*cb_s)[kRTile] = reinterpret_cast<float (*)[kRTile]>(un_s + 2 * GM * kRTile * 4);
+  double (*red_s)[GM][D] = reinterpret_cast<double (*)[GM][D]>(un_s);
 
-  const int unit = blockIdx.x;
-  const int b = unit / a.n_kv, kv = unit % a.n_kv;
+  const int unit = blockIdx.y;
+  const RepHeader* hd = header_of(ra, unit);
+  if (hd->status != kActive) return;
+  const int j = blockIdx.x / ra.tiles, tile = blockIdx.x % ra.tiles;
+  const int j_lo = round == 0 ? 0 : hd->round0_end;
+  const int j_hi = round == 0 ? hd->round0_end : hd->K;
+  if (j < j_lo || j >= j_hi) return;
+  const UnitGeom u = unit_geom(a, unit);
+  const int b = u.b, kv = u.kv;
   const int tid = threadIdx.x;
-  if (ra.n_rep != nullptr && tid == 0) ra.n_rep[unit] = 0;
-  if (a.mask_kv == nullptr || a.mask_kv[unit] == 0) return;   // nothing routed here
-  const int L = a.seq_lens[b];
   const int G = a.group;
   const int B = a.n_bands;
-  const int bs = a.split_tokens / 4;                          // tokens per block
-  const int Lc = min(L, a.max_blocks * kBlockTokens);
-  const int ns = min((Lc + a.split_tokens - 1) / a.split_tokens, a.n_splits);
-  const int nb = min((Lc + bs - 1) / bs, 4 * ns);
-  if (nb <= 0) return;
-  const int64_t R = (int64_t)partial_record_floats(D);
-  const float* recs = a.part + ((int64_t)b * a.n_q + (int64_t)kv * G) * a.n_splits * R;
+  const int blk = hd->order[j];
+  const int t_lo = blk * u.bs + tile * kRTile;
+  const int t_hi = min(min(t_lo + kRTile, blk * u.bs + u.bs), u.Lc);
+  const int nv = max(t_hi - t_lo, 0);     // tokens of this tile
   const bool tierb = a.tierb_delta > 0.0f;
   const int m2 = 2 * a.n_pairs;
   const uint32_t layer_head = ((uint32_t)a.layer << 16) | (uint32_t)kv;
+  double* out_rec = corr_of(ra, unit, j, tile);
+  const int rec = D + 2;
+  if (nv == 0) {
+    for (int i = tid; i < G * rec; i += kRThreads) out_rec[i] = 0.0;
+    return;
+  }
 
-  // ---- queries, band norms, Tier-B factors, bypassed channels ----
+  // ---- queries (bypassed channels zeroed for the compressed key), band norms,
+  // Tier-B factors ----
+  for (int c = tid; c < D; c += kRThreads) opos_s[c] = -1;
   for (int i = tid; i < G * D; i += kRThreads) {
     const int h = i / D, c = i % D;
     const int64_t qi = ((int64_t)b * a.n_q + (int64_t)kv * G + h) * D + c;
-    const float x = QT == WC_F32 ? reinterpret_cast<const float*>(a.q)[qi]
-                                 : bf16_to_f32(reinterpret_cast<const uint16_t*>(a.q)[qi]);
-    q_s[h][c] = x;
-    qk_s[h][c] = x;
+    q_s[h][c] = QT == WC_F32 ? reinterpret_cast<const float*>(a.q)[qi]
+                             : bf16_to_f32(reinterpret_cast<const uint16_t*>(a.q)[qi]);
   }
-  for (int c = tid; c < D; c += kRThreads) opos_s[c] = -1;
   __syncthreads();
-  if (m2 > 0) {
+  if (m2 > 0 && tid < m2) {
     const int32_t* pl = a.pairs + (int64_t)kv * a.n_pairs;
-    if (tid < m2) opos_s[pair_channel(pl[tid >> 1], tid & 1, D, a.interleaved)] = (int8_t)tid;
-    __syncthreads();
-    for (int i = tid; i < G * D; i += kRThreads)
-      if (opos_s[i % D] >= 0) qk_s[i / D][i % D] = 0.0f;
+    opos_s[pair_channel(pl[tid >> 1], tid & 1, D, a.interleaved)] = (int8_t)tid;
   }
   for (int i = tid; i < G * B; i += kRThreads) {
     const int h = i / B, bb = i % B;
@@ -108,293 +312,424 @@ __global__ __launch_bounds__(kRThreads) void repair_kernel(RepairArgs ra) {
   if (tierb && tid < G) {
     float sq = 0.0f, l1 = 0.0f;
     for (int c = 0; c < D; ++c) {
-      sq = fmaf(qk_s[tid][c], qk_s[tid][c], sq);
-      l1 += fabsf(qk_s[tid][c]);
+      const float x = opos_s[c] >= 0 ? 0.0f : q_s[tid][c];
+      sq = fmaf(x, x, sq);
+      l1 += fabsf(x);
     }
-    ab_s[tid] = tierb_factor(sq, l1, L, a.tierb_delta, a.sm_scale);
-  }
-
-  // ---- merged state of each query head from the split records ----
-  if (tid < G) {
-    double M = -INFINITY;
-    for (int j = 0; j < ns; ++j) M = fmax(M, (double)recs[((int64_t)tid * a.n_splits + j) * R + D]);
-    double Ls = 0.0, Ns = 0.0;
-    for (int j = 0; j < ns; ++j) {
-      const float* rc = recs + ((int64_t)tid * a.n_splits + j) * R;
-      const double w = exp((double)rc[D] - M);
-      Ls += w * rc[D + 1];
-      Ns += w * rc[D + 2];
-    }
-    M_s[tid] = M;
-    L_s[tid] = Ls;
-    N_s[tid] = Ns;
-  }
-  __syncthreads();
-  for (int i = tid; i < G * D; i += kRThreads) {
-    const int h = i / D, c = i % D;
-    double o = 0.0;
-    for (int j = 0; j < ns; ++j) {
-      const float* rc = recs + ((int64_t)h * a.n_splits + j) * R;
-      o += exp((double)rc[D] - M_s[h]) * rc[c];
-    }
-    O_s[h][c] = o;
-  }
-  // block totals: sum over the heads of e^{m_j - M} n_{j,w} / L
-  for (int i = tid; i < nb; i += kRThreads) {
-    const int j = i >> 2, w = i & 3;
-    double t = 0.0;
-    for (int h = 0; h < G; ++h) {
-      const float* rc = recs + ((int64_t)h * a.n_splits + j) * R;
-      t += exp((double)rc[D] - M_s[h]) * rc[D + 8 + w] / L_s[h];
-    }
-    T_s[i] = (float)t;
+    ab_s[tid] = tierb_factor(sq, l1, u.L, a.tierb_delta, a.sm_scale);
   }
   __syncthreads();
 
-  // ---- repair order: the budget's largest blocks, ties to the lower index ----
-  const int K = min(ra.max_rep, nb);
-  for (int k = 0; k < K; ++k) {
-    float bv = -2.0f;
-    int bi = 0x7fffffff;
-    for (int i = tid; i < nb; i += kRThreads)
-      if (T_s[i] > bv) {
-        bv = T_s[i];
-        bi = i;
-      }
-    red_v[tid] = bv;
-    red_i[tid] = bi;
-    __syncthreads();
-    for (int o = kRThreads / 2; o > 0; o >>= 1) {
-      if (tid < o) {
-        const float ov = red_v[tid + o];
-        const int oi = red_i[tid + o];
-        if (ov > red_v[tid] || (ov == red_v[tid] && oi < red_i[tid])) {
-          red_v[tid] = ov;
-          red_i[tid] = oi;
-        }
-      }
+  // ---- phase 1: compressed and exact logits, bounds (thread: token i, channel quarter) ----
+  {
+    const int i = tid >> 2, part = tid & 3;
+    const int t = t_lo + i;
+    const bool valid = i < nv;
+    int64_t slot = -1;
+    if (valid) slot = (int64_t)a.table[(int64_t)b * a.max_blocks + t / kBlockTokens] * kBlockTokens +
+                      t % kBlockTokens;
+    if (part == 0) slot_s[i] = slot;
+    const int c0 = part * CH;
+    const int64_t row = valid ? ((slot / kBlockTokens) * a.n_kv + kv) * kBlockTokens + slot % kBlockTokens : 0;
+    if (m2 > 0) {   // the token's bypassed values to LDS (quarter of the row per thread)
+      for (int e = part; e < m2; e += 4) ko_s[i][e] = valid ? a.k_outlier[row * m2 + e] : (uint16_t)0;
       __syncthreads();
     }
-    if (tid == 0) {
-      order_s[k] = red_i[0];
-      T_s[red_i[0]] = -1.0f;
+    // per head: q . khat, q . k and the Tier-B rounding term, channel by channel
+    float dq[GM], dx[GM], cq[GM];
+#pragma unroll
+    for (int h = 0; h < GM; ++h) dq[h] = dx[h] = cq[h] = 0.0f;
+    float s = 0.0f;
+    if (valid) {
+      uint32_t kb[CH / 4];
+      const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.k_data) + row * D + c0);
+#pragma unroll
+      for (int w = 0; w < CH / 16; ++w) {
+        const uint4 x = kp[w];
+        kb[4 * w] = x.x; kb[4 * w + 1] = x.y; kb[4 * w + 2] = x.z; kb[4 * w + 3] = x.w;
+      }
+      uint32_t xb[CH / 2];
+      const uint4* xp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(ra.x_k_data) + row * D + c0);
+#pragma unroll
+      for (int w = 0; w < CH / 8; ++w) {
+        const uint4 x = xp[w];
+        xb[4 * w] = x.x; xb[4 * w + 1] = x.y; xb[4 * w + 2] = x.z; xb[4 * w + 3] = x.w;
+      }
+      const bool int8 = a.kind == WC_KIND_INT8_DITHER;
+      if (int8) s = f16_to_f32(a.k_scale[row]);
+      if (part == 0) vs_s[i] = int8 ? f16_to_f32(a.v_scale[row]) : 1.0f;
+#pragma unroll
+      for (int gi = 0; gi < NG; ++gi) {
+        uint32_t rw[4] = {0, 0, 0, 0};
+        if (int8) {
+          const U4 r = dither_block(c0 / 16 + gi, slot, layer_head, a.key0, a.key1);
+          rw[0] = r.x; rw[1] = r.y; rw[2] = r.z; rw[3] = r.w;
+#pragma unroll
+          for (int w4 = 0; w4 < 4; ++w4) xi_s[i][(c0 + 16 * gi) / 4 + w4] = rw[w4];
+        }
+#pragma unroll
+        for (int w4 = 0; w4 < 4; ++w4) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int c = 16 * gi + 4 * w4 + e;
+            const uint32_t byte = (kb[c >> 2] >> (8 * (c & 3))) & 0xFFu;
+            float kq = int8 ? s * ((float)((int32_t)byte - 128) - dither_value((rw[w4] >> (8 * e)) & 0xFFu))
+                            : e4m3_to_f32(byte);
+            const int op = m2 > 0 ? opos_s[c0 + c] : -1;
+            if (op >= 0) kq = f16_to_f32(ko_s[i][op]);   // bypassed pair: stored fp16
+            const float kx = bf16_to_f32((uint16_t)(xb[c >> 1] >> (16 * (c & 1))));
+#pragma unroll
+            for (int h = 0; h < GM; ++h) {
+              if (h < G) {
+                const float qc = q_s[h][c0 + c];
+                dq[h] = fmaf(qc, kq, dq[h]);
+                dx[h] = fmaf(qc, kx, dx[h]);
+                if (tierb && op >= 0) cq[h] = fmaf(fabsf(qc), fmaf(fabsf(kq), 0x1p-11f, 0x1p-25f), cq[h]);
+              }
+            }
+          }
+        }
+      }
+    } else if (part == 0) {
+      vs_s[i] = 0.0f;
     }
-    __syncthreads();
+    // Tier A: witness bound; Tier B: radius from the key scale (+ rounding of bypassed values)
+    float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (valid && !tierb) {
+#pragma unroll
+      for (int k4 = 0; k4 < 4; ++k4) {
+        const int bb = part + 4 * k4;
+        if (bb < B) wv[k4] = f16_to_f32(a.k_witness[row * B + bb]);
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < GM; ++h) {
+      if (h >= G) continue;
+      float cp = 0.0f;
+      if (!tierb) {
+#pragma unroll
+        for (int k4 = 0; k4 < 4; ++k4) {
+          const int bb = part + 4 * k4;
+          if (bb < B) cp = fmaf(qbn_s[h][bb], wv[k4], cp);
+        }
+      } else if (m2 > 0) {
+        cp = cq[h] * a.sm_scale;
+      }
+      float vq = dq[h], vx = dx[h];
+      vq += __shfl_xor(vq, 1, 4);
+      vq += __shfl_xor(vq, 2, 4);
+      vx += __shfl_xor(vx, 1, 4);
+      vx += __shfl_xor(vx, 2, 4);
+      cp += __shfl_xor(cp, 1, 4);
+      cp += __shfl_xor(cp, 2, 4);
+      if (part == 0) {
+        lq_s[h][i] = vq * a.sm_scale;
+        lx_s[h][i] = vx * a.sm_scale;
+        cb_s[h][i] = tierb ? fmaf(ab_s[h], s, cp) : cp;
+      }
+    }
   }
+  __syncthreads();
 
-  // ---- take the blocks in order until every head passes ----
-  int done = -1;
-  for (int k = 0; k < K && done < 0; ++k) {
-    const int blk = order_s[k];
-    const int b0 = blk * bs, b1 = min(b0 + bs, Lc);
-    for (int tt = b0; tt < b1; tt += kRTile) {
-      // phase 1: compressed and exact logits, bounds (thread: token i, channel quarter)
-      {
-        const int i = tid >> 2, part = tid & 3;
-        const int t = tt + i;
-        const bool valid = t < b1;
-        int64_t slot = -1;
-        if (valid) slot = (int64_t)a.table[(int64_t)b * a.max_blocks + t / kBlockTokens] * kBlockTokens +
-                          t % kBlockTokens;
-        if (part == 0) slot_s[i] = slot;
-        const int c0 = part * CH;
-        const int64_t page = valid ? (slot / kBlockTokens) * a.n_kv + kv : 0;
-        const int off = valid ? (int)(slot % kBlockTokens) : 0;
-        float kq[CH], kx[CH];
-        float s = 0.0f;
+  // ---- phase 2: weights and the L, N corrections (thread: head tid / 16, tokens tid % 16 + 16 k) ----
+  {
+    const int h = tid >> 4, l16 = tid & 15;
+    double dl = 0.0, dn = 0.0;
+    if (h < G) {
+      const double M = hd->M[h];
 #pragma unroll
-        for (int c = 0; c < CH; ++c) kq[c] = kx[c] = 0.0f;
-        if (valid) {
-          if (a.kind == WC_KIND_INT8_DITHER) {
-            const uint8_t* kp = reinterpret_cast<const uint8_t*>(a.k_data) + (page * kBlockTokens + off) * D + c0;
-            s = f16_to_f32(a.k_scale[page * kBlockTokens + off]);
-#pragma unroll
-            for (int gi = 0; gi < NG; ++gi) {
-              const U4 r = dither_block(c0 / 16 + gi, slot, layer_head, a.key0, a.key1);
-              const uint32_t rw[4] = {r.x, r.y, r.z, r.w};
-#pragma unroll
-              for (int w4 = 0; w4 < 4; ++w4) {
-                xi_s[i][(c0 + 16 * gi) / 4 + w4] = rw[w4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                  const int c = 16 * gi + 4 * w4 + j;
-                  const float code = (float)((int32_t)kp[c] - 128);
-                  kq[c] = s * (code - dither_value((rw[w4] >> (8 * j)) & 0xFFu));
-                }
-              }
-            }
-            if (m2 > 0) {
-#pragma unroll
-              for (int c = 0; c < CH; ++c) {
-                const int op = opos_s[c0 + c];
-                if (op >= 0) kq[c] = f16_to_f32(a.k_outlier[(page * kBlockTokens + off) * m2 + op]);
-              }
-            }
-            if (part == 0) vs_s[i] = f16_to_f32(a.v_scale[page * kBlockTokens + off]);
-          } else {   // FP8_RAW
-            const uint8_t* kp = reinterpret_cast<const uint8_t*>(a.k_data) + (page * kBlockTokens + off) * D + c0;
-#pragma unroll
-            for (int c = 0; c < CH; ++c) kq[c] = e4m3_to_f32(kp[c]);
-            if (part == 0) vs_s[i] = 1.0f;
-          }
-          const uint16_t* xp = reinterpret_cast<const uint16_t*>(ra.x_k_data) + (page * kBlockTokens + off) * D + c0;
-#pragma unroll
-          for (int c = 0; c < CH; ++c) kx[c] = bf16_to_f32(xp[c]);
-        } else if (part == 0) {
-          vs_s[i] = 0.0f;
+      for (int k4 = 0; k4 < kRTile / 16; ++k4) {
+        const int i = l16 + 16 * k4;
+        double wq = 0.0, wx = 0.0;
+        if (i < nv) {
+          wq = exp((double)lq_s[h][i] - M);
+          wx = exp((double)lx_s[h][i] - M);
+          dl += wx - wq;
+          dn -= wq * expm1((double)cb_s[h][i]);
         }
-        // Tier A: witness bound; Tier B: radius from the key scale (+ rounding of bypassed values)
-        float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        if (valid && !tierb) {
-#pragma unroll
-          for (int k4 = 0; k4 < 4; ++k4) {
-            const int bb = part + 4 * k4;
-            if (bb < B) wv[k4] = f16_to_f32(a.k_witness[(page * kBlockTokens + off) * B + bb]);
-          }
-        }
-        for (int h = 0; h < G; ++h) {
-          float dq = 0.0f, dx = 0.0f, cp = 0.0f;
-#pragma unroll
-          for (int c = 0; c < CH; ++c) {
-            dq = fmaf(q_s[h][c0 + c], kq[c], dq);
-            dx = fmaf(q_s[h][c0 + c], kx[c], dx);
-          }
-          if (!tierb) {
-#pragma unroll
-            for (int k4 = 0; k4 < 4; ++k4) {
-              const int bb = part + 4 * k4;
-              if (bb < B) cp = fmaf(qbn_s[h][bb], wv[k4], cp);
-            }
-          } else if (m2 > 0) {
-#pragma unroll
-            for (int c = 0; c < CH; ++c)
-              if (opos_s[c0 + c] >= 0) cp = fmaf(fabsf(q_s[h][c0 + c]), fmaf(fabsf(kq[c]), 0x1p-11f, 0x1p-25f), cp);
-            cp *= a.sm_scale;
-          }
-          dq += __shfl_xor(dq, 1, 4);
-          dq += __shfl_xor(dq, 2, 4);
-          dx += __shfl_xor(dx, 1, 4);
-          dx += __shfl_xor(dx, 2, 4);
-          cp += __shfl_xor(cp, 1, 4);
-          cp += __shfl_xor(cp, 2, 4);
-          if (part == 0) {
-            lq_s[h][i] = dq * a.sm_scale;
-            lx_s[h][i] = dx * a.sm_scale;
-            cb_s[h][i] = tierb ? fmaf(ab_s[h], s, cp) : cp;
-          }
-        }
+        wq_s[h][i] = wq;
+        wx_s[h][i] = wx;
       }
-      __syncthreads();
-      // phase 2: weights and the L, N corrections (thread: head tid / 16, tokens tid % 16 + 16 k)
-      {
-        const int h = tid >> 4, l16 = tid & 15;
-        double dl = 0.0, dn = 0.0;
+    }
+    for (int o = 8; o > 0; o >>= 1) {
+      dl += __shfl_xor(dl, o, 16);
+      dn += __shfl_xor(dn, o, 16);
+    }
+    if (h < G && l16 == 0) {
+      dl_s[h] = dl;
+      dn_s[h] = dn;
+    }
+  }
+  __syncthreads();
+
+  // ---- phase 3: the output correction (thread: channel c, token quads sub, sub + NSUB, ..) ----
+  {
+    const int c = tid % D, sub = tid / D;
+    double acc[GM];
+#pragma unroll
+    for (int h = 0; h < GM; ++h) acc[h] = 0.0;
+    constexpr int NQ = kRTile / 4 / NSUB;   // quads per thread
+    uint32_t vb[NQ];
+    uint2 xb[NQ];
+#pragma unroll
+    for (int qq = 0; qq < NQ; ++qq) {
+      const int i0 = 4 * (sub + NSUB * qq);
+      vb[qq] = 0;
+      xb[qq] = make_uint2(0, 0);
+      if (i0 < nv) {
+        const int64_t slot = slot_s[i0];
+        const int64_t page = (slot / kBlockTokens) * a.n_kv + kv;
+        const int64_t vi = page * (kBlockTokens * D) + ((slot % kBlockTokens) >> 2) * D * 4 + c * 4;
+        vb[qq] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(a.v_data) + vi);
+        xb[qq] = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(ra.x_v_data) + vi);
+      }
+    }
+#pragma unroll
+    for (int qq = 0; qq < NQ; ++qq) {
+      const int i0 = 4 * (sub + NSUB * qq);
+      if (i0 >= nv) continue;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = i0 + e;
+        if (i >= nv) break;
+        const uint32_t byte = (vb[qq] >> (8 * e)) & 0xFFu;
+        float vq;
+        if (a.kind == WC_KIND_INT8_DITHER) {
+          const uint32_t xw = xi_s[i][c >> 2];
+          vq = vs_s[i] * ((float)((int32_t)byte - 128) - dither_value((xw >> (8 * (c & 3))) & 0xFFu));
+        } else {
+          vq = e4m3_to_f32(byte);
+        }
+        const uint32_t xw2 = e < 2 ? xb[qq].x : xb[qq].y;
+        const float vx = bf16_to_f32((uint16_t)(xw2 >> (16 * (e & 1))));
+#pragma unroll
+        for (int h = 0; h < GM; ++h)
+          if (h < G) acc[h] += wx_s[h][i] * (double)vx - wq_s[h][i] * (double)vq;
+      }
+    }
+    __syncthreads();   // the logit arrays are dead: their LDS takes the reduction
+    if (sub > 0) {
+#pragma unroll
+      for (int h = 0; h < GM; ++h)
+        if (h < G) red_s[sub - 1][h][c] = acc[h];
+    }
+    __syncthreads();
+    if (sub == 0) {
+#pragma unroll
+      for (int h = 0; h < GM; ++h) {
         if (h < G) {
-          for (int k4 = 0; k4 < kRTile / 16; ++k4) {
-            const int i = l16 + 16 * k4;
-            double wq = 0.0, wx = 0.0;
-            if (tt + i < b1) {
-              wq = exp((double)lq_s[h][i] - M_s[h]);
-              wx = exp((double)lx_s[h][i] - M_s[h]);
-              dl += wx - wq;
-              dn -= wq * expm1((double)cb_s[h][i]);
-            }
-            wq_s[h][i] = wq;
-            wx_s[h][i] = wx;
-          }
-        }
-        for (int o = 8; o > 0; o >>= 1) {
-          dl += __shfl_xor(dl, o, 16);
-          dn += __shfl_xor(dn, o, 16);
-        }
-        if (h < G && l16 == 0) {
-          L_s[h] += dl;
-          N_s[h] += dn;
+          double o = acc[h];
+          for (int s2 = 1; s2 < NSUB; ++s2) o += red_s[s2 - 1][h][c];
+          out_rec[h * rec + c] = o;
         }
       }
-      __syncthreads();
-      // phase 3: the output correction (thread: channel, head subset)
-      {
-        const int c3 = tid % D, hs = tid / D;
-        for (int i = 0; i < kRTile && tt + i < b1; ++i) {
-          const int64_t slot = slot_s[i];
-          const int64_t page = (slot / kBlockTokens) * a.n_kv + kv;
-          const int off = (int)(slot % kBlockTokens);
-          const int64_t vi = page * (kBlockTokens * D) + ((off >> 2) * D + c3) * 4 + (off & 3);
-          const uint8_t byte = reinterpret_cast<const uint8_t*>(a.v_data)[vi];
-          float vq;
-          if (a.kind == WC_KIND_INT8_DITHER) {
-            const uint32_t u = (xi_s[i][c3 >> 2] >> (8 * (c3 & 3))) & 0xFFu;
-            vq = vs_s[i] * ((float)((int32_t)byte - 128) - dither_value(u));
-          } else {
-            vq = e4m3_to_f32(byte);
-          }
-          const float vx = bf16_to_f32(reinterpret_cast<const uint16_t*>(ra.x_v_data)[vi]);
-          for (int h = hs; h < G; h += NHS) O_s[h][c3] += wx_s[h][i] * (double)vx - wq_s[h][i] * (double)vq;
-        }
-      }
-      __syncthreads();
     }
-    // after the block: does every head pass?
-    if (tid == 0) {
-      bool pass = true;
-      for (int h = 0; h < G; ++h) {
-        if (!(L_s[h] > 0.0)) {
-          pass = false;
-          break;
-        }
-        const double am1 = N_s[h] / L_s[h];
-        const double raw = 0.5 * am1 * (2.0 + am1);
-        pass = pass && ((ra.tau >= 1.0f ? raw : fmin(1.0, raw)) <= (double)ra.tau);
+  }
+  if (tid < G) {
+    out_rec[tid * rec + D] = dl_s[tid];
+    out_rec[tid * rec + D + 1] = dn_s[tid];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// scan: add the round's corrections in order, stop at the first passing prefix
+template <int D>
+__global__ __launch_bounds__(kRThreads) void repair_scan_kernel(RepairArgs ra, int round) {
+  const DecodeArgs& a = ra.d;
+  __shared__ double dL_s[kRMaxRep][kRGMax], dN_s[kRMaxRep][kRGMax];
+  __shared__ uint64_t pass_s[kRGMax];
+  __shared__ int done_s;
+
+  const int unit = blockIdx.x;
+  const int tid = threadIdx.x;
+  RepHeader* hd = header_of(ra, unit);
+  if (hd->status != kActive) return;
+  const int G = a.group;
+  const int j_lo = round == 0 ? 0 : hd->round0_end;
+  const int j_hi = round == 0 ? hd->round0_end : hd->K;
+  const bool last = round == 1;
+  const int n = j_hi - j_lo;
+  const int rec = D + 2;
+
+  // per (candidate, head): the tiles' dL, dN added in tile order
+  for (int i = tid; i < n * G; i += kRThreads) {
+    const int jj = i / G, h = i % G;
+    double dl = 0.0, dn = 0.0;
+    for (int k0 = 0; k0 < ra.tiles; k0 += 4) {
+      double l4[4], n4[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double* cr = corr_of(ra, unit, j_lo + jj, min(k0 + e, ra.tiles - 1)) + h * rec;
+        l4[e] = k0 + e < ra.tiles ? cr[D] : 0.0;
+        n4[e] = k0 + e < ra.tiles ? cr[D + 1] : 0.0;
       }
-      stop_s = pass ? k : -1;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        dl += l4[e];
+        dn += n4[e];
+      }
+    }
+    dL_s[jj][h] = dl;
+    dN_s[jj][h] = dn;
+  }
+  __syncthreads();
+  if (tid < G) {
+    double L = hd->L[tid], N = hd->N[tid];
+    uint64_t bits = 0;
+    for (int jj = 0; jj < n; ++jj) {
+      L += dL_s[jj][tid];
+      N += dN_s[jj][tid];
+      if (head_passes(L, N, ra.tau)) bits |= 1ull << jj;
+    }
+    pass_s[tid] = bits;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t all = n >= 64 ? ~0ull : ((1ull << n) - 1);
+    for (int h = 0; h < G; ++h) all &= pass_s[h];
+    done_s = all ? j_lo + __builtin_ctzll(all) : -1;   // last candidate taken
+  }
+  __syncthreads();
+  const int done = done_s;
+  if (done < 0) {
+    if (tid < G) {   // carry the state into the next round
+      double L = hd->L[tid], N = hd->N[tid];
+      for (int jj = 0; jj < n; ++jj) {
+        L += dL_s[jj][tid];
+        N += dN_s[jj][tid];
+      }
+      hd->L[tid] = L;
+      hd->N[tid] = N;
     }
     __syncthreads();
-    done = stop_s;
-  }
-
-  if (ra.rep_list != nullptr)
-    for (int k = tid; k < ra.max_rep; k += kRThreads)
-      ra.rep_list[(int64_t)unit * ra.max_rep + k] = k < K ? order_s[k] : -1;
-  if (done < 0) {
-    if (tid == 0 && ra.n_rep != nullptr) ra.n_rep[unit] = -1;   // left to the whole-head fallback
+    if (tid == 0 && last) {
+      hd->status = kExhausted;
+      if (ra.n_rep != nullptr) ra.n_rep[unit] = -1;   // left to the whole-head fallback
+    }
     return;
   }
-  // repaired: new outputs, meter and raw; the KV head leaves the route mask
-  for (int i = tid; i < G * D; i += kRThreads) {
-    const int h = i / D, c = i % D;
-    const float o = (float)(O_s[h][c] / L_s[h]);
-    const int64_t oi = ((int64_t)b * a.n_q + (int64_t)kv * G + h) * D + c;
-    if (a.out_dtype == WC_F32) reinterpret_cast<float*>(a.out)[oi] = o;
-    else reinterpret_cast<uint16_t*>(a.out)[oi] = f32_to_bf16_rne(o);
-  }
+
+  // repaired after candidate `done`: state, meter and raw; the outputs follow in
+  // the final kernel
   if (tid < G) {
-    const double am1 = N_s[tid] / L_s[tid];
+    double L = hd->L[tid], N = hd->N[tid];
+    for (int jj = 0; jj <= done - j_lo; ++jj) {
+      L += dL_s[jj][tid];
+      N += dN_s[jj][tid];
+    }
+    hd->L[tid] = L;
+    hd->N[tid] = N;
+    const double am1 = N / L;
     const float raw = (float)(0.5 * am1 * (2.0 + am1));
-    const int64_t hi = (int64_t)b * a.n_q + (int64_t)kv * G + tid;
+    const UnitGeom u = unit_geom(a, unit);
+    const int64_t hi = (int64_t)u.b * a.n_q + (int64_t)u.kv * G + tid;
     a.meter[hi] = fminf(1.0f, raw);
     if (a.raw != nullptr) a.raw[hi] = raw;
   }
+  __syncthreads();
   if (tid == 0) {
+    hd->n_taken = done + 1;
+    hd->status = kRepaired;
     ra.mask_kv_out[unit] = 0;
     if (ra.n_rep != nullptr) ra.n_rep[unit] = done + 1;
   }
 }
 
+// ---------------------------------------------------------------------------
+// final: outputs of a repaired KV head, one workgroup per (KV head, query head):
+// the merged unnormalized output from the split records plus the corrections of
+// the taken blocks, summed in a fixed order, over the repaired weight sum
+template <int D>
+__global__ __launch_bounds__(kRThreads) void repair_final_kernel(RepairArgs ra) {
+  const DecodeArgs& a = ra.d;
+  constexpr int CW = 32;                  // channels per workgroup
+  constexpr int NSUB = kRThreads / CW;    // threads per channel
+  __shared__ double red_s[NSUB][CW];
+  __shared__ double w_s[kRThreads];
+  const int unit = blockIdx.x, h = blockIdx.y;
+  const RepHeader* hd = header_of(ra, unit);
+  if (hd->status != kRepaired || h >= a.group) return;
+  const int G = a.group;
+  const int tid = threadIdx.x;
+  const int cl = tid % CW, sub = tid / CW;
+  const int c = blockIdx.z * CW + cl;
+  const int rec = D + 2;
+  const UnitGeom u = unit_geom(a, unit);
+  const int P = hd->n_taken * ra.tiles;      // (candidate, tile) records, candidate-major
+  const double* base = corr_of(ra, unit, 0, 0) + h * rec + c;
+  const size_t stride = (size_t)G * rec;
+  double o = 0.0;
+  constexpr int U = 8;
+  for (int p0 = sub * U; p0 < P; p0 += NSUB * U) {
+    double v[U];
+#pragma unroll
+    for (int e = 0; e < U; ++e) v[e] = p0 + e < P ? base[(size_t)(p0 + e) * stride] : 0.0;
+#pragma unroll
+    for (int e = 0; e < U; ++e) o += v[e];
+  }
+  // the merged output of the split records: split weights once per workgroup
+  // (chunks of kRThreads splits), each thread's share of the splits
+  const int64_t R = (int64_t)partial_record_floats(D);
+  const float* recs = a.part + (((int64_t)u.b * a.n_q + (int64_t)u.kv * G + h) * a.n_splits) * R;
+  const double M = hd->M[h];
+  for (int j0 = 0; j0 < u.ns; j0 += kRThreads) {
+    __syncthreads();
+    if (j0 + tid < u.ns) w_s[tid] = exp((double)recs[(j0 + tid) * R + D] - M);
+    __syncthreads();
+    const int nj = min(kRThreads, u.ns - j0);
+    for (int jb = sub * U; jb < nj; jb += NSUB * U) {
+      float v[U];
+#pragma unroll
+      for (int e = 0; e < U; ++e) v[e] = jb + e < nj ? recs[(j0 + jb + e) * R + c] : 0.0f;
+#pragma unroll
+      for (int e = 0; e < U; ++e)
+        if (jb + e < nj) o += w_s[jb + e] * (double)v[e];
+    }
+  }
+  red_s[sub][cl] = o;
+  __syncthreads();
+  if (sub == 0) {
+    double t = red_s[0][cl];
+    for (int s2 = 1; s2 < NSUB; ++s2) t += red_s[s2][cl];
+    const float of = (float)(t / hd->L[h]);
+    const int64_t oi = ((int64_t)u.b * a.n_q + (int64_t)u.kv * G + h) * D + c;
+    if (a.out_dtype == WC_F32) reinterpret_cast<float*>(a.out)[oi] = of;
+    else reinterpret_cast<uint16_t*>(a.out)[oi] = f32_to_bf16_rne(of);
+  }
+}
+
+template <int D, int QT>
+void launch_repair_d(const RepairArgs& a, hipStream_t st) {
+  const int units = a.d.batch * a.d.n_kv;
+  const dim3 block(kRThreads);
+  hipLaunchKernelGGL((repair_rank_kernel<D>), dim3(units), block, 0, st, a);
+  const dim3 bgrid(a.max_rep * a.tiles, units);
+  for (int round = 0; round < 2; ++round) {
+    if (a.d.group <= 8) hipLaunchKernelGGL((repair_block_kernel<D, QT, 8>), bgrid, block, 0, st, a, round);
+    else hipLaunchKernelGGL((repair_block_kernel<D, QT, kRGMax>), bgrid, block, 0, st, a, round);
+    hipLaunchKernelGGL((repair_scan_kernel<D>), dim3(units), block, 0, st, a, round);
+  }
+  hipLaunchKernelGGL((repair_final_kernel<D>), dim3(units, a.d.group, D / 32), block, 0, st, a);
+}
+
 }  // namespace
 
 hipError_t launch_repair(const RepairArgs& a, hipStream_t st) {
-  const dim3 grid(a.d.batch * a.d.n_kv), block(kRThreads);
   if (a.d.head_dim == 64) {
-    if (a.d.q_dtype == WC_F32) hipLaunchKernelGGL((repair_kernel<64, WC_F32>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((repair_kernel<64, WC_BF16>), grid, block, 0, st, a);
+    if (a.d.q_dtype == WC_F32) launch_repair_d<64, WC_F32>(a, st);
+    else launch_repair_d<64, WC_BF16>(a, st);
   } else {
-    if (a.d.q_dtype == WC_F32) hipLaunchKernelGGL((repair_kernel<128, WC_F32>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((repair_kernel<128, WC_BF16>), grid, block, 0, st, a);
+    if (a.d.q_dtype == WC_F32) launch_repair_d<128, WC_F32>(a, st);
+    else launch_repair_d<128, WC_BF16>(a, st);
   }
   return hipGetLastError();
 }
 
 int repair_max_blocks() { return kRMaxBlocks; }
+
+size_t repair_unit_bytes(int group, int head_dim, int max_rep, int tiles) {
+  const size_t b = kRepHeaderBytes + (size_t)max_rep * tiles * group * (head_dim + 2) * sizeof(double);
+  return (b + 255) / 256 * 256;
+}
 
 }  // namespace wc

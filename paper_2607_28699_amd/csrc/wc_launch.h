@@ -120,7 +120,16 @@ struct RepairArgs {
   uint8_t* mask_kv_out;     // cleared for repaired KV heads (the same array as d.mask_kv)
   int32_t* rep_list;        // [batch][n_kv][max_rep] block order (-1 padded), or null
   int32_t* n_rep;           // [batch][n_kv] blocks taken, 0 not routed, -1 not repaired; or null
+  void* rws;                // repair workspace: per (sequence, KV head) a header and the
+                            // corrections of every (candidate block, 64-token tile)
+  size_t unit_bytes;        // workspace bytes per (sequence, KV head)
+  int tiles;                // 64-token tiles per block
+  int round0_cap;           // > 0: blocks in the first correction round (else the predicted count + 1)
 };
+constexpr int kRepHeaderBytes = 1024;
+// Repair workspace bytes per (sequence, KV head) (a multiple of 256).
+size_t repair_unit_bytes(int group, int head_dim, int max_rep, int tiles);
+inline int repair_tiles(int split_tokens) { return (split_tokens / 4 + 63) / 64; }
 
 struct GateArgs {
   const float* meter;

@@ -113,3 +113,14 @@ def test_workspace_size_and_argument_checks(L):
     assert L.wc_select_outlier_pairs(None, 1, 10, 4, 128, 0, 4, 16, 16, 4096, None) == _lib.WC_EINVAL
     assert L.wc_select_outlier_pairs(16, 1, 10, 4, 128, 0, 4, 16, 16, 8, None) == _lib.WC_EWORKSPACE
     assert L.wc_select_outlier_pairs(16, 1, 10, 4, 128, 0, 0, None, None, 0, None) == _lib.WC_OK
+
+
+def test_split_tokens_query(L):
+    # the library's choice is a multiple of 64, at least 256, and an explicit
+    # request is rounded up to a multiple of 64
+    for batch, n_kv, s in ((4, 4, 32769), (1, 4, 131072), (8, 4, 4096), (1, 1, 10)):
+        st = L.wc_decode_split_tokens(batch, n_kv, s, 0)
+        assert st >= 256 and st % 64 == 0
+    assert L.wc_decode_split_tokens(4, 4, 32769, 100) == 128
+    assert L.wc_decode_split_tokens(4, 0, 100, 0) == 0
+    assert L.wc_decode_split_tokens(-1, 4, 100, 0) == 0

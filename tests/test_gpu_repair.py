@@ -43,7 +43,7 @@ CASES = [
 ]
 
 
-def _run(case, cache, exact, tier, tau, max_blocks, force_valu):
+def _run(case, cache, exact, tier, tau, max_blocks, force_valu, round0=None):
     import torch
 
     import paper_2607_28699_amd as wc
@@ -56,6 +56,8 @@ def _run(case, cache, exact, tier, tau, max_blocks, force_valu):
     delta = 0.0 if tier == "A" else DLOC
     if force_valu:
         os.environ["WITCERT_FORCE_VALU"] = "1"
+    if round0 is not None:
+        os.environ["WITCERT_REPAIR_ROUND0"] = str(round0)
     try:
         ws = wc.decode_workspace(q.shape[0], wl.n_q, wl.n_kv, wl.d, L, SPLIT)
         if tier == "A":
@@ -70,6 +72,7 @@ def _run(case, cache, exact, tier, tau, max_blocks, force_valu):
                                      delta_loc=delta, max_blocks=max_blocks, split_tokens=SPLIT)
     finally:
         os.environ.pop("WITCERT_FORCE_VALU", None)
+        os.environ.pop("WITCERT_REPAIR_ROUND0", None)
     torch.cuda.synchronize()
     cpu = lambda t: t.cpu().numpy()
     return ([cpu(x) for x in before], cpu(out).astype(np.float64), cpu(meter), cpu(raw), cpu(mk),
@@ -163,3 +166,34 @@ def test_block_repair_parity(name, wl, lens, tier, m, max_blocks, path):
     S.say(f"  repaired KV heads: {n_fixed}, left to the fallback: {int((n_rep == -1).sum())}")
     if name != "gqa-small-budget":
         assert n_fixed > 0
+
+
+@pytest.mark.parametrize("round0", [1, 2])
+def test_block_repair_rounds_do_not_change_the_result(round0):
+    """The block corrections run in two rounds (the predicted count first); forcing
+    a first round of 1 or 2 blocks moves work into the second round and must give
+    the same repaired state bit for bit (the corrections are added in the repair
+    order whatever round computed them)."""
+    name, wl, lens, tier, m, max_blocks = CASES[1]
+    case = S.make_case(wl, lens, permute=True, layer=1)
+    refs = S.oracle_write(case, "int8_dither")
+    sm = 1 / np.sqrt(wl.d)
+    g = wl.n_q // wl.n_kv
+    raws = []
+    for b in range(len(lens)):
+        if case["seq_lens"][b] == 0:
+            continue
+        c = refs[b]
+        cb = odec.metered_decode(case["q"][b], c["khat"], c["vhat"], c["kw"], sm, wl.bands, wl.rope_layout)["c"]
+        for h in range(wl.n_q):
+            z = attention.logits(case["q"][b][h], c["khat"][:, h // g], sm)
+            raws.append(mt.raw_from_am1(mt.a_minus_one_logits(z, cb[h])))
+    tau = float(np.quantile(raws, 0.1))
+    cache = S.gpu_cache(case, "int8_dither")
+    exact = S.gpu_cache(case, "bf16")
+    ref = _run(case, cache, exact, tier, tau, max_blocks, False)
+    got = _run(case, cache, exact, tier, tau, max_blocks, False, round0=round0)
+    S.say(f"[repair rounds] round0={round0} blocks {ref[5].ravel().tolist()}")
+    assert np.any(ref[5] > round0), "no KV head needed the second round"
+    for x, y in zip(ref[1:], got[1:]):
+        assert np.array_equal(x, y)
