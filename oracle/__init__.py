@@ -25,6 +25,9 @@ theorem or table) and is written for reading against it, not for speed:
 * ``bypass``     fixed-channel outlier-pair bypass of the key cache with the
                  bypassed channels out of the amax (Sec. 4.2 outlier RoPE pairs;
                  Sec. 6.2 fixed-channel bypass, Tables 5 and 6).
+* ``groupscale`` per-token scales over 32-channel groups (Sec. 6.2 storage
+                 side, Table 4): a token scale and power-of-two group exponents,
+                 the quantizer with them, and the Tier-B radius it implies.
 * ``value``      value side: the output bound of Sec. 3, the value meter and the
                  joint K+V gate (Sec. 4.2 value side and joint event).
 * ``repair``     block-granular repair of gated heads (Sec. 6.3, block-level
@@ -37,4 +40,5 @@ theorem or table) and is written for reading against it, not for speed:
 Parity status of each function is listed in its docstring; every function is
 pinned by a CPU test in ``tests/test_oracle_*.py``.
 """
-from . import attention, bypass, decode, fpformats, gate, meter, philox, quantizer, repair, tierb, value  # noqa: F401
+from . import (attention, bypass, decode, fpformats, gate, groupscale, meter, philox, quantizer,  # noqa: F401
+               repair, tierb, value)

@@ -11,21 +11,24 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import attention, bypass, meter as mt, quantizer, value
+from . import attention, bypass, groupscale, meter as mt, quantizer, value
 from .philox import dither_values
 
 KINDS = ("int8_dither", "fp8_raw", "bf16")
 
 
 def write_cache(kind: str, k: np.ndarray, v: np.ndarray, slots: np.ndarray, layer: int,
-                seed: int, n_bands: int, layout: str = "half", pairs=None) -> dict:
+                seed: int, n_bands: int, layout: str = "half", pairs=None,
+                group_scales: bool = False) -> dict:
     """Quantize one sequence's tokens for every KV head.
 
     k, v: stored inputs [S, n_kv, d] (float); slots: int [S] physical slots.
     pairs: int [n_kv, m] bypassed RoPE pairs of the keys (int8 only; ``bypass``).
+    group_scales: int8 with per-32-channel group exponents (``groupscale``).
     Returns reconstructions khat/vhat [S, n_kv, d], key witness kw [S, n_kv, B],
     for the quantized kinds the value residual and value norms vr, vn [S, n_kv]
-    (``value``) and, for int8, codes and scales; with pairs also the stored fp16 values
+    (``value``) and, for int8, codes and scales (and with group scales the group
+    exponents ke, ve [S, n_kv, d/32]); with pairs also the stored fp16 values
     ko [S, n_kv, 2m] and their channels chans [n_kv, 2m].
     """
     k = np.asarray(k, dtype=np.float64)
@@ -38,6 +41,11 @@ def write_cache(kind: str, k: np.ndarray, v: np.ndarray, slots: np.ndarray, laye
             out[key] = np.empty((S, n_kv, d), dtype=np.int64)
         for key in ("ks", "vs"):
             out[key] = np.empty((S, n_kv))
+    if group_scales:
+        if kind != "int8_dither":
+            raise ValueError("group scales are defined for the int8 cache")
+        for key in ("ke", "ve"):
+            out[key] = np.empty((S, n_kv, d // groupscale.GROUP), dtype=np.int64)
     if pairs is not None:
         if kind != "int8_dither":
             raise ValueError("the outlier bypass is defined for the int8 cache")
@@ -45,7 +53,16 @@ def write_cache(kind: str, k: np.ndarray, v: np.ndarray, slots: np.ndarray, laye
         out["chans"] = np.stack([bypass.bypass_channels(pairs[h], d, layout) for h in range(n_kv)])
         out["ko"] = np.empty((S, n_kv, out["chans"].shape[1]))
     for h in range(n_kv):
-        if kind == "int8_dither" and pairs is not None:
+        if kind == "int8_dither" and group_scales:
+            xi = dither_values(slots, d, layer, h, seed)
+            ch = None if pairs is None else out["chans"][h]
+            kc, ks, ke, ko, kh = groupscale.quantize(k[:, h], xi, ch)
+            vc, vs, ve, _, vh = groupscale.quantize(v[:, h], xi)
+            out["kcode"][:, h], out["ks"][:, h], out["ke"][:, h] = kc, ks, ke
+            out["vcode"][:, h], out["vs"][:, h], out["ve"][:, h] = vc, vs, ve
+            if ko is not None:
+                out["ko"][:, h] = ko
+        elif kind == "int8_dither" and pairs is not None:
             xi = dither_values(slots, d, layer, h, seed)
             kc, ks, ko, kh = bypass.quantize_bypass(k[:, h], xi, out["chans"][h])
             vc, vs, _, vh = quantizer.int8_quantize_slots(v[:, h], slots, layer, h, seed)
