@@ -95,6 +95,10 @@ extern "C" {
  *   v_norm     [num_blocks][n_kv_heads][16] fp16              value side (optional, both or
  *              neither, quantized kinds only): ||vhat_t - v_t|| rounded up and ||v_t||
  *              rounded down, from float64 norms (Sec. 3 output bound; Sec. 4.2 value side)
+ *   k_gexp,
+ *   v_gexp     [num_blocks][n_kv_heads][16] uint16            group scales (optional, both or
+ *              neither, INT8_DITHER only): bits 4g..4g+3 hold the exponent e_g of channel
+ *              group g (channels 32g..32g+31); the group's step is s * 2^-e_g
  * Element type of k_data/v_data: int8 code stored excess-128, i.e. the byte code + 128
  * (INT8_DITHER; codes lie in [-127, 127]), E4M3 byte (FP8_RAW), bf16 (BF16).
  * Band b holds the channels of RoPE pairs b*P .. b*P+P-1, P = head_dim/(2*n_bands)
@@ -110,6 +114,15 @@ extern "C" {
  * second channel, pair 1 first, ...); the pair channels are (j, j + head_dim/2)
  * for WC_ROPE_HALF and (2j, 2j + 1) for WC_ROPE_INTERLEAVED.  Values stay within
  * +-65504.  Values are not bypassed.  m is even, 0 <= m <= 16.
+ *
+ * Group scales (INT8_DITHER; Sec. 6.2 storage side: per token, per group of 32
+ * channels; Table 4 granularity): with k_gexp/v_gexp set, each token keeps its fp16
+ * scale s and every 32-channel group g gets the step s * 2^-e_g, e_g in [0, 15] the
+ * largest exponent with amax_g * 2^e_g <= amax (amax over the token's quantized
+ * channels, amax_g over the group's; 15 for an all-zero group).  Power-of-two
+ * ratios keep every dequantized code an exact fp16 multiple, so the decode's
+ * matrix-core operands stay exact.  Bypassed channels leave amax_g as they leave
+ * amax.
  */
 typedef struct wc_cache {
     int32_t  kind;          /* WC_KIND_*                                       */
@@ -126,6 +139,7 @@ typedef struct wc_cache {
     const int32_t* outlier_pairs;      /* [n_kv_heads][m] device, or NULL when m == 0  */
     void*    k_outlier;                /* see above, or NULL when m == 0               */
     void    *v_resid, *v_norm;          /* value side, or both NULL                     */
+    void    *k_gexp, *v_gexp;           /* group exponents, or both NULL                */
 } wc_cache;
 
 const char* wc_strerror(int status);
@@ -133,13 +147,15 @@ int         wc_version(void);   /* 100*major + minor */
 
 /*
  * Bytes of each array of a cache (k_data, v_data, k_scale, v_scale, k_witness,
- * k_outlier, v_resid, v_norm) written to sizes[0..7]; returns their sum, 0 on bad
- * arguments.  The "exact byte account" of the cache (Sec. 5 memory saving;
- * Sec. 6.2 acceptance; Table 6: 4m bytes per token and KV head for the bypassed
- * pairs; 2 + 2 bytes for the value side when value_side != 0).
+ * k_outlier, v_resid, v_norm, k_gexp, v_gexp) written to sizes[0..9]; returns
+ * their sum, 0 on bad arguments.  The "exact byte account" of the cache (Sec. 5
+ * memory saving; Sec. 6.2 acceptance; Table 6: 4m bytes per token and KV head for
+ * the bypassed pairs; 2 + 2 bytes for the value side when value_side != 0; 2 + 2
+ * bytes for the group exponents when group_scales != 0).
  */
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim,
-                      int n_bands, int n_outlier_pairs, int value_side, size_t sizes[8]);
+                      int n_bands, int n_outlier_pairs, int value_side, int group_scales,
+                      size_t sizes[10]);
 
 /*
  * Fixed outlier-pair set of each KV head (Sec. 6.2 fixed-channel bypass; Sec. 4.2
@@ -166,7 +182,9 @@ int wc_select_outlier_pairs(const void* k, int in_dtype, int64_t n_tok, int n_kv
  *   INT8_DITHER: s = fp16_round_up(fl32(amax/126.5)) per (token, head, tensor);
  *                xi_c = (u_c - 127.5)/256 with u_c the Philox4x32-10 byte of channel c
  *                (key = seed, counter = (c/16, slot lo, slot hi, layer<<16 | h)),
- *                shared by K and V; code = rint_even(fl32(fl32(x*fl32(1/s)) + xi));
+ *                shared by K and V; code = rint_even(fl32(fl32(x*inv) + xi)) with
+ *                inv = fl32(1/s), times 2^e_g with group scales (then k_gexp/v_gexp
+ *                receive the exponents);
  *                with bypassed pairs (n_outlier_pairs > 0) the amax and the codes
  *                skip their channels and k_outlier receives fp16(x) of them;
  *   FP8_RAW:     code = E4M3(x), nearest-even, saturating at +-448;

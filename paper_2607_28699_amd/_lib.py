@@ -35,6 +35,7 @@ class WcCache(ctypes.Structure):
         ("n_outlier_pairs", ctypes.c_int32), ("reserved", ctypes.c_int32),
         ("outlier_pairs", ctypes.c_void_p), ("k_outlier", ctypes.c_void_p),
         ("v_resid", ctypes.c_void_p), ("v_norm", ctypes.c_void_p),
+        ("k_gexp", ctypes.c_void_p), ("v_gexp", ctypes.c_void_p),
     ]
 
 
@@ -61,7 +62,7 @@ def lib() -> ctypes.CDLL:
         "wc_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         "wc_version": (ctypes.c_int, []),
         "wc_cache_bytes": (sz, [ctypes.c_int, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-                                ctypes.c_int, ctypes.c_int, ctypes.POINTER(sz)]),
+                                ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(sz)]),
         "wc_select_workspace_size": (sz, [i64, ctypes.c_int, ctypes.c_int]),
         "wc_select_outlier_pairs": (ctypes.c_int, [vp, ctypes.c_int, i64, ctypes.c_int, ctypes.c_int,
                                                    ctypes.c_int, ctypes.c_int, vp, vp, sz, vp]),

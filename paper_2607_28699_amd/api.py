@@ -42,10 +42,10 @@ def _dev_check(*ts):
 
 
 def cache_bytes(kind: str, num_blocks: int, n_kv: int, head_dim: int, n_bands: int,
-                n_outlier_pairs: int = 0, value_side: bool = False):
-    sizes = (ctypes.c_size_t * 8)()
+                n_outlier_pairs: int = 0, value_side: bool = False, group_scales: bool = False):
+    sizes = (ctypes.c_size_t * 10)()
     total = lib().wc_cache_bytes(KINDS[kind], num_blocks, n_kv, head_dim, n_bands, n_outlier_pairs,
-                                 int(value_side), sizes)
+                                 int(value_side), int(group_scales), sizes)
     if total == 0:
         raise _lib.WitCertError("bad cache geometry")
     return total, list(sizes)
@@ -65,13 +65,15 @@ class PagedCache:
     device: str = "cuda"
     n_outlier_pairs: int = 0
     value_side: bool = False
+    group_scales: bool = False
     tensors: dict = field(default_factory=dict)
 
     def __post_init__(self):
         m = self.n_outlier_pairs
         total, sizes = cache_bytes(self.kind, self.num_blocks, self.n_kv, self.head_dim, self.n_bands, m,
-                                   self.value_side)
-        names = ("k_data", "v_data", "k_scale", "v_scale", "k_witness", "k_outlier", "v_resid", "v_norm")
+                                   self.value_side, self.group_scales)
+        names = ("k_data", "v_data", "k_scale", "v_scale", "k_witness", "k_outlier", "v_resid", "v_norm",
+                 "k_gexp", "v_gexp")
         slots = self.num_blocks * WC_BLOCK_TOKENS * self.n_kv
         shapes = {
             "k_data": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.head_dim),
@@ -82,6 +84,8 @@ class PagedCache:
             "k_outlier": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, 2 * m),
             "v_resid": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
             "v_norm": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
+            "k_gexp": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
+            "v_gexp": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
         }
         # int8 codes are stored excess-128 (byte = code + 128)
         el = {"int8_dither": torch.uint8, "fp8_raw": torch.uint8, "bf16": torch.bfloat16}[self.kind]
@@ -112,7 +116,7 @@ class PagedCache:
                        _ptr(t["k_data"]), _ptr(t["v_data"]), _ptr(t["k_scale"]),
                        _ptr(t["v_scale"]), _ptr(t["k_witness"]), self.n_outlier_pairs, 0,
                        _ptr(t["outlier_pairs"]), _ptr(t["k_outlier"]), _ptr(t["v_resid"]),
-                       _ptr(t["v_norm"]))
+                       _ptr(t["v_norm"]), _ptr(t["k_gexp"]), _ptr(t["v_gexp"]))
 
 
 def quantize_write(cache: PagedCache, k: torch.Tensor, v: torch.Tensor, slots: torch.Tensor) -> None:

@@ -878,7 +878,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
 }  // namespace
 
 bool mfma_decode_supported(const DecodeArgs& a) {
-  return a.head_dim == kD && a.q_dtype == WC_BF16 && a.group <= 16 &&
+  return a.head_dim == kD && a.q_dtype == WC_BF16 && a.group <= 16 && a.k_gexp == nullptr &&
          (a.kind == WC_KIND_BF16 || a.n_bands == 8 || a.n_bands == 16);
 }
 

@@ -47,6 +47,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   __shared__ uint32_t xi_s[kT][D / 4];
   __shared__ float vs_s[kT];
   __shared__ float vr_s[kT], vn_s[kT];   // value side: stored ||vhat - v|| and ||v|| of the tile
+  __shared__ uint32_t ve_s[kT];           // group scales: the tile's value exponent words
+  __shared__ float qg_s[kGMax][8];        // group scales, Tier B: ||q_g||^2 (0..3), ||q_g||_1 (4..7)
   __shared__ float alpha_s[kGMax];
   __shared__ int64_t slot_s[kT];
 
@@ -100,6 +102,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
     }
     __syncthreads();
   }
+  const bool grouped = KIND == WC_KIND_INT8_DITHER && a.k_gexp != nullptr;
   if constexpr (METER) {
     if (a.tierb_delta > 0.0f) {
       for (int h = tid; h < G; h += kThreads) {
@@ -110,8 +113,23 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         }
         ab_s[h] = tierb_factor(sq, l1, L, a.tierb_delta, a.sm_scale);
       }
+      if (grouped) {   // per-group norms of the quantized channels
+        for (int i = tid; i < G * (D / 32); i += kThreads) {
+          const int h = i / (D / 32), gg = i % (D / 32);
+          float sq = 0.0f, l1 = 0.0f;
+          for (int c = 32 * gg; c < 32 * gg + 32; ++c) {
+            sq = fmaf(q_s[h][c], q_s[h][c], sq);
+            l1 += fabsf(q_s[h][c]);
+          }
+          qg_s[h][gg] = sq;
+          qg_s[h][4 + gg] = l1;
+        }
+      }
     }
   }
+  // Tier B over group steps: u_t = sm (rt sqrt(sum_g s_g^2 ||q_g||^2) + sum_g s_g ||q_g||_1 / 256)
+  const float rt = METER && grouped && a.tierb_delta > 0.0f
+                       ? sqrtf(2.0f * logf(2.0f * (float)L / a.tierb_delta) / 12.0f) : 0.0f;
 
   const bool vm = METER && a.meter_v != nullptr;   // value side
   float m_run[4], l_run[4], n_run[4], e_run[4], vmax_run = 0.0f;
@@ -154,12 +172,14 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
           const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.k_data) +
                                                            (page * kBlockTokens + off) * D + c0);
           const float s = f16_to_f32(a.k_scale[page * kBlockTokens + off]);
+          const uint32_t kgw = grouped ? a.k_gexp[page * kBlockTokens + off] : 0u;
 #pragma unroll
           for (int gi = 0; gi < NG; ++gi) {
             const uint4 cw = kp[gi];
             const U4 r = dither_block(c0 / 16 + gi, slot, layer_head, a.key0, a.key1);
             const uint32_t codes[4] = {cw.x, cw.y, cw.z, cw.w};
             const uint32_t rw[4] = {r.x, r.y, r.z, r.w};
+            const float sg = s * group_step_factor(kgw, c0 + 16 * gi);   // the group's step (exact)
 #pragma unroll
             for (int w4 = 0; w4 < 4; ++w4) {
               xi_s[i][(c0 + 16 * gi) / 4 + w4] = rw[w4];
@@ -167,11 +187,14 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
               for (int j = 0; j < 4; ++j) {
                 const float code = (float)((int32_t)((codes[w4] >> (8 * j)) & 0xFFu) - 128);   // excess-128
                 const float xi = dither_value((rw[w4] >> (8 * j)) & 0xFFu);
-                kval[16 * gi + 4 * w4 + j] = s * (code - xi);
+                kval[16 * gi + 4 * w4 + j] = sg * (code - xi);
               }
             }
           }
-          if (part == 0) vs_s[i] = f16_to_f32(a.v_scale[page * kBlockTokens + off]);
+          if (part == 0) {
+            vs_s[i] = f16_to_f32(a.v_scale[page * kBlockTokens + off]);
+            ve_s[i] = grouped ? a.v_gexp[page * kBlockTokens + off] : 0u;
+          }
         } else if constexpr (KIND == WC_KIND_FP8_RAW) {
           const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.k_data) +
                                                            (page * kBlockTokens + off) * D + c0);
@@ -237,7 +260,20 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
               gb = fmaf(fabsf(qo_s[h][part + 4 * k]), fmaf(fabsf(kov[k]), 0x1p-11f, 0x1p-25f), gb);
           gb += __shfl_xor(gb, 1, 4);
           gb += __shfl_xor(gb, 2, 4);
-          if (part == 0) cb_s[h][i] = fmaf(ab_s[h], s, gb * a.sm_scale);
+          if (part == 0) {
+            if (grouped) {
+              const uint32_t kgw = valid ? a.k_gexp[page * kBlockTokens + off] : 0u;
+              float s2 = 0.0f, s1 = 0.0f;
+              for (int gg = 0; gg < D / 32; ++gg) {
+                const float sg = s * group_step_factor(kgw, 32 * gg);
+                s2 = fmaf(sg * sg, qg_s[h][gg], s2);
+                s1 = fmaf(sg, qg_s[h][4 + gg], s1);
+              }
+              cb_s[h][i] = a.sm_scale * (fmaf(rt, sqrtf(s2), s1 * (1.0f / 256.0f)) + gb);
+            } else {
+              cb_s[h][i] = fmaf(ab_s[h], s, gb * a.sm_scale);
+            }
+          }
         }
       } else if constexpr (METER) {
         float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -332,6 +368,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
             if constexpr (KIND == WC_KIND_INT8_DITHER) {
               const uint32_t u = (xi_s[i0 + j][c3 >> 2] >> (8 * (c3 & 3))) & 0xFFu;
               vv[j] = (float)((int32_t)byte - 128) - dither_value(u);   // excess-128 code
+              if (grouped) vv[j] *= group_step_factor(ve_s[i0 + j], c3);
             } else {
               vv[j] = e4m3_to_f32(byte);
             }

@@ -250,6 +250,8 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
   __shared__ int64_t slot_s[kRTile];
   __shared__ double dl_s[GM], dn_s[GM];
   __shared__ uint16_t ko_s[kRTile][32];  // stored fp16 values of the bypassed pairs (2m <= 32)
+  __shared__ float qg_s[GM][8];          // group scales, Tier B: ||q_g||^2 (0..3), ||q_g||_1 (4..7)
+  __shared__ uint32_t ve_s[kRTile];      // group scales: value exponent words of the tile
   // logits and bounds of phases 1-2, then the output reduction of phase 3
   constexpr int kLogitBytes = 3 * GM * kRTile * 4;
   constexpr int kRedBytes = (NSUB > 1 ? NSUB - 1 : 1) * GM * D * 8;
@@ -309,15 +311,22 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
     qbn_s[h][bb] = sqrtf(acc) * a.sm_scale;
   }
   __syncthreads();
+  const bool grouped = a.k_gexp != nullptr;
   if (tierb && tid < G) {
     float sq = 0.0f, l1 = 0.0f;
     for (int c = 0; c < D; ++c) {
       const float x = opos_s[c] >= 0 ? 0.0f : q_s[tid][c];
       sq = fmaf(x, x, sq);
       l1 += fabsf(x);
+      if (grouped && (c & 31) == 31) {   // per-group norms of the quantized channels
+        qg_s[tid][c >> 5] = sq;
+        qg_s[tid][4 + (c >> 5)] = l1;
+        sq = l1 = 0.0f;
+      }
     }
-    ab_s[tid] = tierb_factor(sq, l1, u.L, a.tierb_delta, a.sm_scale);
+    if (!grouped) ab_s[tid] = tierb_factor(sq, l1, u.L, a.tierb_delta, a.sm_scale);
   }
+  const float rt = tierb && grouped ? sqrtf(2.0f * logf(2.0f * (float)u.L / a.tierb_delta) / 12.0f) : 0.0f;
   __syncthreads();
 
   // ---- phase 1: compressed and exact logits, bounds (thread: token i, channel quarter) ----
@@ -340,6 +349,7 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
 #pragma unroll
     for (int h = 0; h < GM; ++h) dq[h] = dx[h] = cq[h] = 0.0f;
     float s = 0.0f;
+    uint32_t kgw = 0;
     if (valid) {
       uint32_t kb[CH / 4];
       const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.k_data) + row * D + c0);
@@ -357,7 +367,11 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
       }
       const bool int8 = a.kind == WC_KIND_INT8_DITHER;
       if (int8) s = f16_to_f32(a.k_scale[row]);
-      if (part == 0) vs_s[i] = int8 ? f16_to_f32(a.v_scale[row]) : 1.0f;
+      if (part == 0) {
+        vs_s[i] = int8 ? f16_to_f32(a.v_scale[row]) : 1.0f;
+        ve_s[i] = grouped ? a.v_gexp[row] : 0u;
+      }
+      kgw = grouped ? a.k_gexp[row] : 0u;
 #pragma unroll
       for (int gi = 0; gi < NG; ++gi) {
         uint32_t rw[4] = {0, 0, 0, 0};
@@ -373,7 +387,8 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
           for (int e = 0; e < 4; ++e) {
             const int c = 16 * gi + 4 * w4 + e;
             const uint32_t byte = (kb[c >> 2] >> (8 * (c & 3))) & 0xFFu;
-            float kq = int8 ? s * ((float)((int32_t)byte - 128) - dither_value((rw[w4] >> (8 * e)) & 0xFFu))
+            const float sg = s * group_step_factor(kgw, c0 + c);
+            float kq = int8 ? sg * ((float)((int32_t)byte - 128) - dither_value((rw[w4] >> (8 * e)) & 0xFFu))
                             : e4m3_to_f32(byte);
             const int op = m2 > 0 ? opos_s[c0 + c] : -1;
             if (op >= 0) kq = f16_to_f32(ko_s[i][op]);   // bypassed pair: stored fp16
@@ -425,7 +440,17 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
       if (part == 0) {
         lq_s[h][i] = vq * a.sm_scale;
         lx_s[h][i] = vx * a.sm_scale;
-        cb_s[h][i] = tierb ? fmaf(ab_s[h], s, cp) : cp;
+        if (tierb && grouped) {
+          float s2 = 0.0f, s1 = 0.0f;
+          for (int gg = 0; gg < D / 32; ++gg) {
+            const float sg = s * group_step_factor(kgw, 32 * gg);
+            s2 = fmaf(sg * sg, qg_s[h][gg], s2);
+            s1 = fmaf(sg, qg_s[h][4 + gg], s1);
+          }
+          cb_s[h][i] = a.sm_scale * (fmaf(rt, sqrtf(s2), s1 * (1.0f / 256.0f))) + cp;
+        } else {
+          cb_s[h][i] = tierb ? fmaf(ab_s[h], s, cp) : cp;
+        }
       }
     }
   }
@@ -496,7 +521,8 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
         float vq;
         if (a.kind == WC_KIND_INT8_DITHER) {
           const uint32_t xw = xi_s[i][c >> 2];
-          vq = vs_s[i] * ((float)((int32_t)byte - 128) - dither_value((xw >> (8 * (c & 3))) & 0xFFu));
+          vq = vs_s[i] * group_step_factor(ve_s[i], c) *
+               ((float)((int32_t)byte - 128) - dither_value((xw >> (8 * (c & 3))) & 0xFFu));
         } else {
           vq = e4m3_to_f32(byte);
         }

@@ -27,6 +27,8 @@ struct WriteArgs {
   uint16_t* k_outlier;      // [blocks][n_kv][16][2 n_pairs] fp16
   uint16_t* v_resid;        // value side (or null): ||vhat - v|| fp16 up, [blocks][n_kv][16]
   uint16_t* v_norm;         // ||v|| fp16 down, same layout
+  uint16_t* k_gexp;         // group scales (or null): 4-bit exponent per 32-channel group,
+  uint16_t* v_gexp;         // [blocks][n_kv][16]
 };
 
 struct SelectArgs {
@@ -82,7 +84,16 @@ struct DecodeArgs {
   const uint16_t* v_norm;
   float* meter_v;           // [batch][n_q]
   float gate_tau_v;
+  // group scales (null: one scale per token): exponent e_g of channel group g in
+  // bits 4g..4g+3, the group's step s * 2^-e_g
+  const uint16_t* k_gexp;
+  const uint16_t* v_gexp;
 };
+
+// 2^-e_g of channel c's group from a token's exponent word (exact).
+__device__ __forceinline__ float group_step_factor(uint32_t gexp, int c) {
+  return ldexpf(1.0f, -(int)((gexp >> (4 * (c >> 5))) & 15u));
+}
 
 // Channel of member `second` of RoPE pair j (pair index clamped into range).
 __host__ __device__ inline int pair_channel(int j, int second, int d, bool interleaved) {

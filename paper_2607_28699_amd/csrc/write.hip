@@ -122,15 +122,32 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
       if (((bmask >> i) & 1u) == 0) ak = fmaxf(ak, fabsf(k[i]));
       av = fmaxf(av, fabsf(v[i]));
     }
+    // group scales (Sec. 6.2 storage side): the 32-channel group of this lane is
+    // lanes g, g^1; its exponent is the largest e <= 15 with amax_g 2^e <= amax
+    const bool grouped = a.k_gexp != nullptr;
+    float akg = 0.0f, avg = 0.0f;
+    if (grouped) {
+      akg = fmaxf(ak, __shfl_xor(ak, 1, LPT));
+      avg = fmaxf(av, __shfl_xor(av, 1, LPT));
+    }
 #pragma unroll
     for (int o = 1; o < LPT; o <<= 1) {
       ak = fmaxf(ak, __shfl_xor(ak, o, LPT));
       av = fmaxf(av, __shfl_xor(av, o, LPT));
     }
+    int ek = 0, ev = 0;
+    if (grouped) {
+      while (ek < 15 && ldexpf(akg, ek + 1) <= ak) ++ek;
+      while (ev < 15 && ldexpf(avg, ev + 1) <= av) ++ev;
+    }
     uint16_t skb, svb;
     float sk, ikk, sv, ivv;
     int8_scale(ak, skb, sk, ikk);
     int8_scale(av, svb, sv, ivv);
+    ikk = ldexpf(ikk, ek);                       // fl32(1/s) 2^e_g: exact
+    ivv = ldexpf(ivv, ev);
+    const double stk = ldexp((double)sk, -ek);   // the group's step s 2^-e_g
+    const double stv = ldexp((double)sv, -ev);
 
     const U4 rnd = dither_block(g, slot, ((uint32_t)a.layer << 16) | (uint32_t)h, a.key0, a.key1);
     const uint32_t words[4] = {rnd.x, rnd.y, rnd.z, rnd.w};
@@ -143,9 +160,9 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
       const float ck = rintf(__fadd_rn(__fmul_rn(byp ? 0.0f : k[i], ikk), xi));
       const float cv = rintf(__fadd_rn(__fmul_rn(v[i], ivv), xi));
       const double rk = byp ? (double)(float)(_Float16)k[i] - (double)k[i]     // fp16(k) - k
-                            : (double)sk * (double)(ck - xi) - (double)k[i];   // khat - k
+                            : stk * (double)(ck - xi) - (double)k[i];          // khat - k
       r2[lth][16 * g + i] = rk * rk;
-      const double rv = (double)sv * (double)(cv - xi) - (double)v[i];         // vhat - v
+      const double rv = stv * (double)(cv - xi) - (double)v[i];                // vhat - v
       vr2 = fma(rv, rv, vr2);
       vn2 = fma((double)v[i], (double)v[i], vn2);
       // codes are stored excess-128: byte = code + 128
@@ -156,6 +173,17 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
         *vd = (uint8_t)((int32_t)cv + 128);
       }
     }
+    // group exponents of the token-head: nibble g/2 from the first lane of each group
+    uint32_t ekw = 0, evw = 0;
+    if (grouped) {
+      ekw = (g & 1) ? 0u : (uint32_t)ek << (4 * (g >> 1));
+      evw = (g & 1) ? 0u : (uint32_t)ev << (4 * (g >> 1));
+#pragma unroll
+      for (int o = 1; o < LPT; o <<= 1) {
+        ekw |= __shfl_xor(ekw, o, LPT);
+        evw |= __shfl_xor(evw, o, LPT);
+      }
+    }
     if (active) {
       uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(a.k_data) +
                                            (bh * kBlockTokens + off) * D + 16 * g);
@@ -163,6 +191,10 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
       if (g == 0) {
         a.k_scale[bh * kBlockTokens + off] = skb;
         a.v_scale[bh * kBlockTokens + off] = svb;
+        if (grouped) {
+          a.k_gexp[bh * kBlockTokens + off] = (uint16_t)ekw;
+          a.v_gexp[bh * kBlockTokens + off] = (uint16_t)evw;
+        }
       }
       if (bmask != 0) {
         // fp16 (nearest-even) values of the bypassed channels, in pair order

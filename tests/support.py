@@ -49,10 +49,10 @@ def case_pairs(case, m):
     return np.stack([obp.select_pairs(k[:, h], m, wl.rope_layout) for h in range(wl.n_kv)])
 
 
-def gpu_cache(case, kind, seed=None, pairs=None, value_side=False):
+def gpu_cache(case, kind, seed=None, pairs=None, value_side=False, group_scales=False):
     """Write every sequence of the case into a fresh GPU cache through wc_quantize_write
     (pairs [n_kv, m]: bypassed RoPE pairs of the keys; value_side: store the value
-    residual and value norms)."""
+    residual and value norms; group_scales: per-32-channel group exponents)."""
     import torch
 
     import paper_2607_28699_amd as wc
@@ -60,7 +60,7 @@ def gpu_cache(case, kind, seed=None, pairs=None, value_side=False):
     m = 0 if pairs is None else int(np.asarray(pairs).shape[1])
     c = wc.PagedCache(kind, case["nblocks"], wl.n_kv, wl.d, wl.bands, layer=case["layer"],
                       seed=wl.philox_seed() if seed is None else seed, rope_layout=wl.rope_layout,
-                      n_outlier_pairs=m, value_side=value_side)
+                      n_outlier_pairs=m, value_side=value_side, group_scales=group_scales)
     if m:
         c.set_outlier_pairs(torch.from_numpy(np.asarray(pairs, dtype=np.int32)))
     dt = torch_dtype(wl)
@@ -88,10 +88,10 @@ def gpu_decode(case, cache, split_tokens=0, out_dtype=None):
     return out.float().cpu().numpy().astype(np.float64), meter.cpu().numpy(), raw.cpu().numpy()
 
 
-def oracle_write(case, kind, pairs=None):
+def oracle_write(case, kind, pairs=None, group_scales=False):
     wl = case["wl"]
     return [odec.write_cache(kind, k, v, s, case["layer"], wl.philox_seed(), wl.bands, wl.rope_layout,
-                             pairs=pairs)
+                             pairs=pairs, group_scales=group_scales)
             for k, v, s in zip(case["k"], case["v"], case["slots"])]
 
 
@@ -133,6 +133,11 @@ def read_cache(cache, slots):
     if t.get("v_resid") is not None:
         out["vr"] = ofp_f16(t["v_resid"].numpy()[blk, :, off])
         out["vn"] = ofp_f16(t["v_norm"].numpy()[blk, :, off])
+    if t.get("k_gexp") is not None:   # group exponents: 4 bits per 32-channel group
+        ng = cache.head_dim // 32
+        for name, key in (("k_gexp", "ke"), ("v_gexp", "ve")):
+            w = t[name].numpy().view(np.uint16)[blk, :, off].astype(np.int64)
+            out[key] = np.stack([(w >> (4 * g)) & 15 for g in range(ng)], axis=-1)
     return out
 
 

@@ -39,26 +39,31 @@ def test_status_strings_and_version(L):
 
 
 def test_cache_byte_account(L):
-    sizes = (ctypes.c_size_t * 8)()
+    sizes = (ctypes.c_size_t * 10)()
     # one KV head, 32768 tokens, d = 128, B = 8: 128 + 128 + 2 + 2 + 16 = 276 B per token
-    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, 0, sizes)
+    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, 0, 0, sizes)
     assert tot == 32768 * 276
-    assert list(sizes) == [32768 * 128, 32768 * 128, 65536, 65536, 32768 * 16, 0, 0, 0]
-    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, 0, sizes) == 32768 * 272
-    assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, 0, 0, sizes) == 32768 * 512
-    assert L.wc_cache_bytes(7, 1, 1, 128, 8, 0, 0, sizes) == 0
+    assert list(sizes) == [32768 * 128, 32768 * 128, 65536, 65536, 32768 * 16, 0, 0, 0, 0, 0]
+    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, 0, 0, sizes) == 32768 * 272
+    assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, 0, 0, 0, sizes) == 32768 * 512
+    assert L.wc_cache_bytes(7, 1, 1, 128, 8, 0, 0, 0, sizes) == 0
     # bypassed pairs: 2m fp16 values per token and KV head (Table 6: 16 B at m = 4)
     for m in (2, 4, 8, 16):
-        tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, m, 0, sizes)
+        tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, m, 0, 0, sizes)
         assert sizes[5] == 32768 * 4 * m and tot == 32768 * (276 + 4 * m)
     for bad in (-2, 3, 18):
-        assert L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, bad, 0, sizes) == 0
-    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 4, 0, sizes) == 0
+        assert L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, bad, 0, 0, sizes) == 0
+    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 4, 0, 0, sizes) == 0
     # value side: 2 + 2 bytes per token-head (residual and value norms), quantized kinds only
-    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, 1, sizes)
+    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, 1, 0, sizes)
     assert tot == 32768 * 280 and sizes[6] == sizes[7] == 65536
-    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, 1, sizes) == 32768 * 276
-    assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, 0, 1, sizes) == 0
+    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, 1, 0, sizes) == 32768 * 276
+    assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, 0, 1, 0, sizes) == 0
+    # group scales: one 16-bit exponent word (4 bits per 32-channel group) per token-head
+    # and tensor, INT8 only (Table 4: the paper's fp16 group scales would be 8 + 8 bytes)
+    tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, 0, 1, sizes)
+    assert tot == 32768 * 280 and sizes[8] == sizes[9] == 65536
+    assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, 0, 1, sizes) == 0
 
 
 def test_workspace_size_and_argument_checks(L):
