@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--outlier-pairs", type=int, default=4,
                     help="bypassed RoPE pairs per KV head for the bypass measurement (0: skip it)")
     ap.add_argument("--tau-v", type=float, default=0.05, help="value-side threshold of the joint gate")
+    ap.add_argument("--no-group-scales", dest="group_scales", action="store_false",
+                    help="skip the measurement over caches with 32-channel group scales")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -164,7 +166,7 @@ def main():
     # With --outlier-pairs m > 0 every layer also gets an INT8 cache whose keys
     # bypass the m RoPE pairs of largest energy over the layer's prefill keys (the
     # fixed per-(layer, KV head) set of the outlier-pair bypass), chosen on the GPU.
-    caches, exact, byp_caches = [], [], []
+    caches, exact, byp_caches, gs_caches = [], [], [], []
     gen0 = None
     m_byp = args.outlier_pairs
     for layer in range(wl.n_layers):
@@ -187,6 +189,14 @@ def main():
             for k, v, sl in gen:
                 wc.quantize_write(cb, k, v, sl)
             byp_caches.append(cb)
+            if args.group_scales:   # the same bypass with per-32-channel group scales
+                cg = wc.PagedCache("int8_dither", lay.nblocks, wl.n_kv, wl.d, wl.bands, layer=layer,
+                                   seed=seed, rope_layout=wl.rope_layout, n_outlier_pairs=m_byp,
+                                   value_side=True, group_scales=True)
+                cg.set_outlier_pairs(cb.tensors["outlier_pairs"])
+                for k, v, sl in gen:
+                    wc.quantize_write(cg, k, v, sl)
+                gs_caches.append(cg)
         torch.cuda.synchronize()
         caches.append(c)
         exact.append(e)
@@ -333,9 +343,10 @@ def main():
             st = steps_in[s]
             for layer in range(wl.n_layers):
                 it = st["layers"][layer]
-                if wl.chunk:
-                    wc.quantize_write(byp_caches[layer], it["ck"], it["cv"], it["cslots"])
-                wc.quantize_write(byp_caches[layer], it["k"], it["v"], st["slots"])
+                for cc in ([byp_caches[layer]] + ([gs_caches[layer]] if gs_caches else [])):
+                    if wl.chunk:
+                        wc.quantize_write(cc, it["ck"], it["cv"], it["cslots"])
+                    wc.quantize_write(cc, it["k"], it["v"], st["slots"])
         ba_ms = timed(lambda i: wc.metered_decode_gate(
             byp_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
             max_len_all, sm, args.tau, ws=ws, out=out, meter=meter, raw=raw, mask_q=mask_q,
@@ -445,6 +456,43 @@ def main():
             "paged_bytes_per_repaired_kv_head": (round(float(np.median(nr[fixed])) * bs * BF16_BYTES)
                                                  if fixed.any() else None),
             "whole_head_bytes": round(whole)}
+
+        # group scales (Sec. 6.2 storage side, Table 4): the same bypass caches with a
+        # 4-bit power-of-two exponent per 32-channel group (+2 + 2 bytes per
+        # token-head), both tiers with the fused gate, and their meters
+        if gs_caches:
+            ga_ms = timed(lambda i: wc.metered_decode_gate(
+                gs_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
+                max_len_all, sm, args.tau, ws=ws, out=out, meter=meter, raw=raw, mask_q=mq_b,
+                mask_kv=mkv_b), reps)
+            gb_ms = timed(lambda i: wc.tierb_decode_attention(
+                gs_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
+                max_len_all, sm, dloc, ws=ws, out=out, meter=meter, raw=raw), reps)
+            cnt_g = {"A": torch.zeros(2, dtype=torch.int32, device=dev),
+                     "B": torch.zeros(2, dtype=torch.int32, device=dev)}
+            raws_g = {"A": [], "B": []}
+            for layer in range(wl.n_layers):
+                q_l = last["layers"][layer]["q"]
+                wc.metered_decode_attention(gs_caches[layer], q_l, table, last["lens"], max_len_all, sm,
+                                            ws=ws, out=out, meter=meter, raw=raw)
+                wc.gate(meter, raw, wl.group, args.tau, n_gated=cnt_g["A"], mask_q=mq_b, mask_kv=mkv_b)
+                raws_g["A"].append(raw.clone())
+                wc.tierb_decode_attention(gs_caches[layer], q_l, table, last["lens"], max_len_all, sm, dloc,
+                                          ws=ws, out=out, meter=meter, raw=raw)
+                wc.gate(meter, raw, wl.group, args.tau, n_gated=cnt_g["B"], mask_q=mq_b, mask_kv=mkv_b)
+                raws_g["B"].append(raw.clone())
+            gsd = {"path": "matrix cores (group exponents in the fp16 operand exponents)"}
+            for tier, ms, nbytes in (("tier_a", ga_ms, INT8_BYTES + 4 * m_byp + 4),
+                                     ("tier_b", gb_ms, TIERB_BYTES + 4 * m_byp + 4)):
+                key = "A" if tier == "tier_a" else "B"
+                gq_, gkv_ = cnt_g[key].cpu().tolist()
+                gbps = float(last["tokens"] * wl.n_kv) * nbytes / (float(np.median(ms)) * 1e-3) / 1e9
+                gsd[tier] = {"median_launch_ms": round(float(np.median(ms)), 4), "GBps": round(gbps, 1),
+                             "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4), "bytes_per_token_head": nbytes,
+                             "raw_median": round(float(torch.cat(raws_g[key]).median().item()), 4),
+                             "gate_fraction_q_heads": round(gq_ / (n_cells * wl.n_q), 4),
+                             "gate_fraction_kv_heads": round(gkv_ / (n_cells * wl.n_kv), 4)}
+            byp["group_scales"] = gsd
     th_per_launch = float(last["tokens"] * wl.n_kv)
     tb_gbps = th_per_launch * TIERB_BYTES / (float(np.median(tb_ms)) * 1e-3) / 1e9
     dec_gbps = th_per_launch * INT8_BYTES / (float(np.median(dec_ms)) * 1e-3) / 1e9

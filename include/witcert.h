@@ -117,11 +117,11 @@ extern "C" {
  *
  * Group scales (INT8_DITHER; Sec. 6.2 storage side: per token, per group of 32
  * channels; Table 4 granularity): with k_gexp/v_gexp set, each token keeps its fp16
- * scale s and every 32-channel group g gets the step s * 2^-e_g, e_g in [0, 15] the
+ * scale s and every 32-channel group g gets the step s * 2^-e_g, e_g in [0, 14] the
  * largest exponent with amax_g * 2^e_g <= amax (amax over the token's quantized
- * channels, amax_g over the group's; 15 for an all-zero group).  Power-of-two
- * ratios keep every dequantized code an exact fp16 multiple, so the decode's
- * matrix-core operands stay exact.  Bypassed channels leave amax_g as they leave
+ * channels, amax_g over the group's; 14 for an all-zero group).  Power-of-two
+ * ratios keep every dequantized code an exact normal fp16 multiple, so the
+ * decode's matrix-core operands stay exact.  Bypassed channels leave amax_g as they leave
  * amax.
  */
 typedef struct wc_cache {

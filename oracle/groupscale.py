@@ -10,12 +10,12 @@ dither and Tier B, whose proxy sums q_c^2 s_c^2 over the channels):
 * Storage reading.  The paper does not state how the group scales are stored.
   Here one fp16 scale per token and tensor (the token scale of the plain
   quantizer, s = fp16_round_up(fl32(amax / 126.5)) over the kept channels) and
-  one exponent e_g in [0, 15] per group: the group's scale is s_g = s * 2^-e_g,
+  one exponent e_g in [0, 14] per group: the group's scale is s_g = s * 2^-e_g,
   with e_g the largest exponent such that amax_g * 2^e_g <= amax (amax_g the
-  group's largest magnitude over its kept channels; 15 for an all-zero group).
-  The group scale is then within a factor 2 of amax_g / 126.5 (or at the 2^-15
-  floor), and power-of-two ratios keep the decode's operands exact (a code
-  times 2^-e is still an exact fp16 number).
+  group's largest magnitude over its kept channels; 14 for an all-zero group).
+  The group scale is then within a factor 2 of amax_g / 126.5 (or at the 2^-14
+  floor), and power-of-two ratios keep the decode's operands exact: a code times
+  2^-e, e <= 14, is still an exact normal fp16 number.
 * Quantization with the stored scales, operation by operation in fp32:
       inv_g = fl32(1/s) * 2^e_g   (exact: a power-of-two scaling)
       y     = fl32(x * inv_g)
@@ -39,7 +39,7 @@ from .fpformats import f16_round_up, f32
 from .quantizer import S_DIV
 
 GROUP = 32
-E_MAX = 15
+E_MAX = 14
 
 
 def keep_mask(d: int, chans=None) -> np.ndarray:

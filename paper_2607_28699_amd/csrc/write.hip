@@ -123,7 +123,8 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
       av = fmaxf(av, fabsf(v[i]));
     }
     // group scales (Sec. 6.2 storage side): the 32-channel group of this lane is
-    // lanes g, g^1; its exponent is the largest e <= 15 with amax_g 2^e <= amax
+    // lanes g, g^1; its exponent is the largest e <= 14 with amax_g 2^e <= amax
+    // (2^-e and every code times 2^-e stay normal fp16 numbers)
     const bool grouped = a.k_gexp != nullptr;
     float akg = 0.0f, avg = 0.0f;
     if (grouped) {
@@ -137,8 +138,8 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
     }
     int ek = 0, ev = 0;
     if (grouped) {
-      while (ek < 15 && ldexpf(akg, ek + 1) <= ak) ++ek;
-      while (ev < 15 && ldexpf(avg, ev + 1) <= av) ++ev;
+      while (ek < 14 && ldexpf(akg, ek + 1) <= ak) ++ek;
+      while (ev < 14 && ldexpf(avg, ev + 1) <= av) ++ev;
     }
     uint16_t skb, svb;
     float sk, ikk, sv, ivv;

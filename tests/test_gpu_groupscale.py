@@ -68,7 +68,9 @@ def test_groupscale_write_bitexact(name, wl, lens, m, layout):
     assert n_grouped > 0
 
 
-def _decode(case, cache, tier, tau, tau_v, force_valu=False):
+def _decode(case, cache, tier, tau, tau_v, force_valu=False, joint=True):
+    import os
+
     import torch
 
     import paper_2607_28699_amd as wc
@@ -78,17 +80,34 @@ def _decode(case, cache, tier, tau, tau_v, force_valu=False):
     lens = torch.from_numpy(case["seq_lens"].astype(np.int32)).cuda()
     L = max(int(case["seq_lens"].max()), 1)
     n = torch.zeros(2, dtype=torch.int32, device="cuda")
-    res = wc.joint_decode_gate(cache, q, table, lens, L, 1 / np.sqrt(wl.d), tau, tau_v,
-                               0.0 if tier == "A" else DLOC, n_gated=n)
+    sm = 1 / np.sqrt(wl.d)
+    if force_valu:
+        os.environ["WITCERT_FORCE_VALU"] = "1"
+    try:
+        if joint:
+            res = wc.joint_decode_gate(cache, q, table, lens, L, sm, tau, tau_v,
+                                       0.0 if tier == "A" else DLOC, n_gated=n)
+        elif tier == "A":
+            res = wc.metered_decode_gate(cache, q, table, lens, L, sm, tau, n_gated=n)
+        else:
+            o, m_, r_ = wc.tierb_decode_attention(cache, q, table, lens, L, sm, DLOC)
+            mq, mk = wc.gate(m_, r_, wl.n_q // wl.n_kv, tau)
+            res = (o, m_, r_, mq, mk)
+    finally:
+        os.environ.pop("WITCERT_FORCE_VALU", None)
     torch.cuda.synchronize()
     return [x.cpu().numpy() for x in res]
 
 
 @pytest.mark.parametrize("name,wl,lens,m", CASES)
 @pytest.mark.parametrize("tier", ["A", "B"])
-def test_groupscale_decode_parity(name, wl, lens, m, tier):
+@pytest.mark.parametrize("path", ["default", "vector"])
+@pytest.mark.parametrize("joint", [True, False])
+def test_groupscale_decode_parity(name, wl, lens, m, tier, path, joint):
     from oracle import value as ov
-    S.say(f"[gs-decode] {name} tier={tier} lens={lens} m={m}")
+    if path == "vector" and wl.d != 128:
+        pytest.skip("head_dim 64 always takes the vector path")
+    S.say(f"[gs-decode] {name} tier={tier} path={path} joint={joint} lens={lens} m={m}")
     case, pairs, refs, cache = _setup(wl, lens, m)
     sm = 1 / np.sqrt(wl.d)
     tol = S.out_tol(wl)
@@ -113,18 +132,26 @@ def test_groupscale_decode_parity(name, wl, lens, m, tier):
     mvs = np.concatenate([r["meter_v"] for r in ref if r is not None])
     tau = float(min(np.quantile(raws, 0.5), 0.9))
     tau_v = float(np.quantile(mvs, 0.5))
-    out, meter, raw, mv, mq, mk = _decode(case, cache, tier, tau, tau_v)
+    if joint:
+        out, meter, raw, mv, mq, mk = _decode(case, cache, tier, tau, tau_v, path == "vector")
+    else:
+        out, meter, raw, mq, mk = _decode(case, cache, tier, tau, tau_v, path == "vector", joint=False)
+        mv = None
     for b, r in enumerate(ref):
         if r is None:
             assert np.all(meter[b] == 0) and np.all(mq[b] == 0)
             continue
         assert S.rel_err(out[b], r["out"]) <= tol, (b, S.rel_err(out[b], r["out"]))
         fin = r["raw"] < 1e30
-        assert np.all(np.abs(raw[b][fin] - r["raw"][fin]) <= tol * np.maximum(r["raw"][fin], 1e-30))
-        assert np.all(np.abs(mv[b] - r["meter_v"]) <= tol * np.maximum(r["meter_v"], 1e-30))
+        assert np.all(np.abs(raw[b][fin] - r["raw"][fin]) <= tol * np.maximum(r["raw"][fin], 1e-30)), \
+            (b, np.max(np.abs(raw[b][fin] - r["raw"][fin]) / np.maximum(r["raw"][fin], 1e-30)))
         assert np.all(meter[b] >= r["tv"])
-        # the joint gate as a function of the GPU's own meters, bit-exact
-        exp_q = ov.joint_gate_q(meter[b], raw[b], mv[b], tau, tau_v)
+        if mv is None:   # the key gate alone
+            exp_q = ogate.gate_q(meter[b], raw[b], tau)
+        else:
+            assert np.all(np.abs(mv[b] - r["meter_v"]) <= tol * np.maximum(r["meter_v"], 1e-30))
+            # the joint gate as a function of the GPU's own meters, bit-exact
+            exp_q = ov.joint_gate_q(meter[b], raw[b], mv[b], tau, tau_v)
         assert np.array_equal(mq[b].astype(bool), np.asarray(exp_q, dtype=bool))
         assert np.array_equal(mk[b].astype(bool), ogate.gate_kv(np.asarray(exp_q)[None], wl.n_q // wl.n_kv)[0].astype(bool))
     S.say(f"  tau={tau:.3g} tau_v={tau_v:.3g} gated q heads {int(mq.sum())}/{mq.size}")

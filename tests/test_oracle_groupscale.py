@@ -5,7 +5,7 @@ What the paper and the mathematics fix, and these tests check:
   group's step (Sec. 4.2 quantizer law; Sec. 6.2 storage validation, max ratio
   1.0000), the bound attained;
 * the group exponent is the largest one that keeps the group inside the token
-  scale's range (brute force over all 16 exponents), so the group step is within
+  scale's range (brute force over all 15 exponents), so the group step is within
   a factor 2 of the group's own amax / 126.5;
 * with every exponent 0 the quantizer is the plain token-scalar one bit for bit
   (codes and reconstructions), and an all-zero group gets the largest exponent;
@@ -61,7 +61,7 @@ def test_exponent_is_the_largest_that_fits():
     for i in range(x.shape[0]):
         for g in range(4):
             ag = np.abs(x[i, 32 * g:32 * g + 32]).max()
-            fits = [k for k in range(16) if ag * 2.0 ** k <= amax[i]]
+            fits = [k for k in range(gs.E_MAX + 1) if ag * 2.0 ** k <= amax[i]]
             assert e[i, g] == max(fits)
             # the group step is within a factor 2 of the group's own amax / 126.5
             sg = s[i] * 2.0 ** -e[i, g]
