@@ -57,14 +57,12 @@ def scales(x: np.ndarray, chans=None):
     ax = np.where(keep_mask(d, chans), np.abs(x), 0.0)
     amax = ax.max(axis=1)
     s = f16_round_up(f32(amax / S_DIV))
-    e = np.empty((n, d // GROUP), dtype=np.int64)
-    for i in range(n):
-        for g in range(d // GROUP):
-            ag = ax[i, g * GROUP:(g + 1) * GROUP].max()
-            k = 0
-            while k < E_MAX and ag * 2.0 ** (k + 1) <= amax[i]:
-                k += 1
-            e[i, g] = k
+    ag = ax.reshape(n, d // GROUP, GROUP).max(axis=2)               # group amaxes [n, d/32]
+    # the largest k <= E_MAX with ag 2^k <= amax: the condition holds for every
+    # smaller k once it holds for k, so e counts the k = 1 .. E_MAX for which it holds
+    e = np.zeros((n, d // GROUP), dtype=np.int64)
+    for k in range(1, E_MAX + 1):
+        e += (ag * 2.0 ** k <= amax[:, None]).astype(np.int64)
     return s, e
 
 

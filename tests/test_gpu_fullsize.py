@@ -129,3 +129,80 @@ def test_matrix_core_and_vector_paths_agree():
         assert np.all(np.abs(a[2] - bv[2]) <= 2e-3 * np.abs(bv[2]))
         out[kind] = a
     _ = torch
+
+
+def test_fullsize_bypass_group_scales():
+    """The bench's third cache at full size (32k context, batch 4): pairs chosen on
+    the GPU from the layer's keys, 32-channel group scales, value side; sampled
+    cells of Tier A, Tier B and the value meter against the oracle."""
+    import torch
+
+    import paper_2607_28699_amd as wc
+    from oracle import bypass as obp
+    from oracle import groupscale as ogs
+    from oracle import philox as oph
+    from oracle import value as ov
+    from synth import torch_gen
+    name = "gqa-28x4-d128-s32k-b4"
+    S.say(f"[fullsize] {name} bypass + group scales")
+    wl = synth.WORKLOADS[name]
+    lens0 = np.full(wl.batch, wl.ctx, dtype=np.int64)
+    extra = BENCH_STEPS + BENCH_WARMUP
+    table, nblocks = synth.block_table(lens0 + extra, permute=False, seed_key=wl.wid)
+    layer, m = 3, 4
+    kv = []
+    for b, L in enumerate(lens0):
+        k, v = torch_gen.gen_kv_layer(wl, layer, b, torch.arange(int(L) + 1, device="cuda"))
+        kv.append((k, v, synth.slots_of(table, b, np.arange(int(L) + 1))))
+    kall = torch.cat([k for k, _, _ in kv])
+    pairs = wc.select_outlier_pairs(kall, m, wl.rope_layout)
+    ka = kall.float().cpu().numpy().astype(np.float64)
+    ref_pairs = np.stack([obp.select_pairs(ka[:, h], m, wl.rope_layout) for h in range(wl.n_kv)])
+    assert np.array_equal(pairs.cpu().numpy(), ref_pairs)
+    del ka
+    cache = wc.PagedCache("int8_dither", nblocks, wl.n_kv, wl.d, wl.bands, layer=layer, seed=wl.philox_seed(),
+                          rope_layout=wl.rope_layout, n_outlier_pairs=m, value_side=True, group_scales=True)
+    cache.set_outlier_pairs(pairs)
+    for k, v, sl in kv:
+        wc.quantize_write(cache, k, v, torch.from_numpy(sl).cuda())
+    q = torch_gen.gen_q_batch(wl, layer, 0, torch.from_numpy(lens0).cuda())
+    lens = torch.from_numpy((lens0 + 1).astype(np.int32)).cuda()
+    tab = torch.from_numpy(table).cuda()
+    max_len = int(lens0.max() + extra)
+    sm = 1 / np.sqrt(wl.d)
+    dloc = wc.tierb_delta_loc(1e-2, wl.n_layers, wl.n_q, 256)
+    out, meter, raw, mv, _, _ = wc.joint_decode_gate(cache, q, tab, lens, max_len, sm, 0.2, 0.05)
+    _, meter_b, raw_b = wc.tierb_decode_attention(cache, q, tab, lens, max_len, sm, dloc)
+    torch.cuda.synchronize()
+    out, meter, raw, mv = (x.cpu().numpy() for x in (out, meter, raw, mv))
+    meter_b, raw_b = meter_b.cpu().numpy(), raw_b.cpu().numpy()
+    rng = np.random.default_rng(23)
+    for b, h in [(int(rng.integers(wl.batch)), int(rng.integers(wl.n_q))) for _ in range(2)]:
+        S.say(f"  cell b={b} h={h}")
+        k, v, sl = kv[b]
+        g = h // wl.group
+        kb = k[:, g].float().cpu().numpy().astype(np.float64)
+        vb = v[:, g].float().cpu().numpy().astype(np.float64)
+        qb = q[b, h:h + 1].float().cpu().numpy().astype(np.float64)
+        chans = obp.bypass_channels(ref_pairs[g], wl.d, wl.rope_layout)
+        xi = oph.dither_values(sl, wl.d, layer, g, wl.philox_seed())
+        kc, ks, ke, ko, kh = ogs.quantize(kb, xi, chans)
+        vc, vs, ve, _, vh = ogs.quantize(vb, xi)
+        kw = oq.witness(kb, kh, wl.bands, wl.rope_layout)
+        ra = odec.metered_decode(qb, kh[:, None], vh[:, None], kw[:, None], sm, wl.bands, wl.rope_layout)
+        rb = ogs.tierb_decode(qb, kh[:, None], vh[:, None], ks[:, None], ke[:, None], sm, dloc, ko[:, None],
+                              chans[None])
+        tv = odec.true_tv(qb, kb[:, None], kh[:, None], sm)
+        j = ov.joint_decode(qb, kh[:, None], vh[:, None], ra["c"], ov.value_residual(vb[:, None], vh[:, None]),
+                            ov.value_norm(vb[:, None]), sm)
+        assert S.rel_err(out[b, h], ra["out"][0]) <= 2e-3
+        assert abs(raw[b, h] - ra["raw"][0]) <= 2e-3 * ra["raw"][0]
+        assert abs(raw_b[b, h] - rb["raw"][0]) <= 2e-3 * rb["raw"][0]
+        assert abs(mv[b, h] - j["meter_v"][0]) <= 2e-3 * j["meter_v"][0]
+        assert meter[b, h] >= tv[0] and meter_b[b, h] >= tv[0]
+        pick = rng.choice(len(sl), 512, replace=False)
+        got = S.read_cache(cache, sl[pick])
+        assert np.array_equal(got["k"][:, g].astype(np.int64), kc[pick])
+        assert np.array_equal(got["v"][:, g].astype(np.int64), vc[pick])
+        assert np.array_equal(got["ke"][:, g], ke[pick]) and np.array_equal(got["ve"][:, g], ve[pick])
+        assert np.array_equal(got["ks"][:, g], ks[pick])
