@@ -99,7 +99,7 @@ def cpu_baseline(wl, lens, tau, seconds, np, torch):
     sm = 1.0 / np.sqrt(wl.d)
     timed, tokens, samples = 0.0, 0, 0
     layer_ids = list(range(wl.n_layers))
-    for i in range(64):
+    for i in range(256):
         seq = i % len(lens)
         layer = layer_ids[(i * 7) % len(layer_ids)]
         L = int(lens[seq])
@@ -166,7 +166,7 @@ def main():
     # With --outlier-pairs m > 0 every layer also gets an INT8 cache whose keys
     # bypass the m RoPE pairs of largest energy over the layer's prefill keys (the
     # fixed per-(layer, KV head) set of the outlier-pair bypass), chosen on the GPU.
-    caches, exact, byp_caches, gs_caches = [], [], [], []
+    caches, exact, byp_caches, gs_caches, fp8_caches = [], [], [], [], []
     gen0 = None
     m_byp = args.outlier_pairs
     for layer in range(wl.n_layers):
@@ -178,9 +178,13 @@ def main():
             L = int(lens0[b])
             k, v = torch_gen.gen_kv_layer(wl, layer, b, torch.arange(L, device=dev))
             gen.append((k, v, torch.from_numpy(lay.slots(b, np.arange(L), np)).to(dev)))
+        f8 = wc.PagedCache("fp8_raw", lay.nblocks, wl.n_kv, wl.d, wl.bands, layer=layer,
+                           rope_layout=wl.rope_layout)   # the second black-box quantizer
         for k, v, sl in gen:
             wc.quantize_write(c, k, v, sl)
             wc.quantize_write(e, k, v, sl)
+            wc.quantize_write(f8, k, v, sl)
+        fp8_caches.append(f8)
         if m_byp:
             cb = wc.PagedCache("int8_dither", lay.nblocks, wl.n_kv, wl.d, wl.bands, layer=layer, seed=seed,
                                rope_layout=wl.rope_layout, n_outlier_pairs=m_byp, value_side=True)
@@ -320,6 +324,37 @@ def main():
         exact[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
         max_len_all, sm, mask_kv, out, ws=ws), reps)
     routed = float(mask_kv.float().mean().item())    # the route mask the fallback timing used
+    # the raw fp8 E4M3 cast (no scale) through the same meter: the decode-step tokens
+    # as the timed steps wrote them, per-call time, and the gate fractions of both
+    # quantizers at every tau of the sweep over the last step's layers (Tier A)
+    for s_ in range(K + W):
+        st_ = steps_in[s_]
+        for layer in range(wl.n_layers):
+            it = st_["layers"][layer]
+            if wl.chunk:
+                wc.quantize_write(fp8_caches[layer], it["ck"], it["cv"], it["cslots"])
+            wc.quantize_write(fp8_caches[layer], it["k"], it["v"], st_["slots"])
+    f8_ms = timed(lambda i: wc.metered_decode_gate(
+        fp8_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
+        max_len_all, sm, args.tau, ws=ws, out=out, meter=meter, raw=raw, mask_q=mask_q,
+        mask_kv=mask_kv), reps)
+    taus = (0.05, 0.1, 0.2)
+    sweep = {}
+    for qname, cl in (("int8_dither", caches), ("fp8_raw", fp8_caches)):
+        mets, raws_s = [], []
+        for layer in range(wl.n_layers):
+            wc.metered_decode_attention(cl[layer], last["layers"][layer]["q"], table, last["lens"], max_len_all,
+                                        sm, ws=ws, out=out, meter=meter, raw=raw)
+            mets.append(meter.clone())
+            raws_s.append(raw.clone())
+        mt_all, rw_all = torch.stack(mets), torch.stack(raws_s)     # [layers, batch, n_q]
+        entry = {"raw_median": round(float(rw_all.median().item()), 4)}
+        for tau in taus:
+            gq_t = (mt_all > tau) if tau < 1 else (rw_all > tau)
+            gkv_t = gq_t.view(wl.n_layers, lay.batch, wl.n_kv, wl.group).any(dim=-1)
+            entry[f"tau_{tau}"] = {"fraction_q_heads": round(float(gq_t.float().mean().item()), 4),
+                                   "fraction_kv_heads": round(float(gkv_t.float().mean().item()), 4)}
+        sweep[qname] = entry
     # Tier-B certificate (Sec. 4.2) over the same caches: per-call time and, over
     # every layer of the last step, its gate fractions (delta_req 1e-2 over
     # layers x query heads x 256 steps)
@@ -539,6 +574,15 @@ def main():
                            "frac_hbm": round(fb_gbps / HBM_PEAK_GBPS, 4), "routed_kv_fraction": routed},
         "gate": {"tau": args.tau, "fraction_q_heads": round(frac_q, 4),
                  "fraction_kv_heads": round(frac_kv, 4)},
+        "fp8_raw_decode": {"median_launch_ms": round(float(np.median(f8_ms)), 4),
+                           "GBps": round(th_per_launch * FP8_BYTES / (float(np.median(f8_ms)) * 1e-3) / 1e9, 1),
+                           "frac_hbm": round(th_per_launch * FP8_BYTES / (float(np.median(f8_ms)) * 1e-3) / 1e9
+                                             / HBM_PEAK_GBPS, 4),
+                           "bytes_per_token_head": FP8_BYTES},
+        "gate_sweep": sweep,
+        "kv_bytes_per_token": {"int8_dither": wl.n_layers * wl.n_kv * INT8_BYTES,
+                               "fp8_raw": wl.n_layers * wl.n_kv * FP8_BYTES,
+                               "bf16": wl.n_layers * wl.n_kv * BF16_BYTES},
         "tierb": {"median_launch_ms": round(float(np.median(tb_ms)), 4), "GBps": round(tb_gbps, 1),
                   "frac_hbm": round(tb_gbps / HBM_PEAK_GBPS, 4), "bytes_per_token_head": TIERB_BYTES,
                   "delta_req": 1e-2, "delta_loc": dloc,
