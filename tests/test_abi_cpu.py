@@ -129,3 +129,33 @@ def test_split_tokens_query(L):
     assert L.wc_decode_split_tokens(4, 4, 32769, 100) == 128
     assert L.wc_decode_split_tokens(4, 0, 100, 0) == 0
     assert L.wc_decode_split_tokens(-1, 4, 100, 0) == 0
+
+
+def test_group_scale_and_repair_argument_checks(L):
+    # group exponents: both arrays or neither, INT8 only, 16-byte aligned
+    c = _lib.WcCache(0, 128, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16, 0, 0, None, None, None, None, 16, None)
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
+    c.v_gexp = 24
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
+    c.v_gexp, c.kind = 16, _lib.WC_KIND_FP8_RAW
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
+    c.kind = _lib.WC_KIND_INT8_DITHER
+    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 0, None) == _lib.WC_OK   # no tokens
+    # repair workspace: a 1 KB header and one record of G (d + 2) doubles per
+    # (candidate block, 64-token tile) for every (sequence, KV head)
+    st = L.wc_decode_split_tokens(4, 4, 32778, 0)
+    tiles = (st // 4 + 63) // 64
+    unit = 1024 + 64 * tiles * 7 * 130 * 8
+    assert L.wc_block_repair_workspace_size(4, 28, 4, 128, 32778, 0, 64) == 16 * ((unit + 255) // 256 * 256)
+    assert L.wc_block_repair_workspace_size(4, 28, 4, 128, 32778, 0, 65) == 0
+    assert L.wc_block_repair_workspace_size(4, 27, 4, 128, 32778, 0, 8) == 0
+    ex = _lib.WcCache(_lib.WC_KIND_BF16, 128, 1, 0, 0, 0, 1, 0, 16, 16)
+    c.k_gexp = c.v_gexp = None
+
+    def rep(max_rep, rws, rws_bytes):
+        return L.wc_block_repair(ctypes.byref(c), ctypes.byref(ex), 16, 1, 1, 7, 16, 4, 16, 64, 0.1, 0, 0.0,
+                                 0.2, max_rep, 16, 1 << 30, 16, 0, 16, 16, 16, None, None, rws, rws_bytes, None)
+    assert rep(65, 256, 1 << 30) == _lib.WC_EINVAL            # budget above 64 blocks
+    assert rep(8, None, 1 << 30) == _lib.WC_EINVAL            # no repair workspace
+    assert rep(8, 16, 1 << 30) == _lib.WC_EINVAL              # not 256-byte aligned
+    assert rep(8, 256, 64) == _lib.WC_EWORKSPACE              # too small

@@ -205,3 +205,41 @@ def test_groupscale_block_repair():
             fixed += 1
     S.say(f"  repaired KV heads: {fixed}")
     assert fixed > 0
+
+
+def test_groupscale_graph_replay_is_bit_identical():
+    import torch
+
+    import paper_2607_28699_amd as wc
+    S.say("[gs-decode] graph replay")
+    case, _, _, cache = _setup(W_GQA, [700, 300], 4)
+    q = torch.from_numpy(case["q"]).to("cuda", torch.bfloat16)
+    table = torch.from_numpy(case["table"]).cuda()
+    lens = torch.from_numpy(case["seq_lens"].astype(np.int32)).cuda()
+    ws = wc.decode_workspace(2, 28, 4, 128, 700)
+    out = torch.empty((2, 28, 128), device="cuda")
+    meter = torch.empty((2, 28), device="cuda")
+    raw = torch.empty((2, 28), device="cuda")
+    mv = torch.empty((2, 28), device="cuda")
+    mq = torch.empty((2, 28), dtype=torch.uint8, device="cuda")
+    mk = torch.empty((2, 4), dtype=torch.uint8, device="cuda")
+    args = (cache, q, table, lens, 700, 1 / np.sqrt(128), 0.2, 0.05, DLOC)
+    kw = dict(ws=ws, out=out, meter=meter, raw=raw, meter_v=mv, mask_q=mq, mask_kv=mk)
+    wc.joint_decode_gate(*args, **kw)
+    torch.cuda.synchronize()
+    eager = [x.clone() for x in (out, meter, raw, mv, mq, mk)]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            wc.joint_decode_gate(*args, **kw)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for x in (out, meter, raw, mv, mq, mk):
+            x.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip((out, meter, raw, mv, mq, mk), eager):
+            assert torch.equal(a, b)

@@ -197,3 +197,62 @@ def test_block_repair_rounds_do_not_change_the_result(round0):
     assert np.any(ref[5] > round0), "no KV head needed the second round"
     for x, y in zip(ref[1:], got[1:]):
         assert np.array_equal(x, y)
+
+
+def test_block_repair_graph_replay_is_bit_identical():
+    """Metered decode with the gate and block repair captured in one HIP graph:
+    every replay (eager work and synchronizations in between) equals the eager run."""
+    import torch
+
+    import paper_2607_28699_amd as wc
+    name, wl, lens, tier, m, max_blocks = CASES[1]
+    S.say("[repair] graph replay")
+    case = S.make_case(wl, lens, permute=True, layer=1)
+    cache = S.gpu_cache(case, "int8_dither")
+    exact = S.gpu_cache(case, "bf16")
+    q = torch.from_numpy(case["q"]).to("cuda", S.torch_dtype(wl))
+    table = torch.from_numpy(case["table"]).cuda()
+    lens_t = torch.from_numpy(case["seq_lens"].astype(np.int32)).cuda()
+    L = int(case["seq_lens"].max())
+    sm = 1 / np.sqrt(wl.d)
+    B = q.shape[0]
+    ws = wc.decode_workspace(B, wl.n_q, wl.n_kv, wl.d, L, SPLIT)
+    rws = wc.repair_workspace(B, wl.n_q, wl.n_kv, wl.d, L, max_blocks, SPLIT)
+    out = torch.empty((B, wl.n_q, wl.d), device="cuda")
+    meter = torch.empty((B, wl.n_q), device="cuda")
+    raw = torch.empty_like(meter)
+    mq = torch.empty((B, wl.n_q), dtype=torch.uint8, device="cuda")
+    mk = torch.empty((B, wl.n_kv), dtype=torch.uint8, device="cuda")
+    nrep = torch.empty((B, wl.n_kv), dtype=torch.int32, device="cuda")
+    rl = torch.empty((B, wl.n_kv, max_blocks), dtype=torch.int32, device="cuda")
+    # a threshold that routes most heads but that a few blocks can meet
+    _, _, r0 = wc.metered_decode_attention(cache, q, table, lens_t, L, sm, split_tokens=SPLIT)
+    r0 = r0.cpu().numpy()[case["seq_lens"] > 0]
+    tau = float(np.quantile(r0, 0.2))
+
+    def step():
+        wc.metered_decode_gate(cache, q, table, lens_t, L, sm, tau, ws=ws, out=out, meter=meter, raw=raw,
+                               mask_q=mq, mask_kv=mk, split_tokens=SPLIT)
+        wc.block_repair(cache, exact, q, table, lens_t, L, sm, tau, ws, out, meter, raw, mk,
+                        max_blocks=max_blocks, split_tokens=SPLIT, repaired=rl, n_repaired=nrep, repair_ws=rws)
+    step()
+    torch.cuda.synchronize()
+    eager = [x.clone() for x in (out, meter, raw, mk, nrep, rl)]
+    assert int((eager[4] > 0).sum()) > 0, "nothing repaired"
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            step()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for x in (out, meter, raw):
+            x.zero_()
+        mk.fill_(7)
+        nrep.fill_(-9)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip((out, meter, raw, mk, nrep, rl), eager):
+            assert torch.equal(a, b)
