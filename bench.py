@@ -24,11 +24,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0       # MI355X HBM3E
-INT8_BYTES = 276             # per token-head at d=128, B=8: 128+128 codes, 2+2 scales, 16 witness
-FP8_BYTES = 272
-BF16_BYTES = 512
-TIERB_BYTES = 276 - 16       # the Tier-B certificate reads no witness
-WRITE_BYTES_BF16_IN = 512 + 276
+# algorithmic bytes per token-head, set from the workload's shape in main(); at
+# d = 128, B = 8: 128 + 128 codes, 2 + 2 scales, 16 witness = 276 (INT8), 272 (fp8),
+# 512 (bf16), 260 (Tier B reads no witness), 512 in + 276 out for a bf16 write
+INT8_BYTES = FP8_BYTES = BF16_BYTES = TIERB_BYTES = WRITE_BYTES_BF16_IN = 0
 REPAIR_BUDGET = 64           # blocks per KV head that block repair may page in
 DECODE_KERNEL_SRC = os.path.join(ROOT, "paper_2607_28699_amd", "csrc")
 
@@ -154,6 +153,12 @@ def main():
     from synth import torch_gen
 
     wl = synth.WORKLOADS[args.workload]
+    global INT8_BYTES, FP8_BYTES, BF16_BYTES, TIERB_BYTES, WRITE_BYTES_BF16_IN
+    INT8_BYTES = 2 * wl.d + 4 + 2 * wl.bands
+    FP8_BYTES = 2 * wl.d + 2 * wl.bands
+    BF16_BYTES = 4 * wl.d
+    TIERB_BYTES = INT8_BYTES - 2 * wl.bands
+    WRITE_BYTES_BF16_IN = 2 * wl.d * (4 if wl.dtype == "f32" else 2) + INT8_BYTES   # inputs in, cache out
     dev = "cuda"
     K, W = args.steps, args.warmup
     lens0 = (synth.serving_lengths(wl.batch, wl.len_lo, wl.ctx) if wl.ragged
@@ -233,7 +238,10 @@ def main():
         steps_in.append({"lens": lens, "slots": slots, "tokens": int((lens0 + s + 1).sum()),
                          "layers": per_layer})
     max_len_all = int(lens0.max() + K + W)
-    ws = wc.decode_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all)
+    # split length of every decode call, balanced over the batch's tokens (the host
+    # knows the lengths; equal to the library default for equal lengths)
+    ST = wc.split_tokens_for(lay.batch, wl.n_kv, max_len_all, total_tokens=int((lens0 + K + W).sum()))
+    ws = wc.decode_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all, ST)
     out = torch.empty((lay.batch, wl.n_q, wl.d), dtype=torch.bfloat16, device=dev)
     meter = torch.empty((lay.batch, wl.n_q), dtype=torch.float32, device=dev)
     raw = torch.empty_like(meter)
@@ -251,10 +259,10 @@ def main():
             wc.quantize_write_pair(caches[layer], exact[layer], it["k"], it["v"], st["slots"])
             # metered decode with the gate in its split merge, then the exact fallback
             wc.metered_decode_gate(caches[layer], it["q"], table, st["lens"], max_len_all, sm, args.tau,
-                                   ws=ws, out=out, meter=meter, raw=raw, mask_q=mask_q,
+                                   ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mask_q,
                                    mask_kv=mask_kv, n_gated=counts)
             wc.exact_decode_attention(exact[layer], it["q"], table, st["lens"], max_len_all, sm,
-                                      mask_kv, out, ws=ws)
+                                      mask_kv, out, ws=ws, split_tokens=ST)
 
     # one decode step per HIP graph (all layers), replayed back to back: the timed
     # region is GPU work only, as in a graph-captured serving loop
@@ -318,11 +326,11 @@ def main():
     reps = 2 * wl.n_layers
     dec_ms = timed(lambda i: wc.metered_decode_gate(
         caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
-        max_len_all, sm, args.tau, ws=ws, out=out, meter=meter, raw=raw, mask_q=mask_q,
+        max_len_all, sm, args.tau, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mask_q,
         mask_kv=mask_kv), reps)
     fb_ms = timed(lambda i: wc.exact_decode_attention(
         exact[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
-        max_len_all, sm, mask_kv, out, ws=ws), reps)
+        max_len_all, sm, mask_kv, out, ws=ws, split_tokens=ST), reps)
     routed = float(mask_kv.float().mean().item())    # the route mask the fallback timing used
     # the raw fp8 E4M3 cast (no scale) through the same meter: the decode-step tokens
     # as the timed steps wrote them, per-call time, and the gate fractions of both
@@ -336,7 +344,7 @@ def main():
             wc.quantize_write(fp8_caches[layer], it["k"], it["v"], st_["slots"])
     f8_ms = timed(lambda i: wc.metered_decode_gate(
         fp8_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
-        max_len_all, sm, args.tau, ws=ws, out=out, meter=meter, raw=raw, mask_q=mask_q,
+        max_len_all, sm, args.tau, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mask_q,
         mask_kv=mask_kv), reps)
     taus = (0.05, 0.1, 0.2)
     sweep = {}
@@ -344,7 +352,7 @@ def main():
         mets, raws_s = [], []
         for layer in range(wl.n_layers):
             wc.metered_decode_attention(cl[layer], last["layers"][layer]["q"], table, last["lens"], max_len_all,
-                                        sm, ws=ws, out=out, meter=meter, raw=raw)
+                                        sm, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw)
             mets.append(meter.clone())
             raws_s.append(raw.clone())
         mt_all, rw_all = torch.stack(mets), torch.stack(raws_s)     # [layers, batch, n_q]
@@ -361,12 +369,12 @@ def main():
     dloc = wc.tierb_delta_loc(1e-2, wl.n_layers, wl.n_q, 256)
     tb_ms = timed(lambda i: wc.tierb_decode_attention(
         caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
-        max_len_all, sm, dloc, ws=ws, out=out, meter=meter, raw=raw), reps)
+        max_len_all, sm, dloc, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw), reps)
     counts_b = torch.zeros(2, dtype=torch.int32, device=dev)
     mq_b, mkv_b = torch.empty_like(mask_q), torch.empty_like(mask_kv)
     for layer in range(wl.n_layers):
         wc.tierb_decode_attention(caches[layer], last["layers"][layer]["q"], table, last["lens"],
-                                  max_len_all, sm, dloc, ws=ws, out=out, meter=meter, raw=raw)
+                                  max_len_all, sm, dloc, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw)
         wc.gate(meter, raw, wl.group, args.tau, n_gated=counts_b, mask_q=mq_b, mask_kv=mkv_b)
     gqb, gkvb = counts_b.cpu().tolist()
 
@@ -384,21 +392,21 @@ def main():
                     wc.quantize_write(cc, it["k"], it["v"], st["slots"])
         ba_ms = timed(lambda i: wc.metered_decode_gate(
             byp_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
-            max_len_all, sm, args.tau, ws=ws, out=out, meter=meter, raw=raw, mask_q=mask_q,
+            max_len_all, sm, args.tau, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mask_q,
             mask_kv=mask_kv), reps)
         bb_ms = timed(lambda i: wc.tierb_decode_attention(
             byp_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
-            max_len_all, sm, dloc, ws=ws, out=out, meter=meter, raw=raw), reps)
+            max_len_all, sm, dloc, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw), reps)
         cnt = {"A": torch.zeros(2, dtype=torch.int32, device=dev), "B": torch.zeros(2, dtype=torch.int32, device=dev)}
         raws = {"A": [], "B": []}
         for layer in range(wl.n_layers):
             q_l = last["layers"][layer]["q"]
-            wc.metered_decode_attention(byp_caches[layer], q_l, table, last["lens"], max_len_all, sm, ws=ws,
+            wc.metered_decode_attention(byp_caches[layer], q_l, table, last["lens"], max_len_all, sm, ws=ws, split_tokens=ST,
                                         out=out, meter=meter, raw=raw)
             wc.gate(meter, raw, wl.group, args.tau, n_gated=cnt["A"], mask_q=mq_b, mask_kv=mkv_b)
             raws["A"].append(raw.clone())
             wc.tierb_decode_attention(byp_caches[layer], q_l, table, last["lens"], max_len_all, sm, dloc,
-                                      ws=ws, out=out, meter=meter, raw=raw)
+                                      ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw)
             wc.gate(meter, raw, wl.group, args.tau, n_gated=cnt["B"], mask_q=mq_b, mask_kv=mkv_b)
             raws["B"].append(raw.clone())
         # the fixed pair set itself: one layer's prefill keys, every KV head
@@ -429,14 +437,14 @@ def main():
         mv = torch.empty_like(meter)
         jt_ms = timed(lambda i: wc.joint_decode_gate(
             byp_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
-            max_len_all, sm, args.tau, args.tau_v, dloc, ws=ws, out=out, meter=meter, raw=raw, meter_v=mv,
+            max_len_all, sm, args.tau, args.tau_v, dloc, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, meter_v=mv,
             mask_q=mask_q, mask_kv=mask_kv), reps)
         cj = torch.zeros(2, dtype=torch.int32, device=dev)
         pass_k = pass_v = 0
         mvs = []
         for layer in range(wl.n_layers):
             wc.joint_decode_gate(byp_caches[layer], last["layers"][layer]["q"], table, last["lens"], max_len_all,
-                                 sm, args.tau, args.tau_v, dloc, ws=ws, out=out, meter=meter, raw=raw,
+                                 sm, args.tau, args.tau_v, dloc, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw,
                                  meter_v=mv, mask_q=mq_b, mask_kv=mkv_b, n_gated=cj)
             pass_k += int((meter <= args.tau).sum().item())
             pass_v += int((mv <= args.tau_v).sum().item())
@@ -460,15 +468,15 @@ def main():
         # (metered decode + gate + repair) minus the metered decode + gate alone.
         nrep = torch.empty((lay.batch, wl.n_kv), dtype=torch.int32, device=dev)
         rlist = torch.empty((lay.batch, wl.n_kv, REPAIR_BUDGET), dtype=torch.int32, device=dev)
-        rws = wc.repair_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all, REPAIR_BUDGET)
+        rws = wc.repair_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all, REPAIR_BUDGET, ST)
 
         def dec_rep(i):
             layer = i % wl.n_layers
             q_l = last["layers"][layer]["q"]
             wc.metered_decode_gate(byp_caches[layer], q_l, table, last["lens"], max_len_all, sm, args.tau,
-                                   ws=ws, out=out, meter=meter, raw=raw, mask_q=mq_b, mask_kv=mkv_b)
+                                   ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mq_b, mask_kv=mkv_b)
             wc.block_repair(byp_caches[layer], exact[layer], q_l, table, last["lens"], max_len_all, sm,
-                            args.tau, ws, out, meter, raw, mkv_b, max_blocks=REPAIR_BUDGET,
+                            args.tau, ws, out, meter, raw, mkv_b, max_blocks=REPAIR_BUDGET, split_tokens=ST,
                             repaired=rlist, n_repaired=nrep, repair_ws=rws)
         dr_ms = timed(dec_rep, reps)
         nreps = []
@@ -478,7 +486,7 @@ def main():
         nr = torch.cat(nreps).flatten().cpu().numpy()
         routed_r = nr != 0
         fixed = nr > 0
-        bs = wc.split_tokens_for(lay.batch, wl.n_kv, max_len_all) // 4
+        bs = ST // 4
         rep_ms = max(float(np.median(dr_ms)) - float(np.median(ba_ms)), 0.0)
         del rws
         whole = float(np.mean(last["lens"].cpu().numpy())) * BF16_BYTES
@@ -498,22 +506,22 @@ def main():
         if gs_caches:
             ga_ms = timed(lambda i: wc.metered_decode_gate(
                 gs_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
-                max_len_all, sm, args.tau, ws=ws, out=out, meter=meter, raw=raw, mask_q=mq_b,
+                max_len_all, sm, args.tau, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mq_b,
                 mask_kv=mkv_b), reps)
             gb_ms = timed(lambda i: wc.tierb_decode_attention(
                 gs_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
-                max_len_all, sm, dloc, ws=ws, out=out, meter=meter, raw=raw), reps)
+                max_len_all, sm, dloc, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw), reps)
             cnt_g = {"A": torch.zeros(2, dtype=torch.int32, device=dev),
                      "B": torch.zeros(2, dtype=torch.int32, device=dev)}
             raws_g = {"A": [], "B": []}
             for layer in range(wl.n_layers):
                 q_l = last["layers"][layer]["q"]
                 wc.metered_decode_attention(gs_caches[layer], q_l, table, last["lens"], max_len_all, sm,
-                                            ws=ws, out=out, meter=meter, raw=raw)
+                                            ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw)
                 wc.gate(meter, raw, wl.group, args.tau, n_gated=cnt_g["A"], mask_q=mq_b, mask_kv=mkv_b)
                 raws_g["A"].append(raw.clone())
                 wc.tierb_decode_attention(gs_caches[layer], q_l, table, last["lens"], max_len_all, sm, dloc,
-                                          ws=ws, out=out, meter=meter, raw=raw)
+                                          ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw)
                 wc.gate(meter, raw, wl.group, args.tau, n_gated=cnt_g["B"], mask_q=mq_b, mask_kv=mkv_b)
                 raws_g["B"].append(raw.clone())
             gsd = {"path": "matrix cores (group exponents in the fp16 operand exponents)"}
@@ -564,7 +572,7 @@ def main():
         "config": {"workload": wl.name, "layers": wl.n_layers, "n_q": wl.n_q, "n_kv": wl.n_kv,
                    "head_dim": wl.d, "bands": wl.bands, "batch": lay.batch,
                    "context": int(lens0.max()), "mean_context": float(lens0.mean()),
-                   "tau": args.tau, "cache": "int8 dither + fp16 scales + fp16 key witness",
+                   "tau": args.tau, "split_tokens": ST, "cache": "int8 dither + fp16 scales + fp16 key witness",
                    "fallback": "bf16 exact cache in HBM"},
         "roofline": roof,
         "metered_decode": {"median_launch_ms": round(float(np.median(dec_ms)), 4), "GBps": round(dec_gbps, 1),

@@ -233,9 +233,15 @@ size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int he
  * Tokens per KV split that the decode calls use for these sizes: split_tokens
  * rounded up to a multiple of 64, or, for 0, the library's choice (about 512
  * workgroups over the batch's KV heads, at least 256 tokens).  wc_block_repair's
- * blocks are quarters of it.  Returns 0 for invalid sizes.
+ * blocks are quarters of it.  With total_tokens > 0 (the sum of the batch's
+ * sequence lengths, known to the caller on the host) and split_tokens = 0 the
+ * choice balances the workgroups over the total instead of the longest
+ * sequence: pass the result as split_tokens to the decode calls and
+ * wc_decode_workspace_size for ragged batches (the same value as the default for
+ * equal lengths).  Returns 0 for invalid sizes.
  */
-int wc_decode_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int split_tokens);
+int wc_decode_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int64_t total_tokens,
+                           int split_tokens);
 
 /*
  * Metered decode attention (the read path of the meter loop, Sec. 6).  For each
@@ -335,9 +341,11 @@ int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int 
  * decode call (Tier A, or Tier B with delta_loc > 0) over the same cache, queries,
  * table, lengths and split_tokens, whose workspace `ws` still holds its partial
  * records, and whose gate set mask_kv.  For every KV head with mask_kv != 0:
- *   blocks are the quarters of the decode's KV splits, block i covering tokens
- *   [i*bs, (i+1)*bs), bs = split_tokens/4 (split_tokens as chosen for the decode:
- *   0 selects the library's choice for the same sizes);
+ *   blocks are the decode waves' parts of the KV splits: block i is part i%4 of
+ *   split i/4, the split's 16-token pages divided into four runs of
+ *   ceil(pages/4) pages (quarters, split_tokens/4 tokens each, for a full split;
+ *   the last runs of a sequence's last split are shorter or empty), split_tokens
+ *   as chosen for the decode (0 selects the library's choice for the same sizes);
  *   share_{h,i} = sum_{t in i} ptilde_{h,t} (e^{c_{h,t}} - 1) (they add up to A_h - 1),
  *   taken in decreasing order of sum_h share_{h,i} (ties to the lower i), at most
  *   max_repair_blocks (1 .. 64) of them;
@@ -348,8 +356,8 @@ int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int 
  * state and its mask_kv cleared (no whole-head fallback needed); otherwise nothing
  * of it changes.  repaired[b][g][0..max_repair_blocks-1] receives the block order
  * (-1 padded; may be NULL) and n_repaired[b][g] the number of blocks taken (0: not
- * routed, -1: the budget did not suffice; may be NULL).  At most 4096 blocks per
- * sequence.  out must be the decode's output array (out_dtype as there).
+ * routed, -1: the budget did not suffice; may be NULL).  At most 4096 blocks (1024
+ * splits) per sequence.  out must be the decode's output array (out_dtype as there).
  * repair_ws (repair_ws_bytes >= wc_block_repair_workspace_size for the same sizes,
  * caller-owned device memory, no initialization needed) holds the per-KV-head
  * state and the block corrections; the blocks' corrections are computed in

@@ -72,7 +72,7 @@ def lib() -> ctypes.CDLL:
                                       ctypes.c_int, ctypes.c_int, vp, vp]),
         "wc_decode_workspace_size": (sz, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                           i64, ctypes.c_int]),
-        "wc_decode_split_tokens": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, i64, ctypes.c_int]),
+        "wc_decode_split_tokens": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, i64, i64, ctypes.c_int]),
         "wc_metered_decode_attention": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int,
                                                        ctypes.c_int, vp, ctypes.c_int, vp, i64, f32,
                                                        vp, ctypes.c_int, vp, vp, ctypes.c_int, vp,

@@ -176,9 +176,11 @@ def decode_workspace(batch: int, n_q: int, n_kv: int, head_dim: int, max_seq_len
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
-def split_tokens_for(batch: int, n_kv: int, max_seq_len: int, split_tokens: int = 0) -> int:
-    """Tokens per KV split of the decode calls (block repair's blocks are quarters)."""
-    n = lib().wc_decode_split_tokens(batch, n_kv, max_seq_len, split_tokens)
+def split_tokens_for(batch: int, n_kv: int, max_seq_len: int, split_tokens: int = 0,
+                     total_tokens: int = 0) -> int:
+    """Tokens per KV split of the decode calls (block repair's blocks are quarters);
+    with total_tokens (the sum of the sequence lengths) balanced over the batch."""
+    n = lib().wc_decode_split_tokens(batch, n_kv, max_seq_len, total_tokens, split_tokens)
     if n <= 0:
         raise _lib.WitCertError("bad split geometry")
     return n

@@ -201,9 +201,12 @@ size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int he
   return wc::records_bytes(batch, n_q_heads, ns, head_dim) + wc::gate_unit_bytes(batch, n_kv_heads);
 }
 
-int wc_decode_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int split_tokens) {
-  if (batch < 0 || n_kv_heads < 1 || max_seq_len < 0 || split_tokens < 0) return 0;
-  return wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens);
+int wc_decode_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int64_t total_tokens,
+                           int split_tokens) {
+  if (batch < 0 || n_kv_heads < 1 || max_seq_len < 0 || total_tokens < 0 || split_tokens < 0) return 0;
+  if (split_tokens > 0 || total_tokens == 0)
+    return wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens);
+  return wc::choose_split_tokens_total(n_kv_heads, max_seq_len, total_tokens);
 }
 
 static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int batch,
@@ -389,8 +392,7 @@ int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q,
                     seq_lens, max_seq_len, sm_scale, out, out_dtype, split_tokens,
                     const_cast<void*>(ws), ws_bytes, a);   // the records are only read
   if (s != WC_OK) return s;
-  if ((max_seq_len + a.split_tokens / 4 - 1) / (a.split_tokens / 4) > wc::repair_max_blocks())
-    return WC_EUNSUPPORTED;
+  if (4 * (int64_t)a.n_splits > wc::repair_max_blocks()) return WC_EUNSUPPORTED;   // 4 blocks per split
   if (batch == 0) return WC_OK;
   if (!repair_ws || reinterpret_cast<uintptr_t>(repair_ws) % 256) return WC_EINVAL;
   if (repair_ws_bytes < wc_block_repair_workspace_size(batch, n_q_heads, cache->n_kv_heads,

@@ -608,12 +608,12 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   // the wave index is uniform: page addresses then live in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
-  const int unit = blockIdx.y;
+  const int unit = decode_unit(), split = decode_split(a.n_splits);
   const int b = unit / a.n_kv, kv = unit % a.n_kv;
   gate_clear(a, unit);
   const int G = a.group;
   const int B = a.n_bands;
-  const int wg_begin = blockIdx.x * a.split_tokens;
+  const int wg_begin = split * a.split_tokens;
   const int32_t* trow = a.table + (int64_t)b * a.max_blocks;
   // The workgroup's queries (G x 256 bytes) are requested first, once per
   // workgroup (thread = 16 bytes of one head), and shared through LDS below: every
@@ -638,12 +638,13 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   // whole workgroup: a KV head not routed here, or a split past the sequence end
   // (evaluated together, so that the length load is not held back behind the mask)
   const bool unrouted = a.mask_kv != nullptr && a.mask_kv[unit] == 0;
-  if (unrouted | (blockIdx.x >= a.n_splits) | (wg_begin >= L)) return;
+  if (unrouted | (split >= a.n_splits) | (wg_begin >= L)) return;
   const int wg_end = min(min(L, wg_begin + a.split_tokens), a.max_blocks * kBlockTokens);
-  // this wave's share: a quarter of the split (split_tokens / 4 tokens, a whole
-  // number of pages), also in a sequence's last split, so that the wave ranges are
-  // the fixed blocks whose meter shares the record carries (block repair)
-  const int ppw = ppw_full;
+  // this wave's share: a quarter of the workgroup's pages (rounded up; a full
+  // split gives split_tokens / 4 tokens), the blocks whose meter shares the record
+  // carries (block repair); a sequence's last split is divided the same way, so
+  // that all four waves share a short sequence
+  const int ppw = ((wg_end - wg_begin + kBlockTokens - 1) / kBlockTokens + kWaves - 1) / kWaves;
   const int t_begin = min(wg_begin + wave * ppw * kBlockTokens, wg_end);
   const int t_end = min(wg_end, t_begin + ppw * kBlockTokens);
 
@@ -1023,7 +1024,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       }
     }
     if (isnan(nsum)) nsum = INFINITY;
-    float* rec = a.part + (((int64_t)b * a.n_q + (int64_t)kv * G + r) * a.n_splits + blockIdx.x) * R;
+    float* rec = a.part + (((int64_t)b * a.n_q + (int64_t)kv * G + r) * a.n_splits + split) * R;
 #pragma unroll
     for (int i = 0; i < 32; i += 4) {
       float4 sum = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
@@ -1088,7 +1089,7 @@ void launch_decode_mfma_g(const DecodeArgs& a, bool metered, bool tb, bool byp, 
 }
 
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st) {
-  const dim3 grid(a.n_splits, a.batch * a.n_kv);
+  const dim3 grid(a.n_splits, a.batch * a.n_kv);   // split index rotated by the unit: decode_split()
   const dim3 block(64 * kWaves);
   const bool tb = metered && a.tierb_delta > 0.0f;   // Tier B: INT8 dithered cache only
   const bool byp = metered && a.n_pairs > 0;        // bypassed pairs: INT8 keys only

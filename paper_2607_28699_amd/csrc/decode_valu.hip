@@ -52,8 +52,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   __shared__ float alpha_s[kGMax];
   __shared__ int64_t slot_s[kT];
 
-  const int split = blockIdx.x;
-  const int unit = blockIdx.y;
+  const int split = decode_split(a.n_splits);
+  const int unit = decode_unit();
   const int b = unit / a.n_kv, kv = unit % a.n_kv;
   gate_clear(a, unit);
   if (a.mask_kv != nullptr && a.mask_kv[unit] == 0) return;
@@ -143,7 +143,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) nb_run[k][q4] = 0.0f;
   }
-  const int blk_tokens = a.split_tokens / 4;
+  // the split's four blocks: page-aligned quarters of its pages (rounded up)
+  const int blk_tokens = ((t_end - t_begin + kBlockTokens - 1) / kBlockTokens + 3) / 4 * kBlockTokens;
   const int c3 = tid % D, hs = tid / D;
   float acc[HPT];
 #pragma unroll
@@ -610,6 +611,17 @@ hipError_t launch_d(const DecodeArgs& a, bool metered, hipStream_t st) {
 }
 
 }  // namespace
+
+int choose_split_tokens_total(int n_kv, int64_t max_seq_len, int64_t total_tokens) {
+  // about 512 workgroups over all (sequence, KV head) token ranges: a long sequence
+  // gets many splits, a short one one
+  int64_t st = (total_tokens * n_kv + 511) / 512;
+  st = (st + 63) / 64 * 64;
+  if (st < 256) st = 256;
+  const int64_t cap = (max_seq_len + 63) / 64 * 64;
+  if (st > cap && cap >= 256) st = cap;
+  return (int)st;
+}
 
 int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested) {
   if (requested > 0) return (requested + 63) / 64 * 64;

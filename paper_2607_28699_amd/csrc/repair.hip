@@ -9,8 +9,8 @@
 //   rank   one workgroup per (sequence, KV head): the merged state of each query
 //          head (max M, weight sum L, meter numerator N) in float64 from the split
 //          records of the metered decode that routed it; the block totals (sum over
-//          the G heads of the block's share; a block is a quarter of a split, whose
-//          numerator the records carry); the repair order (largest first, ties to
+//          the G heads of the block's share; a block is one decode wave's part of a
+//          split, whose numerator the records carry); the repair order (largest first, ties to
 //          the lower block) up to the budget; and a predicted block count, the
 //          first prefix after which every head passes when only N moves (the
 //          exact logits usually move L very little);
@@ -73,18 +73,28 @@ __device__ __forceinline__ bool head_passes(double L, double N, float tau) {
 }
 
 struct UnitGeom {
-  int b, kv, L, Lc, ns, nb, bs;
+  int b, kv, L, Lc, ns, nb;
 };
 __device__ __forceinline__ UnitGeom unit_geom(const DecodeArgs& a, int unit) {
   UnitGeom u;
   u.b = unit / a.n_kv;
   u.kv = unit % a.n_kv;
   u.L = a.seq_lens[u.b];
-  u.bs = a.split_tokens / 4;
   u.Lc = min(u.L, a.max_blocks * kBlockTokens);
   u.ns = min((u.Lc + a.split_tokens - 1) / a.split_tokens, a.n_splits);
-  u.nb = min((u.Lc + u.bs - 1) / u.bs, 4 * u.ns);
+  u.nb = 4 * u.ns;
   return u;
+}
+
+// Tokens [b0, b1) of block i: part i % 4 of split i / 4, the decode wave's range (a
+// quarter of the split's pages, rounded up; the last parts of a short split may be
+// empty).
+__device__ __forceinline__ void block_range(int i, int Lc, int split_tokens, int& b0, int& b1) {
+  const int s0 = (i >> 2) * split_tokens;
+  const int s1 = min(s0 + split_tokens, Lc);
+  const int ppw = ((s1 - s0 + kBlockTokens - 1) / kBlockTokens + 3) / 4 * kBlockTokens;
+  b0 = min(s0 + (i & 3) * ppw, s1);
+  b1 = min(b0 + ppw, s1);
 }
 
 // ---------------------------------------------------------------------------
@@ -274,8 +284,10 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
   const int G = a.group;
   const int B = a.n_bands;
   const int blk = hd->order[j];
-  const int t_lo = blk * u.bs + tile * kRTile;
-  const int t_hi = min(min(t_lo + kRTile, blk * u.bs + u.bs), u.Lc);
+  int b0, b1;
+  block_range(blk, u.Lc, a.split_tokens, b0, b1);
+  const int t_lo = b0 + tile * kRTile;
+  const int t_hi = min(t_lo + kRTile, b1);
   const int nv = max(t_hi - t_lo, 0);     // tokens of this tile
   const bool tierb = a.tierb_delta > 0.0f;
   const int m2 = 2 * a.n_pairs;

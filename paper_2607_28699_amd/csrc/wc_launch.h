@@ -111,9 +111,21 @@ __device__ __forceinline__ float tierb_factor(float q_sq, float q_l1, int n_toke
   return sm_scale * (sqrtf(q_sq) * sqrtf(2.0f * lg / 12.0f) + q_l1 * (1.0f / 256.0f));
 }
 
+// Decode grids are (splits, units).  Workgroups go to the eight XCDs round-robin in
+// linear order (x fastest), so with the split index equal to x a split count that
+// is a multiple of 8 would send every unit's split j to XCD j mod 8 -- and a
+// sequence's first split (always present, while later ones exist only for long
+// sequences) to the same XCD for every unit.  The split index is therefore
+// rotated by the unit: split = (x + unit) mod n_splits, which gives every XCD a
+// share of every unit's splits whatever the split count.
+__device__ __forceinline__ int decode_unit() { return blockIdx.y; }
+__device__ __forceinline__ int decode_split(int n_splits) {
+  return (int)(((uint32_t)blockIdx.x + (uint32_t)blockIdx.y) % (uint32_t)n_splits);
+}
+
 // Clears the gate outputs of one (sequence, KV head) ahead of the merge.
 __device__ __forceinline__ void gate_clear(const DecodeArgs& a, int unit) {
-  if (a.gate_mask_q != nullptr && blockIdx.x == 0 && threadIdx.x == 0) {
+  if (a.gate_mask_q != nullptr && decode_split(a.n_splits) == 0 && threadIdx.x == 0) {
     a.gate_mask_kv[unit] = 0;
     a.gate_unit[unit] = 0;
   }
@@ -154,6 +166,8 @@ struct GateArgs {
 
 // Tokens per KV split chosen by the library (multiple of 64).
 int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested);
+// The same, balanced over the batch's total tokens (ragged batches).
+int choose_split_tokens_total(int n_kv, int64_t max_seq_len, int64_t total_tokens);
 inline int64_t n_splits_for(int64_t max_seq_len, int split_tokens) {
   return max_seq_len <= 0 ? 1 : (max_seq_len + split_tokens - 1) / split_tokens;
 }

@@ -124,11 +124,18 @@ def test_split_tokens_query(L):
     # the library's choice is a multiple of 64, at least 256, and an explicit
     # request is rounded up to a multiple of 64
     for batch, n_kv, s in ((4, 4, 32769), (1, 4, 131072), (8, 4, 4096), (1, 1, 10)):
-        st = L.wc_decode_split_tokens(batch, n_kv, s, 0)
+        st = L.wc_decode_split_tokens(batch, n_kv, s, 0, 0)
         assert st >= 256 and st % 64 == 0
-    assert L.wc_decode_split_tokens(4, 4, 32769, 100) == 128
-    assert L.wc_decode_split_tokens(4, 0, 100, 0) == 0
-    assert L.wc_decode_split_tokens(-1, 4, 100, 0) == 0
+        # balanced over the total tokens: the same choice when every length is s
+        if s >= 256:
+            assert L.wc_decode_split_tokens(batch, n_kv, s, batch * s, 0) == st
+    assert L.wc_decode_split_tokens(4, 4, 32769, 0, 100) == 128
+    assert L.wc_decode_split_tokens(4, 0, 100, 0, 0) == 0
+    assert L.wc_decode_split_tokens(-1, 4, 100, 0, 0) == 0
+    # a ragged batch (64 sequences, 496k tokens, longest 32k): splits of ~3.9k tokens
+    # instead of 16k from the longest alone
+    assert L.wc_decode_split_tokens(64, 4, 32768, 0, 0) == 16384
+    assert L.wc_decode_split_tokens(64, 4, 32768, 496384, 0) == 3904
 
 
 def test_group_scale_and_repair_argument_checks(L):
@@ -143,7 +150,7 @@ def test_group_scale_and_repair_argument_checks(L):
     assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 0, None) == _lib.WC_OK   # no tokens
     # repair workspace: a 1 KB header and one record of G (d + 2) doubles per
     # (candidate block, 64-token tile) for every (sequence, KV head)
-    st = L.wc_decode_split_tokens(4, 4, 32778, 0)
+    st = L.wc_decode_split_tokens(4, 4, 32778, 0, 0)
     tiles = (st // 4 + 63) // 64
     unit = 1024 + 64 * tiles * 7 * 130 * 8
     assert L.wc_block_repair_workspace_size(4, 28, 4, 128, 32778, 0, 64) == 16 * ((unit + 255) // 256 * 256)

@@ -1,7 +1,7 @@
 """GPU parity of block-granular repair (Sec. 6.3, block-level paging) against the oracle.
 
 After a metered decode with its gate, wc_block_repair takes the routed KV heads'
-blocks (quarters of the decode's splits) in decreasing order of their meter shares
+blocks (the decode waves' parts of its splits) in decreasing order of their meter shares
 until every query head passes tau:
 * the number of blocks taken matches the oracle's minimal count (a count whose
   stopping state lies within 1e-3 relative of tau is accepted either way), and the
@@ -118,7 +118,6 @@ def test_block_repair_parity(name, wl, lens, tier, m, max_blocks, path):
     before, out, meter, raw, mk, n_rep, rep = _run(case, cache, exact, tier, tau, max_blocks, path == "vector")
     out0, meter0, raw0, mk0 = before
     tol = S.out_tol(wl)
-    bs = SPLIT // 4
     n_fixed = 0
     for b in range(len(lens)):
         for kv in range(wl.n_kv):
@@ -132,7 +131,7 @@ def test_block_repair_parity(name, wl, lens, tier, m, max_blocks, path):
             # the exact store holds bf16 (the fallback cache): repaired blocks take those values
             kx = synth.bf16_round(case["k"][b][:, kv]).astype(np.float64)
             vx = synth.bf16_round(case["v"][b][:, kv]).astype(np.float64)
-            ranges = orep.block_ranges(S_, bs)
+            ranges = orep.split_blocks(S_, SPLIT)
             res = orep.block_repair(case["q"][b][hs], c["khat"][:, kv], c["vhat"][:, kv], kx, vx,
                                     bounds[b][hs], ranges, sm, tau, max_blocks)
             # the order: same blocks up to swaps of near-equal totals

@@ -82,3 +82,26 @@ def test_order_and_minimal_stop():
     q, k, v, kh, vh, cb = _case(np.random.default_rng(43), q_scale=2.0)
     res = orep.block_repair(q, kh, vh, k, v, cb, orep.block_ranges(300, 32), 1 / np.sqrt(32), 1e-6, 2)
     assert res["n_blocks"] == -1
+
+
+def test_split_blocks_partition():
+    """The decode's blocks: four page-aligned parts per split, covering [0, S) once;
+    quarters of a full split; a last split divided as evenly as pages allow."""
+    for S, st in ((300, 256), (4106, 256), (32770, 1088), (600, 3904), (1, 256), (16, 64), (33, 64)):
+        bl = orep.split_blocks(S, st)
+        assert len(bl) == 4 * (-(-S // st))
+        covered = np.zeros(S, dtype=int)
+        prev = 0
+        for t0, t1 in bl:
+            assert t0 == prev and t0 <= t1          # in order, contiguous, possibly empty
+            covered[t0:t1] += 1
+            prev = t1
+            if t1 > t0:
+                assert t0 % 16 == 0                 # page-aligned starts
+        assert prev == S and np.all(covered == 1)
+        for j in range(S // st):                    # full splits: exact quarters
+            assert bl[4 * j:4 * j + 4] == [(j * st + w * st // 4, j * st + (w + 1) * st // 4) for w in range(4)]
+    # a 600-token sequence in one 3904-token split: 38 pages -> 10, 10, 10, 8 pages
+    assert [t1 - t0 for t0, t1 in orep.split_blocks(600, 3904)] == [160, 160, 160, 120]
+    # a single page: the first part takes it
+    assert [t1 - t0 for t0, t1 in orep.split_blocks(10, 256)] == [10, 0, 0, 0]
