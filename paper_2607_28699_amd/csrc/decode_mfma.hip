@@ -87,12 +87,12 @@ __device__ __forceinline__ uint32_t ucodes2(uint32_t xb, uint32_t sel) {
 __device__ __forceinline__ uint32_t dith2(uint32_t u, uint32_t sel) {
   return perm(0x68686868u, u, sel);
 }
-// Two E4M3 bytes -> fp16 pair holding value / 256 (exact; the 256 is folded
-// into the scale): sign to bit 15, exponent/mantissa bits shifted by 7.
-__device__ __forceinline__ uint32_t e4m3pair(uint32_t b0, uint32_t b1) {
-  const uint32_t lo = ((b0 & 0x7Fu) << 7) | ((b0 & 0x80u) << 8);
-  const uint32_t hi = ((b1 & 0x7Fu) << 7) | ((b1 & 0x80u) << 8);
-  return lo | (hi << 16);
+// Two E4M3 bytes (bytes 0, 1 of w, or 2, 3 with HI) -> fp16 pair, one gfx950
+// conversion instruction at scale 1: every E4M3 value, subnormals included, is
+// a normal fp16 number (|x| in [2^-9, 448]), so the conversion is exact.
+template <bool HI>
+__device__ __forceinline__ uint32_t e4m3x2(uint32_t w) {
+  return as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, HI));
 }
 // Two bf16 -> fp16 pair (exact for |x| in the fp16 normal range).
 __device__ __forceinline__ uint32_t bf16pair_to_f16(uint32_t w) {
@@ -213,7 +213,7 @@ struct WaveConst {
   s8_t qbf[4];     // bf16 queries (bf16 cache)
   h8_t qnop;       // band norms * sm_scale * log2(e), hi (g < 2) / lo (g >= 2) parts
   float s1_init;   // 2303 sum(q) / 512: the dither offset, preloaded into the code accumulator
-  float lmul;      // logit multiplier: sm_scale * log2(e) (times 256 for fp8 operands)
+  float lmul;      // logit multiplier: sm_scale * log2(e)
   float ab2;       // Tier B: (alpha_h + beta_h) * log2(e)
   h8_t qo;         // bypassed pairs: fp16 queries at the stored values 8g .. 8g+7
   h8_t qa;         // their magnitudes (Tier B rounding term)
@@ -339,8 +339,8 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const uint32_t x = cur.kw[2 * kt + j];
-        c[2 * j] = e4m3pair(x & 0xFFu, (x >> 8) & 0xFFu);
-        c[2 * j + 1] = e4m3pair((x >> 16) & 0xFFu, x >> 24);
+        c[2 * j] = e4m3x2<false>(x);
+        c[2 * j + 1] = e4m3x2<true>(x);
       }
       s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(pack8(c[0], c[1], c[2], c[3]), wc.qop[kt], s1, 0, 0, 0);
     }
@@ -565,8 +565,8 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
 #pragma unroll
     for (int jt = 0; jt < 8; ++jt) {
       const uint32_t x = cur.vw[jt];
-      uint32_t lo = e4m3pair(x & 0xFFu, (x >> 8) & 0xFFu);
-      uint32_t hi = e4m3pair((x >> 16) & 0xFFu, x >> 24);
+      uint32_t lo = e4m3x2<false>(x);
+      uint32_t hi = e4m3x2<true>(x);
       if constexpr (!FULL) {
         // tokens past the end may hold any byte pattern (the 0x7F NaN code): zero them
         if (!vtok[0]) lo &= 0xFFFF0000u;
@@ -747,7 +747,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   }
   wc.layer_head = ((uint32_t)a.layer << 16) | (uint32_t)kv;
   wc.wit_ok = 8 * (g & 1) < B;
-  wc.lmul = a.sm_scale * kLog2e * (KIND == WC_KIND_FP8_RAW ? 256.0f : 1.0f);
+  wc.lmul = a.sm_scale * kLog2e;
   // B operands of QK: the kt-th MFMA uses channels 32g + 8kt .. 32g + 8kt + 7.
   float qsum = 0.0f;   // sum of the fp16 queries of head r over all channels
 #pragma unroll
@@ -979,8 +979,6 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     const float w2 = __shfl(st.wsg[2], r, 64), w3 = __shfl(st.wsg[3], r, 64);
     wsum = g == 0 ? w0 : (g == 1 ? w1 : (g == 2 ? w2 : w3));
   }
-  // fp8 value operands hold value / 256
-  constexpr float unscale = KIND == WC_KIND_FP8_RAW ? 256.0f : 1.0f;
   // rows 4g+e of tile jt hold channel 8(4g+e)+jt = 32g + 8e + jt
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -990,7 +988,6 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       v[jt] = st.o1[jt][e];
       if constexpr (KIND == WC_KIND_INT8_DITHER)
         v[jt] = fmaf(st.o2[jt][e] - kDOff * wsum, -0.001953125f, v[jt] - kCOff * wsum);
-      if constexpr (unscale != 1.0f) v[jt] *= unscale;
     }
     float4* dst = reinterpret_cast<float4*>(&acc_s[wave][r][32 * g + 8 * e]);
     dst[0] = make_float4(v[0], v[1], v[2], v[3]);
