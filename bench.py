@@ -139,7 +139,8 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the hot path shards by sequence and KV head, see DESIGN.md)", file=sys.stderr)
+              "(the hot path would shard by sequence and KV head, one process per GPU, "
+              "with no communication inside a layer's decode)", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
