@@ -63,6 +63,25 @@ def test_metered_decode_parity(name, wl, lens, split, kind):
     _check(case, res, out, meter, raw)
 
 
+def test_fp8_subnormal_codes():
+    """Keys and values scaled by 2^-6 so that a large share of the E4M3 codes are
+    subnormal (exponent field 0): the decode's conversion of every code must be
+    exact, so the parity bar is the same as above."""
+    S.say("[decode] fp8 subnormal codes")
+    case = S.make_case(W_GQA, [700, 77], permute=True, layer=2)
+    case["k"] = [k * np.float32(2.0 ** -6) for k in case["k"]]
+    case["v"] = [v * np.float32(2.0 ** -6) for v in case["v"]]
+    cache = S.gpu_cache(case, "fp8_raw")
+    codes = S.read_cache(cache, case["slots"][0])
+    for name in ("k", "v"):
+        x = codes[name].astype(np.int64)
+        sub = ((x & 0x78) == 0) & ((x & 0x07) != 0)
+        assert sub.mean() > 0.05, (name, sub.mean())
+    out, meter, raw = S.gpu_decode(case, cache)
+    res = S.oracle_decode(case, S.oracle_write(case, "fp8_raw"))
+    _check(case, res, out, meter, raw)
+
+
 def test_split_count_invariance():
     S.say("[decode] split invariance")
     case = S.make_case(W_GQA, [2000, 1500], permute=True)
