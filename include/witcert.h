@@ -194,7 +194,8 @@ int wc_select_outlier_pairs(const void* k, int in_dtype, int64_t n_tok, int n_kv
  * when the cache has a value side, ||vhat - v|| rounded up and ||v|| rounded down to
  * fp16 (float64 norms).
  *   k, v          [n_tok][n_kv_heads][head_dim], in_dtype WC_F32 or WC_BF16 (post-RoPE keys)
- *   slot_mapping  [n_tok] int64 device; slot < 0 skips the token
+ *   slot_mapping  [n_tok] int64 device; a slot < 0 or >= num_blocks * 16 skips the token
+ *                 (no write outside the cache)
  */
 int wc_quantize_write(const wc_cache* cache, const void* k, const void* v, int in_dtype,
                       const int64_t* slot_mapping, int64_t n_tok, void* stream);
@@ -258,7 +259,10 @@ int wc_decode_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int64
  * The KV axis is split into chunks whose partial (max, sum, A-1 numerator, output)
  * are merged under the LSE weights; A merges exactly like the output (Sec. 6.2).
  *   q            [batch][n_q_heads][head_dim], q_dtype WC_F32 or WC_BF16
- *   block_table  [batch][max_blocks_per_seq] int32;  seq_lens [batch] int32 (>= 0)
+ *   block_table  [batch][max_blocks_per_seq] int32 entries in [0, cache->num_blocks);
+ *                the kernels never read outside the cache, but the result for a
+ *                token whose entry lies outside it is unspecified
+ *   seq_lens     [batch] int32 (>= 0)
  *   max_seq_len  host-side upper bound of seq_lens (sizes the split grid)
  *   out          [batch][n_q_heads][head_dim], out_dtype WC_F32 or WC_BF16
  *   meter, raw   [batch][n_q_heads] fp32 (raw may be NULL)

@@ -116,6 +116,7 @@ static int write_common(const wc_cache* cache, const wc_cache* exact, const void
   a.key0 = (uint32_t)cache->seed;
   a.key1 = (uint32_t)(cache->seed >> 32);
   a.n_tok = n_tok;
+  a.n_slots = cache->num_blocks * WC_BLOCK_TOKENS;   // (an exact copy has at least as many blocks)
   a.k = k;
   a.v = v;
   a.slots = slot_mapping;
@@ -239,6 +240,7 @@ static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int 
   a.q = q;
   a.table = block_table;
   a.seq_lens = seq_lens;
+  a.num_blocks = cache->num_blocks;
   a.part = static_cast<float*>(ws);
   a.gate_unit = reinterpret_cast<int32_t*>(static_cast<char*>(ws) +
                                            wc::records_bytes(batch, n_q_heads, ns, cache->head_dim));
@@ -405,6 +407,7 @@ int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q,
   a.tierb_delta = tierb ? delta_loc : 0.0f;
   wc::RepairArgs r{};
   r.d = a;
+  r.d.num_blocks = exact->num_blocks < cache->num_blocks ? exact->num_blocks : cache->num_blocks;
   r.x_k_data = exact->k_data;
   r.x_v_data = exact->v_data;
   r.tau = tau;

@@ -158,7 +158,10 @@ __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool val
   constexpr int KB = KIND == WC_KIND_BF16 ? 64 : 32;   // bytes per lane and tensor
   constexpr int PB = kBlockTokens * kD * (KB / 32);    // bytes per page and tensor
   p.blk = blk;
-  const int64_t page = (int64_t)blk * a.n_kv + kv;
+  // an entry outside the cache reads zeros: its resources start at the cache's first
+  // page and cover nothing, so no address outside the cache is ever formed
+  valid = valid && (int64_t)(uint32_t)blk < a.num_blocks;
+  const int64_t page = valid ? (int64_t)blk * a.n_kv + kv : 0;
   const auto kr = page_rsrc(reinterpret_cast<const uint8_t*>(a.k_data) + page * PB, valid ? PB : 0);
   const auto vr = page_rsrc(reinterpret_cast<const uint8_t*>(a.v_data) + page * PB, valid ? PB : 0);
   const int koff = r * (kD * (KB / 32)) + KB * g;

@@ -157,10 +157,11 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
     {
       const int i = tid >> 2, part = tid & 3;
       const int t = t0 + i;
-      const bool valid = t < t_end;
+      // a table entry outside the cache leaves the token out (no access outside it)
+      const int32_t e = t < t_end ? a.table[(int64_t)b * a.max_blocks + t / kBlockTokens] : -1;
+      const bool valid = t < t_end && (int64_t)(uint32_t)e < a.num_blocks;
       int64_t slot = -1;
-      if (valid) slot = (int64_t)a.table[(int64_t)b * a.max_blocks + t / kBlockTokens] * kBlockTokens +
-                        t % kBlockTokens;
+      if (valid) slot = (int64_t)e * kBlockTokens + t % kBlockTokens;
       if (part == 0) slot_s[i] = slot;
       const int c0 = part * CH;
       const int64_t page = valid ? (slot / kBlockTokens) * a.n_kv + kv : 0;
@@ -347,7 +348,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
       for (int qd = 0; qd < kT / 4; ++qd) {
         const int i0 = 4 * qd;
         const int64_t slot = slot_s[i0];
-        if (slot < 0) break;
+        if (slot < 0) continue;   // past the end, or a table entry outside the cache
         const int64_t page = (slot / kBlockTokens) * a.n_kv + kv;
         const int off = (int)(slot % kBlockTokens);   // multiple of 4
         float vv[4];

@@ -345,10 +345,11 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
   {
     const int i = tid >> 2, part = tid & 3;
     const int t = t_lo + i;
-    const bool valid = i < nv;
+    // a table entry outside the caches leaves the token out (no access outside them)
+    const int32_t e = i < nv ? a.table[(int64_t)b * a.max_blocks + t / kBlockTokens] : -1;
+    const bool valid = i < nv && (int64_t)(uint32_t)e < a.num_blocks;
     int64_t slot = -1;
-    if (valid) slot = (int64_t)a.table[(int64_t)b * a.max_blocks + t / kBlockTokens] * kBlockTokens +
-                      t % kBlockTokens;
+    if (valid) slot = (int64_t)e * kBlockTokens + t % kBlockTokens;
     if (part == 0) slot_s[i] = slot;
     const int c0 = part * CH;
     const int64_t row = valid ? ((slot / kBlockTokens) * a.n_kv + kv) * kBlockTokens + slot % kBlockTokens : 0;
@@ -513,8 +514,8 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
       const int i0 = 4 * (sub + NSUB * qq);
       vb[qq] = 0;
       xb[qq] = make_uint2(0, 0);
-      if (i0 < nv) {
-        const int64_t slot = slot_s[i0];
+      const int64_t slot = i0 < nv ? slot_s[i0] : -1;
+      if (slot >= 0) {   // (a table entry outside the caches left the quad out)
         const int64_t page = (slot / kBlockTokens) * a.n_kv + kv;
         const int64_t vi = page * (kBlockTokens * D) + ((slot % kBlockTokens) >> 2) * D * 4 + c * 4;
         vb[qq] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(a.v_data) + vi);

@@ -12,6 +12,7 @@ struct WriteArgs {
   int kind, head_dim, n_kv, n_bands, interleaved, layer, in_dtype;
   uint32_t key0, key1;
   int64_t n_tok;
+  int64_t n_slots;          // slots of the cache(s): a slot outside [0, n_slots) is skipped
   const void* k;
   const void* v;
   const int64_t* slots;
@@ -58,6 +59,8 @@ struct DecodeArgs {
   const void* q;
   const int32_t* table;
   const int32_t* seq_lens;
+  int64_t num_blocks;       // blocks of the cache(s) read: a table entry outside [0, num_blocks)
+                            // is read as a page of zeros (no access outside the cache)
   const uint8_t* mask_kv;   // exact fallback: only routed (b, kv) units run
   float* part;              // partial records [batch][n_q][n_splits][D + 12]
   void* out;

@@ -85,7 +85,7 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
   const int64_t tok = in_range ? th / a.n_kv : 0;
   const int h = in_range ? (int)(th % a.n_kv) : 0;
   const int64_t slot = in_range ? a.slots[tok] : -1;
-  const bool active = in_range && slot >= 0;
+  const bool active = in_range && slot >= 0 && slot < a.n_slots;   // others are skipped
 
   float k[16], v[16];
   if (active) {
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
   const int64_t blk = active ? slot / kBlockTokens : 0;
   const int off = active ? (int)(slot % kBlockTokens) : 0;
   const int64_t bh = blk * a.n_kv + h;        // (block, head) page index
-  if (g == 0) slot_s[lth] = slot;
+  if (g == 0) slot_s[lth] = active ? slot : -1;   // the witness pass skips what this one skipped
 
   double vr2 = 0.0, vn2 = 0.0;   // value side: ||vhat - v||^2 and ||v||^2 of this lane's channels
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
