@@ -422,8 +422,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
 // (Sec. 6.2: A merges exactly like the output).  256 threads: the split maxima and
 // weights are reduced in LDS, then thread (channel, half) sums every other split
 // with all its loads independent.
-constexpr int kMergeWaves = 4;
-constexpr int kMergeThreads = 64 * kMergeWaves;
+constexpr int kMergeWaves = 4;   // waves per merge workgroup when a head has more than 32 splits
 
 // Split-KV merge (Sec. 6.2): one workgroup per (sequence, query head).  Splits
 // go 32 at a time to the four waves in turn.  In a chunk, lane j % 32 holds the
@@ -431,11 +430,11 @@ constexpr int kMergeThreads = 64 * kMergeWaves;
 // of all 32 partial outputs; all of a chunk's loads are issued together, and the
 // split weights reach the channel lanes through readlane.  The waves' running
 // states are combined in LDS at the end.
-template <int D, bool METER, bool VM>
-__global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
+template <int D, bool METER, bool VM, int NW>
+__global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
   constexpr int C = D / 64;   // channels per lane
-  __shared__ float st_s[kMergeWaves][5];
-  __shared__ float acc_s[kMergeWaves][D];
+  __shared__ float st_s[NW][5];
+  __shared__ float acc_s[NW][D];
   const int bh = blockIdx.x;
   const int b = bh / a.n_q, h = bh % a.n_q;
   if (a.mask_kv != nullptr && a.mask_kv[b * a.n_kv + h / a.group] == 0) return;
@@ -450,7 +449,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
   // The records of a chunk are requested before the sequence length is known;
   // records past the last active split are read but not used.
   int ns = -1;
-  for (int j0 = 32 * wave; j0 < a.n_splits; j0 += 32 * kMergeWaves) {
+  for (int j0 = 32 * wave; j0 < a.n_splits; j0 += 32 * NW) {
     const int nr = min(32, a.n_splits - j0);    // records that exist in the workspace
     const float4 t = *reinterpret_cast<const float4*>(rec0 + (int64_t)(j0 + min(jl, nr - 1)) * R + D);
     const float tv = VM ? rec0[(int64_t)(j0 + min(jl, nr - 1)) * R + D + 4] : 0.0f;
@@ -526,10 +525,10 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
   if (wave != 0) return;
   float Mt = -INFINITY;
 #pragma unroll
-  for (int w = 0; w < kMergeWaves; ++w) Mt = fmaxf(Mt, st_s[w][0]);
-  float f[kMergeWaves], lt = 0.0f, nt = 0.0f, et = 0.0f, vt = 0.0f;
+  for (int w = 0; w < NW; ++w) Mt = fmaxf(Mt, st_s[w][0]);
+  float f[NW], lt = 0.0f, nt = 0.0f, et = 0.0f, vt = 0.0f;
 #pragma unroll
-  for (int w = 0; w < kMergeWaves; ++w) {
+  for (int w = 0; w < NW; ++w) {
     f[w] = st_s[w][0] == -INFINITY ? 0.0f : __expf(st_s[w][0] - Mt);
     lt = fmaf(f[w], st_s[w][1], lt);
     if constexpr (METER) nt = fmaf(f[w], st_s[w][2], nt);
@@ -542,7 +541,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
   for (int c = 0; c < C; ++c) {
     float o = 0.0f;
 #pragma unroll
-    for (int w = 0; w < kMergeWaves; ++w) o = fmaf(f[w], acc_s[w][C * lane + c], o);
+    for (int w = 0; w < NW; ++w) o = fmaf(f[w], acc_s[w][C * lane + c], o);
     o = ns > 0 ? o / lt : 0.0f;
     const int64_t oi = (int64_t)bh * D + C * lane + c;
     if (a.out_dtype == WC_F32)
@@ -637,12 +636,19 @@ int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested)
   return (int)st;
 }
 
+template <int D, int NW>
+void launch_merge_w(const DecodeArgs& a, bool metered, hipStream_t st) {
+  const dim3 grid(a.batch * a.n_q), block(64 * NW);
+  if (!metered) hipLaunchKernelGGL((merge_kernel<D, false, false, NW>), grid, block, 0, st, a);
+  else if (a.meter_v != nullptr) hipLaunchKernelGGL((merge_kernel<D, true, true, NW>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((merge_kernel<D, true, false, NW>), grid, block, 0, st, a);
+}
+
+// One wave per head takes up to 32 records in one round trip; more splits get four.
 template <int D>
 void launch_merge_d(const DecodeArgs& a, bool metered, hipStream_t st) {
-  const dim3 grid(a.batch * a.n_q), block(kMergeThreads);
-  if (!metered) hipLaunchKernelGGL((merge_kernel<D, false, false>), grid, block, 0, st, a);
-  else if (a.meter_v != nullptr) hipLaunchKernelGGL((merge_kernel<D, true, true>), grid, block, 0, st, a);
-  else hipLaunchKernelGGL((merge_kernel<D, true, false>), grid, block, 0, st, a);
+  if (a.n_splits <= 32) launch_merge_w<D, 1>(a, metered, st);
+  else launch_merge_w<D, kMergeWaves>(a, metered, st);
 }
 
 hipError_t launch_merge(const DecodeArgs& a, bool metered, hipStream_t st) {
