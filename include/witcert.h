@@ -318,6 +318,34 @@ int wc_metered_decode_gate(const wc_cache* cache, const void* q, int q_dtype, in
                            size_t ws_bytes, void* stream);
 
 /*
+ * One decode step of the meter loop (Sec. 6, boxed meter loop: write the step's
+ * token, then the metered read path and the gate): results equal
+ *   wc_quantize_write_pair(cache, exact, new_k, new_v, in_dtype, new_slots, batch)
+ * followed by wc_metered_decode_gate(cache, q, ...) with the remaining arguments.
+ * Where the decode runs on the matrix cores and in_dtype is WC_BF16 this is one
+ * launch: the workgroup whose KV split holds a sequence's new token quantizes and
+ * stores it (codes, scales, witness, exact copy) before it reads its pages;
+ * otherwise the two calls run back to back on `stream`.
+ *   new_k, new_v [batch][n_kv_heads][head_dim] in in_dtype (WC_BF16 or WC_F32),
+ *                the step's token of each sequence
+ *   new_slots    [batch] int64: the slot of each sequence's last position
+ *                (seq_lens[b] - 1: block_table[b][(seq_lens[b] - 1) / 16] * 16 +
+ *                (seq_lens[b] - 1) % 16), or < 0 for a sequence without a new
+ *                token (seq_lens[b] == 0 needs < 0); any other slot makes the
+ *                result unspecified (the write may land after the read)
+ *   exact        the bf16 exact cache that the fallback reads (as in
+ *                wc_quantize_write_pair)
+ * Other arguments and checks as wc_quantize_write_pair and wc_metered_decode_gate.
+ */
+int wc_step_metered_decode_gate(const wc_cache* cache, const wc_cache* exact, const void* new_k,
+                                const void* new_v, int in_dtype, const int64_t* new_slots, const void* q,
+                                int q_dtype, int batch, int n_q_heads, const int32_t* block_table,
+                                int max_blocks_per_seq, const int32_t* seq_lens, int64_t max_seq_len,
+                                float sm_scale, void* out, int out_dtype, float* meter, float* raw,
+                                int split_tokens, float tau, uint8_t* mask_q, uint8_t* mask_kv,
+                                int32_t* n_gated, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Joint key + value certificate with its gate (Sec. 3 output bound; Sec. 4.2 value
  * side and joint event): wc_metered_decode_gate (delta_loc == 0: Tier A, the
  * witness bound) or Tier B (0 < delta_loc < 1, as wc_tierb_decode_attention), plus

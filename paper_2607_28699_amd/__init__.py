@@ -17,6 +17,7 @@ from .api import (  # noqa: F401
     joint_decode_gate,
     metered_decode_attention,
     metered_decode_gate,
+    step_metered_decode_gate,
     quantize_write,
     quantize_write_pair,
     repair_workspace,

@@ -90,8 +90,10 @@ size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim
   return total;
 }
 
-static int write_common(const wc_cache* cache, const wc_cache* exact, const void* k, const void* v,
-                        int in_dtype, const int64_t* slot_mapping, int64_t n_tok, void* stream) {
+// The write's arguments after its checks (WC_OK with a.n_tok == 0: nothing to do).
+static int write_args(const wc_cache* cache, const wc_cache* exact, const void* k, const void* v,
+                      int in_dtype, const int64_t* slot_mapping, int64_t n_tok, wc::WriteArgs& a) {
+  a = wc::WriteArgs{};
   int st = check_cache(cache, false);
   if (st != WC_OK) return st;
   if (exact != nullptr) {
@@ -105,7 +107,6 @@ static int write_common(const wc_cache* cache, const wc_cache* exact, const void
   if (n_tok < 0 || (in_dtype != WC_F32 && in_dtype != WC_BF16)) return WC_EINVAL;
   if (n_tok == 0) return WC_OK;
   if (!k || !v || !slot_mapping || !aligned16(k) || !aligned16(v)) return WC_EINVAL;
-  wc::WriteArgs a{};
   a.kind = cache->kind;
   a.head_dim = cache->head_dim;
   a.n_kv = cache->n_kv_heads;
@@ -134,6 +135,14 @@ static int write_common(const wc_cache* cache, const wc_cache* exact, const void
   a.v_norm = static_cast<uint16_t*>(cache->v_norm);
   a.k_gexp = static_cast<uint16_t*>(cache->k_gexp);
   a.v_gexp = static_cast<uint16_t*>(cache->v_gexp);
+  return WC_OK;
+}
+
+static int write_common(const wc_cache* cache, const wc_cache* exact, const void* k, const void* v,
+                        int in_dtype, const int64_t* slot_mapping, int64_t n_tok, void* stream) {
+  wc::WriteArgs a;
+  const int st = write_args(cache, exact, k, v, in_dtype, slot_mapping, n_tok, a);
+  if (st != WC_OK || a.n_tok == 0) return st;
   return hip_status(wc::launch_quantize_write(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -338,6 +347,44 @@ int wc_metered_decode_gate(const wc_cache* cache, const void* q, int q_dtype, in
   a.gate_count = n_gated;
   a.gate_tau = tau;
   return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
+}
+
+int wc_step_metered_decode_gate(const wc_cache* cache, const wc_cache* exact, const void* new_k,
+                                const void* new_v, int in_dtype, const int64_t* new_slots, const void* q,
+                                int q_dtype, int batch, int n_q_heads, const int32_t* block_table,
+                                int max_blocks_per_seq, const int32_t* seq_lens, int64_t max_seq_len,
+                                float sm_scale, void* out, int out_dtype, float* meter, float* raw,
+                                int split_tokens, float tau, uint8_t* mask_q, uint8_t* mask_kv,
+                                int32_t* n_gated, void* ws, size_t ws_bytes, void* stream) {
+  if (exact == nullptr) return WC_EINVAL;
+  wc::WriteArgs w;
+  int s = write_args(cache, exact, new_k, new_v, in_dtype, new_slots, batch, w);
+  if (s != WC_OK) return s;
+  s = check_cache(cache, true);
+  if (s != WC_OK) return s;
+  if (cache->kind == WC_KIND_BF16) return WC_EINVAL;
+  if (!(tau >= 0.0f)) return WC_EINVAL;
+  if (batch > 0 && (!meter || !mask_q || !mask_kv)) return WC_EINVAL;
+  wc::DecodeArgs a{};
+  s = decode_common(cache, q, q_dtype, batch, n_q_heads, block_table, max_blocks_per_seq,
+                    seq_lens, max_seq_len, sm_scale, out, out_dtype, split_tokens, ws, ws_bytes, a);
+  if (s != WC_OK) return s;
+  a.meter = meter;
+  a.raw = raw;
+  a.gate_mask_q = mask_q;
+  a.gate_mask_kv = mask_kv;
+  a.gate_count = n_gated;
+  a.gate_tau = tau;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (batch == 0) return WC_OK;
+  if (wc::step_write_fusable(a) && in_dtype == WC_BF16) {
+    // one launch: the workgroup holding a sequence's new token writes it first
+    a.sw = w;
+    a.step_write = 1;
+    return hip_status(wc::launch_decode(a, true, st));
+  }
+  const hipError_t e = wc::launch_quantize_write(w, st);
+  return hip_status(e != hipSuccess ? e : wc::launch_decode(a, true, st));
 }
 
 int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int batch,

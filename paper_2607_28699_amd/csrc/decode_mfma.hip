@@ -34,6 +34,7 @@
 
 #include "wc_device.h"
 #include "wc_launch.h"
+#include "write_dev.h"
 
 namespace wc {
 
@@ -596,6 +597,23 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   }
 }
 
+// The new token of sequence b, KV head kv (the step's token of that sequence, by
+// the workgroup that reads it): lanes 0 .. kD/16 - 1 of wave 0 quantize and store
+// it as the write kernel does (write_dev.h), then the witness bands; the barrier
+// after the stores comes before any wave of the workgroup requests a page.
+template <int KIND>
+__device__ __forceinline__ void step_write(const DecodeArgs& a, int b, int kv, int wave, int lane, double* r2row,
+                                        int64_t* slot_sh) {
+  constexpr int LPT = kD / 16;
+  if (wave == 0 && lane < LPT) {
+    const int64_t slot = write_token_head<kD, KIND, uint16_t>(a.sw, b, kv, true, lane, r2row);
+    if (lane == 0) *slot_sh = slot;
+  }
+  __syncthreads();
+  if (wave == 0 && lane < a.sw.n_bands) witness_band<kD>(a.sw, r2row, *slot_sh, kv, lane);
+  __syncthreads();
+}
+
 template <int KIND, bool METER, bool HALF, bool TB, bool BYP, bool VM, bool GS>
 __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
@@ -607,6 +625,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   // (1), the Tier-B group norms (2), the witness bound (1) and the bypassed pairs (2),
   // the same in every wave: one copy in LDS instead of registers, read per page
   __shared__ uint4 qop_s[GS ? 10 : 1][64];
+  __shared__ double wr_s[METER ? kD : 1];   // a decode step's new token: squared key residuals
+  __shared__ int64_t wslot_s;
 
   // the wave index is uniform: page addresses then live in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -642,6 +662,9 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   // (evaluated together, so that the length load is not held back behind the mask)
   const bool unrouted = a.mask_kv != nullptr && a.mask_kv[unit] == 0;
   if (unrouted | (split >= a.n_splits) | (wg_begin >= L)) return;
+  if constexpr (METER) {
+    if (a.step_write && split == (L - 1) / a.split_tokens) step_write<KIND>(a, b, kv, wave, lane, wr_s, &wslot_s);
+  }
   const int wg_end = min(min(L, wg_begin + a.split_tokens), a.max_blocks * kBlockTokens);
   // this wave's share: a quarter of the workgroup's pages (rounded up; a full
   // split gives split_tokens / 4 tokens), the blocks whose meter shares the record
@@ -1053,6 +1076,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
 }
 
 }  // namespace
+
+bool step_write_fusable(const DecodeArgs& a) { return a.use_mfma && mfma_decode_supported(a); }
 
 bool mfma_decode_supported(const DecodeArgs& a) {
   return a.head_dim == kD && a.q_dtype == WC_BF16 && a.group <= 16 &&

@@ -91,6 +91,10 @@ struct DecodeArgs {
   // bits 4g..4g+3, the group's step s * 2^-e_g
   const uint16_t* k_gexp;
   const uint16_t* v_gexp;
+  // a decode step's new tokens (one per sequence, its last): written by the
+  // matrix-core decode before it reads them (step_write != 0), else nothing
+  WriteArgs sw;
+  int step_write;
 };
 
 // 2^-e_g of channel c's group from a token's exponent word (exact).
@@ -197,6 +201,9 @@ int select_chunks(int64_t n_tok);   // row chunks of the pair-energy pass
 hipError_t launch_decode(const DecodeArgs& a, bool metered, hipStream_t st);
 bool mfma_decode_supported(const DecodeArgs& a);
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st);
+// The decode call would run on the matrix cores (where a step's new tokens can be
+// written by the decode kernel itself).
+bool step_write_fusable(const DecodeArgs& a);
 hipError_t launch_merge(const DecodeArgs& a, bool metered, hipStream_t st);
 hipError_t launch_gate(const GateArgs& a, hipStream_t st);
 hipError_t launch_repair(const RepairArgs& a, hipStream_t st);

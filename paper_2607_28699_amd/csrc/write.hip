@@ -1,73 +1,17 @@
 // Write path of the certified cache: dithered INT8 quantizer, raw fp8 cast, bf16
 // copy, and the residual witness (Sec. 4.2 subtractive dither; Sec. 6.2 research
-// kernels and storage side; Sec. 4.1 Eq. witness).
-//
-// One token-head (one token of one KV head, K and V together) is handled by
-// D/16 lanes, lane g owning channels 16g .. 16g+15 -- exactly one Philox call
-// of dither, shared by K and V.  Key residuals go through LDS so that any band
-// map can be summed; each band norm is then rounded up to fp16.  The residuals
-// are exact in float64 (a dequantized value needs 28 bits), and squares, sums and
-// square roots are taken in float64 too, so the stored witness is the fp16
-// round-up of the float64 band norm.
+// kernels and storage side; Sec. 4.1 Eq. witness).  The per-token-head work is in
+// write_dev.h; here are the write kernel (D/16 lanes per token-head, the witness
+// after a workgroup barrier), the black-box witness and the pair selection.
 #include "wc_device.h"
 #include "wc_launch.h"
+#include "write_dev.h"
 
 namespace wc {
 
 namespace {
 
 constexpr int kWriteThreads = 256;
-
-template <int D, typename TIn>
-__device__ __forceinline__ void load16(const TIn* src, float (&x)[16]) {
-  if constexpr (sizeof(TIn) == 4) {
-    const float4* p = reinterpret_cast<const float4*>(src);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float4 v = p[i];
-      x[4 * i] = v.x; x[4 * i + 1] = v.y; x[4 * i + 2] = v.z; x[4 * i + 3] = v.w;
-    }
-  } else {
-    const uint4* p = reinterpret_cast<const uint4*>(src);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      uint4 v = p[i];
-      uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        x[8 * i + 2 * j] = bf16_to_f32((uint16_t)(w[j] & 0xFFFFu));
-        x[8 * i + 2 * j + 1] = bf16_to_f32((uint16_t)(w[j] >> 16));
-      }
-    }
-  }
-}
-
-// Per-token, per-head fp16 scale s = round_up(fl32(amax / 126.5)) and fl32(1/s).
-__device__ __forceinline__ void int8_scale(float amax, uint16_t& s_bits, float& s, float& inv) {
-  s_bits = f16_round_up(__fdiv_rn(amax, 126.5f));
-  s = f16_to_f32(s_bits);
-  inv = s > 0.0f ? __fdiv_rn(1.0f, s) : 0.0f;
-}
-
-// bf16 copy of one token-head's 16 channels (this lane's share) into an exact cache.
-template <int D>
-__device__ __forceinline__ void store_exact(void* k_data, void* v_data, int64_t bh, int off, int g,
-                                            const float (&k)[16], const float (&v)[16]) {
-  uint32_t kw[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i)
-    kw[i] = (uint32_t)f32_to_bf16_rne(k[2 * i]) | ((uint32_t)f32_to_bf16_rne(k[2 * i + 1]) << 16);
-  uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(k_data) + (bh * kBlockTokens + off) * D +
-                                       16 * g);
-  kd[0] = make_uint4(kw[0], kw[1], kw[2], kw[3]);
-  kd[1] = make_uint4(kw[4], kw[5], kw[6], kw[7]);
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    uint16_t* vd = reinterpret_cast<uint16_t*>(v_data) + bh * (kBlockTokens * D) +
-                   ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
-    *vd = f32_to_bf16_rne(v[i]);
-  }
-}
 
 template <int D, int KIND, typename TIn>
 __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs a) {
@@ -82,193 +26,19 @@ __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs
   const int64_t th = (int64_t)blockIdx.x * TH + lth;
   const int64_t total = a.n_tok * (int64_t)a.n_kv;
   const bool in_range = th < total;
-  const int64_t tok = in_range ? th / a.n_kv : 0;
-  const int h = in_range ? (int)(th % a.n_kv) : 0;
-  const int64_t slot = in_range ? a.slots[tok] : -1;
-  const bool active = in_range && slot >= 0 && slot < a.n_slots;   // others are skipped
-
-  float k[16], v[16];
-  if (active) {
-    const TIn* kp = reinterpret_cast<const TIn*>(a.k) + (tok * a.n_kv + h) * D + 16 * g;
-    const TIn* vp = reinterpret_cast<const TIn*>(a.v) + (tok * a.n_kv + h) * D + 16 * g;
-    load16<D>(kp, k);
-    load16<D>(vp, v);
-  } else {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) k[i] = v[i] = 0.0f;
-  }
-  const int64_t blk = active ? slot / kBlockTokens : 0;
-  const int off = active ? (int)(slot % kBlockTokens) : 0;
-  const int64_t bh = blk * a.n_kv + h;        // (block, head) page index
-  if (g == 0) slot_s[lth] = active ? slot : -1;   // the witness pass skips what this one skipped
-
-  double vr2 = 0.0, vn2 = 0.0;   // value side: ||vhat - v||^2 and ||v||^2 of this lane's channels
-  if constexpr (KIND == WC_KIND_INT8_DITHER) {
-    // Bypassed key channels of this lane (outlier RoPE pairs, Sec. 6.2): out of the
-    // amax, code 0, value kept in fp16 (bit i: channel 16g + i).
-    uint32_t bmask = 0;
-    const int32_t* plist = a.pairs + (int64_t)h * a.n_pairs;
-    for (int i = 0; i < a.n_pairs; ++i) {
-      const int j = plist[i];
-#pragma unroll
-      for (int sec = 0; sec < 2; ++sec) {
-        const int c = pair_channel(j, sec, D, a.interleaved) - 16 * g;
-        if (c >= 0 && c < 16) bmask |= 1u << c;
-      }
-    }
-    float ak = 0.0f, av = 0.0f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      if (((bmask >> i) & 1u) == 0) ak = fmaxf(ak, fabsf(k[i]));
-      av = fmaxf(av, fabsf(v[i]));
-    }
-    // group scales (Sec. 6.2 storage side): the 32-channel group of this lane is
-    // lanes g, g^1; its exponent is the largest e <= 14 with amax_g 2^e <= amax
-    // (2^-e and every code times 2^-e stay normal fp16 numbers)
-    const bool grouped = a.k_gexp != nullptr;
-    float akg = 0.0f, avg = 0.0f;
-    if (grouped) {
-      akg = fmaxf(ak, __shfl_xor(ak, 1, LPT));
-      avg = fmaxf(av, __shfl_xor(av, 1, LPT));
-    }
-#pragma unroll
-    for (int o = 1; o < LPT; o <<= 1) {
-      ak = fmaxf(ak, __shfl_xor(ak, o, LPT));
-      av = fmaxf(av, __shfl_xor(av, o, LPT));
-    }
-    int ek = 0, ev = 0;
-    if (grouped) {
-      while (ek < 14 && ldexpf(akg, ek + 1) <= ak) ++ek;
-      while (ev < 14 && ldexpf(avg, ev + 1) <= av) ++ev;
-    }
-    uint16_t skb, svb;
-    float sk, ikk, sv, ivv;
-    int8_scale(ak, skb, sk, ikk);
-    int8_scale(av, svb, sv, ivv);
-    ikk = ldexpf(ikk, ek);                       // fl32(1/s) 2^e_g: exact
-    ivv = ldexpf(ivv, ev);
-    const double stk = ldexp((double)sk, -ek);   // the group's step s 2^-e_g
-    const double stv = ldexp((double)sv, -ev);
-
-    const U4 rnd = dither_block(g, slot, ((uint32_t)a.layer << 16) | (uint32_t)h, a.key0, a.key1);
-    const uint32_t words[4] = {rnd.x, rnd.y, rnd.z, rnd.w};
-    uint32_t kc[4] = {0, 0, 0, 0};
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const bool byp = (bmask >> i) & 1u;
-      const float xi = dither_value((words[i >> 2] >> (8 * (i & 3))) & 0xFFu);
-      // a bypassed channel quantizes 0 (|xi| < 1/2, so its code is 0)
-      const float ck = rintf(__fadd_rn(__fmul_rn(byp ? 0.0f : k[i], ikk), xi));
-      const float cv = rintf(__fadd_rn(__fmul_rn(v[i], ivv), xi));
-      const double rk = byp ? (double)(float)(_Float16)k[i] - (double)k[i]     // fp16(k) - k
-                            : stk * (double)(ck - xi) - (double)k[i];          // khat - k
-      r2[lth][16 * g + i] = rk * rk;
-      const double rv = stv * (double)(cv - xi) - (double)v[i];                // vhat - v
-      vr2 = fma(rv, rv, vr2);
-      vn2 = fma((double)v[i], (double)v[i], vn2);
-      // codes are stored excess-128: byte = code + 128
-      kc[i >> 2] |= ((uint32_t)((int32_t)ck + 128) & 0xFFu) << (8 * (i & 3));
-      if (active) {
-        uint8_t* vd = reinterpret_cast<uint8_t*>(a.v_data) + bh * (kBlockTokens * D) +
-                      ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
-        *vd = (uint8_t)((int32_t)cv + 128);
-      }
-    }
-    // group exponents of the token-head: nibble g/2 from the first lane of each group
-    uint32_t ekw = 0, evw = 0;
-    if (grouped) {
-      ekw = (g & 1) ? 0u : (uint32_t)ek << (4 * (g >> 1));
-      evw = (g & 1) ? 0u : (uint32_t)ev << (4 * (g >> 1));
-#pragma unroll
-      for (int o = 1; o < LPT; o <<= 1) {
-        ekw |= __shfl_xor(ekw, o, LPT);
-        evw |= __shfl_xor(evw, o, LPT);
-      }
-    }
-    if (active) {
-      uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(a.k_data) +
-                                           (bh * kBlockTokens + off) * D + 16 * g);
-      *kd = make_uint4(kc[0], kc[1], kc[2], kc[3]);
-      if (g == 0) {
-        a.k_scale[bh * kBlockTokens + off] = skb;
-        a.v_scale[bh * kBlockTokens + off] = svb;
-        if (grouped) {
-          a.k_gexp[bh * kBlockTokens + off] = (uint16_t)ekw;
-          a.v_gexp[bh * kBlockTokens + off] = (uint16_t)evw;
-        }
-      }
-      if (bmask != 0) {
-        // fp16 (nearest-even) values of the bypassed channels, in pair order
-        const TIn* kp = reinterpret_cast<const TIn*>(a.k) + (tok * a.n_kv + h) * D;
-        uint16_t* orow = a.k_outlier + (bh * kBlockTokens + off) * (int64_t)(2 * a.n_pairs);
-        for (int i = 0; i < a.n_pairs; ++i) {
-          const int j = plist[i];
-#pragma unroll
-          for (int sec = 0; sec < 2; ++sec) {
-            const int c = pair_channel(j, sec, D, a.interleaved);
-            if (c >= 16 * g && c < 16 * g + 16) {
-              const float x = sizeof(TIn) == 4 ? (float)reinterpret_cast<const float*>(kp)[c]
-                                               : bf16_to_f32(reinterpret_cast<const uint16_t*>(kp)[c]);
-              orow[2 * i + sec] = f16_bits((_Float16)x);
-            }
-          }
-        }
-      }
-    }
-  } else if constexpr (KIND == WC_KIND_FP8_RAW) {
-    uint32_t kc[4] = {0, 0, 0, 0};
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const uint32_t bk = f32_to_e4m3_sat(k[i]);
-      const uint32_t bv = f32_to_e4m3_sat(v[i]);
-      const double rk = (double)e4m3_to_f32(bk) - (double)k[i];
-      r2[lth][16 * g + i] = rk * rk;
-      const double rv = (double)e4m3_to_f32(bv) - (double)v[i];
-      vr2 = fma(rv, rv, vr2);
-      vn2 = fma((double)v[i], (double)v[i], vn2);
-      kc[i >> 2] |= bk << (8 * (i & 3));
-      if (active) {
-        uint8_t* vd = reinterpret_cast<uint8_t*>(a.v_data) + bh * (kBlockTokens * D) +
-                      ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
-        *vd = (uint8_t)bv;
-      }
-    }
-    if (active) {
-      uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(a.k_data) +
-                                           (bh * kBlockTokens + off) * D + 16 * g);
-      *kd = make_uint4(kc[0], kc[1], kc[2], kc[3]);
-    }
-  } else {  // WC_KIND_BF16: exact cache, no witness
-    if (active) store_exact<D>(a.k_data, a.v_data, bh, off, g, k, v);
-    return;
-  }
-  if (active && a.x_k_data != nullptr) store_exact<D>(a.x_k_data, a.x_v_data, bh, off, g, k, v);
-  if (a.v_resid != nullptr) {   // value side (Sec. 3 output bound): residual norm up, value norm down
-#pragma unroll
-    for (int o = 1; o < LPT; o <<= 1) {
-      vr2 += __shfl_xor(vr2, o, LPT);
-      vn2 += __shfl_xor(vn2, o, LPT);
-    }
-    if (active && g == 0) {
-      a.v_resid[bh * kBlockTokens + off] = f16_round_up_f64(sqrt(vr2));
-      a.v_norm[bh * kBlockTokens + off] = f16_round_down_f64(sqrt(vn2));
-    }
-  }
+  const int64_t slot = write_token_head<D, KIND, TIn>(a, in_range ? th / a.n_kv : 0,
+                                                      in_range ? (int)(th % a.n_kv) : 0, in_range, g, r2[lth]);
+  if constexpr (KIND == WC_KIND_BF16) return;   // an exact cache has no witness
+  if (g == 0) slot_s[lth] = slot;
 
   // ---- witness: band norms of the key residual, rounded up to fp16 ----
   __syncthreads();
   const int B = a.n_bands;
-  const int per_band = D / B;
   for (int item = tid; item < TH * B; item += kWriteThreads) {
-    const int t = item / B, b = item % B;
+    const int t = item / B;
     const int64_t th2 = (int64_t)blockIdx.x * TH + t;
-    const int64_t s2 = slot_s[t];
-    if (th2 >= total || s2 < 0) continue;
-    const int h2 = (int)(th2 % a.n_kv);
-    double acc = 0.0;
-    for (int kk = 0; kk < per_band; ++kk) acc += r2[t][band_channel(b, kk, D, B, a.interleaved)];
-    const int64_t bh2 = (s2 / kBlockTokens) * a.n_kv + h2;
-    a.k_witness[(bh2 * kBlockTokens + s2 % kBlockTokens) * B + b] = f16_round_up_f64(sqrt(acc));
+    if (th2 >= total) continue;
+    witness_band<D>(a, r2[t], slot_s[t], (int)(th2 % a.n_kv), item % B);
   }
 }
 
