@@ -257,11 +257,13 @@ def main():
             # new tokens into the quantized cache and the exact bf16 copy in one pass
             if wl.chunk:
                 wc.quantize_write_pair(caches[layer], exact[layer], it["ck"], it["cv"], it["cslots"])
-            wc.quantize_write_pair(caches[layer], exact[layer], it["k"], it["v"], st["slots"])
-            # metered decode with the gate in its split merge, then the exact fallback
-            wc.metered_decode_gate(caches[layer], it["q"], table, st["lens"], max_len_all, sm, args.tau,
-                                   ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mask_q,
-                                   mask_kv=mask_kv, n_gated=counts)
+            # the step's token of every sequence into the quantized cache and the exact
+            # copy, and the metered decode with the gate in its split merge, in one launch
+            wc.step_metered_decode_gate(caches[layer], exact[layer], it["k"], it["v"], st["slots"], it["q"],
+                                        table, st["lens"], max_len_all, sm, args.tau, ws=ws, split_tokens=ST,
+                                        out=out, meter=meter, raw=raw, mask_q=mask_q, mask_kv=mask_kv,
+                                        n_gated=counts)
+            # then the exact fallback
             wc.exact_decode_attention(exact[layer], it["q"], table, st["lens"], max_len_all, sm,
                                       mask_kv, out, ws=ws, split_tokens=ST)
 
