@@ -33,6 +33,8 @@ CASES = [
     ("vector-path", W_GQA, [300, 33], 64, "int8_dither", dict(force_valu=True)),
     ("fp32-inputs", W_GQA, [300, 33], 64, "int8_dither", dict(f32_inputs=True)),
     ("tiny-d64", W_TINY, [200, 0, 57], 64, "int8_dither", {}),
+    # sequence 1 has context but no token this step (slot -1, its context all written)
+    ("no-token-row", W_GQA, [300, 40, 90], 64, "int8_dither", dict(idle=(1,))),
 ]
 
 
@@ -64,18 +66,20 @@ def test_step_equals_write_then_decode(name, wl, lens, split, kind, opts):
     batch = len(lens)
     # everything but each sequence's last token is already in the caches
     caches = [_caches(case, kind, opts, pairs) for _ in range(2)]
+    idle = opts.get("idle", ())
     for b, n in enumerate(lens):
-        if n > 1:
-            k = torch.from_numpy(case["k"][b][:-1]).to("cuda", in_dt)
-            v = torch.from_numpy(case["v"][b][:-1]).to("cuda", in_dt)
-            sl = torch.from_numpy(case["slots"][b][:-1].astype(np.int64)).cuda()
+        pre = n if b in idle else n - 1
+        if pre > 0:
+            k = torch.from_numpy(case["k"][b][:pre]).to("cuda", in_dt)
+            v = torch.from_numpy(case["v"][b][:pre]).to("cuda", in_dt)
+            sl = torch.from_numpy(case["slots"][b][:pre].astype(np.int64)).cuda()
             for c, e in caches:
                 wc.quantize_write_pair(c, e, k, v, sl)
     new_k = np.zeros((batch, wl.n_kv, wl.d), np.float32)
     new_v = np.zeros((batch, wl.n_kv, wl.d), np.float32)
     new_slots = np.full(batch, -1, np.int64)
     for b, n in enumerate(lens):
-        if n > 0:
+        if n > 0 and b not in idle:
             new_k[b], new_v[b], new_slots[b] = case["k"][b][-1], case["v"][b][-1], case["slots"][b][-1]
     nk = torch.from_numpy(new_k).to("cuda", in_dt)
     nv = torch.from_numpy(new_v).to("cuda", in_dt)
