@@ -625,7 +625,10 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   // (1), the Tier-B group norms (2), the witness bound (1) and the bypassed pairs (2),
   // the same in every wave: one copy in LDS instead of registers, read per page
   __shared__ uint4 qop_s[GS ? 10 : 1][64];
-  __shared__ double wr_s[METER ? kD : 1];   // a decode step's new token: squared key residuals
+  // a decode step's new token (plain Tier A caches, the variants the step call
+  // fuses; the others keep their registers): its squared key residuals
+  constexpr bool kStep = METER && !TB && !BYP && !VM && !GS;
+  __shared__ double wr_s[kStep ? kD : 1];
   __shared__ int64_t wslot_s;
 
   // the wave index is uniform: page addresses then live in scalar registers
@@ -662,7 +665,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   // (evaluated together, so that the length load is not held back behind the mask)
   const bool unrouted = a.mask_kv != nullptr && a.mask_kv[unit] == 0;
   if (unrouted | (split >= a.n_splits) | (wg_begin >= L)) return;
-  if constexpr (METER) {
+  if constexpr (kStep) {
     if (a.step_write && split == (L - 1) / a.split_tokens) step_write<KIND>(a, b, kv, wave, lane, wr_s, &wslot_s);
   }
   const int wg_end = min(min(L, wg_begin + a.split_tokens), a.max_blocks * kBlockTokens);
@@ -1077,7 +1080,12 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
 
 }  // namespace
 
-bool step_write_fusable(const DecodeArgs& a) { return a.use_mfma && mfma_decode_supported(a); }
+bool step_write_fusable(const DecodeArgs& a) {
+  // the kernel variants that carry the step write: Tier A over a cache without
+  // bypassed pairs or group scales
+  return a.use_mfma && mfma_decode_supported(a) && a.tierb_delta <= 0.0f && a.meter_v == nullptr &&
+         a.k_gexp == nullptr && a.n_pairs == 0;
+}
 
 bool mfma_decode_supported(const DecodeArgs& a) {
   return a.head_dim == kD && a.q_dtype == WC_BF16 && a.group <= 16 &&
