@@ -64,7 +64,7 @@ const char* wc_strerror(int status) {
   }
 }
 
-int wc_version(void) { return 100; }
+int wc_version(void) { return 101; }   // 1.1: wc_step_metered_decode_gate
 
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim, int n_bands,
                       int n_outlier_pairs, int value_side, int group_scales, size_t sizes[10]) {
