@@ -322,10 +322,11 @@ int wc_metered_decode_gate(const wc_cache* cache, const void* q, int q_dtype, in
  * token, then the metered read path and the gate): results equal
  *   wc_quantize_write_pair(cache, exact, new_k, new_v, in_dtype, new_slots, batch)
  * followed by wc_metered_decode_gate(cache, q, ...) with the remaining arguments.
- * Where the decode runs on the matrix cores and in_dtype is WC_BF16 this is one
- * launch: the workgroup whose KV split holds a sequence's new token quantizes and
- * stores it (codes, scales, witness, exact copy) before it reads its pages;
- * otherwise the two calls run back to back on `stream`.
+ * Where the decode runs on the matrix cores, in_dtype is WC_BF16 and the cache has
+ * no bypassed pairs and no group scales, this is one launch: the workgroup whose
+ * KV split holds a sequence's new token quantizes and stores it (codes, scales,
+ * witness, exact copy) before it reads its pages; otherwise the two calls run
+ * back to back on `stream`.
  *   new_k, new_v [batch][n_kv_heads][head_dim] in in_dtype (WC_BF16 or WC_F32),
  *                the step's token of each sequence
  *   new_slots    [batch] int64: the slot of each sequence's last position
