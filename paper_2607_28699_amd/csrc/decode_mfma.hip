@@ -611,6 +611,9 @@ __device__ __forceinline__ void step_write(const DecodeArgs& a, int b, int kv, i
   }
   __syncthreads();
   if (wave == 0 && lane < a.sw.n_bands) witness_band<kD>(a.sw, r2row, *slot_sh, kv, lane);
+  // wave 0's stores are complete (acknowledged) before the barrier, not only ordered
+  // by it: no wave can then read the page before the new token is in it
+  if (wave == 0) __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 }
 
