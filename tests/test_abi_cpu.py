@@ -166,3 +166,23 @@ def test_group_scale_and_repair_argument_checks(L):
     assert rep(8, None, 1 << 30) == _lib.WC_EINVAL            # no repair workspace
     assert rep(8, 16, 1 << 30) == _lib.WC_EINVAL              # not 256-byte aligned
     assert rep(8, 256, 64) == _lib.WC_EWORKSPACE              # too small
+
+
+def test_step_call_argument_checks(L):
+    """wc_step_metered_decode_gate checks the write's and the decode's arguments on
+    the host before anything is launched."""
+    c = _lib.WcCache(_lib.WC_KIND_INT8_DITHER, 128, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16, 0, 0,
+                     None, None, None, None)
+    ex = _lib.WcCache(_lib.WC_KIND_BF16, 128, 1, 0, 0, 0, 1, 0, 16, 16)
+
+    def step(cache, exact, in_dtype=_lib.WC_BF16, new_k=16, ws_bytes=1 << 30, ws=256, tau=0.2):
+        return L.wc_step_metered_decode_gate(
+            cache, exact, new_k, 16, in_dtype, 16, 16, _lib.WC_BF16, 1, 7, 16, 4, 16, 64, 0.1, 16, 0,
+            16, 16, 0, tau, 16, 16, None, ws, ws_bytes, None)
+    assert step(ctypes.byref(c), None) == _lib.WC_EINVAL                       # no exact cache
+    assert step(ctypes.byref(c), ctypes.byref(c)) == _lib.WC_EINVAL            # exact must be bf16
+    assert step(ctypes.byref(c), ctypes.byref(ex), in_dtype=_lib.WC_F16) == _lib.WC_EINVAL
+    assert step(ctypes.byref(c), ctypes.byref(ex), new_k=8) == _lib.WC_EINVAL  # misaligned input
+    assert step(ctypes.byref(c), ctypes.byref(ex), tau=-1.0) == _lib.WC_EINVAL
+    assert step(ctypes.byref(c), ctypes.byref(ex), ws_bytes=64) == _lib.WC_EWORKSPACE
+    assert step(ctypes.byref(ex), ctypes.byref(ex)) == _lib.WC_EINVAL         # the metered cache is quantized
