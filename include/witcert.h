@@ -82,10 +82,20 @@ extern "C" {
 
 /*
  * One layer's paged cache.  Slot s lives in block s/16 at offset s%16.
- * Memory layout (elements; sizes from wc_cache_bytes):
- *   k_data     [num_blocks][n_kv_heads][16][head_dim]         token-major
- *   v_data     [num_blocks][n_kv_heads][4][head_dim][4]       token quads, channel-major
- *              (token o of a block, channel c -> ((o/4)*head_dim + c)*4 + o%4)
+ * Memory layout (sizes from wc_cache_bytes):
+ *   k_data,
+ *   v_data     [num_blocks][n_kv_heads][page], a page (16 tokens, 16*head_dim elements
+ *              of E bytes: 1 for the quantized kinds, 2 for BF16) stored as 16-byte
+ *              pieces [CL][4][16][16 bytes], CL = head_dim*E/64: piece (i, g, r) at byte
+ *              ((i*4 + g)*16 + r)*16 of the page, so that each 16-byte load of a wave
+ *              covers whole cache lines.
+ *              k_data: piece (i, g, r) = bytes (g*CL + i)*16 .. +15 of token r's row
+ *                (its head_dim elements in channel order): token r, channel c at byte
+ *                ((p%CL*4 + p/CL)*16 + r)*16 + (c*E)%16, p = c*E/16.
+ *              v_data: token quad q (tokens 4q .. 4q+3) has a row of head_dim x 4
+ *                elements (channel c, token 4q+u at element 4c + u); piece (i, q, r) =
+ *                bytes (r*CL + i)*16 .. +15 of that row: token t, channel c at byte
+ *                ((p%CL*4 + t/4)*16 + p/CL)*16 + b%16, b = (4c + t%4)*E, p = b/16.
  *   k_scale,
  *   v_scale    [num_blocks][n_kv_heads][16] fp16              INT8_DITHER only, else NULL
  *   k_witness  [num_blocks][n_kv_heads][16][n_bands] fp16     NULL for BF16

@@ -75,9 +75,12 @@ class PagedCache:
         names = ("k_data", "v_data", "k_scale", "v_scale", "k_witness", "k_outlier", "v_resid", "v_norm",
                  "k_gexp", "v_gexp")
         slots = self.num_blocks * WC_BLOCK_TOKENS * self.n_kv
+        # pages of 16-byte pieces [CL][4][16][16 bytes], CL = head_dim * E / 64 (E bytes per element)
+        esz = 2 if self.kind == "bf16" else 1
+        piece_shape = (self.num_blocks, self.n_kv, self.head_dim * esz // 64, 4, WC_BLOCK_TOKENS, 16 // esz)
         shapes = {
-            "k_data": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.head_dim),
-            "v_data": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS // 4, self.head_dim, 4),
+            "k_data": piece_shape,
+            "v_data": piece_shape,
             "k_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
             "v_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
             "k_witness": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.n_bands),

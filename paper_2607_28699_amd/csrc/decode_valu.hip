@@ -171,13 +171,12 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
       for (int c = 0; c < CH; ++c) kval[c] = 0.0f;
       if (valid) {
         if constexpr (KIND == WC_KIND_INT8_DITHER) {
-          const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.k_data) +
-                                                           (page * kBlockTokens + off) * D + c0);
+          const uint8_t* kpg = reinterpret_cast<const uint8_t*>(a.k_data) + page * (kBlockTokens * D);
           const float s = f16_to_f32(a.k_scale[page * kBlockTokens + off]);
           const uint32_t kgw = grouped ? a.k_gexp[page * kBlockTokens + off] : 0u;
 #pragma unroll
           for (int gi = 0; gi < NG; ++gi) {
-            const uint4 cw = kp[gi];
+            const uint4 cw = *reinterpret_cast<const uint4*>(kpg + kpage_off(off, c0 + 16 * gi, D, 1));
             const U4 r = dither_block(c0 / 16 + gi, slot, layer_head, a.key0, a.key1);
             const uint32_t codes[4] = {cw.x, cw.y, cw.z, cw.w};
             const uint32_t rw[4] = {r.x, r.y, r.z, r.w};
@@ -198,11 +197,10 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
             ve_s[i] = grouped ? a.v_gexp[page * kBlockTokens + off] : 0u;
           }
         } else if constexpr (KIND == WC_KIND_FP8_RAW) {
-          const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.k_data) +
-                                                           (page * kBlockTokens + off) * D + c0);
+          const uint8_t* kpg = reinterpret_cast<const uint8_t*>(a.k_data) + page * (kBlockTokens * D);
 #pragma unroll
           for (int gi = 0; gi < NG; ++gi) {
-            const uint4 cw = kp[gi];
+            const uint4 cw = *reinterpret_cast<const uint4*>(kpg + kpage_off(off, c0 + 16 * gi, D, 1));
             const uint32_t codes[4] = {cw.x, cw.y, cw.z, cw.w};
 #pragma unroll
             for (int w4 = 0; w4 < 4; ++w4)
@@ -212,11 +210,10 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
           }
           if (part == 0) vs_s[i] = 1.0f;
         } else {
-          const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a.k_data) +
-                                                           (page * kBlockTokens + off) * D + c0);
+          const uint8_t* kpg = reinterpret_cast<const uint8_t*>(a.k_data) + page * (kBlockTokens * D * 2);
 #pragma unroll
           for (int v4 = 0; v4 < CH / 8; ++v4) {
-            const uint4 cw = kp[v4];
+            const uint4 cw = *reinterpret_cast<const uint4*>(kpg + kpage_off(off, c0 + 8 * v4, D, 2));
             const uint32_t wds[4] = {cw.x, cw.y, cw.z, cw.w};
 #pragma unroll
             for (int w4 = 0; w4 < 4; ++w4) {
@@ -353,17 +350,15 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         const int off = (int)(slot % kBlockTokens);   // multiple of 4
         float vv[4];
         if constexpr (KIND == WC_KIND_BF16) {
-          const uint2 w = *reinterpret_cast<const uint2*>(
-              reinterpret_cast<const uint16_t*>(a.v_data) + page * (kBlockTokens * D) +
-              ((off >> 2) * D + c3) * 4);
+          const uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint8_t*>(a.v_data) +
+                                                          page * (kBlockTokens * D * 2) + vpage_off(off, c3, D, 2));
           vv[0] = bf16_to_f32((uint16_t)(w.x & 0xFFFFu));
           vv[1] = bf16_to_f32((uint16_t)(w.x >> 16));
           vv[2] = bf16_to_f32((uint16_t)(w.y & 0xFFFFu));
           vv[3] = bf16_to_f32((uint16_t)(w.y >> 16));
         } else {
-          const uint32_t w = *reinterpret_cast<const uint32_t*>(
-              reinterpret_cast<const uint8_t*>(a.v_data) + page * (kBlockTokens * D) +
-              ((off >> 2) * D + c3) * 4);
+          const uint32_t w = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(a.v_data) +
+                                                              page * (kBlockTokens * D) + vpage_off(off, c3, D, 1));
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const uint32_t byte = (w >> (8 * j)) & 0xFFu;

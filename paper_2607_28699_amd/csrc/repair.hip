@@ -365,17 +365,19 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
     uint32_t kgw = 0;
     if (valid) {
       uint32_t kb[CH / 4];
-      const uint4* kp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(a.k_data) + row * D + c0);
+      const int64_t kpage = row / kBlockTokens;   // (block, KV head) page
+      const int koff = (int)(row % kBlockTokens);
+      const uint8_t* kpg = reinterpret_cast<const uint8_t*>(a.k_data) + kpage * (kBlockTokens * D);
 #pragma unroll
       for (int w = 0; w < CH / 16; ++w) {
-        const uint4 x = kp[w];
+        const uint4 x = *reinterpret_cast<const uint4*>(kpg + kpage_off(koff, c0 + 16 * w, D, 1));
         kb[4 * w] = x.x; kb[4 * w + 1] = x.y; kb[4 * w + 2] = x.z; kb[4 * w + 3] = x.w;
       }
       uint32_t xb[CH / 2];
-      const uint4* xp = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(ra.x_k_data) + row * D + c0);
+      const uint8_t* xpg = reinterpret_cast<const uint8_t*>(ra.x_k_data) + kpage * (kBlockTokens * D * 2);
 #pragma unroll
       for (int w = 0; w < CH / 8; ++w) {
-        const uint4 x = xp[w];
+        const uint4 x = *reinterpret_cast<const uint4*>(xpg + kpage_off(koff, c0 + 8 * w, D, 2));
         xb[4 * w] = x.x; xb[4 * w + 1] = x.y; xb[4 * w + 2] = x.z; xb[4 * w + 3] = x.w;
       }
       const bool int8 = a.kind == WC_KIND_INT8_DITHER;
@@ -517,9 +519,11 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
       const int64_t slot = i0 < nv ? slot_s[i0] : -1;
       if (slot >= 0) {   // (a table entry outside the caches left the quad out)
         const int64_t page = (slot / kBlockTokens) * a.n_kv + kv;
-        const int64_t vi = page * (kBlockTokens * D) + ((slot % kBlockTokens) >> 2) * D * 4 + c * 4;
-        vb[qq] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(a.v_data) + vi);
-        xb[qq] = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(ra.x_v_data) + vi);
+        const int t = (int)(slot % kBlockTokens);   // first token of the quad
+        vb[qq] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(a.v_data) +
+                                                    page * (kBlockTokens * D) + vpage_off(t, c, D, 1));
+        xb[qq] = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint8_t*>(ra.x_v_data) +
+                                                 page * (kBlockTokens * D * 2) + vpage_off(t, c, D, 2));
       }
     }
 #pragma unroll

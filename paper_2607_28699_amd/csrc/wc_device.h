@@ -124,6 +124,24 @@ __device__ __forceinline__ float e4m3_to_f32(uint32_t b) {
   return (b & 0x80u) ? -v : v;
 }
 
+// ---- page layout of the key and value arrays --------------------------------
+// A page (16 tokens of one KV head) is stored as 16-byte pieces, ordered so that
+// every 16-byte load instruction of the matrix-core decode covers whole cache
+// lines: piece (i, g, r) lies at byte ((i*4 + g)*16 + r)*16, i < CL = D*E/64
+// (E bytes per element).  Keys: piece (i, g, r) holds bytes (g*CL + i)*16 ..
+// +15 of token r's row (D elements, channel order).  Values: token quad q's
+// row holds D channels x 4 tokens (token t of the quad, channel c at element
+// 4c + t), and piece (i, q, r) holds its bytes (r*CL + i)*16 .. +15.
+// Offsets in bytes within the page.
+__host__ __device__ inline int kpage_off(int t, int c, int D, int E) {
+  const int CL = D * E / 64, b = c * E, p = b >> 4;
+  return (((p % CL) * 4 + p / CL) * 16 + t) * 16 + (b & 15);
+}
+__host__ __device__ inline int vpage_off(int t, int c, int D, int E) {
+  const int CL = D * E / 64, b = (4 * c + (t & 3)) * E, p = b >> 4;
+  return (((p % CL) * 4 + (t >> 2)) * 16 + p / CL) * 16 + (b & 15);
+}
+
 // ---- band map -----------------------------------------------------------------
 // Band of channel c: pairs are (j, j + D/2) (rotate-half) or (2j, 2j+1)
 // (interleaved); band b holds pairs b*P .. b*P+P-1 with P = D / (2B).

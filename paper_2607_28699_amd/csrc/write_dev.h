@@ -56,16 +56,13 @@ __device__ __forceinline__ void store_exact(void* k_data, void* v_data, int64_t 
 #pragma unroll
   for (int i = 0; i < 8; ++i)
     kw[i] = (uint32_t)f32_to_bf16_rne(k[2 * i]) | ((uint32_t)f32_to_bf16_rne(k[2 * i + 1]) << 16);
-  uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(k_data) + (bh * kBlockTokens + off) * D +
-                                       16 * g);
-  kd[0] = make_uint4(kw[0], kw[1], kw[2], kw[3]);
-  kd[1] = make_uint4(kw[4], kw[5], kw[6], kw[7]);
+  uint8_t* kpg = reinterpret_cast<uint8_t*>(k_data) + bh * (kBlockTokens * D * 2);
+  *reinterpret_cast<uint4*>(kpg + kpage_off(off, 16 * g, D, 2)) = make_uint4(kw[0], kw[1], kw[2], kw[3]);
+  *reinterpret_cast<uint4*>(kpg + kpage_off(off, 16 * g + 8, D, 2)) = make_uint4(kw[4], kw[5], kw[6], kw[7]);
+  uint8_t* vpg = reinterpret_cast<uint8_t*>(v_data) + bh * (kBlockTokens * D * 2);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    uint16_t* vd = reinterpret_cast<uint16_t*>(v_data) + bh * (kBlockTokens * D) +
-                   ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
-    *vd = f32_to_bf16_rne(v[i]);
-  }
+  for (int i = 0; i < 16; ++i)
+    *reinterpret_cast<uint16_t*>(vpg + vpage_off(off, 16 * g + i, D, 2)) = f32_to_bf16_rne(v[i]);
 }
 
 // One token-head of the write (token tok, KV head h; in_range false: nothing to
@@ -165,11 +162,9 @@ __device__ __forceinline__ int64_t write_token_head(const WriteArgs& a, int64_t 
       vn2 = fma((double)v[i], (double)v[i], vn2);
       // codes are stored excess-128: byte = code + 128
       kc[i >> 2] |= ((uint32_t)((int32_t)ck + 128) & 0xFFu) << (8 * (i & 3));
-      if (active) {
-        uint8_t* vd = reinterpret_cast<uint8_t*>(a.v_data) + bh * (kBlockTokens * D) +
-                      ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
-        *vd = (uint8_t)((int32_t)cv + 128);
-      }
+      if (active)
+        reinterpret_cast<uint8_t*>(a.v_data)[bh * (kBlockTokens * D) + vpage_off(off, 16 * g + i, D, 1)] =
+            (uint8_t)((int32_t)cv + 128);
     }
     // group exponents of the token-head: nibble g/2 from the first lane of each group
     uint32_t ekw = 0, evw = 0;
@@ -183,9 +178,8 @@ __device__ __forceinline__ int64_t write_token_head(const WriteArgs& a, int64_t 
       }
     }
     if (active) {
-      uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(a.k_data) +
-                                           (bh * kBlockTokens + off) * D + 16 * g);
-      *kd = make_uint4(kc[0], kc[1], kc[2], kc[3]);
+      *reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(a.k_data) + bh * (kBlockTokens * D) +
+                                kpage_off(off, 16 * g, D, 1)) = make_uint4(kc[0], kc[1], kc[2], kc[3]);
       if (g == 0) {
         a.k_scale[bh * kBlockTokens + off] = skb;
         a.v_scale[bh * kBlockTokens + off] = svb;
@@ -224,16 +218,13 @@ __device__ __forceinline__ int64_t write_token_head(const WriteArgs& a, int64_t 
       vr2 = fma(rv, rv, vr2);
       vn2 = fma((double)v[i], (double)v[i], vn2);
       kc[i >> 2] |= bk << (8 * (i & 3));
-      if (active) {
-        uint8_t* vd = reinterpret_cast<uint8_t*>(a.v_data) + bh * (kBlockTokens * D) +
-                      ((off >> 2) * D + 16 * g + i) * 4 + (off & 3);
-        *vd = (uint8_t)bv;
-      }
+      if (active)
+        reinterpret_cast<uint8_t*>(a.v_data)[bh * (kBlockTokens * D) + vpage_off(off, 16 * g + i, D, 1)] =
+            (uint8_t)bv;
     }
     if (active) {
-      uint4* kd = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(a.k_data) +
-                                           (bh * kBlockTokens + off) * D + 16 * g);
-      *kd = make_uint4(kc[0], kc[1], kc[2], kc[3]);
+      *reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(a.k_data) + bh * (kBlockTokens * D) +
+                                kpage_off(off, 16 * g, D, 1)) = make_uint4(kc[0], kc[1], kc[2], kc[3]);
     }
   } else {  // WC_KIND_BF16: exact cache, no witness
     if (active) store_exact<D>(a.k_data, a.v_data, bh, off, g, k, v);

@@ -118,8 +118,19 @@ def read_cache(cache, slots):
     out = {}
     kd = t["k_data"].numpy() if cache.kind != "bf16" else t["k_data"].view(__import__("torch").int16).numpy()
     vd = t["v_data"].numpy() if cache.kind != "bf16" else t["v_data"].view(__import__("torch").int16).numpy()
-    out["k"] = kd[blk, :, off, :]
-    out["v"] = vd[blk, :, off // 4, :, off % 4]
+    # pages of 16-byte pieces [CL][4][16][16 bytes] (include/witcert.h): key row bytes
+    # (g*CL + i)*16 .. of token t in piece (i, g, t); value quad q's row (channel c,
+    # token t%4 at element 4c + t%4) bytes (r*CL + i)*16 .. in piece (i, q, r)
+    esz = 2 if cache.kind == "bf16" else 1
+    d = cache.head_dim
+    cl = d * esz // 64
+    c = np.arange(d)
+    kb = c * esz
+    ki, kg, kj = (kb // 16) % cl, (kb // 16) // cl, (kb % 16) // esz
+    out["k"] = kd[blk[:, None], :, ki[None, :], kg[None, :], off[:, None], kj[None, :]].transpose(0, 2, 1)
+    vb = (4 * c[None, :] + (off % 4)[:, None]) * esz
+    vi, vr, vj = (vb // 16) % cl, (vb // 16) // cl, (vb % 16) // esz
+    out["v"] = vd[blk[:, None], :, vi, (off // 4)[:, None], vr, vj].transpose(0, 2, 1)
     if cache.kind == "int8_dither":   # stored excess-128
         out["k"] = out["k"].astype(np.int16) - 128
         out["v"] = out["v"].astype(np.int16) - 128
