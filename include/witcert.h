@@ -36,7 +36,8 @@
  *     no memset nodes).
  *   - Return value: WC_OK (0) or a negative WC_E* code; nothing is enqueued
  *     when an argument check fails.  wc_strerror names the codes.  No C++
- *     exception crosses this boundary.  The library keeps no state and is
+ *     exception crosses this boundary.  The library keeps no state (apart from
+ *     the static scratch of wc_step_metered_decode_gate_noalloc) and is
  *     thread-safe.
  *   - Pointers must be 16-byte aligned; shapes are row-major, innermost last.
  *   - Preconditions not checked on the device: finite inputs, |x| <= 8.28e6
@@ -63,6 +64,7 @@ extern "C" {
 #define WC_EUNSUPPORTED   -2   /* valid but not built (e.g. head_dim 96)        */
 #define WC_EHIP           -3   /* the HIP runtime rejected a launch             */
 #define WC_EWORKSPACE     -4   /* workspace smaller than wc_decode_workspace_size */
+#define WC_ESCRATCH       -5   /* sizes need more than WC_NOALLOC_SCRATCH_BYTES  */
 
 /* ---- element types ---------------------------------------------------- */
 #define WC_F32   0
@@ -446,6 +448,33 @@ int wc_exact_decode_attention(const wc_cache* exact, const void* q, int q_dtype,
                               int64_t max_seq_len, float sm_scale, const uint8_t* mask_kv,
                               void* out, int out_dtype, int split_tokens, void* ws,
                               size_t ws_bytes, void* stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): wc_step_metered_decode_gate
+ * without a workspace argument.  The split records and gate counters live in a
+ * static device array of WC_NOALLOC_SCRATCH_BYTES bytes inside the library, one copy
+ * per GPU, held until the process ends; the call allocates and frees nothing.
+ *   - Returns WC_ESCRATCH (nothing enqueued) when wc_decode_workspace_size(batch,
+ *     n_q_heads, cache->n_kv_heads, cache->head_dim, max_seq_len, split_tokens)
+ *     exceeds WC_NOALLOC_SCRATCH_BYTES (e.g. 4 sequences of 32k tokens x 28 query
+ *     heads need about 2 MiB; 64 sequences up to 32k with a balanced split about 9 MiB).
+ *   - Every call on one GPU uses that GPU's array: calls that overlap on one GPU
+ *     (other streams, other threads) race and give undefined results.  The array
+ *     needs no initialization (the decode clears what it reads back).
+ *   - The array's device address is looked up on the first call on each device
+ *     (that device current); make that first call outside a graph capture.
+ * Other arguments, checks and results as wc_step_metered_decode_gate.
+ */
+#define WC_NOALLOC_SCRATCH_BYTES (16u << 20)
+int wc_step_metered_decode_gate_noalloc(const wc_cache* cache, const wc_cache* exact, const void* new_k,
+                                        const void* new_v, int in_dtype, const int64_t* new_slots,
+                                        const void* q, int q_dtype, int batch, int n_q_heads,
+                                        const int32_t* block_table, int max_blocks_per_seq,
+                                        const int32_t* seq_lens, int64_t max_seq_len, float sm_scale,
+                                        void* out, int out_dtype, float* meter, float* raw, int split_tokens,
+                                        float tau, uint8_t* mask_q, uint8_t* mask_kv, int32_t* n_gated,
+                                        void* stream);
 
 #ifdef __cplusplus
 }

@@ -18,6 +18,7 @@ from .api import (  # noqa: F401
     metered_decode_attention,
     metered_decode_gate,
     step_metered_decode_gate,
+    step_metered_decode_gate_noalloc,
     quantize_write,
     quantize_write_pair,
     repair_workspace,

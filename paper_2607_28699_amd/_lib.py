@@ -10,7 +10,8 @@ import os
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libwitcert.so")
 
-WC_OK, WC_EINVAL, WC_EUNSUPPORTED, WC_EHIP, WC_EWORKSPACE = 0, -1, -2, -3, -4
+WC_OK, WC_EINVAL, WC_EUNSUPPORTED, WC_EHIP, WC_EWORKSPACE, WC_ESCRATCH = 0, -1, -2, -3, -4, -5
+WC_NOALLOC_SCRATCH_BYTES = 16 << 20
 WC_F32, WC_BF16, WC_F16 = 0, 1, 2
 WC_KIND_INT8_DITHER, WC_KIND_FP8_RAW, WC_KIND_BF16 = 0, 1, 2
 WC_ROPE_HALF, WC_ROPE_INTERLEAVED = 0, 1
@@ -20,7 +21,8 @@ EXPORTS = (
     "wc_strerror", "wc_version", "wc_cache_bytes", "wc_quantize_write", "wc_quantize_write_pair",
     "wc_witness", "wc_select_workspace_size", "wc_select_outlier_pairs", "wc_decode_workspace_size",
     "wc_decode_split_tokens", "wc_metered_decode_attention",
-    "wc_metered_decode_gate", "wc_step_metered_decode_gate", "wc_tierb_decode_attention", "wc_joint_decode_gate", "wc_gate",
+    "wc_metered_decode_gate", "wc_step_metered_decode_gate", "wc_step_metered_decode_gate_noalloc",
+    "wc_tierb_decode_attention", "wc_joint_decode_gate", "wc_gate",
     "wc_exact_decode_attention", "wc_block_repair", "wc_block_repair_workspace_size",
 )
 
@@ -85,6 +87,10 @@ def lib() -> ctypes.CDLL:
                                                        ctypes.c_int, ctypes.c_int, vp, ctypes.c_int, vp, i64,
                                                        f32, vp, ctypes.c_int, vp, vp, ctypes.c_int, f32, vp,
                                                        vp, vp, vp, sz, vp]),
+        "wc_step_metered_decode_gate_noalloc": (ctypes.c_int, [cp, cp, vp, vp, ctypes.c_int, vp, vp,
+                                                               ctypes.c_int, ctypes.c_int, ctypes.c_int, vp,
+                                                               ctypes.c_int, vp, i64, f32, vp, ctypes.c_int, vp,
+                                                               vp, ctypes.c_int, f32, vp, vp, vp, vp]),
         "wc_tierb_decode_attention": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int,
                                                      ctypes.c_int, vp, ctypes.c_int, vp, i64, f32,
                                                      vp, ctypes.c_int, vp, vp, ctypes.c_int, f32,

@@ -288,6 +288,28 @@ def step_metered_decode_gate(cache: PagedCache, exact: PagedCache, new_k: torch.
     return out, meter, raw, mask_q, mask_kv
 
 
+def step_metered_decode_gate_noalloc(cache: PagedCache, exact: PagedCache, new_k: torch.Tensor,
+                                     new_v: torch.Tensor, new_slots: torch.Tensor, q: torch.Tensor,
+                                     block_table: torch.Tensor, seq_lens: torch.Tensor, max_seq_len: int,
+                                     sm_scale: float, tau: float, out, meter, raw, mask_q, mask_kv,
+                                     split_tokens: int = 0, n_gated=None):
+    """step_metered_decode_gate for callers that cannot allocate: no workspace (the
+    library's static per-GPU scratch holds the split records); every output is the
+    caller's."""
+    _dev_check(q, block_table, seq_lens, new_k, new_v, new_slots)
+    batch, n_q, d = q.shape
+    assert new_slots.dtype == torch.int64 and new_k.shape == new_v.shape == (batch, cache.n_kv, d)
+    assert new_k.dtype == new_v.dtype
+    c, e = cache.struct(), exact.struct()
+    check(lib().wc_step_metered_decode_gate_noalloc(
+        ctypes.byref(c), ctypes.byref(e), _ptr(new_k), _ptr(new_v), _dt(new_k), _ptr(new_slots), _ptr(q),
+        _dt(q), batch, n_q, _ptr(block_table), block_table.shape[1], _ptr(seq_lens), max_seq_len,
+        float(sm_scale), _ptr(out), _dt(out), _ptr(meter), _ptr(raw), split_tokens, float(tau),
+        _ptr(mask_q), _ptr(mask_kv), _ptr(n_gated), _stream()),
+        "wc_step_metered_decode_gate_noalloc")
+    return out, meter, raw, mask_q, mask_kv
+
+
 def joint_decode_gate(cache: PagedCache, q: torch.Tensor, block_table: torch.Tensor,
                       seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float, tau: float = 0.2,
                       tau_v: float = 0.05, delta_loc: float = 0.0, out_dtype=torch.float32,

@@ -5,6 +5,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
+
 #include "wc_launch.h"
 
 namespace {
@@ -49,6 +51,29 @@ int check_cache(const wc_cache* c, bool need_witness, bool witness_optional = fa
 
 int hip_status(hipError_t e) { return e == hipSuccess ? WC_OK : WC_EHIP; }
 
+// Scratch of wc_step_metered_decode_gate_noalloc (the decode's split records and
+// gate counters) for callers that cannot allocate: a fixed array in device
+// memory, one copy per GPU, held until the process ends.  In host code `scratch`
+// names a host-side stand-in, never the device memory: kernels get the address
+// hipGetSymbolAddress returns on each device, looked up once per device on its
+// first use there (with that device current) and kept in scratch_dev.
+__device__ __attribute__((aligned(256))) uint8_t scratch[WC_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::atomic<void*> scratch_dev[kMaxDevices];
+
+int scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return WC_EHIP;
+  if (dev >= kMaxDevices) return WC_EUNSUPPORTED;
+  void* p = scratch_dev[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return WC_EHIP;
+    scratch_dev[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return WC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -60,11 +85,12 @@ const char* wc_strerror(int status) {
     case WC_EUNSUPPORTED: return "unsupported configuration";
     case WC_EHIP: return "HIP launch error";
     case WC_EWORKSPACE: return "workspace too small";
+    case WC_ESCRATCH: return "sizes exceed the static scratch of the no-allocation entry point";
     default: return "unknown status";
   }
 }
 
-int wc_version(void) { return 101; }   // 1.1: wc_step_metered_decode_gate
+int wc_version(void) { return 102; }   // 1.2: wc_step_metered_decode_gate_noalloc
 
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim, int n_bands,
                       int n_outlier_pairs, int value_side, int group_scales, size_t sizes[10]) {
@@ -349,13 +375,13 @@ int wc_metered_decode_gate(const wc_cache* cache, const void* q, int q_dtype, in
   return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
 }
 
-int wc_step_metered_decode_gate(const wc_cache* cache, const wc_cache* exact, const void* new_k,
-                                const void* new_v, int in_dtype, const int64_t* new_slots, const void* q,
-                                int q_dtype, int batch, int n_q_heads, const int32_t* block_table,
-                                int max_blocks_per_seq, const int32_t* seq_lens, int64_t max_seq_len,
-                                float sm_scale, void* out, int out_dtype, float* meter, float* raw,
-                                int split_tokens, float tau, uint8_t* mask_q, uint8_t* mask_kv,
-                                int32_t* n_gated, void* ws, size_t ws_bytes, void* stream) {
+static int step_common(const wc_cache* cache, const wc_cache* exact, const void* new_k,
+                       const void* new_v, int in_dtype, const int64_t* new_slots, const void* q,
+                       int q_dtype, int batch, int n_q_heads, const int32_t* block_table,
+                       int max_blocks_per_seq, const int32_t* seq_lens, int64_t max_seq_len,
+                       float sm_scale, void* out, int out_dtype, float* meter, float* raw,
+                       int split_tokens, float tau, uint8_t* mask_q, uint8_t* mask_kv,
+                       int32_t* n_gated, void* ws, size_t ws_bytes, void* stream) {
   if (exact == nullptr) return WC_EINVAL;
   wc::WriteArgs w;
   int s = write_args(cache, exact, new_k, new_v, in_dtype, new_slots, batch, w);
@@ -385,6 +411,40 @@ int wc_step_metered_decode_gate(const wc_cache* cache, const wc_cache* exact, co
   }
   const hipError_t e = wc::launch_quantize_write(w, st);
   return hip_status(e != hipSuccess ? e : wc::launch_decode(a, true, st));
+}
+
+int wc_step_metered_decode_gate(const wc_cache* cache, const wc_cache* exact, const void* new_k,
+                                const void* new_v, int in_dtype, const int64_t* new_slots, const void* q,
+                                int q_dtype, int batch, int n_q_heads, const int32_t* block_table,
+                                int max_blocks_per_seq, const int32_t* seq_lens, int64_t max_seq_len,
+                                float sm_scale, void* out, int out_dtype, float* meter, float* raw,
+                                int split_tokens, float tau, uint8_t* mask_q, uint8_t* mask_kv,
+                                int32_t* n_gated, void* ws, size_t ws_bytes, void* stream) {
+  return step_common(cache, exact, new_k, new_v, in_dtype, new_slots, q, q_dtype, batch, n_q_heads,
+                     block_table, max_blocks_per_seq, seq_lens, max_seq_len, sm_scale, out, out_dtype, meter,
+                     raw, split_tokens, tau, mask_q, mask_kv, n_gated, ws, ws_bytes, stream);
+}
+
+int wc_step_metered_decode_gate_noalloc(const wc_cache* cache, const wc_cache* exact, const void* new_k,
+                                        const void* new_v, int in_dtype, const int64_t* new_slots,
+                                        const void* q, int q_dtype, int batch, int n_q_heads,
+                                        const int32_t* block_table, int max_blocks_per_seq,
+                                        const int32_t* seq_lens, int64_t max_seq_len, float sm_scale,
+                                        void* out, int out_dtype, float* meter, float* raw, int split_tokens,
+                                        float tau, uint8_t* mask_q, uint8_t* mask_kv, int32_t* n_gated,
+                                        void* stream) {
+  if (cache == nullptr) return WC_EINVAL;
+  // (a size of 0 means invalid sizes: step_common reports those)
+  const size_t need = wc_decode_workspace_size(batch, n_q_heads, cache->n_kv_heads, cache->head_dim,
+                                               max_seq_len, split_tokens);
+  if (need > (size_t)WC_NOALLOC_SCRATCH_BYTES) return WC_ESCRATCH;
+  void* ws = nullptr;
+  const int s = scratch_address(&ws);
+  if (s != WC_OK) return s;
+  return step_common(cache, exact, new_k, new_v, in_dtype, new_slots, q, q_dtype, batch, n_q_heads,
+                     block_table, max_blocks_per_seq, seq_lens, max_seq_len, sm_scale, out, out_dtype, meter,
+                     raw, split_tokens, tau, mask_q, mask_kv, n_gated, ws, (size_t)WC_NOALLOC_SCRATCH_BYTES,
+                     stream);
 }
 
 int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int batch,

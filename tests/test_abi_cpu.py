@@ -186,3 +186,25 @@ def test_step_call_argument_checks(L):
     assert step(ctypes.byref(c), ctypes.byref(ex), tau=-1.0) == _lib.WC_EINVAL
     assert step(ctypes.byref(c), ctypes.byref(ex), ws_bytes=64) == _lib.WC_EWORKSPACE
     assert step(ctypes.byref(ex), ctypes.byref(ex)) == _lib.WC_EINVAL         # the metered cache is quantized
+
+
+def test_noalloc_step_call_checks(L):
+    """wc_step_metered_decode_gate_noalloc refuses sizes beyond its static scratch
+    before touching any device, and a missing cache."""
+    c = _lib.WcCache(_lib.WC_KIND_INT8_DITHER, 128, 4, 8, 0, 0, 1 << 20, 0, 16, 16, 16, 16, 16, 0, 0,
+                     None, None, None, None)
+    ex = _lib.WcCache(_lib.WC_KIND_BF16, 128, 4, 0, 0, 0, 1 << 20, 0, 16, 16)
+
+    def step(cache, batch, max_len, split=0):
+        return L.wc_step_metered_decode_gate_noalloc(
+            cache, ctypes.byref(ex), 16, 16, _lib.WC_BF16, 16, 16, _lib.WC_BF16, batch, 28, 16,
+            (max_len + 15) // 16, 16, max_len, 0.1, 16, _lib.WC_BF16, 16, 16, split, 0.2, 16, 16, None, None)
+    need = L.wc_decode_workspace_size(512, 28, 4, 128, 1 << 17, 256)
+    assert need > _lib.WC_NOALLOC_SCRATCH_BYTES
+    assert step(ctypes.byref(c), 512, 1 << 17, 256) == _lib.WC_ESCRATCH
+    assert step(None, 4, 32768) == _lib.WC_EINVAL
+    assert L.wc_strerror(_lib.WC_ESCRATCH).startswith(b"sizes exceed the static scratch")
+    # the workloads' sizes fit: 4 x 32k and the 64-sequence serving mix's balanced split
+    assert L.wc_decode_workspace_size(4, 28, 4, 128, 32768 + 64, 0) <= _lib.WC_NOALLOC_SCRATCH_BYTES
+    st = L.wc_decode_split_tokens(64, 4, 32768 + 64, 64 * 7756, 0)
+    assert L.wc_decode_workspace_size(64, 28, 4, 128, 32768 + 64, st) <= _lib.WC_NOALLOC_SCRATCH_BYTES
