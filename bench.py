@@ -53,6 +53,8 @@ def parse():
     ap.add_argument("--no-group-scales", dest="group_scales", action="store_false",
                     help="skip the measurement over caches with 32-channel group scales")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-workloads", dest="other_workloads", action="store_false",
+                    help="skip the per-call figures of the 4k, 131k and serving workloads")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter calibration)")
@@ -68,6 +70,32 @@ def copy_calibration():
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes_each_way": n, "launches": 3}), flush=True)
+
+
+def make_timer(np, torch):
+    """timed(fn, reps): fn(0) .. fn(reps - 1) captured back to back in one HIP graph,
+    the graph replayed five times between events recorded on the launching stream;
+    per-call milliseconds of each replay."""
+    def timed(fn, reps, replays=5):
+        fn(0)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(reps):
+                fn(i)
+        g.replay()
+        torch.cuda.synchronize()
+        per_call = []
+        for _ in range(replays):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            per_call.append(e0.elapsed_time(e1) / reps)
+        del g
+        return np.array(per_call)
+    return timed
 
 
 class Layout:
@@ -128,11 +156,114 @@ def cpu_baseline(wl, lens, tau, seconds, np, torch):
             break
     info = threadpoolctl.threadpool_info()
     blas = max([p.get("num_threads", 1) for p in info if p.get("user_api") == "blas"] or [1])
+    # the same cell on one core (BLAS limited to one thread): the single-core figure
+    one_t, one_tok = 0.0, 0
+    with threadpoolctl.threadpool_limits(limits=1):
+        while one_t < min(seconds / 4, 5.0):
+            t0 = time.perf_counter()
+            new = odec.write_cache("int8_dither", kn, vn, slots[L:], layer, wl.philox_seed(), wl.bands,
+                                   wl.rope_layout)
+            res = odec.metered_decode(q, np.concatenate([cache["khat"], new["khat"]]),
+                                      np.concatenate([cache["vhat"], new["vhat"]]),
+                                      np.concatenate([cache["kw"], new["kw"]]), sm, wl.bands, wl.rope_layout)
+            mq = ogate.gate_q(res["meter"], res["raw"], tau)
+            ex = odec.exact_decode(q, np.concatenate([k, kn]), np.concatenate([v, vn]), sm)
+            _ = ogate.apply_fallback(res["out"], ex["out"], ogate.gate_kv(mq[None], wl.group)[0], wl.group)
+            one_t += time.perf_counter() - t0
+            one_tok += L + 1
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = os.cpu_count()
     return {"value": tokens / timed, "unit": "KV tokens/s", "cores": int(blas), "kind": "oracle",
+            "os_cpu_count": os.cpu_count(), "affinity_cpus": affinity, "blas_threads": int(blas),
+            "single_core_value": one_tok / one_t,
             "sample": (f"{samples} (sequence, layer) cells at context {int(lens[0])}: new-token write, "
                        f"metered decode of all {wl.n_q} query heads, gate at tau={tau}, exact fallback; "
                        f"{timed:.1f} s of oracle time (float64 numpy; BLAS threads={blas}, "
-                       f"elementwise single-threaded)")}
+                       f"elementwise single-threaded); single_core_value: the last cell again with "
+                       f"BLAS limited to one thread for {one_t:.1f} s")}
+
+
+# distinct layer caches per other workload: enough that the captured calls read
+# well past the 256 MB MALL (4k x 8: 36 MB per layer; 131k x 1: 145 MB; serving: 550 MB)
+OTHER_WORKLOADS = {"gqa-28x4-d128-s4k-b8": 28, "gqa-28x4-d128-s131k-b1": 8, "serving-64seq-paged": 2}
+
+
+def other_workload(name, n_layers, tau, timed, np, torch):
+    """Per-call figures of another workload's hot path: the metered INT8 decode with
+    the gate, the exact fallback of the KV heads it routes, and the prefill write
+    (quant + witness + exact copy); each call captured back to back over distinct
+    layer caches and timed from graph replays, as for the main workload."""
+    import paper_2607_28699_amd as wc
+    import synth
+    from synth import torch_gen
+    wl = synth.WORKLOADS[name]
+    dev = "cuda"
+    lens = (synth.serving_lengths(wl.batch, wl.len_lo, wl.ctx) if wl.ragged
+            else np.full(wl.batch, wl.ctx, dtype=np.int64))
+    lay = Layout(wl.replace(chunk=0), lens, 0, np)
+    caches, exact, qs = [], [], []
+    wr_in = None
+    for layer in range(n_layers):
+        c = wc.PagedCache("int8_dither", lay.nblocks, wl.n_kv, wl.d, wl.bands, layer=layer,
+                          seed=wl.philox_seed(), rope_layout=wl.rope_layout)
+        e = wc.PagedCache("bf16", lay.nblocks, wl.n_kv, wl.d, 0, layer=layer)
+        ks, vs, ss = [], [], []
+        for b in range(lay.batch):
+            k, v = torch_gen.gen_kv_layer(wl, layer, b, torch.arange(int(lens[b]), device=dev))
+            ks.append(k)
+            vs.append(v)
+            ss.append(torch.from_numpy(lay.slots(b, np.arange(int(lens[b])), np)).to(dev))
+        k, v, sl = torch.cat(ks), torch.cat(vs), torch.cat(ss)
+        wc.quantize_write_pair(c, e, k, v, sl)
+        if layer == 0:
+            wr_in = (k, v, sl)
+        del ks, vs
+        caches.append(c)
+        exact.append(e)
+        qs.append(torch_gen.gen_q_batch(wl, layer, 0, torch.from_numpy(lens - 1).to(dev)))
+    torch.cuda.synchronize()
+    table = torch.from_numpy(lay.table).to(dev)
+    seq_lens = torch.from_numpy(lens.astype(np.int32)).to(dev)
+    L = int(lens.max())
+    ST = wc.split_tokens_for(lay.batch, wl.n_kv, L, total_tokens=int(lens.sum()))
+    ws = wc.decode_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, L, ST)
+    out = torch.empty((lay.batch, wl.n_q, wl.d), dtype=torch.bfloat16, device=dev)
+    meter = torch.empty((lay.batch, wl.n_q), dtype=torch.float32, device=dev)
+    raw = torch.empty_like(meter)
+    mask_q = torch.empty((lay.batch, wl.n_q), dtype=torch.uint8, device=dev)
+    mask_kv = torch.empty((lay.batch, wl.n_kv), dtype=torch.uint8, device=dev)
+    sm = 1.0 / np.sqrt(wl.d)
+    reps = 56
+    dec_ms = float(np.median(timed(lambda i: wc.metered_decode_gate(
+        caches[i % n_layers], qs[i % n_layers], table, seq_lens, L, sm, tau, ws=ws, split_tokens=ST, out=out,
+        meter=meter, raw=raw, mask_q=mask_q, mask_kv=mask_kv), reps)))
+    routed = float(mask_kv.float().mean().item())
+    fb_ms = float(np.median(timed(lambda i: wc.exact_decode_attention(
+        exact[i % n_layers], qs[i % n_layers], table, seq_lens, L, sm, mask_kv, out, ws=ws, split_tokens=ST),
+        reps)))
+    k, v, sl = wr_in
+    wr_ms = float(np.median(timed(lambda i: wc.quantize_write_pair(caches[0], exact[0], k, v, sl), 4)))
+    th = float(lens.sum()) * wl.n_kv                     # token-heads per call
+    int8_b, bf16_b = 2 * wl.d + 4 + 2 * wl.bands, 4 * wl.d
+    wr_b = 2 * wl.d * 2 + int8_b + bf16_b                 # bf16 K, V in; INT8 cache + exact copy out
+    gb = lambda nbytes, ms: nbytes / (ms * 1e-3) / 1e9
+    res = {"batch": lay.batch, "context": L, "mean_context": float(lens.mean()), "split_tokens": ST,
+           "layer_caches": n_layers,
+           "metered_decode": {"median_launch_ms": round(dec_ms, 4), "GBps": round(gb(th * int8_b, dec_ms), 1),
+                              "frac_hbm": round(gb(th * int8_b, dec_ms) / HBM_PEAK_GBPS, 4),
+                              "bytes_per_token_head": int8_b},
+           "exact_fallback": {"median_launch_ms": round(fb_ms, 4), "routed_kv_fraction": routed,
+                              "GBps": round(gb(th * routed * bf16_b, fb_ms), 1),
+                              "frac_hbm": round(gb(th * routed * bf16_b, fb_ms) / HBM_PEAK_GBPS, 4)},
+           "write_pair": {"median_launch_ms": round(wr_ms, 4), "token_heads": int(k.shape[0] * wl.n_kv),
+                          "bytes_per_token_head": wr_b,
+                          "GBps": round(gb(k.shape[0] * wl.n_kv * wr_b, wr_ms), 1),
+                          "frac_hbm": round(gb(k.shape[0] * wl.n_kv * wr_b, wr_ms) / HBM_PEAK_GBPS, 4)}}
+    del caches, exact, qs, ws, wr_in
+    torch.cuda.empty_cache()
+    return res
 
 
 def main():
@@ -298,25 +429,7 @@ def main():
 
     # ---- per-call timing: reps calls captured back to back in one HIP graph, the
     # replays timed with events on the launch stream (no host gaps between calls) ----
-    def timed(fn, reps, replays=5):
-        fn(0)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for i in range(reps):
-                fn(i)
-        g.replay()
-        torch.cuda.synchronize()
-        per_call = []
-        for _ in range(replays):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            g.replay()
-            e1.record()
-            torch.cuda.synchronize()
-            per_call.append(e0.elapsed_time(e1) / reps)
-        del g
-        return np.array(per_call)
+    timed = make_timer(np, torch)
 
     # quantize+witness write of the prefill: layer 0's sequences, each call
     # rewriting the same slots with the same values
@@ -546,38 +659,48 @@ def main():
     fb_gbps = fb_bytes / (float(np.median(fb_ms)) * 1e-3) / 1e9 if routed > 0 else 0.0
     write_gbps = write_tokens * WRITE_BYTES_BF16_IN / (write_ms * 1e-3) / 1e9   # per prefill of one layer
 
-    dominant = "metered_decode" if float(np.median(dec_ms)) >= float(np.median(fb_ms)) else "exact_fallback"
-    traffic = None
-    prof = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
-    if os.path.exists(prof):
+    # The roofline object is the metric's kernel: the metered INT8 decode with its
+    # fused gate (decode_mfma_kernel + merge_kernel), 276 algorithmic bytes per
+    # token-head over the call's token-heads, per-call time from the event-timed
+    # graph replays above.  The exact fallback gets an object of its own.
+    def traffic_of(key):
+        prof = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
+        if not os.path.exists(prof):
+            return None
         with open(prof) as fh:
             pj = json.load(fh)
-        if pj.get("kernel_source_hash") == kernel_source_hash():
-            traffic = pj.get("bytes_per_launch", {}).get(dominant)
-    if dominant == "metered_decode":
-        roof = {"kernel": "metered decode with gate (decode_mfma_kernel + merge_kernel)", "bound": "hbm",
-                "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                "algorithmic_bytes_per_launch": th_per_launch * INT8_BYTES,
-                "median_launch_ms": round(float(np.median(dec_ms)), 4)}
-    else:
-        roof = {"kernel": "exact bf16 fallback (decode_mfma_kernel + merge_kernel)", "bound": "hbm",
-                "achieved": round(fb_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(fb_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                "algorithmic_bytes_per_launch": fb_bytes,
-                "median_launch_ms": round(float(np.median(fb_ms)), 4)}
+        if pj.get("kernel_source_hash") != kernel_source_hash():
+            return None
+        return pj.get("bytes_per_launch", {}).get(key)
+
+    roof = {"kernel": "metered INT8 decode with the gate (decode_mfma_kernel + merge_kernel)", "bound": "hbm",
+            "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic_of("metered_decode"),
+            "algorithmic_bytes_per_launch": th_per_launch * INT8_BYTES,
+            "bytes_per_token_head": INT8_BYTES, "token_heads_per_launch": th_per_launch,
+            "median_launch_ms": round(float(np.median(dec_ms)), 4)}
+    roof_fb = {"kernel": "exact bf16 fallback (decode_mfma_kernel + merge_kernel)", "bound": "hbm",
+               "achieved": round(fb_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+               "frac": round(fb_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic_of("exact_fallback"),
+               "algorithmic_bytes_per_launch": fb_bytes, "bytes_per_token_head": BF16_BYTES,
+               "routed_kv_fraction": routed, "median_launch_ms": round(float(np.median(fb_ms)), 4)}
 
     line = {
         "metric": "metered INT8 decode-attn KV tokens/s & HBM GB/s (% peak); quant+witness GB/s",
         "value": round(value, 1), "unit": "KV tokens/s", "n_gpus": 1, "steps": K, "warmup": W,
         "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "vs_baseline": None,
+        "dtype": "fp16 MFMA operands (exact int8 codes and dither), fp32 accumulate; bf16 q, K/V inputs and out",
+        "data": "synthetic",
         "config": {"workload": wl.name, "layers": wl.n_layers, "n_q": wl.n_q, "n_kv": wl.n_kv,
                    "head_dim": wl.d, "bands": wl.bands, "batch": lay.batch,
                    "context": int(lens0.max()), "mean_context": float(lens0.mean()),
                    "tau": args.tau, "split_tokens": ST, "cache": "int8 dither + fp16 scales + fp16 key witness",
                    "fallback": "bf16 exact cache in HBM"},
         "roofline": roof,
+        "roofline_exact_fallback": roof_fb,
+        "value_note": ("KV tokens attended per second over whole decode steps; each step includes the bf16 "
+                       "exact-fallback re-read of the routed KV heads (routed fraction in gate)"),
         "metered_decode": {"median_launch_ms": round(float(np.median(dec_ms)), 4), "GBps": round(dec_gbps, 1),
                            "frac_hbm": round(dec_gbps / HBM_PEAK_GBPS, 4),
                            "bytes_per_token_head": INT8_BYTES},
@@ -605,6 +728,12 @@ def main():
                           "token_heads": write_tokens},
         "kernel_source_hash": kernel_source_hash(),
     }
+    if args.other_workloads and args.workload == "gqa-28x4-d128-s32k-b4":
+        # free the main workload's caches first
+        del caches, exact, byp_caches, gs_caches, fp8_caches, graphs, steps_in
+        torch.cuda.empty_cache()
+        line["other_workloads"] = {n: other_workload(n, nl, args.tau, timed, np, torch)
+                                   for n, nl in OTHER_WORKLOADS.items()}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, lens0, args.tau, args.cpu_seconds, np, torch)
     print(json.dumps(line), flush=True)

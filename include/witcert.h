@@ -309,6 +309,17 @@ int wc_metered_decode_attention(const wc_cache* cache, const void* q, int q_dtyp
  * delta_loc in (0, 1) is the per-(layer, head, step) budget, e.g. delta_req /
  * (layers * query heads * steps).
  */
+/*
+ * Per-(layer, head, step) failure budget of Tier B (Sec. 4.2, request-level
+ * budget by the union bound over the request's certificates):
+ *   delta_loc = delta_req / (n_layers * n_q_heads * n_steps),
+ * delta_req in (0, 1) the request's budget, n_steps the decode steps it runs
+ * (the serving experiments of Sec. 6.2 take 256).  Returns -1 for invalid
+ * arguments.  Pass the result (rounded to float) as wc_tierb_decode_attention's
+ * delta_loc.
+ */
+double wc_tierb_delta_loc(double delta_req, int n_layers, int n_q_heads, int n_steps);
+
 int wc_tierb_decode_attention(const wc_cache* cache, const void* q, int q_dtype, int batch,
                               int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
                               const int32_t* seq_lens, int64_t max_seq_len, float sm_scale,

@@ -2,8 +2,9 @@
 
 TEST INFRASTRUCTURE ONLY (see the package header).
 
-Definitions followed (Sec. 4.2 "Outlier RoPE pairs"; Sec. 6.2 "Fixed-channel
-outlier bypass: two steps that must both be taken", Tables 5 and 6):
+Definitions followed (Sec. 4.2, outlier RoPE pairs; Sec. 6.2, fixed-channel
+bypass, where keeping the pairs in fp16 and taking them out of the amax are both
+needed; Tables 5 and 6):
 
 * A small set P of m RoPE frequency pairs per (layer, KV head) is kept in fp16
   instead of INT8.  A pair is bypassed whole (both of its channels), because

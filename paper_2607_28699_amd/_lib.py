@@ -22,7 +22,7 @@ EXPORTS = (
     "wc_witness", "wc_select_workspace_size", "wc_select_outlier_pairs", "wc_decode_workspace_size",
     "wc_decode_split_tokens", "wc_metered_decode_attention",
     "wc_metered_decode_gate", "wc_step_metered_decode_gate", "wc_step_metered_decode_gate_noalloc",
-    "wc_tierb_decode_attention", "wc_joint_decode_gate", "wc_gate",
+    "wc_tierb_decode_attention", "wc_tierb_delta_loc", "wc_joint_decode_gate", "wc_gate",
     "wc_exact_decode_attention", "wc_block_repair", "wc_block_repair_workspace_size",
 )
 
@@ -91,6 +91,7 @@ def lib() -> ctypes.CDLL:
                                                                ctypes.c_int, ctypes.c_int, ctypes.c_int, vp,
                                                                ctypes.c_int, vp, i64, f32, vp, ctypes.c_int, vp,
                                                                vp, ctypes.c_int, f32, vp, vp, vp, vp]),
+        "wc_tierb_delta_loc": (ctypes.c_double, [ctypes.c_double, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
         "wc_tierb_decode_attention": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int,
                                                      ctypes.c_int, vp, ctypes.c_int, vp, i64, f32,
                                                      vp, ctypes.c_int, vp, vp, ctypes.c_int, f32,

@@ -210,8 +210,11 @@ def metered_decode_attention(cache: PagedCache, q: torch.Tensor, block_table: to
 
 
 def tierb_delta_loc(delta_req: float, n_layers: int, n_q_heads: int, n_steps: int) -> float:
-    """Per-(layer, head, step) failure budget delta_req / (L * H * T) (Sec. 4.2)."""
-    return float(delta_req) / (n_layers * n_q_heads * n_steps)
+    """Per-(layer, head, step) failure budget of Tier B (wc_tierb_delta_loc)."""
+    d = lib().wc_tierb_delta_loc(float(delta_req), int(n_layers), int(n_q_heads), int(n_steps))
+    if d <= 0.0:
+        raise _lib.WitCertError("wc_tierb_delta_loc: invalid arguments")
+    return float(d)
 
 
 def tierb_decode_attention(cache: PagedCache, q: torch.Tensor, block_table: torch.Tensor,

@@ -331,6 +331,11 @@ int wc_metered_decode_attention(const wc_cache* cache, const void* q, int q_dtyp
   return hip_status(wc::launch_decode(a, true, static_cast<hipStream_t>(stream)));
 }
 
+double wc_tierb_delta_loc(double delta_req, int n_layers, int n_q_heads, int n_steps) {
+  if (!(delta_req > 0.0 && delta_req < 1.0) || n_layers < 1 || n_q_heads < 1 || n_steps < 1) return -1.0;
+  return delta_req / ((double)n_layers * (double)n_q_heads * (double)n_steps);
+}
+
 int wc_tierb_decode_attention(const wc_cache* cache, const void* q, int q_dtype, int batch,
                               int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
                               const int32_t* seq_lens, int64_t max_seq_len, float sm_scale,

@@ -174,3 +174,8 @@ def out_tol(wl):
 
 
 _ = ofp  # the oracle's format helpers are the reference for fp16 values
+
+
+def bf16_bits_to_f32(bits):
+    """bf16 bit patterns (any integer dtype) -> float32 values."""
+    return (np.asarray(bits).astype(np.uint16).astype(np.uint32) << 16).view(np.float32)

@@ -208,3 +208,11 @@ def test_noalloc_step_call_checks(L):
     assert L.wc_decode_workspace_size(4, 28, 4, 128, 32768 + 64, 0) <= _lib.WC_NOALLOC_SCRATCH_BYTES
     st = L.wc_decode_split_tokens(64, 4, 32768 + 64, 64 * 7756, 0)
     assert L.wc_decode_workspace_size(64, 28, 4, 128, 32768 + 64, st) <= _lib.WC_NOALLOC_SCRATCH_BYTES
+
+
+def test_tierb_delta_loc(L):
+    """The request-level budget split over layers x query heads x steps (Sec. 4.2)."""
+    assert L.wc_tierb_delta_loc(1e-2, 28, 28, 256) == pytest.approx(1e-2 / (28 * 28 * 256), rel=1e-15)
+    assert L.wc_tierb_delta_loc(0.5, 1, 1, 1) == 0.5
+    for bad in ((0.0, 1, 1, 1), (1.0, 1, 1, 1), (1e-2, 0, 1, 1), (1e-2, 1, 0, 1), (1e-2, 1, 1, 0)):
+        assert L.wc_tierb_delta_loc(*bad) == -1.0

@@ -83,18 +83,27 @@ def test_fp8_subnormal_codes():
 
 
 def test_split_count_invariance():
+    """The LSE merge is exact in exact arithmetic (Sec. 6.2): outputs of different
+    split counts differ only by the rounding of the fp16 PV weights, each at most
+    2^-11 relative in either run, so |o - o'| <= 2 * 2^-11 * max_t |vhat_t - o|
+    per query head (the weights are normalized by the same rounded sum); raw is
+    formed from fp32 weights and agrees to 1e-4 relative."""
     S.say("[decode] split invariance")
     case = S.make_case(W_GQA, [2000, 1500], permute=True)
     cache = S.gpu_cache(case, "int8_dither")
+    ref = S.oracle_write(case, "int8_dither")
     o1, m1, r1 = S.gpu_decode(case, cache, split_tokens=64)
     o2, m2, r2 = S.gpu_decode(case, cache, split_tokens=2048)
     o3, m3, r3 = S.gpu_decode(case, cache, split_tokens=0)
-    # the merge is exact in exact arithmetic; numerically the splits differ by the
-    # rounding of the fp16 softmax weights relative to each split's running max
-    tol = S.out_tol(W_GQA)
-    for o, r in ((o2, r2), (o3, r3)):
-        assert S.rel_err(o, o1) < tol
-        assert np.all(np.abs(r - r1) <= tol * np.abs(r1))
+    for b, c in enumerate(ref):
+        vh = c["vhat"]                                        # [S, n_kv, d]
+        for h in range(W_GQA.n_q):
+            g = h // W_GQA.group
+            spread = np.max(np.abs(vh[:, g, :] - o1[b, h][None, :]))
+            for o in (o2, o3):
+                assert np.max(np.abs(o[b, h] - o1[b, h])) <= 2.0 ** -10 * spread, (b, h)
+    for r in (r2, r3):
+        assert np.all(np.abs(r - r1) <= 1e-4 * np.abs(r1))
 
 
 def test_bf16_output_is_rounded_fp32_output():

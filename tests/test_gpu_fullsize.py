@@ -1,9 +1,13 @@
 """Parity at the full workload sizes, in the launch configuration bench.py times.
 
-One layer of each long-context workload is written through wc_quantize_write and
-decoded with the same split choice as the benchmark (max_seq_len = prefill +
-steps + warmup); sampled (sequence, query head) cells are recomputed by the
-oracle one by one from the stored inputs of that cell, and sampled tokens'
+One layer of each long-context workload is prefilled through
+wc_quantize_write_pair (quantized cache and bf16 exact copy), then one decode step
+runs through wc_step_metered_decode_gate -- the call bench.py times, the step's
+token written by the decode kernel itself -- with bench.py's split choice
+(max_seq_len = prefill + steps + warmup, the split balanced over the batch's
+total tokens; the serving mix with all 64 sequences).  Sampled (sequence, query
+head) cells, the shortest and the longest sequence among them, are recomputed by
+the oracle one by one from the stored inputs of that cell, and sampled tokens'
 codes are compared bit-exactly.  Also: the matrix-core and vector-ALU decode
 paths agree on the same cache.
 """
@@ -24,7 +28,7 @@ pytestmark = pytest.mark.gpu
 BENCH_STEPS, BENCH_WARMUP = 8, 2
 
 
-def _setup(name, n_lens=None):
+def _setup(name):
     import torch
 
     import paper_2607_28699_amd as wc
@@ -32,26 +36,31 @@ def _setup(name, n_lens=None):
     wl = synth.WORKLOADS[name]
     lens0 = (synth.serving_lengths(wl.batch, wl.len_lo, wl.ctx) if wl.ragged
              else np.full(wl.batch, wl.ctx, dtype=np.int64))
-    if n_lens is not None:
-        lens0 = lens0[:n_lens]
     extra = BENCH_STEPS + BENCH_WARMUP
     table, nblocks = synth.block_table(lens0 + extra, permute=wl.ragged, seed_key=wl.wid)
     layer = 5
     cache = wc.PagedCache("int8_dither", nblocks, wl.n_kv, wl.d, wl.bands, layer=layer,
                           seed=wl.philox_seed(), rope_layout=wl.rope_layout)
-    kv = []
+    exact = wc.PagedCache("bf16", nblocks, wl.n_kv, wl.d, 0, layer=layer)
+    kv, new_k, new_v, new_slots = [], [], [], []
     for b, L in enumerate(lens0):
         pos = torch.arange(int(L) + 1, device="cuda")
         k, v = torch_gen.gen_kv_layer(wl, layer, b, pos)
         sl = synth.slots_of(table, b, np.arange(int(L) + 1))
-        wc.quantize_write(cache, k, v, torch.from_numpy(sl).cuda())
+        wc.quantize_write_pair(cache, exact, k[:-1], v[:-1], torch.from_numpy(sl[:-1]).cuda())
         kv.append((k, v, sl))
+        new_k.append(k[-1])
+        new_v.append(v[-1])
+        new_slots.append(int(sl[-1]))
     pos = torch.from_numpy(lens0).cuda()
     q = torch_gen.gen_q_batch(wl, layer, 0, pos)
     lens = torch.from_numpy((lens0 + 1).astype(np.int32)).cuda()
     tab = torch.from_numpy(table).cuda()
     max_len = int(lens0.max() + extra)
-    return wl, lens0, cache, kv, q, tab, lens, max_len, layer
+    # bench.py's split: balanced over the batch's total tokens at the last timed step
+    st = wc.split_tokens_for(len(lens0), wl.n_kv, max_len, total_tokens=int((lens0 + extra).sum()))
+    step = (torch.stack(new_k), torch.stack(new_v), torch.tensor(new_slots, dtype=torch.int64, device="cuda"))
+    return wl, lens0, cache, exact, kv, q, tab, lens, max_len, layer, st, step
 
 
 def _cell_check(wl, kv, q, b, h, layer):
@@ -71,42 +80,52 @@ def _cell_check(wl, kv, q, b, h, layer):
     return res, tv, kc, vc, ks
 
 
-@pytest.mark.parametrize("name,n_lens", [("gqa-28x4-d128-s32k-b4", None),
-                                         ("gqa-28x4-d128-s131k-b1", None),
-                                         ("serving-64seq-paged", 16)])
-def test_fullsize_sampled_cells(name, n_lens):
+@pytest.mark.parametrize("name", ["gqa-28x4-d128-s32k-b4", "gqa-28x4-d128-s131k-b1", "serving-64seq-paged"])
+def test_fullsize_sampled_cells(name):
     import torch
 
     import paper_2607_28699_amd as wc
     S.say(f"[fullsize] {name}")
-    wl, lens0, cache, kv, q, tab, lens, max_len, layer = _setup(name, n_lens)
-    out, meter, raw = wc.metered_decode_attention(cache, q, tab, lens, max_len, 1 / np.sqrt(wl.d))
+    wl, lens0, cache, exact, kv, q, tab, lens, max_len, layer, st, (nk, nv, ns) = _setup(name)
+    sm = 1 / np.sqrt(wl.d)
+    tau = 0.2
+    out, meter, raw, mask_q, mask_kv = wc.step_metered_decode_gate(cache, exact, nk, nv, ns, q, tab, lens,
+                                                                   max_len, sm, tau, split_tokens=st)
     dloc = wc.tierb_delta_loc(1e-2, wl.n_layers, wl.n_q, 256)
-    _, meter_b, raw_b = wc.tierb_decode_attention(cache, q, tab, lens, max_len, 1 / np.sqrt(wl.d), dloc)
+    _, meter_b, raw_b = wc.tierb_decode_attention(cache, q, tab, lens, max_len, sm, dloc, split_tokens=st)
     torch.cuda.synchronize()
     out, meter, raw = out.cpu().numpy(), meter.cpu().numpy(), raw.cpu().numpy()
+    mask_q, mask_kv = mask_q.cpu().numpy(), mask_kv.cpu().numpy()
     meter_b, raw_b = meter_b.cpu().numpy(), raw_b.cpu().numpy()
+    # the gate as a function of the GPU's meter (the end-to-end decision is in the gate tests)
+    assert np.array_equal(mask_q, (meter > tau).astype(np.uint8))
+    assert np.array_equal(mask_kv, mask_q.reshape(len(lens0), wl.n_kv, wl.group).max(-1))
     rng = np.random.default_rng(17)
-    cells = [(int(rng.integers(len(lens0))), int(rng.integers(wl.n_q))) for _ in range(3)]
+    seqs = sorted({int(np.argmin(lens0)), int(np.argmax(lens0)), int(rng.integers(len(lens0)))})
+    cells = [(b, int(rng.integers(wl.n_q))) for b in seqs]
     for b, h in cells:
-        S.say(f"  cell b={b} h={h} L={int(lens0[b]) + 1}")
+        S.say(f"  cell b={b} h={h} L={int(lens0[b]) + 1} split={st}")
         res, tv, kc, vc, ks = _cell_check(wl, kv, q, b, h, layer)
         assert S.rel_err(out[b, h], res["out"][0]) <= 2e-3
         assert abs(raw[b, h] - res["raw"][0]) <= 2e-3 * res["raw"][0]
         assert meter[b, h] >= tv[0]
         # the Tier-B certificate of the same cell (Sec. 4.2)
         rb = tierb.tierb_decode(q[b, h:h + 1].float().cpu().numpy().astype(np.float64), res["khat"][:, None],
-                                res["vhat"][:, None], ks[:, None], 1 / np.sqrt(wl.d), dloc)
+                                res["vhat"][:, None], ks[:, None], sm, dloc)
         assert abs(raw_b[b, h] - rb["raw"][0]) <= 2e-3 * rb["raw"][0]
         assert meter_b[b, h] >= tv[0]
-        # codes of sampled tokens of this cell, bit-exact
+        # codes of sampled tokens of this cell (the step's token among them), bit-exact
         sl = kv[b][2]
-        pick = rng.choice(len(sl), 512, replace=False)
+        pick = np.unique(np.concatenate([rng.choice(len(sl), min(512, len(sl)), replace=False), [len(sl) - 1]]))
         got = S.read_cache(cache, sl[pick])
         g = h // wl.group
         assert np.array_equal(got["k"][:, g].astype(np.int64), kc[pick])
         assert np.array_equal(got["v"][:, g].astype(np.int64), vc[pick])
         assert np.array_equal(got["ks"][:, g], ks[pick])
+        # the exact copy holds the bf16 inputs
+        gx = S.read_cache(exact, sl[pick])
+        kin = kv[b][0][:, g].float().cpu().numpy()[pick]
+        assert np.array_equal(S.bf16_bits_to_f32(gx["k"][:, g]), kin)
 
 
 def test_matrix_core_and_vector_paths_agree():

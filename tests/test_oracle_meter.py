@@ -2,7 +2,8 @@
 
 * the Sec. 3 counterexample: TV and Eq. (flawed) values printed in the paper;
 * Theorem (sound replacement) checked adversarially on >= 500,000 random cells
-  (extreme sign patterns, peaked and flat distributions, large c), with the
+  (Sec. 3 adversarial suite: residual signs all one way or alternating, softmax
+  mass on one token or spread evenly, bounds up to several units), with the
   sign convention p_t = ptilde_t e^{-eps_t} / Z of the machine-checked statement;
 * closed forms: constant c gives (e^{2c} - 1)/2; A >= 1;
 * 50-digit mpmath evaluation of the same definition on tiny cells;
