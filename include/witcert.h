@@ -41,7 +41,9 @@
  *     thread-safe.
  *   - Pointers must be 16-byte aligned; shapes are row-major, innermost last.
  *   - Preconditions not checked on the device: finite inputs, |x| <= 8.28e6
- *     (keeps fp16 scales finite), |x| <= 448 for the fp8 cache, |q| < 65504,
+ *     (keeps fp16 scales finite; the decode handles every fp16 value scale and
+ *     every finite bf16 value of the exact cache), |x| <= 448 for the fp8 cache,
+ *     |q| < 65504,
  *     block-table entries < num_blocks, slots < num_blocks * 16, every
  *     seq_lens[b] <= max_seq_len and <= max_blocks_per_seq * 16, outlier pair
  *     lists ascending and distinct (out-of-range pair indices are clamped, so a

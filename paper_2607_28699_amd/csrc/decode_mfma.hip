@@ -52,8 +52,10 @@ constexpr int kRow = 272;  // LDS bytes per token row of the dither transpose (2
 // The running max is raised only when a page exceeds it by more than kSlack, so
 // softmax weights stay below e^2.  Weights enter the fp16 PV operand multiplied
 // by 2^8 (cancelled by the same factor in the weight sum), which keeps small
-// weights out of the fp16 subnormal range; the product stays below 65504 for
-// value scales up to 34.
+// weights out of the fp16 subnormal range.  The INT8 operand p s^v 2^8 also
+// carries 2^-ve, ve a running value exponent (0 at the start, raised to cover a
+// page's largest value scale, with the accumulators rescaled by the exact power
+// of two), so it stays below e^2 2^8 < 65504 for any fp16 value scale.
 constexpr float kSlack = 2.0f;
 constexpr float kDOff = 2303.0f;   // 2048 + 255: D = 2u + 2048 = 512 xi + 2303
 constexpr float kCOff = 1152.0f;   // 1024 + 128: value operand 1024 + u = code + 1152
@@ -99,6 +101,14 @@ __device__ __forceinline__ uint32_t e4m3x2(uint32_t w) {
 __device__ __forceinline__ uint32_t bf16pair_to_f16(uint32_t w) {
   const float a = bf16_to_f32((uint16_t)(w & 0xFFFFu));
   const float b = bf16_to_f32((uint16_t)(w >> 16));
+  return as_u32(h2_t{(_Float16)a, (_Float16)b});
+}
+
+// The same times 2^k (k <= 0, a power of two in f32): exact unless the result
+// leaves the fp16 normal range.
+__device__ __forceinline__ uint32_t bf16pair_to_f16_scaled(uint32_t w, float two_k) {
+  const float a = bf16_to_f32((uint16_t)(w & 0xFFFFu)) * two_k;
+  const float b = bf16_to_f32((uint16_t)(w >> 16)) * two_k;
   return as_u32(h2_t{(_Float16)a, (_Float16)b});
 }
 
@@ -214,6 +224,8 @@ __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool val
 struct WaveState {
   f4_t o1[8], o2[8];
   float m, l, n, wsum;   // running max (log2 units), sum of weights, meter numerator, sum of fp16 weights
+  int ve;                // INT8 value exponent (wave-uniform, scalar): PV weights carry 2^-ve, and 2^ve
+                         // bounds the value scales seen so far
   float ev, vmax;        // value side: sum of weights x stored ||vhat - v||, largest stored ||v||
   f4_t wsg;              // group scales: sum of fp16 weights x 2^-e_g per group (rows 0..3)
 };
@@ -481,6 +493,37 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       st.o2[j] *= alpha;
     }
   }
+  if constexpr (KIND == WC_KIND_INT8_DITHER) {
+    // a value scale above 2^ve raises ve to cover the page (rare: value scales of a
+    // sequence vary little); the accumulated weights are rescaled by 2^(ve - ve')
+    // (tokens past the end may hold any stale scale: left out)
+    uint32_t vsx = cur.vs.x, vsy = cur.vs.y;
+    if constexpr (!FULL) {
+      const int tq = t_end - (t0 + 4 * g);   // valid tokens among 4g .. 4g+3
+      vsx &= tq >= 2 ? 0xFFFFFFFFu : (tq == 1 ? 0x0000FFFFu : 0u);
+      vsy &= tq >= 4 ? 0xFFFFFFFFu : (tq == 3 ? 0x0000FFFFu : 0u);
+    }
+    const h2_t pm2 = __builtin_elementwise_max(as_h2(vsx), as_h2(vsy));
+    const float pmax = fmaxf((float)pm2[0], (float)pm2[1]);
+    if (__ballot(pmax > __builtin_bit_cast(float, (uint32_t)(127 + st.ve) << 23)) != 0) {
+      const float wmax = xor_max(xor_max(xor_max(xor_max(xor_max(xor_max(pmax, 1), 2), 4), 8), 16), 32);
+      int e2;
+      (void)frexpf(wmax, &e2);                    // wmax < 2^e2 (e2 <= 16 for fp16 scales)
+      const int ve_new = __builtin_amdgcn_readfirstlane(max(st.ve, e2));
+      const float alpha = __builtin_bit_cast(float, (uint32_t)(127 + st.ve - ve_new) << 23);   // 2^(ve - ve')
+      st.ve = ve_new;
+      st.wsum *= alpha;
+      if constexpr (GS) st.wsg *= alpha;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        st.o1[j] *= alpha;
+        st.o2[j] *= alpha;
+      }
+    }
+  }
+  // 2^-ve as fp16 bits in both halves (normal up to ve = 14, subnormal above; exact)
+  const uint32_t vmul_h = st.ve <= 14 ? (uint32_t)(15 - st.ve) << 10 : 1u << (24 - st.ve);
+  const h2_t vmul = as_h2(vmul_h * 0x00010001u);
   const float mo = st.m - kWExp;
   _Float16 wh[NT];
 #pragma unroll
@@ -503,7 +546,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       st.n += valid[e] ? term : 0.0f;
     }
     float w = p;
-    if constexpr (KIND == WC_KIND_INT8_DITHER) w = fmaf((float)vsh[e >> 1][e & 1], p, 0.0f);
+    if constexpr (KIND == WC_KIND_INT8_DITHER) w = fmaf((float)(vsh[e >> 1] * vmul)[e & 1], p, 0.0f);
     wh[e] = valid[e] ? (_Float16)w : (_Float16)0.0f;
   }
   const h2_t one = h2_t{(_Float16)1.0f, (_Float16)1.0f};
@@ -588,16 +631,44 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(lo, hi), wop, st.o1[jt], 0, 0, 0);
     }
   } else {
+    // bf16 values enter PV as fp16 times 2^-ve: a value above 2^(15 + ve) raises ve
+    // (rare), with the output accumulators rescaled by the exact power of two
+    // (tokens past the end may hold any bytes: they are zeroed first)
+    uint32_t vw[16];
+    {
+      const int tq = FULL ? 4 : t_end - (t0 + 4 * g);   // valid tokens among 4g .. 4g+3
+      const uint32_t m01 = tq >= 2 ? 0xFFFFFFFFu : (tq == 1 ? 0x0000FFFFu : 0u);
+      const uint32_t m23 = tq >= 4 ? 0xFFFFFFFFu : (tq == 3 ? 0x0000FFFFu : 0u);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) vw[i] = cur.vw[i] & ((i & 1) ? m23 : m01);
+    }
+    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+    u16x2 am = u16x2{0, 0};
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, vw[i] & 0x7FFF7FFFu));
+    const float pmax = __builtin_bit_cast(float, (uint32_t)max(am[0], am[1]) << 16);
+    if (__ballot(pmax > __builtin_bit_cast(float, (uint32_t)(142 + st.ve) << 23)) != 0) {
+      const float wmax = xor_max(xor_max(xor_max(xor_max(xor_max(xor_max(pmax, 1), 2), 4), 8), 16), 32);
+      int e2;
+      (void)frexpf(wmax, &e2);                    // wmax < 2^e2
+      const int ve_new = __builtin_amdgcn_readfirstlane(max(st.ve, e2 - 15));
+      const float alpha = __builtin_bit_cast(float, (uint32_t)(127 + st.ve - ve_new) << 23);
+      st.ve = ve_new;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) st.o1[j] *= alpha;
+    }
+    const float vsc = __builtin_bit_cast(float, (uint32_t)(127 - st.ve) << 23);   // 2^-ve
 #pragma unroll
     for (int jt = 0; jt < 8; ++jt) {
       // bf16 values of channel 8r+jt, tokens 4g..4g+3: 8 bytes at offset 8*jt
-      uint32_t lo = bf16pair_to_f16(cur.vw[2 * jt]);
-      uint32_t hi = bf16pair_to_f16(cur.vw[2 * jt + 1]);
-      if constexpr (!FULL) {
-        if (!vtok[0]) lo &= 0xFFFF0000u;
-        if (!vtok[1]) lo &= 0x0000FFFFu;
-        if (!vtok[2]) hi &= 0xFFFF0000u;
-        if (!vtok[3]) hi &= 0x0000FFFFu;
+      uint32_t lo, hi;
+      if (st.ve == 0) {
+        lo = bf16pair_to_f16(vw[2 * jt]);
+        hi = bf16pair_to_f16(vw[2 * jt + 1]);
+      } else {
+        lo = bf16pair_to_f16_scaled(vw[2 * jt], vsc);
+        hi = bf16pair_to_f16_scaled(vw[2 * jt + 1], vsc);
       }
       st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(lo, hi), wop, st.o1[jt], 0, 0, 0);
     }
@@ -629,7 +700,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
   __shared__ float qn_s[kWaves][16][16];
   __shared__ __attribute__((aligned(16))) float acc_s[kWaves][16][kD];
-  __shared__ float ml_s[kWaves][16][5];
+  __shared__ float ml_s[kWaves][16][6];
   __shared__ uint4 q_lds[16][17];   // the workgroup's queries, bf16 rows of 256 bytes (+16 pad)
   // group scales: the fp16 B operands of the query products (4), the dither offset
   // (1), the Tier-B group norms (2), the witness bound (1) and the bypassed pairs (2),
@@ -942,6 +1013,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   }
   st.m = -INFINITY;
   st.l = st.n = st.wsum = 0.0f;
+  st.ve = 0;
   st.wsg = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
   st.ev = st.vmax = 0.0f;
   uint8_t* my_dsh = dsh[KIND == WC_KIND_INT8_DITHER ? wave : 0];
@@ -1038,6 +1110,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     ml_s[wave][r][2] = st.n;
     ml_s[wave][r][3] = st.ev;
     ml_s[wave][r][4] = st.vmax;
+    ml_s[wave][r][5] = (float)st.ve;
   }
   __syncthreads();
   const int64_t R = (int64_t)partial_record_floats(kD);
@@ -1060,6 +1133,11 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       }
     }
     if (isnan(nsum)) nsum = INFINITY;
+    // the output accumulators also carry each wave's 2^-ve (INT8 and bf16 values)
+    float fo[kWaves];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w)
+      fo[w] = KIND != WC_KIND_FP8_RAW ? f[w] * exp2_fast(ml_s[w][r][5]) : f[w];
     float* rec = a.part + (((int64_t)b * a.n_q + (int64_t)kv * G + r) * a.n_splits + split) * R;
 #pragma unroll
     for (int i = 0; i < 32; i += 4) {
@@ -1067,10 +1145,10 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
         const float4 x = *reinterpret_cast<const float4*>(&acc_s[w][r][32 * g + i]);
-        sum.x = fmaf(f[w], x.x, sum.x);
-        sum.y = fmaf(f[w], x.y, sum.y);
-        sum.z = fmaf(f[w], x.z, sum.z);
-        sum.w = fmaf(f[w], x.w, sum.w);
+        sum.x = fmaf(fo[w], x.x, sum.x);
+        sum.y = fmaf(fo[w], x.y, sum.y);
+        sum.z = fmaf(fo[w], x.z, sum.z);
+        sum.w = fmaf(fo[w], x.w, sum.w);
       }
       *reinterpret_cast<float4*>(rec + 32 * g + i) = sum;
     }
