@@ -10,11 +10,11 @@ certificate is recomputed, until it falls back to the threshold (Sec. 6.3).
 
 Definitions followed, with our readings where the paper leaves a choice:
 
-* Blocks: consecutive token ranges (the caller's partition; the paper uses
-  256-token blocks at S = 32768).  ``split_blocks`` is the partition the decode
-  records: each KV split of ``split_tokens`` tokens is divided into four
-  page-aligned parts of ceil(pages / 4) pages, the last parts taking what is
-  left (possibly nothing) -- quarters of the split for a full split.
+* Blocks: fixed runs of BLOCK_TOKENS = 256 consecutive tokens of the sequence,
+  block j holding positions 256j .. 256j + 255 (the last one shorter): Sec. 6.3
+  divides S = 32768 into n_b = 128 blocks (``paper_blocks``).  The definitions
+  below take any partition into consecutive ranges (``block_ranges``), so the
+  pins can use small blocks on small cases.
 * Order: for a KV head with G query heads, blocks are ranked by the sum over the
   G heads of their shares, largest first, ties to the lower block index (the
   exact values of a block serve every query head of its KV head).
@@ -43,17 +43,12 @@ def block_ranges(seq_len: int, block_tokens: int) -> list:
     return [(t, min(t + block_tokens, seq_len)) for t in range(0, seq_len, block_tokens)]
 
 
-def split_blocks(seq_len: int, split_tokens: int, page: int = 16) -> list:
-    """[(t0, t1)] * (4 per split): the four page-aligned parts of every split."""
-    out = []
-    for s0 in range(0, seq_len, split_tokens):
-        s1 = min(s0 + split_tokens, seq_len)
-        per = -(-max(s1 - s0, 0) // page)          # pages of the split
-        ppw = -(-per // 4) * page                  # tokens per part
-        for w in range(4):
-            b0 = min(s0 + w * ppw, s1)
-            out.append((b0, min(b0 + ppw, s1)))
-    return out
+BLOCK_TOKENS = 256
+
+
+def paper_blocks(seq_len: int) -> list:
+    """The repair blocks of a sequence: consecutive 256-token runs (Sec. 6.3)."""
+    return block_ranges(seq_len, BLOCK_TOKENS)
 
 
 def block_shares(ptilde: np.ndarray, c: np.ndarray, ranges: list) -> np.ndarray:

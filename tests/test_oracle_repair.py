@@ -84,24 +84,18 @@ def test_order_and_minimal_stop():
     assert res["n_blocks"] == -1
 
 
-def test_split_blocks_partition():
-    """The decode's blocks: four page-aligned parts per split, covering [0, S) once;
-    quarters of a full split; a last split divided as evenly as pages allow."""
-    for S, st in ((300, 256), (4106, 256), (32770, 1088), (600, 3904), (1, 256), (16, 64), (33, 64)):
-        bl = orep.split_blocks(S, st)
-        assert len(bl) == 4 * (-(-S // st))
+def test_paper_blocks():
+    """Sec. 6.3's blocks: S = 32768 tokens give n_b = 128 blocks of 256 tokens; any
+    length is covered once by consecutive blocks, only the last one shorter, and
+    the partition depends on nothing but the sequence length."""
+    bl = orep.paper_blocks(32768)
+    assert len(bl) == 128 and all(t1 - t0 == 256 for t0, t1 in bl)
+    for S in (1, 255, 256, 257, 300, 4106, 32770, 131073):
+        bl = orep.paper_blocks(S)
+        assert len(bl) == -(-S // 256)
         covered = np.zeros(S, dtype=int)
-        prev = 0
-        for t0, t1 in bl:
-            assert t0 == prev and t0 <= t1          # in order, contiguous, possibly empty
+        for j, (t0, t1) in enumerate(bl):
+            assert t0 == 256 * j and 0 < t1 - t0 <= 256
             covered[t0:t1] += 1
-            prev = t1
-            if t1 > t0:
-                assert t0 % 16 == 0                 # page-aligned starts
-        assert prev == S and np.all(covered == 1)
-        for j in range(S // st):                    # full splits: exact quarters
-            assert bl[4 * j:4 * j + 4] == [(j * st + w * st // 4, j * st + (w + 1) * st // 4) for w in range(4)]
-    # a 600-token sequence in one 3904-token split: 38 pages -> 10, 10, 10, 8 pages
-    assert [t1 - t0 for t0, t1 in orep.split_blocks(600, 3904)] == [160, 160, 160, 120]
-    # a single page: the first part takes it
-    assert [t1 - t0 for t0, t1 in orep.split_blocks(10, 256)] == [10, 0, 0, 0]
+        assert np.all(covered == 1) and bl[-1][1] == S
+        assert all(t1 - t0 == 256 for t0, t1 in bl[:-1])
