@@ -578,13 +578,13 @@ def main():
                         "gate_fraction_kv_heads": round(gkvj / (n_cells * wl.n_kv), 4)}
 
         # block-granular repair (Sec. 6.3) of the KV heads the Tier-A gate routes over
-        # the same caches: blocks are quarters of the decode's splits, paged in from
+        # the same caches: fixed 256-token blocks, paged in from
         # the exact bf16 cache in decreasing order of their meter shares until every
         # query head passes tau, at most REPAIR_BUDGET blocks per KV head.  Timed as
         # (metered decode + gate + repair) minus the metered decode + gate alone.
         nrep = torch.empty((lay.batch, wl.n_kv), dtype=torch.int32, device=dev)
         rlist = torch.empty((lay.batch, wl.n_kv, REPAIR_BUDGET), dtype=torch.int32, device=dev)
-        rws = wc.repair_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all, REPAIR_BUDGET, ST)
+        rws = wc.repair_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, REPAIR_BUDGET)
 
         def dec_rep(i):
             layer = i % wl.n_layers
@@ -602,7 +602,7 @@ def main():
         nr = torch.cat(nreps).flatten().cpu().numpy()
         routed_r = nr != 0
         fixed = nr > 0
-        bs = ST // 4
+        bs = 256   # repair blocks: fixed 256-token runs
         rep_ms = max(float(np.median(dr_ms)) - float(np.median(ba_ms)), 0.0)
         del rws
         whole = float(np.mean(last["lens"].cpu().numpy())) * BF16_BYTES

@@ -237,9 +237,10 @@ int wc_witness(const void* x, int x_dtype, const void* xhat, int xhat_dtype, int
 /*
  * Workspace bytes needed by wc_metered_decode_attention / wc_exact_decode_attention
  * for these sizes.  split_tokens as passed to the decode call (0 = library choice).
- * The workspace holds the per-split partial records and, for the fused gate,
- * one int32 per (sequence, KV head); it needs no initialization.  Calls that
- * share a workspace must not run concurrently.
+ * The workspace holds the per-split partial records, for the fused gate one int32
+ * per (sequence, KV head), and the meter numerators of the block segments that
+ * wc_block_repair reads; it needs no initialization.  Calls that share a
+ * workspace must not run concurrently.
  */
 size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
                                 int64_t max_seq_len, int split_tokens);
@@ -247,8 +248,8 @@ size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int he
 /*
  * Tokens per KV split that the decode calls use for these sizes: split_tokens
  * rounded up to a multiple of 64, or, for 0, the library's choice (about 512
- * workgroups over the batch's KV heads, at least 256 tokens).  wc_block_repair's
- * blocks are quarters of it.  With total_tokens > 0 (the sum of the batch's
+ * workgroups over the batch's KV heads, at least 256 tokens).  With
+ * total_tokens > 0 (the sum of the batch's
  * sequence lengths, known to the caller on the host) and split_tokens = 0 the
  * choice balances the workgroups over the total instead of the longest
  * sequence: pass the result as split_tokens to the decode calls and
@@ -399,12 +400,11 @@ int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int 
  * decode call (Tier A, or Tier B with delta_loc > 0) over the same cache, queries,
  * table, lengths and split_tokens, whose workspace `ws` still holds its partial
  * records, and whose gate set mask_kv.  For every KV head with mask_kv != 0:
- *   blocks are the decode waves' parts of the KV splits: block i is part i%4 of
- *   split i/4, the split's 16-token pages divided into four runs of
- *   ceil(pages/4) pages (quarters, split_tokens/4 tokens each, for a full split;
- *   the last runs of a sequence's last split are shorter or empty), split_tokens
- *   as chosen for the decode (0 selects the library's choice for the same sizes);
+ *   blocks are fixed runs of 256 tokens of the sequence (Sec. 6.3: S = 32768 in 128
+ *   blocks), block i holding positions 256i .. 256i+255 (the last one shorter),
+ *   whatever split_tokens the decode used;
  *   share_{h,i} = sum_{t in i} ptilde_{h,t} (e^{c_{h,t}} - 1) (they add up to A_h - 1),
+ *   from the block segments the decode recorded in its workspace,
  *   taken in decreasing order of sum_h share_{h,i} (ties to the lower i), at most
  *   max_repair_blocks (1 .. 64) of them;
  *   a taken block contributes exact logits and values (from the bf16 cache `exact`)
@@ -414,8 +414,8 @@ int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int 
  * state and its mask_kv cleared (no whole-head fallback needed); otherwise nothing
  * of it changes.  repaired[b][g][0..max_repair_blocks-1] receives the block order
  * (-1 padded; may be NULL) and n_repaired[b][g] the number of blocks taken (0: not
- * routed, -1: the budget did not suffice; may be NULL).  At most 4096 blocks (1024
- * splits) per sequence.  out must be the decode's output array (out_dtype as there).
+ * routed, -1: the budget did not suffice; may be NULL).  At most 4096 blocks
+ * (1,048,576 tokens) per sequence.  out must be the decode's output array (out_dtype as there).
  * repair_ws (repair_ws_bytes >= wc_block_repair_workspace_size for the same sizes,
  * caller-owned device memory, no initialization needed) holds the per-KV-head
  * state and the block corrections; the blocks' corrections are computed in
@@ -431,11 +431,11 @@ int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q,
                     size_t repair_ws_bytes, void* stream);
 
 /*
- * Bytes of the repair workspace of wc_block_repair for these sizes (split_tokens
- * as passed to the decode call, 0 = library choice); 0 for invalid sizes.
+ * Bytes of the repair workspace of wc_block_repair for these sizes; 0 for invalid
+ * sizes.
  */
 size_t wc_block_repair_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
-                                      int64_t max_seq_len, int split_tokens, int max_repair_blocks);
+                                      int max_repair_blocks);
 
 /*
  * Gate (the meter loop's gate, Sec. 6; certified vs risk-ranked, Sec. 4.3):

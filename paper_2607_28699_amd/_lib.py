@@ -105,7 +105,7 @@ def lib() -> ctypes.CDLL:
                                            ctypes.c_int, vp, sz, vp, ctypes.c_int, vp, vp, vp, vp, vp,
                                            vp, sz, vp]),
         "wc_block_repair_workspace_size": (sz, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-                                                i64, ctypes.c_int, ctypes.c_int]),
+                                                ctypes.c_int]),
         "wc_gate": (ctypes.c_int, [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, f32, vp, vp,
                                    vp, vp]),
         "wc_exact_decode_attention": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int,

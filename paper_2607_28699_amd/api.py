@@ -346,14 +346,14 @@ def block_repair(cache: PagedCache, exact: PagedCache, q: torch.Tensor, block_ta
                  delta_loc: float = 0.0, max_blocks: int = 16, split_tokens: int = 0,
                  repaired: torch.Tensor | None = None, n_repaired: torch.Tensor | None = None,
                  repair_ws: torch.Tensor | None = None):
-    """Block repair of the KV heads a metered decode (same ws, split_tokens) routed:
+    """Block repair (fixed 256-token blocks) of the KV heads a metered decode (same ws,
+    split_tokens) routed:
     updates out, meter, raw and mask_kv in place -> (n_repaired [batch, n_kv],
     repaired [batch, n_kv, max_blocks])."""
     _dev_check(q, block_table, seq_lens, ws, out, meter, raw, mask_kv)
     batch, n_q, d = q.shape
     if repair_ws is None:
-        repair_ws = repair_workspace(batch, n_q, cache.n_kv, d, max_seq_len, max_blocks, split_tokens,
-                                     device=q.device)
+        repair_ws = repair_workspace(batch, n_q, cache.n_kv, d, max_blocks, device=q.device)
     if n_repaired is None:
         n_repaired = torch.empty((batch, cache.n_kv), dtype=torch.int32, device=q.device)
     if repaired is None:
@@ -369,11 +369,10 @@ def block_repair(cache: PagedCache, exact: PagedCache, q: torch.Tensor, block_ta
     return n_repaired, repaired
 
 
-def repair_workspace(batch: int, n_q: int, n_kv: int, head_dim: int, max_seq_len: int,
-                     max_blocks: int = 16, split_tokens: int = 0, device="cuda") -> torch.Tensor:
+def repair_workspace(batch: int, n_q: int, n_kv: int, head_dim: int, max_blocks: int = 16,
+                     device="cuda") -> torch.Tensor:
     """Device workspace of block_repair for these sizes."""
-    n = lib().wc_block_repair_workspace_size(batch, n_q, n_kv, head_dim, max_seq_len, split_tokens,
-                                             max_blocks)
+    n = lib().wc_block_repair_workspace_size(batch, n_q, n_kv, head_dim, max_blocks)
     if n == 0:
         raise _lib.WitCertError("bad repair workspace geometry")
     return torch.empty(n, dtype=torch.uint8, device=device)

@@ -234,7 +234,8 @@ size_t wc_decode_workspace_size(int batch, int n_q_heads, int n_kv_heads, int he
     return 0;
   const int st = wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens);
   const int64_t ns = wc::n_splits_for(max_seq_len, st);
-  return wc::records_bytes(batch, n_q_heads, ns, head_dim) + wc::gate_unit_bytes(batch, n_kv_heads);
+  return wc::records_bytes(batch, n_q_heads, ns, head_dim) + wc::gate_unit_bytes(batch, n_kv_heads) +
+         wc::share_bytes(batch, n_q_heads, ns, st);
 }
 
 int wc_decode_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int64_t total_tokens,
@@ -279,6 +280,10 @@ static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int 
   a.part = static_cast<float*>(ws);
   a.gate_unit = reinterpret_cast<int32_t*>(static_cast<char*>(ws) +
                                            wc::records_bytes(batch, n_q_heads, ns, cache->head_dim));
+  a.shares = reinterpret_cast<float4*>(static_cast<char*>(ws) +
+                                       wc::records_bytes(batch, n_q_heads, ns, cache->head_dim) +
+                                       wc::gate_unit_bytes(batch, cache->n_kv_heads));
+  a.share_slots = wc::share_slots(st);
   a.out = out;
   a.kind = cache->kind;
   a.head_dim = cache->head_dim;
@@ -506,12 +511,12 @@ int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q,
                     seq_lens, max_seq_len, sm_scale, out, out_dtype, split_tokens,
                     const_cast<void*>(ws), ws_bytes, a);   // the records are only read
   if (s != WC_OK) return s;
-  if (4 * (int64_t)a.n_splits > wc::repair_max_blocks()) return WC_EUNSUPPORTED;   // 4 blocks per split
+  if ((max_seq_len + wc::kRepairBlockTokens - 1) / wc::kRepairBlockTokens > wc::repair_max_blocks())
+    return WC_EUNSUPPORTED;
   if (batch == 0) return WC_OK;
   if (!repair_ws || reinterpret_cast<uintptr_t>(repair_ws) % 256) return WC_EINVAL;
   if (repair_ws_bytes < wc_block_repair_workspace_size(batch, n_q_heads, cache->n_kv_heads,
-                                                       cache->head_dim, max_seq_len, split_tokens,
-                                                       max_repair_blocks))
+                                                       cache->head_dim, max_repair_blocks))
     return WC_EWORKSPACE;
   a.meter = meter;
   a.raw = raw;
@@ -532,19 +537,18 @@ int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q,
   // (default: the predicted count plus one); the result does not depend on it
   const char* r0 = getenv("WITCERT_REPAIR_ROUND0");
   r.round0_cap = r0 != nullptr ? atoi(r0) : 0;
-  r.tiles = wc::repair_tiles(a.split_tokens);
+  r.tiles = wc::kRepairTiles;
   r.unit_bytes = wc::repair_unit_bytes(a.group, a.head_dim, max_repair_blocks, r.tiles);
   return hip_status(wc::launch_repair(r, static_cast<hipStream_t>(stream)));
 }
 
 size_t wc_block_repair_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
-                                      int64_t max_seq_len, int split_tokens, int max_repair_blocks) {
+                                      int max_repair_blocks) {
   if (batch < 0 || n_kv_heads < 1 || n_q_heads < 1 || n_q_heads % n_kv_heads || head_dim < 1 ||
-      max_seq_len < 0 || split_tokens < 0 || max_repair_blocks < 1 || max_repair_blocks > 64)
+      max_repair_blocks < 1 || max_repair_blocks > 64)
     return 0;
-  const int st = wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens);
   const size_t unit = wc::repair_unit_bytes(n_q_heads / n_kv_heads, head_dim, max_repair_blocks,
-                                            wc::repair_tiles(st));
+                                            wc::kRepairTiles);
   const size_t total = (size_t)batch * n_kv_heads * unit;
   return total > 0 ? total : 256;
 }

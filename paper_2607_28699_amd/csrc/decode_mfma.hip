@@ -224,6 +224,7 @@ __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool val
 struct WaveState {
   f4_t o1[8], o2[8];
   float m, l, n, wsum;   // running max (log2 units), sum of weights, meter numerator, sum of fp16 weights
+  float nb;              // meter numerator of the current block segment (block repair's shares)
   int ve;                // INT8 value exponent (wave-uniform, scalar): PV weights carry 2^-ve, and 2^ve
                          // bounds the value scales seen so far
   float ev, vmax;        // value side: sum of weights x stored ||vhat - v||, largest stored ||v||
@@ -484,6 +485,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     st.m = m_new;
     st.l *= alpha;
     st.n *= alpha;
+    st.nb *= alpha;
     st.wsum *= alpha;
     if constexpr (GS) st.wsg *= alpha;
     if constexpr (VM) st.ev *= alpha;
@@ -542,8 +544,9 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       const float c = cbv[e];
       const float small = p * exp2m1_small(__builtin_amdgcn_fmed3f(c, 0.0f, kTaylorMax));
       const float big = exp2_fast(x + c) - p;
-      const float term = c > kTaylorMax ? big : small;
-      st.n += valid[e] ? term : 0.0f;
+      const float term = valid[e] ? (c > kTaylorMax ? big : small) : 0.0f;
+      st.n += term;
+      st.nb += term;
     }
     float w = p;
     if constexpr (KIND == WC_KIND_INT8_DITHER) w = fmaf((float)(vsh[e >> 1] * vmul)[e & 1], p, 0.0f);
@@ -675,6 +678,29 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   }
 }
 
+// Block segments (block repair's shares, Sec. 6.3): the wave's pages split at the
+// 256-token repair blocks.  A segment's numerator (summed over the lanes of each
+// head) goes with its frame, first page and length into the next of the wave's
+// share slots; every slot the wave owns is written (unused ones with 0 pages).
+struct Segment {
+  int first;   // first page of the open segment
+  int slot;    // next share slot of this wave
+};
+template <bool HALF>
+__device__ __forceinline__ void flush_segment(const DecodeArgs& a, WaveState& st, Segment& sg, int last_page,
+                                              float4* my_slots, int r, int g) {
+  float t = st.nb;
+  if constexpr (HALF) t += __shfl_xor(t, 8, 64);   // lanes r and r + 8 hold tokens of head r
+  t += __shfl_xor(t, 16, 64);
+  t += __shfl_xor(t, 32, 64);
+  if (g == 0 && r < a.group && sg.slot < a.share_slots / kWaves)
+    my_slots[sg.slot] = make_float4(t, (st.m - kWExp) * kLn2, __builtin_bit_cast(float, sg.first),
+                                    __builtin_bit_cast(float, last_page - sg.first));
+  ++sg.slot;
+  sg.first = last_page;
+  st.nb = 0.0f;
+}
+
 // The new token of sequence b, KV head kv (the step's token of that sequence, by
 // the workgroup that reads it): lanes 0 .. kD/16 - 1 of wave 0 quantize and store
 // it as the write kernel does (write_dev.h), then the witness bands; the barrier
@@ -751,9 +777,8 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   }
   const int wg_end = min(min(L, wg_begin + a.split_tokens), a.max_blocks * kBlockTokens);
   // this wave's share: a quarter of the workgroup's pages (rounded up; a full
-  // split gives split_tokens / 4 tokens), the blocks whose meter shares the record
-  // carries (block repair); a sequence's last split is divided the same way, so
-  // that all four waves share a short sequence
+  // split gives split_tokens / 4 tokens); a sequence's last split is divided the
+  // same way, so that all four waves share a short sequence
   const int ppw = ((wg_end - wg_begin + kBlockTokens - 1) / kBlockTokens + kWaves - 1) / kWaves;
   const int t_begin = min(wg_begin + wave * ppw * kBlockTokens, wg_end);
   const int t_end = min(wg_end, t_begin + ppw * kBlockTokens);
@@ -1012,7 +1037,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     st.o2[j] = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
   }
   st.m = -INFINITY;
-  st.l = st.n = st.wsum = 0.0f;
+  st.l = st.n = st.wsum = st.nb = 0.0f;
   st.ve = 0;
   st.wsg = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
   st.ev = st.vmax = 0.0f;
@@ -1029,6 +1054,17 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     else if (left4 > np) __builtin_amdgcn_s_setprio(1);
     else __builtin_amdgcn_s_setprio(0);
   };
+  // block segments: a page that starts a 256-token repair block closes the open
+  // segment (wave-uniform test)
+  const bool rec_shares = METER && a.shares != nullptr;
+  Segment sg{t_begin / kBlockTokens, 0};
+  float4* my_slots = rec_shares ? a.shares + (((int64_t)b * a.n_q + (int64_t)kv * G + (hv ? r : 0)) * a.n_splits +
+                                              split) * a.share_slots + wave * (a.share_slots / kWaves)
+                                : nullptr;
+  auto seg_check = [&](int t0) {
+    if (rec_shares && (t0 & (kRepairBlockTokens - 1)) == 0 && t0 / kBlockTokens > sg.first)
+      flush_segment<HALF>(a, st, sg, t0 / kBlockTokens, my_slots, r, g);
+  };
   for (int c0 = 0; c0 < np;) {
     const int tb = t_begin + c0 * kBlockTokens;
     // No early exit from this loop: a break lets the compiler's load counting
@@ -1037,15 +1073,20 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       set_priority(c0 + j);
       load_page<KIND, METER, TB, BYP, VM, GS>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
       __builtin_amdgcn_sched_barrier(0);
+      seg_check(tb + j * kBlockTokens);
       process_page<KIND, METER, true, HALF, TB, BYP, VM, GS>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
       load_page<KIND, METER, TB, BYP, VM, GS>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
       __builtin_amdgcn_sched_barrier(0);
-      if (j + 1 < nc)
+      if (j + 1 < nc) {
+        seg_check(tb + (j + 1) * kBlockTokens);
         process_page<KIND, METER, true, HALF, TB, BYP, VM, GS>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      }
       load_page<KIND, METER, TB, BYP, VM, GS>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
       __builtin_amdgcn_sched_barrier(0);
-      if (j + 2 < nc)
+      if (j + 2 < nc) {
+        seg_check(tb + (j + 2) * kBlockTokens);
         process_page<KIND, METER, true, HALF, TB, BYP, VM, GS>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      }
     }
     c0 += 64;
     if (c0 < np) start_chunk(c0);
@@ -1054,7 +1095,14 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   const int t_last = t_begin + np * kBlockTokens;
   if (t_last < t_end) {   // a partial last page: tokens from t_end on are masked
     load_page<KIND, METER, TB, BYP, VM, GS>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
+    seg_check(t_last);
     process_page<KIND, METER, false, HALF, TB, BYP, VM, GS>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
+  }
+  if (rec_shares) {
+    // the last segment, then the wave's unused slots (0 pages)
+    if (t_end > t_begin) flush_segment<HALF>(a, st, sg, (t_end + kBlockTokens - 1) / kBlockTokens, my_slots, r, g);
+    for (int sl = sg.slot; sl < a.share_slots / kWaves; ++sl)
+      if (g == 0 && r < G) my_slots[sl] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
   }
 
   // ---- merge the four waves of the workgroup, write one partial record ----
@@ -1158,9 +1206,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       rec[kD + 2] = nsum;
       rec[kD + 3] = esum;
       rec[kD + 4] = vmax;
-      // meter shares of the four blocks (one per wave), same units as nsum
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) rec[kD + 8 + w] = f[w] * ml_s[w][r][2];
+
     }
   }
 

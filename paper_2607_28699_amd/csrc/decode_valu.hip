@@ -133,18 +133,37 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
 
   const bool vm = METER && a.meter_v != nullptr;   // value side
   float m_run[4], l_run[4], n_run[4], e_run[4], vmax_run = 0.0f;
-  float nb_run[4][4];   // meter numerators of the split's four blocks (quarters), per head slot
+  float nb_run[4];   // meter numerator of the open block segment, per head slot
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     m_run[k] = -INFINITY;
     l_run[k] = 0.0f;
     n_run[k] = 0.0f;
     e_run[k] = 0.0f;
-#pragma unroll
-    for (int q4 = 0; q4 < 4; ++q4) nb_run[k][q4] = 0.0f;
+    nb_run[k] = 0.0f;
   }
-  // the split's four blocks: page-aligned quarters of its pages (rounded up)
-  const int blk_tokens = ((t_end - t_begin + kBlockTokens - 1) / kBlockTokens + 3) / 4 * kBlockTokens;
+  // Block segments (block repair's shares, Sec. 6.3): the split's tiles (64
+  // tokens, each inside one 256-token repair block) grouped by repair block; a
+  // segment's numerator, frame, first page and length go to the split's next
+  // share slot, and every slot of the split is written (unused ones with 0 pages).
+  const bool rec_shares = METER && a.shares != nullptr;
+  int seg_first = t_begin / kBlockTokens, seg_slot = 0;
+  auto flush_segment = [&](int last_page) {
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int h = wave + 4 * k;
+        if (h < G && seg_slot < a.share_slots)
+          a.shares[(((int64_t)b * a.n_q + (int64_t)kv * G + h) * a.n_splits + split) * a.share_slots + seg_slot] =
+              make_float4(nb_run[k], m_run[k], __builtin_bit_cast(float, seg_first),
+                          __builtin_bit_cast(float, last_page - seg_first));
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) nb_run[k] = 0.0f;
+    ++seg_slot;
+    seg_first = last_page;
+  };
   const int c3 = tid % D, hs = tid / D;
   float acc[HPT];
 #pragma unroll
@@ -152,6 +171,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   const uint32_t layer_head = ((uint32_t)a.layer << 16) | (uint32_t)kv;
 
   for (int t0 = t_begin; t0 < t_end; t0 += kT) {
+    if (rec_shares && (t0 & (kRepairBlockTokens - 1)) == 0 && t0 / kBlockTokens > seg_first)
+      flush_segment(t0 / kBlockTokens);
     __syncthreads();
     // ---------------- phase 1: logits and per-token bounds ----------------
     {
@@ -318,12 +339,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         if constexpr (METER) {
           const float nn = fmaf(alpha, n_run[k], wave_sum(term));
           n_run[k] = isnan(nn) ? INFINITY : nn;
-          const int qb = (t0 + lane - t_begin) / blk_tokens;   // this token's block in the split
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4) {
-            const float nbq = fmaf(alpha, nb_run[k][q4], wave_sum(qb == q4 ? term : 0.0f));
-            nb_run[k][q4] = isnan(nbq) ? INFINITY : nbq;
-          }
+          const float nbq = fmaf(alpha, nb_run[k], wave_sum(term));
+          nb_run[k] = isnan(nbq) ? INFINITY : nbq;
         }
         if (vm) {
           e_run[k] = fmaf(alpha, e_run[k], wave_sum(p * vr_s[lane]));
@@ -386,6 +403,19 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
     }
   }
 
+  if (rec_shares) {
+    flush_segment((t_end + kBlockTokens - 1) / kBlockTokens);
+    if (lane == 0) {
+      for (int sl = seg_slot; sl < a.share_slots; ++sl)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int h = wave + 4 * k;
+          if (h < G)
+            a.shares[(((int64_t)b * a.n_q + (int64_t)kv * G + h) * a.n_splits + split) * a.share_slots + sl] =
+                make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        }
+    }
+  }
   const int64_t R = (int64_t)partial_record_floats(D);
   const int64_t rec_base = ((int64_t)b * a.n_q + (int64_t)kv * G) * a.n_splits + split;
 #pragma unroll
@@ -404,8 +434,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         rec[D + 2] = n_run[k];
         rec[D + 3] = e_run[k];
         rec[D + 4] = vmax_run;
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) rec[D + 8 + q4] = nb_run[k][q4];
+
       }
     }
   }

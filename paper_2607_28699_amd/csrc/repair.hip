@@ -9,9 +9,10 @@
 //   rank   one workgroup per (sequence, KV head): the merged state of each query
 //          head (max M, weight sum L, meter numerator N) in float64 from the split
 //          records of the metered decode that routed it; the block totals (sum over
-//          the G heads of the block's share; a block is one decode wave's part of a
-//          split, whose numerator the records carry); the repair order (largest first, ties to
-//          the lower block) up to the budget; and a predicted block count, the
+//          the G heads of the block's share; a block is a fixed run of 256 tokens,
+//          its share the sum of the block segments the decode recorded); the repair
+//          order (largest first, ties to the lower block) up to the budget; and a
+//          predicted block count, the
 //          first prefix after which every head passes when only N moves (the
 //          exact logits usually move L very little);
 //   block  one workgroup per (candidate, 64-token tile, routed KV head) of a round:
@@ -82,19 +83,32 @@ __device__ __forceinline__ UnitGeom unit_geom(const DecodeArgs& a, int unit) {
   u.L = a.seq_lens[u.b];
   u.Lc = min(u.L, a.max_blocks * kBlockTokens);
   u.ns = min((u.Lc + a.split_tokens - 1) / a.split_tokens, a.n_splits);
-  u.nb = 4 * u.ns;
+  u.nb = (u.Lc + kRepairBlockTokens - 1) / kRepairBlockTokens;
   return u;
 }
 
-// Tokens [b0, b1) of block i: part i % 4 of split i / 4, the decode wave's range (a
-// quarter of the split's pages, rounded up; the last parts of a short split may be
-// empty).
-__device__ __forceinline__ void block_range(int i, int Lc, int split_tokens, int& b0, int& b1) {
-  const int s0 = (i >> 2) * split_tokens;
-  const int s1 = min(s0 + split_tokens, Lc);
-  const int ppw = ((s1 - s0 + kBlockTokens - 1) / kBlockTokens + 3) / 4 * kBlockTokens;
-  b0 = min(s0 + (i & 3) * ppw, s1);
-  b1 = min(b0 + ppw, s1);
+// Tokens [b0, b1) of block i: the fixed 256-token run (Sec. 6.3).
+__device__ __forceinline__ void block_range(int i, int Lc, int& b0, int& b1) {
+  b0 = min(i * kRepairBlockTokens, Lc);
+  b1 = min(b0 + kRepairBlockTokens, Lc);
+}
+
+// Share of block i for query head h (rows of G heads): the sum of the block's
+// segments e^{m - M_h} n over the splits that overlap it, in split and slot order.
+__device__ __forceinline__ double block_share(const DecodeArgs& a, const float4* sh_unit, int i, int h,
+                                              int ns, double M) {
+  const int j0 = i * kRepairBlockTokens / a.split_tokens;
+  const int j1 = min((i * kRepairBlockTokens + kRepairBlockTokens - 1) / a.split_tokens, ns - 1);
+  double t = 0.0;
+  for (int j = j0; j <= j1; ++j) {
+    const float4* e = sh_unit + ((int64_t)h * a.n_splits + j) * a.share_slots;
+    for (int sl = 0; sl < a.share_slots; ++sl) {
+      const float4 x = e[sl];
+      const int first = __builtin_bit_cast(int, x.z), pages = __builtin_bit_cast(int, x.w);
+      if (pages > 0 && first * kBlockTokens / kRepairBlockTokens == i) t += exp((double)x.y - M) * (double)x.x;
+    }
+  }
+  return t;
 }
 
 // ---------------------------------------------------------------------------
@@ -150,21 +164,11 @@ __global__ __launch_bounds__(kRThreads) void repair_rank_kernel(RepairArgs ra) {
     }
   }
   __syncthreads();
-  // block totals: sum over the heads of e^{m_j - M} n_{j,w} / L (the heads' loads
-  // issued together)
+  // block totals: sum over the heads of the block's share / L
+  const float4* sh_unit = a.shares + ((int64_t)u.b * a.n_q + (int64_t)u.kv * G) * a.n_splits * a.share_slots;
   for (int i = tid; i < u.nb; i += kRThreads) {
-    const int j = i >> 2, w = i & 3;
-    float mv[kRGMax], nv[kRGMax];
-#pragma unroll
-    for (int h = 0; h < kRGMax; ++h) {
-      const float* rc = recs + ((int64_t)(h < G ? h : 0) * a.n_splits + j) * R;
-      mv[h] = rc[D];
-      nv[h] = rc[D + 8 + w];
-    }
     double t = 0.0;
-#pragma unroll
-    for (int h = 0; h < kRGMax; ++h)
-      if (h < G) t += exp((double)mv[h] - M_s[h]) * nv[h] / L_s[h];
+    for (int h = 0; h < G; ++h) t += block_share(a, sh_unit, i, h, u.ns, M_s[h]) / L_s[h];
     T_s[i] = t;
   }
   __syncthreads();
@@ -211,9 +215,7 @@ __global__ __launch_bounds__(kRThreads) void repair_rank_kernel(RepairArgs ra) {
   // predicted count: per head, N minus the taken shares (L held fixed)
   for (int i = tid; i < G * K; i += kRThreads) {
     const int h = i / K, k = i % K;
-    const int blk = order_s[k];
-    const float* rc = recs + ((int64_t)h * a.n_splits + (blk >> 2)) * R;
-    sh_s[h][k] = (float)(exp((double)rc[D] - M_s[h]) * rc[D + 8 + (blk & 3)]);
+    sh_s[h][k] = (float)block_share(a, sh_unit, order_s[k], h, u.ns, M_s[h]);
   }
   __syncthreads();
   if (tid < G) {
@@ -285,7 +287,7 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
   const int B = a.n_bands;
   const int blk = hd->order[j];
   int b0, b1;
-  block_range(blk, u.Lc, a.split_tokens, b0, b1);
+  block_range(blk, u.Lc, b0, b1);
   const int t_lo = b0 + tile * kRTile;
   const int t_hi = min(t_lo + kRTile, b1);
   const int nv = max(t_hi - t_lo, 0);     // tokens of this tile
@@ -616,13 +618,17 @@ __global__ __launch_bounds__(kRThreads) void repair_scan_kernel(RepairArgs ra, i
     dN_s[jj][h] = dn;
   }
   __syncthreads();
+  // once every block of the sequence is taken no compressed token is left: the
+  // numerator is 0 by definition (the corrections would leave the rounding of
+  // the records' fp32 sums)
+  const int nb_all = unit_geom(a, unit).nb;
   if (tid < G) {
     double L = hd->L[tid], N = hd->N[tid];
     uint64_t bits = 0;
     for (int jj = 0; jj < n; ++jj) {
       L += dL_s[jj][tid];
       N += dN_s[jj][tid];
-      if (head_passes(L, N, ra.tau)) bits |= 1ull << jj;
+      if (head_passes(L, j_lo + jj + 1 >= nb_all ? 0.0 : N, ra.tau)) bits |= 1ull << jj;
     }
     pass_s[tid] = bits;
   }
@@ -660,6 +666,7 @@ __global__ __launch_bounds__(kRThreads) void repair_scan_kernel(RepairArgs ra, i
       L += dL_s[jj][tid];
       N += dN_s[jj][tid];
     }
+    if (done + 1 >= nb_all) N = 0.0;
     hd->L[tid] = L;
     hd->N[tid] = N;
     const double am1 = N / L;

@@ -62,7 +62,11 @@ struct DecodeArgs {
   int64_t num_blocks;       // blocks of the cache(s) read: a table entry outside [0, num_blocks)
                             // is read as a page of zeros (no access outside the cache)
   const uint8_t* mask_kv;   // exact fallback: only routed (b, kv) units run
-  float* part;              // partial records [batch][n_q][n_splits][D + 12]
+  float* part;              // partial records [batch][n_q][n_splits][D + 8]
+  // meter numerators of block segments (metered decodes; null: not recorded):
+  // [batch][n_q][n_splits][share_slots] float4 (see share_slots())
+  float4* shares;
+  int share_slots;
   void* out;
   float* meter;
   float* raw;
@@ -157,9 +161,12 @@ struct RepairArgs {
   int round0_cap;           // > 0: blocks in the first correction round (else the predicted count + 1)
 };
 constexpr int kRepHeaderBytes = 1024;
+// Repair blocks: fixed runs of 256 tokens of the sequence (Sec. 6.3), corrected in
+// 64-token tiles.
+constexpr int kRepairBlockTokens = 256;
+constexpr int kRepairTiles = kRepairBlockTokens / 64;
 // Repair workspace bytes per (sequence, KV head) (a multiple of 256).
 size_t repair_unit_bytes(int group, int head_dim, int max_rep, int tiles);
-inline int repair_tiles(int split_tokens) { return (split_tokens / 4 + 63) / 64; }
 
 struct GateArgs {
   const float* meter;
@@ -180,18 +187,36 @@ inline int64_t n_splits_for(int64_t max_seq_len, int split_tokens) {
 }
 // Partial record of one (query head, split): head_dim output floats, then the
 // running max (natural log units), weight sum, meter numerator, value-side
-// numerator sum p rho, the largest stored value norm, three spare floats, and the
-// meter numerators of the split's four blocks (quarters of split_tokens tokens).
+// numerator sum p rho, the largest stored value norm and three spare floats.
 // Weights are e^{logit - max}; the record is a multiple of 16 bytes.
-__host__ __device__ inline size_t partial_record_floats(int head_dim) { return (size_t)head_dim + 12; }
-// Workspace: the partial records, then one int32 per (sequence, KV head) for the
-// fused gate; each part rounded up to 256 bytes.
+__host__ __device__ inline size_t partial_record_floats(int head_dim) { return (size_t)head_dim + 8; }
+// Block segments of a metered decode (block repair's shares, Sec. 6.3): a segment
+// is the part of one work item's token range (a matrix-core wave's pages, the
+// vector path's split) that lies in one 256-token repair block.  Each (query head,
+// split) has share_slots() entries float4 {numerator sum_t e^{logit_t - m}
+// (e^{c_t} - 1) over the segment, frame m (natural log), first page (int bits),
+// pages (int bits, 0: unused slot)}; the matrix-core wave w owns slots
+// [w * S / 4, (w + 1) * S / 4), the vector path's workgroup all S of its split, and
+// every owned slot is written.
+inline int share_slots(int split_tokens) {
+  const int pages = split_tokens / 16;
+  const int ppw = (pages + 3) / 4;                        // pages of one wave, at most
+  const int per_wave = (ppw + 14) / 16 + 1;              // repair blocks such a run can touch
+  const int per_split = (pages + 14) / 16 + 1;
+  const int q = per_wave > (per_split + 3) / 4 ? per_wave : (per_split + 3) / 4;
+  return 4 * q;
+}
+// Workspace: the partial records, one int32 per (sequence, KV head) for the fused
+// gate, then the block segments; each part rounded up to 256 bytes.
 inline size_t records_bytes(int batch, int n_q, int64_t n_splits, int head_dim) {
   const size_t b = (size_t)batch * n_q * n_splits * partial_record_floats(head_dim) * sizeof(float);
   return (b + 255) / 256 * 256;
 }
 inline size_t gate_unit_bytes(int batch, int n_kv) {
   return ((size_t)batch * n_kv * sizeof(int32_t) + 255) / 256 * 256;
+}
+inline size_t share_bytes(int batch, int n_q, int64_t n_splits, int split_tokens) {
+  return (size_t)batch * n_q * n_splits * share_slots(split_tokens) * 16;
 }
 
 hipError_t launch_quantize_write(const WriteArgs& a, hipStream_t st);

@@ -69,9 +69,12 @@ def test_cache_byte_account(L):
 def test_workspace_size_and_argument_checks(L):
     n = L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 0)
     assert n > 0 and n % 4 == 0
-    # partial records (batch, q heads, 64 splits, head_dim + 12 floats), then one int32
-    # per (sequence, KV head) for the fused gate; each part rounded up to 256 bytes
-    assert L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 512) == 4 * 28 * 64 * 140 * 4 + 256
+    # partial records (batch, q heads, 64 splits, head_dim + 8 floats), one int32 per
+    # (sequence, KV head) for the fused gate, each part rounded up to 256 bytes, then
+    # the block segments: per (query head, split) 4 waves x 2 slots of 16 bytes (a
+    # wave's 8 pages touch at most 2 of the 256-token repair blocks)
+    assert L.wc_decode_workspace_size(4, 28, 4, 128, 32768, 512) == \
+        4 * 28 * 64 * 136 * 4 + 256 + 4 * 28 * 64 * 8 * 16
     assert L.wc_decode_workspace_size(-1, 28, 4, 128, 100, 0) == 0
     # null cache / pointers are rejected before anything is launched
     assert L.wc_quantize_write(None, None, None, 0, None, 1, None) == _lib.WC_EINVAL
@@ -150,12 +153,12 @@ def test_group_scale_and_repair_argument_checks(L):
     assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 0, None) == _lib.WC_OK   # no tokens
     # repair workspace: a 1 KB header and one record of G (d + 2) doubles per
     # (candidate block, 64-token tile) for every (sequence, KV head)
-    st = L.wc_decode_split_tokens(4, 4, 32778, 0, 0)
-    tiles = (st // 4 + 63) // 64
-    unit = 1024 + 64 * tiles * 7 * 130 * 8
-    assert L.wc_block_repair_workspace_size(4, 28, 4, 128, 32778, 0, 64) == 16 * ((unit + 255) // 256 * 256)
-    assert L.wc_block_repair_workspace_size(4, 28, 4, 128, 32778, 0, 65) == 0
-    assert L.wc_block_repair_workspace_size(4, 27, 4, 128, 32778, 0, 8) == 0
+    # (candidate block, 64-token tile) for every (sequence, KV head); blocks are
+    # fixed 256-token runs, so four tiles each
+    unit = 1024 + 64 * 4 * 7 * 130 * 8
+    assert L.wc_block_repair_workspace_size(4, 28, 4, 128, 64) == 16 * ((unit + 255) // 256 * 256)
+    assert L.wc_block_repair_workspace_size(4, 28, 4, 128, 65) == 0
+    assert L.wc_block_repair_workspace_size(4, 27, 4, 128, 8) == 0
     ex = _lib.WcCache(_lib.WC_KIND_BF16, 128, 1, 0, 0, 0, 1, 0, 16, 16)
     c.k_gexp = c.v_gexp = None
 

@@ -197,7 +197,7 @@ def test_groupscale_block_repair():
             c = refs[b]
             kx = synth.bf16_round(case["k"][b][:, kv]).astype(np.float64)
             vx = synth.bf16_round(case["v"][b][:, kv]).astype(np.float64)
-            ranges = orep.split_blocks(int(case["seq_lens"][b]), split)
+            ranges = orep.paper_blocks(int(case["seq_lens"][b]))
             st = orep.repaired_state(case["q"][b][hs], c["khat"][:, kv], c["vhat"][:, kv], kx, vx,
                                      bounds[b][hs], rep[b, kv, :n_rep[b, kv]], ranges, sm)
             assert S.rel_err(out[b, hs], st["out"]) <= S.out_tol(wl)
