@@ -26,8 +26,8 @@ theorem or table) and is written for reading against it, not for speed:
                  bypassed channels out of the amax (Sec. 4.2 outlier RoPE pairs;
                  Sec. 6.2 fixed-channel bypass, Tables 5 and 6).
 * ``groupscale`` per-token scales over 32-channel groups (Sec. 6.2 storage
-                 side, Table 4): a token scale and power-of-two group exponents,
-                 the quantizer with them, and the Tier-B radius it implies.
+                 side, Table 4): one fp16 scale per token and group, the
+                 quantizer with them, and the Tier-B radius it implies.
 * ``value``      value side: the output bound of Sec. 3, the value meter and the
                  joint K+V gate (Sec. 4.2 value side and joint event).
 * ``repair``     block-granular repair of gated heads (Sec. 6.3, block-level

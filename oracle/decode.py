@@ -24,28 +24,26 @@ def write_cache(kind: str, k: np.ndarray, v: np.ndarray, slots: np.ndarray, laye
 
     k, v: stored inputs [S, n_kv, d] (float); slots: int [S] physical slots.
     pairs: int [n_kv, m] bypassed RoPE pairs of the keys (int8 only; ``bypass``).
-    group_scales: int8 with per-32-channel group exponents (``groupscale``).
+    group_scales: int8 with one fp16 scale per token and 32-channel group
+    (``groupscale``).
     Returns reconstructions khat/vhat [S, n_kv, d], key witness kw [S, n_kv, B],
     for the quantized kinds the value residual and value norms vr, vn [S, n_kv]
-    (``value``) and, for int8, codes and scales (and with group scales the group
-    exponents ke, ve [S, n_kv, d/32]); with pairs also the stored fp16 values
-    ko [S, n_kv, 2m] and their channels chans [n_kv, 2m].
+    (``value``) and, for int8, codes and scales ks, vs ([S, n_kv], or with group
+    scales [S, n_kv, d/32]); with pairs also the stored fp16 values ko [S, n_kv, 2m]
+    and their channels chans [n_kv, 2m].
     """
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
     S, n_kv, d = k.shape
     out = {"khat": np.empty_like(k), "vhat": np.empty_like(v),
            "kw": np.zeros((S, n_kv, n_bands))}
+    if group_scales and kind != "int8_dither":
+        raise ValueError("group scales are defined for the int8 cache")
     if kind == "int8_dither":
         for key in ("kcode", "vcode"):
             out[key] = np.empty((S, n_kv, d), dtype=np.int64)
         for key in ("ks", "vs"):
-            out[key] = np.empty((S, n_kv))
-    if group_scales:
-        if kind != "int8_dither":
-            raise ValueError("group scales are defined for the int8 cache")
-        for key in ("ke", "ve"):
-            out[key] = np.empty((S, n_kv, d // groupscale.GROUP), dtype=np.int64)
+            out[key] = np.empty((S, n_kv, d // groupscale.GROUP) if group_scales else (S, n_kv))
     if pairs is not None:
         if kind != "int8_dither":
             raise ValueError("the outlier bypass is defined for the int8 cache")
@@ -56,10 +54,10 @@ def write_cache(kind: str, k: np.ndarray, v: np.ndarray, slots: np.ndarray, laye
         if kind == "int8_dither" and group_scales:
             xi = dither_values(slots, d, layer, h, seed)
             ch = None if pairs is None else out["chans"][h]
-            kc, ks, ke, ko, kh = groupscale.quantize(k[:, h], xi, ch)
-            vc, vs, ve, _, vh = groupscale.quantize(v[:, h], xi)
-            out["kcode"][:, h], out["ks"][:, h], out["ke"][:, h] = kc, ks, ke
-            out["vcode"][:, h], out["vs"][:, h], out["ve"][:, h] = vc, vs, ve
+            kc, ks, ko, kh = groupscale.quantize(k[:, h], xi, ch)
+            vc, vs, _, vh = groupscale.quantize(v[:, h], xi)
+            out["kcode"][:, h], out["ks"][:, h] = kc, ks
+            out["vcode"][:, h], out["vs"][:, h] = vc, vs
             if ko is not None:
                 out["ko"][:, h] = ko
         elif kind == "int8_dither" and pairs is not None:

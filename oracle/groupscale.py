@@ -1,31 +1,28 @@
-"""Per-token scales over 32-channel groups for the dithered INT8 cache.
+"""Per-token, per-32-channel-group scales for the dithered INT8 cache.
 
 TEST INFRASTRUCTURE ONLY (see the package header).
 
-Definitions followed (Sec. 6.2, storage side: "scale per token, per group of G_c
-channels", G_c = 32 as the default, Table 4 (granularity); Sec. 4.2 subtractive
-dither and Tier B, whose proxy sums q_c^2 s_c^2 over the channels):
+Definitions followed (Sec. 6.2, storage side: the serving store scales each
+token per group of G_c channels, G_c = 32 the default; Table 4 (granularity):
+272 bytes per token and KV head for K + V at G_c = 32, i.e. per side 128 codes
+and four 2-byte scales; Sec. 4.2 subtractive dither and Tier B, whose proxy sums
+q_c^2 s_c^2 over the channels):
 
 * Groups: channels 32g .. 32g+31 of the stored vector (d/32 groups).
-* Storage reading.  The paper does not state how the group scales are stored.
-  Here one fp16 scale per token and tensor (the token scale of the plain
-  quantizer, s = fp16_round_up(fl32(amax / 126.5)) over the kept channels) and
-  one exponent e_g in [0, 14] per group: the group's scale is s_g = s * 2^-e_g,
-  with e_g the largest exponent such that amax_g * 2^e_g <= amax (amax_g the
-  group's largest magnitude over its kept channels; 14 for an all-zero group).
-  The group scale is then within a factor 2 of amax_g / 126.5 (or at the 2^-14
-  floor), and power-of-two ratios keep the decode's operands exact: a code times
-  2^-e, e <= 14, is still an exact normal fp16 number.
-* Quantization with the stored scales, operation by operation in fp32:
-      inv_g = fl32(1/s) * 2^e_g   (exact: a power-of-two scaling)
-      y     = fl32(x * inv_g)
-      z     = fl32(y + xi)
+* Each group g of each token has its own fp16 scale, formed like the token
+  scale of the plain quantizer (Sec. 4.2, s = amax / (Q - 1/2); reading: fp32
+  quotient rounded up to fp16):
+      s_g = fp16_round_up(fl32(amax_g / 126.5)),
+  amax_g the group's largest magnitude over its quantized channels (0 for an
+  all-zero group, whose codes are then 0).
+* Quantization with the stored scale, operation by operation in fp32:
+      inv_g = fl32(1 / s_g),  y = fl32(x * inv_g),  z = fl32(y + xi),
       code  = round-half-to-even(z)
-  Since amax_g 2^e_g <= amax, |y| is bounded exactly as in the plain quantizer,
-  so no code is ever clipped.  Decoding is exact: xhat = s 2^-e_g (code - xi).
-* Bypassed pairs (``bypass``) leave both the token amax and the group amaxes;
-  their codes are 0 and their values are the stored fp16 values.
-* Tier B: the residual of channel c is the lattice-dither residual of step s_g(c),
+  (|y| <= 126.5 (1 + 2^-24) since s_g >= amax_g / 126.5, so no code is clipped);
+  decoding is exact: xhat = s_g (code - xi).
+* Bypassed pairs (``bypass``) leave the group amaxes; their codes are 0 and their
+  values are the stored fp16 values.
+* Tier B: the residual of channel c is the lattice-dither residual of step s_{g(c)},
   so varsigma_t^2 = (sm^2 / 12) sum_g s_{t,g}^2 ||q_g||^2 and the lattice bias is
   sm sum_g s_{t,g} ||q_g||_1 / 256 (both over the kept channels); the bypassed
   channels add their fp16 rounding term as in ``bypass.radius``.
@@ -39,7 +36,13 @@ from .fpformats import f16_round_up, f32
 from .quantizer import S_DIV
 
 GROUP = 32
-E_MAX = 14
+
+
+def bytes_per_token_head(d: int, group: int | None, code_bytes: int = 1, scale_bytes: int = 2) -> int:
+    """K + V storage of one token and KV head: codes plus one scale per group and
+    side (group None: one scale per token and side), the byte account of Table 4."""
+    per_side = d * code_bytes + scale_bytes * (1 if group is None else d // group)
+    return 2 * per_side
 
 
 def keep_mask(d: int, chans=None) -> np.ndarray:
@@ -50,68 +53,59 @@ def keep_mask(d: int, chans=None) -> np.ndarray:
     return keep
 
 
-def scales(x: np.ndarray, chans=None):
-    """Token scale s [n] (fp16 round-up, as float64) and group exponents e [n, d/32]."""
+def scales(x: np.ndarray, chans=None) -> np.ndarray:
+    """Group scales s [n, d/32] (fp16 round-up of fl32(amax_g / 126.5), as float64)."""
     x = np.asarray(x, dtype=np.float64)
     n, d = x.shape
     ax = np.where(keep_mask(d, chans), np.abs(x), 0.0)
-    amax = ax.max(axis=1)
-    s = f16_round_up(f32(amax / S_DIV))
-    ag = ax.reshape(n, d // GROUP, GROUP).max(axis=2)               # group amaxes [n, d/32]
-    # the largest k <= E_MAX with ag 2^k <= amax: the condition holds for every
-    # smaller k once it holds for k, so e counts the k = 1 .. E_MAX for which it holds
-    e = np.zeros((n, d // GROUP), dtype=np.int64)
-    for k in range(1, E_MAX + 1):
-        e += (ag * 2.0 ** k <= amax[:, None]).astype(np.int64)
-    return s, e
+    ag = ax.reshape(n, d // GROUP, GROUP).max(axis=2)
+    return f16_round_up(f32(ag / S_DIV))
 
 
-def group_steps(s: np.ndarray, e: np.ndarray) -> np.ndarray:
-    """Per-channel scale s_c = s 2^-e_{g(c)}, [n, d]."""
-    return np.repeat(np.asarray(s, dtype=np.float64)[:, None] * 2.0 ** -np.asarray(e, dtype=np.float64),
-                     GROUP, axis=1)
+def channel_steps(s: np.ndarray) -> np.ndarray:
+    """Per-channel step s_{g(c)}, [n, d]."""
+    return np.repeat(np.asarray(s, dtype=np.float64), GROUP, axis=-1)
 
 
 def encode(x: np.ndarray, xi: np.ndarray, chans=None):
-    """Codes (int64 [n, d]), token scales s [n] and group exponents e [n, d/32]."""
+    """Codes (int64 [n, d]) and group scales s [n, d/32]."""
     x = np.asarray(x, dtype=np.float64)
     keep = keep_mask(x.shape[-1], chans)
-    s, e = scales(x, chans)
+    s = scales(x, chans)
     with np.errstate(divide="ignore"):
-        inv_s = np.where(s > 0, f32(1.0 / np.where(s > 0, s, 1.0)), 0.0)
-    inv_c = np.repeat(inv_s[:, None] * 2.0 ** e, GROUP, axis=1)
-    y = f32(np.where(keep, x, 0.0) * inv_c)
+        inv = np.where(s > 0, f32(1.0 / np.where(s > 0, s, 1.0)), 0.0)
+    y = f32(np.where(keep, x, 0.0) * channel_steps(inv))
     z = f32(y + xi)
     code = np.rint(z).astype(np.int64)
     code[:, ~keep] = 0
-    return code, s, e
+    return code, s
 
 
-def decode(code: np.ndarray, s: np.ndarray, e: np.ndarray, xi: np.ndarray) -> np.ndarray:
-    """xhat = s 2^-e_g (code - xi), exact in float64."""
-    return group_steps(s, e) * (np.asarray(code, dtype=np.float64) - xi)
+def decode(code: np.ndarray, s: np.ndarray, xi: np.ndarray) -> np.ndarray:
+    """xhat = s_g (code - xi), exact in float64."""
+    return channel_steps(s) * (np.asarray(code, dtype=np.float64) - xi)
 
 
 def quantize(x: np.ndarray, xi: np.ndarray, chans=None):
-    """(code, s, e, ovals or None, xhat) of rows x [n, d] with dither xi [n, d]."""
+    """(code, s, ovals or None, xhat) of rows x [n, d] with dither xi [n, d]."""
     x = np.asarray(x, dtype=np.float64)
-    code, s, e = encode(x, xi, chans)
-    xh = decode(code, s, e, xi)
+    code, s = encode(x, xi, chans)
+    xh = decode(code, s, xi)
     ovals = None
     if chans is not None and len(chans):
         ch = np.asarray(chans, dtype=np.int64)
         ovals = bypass.f16_nearest(x[:, ch])
         xh[:, ch] = ovals
-    return code, s, e, ovals, xh
+    return code, s, ovals, xh
 
 
-def radius(q: np.ndarray, s_tok: np.ndarray, e: np.ndarray, sm_scale: float, n_tokens: int,
-           dloc: float, ovals=None, chans=None) -> np.ndarray:
-    """Tier-B radius u_t [S] of one query head over group-scaled keys."""
+def radius(q: np.ndarray, s: np.ndarray, sm_scale: float, n_tokens: int, dloc: float, ovals=None,
+           chans=None) -> np.ndarray:
+    """Tier-B radius u_t [S] of one query head over group-scaled keys (s [S, d/32])."""
     q = np.asarray(q, dtype=np.float64)
     keep = keep_mask(q.shape[-1], chans)
     qk = np.where(keep, q, 0.0)
-    sc = group_steps(s_tok, e)                              # [S, d]
+    sc = channel_steps(s)                                   # [S, d]
     var = sm_scale ** 2 / 12.0 * (sc ** 2 @ qk ** 2)
     bias = sm_scale * (sc @ np.abs(qk)) / 256.0
     u = bias + np.sqrt(2.0 * var * np.log(2.0 * n_tokens / dloc))
@@ -120,12 +114,12 @@ def radius(q: np.ndarray, s_tok: np.ndarray, e: np.ndarray, sm_scale: float, n_t
     return u
 
 
-def tierb_decode(q: np.ndarray, khat: np.ndarray, vhat: np.ndarray, ks: np.ndarray, ke: np.ndarray,
-                 sm_scale: float, dloc: float, ko=None, chans=None) -> dict:
+def tierb_decode(q: np.ndarray, khat: np.ndarray, vhat: np.ndarray, ks: np.ndarray, sm_scale: float,
+                 dloc: float, ko=None, chans=None) -> dict:
     """Tier-B decode step over a group-scaled cache.
 
-    q [n_q, d]; khat, vhat [S, n_kv, d]; ks [S, n_kv] token scales; ke [S, n_kv, d/32]
-    group exponents; with bypassed pairs ko [S, n_kv, 2m] and chans [n_kv, 2m].
+    q [n_q, d]; khat, vhat [S, n_kv, d]; ks [S, n_kv, d/32] key group scales; with
+    bypassed pairs ko [S, n_kv, 2m] and chans [n_kv, 2m].
     Returns out, raw, meter [n_q] and u [n_q, S].
     """
     q = np.asarray(q, dtype=np.float64)
@@ -139,7 +133,7 @@ def tierb_decode(q: np.ndarray, khat: np.ndarray, vhat: np.ndarray, ks: np.ndarr
         kv = h // g
         z = attention.logits(q[h], khat[:, kv], sm_scale)
         p = attention.softmax(z)
-        u = radius(q[h], ks[:, kv], ke[:, kv], sm_scale, S, dloc,
+        u = radius(q[h], ks[:, kv], sm_scale, S, dloc,
                    None if ko is None else ko[:, kv], None if chans is None else chans[kv])
         out[h] = p @ vhat[:, kv]
         raw[h] = mt.raw_from_am1(mt.a_minus_one_logits(z, u))
