@@ -616,9 +616,10 @@ def main():
                                                  if fixed.any() else None),
             "whole_head_bytes": round(whole)}
 
-        # group scales (Sec. 6.2 storage side, Table 4): the same bypass caches with a
-        # 4-bit power-of-two exponent per 32-channel group (+2 + 2 bytes per
-        # token-head), both tiers with the fused gate, and their meters
+        # group scales (Sec. 6.2 storage side, Table 4): the same bypass caches with one
+        # fp16 scale per token and 32-channel group (8 bytes per side instead of 2),
+        # both tiers with the fused gate, and their meters; these decodes run on the
+        # vector ALUs
         if gs_caches:
             ga_ms = timed(lambda i: wc.metered_decode_gate(
                 gs_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
@@ -640,9 +641,9 @@ def main():
                                           ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw)
                 wc.gate(meter, raw, wl.group, args.tau, n_gated=cnt_g["B"], mask_q=mq_b, mask_kv=mkv_b)
                 raws_g["B"].append(raw.clone())
-            gsd = {"path": "matrix cores (group exponents in the fp16 operand exponents)"}
-            for tier, ms, nbytes in (("tier_a", ga_ms, INT8_BYTES + 4 * m_byp + 4),
-                                     ("tier_b", gb_ms, TIERB_BYTES + 4 * m_byp + 4)):
+            gsd = {"path": "vector ALUs (fp16 group scales)"}
+            for tier, ms, nbytes in (("tier_a", ga_ms, INT8_BYTES + 4 * m_byp + 12),
+                                     ("tier_b", gb_ms, TIERB_BYTES + 4 * m_byp + 12)):
                 key = "A" if tier == "tier_a" else "B"
                 gq_, gkv_ = cnt_g[key].cpu().tolist()
                 gbps = float(last["tokens"] * wl.n_kv) * nbytes / (float(np.median(ms)) * 1e-3) / 1e9

@@ -101,7 +101,8 @@ extern "C" {
  *                bytes (r*CL + i)*16 .. +15 of that row: token t, channel c at byte
  *                ((p%CL*4 + t/4)*16 + p/CL)*16 + b%16, b = (4c + t%4)*E, p = b/16.
  *   k_scale,
- *   v_scale    [num_blocks][n_kv_heads][16] fp16              INT8_DITHER only, else NULL
+ *   v_scale    [num_blocks][n_kv_heads][16] fp16              INT8_DITHER only, else NULL;
+ *              with group_scales [num_blocks][n_kv_heads][16][head_dim/32] fp16
  *   k_witness  [num_blocks][n_kv_heads][16][n_bands] fp16     NULL for BF16
  *   k_outlier  [num_blocks][n_kv_heads][16][2m] fp16          keys of the bypassed pairs
  *              (m = n_outlier_pairs > 0 only, else NULL)
@@ -109,10 +110,6 @@ extern "C" {
  *   v_norm     [num_blocks][n_kv_heads][16] fp16              value side (optional, both or
  *              neither, quantized kinds only): ||vhat_t - v_t|| rounded up and ||v_t||
  *              rounded down, from float64 norms (Sec. 3 output bound; Sec. 4.2 value side)
- *   k_gexp,
- *   v_gexp     [num_blocks][n_kv_heads][16] uint16            group scales (optional, both or
- *              neither, INT8_DITHER only): bits 4g..4g+3 hold the exponent e_g of channel
- *              group g (channels 32g..32g+31); the group's step is s * 2^-e_g
  * Element type of k_data/v_data: int8 code stored excess-128, i.e. the byte code + 128
  * (INT8_DITHER; codes lie in [-127, 127]), E4M3 byte (FP8_RAW), bf16 (BF16).
  * Band b holds the channels of RoPE pairs b*P .. b*P+P-1, P = head_dim/(2*n_bands)
@@ -130,13 +127,12 @@ extern "C" {
  * +-65504.  Values are not bypassed.  m is even, 0 <= m <= 16.
  *
  * Group scales (INT8_DITHER; Sec. 6.2 storage side: per token, per group of 32
- * channels; Table 4 granularity): with k_gexp/v_gexp set, each token keeps its fp16
- * scale s and every 32-channel group g gets the step s * 2^-e_g, e_g in [0, 14] the
- * largest exponent with amax_g * 2^e_g <= amax (amax over the token's quantized
- * channels, amax_g over the group's; 14 for an all-zero group).  Power-of-two
- * ratios keep every dequantized code an exact normal fp16 multiple, so the
- * decode's matrix-core operands stay exact.  Bypassed channels leave amax_g as they leave
- * amax.
+ * channels; Table 4: 272 bytes per token-head for K + V): with group_scales = 1,
+ * every token has one fp16 scale per 32-channel group g (channels 32g..32g+31) and
+ * tensor, s_g = fp16_round_up(fl32(amax_g / 126.5)) over the group's quantized
+ * channels (bypassed channels leave amax_g), stored in k_scale / v_scale in place
+ * of the token scale; codes use fl32(1/s_g).  The decode of a group-scaled cache
+ * runs on the vector ALUs.
  */
 typedef struct wc_cache {
     int32_t  kind;          /* WC_KIND_*                                       */
@@ -149,11 +145,10 @@ typedef struct wc_cache {
     uint64_t seed;          /* Philox4x32-10 key (low word = key[0])           */
     void *k_data, *v_data, *k_scale, *v_scale, *k_witness;
     int32_t  n_outlier_pairs;          /* m: bypassed RoPE pairs per KV head (0: none) */
-    int32_t  reserved;                 /* 0                                            */
+    int32_t  group_scales;             /* 1: one fp16 scale per 32-channel group, 0: per token */
     const int32_t* outlier_pairs;      /* [n_kv_heads][m] device, or NULL when m == 0  */
     void*    k_outlier;                /* see above, or NULL when m == 0               */
     void    *v_resid, *v_norm;          /* value side, or both NULL                     */
-    void    *k_gexp, *v_gexp;           /* group exponents, or both NULL                */
 } wc_cache;
 
 const char* wc_strerror(int status);
@@ -161,15 +156,15 @@ int         wc_version(void);   /* 100*major + minor */
 
 /*
  * Bytes of each array of a cache (k_data, v_data, k_scale, v_scale, k_witness,
- * k_outlier, v_resid, v_norm, k_gexp, v_gexp) written to sizes[0..9]; returns
- * their sum, 0 on bad arguments.  The "exact byte account" of the cache (Sec. 5
- * memory saving; Sec. 6.2 acceptance; Table 6: 4m bytes per token and KV head for
- * the bypassed pairs; 2 + 2 bytes for the value side when value_side != 0; 2 + 2
- * bytes for the group exponents when group_scales != 0).
+ * k_outlier, v_resid, v_norm) written to sizes[0..7]; returns their sum, 0 on bad
+ * arguments.  The "exact byte account" of the cache (Sec. 5 memory saving; Sec.
+ * 6.2 acceptance; Table 4: 2 bytes per scale, one per token or one per 32-channel
+ * group and side when group_scales != 0; Table 6: 4m bytes per token and KV head
+ * for the bypassed pairs; 2 + 2 bytes for the value side when value_side != 0).
  */
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim,
                       int n_bands, int n_outlier_pairs, int value_side, int group_scales,
-                      size_t sizes[10]);
+                      size_t sizes[8]);
 
 /*
  * Fixed outlier-pair set of each KV head (Sec. 6.2 fixed-channel bypass; Sec. 4.2
@@ -193,12 +188,12 @@ int wc_select_outlier_pairs(const void* k, int in_dtype, int64_t n_tok, int n_kv
 /*
  * Write path (Sec. 4.2 subtractive dither; Sec. 6.2 research kernels and storage
  * side; Sec. 4.1 Eq. witness).  For every token i < n_tok and KV head h:
- *   INT8_DITHER: s = fp16_round_up(fl32(amax/126.5)) per (token, head, tensor);
+ *   INT8_DITHER: s = fp16_round_up(fl32(amax/126.5)) per (token, head, tensor), or
+ *                per 32-channel group with group scales;
  *                xi_c = (u_c - 127.5)/256 with u_c the Philox4x32-10 byte of channel c
  *                (key = seed, counter = (c/16, slot lo, slot hi, layer<<16 | h)),
  *                shared by K and V; code = rint_even(fl32(fl32(x*inv) + xi)) with
- *                inv = fl32(1/s), times 2^e_g with group scales (then k_gexp/v_gexp
- *                receive the exponents);
+ *                inv = fl32(1/s) (of the channel's group);
  *                with bypassed pairs (n_outlier_pairs > 0) the amax and the codes
  *                skip their channels and k_outlier receives fp16(x) of them;
  *   FP8_RAW:     code = E4M3(x), nearest-even, saturating at +-448;

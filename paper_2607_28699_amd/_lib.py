@@ -34,10 +34,9 @@ class WcCache(ctypes.Structure):
         ("num_blocks", ctypes.c_int64), ("seed", ctypes.c_uint64),
         ("k_data", ctypes.c_void_p), ("v_data", ctypes.c_void_p), ("k_scale", ctypes.c_void_p),
         ("v_scale", ctypes.c_void_p), ("k_witness", ctypes.c_void_p),
-        ("n_outlier_pairs", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("n_outlier_pairs", ctypes.c_int32), ("group_scales", ctypes.c_int32),
         ("outlier_pairs", ctypes.c_void_p), ("k_outlier", ctypes.c_void_p),
         ("v_resid", ctypes.c_void_p), ("v_norm", ctypes.c_void_p),
-        ("k_gexp", ctypes.c_void_p), ("v_gexp", ctypes.c_void_p),
     ]
 
 

@@ -43,7 +43,7 @@ def _dev_check(*ts):
 
 def cache_bytes(kind: str, num_blocks: int, n_kv: int, head_dim: int, n_bands: int,
                 n_outlier_pairs: int = 0, value_side: bool = False, group_scales: bool = False):
-    sizes = (ctypes.c_size_t * 10)()
+    sizes = (ctypes.c_size_t * 8)()
     total = lib().wc_cache_bytes(KINDS[kind], num_blocks, n_kv, head_dim, n_bands, n_outlier_pairs,
                                  int(value_side), int(group_scales), sizes)
     if total == 0:
@@ -72,8 +72,7 @@ class PagedCache:
         m = self.n_outlier_pairs
         total, sizes = cache_bytes(self.kind, self.num_blocks, self.n_kv, self.head_dim, self.n_bands, m,
                                    self.value_side, self.group_scales)
-        names = ("k_data", "v_data", "k_scale", "v_scale", "k_witness", "k_outlier", "v_resid", "v_norm",
-                 "k_gexp", "v_gexp")
+        names = ("k_data", "v_data", "k_scale", "v_scale", "k_witness", "k_outlier", "v_resid", "v_norm")
         slots = self.num_blocks * WC_BLOCK_TOKENS * self.n_kv
         # pages of 16-byte pieces [CL][4][16][16 bytes], CL = head_dim * E / 64 (E bytes per element)
         esz = 2 if self.kind == "bf16" else 1
@@ -81,14 +80,15 @@ class PagedCache:
         shapes = {
             "k_data": piece_shape,
             "v_data": piece_shape,
-            "k_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
-            "v_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
+            # one fp16 scale per token, or per 32-channel group (Table 4)
+            "k_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS) + ((self.head_dim // 32,)
+                                                                        if self.group_scales else ()),
+            "v_scale": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS) + ((self.head_dim // 32,)
+                                                                        if self.group_scales else ()),
             "k_witness": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, self.n_bands),
             "k_outlier": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS, 2 * m),
             "v_resid": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
             "v_norm": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
-            "k_gexp": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
-            "v_gexp": (self.num_blocks, self.n_kv, WC_BLOCK_TOKENS),
         }
         # int8 codes are stored excess-128 (byte = code + 128)
         el = {"int8_dither": torch.uint8, "fp8_raw": torch.uint8, "bf16": torch.bfloat16}[self.kind]
@@ -117,9 +117,9 @@ class PagedCache:
         return WcCache(KINDS[self.kind], self.head_dim, self.n_kv, self.n_bands,
                        LAYOUTS[self.rope_layout], self.layer, self.num_blocks, self.seed,
                        _ptr(t["k_data"]), _ptr(t["v_data"]), _ptr(t["k_scale"]),
-                       _ptr(t["v_scale"]), _ptr(t["k_witness"]), self.n_outlier_pairs, 0,
-                       _ptr(t["outlier_pairs"]), _ptr(t["k_outlier"]), _ptr(t["v_resid"]),
-                       _ptr(t["v_norm"]), _ptr(t["k_gexp"]), _ptr(t["v_gexp"]))
+                       _ptr(t["v_scale"]), _ptr(t["k_witness"]), self.n_outlier_pairs,
+                       1 if self.group_scales else 0, _ptr(t["outlier_pairs"]), _ptr(t["k_outlier"]),
+                       _ptr(t["v_resid"]), _ptr(t["v_norm"]))
 
 
 def quantize_write(cache: PagedCache, k: torch.Tensor, v: torch.Tensor, slots: torch.Tensor) -> None:

@@ -42,10 +42,7 @@ int check_cache(const wc_cache* c, bool need_witness, bool witness_optional = fa
   if (c->v_resid != nullptr &&
       (c->kind == WC_KIND_BF16 || !aligned16(c->v_resid) || !aligned16(c->v_norm)))
     return WC_EINVAL;
-  if ((c->k_gexp != nullptr) != (c->v_gexp != nullptr)) return WC_EINVAL;   // group scales: both or neither
-  if (c->k_gexp != nullptr &&
-      (c->kind != WC_KIND_INT8_DITHER || !aligned16(c->k_gexp) || !aligned16(c->v_gexp)))
-    return WC_EINVAL;
+  if (c->group_scales != 0 && (c->group_scales != 1 || c->kind != WC_KIND_INT8_DITHER)) return WC_EINVAL;
   return WC_OK;
 }
 
@@ -93,7 +90,7 @@ const char* wc_strerror(int status) {
 int wc_version(void) { return 102; }   // 1.2: wc_step_metered_decode_gate_noalloc
 
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim, int n_bands,
-                      int n_outlier_pairs, int value_side, int group_scales, size_t sizes[10]) {
+                      int n_outlier_pairs, int value_side, int group_scales, size_t sizes[8]) {
   if (kind < WC_KIND_INT8_DITHER || kind > WC_KIND_BF16 || num_blocks < 0 || n_kv_heads < 1 ||
       head_dim < 1 || (kind != WC_KIND_BF16 && n_bands < 1))
     return 0;
@@ -101,15 +98,15 @@ size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim
       2 * n_outlier_pairs > head_dim || (n_outlier_pairs && kind != WC_KIND_INT8_DITHER))
     return 0;
   if (value_side && kind == WC_KIND_BF16) return 0;
-  if (group_scales && kind != WC_KIND_INT8_DITHER) return 0;
+  if (group_scales && (kind != WC_KIND_INT8_DITHER || head_dim % 32)) return 0;
   const size_t slots = (size_t)num_blocks * WC_BLOCK_TOKENS * (size_t)n_kv_heads;
-  size_t s[10];
+  size_t s[8];
   s[0] = s[1] = slots * head_dim * elem_bytes(kind);
-  s[2] = s[3] = kind == WC_KIND_INT8_DITHER ? slots * 2 : 0;
+  // one fp16 scale per token, or per 32-channel group (Table 4)
+  s[2] = s[3] = kind == WC_KIND_INT8_DITHER ? slots * 2 * (group_scales ? head_dim / 32 : 1) : 0;
   s[4] = kind == WC_KIND_BF16 ? 0 : slots * n_bands * 2;
   s[5] = slots * (size_t)n_outlier_pairs * 4;   // 2m fp16 values per token-head
   s[6] = s[7] = value_side ? slots * 2 : 0;     // value residual, value norm
-  s[8] = s[9] = group_scales ? slots * 2 : 0;   // group exponents, 4 bits per group
   if (sizes) memcpy(sizes, s, sizeof(s));
   size_t total = 0;
   for (size_t x : s) total += x;
@@ -159,8 +156,7 @@ static int write_args(const wc_cache* cache, const wc_cache* exact, const void* 
   a.k_outlier = static_cast<uint16_t*>(cache->k_outlier);
   a.v_resid = static_cast<uint16_t*>(cache->v_resid);
   a.v_norm = static_cast<uint16_t*>(cache->v_norm);
-  a.k_gexp = static_cast<uint16_t*>(cache->k_gexp);
-  a.v_gexp = static_cast<uint16_t*>(cache->v_gexp);
+  a.group_scales = cache->group_scales;
   return WC_OK;
 }
 
@@ -307,8 +303,7 @@ static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int 
   a.k_outlier = static_cast<const uint16_t*>(cache->k_outlier);
   a.v_resid = static_cast<const uint16_t*>(cache->v_resid);
   a.v_norm = static_cast<const uint16_t*>(cache->v_norm);
-  a.k_gexp = static_cast<const uint16_t*>(cache->k_gexp);
-  a.v_gexp = static_cast<const uint16_t*>(cache->v_gexp);
+  a.group_scales = cache->group_scales;
   // WITCERT_FORCE_VALU=1 selects the vector-ALU kernels even where the
   // matrix-core ones apply (used to cross-check the two paths)
   const char* force = getenv("WITCERT_FORCE_VALU");

@@ -76,11 +76,6 @@ constexpr uint32_t kSelH1 = 0x07060302u;   // high halves of lo and hi
 __device__ __forceinline__ uint32_t codes2(uint32_t xb, uint32_t sel) {
   return as_u32(as_h2(perm(0x64646464u, xb, sel)) - h2_t{(_Float16)1152.0f, (_Float16)1152.0f});
 }
-// The same times 2^-e (group scales): hi = 0x64646464 - e * 0x04040404 lowers the
-// exponent of 1024 + u by e, c = 1152 2^-e in both halves; exact for e <= 14.
-__device__ __forceinline__ uint32_t codes2e(uint32_t xb, uint32_t sel, uint32_t hi, uint32_t c) {
-  return as_u32(as_h2(perm(hi, xb, sel)) - as_h2(c));
-}
 // Two stored bytes u -> fp16 1024 + u = code + 1152 (exact): the value operand of
 // PV, whose 1152 offset is removed once at the end with the weight sum.
 __device__ __forceinline__ uint32_t ucodes2(uint32_t xb, uint32_t sel) {
@@ -112,18 +107,6 @@ __device__ __forceinline__ uint32_t bf16pair_to_f16_scaled(uint32_t w, float two
   return as_u32(h2_t{(_Float16)a, (_Float16)b});
 }
 
-// fp16 bits of 2^-e (e <= 14: a normal number).
-__device__ __forceinline__ uint32_t f16_pow2_neg(uint32_t e) { return (15u - e) << 10; }
-// Two fp16 values x*2^-e from fp16 bits: the exponent field lowered by e in both halves
-// (no borrow: the operands are normal numbers with exponent fields above e).
-__device__ __forceinline__ uint32_t f16x2_scale_down(uint32_t h2bits, uint32_t e_lo, uint32_t e_hi) {
-  return h2bits - ((e_lo << 10) | (e_hi << 26));
-}
-// fp16 x in hi + lo parts.
-__device__ __forceinline__ void f16_split(float x, _Float16& hi, _Float16& lo) {
-  hi = (_Float16)x;
-  lo = (_Float16)(x - (float)hi);
-}
 
 __device__ __forceinline__ h8_t pack8(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
   return __builtin_bit_cast(h8_t, make_uint4(a, b, c, d));
@@ -144,8 +127,6 @@ struct PageRegs {
   uint4 wit;         // witness bands 8(g%2).. of token r (garbage where 8(g%2) >= n_bands)
   uint4 ov;          // fp16 keys of bypassed pairs: values 8g .. 8g+7 of token r (when 8g < 2m)
   uint2 vr, vn;      // value side: stored ||vhat - v|| and ||v|| of tokens 4g..4g+3
-  uint32_t kge;      // group scales: key exponent words of tokens 2(r/2), 2(r/2)+1
-  uint2 vge;         // group scales: value exponent words of tokens 4g..4g+3
   int blk;           // cache block of the page (wave-uniform)
 };
 
@@ -168,7 +149,7 @@ __device__ __forceinline__ uint2 bload8(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kPageAux));
 }
 
-template <int KIND, bool METER, bool TB, bool BYP, bool VM, bool GS>
+template <int KIND, bool METER, bool TB, bool BYP, bool VM>
 __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool valid, int kv, int r,
                                           int g, int wit_off, PageRegs<KIND>& p) {
   constexpr int KB = KIND == WC_KIND_BF16 ? 64 : 32;   // bytes per lane and tensor
@@ -211,11 +192,6 @@ __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool val
     p.vr = bload8(page_rsrc(a.v_resid + page * kBlockTokens, sb), 8 * g);
     p.vn = bload8(page_rsrc(a.v_norm + page * kBlockTokens, sb), 8 * g);
   }
-  if constexpr (GS) {
-    const int sb = valid ? 2 * kBlockTokens : 0;
-    p.kge = __builtin_amdgcn_raw_buffer_load_b32(page_rsrc(a.k_gexp + page * kBlockTokens, sb), 4 * (r >> 1), 0, kPageAux);
-    p.vge = bload8(page_rsrc(a.v_gexp + page * kBlockTokens, sb), 8 * g);
-  }
 }
 
 // Running state of one wave.  Logits are kept in log2 units; every weight carries
@@ -228,7 +204,6 @@ struct WaveState {
   int ve;                // INT8 value exponent (wave-uniform, scalar): PV weights carry 2^-ve, and 2^ve
                          // bounds the value scales seen so far
   float ev, vmax;        // value side: sum of weights x stored ||vhat - v||, largest stored ||v||
-  f4_t wsg;              // group scales: sum of fp16 weights x 2^-e_g per group (rows 0..3)
 };
 
 // Per-wave constants of the page loop.
@@ -243,12 +218,6 @@ struct WaveConst {
   h8_t qa;         // their magnitudes (Tier B rounding term)
   float gmul;      // Tier B: sm_scale * 2^-11 * log2(e)
   float gc;        // Tier B: sm_scale * 2^-25 * log2(e) * sum |q_c| over the bypassed channels
-  h8_t qoff;       // group scales: B operand of the dither-offset product, 2303/512 sum_{c in g} q_c
-                   // for groups 0..3 in fp16 hi (k 0..3) and lo (k 4..7) parts (lane group 0)
-  h8_t qg1, qg2;   // group scales, Tier B: sm log2(e) ||q_g||_1 / 256 and 2^-14 ||q_g||^2, hi + lo
-  float rtl;       // group scales, Tier B: sm log2(e) sqrt(2 log(2S / delta) / 12)
-  const uint4* qsh; // group scales: this lane's operands in LDS (qop, qoff, qg1, qg2, qnop, qo, qa;
-                    // stride 64)
   uint32_t layer_head;
   bool wit_ok;
   bool ov_lo, ov_hi;   // this lane's stored values 8g..8g+3, 8g+4..8g+7 exist (< 2m)
@@ -287,44 +256,15 @@ __device__ __forceinline__ uint32_t dpp_from_upper8(uint32_t v) {
 }
 
 // One 16-token page.  FULL: every token of the page is below t_end (no masking).
-template <int KIND, bool METER, bool FULL, bool HALF, bool TB, bool BYP, bool VM, bool GS>
+template <int KIND, bool METER, bool FULL, bool HALF, bool TB, bool BYP, bool VM>
 __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs<KIND>& cur, int t0,
                                              int t_end, int r, int g, const WaveConst& wc,
                                              uint8_t* my_dsh, WaveState& st) {
   // ---------------- QK^T and the bound ----------------
   const f4_t z4 = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
   f4_t s1 = z4, s2 = z4;   // code products, dither products
-  f4_t c1 = z4, c2 = z4;   // group scales, Tier B: sum_g 2^-e_g (.) and sum_g 4^-e_g (.) per token
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
-    // Group scales: lane group g holds channels 32g..32g+31 = group g of token r, so
-    // its code and dither operands carry the factor 2^-e of that group, exactly
-    // (the fp16 exponent field is lowered by e); the dither offset 2303/512 times
-    // sum_g 2^-e_g sum_{c in g} q_c comes from one more product.
-    uint32_t ek = 0;
-    if constexpr (GS) {
-      const uint32_t tw = (r & 1) ? (cur.kge >> 16) : (cur.kge & 0xFFFFu);   // token r's exponents
-      ek = (tw >> (4 * g)) & 15u;
-      uint32_t aw0 = 0, aw1 = 0, bw0 = 0, bw1 = 0;
-      if (g == 0) {
-        aw0 = f16_pow2_neg(tw & 15u) | (f16_pow2_neg((tw >> 4) & 15u) << 16);
-        aw1 = f16_pow2_neg((tw >> 8) & 15u) | (f16_pow2_neg((tw >> 12) & 15u) << 16);
-        if constexpr (TB) {   // 2^(14 - 2e): normal for e <= 14
-          bw0 = ((29u - 2u * (tw & 15u)) << 10) | ((29u - 2u * ((tw >> 4) & 15u)) << 26);
-          bw1 = ((29u - 2u * ((tw >> 8) & 15u)) << 10) | ((29u - 2u * ((tw >> 12) & 15u)) << 26);
-        }
-      }
-      const h8_t aoff = pack8(aw0, aw1, aw0, aw1);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aoff, __builtin_bit_cast(h8_t, wc.qsh[4 * 64]), z4, 0, 0, 0);
-      if constexpr (TB) {
-        c1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(aoff, __builtin_bit_cast(h8_t, wc.qsh[5 * 64]), z4, 0, 0, 0);
-        c2 = __builtin_amdgcn_mfma_f32_16x16x32_f16(pack8(bw0, bw1, bw0, bw1),
-                                                    __builtin_bit_cast(h8_t, wc.qsh[6 * 64]), z4, 0, 0, 0);
-      }
-    } else {
-      s1 = f4_t{wc.s1_init, wc.s1_init, wc.s1_init, wc.s1_init};
-    }
-    const uint32_t hik = 0x64646464u - ek * 0x04040404u;           // (1024 + u) 2^-e
-    const uint32_t c1152 = (0x6480u - (ek << 10)) * 0x00010001u;   // 1152 2^-e, both halves
+    s1 = f4_t{wc.s1_init, wc.s1_init, wc.s1_init, wc.s1_init};
     const int64_t slot = (int64_t)cur.blk * kBlockTokens + r;
     const U4 r0 = dither_block(2 * g, slot, wc.layer_head, a.key0, a.key1);
     const U4 r1 = dither_block(2 * g + 1, slot, wc.layer_head, a.key0, a.key1);
@@ -338,19 +278,10 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
       const uint32_t x0 = cur.kw[2 * kt], x1 = cur.kw[2 * kt + 1];   // excess-128 codes
-      h8_t ka;
-      if constexpr (GS)
-        ka = pack8(codes2e(x0, kSelLo, hik, c1152), codes2e(x0, kSelHi, hik, c1152),
-                   codes2e(x1, kSelLo, hik, c1152), codes2e(x1, kSelHi, hik, c1152));
-      else
-        ka = pack8(codes2(x0, kSelLo), codes2(x0, kSelHi), codes2(x1, kSelLo), codes2(x1, kSelHi));
-      const h8_t qb = GS ? __builtin_bit_cast(h8_t, wc.qsh[kt * 64]) : wc.qop[kt];
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qb, s1, 0, 0, 0);
-      h8_t kd = pack8(dq[4 * kt], dq[4 * kt + 1], dq[4 * kt + 2], dq[4 * kt + 3]);
-      if constexpr (GS)
-        kd = pack8(f16x2_scale_down(dq[4 * kt], ek, ek), f16x2_scale_down(dq[4 * kt + 1], ek, ek),
-                   f16x2_scale_down(dq[4 * kt + 2], ek, ek), f16x2_scale_down(dq[4 * kt + 3], ek, ek));
-      s2 = __builtin_amdgcn_mfma_f32_16x16x32_f16(kd, qb, s2, 0, 0, 0);
+      const h8_t ka = pack8(codes2(x0, kSelLo), codes2(x0, kSelHi), codes2(x1, kSelLo), codes2(x1, kSelHi));
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, wc.qop[kt], s1, 0, 0, 0);
+      const h8_t kd = pack8(dq[4 * kt], dq[4 * kt + 1], dq[4 * kt + 2], dq[4 * kt + 3]);
+      s2 = __builtin_amdgcn_mfma_f32_16x16x32_f16(kd, wc.qop[kt], s2, 0, 0, 0);
     }
     // dither of this page to LDS (row = token r, channels 32g..32g+31)
     uint4* dst = reinterpret_cast<uint4*>(my_dsh + r * kRow + 64 * g);
@@ -379,7 +310,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   if constexpr (METER && !TB) {
     const uint4 w = wc.wit_ok ? cur.wit : make_uint4(0, 0, 0, 0);
     cb = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, w),
-                                                GS ? __builtin_bit_cast(h8_t, wc.qsh[7 * 64]) : wc.qnop, cb, 0, 0, 0);
+                                                wc.qnop, cb, 0, 0, 0);
   }
   // bypassed pairs (Sec. 6.2): q . khat over their channels from the stored fp16
   // values (the query operand of the code products is zero there), and for Tier B
@@ -389,11 +320,11 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     const uint32_t o0 = wc.ov_lo ? cur.ov.x : 0u, o1 = wc.ov_lo ? cur.ov.y : 0u;
     const uint32_t o2 = wc.ov_hi ? cur.ov.z : 0u, o3 = wc.ov_hi ? cur.ov.w : 0u;
     so = __builtin_amdgcn_mfma_f32_16x16x32_f16(pack8(o0, o1, o2, o3),
-                                                GS ? __builtin_bit_cast(h8_t, wc.qsh[8 * 64]) : wc.qo, so, 0, 0, 0);
+                                                wc.qo, so, 0, 0, 0);
     if constexpr (TB) {
       constexpr uint32_t kAbs = 0x7FFF7FFFu;
       go = __builtin_amdgcn_mfma_f32_16x16x32_f16(pack8(o0 & kAbs, o1 & kAbs, o2 & kAbs, o3 & kAbs),
-                                                  GS ? __builtin_bit_cast(h8_t, wc.qsh[9 * 64]) : wc.qa, go, 0, 0, 0);
+                                                  wc.qa, go, 0, 0, 0);
     }
   }
 
@@ -405,11 +336,9 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   constexpr int NT = HALF ? 2 : 4;
   const bool upper = HALF && r >= 8;
   const int tok0 = 4 * g + (upper ? 2 : 0);            // first token of this lane
-  float scv[4], cbv[4], sov[4], gov[4], c1v[4], c2v[4];
+  float scv[4], cbv[4], sov[4], gov[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    c1v[e] = c1[e];
-    c2v[e] = c2[e];
     scv[e] = s1[e];
     if constexpr (KIND == WC_KIND_INT8_DITHER) scv[e] = fmaf(s2[e], -0.001953125f, scv[e]);   // q . (code + xi)
     cbv[e] = cb[e];
@@ -436,12 +365,6 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       ksw0 = upper ? cur.ks.y : cur.ks.x;
       vsw0 = upper ? cur.vs.y : cur.vs.x;
     }
-    if constexpr (TB && GS) {
-      c1v[0] = dpp_from_lower8(c1v[0], c1v[2]);
-      c1v[1] = dpp_from_lower8(c1v[1], c1v[3]);
-      c2v[0] = dpp_from_lower8(c2v[0], c2v[2]);
-      c2v[1] = dpp_from_lower8(c2v[1], c2v[3]);
-    }
   }
   const h2_t ksh[2] = {as_h2(ksw0), as_h2(ksw1)};
   const h2_t vsh[2] = {as_h2(vsw0), as_h2(vsw1)};
@@ -454,11 +377,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
 #pragma unroll
     for (int e = 0; e < NT; ++e) {
       const float extra = BYP ? fmaf(gov[e], wc.gmul, wc.gc) : 0.0f;
-      if constexpr (GS)   // u_t = s_t (rt sqrt(sum_g 4^-e_g ||q_g||^2) + sum_g 2^-e_g ||q_g||_1 / 256)
-        cbv[e] = fmaf((float)ksh[e >> 1][e & 1],
-                      fmaf(wc.rtl, __builtin_amdgcn_sqrtf(fmaxf(c2v[e], 0.0f)), c1v[e]), extra);
-      else
-        cbv[e] = fmaf((float)ksh[e >> 1][e & 1], wc.ab2, extra);
+      cbv[e] = fmaf((float)ksh[e >> 1][e & 1], wc.ab2, extra);
     }
   }
   bool valid[NT];
@@ -487,7 +406,6 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     st.n *= alpha;
     st.nb *= alpha;
     st.wsum *= alpha;
-    if constexpr (GS) st.wsg *= alpha;
     if constexpr (VM) st.ev *= alpha;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -515,8 +433,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       const float alpha = __builtin_bit_cast(float, (uint32_t)(127 + st.ve - ve_new) << 23);   // 2^(ve - ve')
       st.ve = ve_new;
       st.wsum *= alpha;
-      if constexpr (GS) st.wsg *= alpha;
-#pragma unroll
+  #pragma unroll
       for (int j = 0; j < 8; ++j) {
         st.o1[j] *= alpha;
         st.o2[j] *= alpha;
@@ -558,12 +475,12 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     // the PV operand of head r takes tokens 4g+2, 4g+3 back from lane r + 8
     const uint32_t w01 = as_u32(h2_t{wh[0], wh[1]});
     wop = pack4(w01, dpp_from_upper8(w01));
-    if constexpr (KIND == WC_KIND_INT8_DITHER && !GS)
+    if constexpr (KIND == WC_KIND_INT8_DITHER)
       st.wsum = __builtin_amdgcn_fdot2(as_h2(w01), one, st.wsum, false);
   } else {
     const h2_t w01 = h2_t{wh[0], wh[1]}, w23 = h2_t{wh[NT - 2], wh[NT - 1]};
     wop = h4_t{wh[0], wh[1], wh[NT - 2], wh[NT - 1]};
-    if constexpr (KIND == WC_KIND_INT8_DITHER && !GS)
+    if constexpr (KIND == WC_KIND_INT8_DITHER)
       st.wsum = __builtin_amdgcn_fdot2(w23, one, __builtin_amdgcn_fdot2(w01, one, st.wsum, false), false);
   }
   // validity of tokens 4g .. 4g+3 (the k index of the PV operands)
@@ -583,37 +500,14 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&rows[1]);
     const uint32_t* r2 = reinterpret_cast<const uint32_t*>(&rows[2]);
     const uint32_t* r3 = reinterpret_cast<const uint32_t*>(&rows[3]);
-    // Group scales: channels 8r..8r+7 lie in group r/4; token 4g+t carries 2^-e_t of
-    // that group, entered through the exponent bytes of its operands (value codes:
-    // a per-token high byte; dither: the exponent field lowered by e_t).  The
-    // offsets are removed at the end with the per-group weight sums, one more
-    // product of the weights with 2^-e_{t,g} (rows 0..3 = groups).
-    uint32_t hie = 0x64646464u, sel_lo = kSelLo, sel_hi = kSelHi, dsub01 = 0, dsub23 = 0;
-    if constexpr (GS) {
-      const int sh = 4 * (r >> 2);
-      const uint32_t e0 = (cur.vge.x >> sh) & 15u, e1 = (cur.vge.x >> (16 + sh)) & 15u;
-      const uint32_t e2 = (cur.vge.y >> sh) & 15u, e3 = (cur.vge.y >> (16 + sh)) & 15u;
-      hie = 0x64646464u - 4u * (e0 | (e1 << 8) | (e2 << 16) | (e3 << 24));
-      sel_lo = 0x05010400u;   // bytes u0, E0, u1, E1
-      sel_hi = 0x07030602u;   // bytes u2, E2, u3, E3
-      dsub01 = (e0 << 10) | (e1 << 26);
-      dsub23 = (e2 << 10) | (e3 << 26);
-      uint32_t aw0 = 0, aw1 = 0;
-      if (r < 4) {
-        const int s4 = 4 * r;
-        aw0 = f16_pow2_neg((cur.vge.x >> s4) & 15u) | (f16_pow2_neg((cur.vge.x >> (16 + s4)) & 15u) << 16);
-        aw1 = f16_pow2_neg((cur.vge.y >> s4) & 15u) | (f16_pow2_neg((cur.vge.y >> (16 + s4)) & 15u) << 16);
-      }
-      st.wsg = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(aw0, aw1), wop, st.wsg, 0, 0, 0);
-    }
 #pragma unroll
     for (int jt = 0; jt < 8; ++jt) {
       const uint32_t x = cur.vw[jt];     // codes (excess-128) of channel 8r+jt, tokens 4g..4g+3
-      st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(perm(hie, x, sel_lo), perm(hie, x, sel_hi)), wop,
+      st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(ucodes2(x, kSelLo), ucodes2(x, kSelHi)), wop,
                                                         st.o1[jt], 0, 0, 0);
       const uint32_t sel = (jt & 1) ? kSelH1 : kSelH0;
-      const uint32_t d01 = perm(r1[jt >> 1], r0[jt >> 1], sel) - dsub01;
-      const uint32_t d23 = perm(r3[jt >> 1], r2[jt >> 1], sel) - dsub23;
+      const uint32_t d01 = perm(r1[jt >> 1], r0[jt >> 1], sel);
+      const uint32_t d23 = perm(r3[jt >> 1], r2[jt >> 1], sel);
       st.o2[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(d01, d23), wop, st.o2[jt], 0, 0, 0);
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);   // LDS reads done before the next page overwrites
@@ -721,20 +615,16 @@ __device__ __forceinline__ void step_write(const DecodeArgs& a, int b, int kv, i
   __syncthreads();
 }
 
-template <int KIND, bool METER, bool HALF, bool TB, bool BYP, bool VM, bool GS>
+template <int KIND, bool METER, bool HALF, bool TB, bool BYP, bool VM>
 __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
   __shared__ float qn_s[kWaves][16][16];
   __shared__ __attribute__((aligned(16))) float acc_s[kWaves][16][kD];
   __shared__ float ml_s[kWaves][16][6];
   __shared__ uint4 q_lds[16][17];   // the workgroup's queries, bf16 rows of 256 bytes (+16 pad)
-  // group scales: the fp16 B operands of the query products (4), the dither offset
-  // (1), the Tier-B group norms (2), the witness bound (1) and the bypassed pairs (2),
-  // the same in every wave: one copy in LDS instead of registers, read per page
-  __shared__ uint4 qop_s[GS ? 10 : 1][64];
   // a decode step's new token (plain Tier A caches, the variants the step call
   // fuses; the others keep their registers): its squared key residuals
-  constexpr bool kStep = METER && !TB && !BYP && !VM && !GS;
+  constexpr bool kStep = METER && !TB && !BYP && !VM;
   __shared__ double wr_s[kStep ? kD : 1];
   __shared__ int64_t wslot_s;
 
@@ -800,9 +690,9 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     nc = min(64, np - c0);
     if (c0 == 0 && pg0 == pg_spec && nc <= nc_spec) tv = tv_spec;   // the early request holds them
     else tv = lane < nc ? trow[pg0 + c0 + lane] : 0;
-    load_page<KIND, METER, TB, BYP, VM, GS>(a, blk_at(0), true, kv, r, g, wit_off, p0);
+    load_page<KIND, METER, TB, BYP, VM>(a, blk_at(0), true, kv, r, g, wit_off, p0);
     __builtin_amdgcn_sched_barrier(0);
-    load_page<KIND, METER, TB, BYP, VM, GS>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
+    load_page<KIND, METER, TB, BYP, VM>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
     __builtin_amdgcn_sched_barrier(0);
   };
   if (np > 0) start_chunk(0);
@@ -900,18 +790,6 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       wc.qop[kt] = pack8(w[0], w[1], w[2], w[3]);
     }
   }
-  wc.qoff = pack8(0, 0, 0, 0);
-  if constexpr (GS) {
-    // this lane group's channels are group g of head r: 2303/512 sum_{c in g} q_c,
-    // gathered into lane group 0 as fp16 hi (k 0..3) and lo (k 4..7) parts
-    const float x = kDOff * 0.001953125f * qsum;
-    _Float16 hi[4], lo[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) f16_split(__shfl(x, r + 16 * i, 64), hi[i], lo[i]);
-    if (g == 0)
-      wc.qoff = pack8(as_u32(h2_t{hi[0], hi[1]}), as_u32(h2_t{hi[2], hi[3]}), as_u32(h2_t{lo[0], lo[1]}),
-                      as_u32(h2_t{lo[2], lo[3]}));
-  }
   qsum += __shfl_xor(qsum, 16, 64);
   qsum += __shfl_xor(qsum, 32, 64);
   wc.s1_init = kDOff * qsum * 0.001953125f;
@@ -926,27 +804,6 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       const float x = bf16_to_f32((uint16_t)((qk[i >> 1] >> (16 * (i & 1))) & 0xFFFFu));
       sq = fmaf(x, x, sq);
       l1 += fabsf(x);
-    }
-    wc.qg1 = wc.qg2 = pack8(0, 0, 0, 0);
-    wc.rtl = 0.0f;
-    if constexpr (GS) {
-      // per group (this lane group's channels): sm log2(e) ||q_g||_1 / 256 and
-      // 2^-14 ||q_g||^2, gathered into lane group 0 in fp16 hi + lo parts
-      const float y1 = l1 * (a.sm_scale * kLog2e * (1.0f / 256.0f));
-      const float y2 = sq * 0x1p-14f;
-      _Float16 h1[4], l1h[4], h2[4], l2h[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f16_split(__shfl(y1, r + 16 * i, 64), h1[i], l1h[i]);
-        f16_split(__shfl(y2, r + 16 * i, 64), h2[i], l2h[i]);
-      }
-      if (g == 0) {
-        wc.qg1 = pack8(as_u32(h2_t{h1[0], h1[1]}), as_u32(h2_t{h1[2], h1[3]}), as_u32(h2_t{l1h[0], l1h[1]}),
-                       as_u32(h2_t{l1h[2], l1h[3]}));
-        wc.qg2 = pack8(as_u32(h2_t{h2[0], h2[1]}), as_u32(h2_t{h2[2], h2[3]}), as_u32(h2_t{l2h[0], l2h[1]}),
-                       as_u32(h2_t{l2h[2], l2h[3]}));
-      }
-      wc.rtl = a.sm_scale * kLog2e * sqrtf(2.0f * logf(2.0f * (float)L / a.tierb_delta) / 12.0f);
     }
     sq += __shfl_xor(sq, 16, 64);
     sq += __shfl_xor(sq, 32, 64);
@@ -1009,27 +866,6 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     wc.qnop = pack8(hw[0], hw[1], hw[2], hw[3]);
   }
 
-  wc.qsh = &qop_s[0][lane];
-  if constexpr (GS) {
-    if (wave == 0) {
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt) qop_s[kt][lane] = __builtin_bit_cast(uint4, wc.qop[kt]);
-      qop_s[4][lane] = __builtin_bit_cast(uint4, wc.qoff);
-      if constexpr (TB) {
-        qop_s[5][lane] = __builtin_bit_cast(uint4, wc.qg1);
-        qop_s[6][lane] = __builtin_bit_cast(uint4, wc.qg2);
-      }
-      qop_s[7][lane] = __builtin_bit_cast(uint4, wc.qnop);
-      if constexpr (BYP) {
-        qop_s[8][lane] = __builtin_bit_cast(uint4, wc.qo);
-        qop_s[9][lane] = __builtin_bit_cast(uint4, wc.qa);
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-  }
-
   WaveState st;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
@@ -1039,7 +875,6 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   st.m = -INFINITY;
   st.l = st.n = st.wsum = st.nb = 0.0f;
   st.ve = 0;
-  st.wsg = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
   st.ev = st.vmax = 0.0f;
   uint8_t* my_dsh = dsh[KIND == WC_KIND_INT8_DITHER ? wave : 0];
 
@@ -1071,21 +906,21 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     // assume the ring order may differ on the back edge and wait for every page.
     for (int j = 0; j < nc; j += 3) {
       set_priority(c0 + j);
-      load_page<KIND, METER, TB, BYP, VM, GS>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
+      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
       __builtin_amdgcn_sched_barrier(0);
       seg_check(tb + j * kBlockTokens);
-      process_page<KIND, METER, true, HALF, TB, BYP, VM, GS>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
-      load_page<KIND, METER, TB, BYP, VM, GS>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
+      process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 1 < nc) {
         seg_check(tb + (j + 1) * kBlockTokens);
-        process_page<KIND, METER, true, HALF, TB, BYP, VM, GS>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+        process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
       }
-      load_page<KIND, METER, TB, BYP, VM, GS>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
+      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 2 < nc) {
         seg_check(tb + (j + 2) * kBlockTokens);
-        process_page<KIND, METER, true, HALF, TB, BYP, VM, GS>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+        process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
       }
     }
     c0 += 64;
@@ -1094,9 +929,9 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __builtin_amdgcn_s_setprio(0);
   const int t_last = t_begin + np * kBlockTokens;
   if (t_last < t_end) {   // a partial last page: tokens from t_end on are masked
-    load_page<KIND, METER, TB, BYP, VM, GS>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
+    load_page<KIND, METER, TB, BYP, VM>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
     seg_check(t_last);
-    process_page<KIND, METER, false, HALF, TB, BYP, VM, GS>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
+    process_page<KIND, METER, false, HALF, TB, BYP, VM>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
   }
   if (rec_shares) {
     // the last segment, then the wave's unused slots (0 pages)
@@ -1109,7 +944,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   if constexpr (HALF) {   // lanes r and r + 8 hold different tokens of head r
     st.l += __shfl_xor(st.l, 8, 64);
     if constexpr (METER) st.n += __shfl_xor(st.n, 8, 64);
-    if constexpr (KIND == WC_KIND_INT8_DITHER && !GS) st.wsum += __shfl_xor(st.wsum, 8, 64);
+    if constexpr (KIND == WC_KIND_INT8_DITHER) st.wsum += __shfl_xor(st.wsum, 8, 64);
     if constexpr (VM) {
       st.ev += __shfl_xor(st.ev, 8, 64);
       st.vmax = fmaxf(st.vmax, __shfl_xor(st.vmax, 8, 64));
@@ -1127,17 +962,11 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     st.n += __shfl_xor(st.n, 16, 64);
     st.n += __shfl_xor(st.n, 32, 64);
   }
-  if constexpr (KIND == WC_KIND_INT8_DITHER && !GS) {
+  if constexpr (KIND == WC_KIND_INT8_DITHER) {
     st.wsum += __shfl_xor(st.wsum, 16, 64);
     st.wsum += __shfl_xor(st.wsum, 32, 64);
   }
-  // the weight sum that goes with this lane's output rows: group g (channels 32g..)
-  float wsum = st.wsum;
-  if constexpr (GS) {   // lane r (group row block 0) holds the sums of head r's groups
-    const float w0 = __shfl(st.wsg[0], r, 64), w1 = __shfl(st.wsg[1], r, 64);
-    const float w2 = __shfl(st.wsg[2], r, 64), w3 = __shfl(st.wsg[3], r, 64);
-    wsum = g == 0 ? w0 : (g == 1 ? w1 : (g == 2 ? w2 : w3));
-  }
+  const float wsum = st.wsum;
   // rows 4g+e of tile jt hold channel 8(4g+e)+jt = 32g + 8e + jt
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -1218,25 +1047,26 @@ bool step_write_fusable(const DecodeArgs& a) {
   // the kernel variants that carry the step write: Tier A over a cache without
   // bypassed pairs or group scales
   return a.use_mfma && mfma_decode_supported(a) && a.tierb_delta <= 0.0f && a.meter_v == nullptr &&
-         a.k_gexp == nullptr && a.n_pairs == 0;
+         a.n_pairs == 0;
 }
 
 bool mfma_decode_supported(const DecodeArgs& a) {
-  return a.head_dim == kD && a.q_dtype == WC_BF16 && a.group <= 16 &&
+  // (a group-scaled cache -- one fp16 scale per 32-channel group -- takes the vector path)
+  return a.head_dim == kD && a.q_dtype == WC_BF16 && a.group <= 16 && a.group_scales == 0 &&
          (a.kind == WC_KIND_BF16 || a.n_bands == 8 || a.n_bands == 16);
 }
 
-template <bool HALF, bool VM, bool GS>
+template <bool HALF, bool VM>
 void launch_decode_mfma_int8(const DecodeArgs& a, bool tb, bool byp, const dim3& grid, const dim3& block,
                              hipStream_t st) {
   if (tb && byp) {
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, true, VM, GS>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, true, VM>), grid, block, 0, st, a);
   } else if (tb) {
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, false, VM, GS>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, false, VM>), grid, block, 0, st, a);
   } else if (byp) {
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, true, VM, GS>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, true, VM>), grid, block, 0, st, a);
   } else {
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, false, VM, GS>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, false, VM>), grid, block, 0, st, a);
   }
 }
 
@@ -1245,13 +1075,11 @@ void launch_decode_mfma_g(const DecodeArgs& a, bool metered, bool tb, bool byp, 
                           const dim3& block, hipStream_t st) {
   if (!metered) {
     if constexpr (!VM)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, HALF, false, false, false, false>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, HALF, false, false, false>), grid, block, 0, st, a);
   } else if (a.kind == WC_KIND_FP8_RAW) {
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, HALF, false, false, VM, false>), grid, block, 0, st, a);
-  } else if (a.k_gexp != nullptr) {
-    launch_decode_mfma_int8<HALF, VM, true>(a, tb, byp, grid, block, st);
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, HALF, false, false, VM>), grid, block, 0, st, a);
   } else {
-    launch_decode_mfma_int8<HALF, VM, false>(a, tb, byp, grid, block, st);
+    launch_decode_mfma_int8<HALF, VM>(a, tb, byp, grid, block, st);
   }
 }
 

@@ -47,7 +47,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   __shared__ uint32_t xi_s[kT][D / 4];
   __shared__ float vs_s[kT];
   __shared__ float vr_s[kT], vn_s[kT];   // value side: stored ||vhat - v|| and ||v|| of the tile
-  __shared__ uint32_t ve_s[kT];           // group scales: the tile's value exponent words
+  __shared__ float vg_s[kT][D / 32];      // group scales: the tile's value group scales
   __shared__ float qg_s[kGMax][8];        // group scales, Tier B: ||q_g||^2 (0..3), ||q_g||_1 (4..7)
   __shared__ float alpha_s[kGMax];
   __shared__ int64_t slot_s[kT];
@@ -102,7 +102,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
     }
     __syncthreads();
   }
-  const bool grouped = KIND == WC_KIND_INT8_DITHER && a.k_gexp != nullptr;
+  const bool grouped = KIND == WC_KIND_INT8_DITHER && a.group_scales != 0;
   if constexpr (METER) {
     if (a.tierb_delta > 0.0f) {
       for (int h = tid; h < G; h += kThreads) {
@@ -193,15 +193,14 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
       if (valid) {
         if constexpr (KIND == WC_KIND_INT8_DITHER) {
           const uint8_t* kpg = reinterpret_cast<const uint8_t*>(a.k_data) + page * (kBlockTokens * D);
-          const float s = f16_to_f32(a.k_scale[page * kBlockTokens + off]);
-          const uint32_t kgw = grouped ? a.k_gexp[page * kBlockTokens + off] : 0u;
+          const int64_t srow = page * kBlockTokens + off;
 #pragma unroll
           for (int gi = 0; gi < NG; ++gi) {
             const uint4 cw = *reinterpret_cast<const uint4*>(kpg + kpage_off(off, c0 + 16 * gi, D, 1));
             const U4 r = dither_block(c0 / 16 + gi, slot, layer_head, a.key0, a.key1);
             const uint32_t codes[4] = {cw.x, cw.y, cw.z, cw.w};
             const uint32_t rw[4] = {r.x, r.y, r.z, r.w};
-            const float sg = s * group_step_factor(kgw, c0 + 16 * gi);   // the group's step (exact)
+            const float sg = scale_of(a.k_scale, srow, c0 + 16 * gi, D, grouped);   // the channels' step
 #pragma unroll
             for (int w4 = 0; w4 < 4; ++w4) {
               xi_s[i][(c0 + 16 * gi) / 4 + w4] = rw[w4];
@@ -213,10 +212,9 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
               }
             }
           }
-          if (part == 0) {
-            vs_s[i] = f16_to_f32(a.v_scale[page * kBlockTokens + off]);
-            ve_s[i] = grouped ? a.v_gexp[page * kBlockTokens + off] : 0u;
-          }
+          if (part == 0) vs_s[i] = grouped ? 1.0f : f16_to_f32(a.v_scale[srow]);   // (groups: per channel below)
+          if (grouped)
+            for (int gg = part; gg < D / 32; gg += 4) vg_s[i][gg] = f16_to_f32(a.v_scale[srow * (D / 32) + gg]);
         } else if constexpr (KIND == WC_KIND_FP8_RAW) {
           const uint8_t* kpg = reinterpret_cast<const uint8_t*>(a.k_data) + page * (kBlockTokens * D);
 #pragma unroll
@@ -246,6 +244,8 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         }
       } else if (part == 0) {
         vs_s[i] = 0.0f;
+        if (grouped)
+          for (int gg = 0; gg < D / 32; ++gg) vg_s[i][gg] = 0.0f;
       }
       if (vm && part == 0) {
         vr_s[i] = valid ? f16_to_f32(a.v_resid[page * kBlockTokens + off]) : 0.0f;
@@ -270,7 +270,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         if (part == 0) logit_s[h][i] = valid ? d * a.sm_scale : -INFINITY;
       }
       if (METER && a.tierb_delta > 0.0f) {   // Tier B: u_t = (alpha_h + beta_h) s_t, no witness
-        const float s = valid ? f16_to_f32(a.k_scale[page * kBlockTokens + off]) : 0.0f;
+        const float s = valid && !grouped ? f16_to_f32(a.k_scale[page * kBlockTokens + off]) : 0.0f;
         for (int h = 0; h < G; ++h) {
           // fp16 rounding bound of the bypassed channels: sm sum |q_c| (2^-11 |khat_c| + 2^-25)
           float gb = 0.0f;
@@ -282,10 +282,9 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
           gb += __shfl_xor(gb, 2, 4);
           if (part == 0) {
             if (grouped) {
-              const uint32_t kgw = valid ? a.k_gexp[page * kBlockTokens + off] : 0u;
               float s2 = 0.0f, s1 = 0.0f;
               for (int gg = 0; gg < D / 32; ++gg) {
-                const float sg = s * group_step_factor(kgw, 32 * gg);
+                const float sg = valid ? scale_of(a.k_scale, page * kBlockTokens + off, 32 * gg, D, true) : 0.0f;
                 s2 = fmaf(sg * sg, qg_s[h][gg], s2);
                 s1 = fmaf(sg, qg_s[h][4 + gg], s1);
               }
@@ -382,7 +381,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
             if constexpr (KIND == WC_KIND_INT8_DITHER) {
               const uint32_t u = (xi_s[i0 + j][c3 >> 2] >> (8 * (c3 & 3))) & 0xFFu;
               vv[j] = (float)((int32_t)byte - 128) - dither_value(u);   // excess-128 code
-              if (grouped) vv[j] *= group_step_factor(ve_s[i0 + j], c3);
+              if (grouped) vv[j] *= vg_s[i0 + j][c3 >> 5];
             } else {
               vv[j] = e4m3_to_f32(byte);
             }

@@ -258,12 +258,11 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
   __shared__ int8_t opos_s[D];           // stored-value position of a bypassed channel, else -1
   __shared__ double wq_s[GM][kRTile], wx_s[GM][kRTile];
   __shared__ uint32_t xi_s[kRTile][D / 16 * 4];
-  __shared__ float vs_s[kRTile];
+  __shared__ float vs_s[kRTile][4];      // value scale of each token and 32-channel group
   __shared__ int64_t slot_s[kRTile];
   __shared__ double dl_s[GM], dn_s[GM];
   __shared__ uint16_t ko_s[kRTile][32];  // stored fp16 values of the bypassed pairs (2m <= 32)
   __shared__ float qg_s[GM][8];          // group scales, Tier B: ||q_g||^2 (0..3), ||q_g||_1 (4..7)
-  __shared__ uint32_t ve_s[kRTile];      // group scales: value exponent words of the tile
   // logits and bounds of phases 1-2, then the output reduction of phase 3
   constexpr int kLogitBytes = 3 * GM * kRTile * 4;
   constexpr int kRedBytes = (NSUB > 1 ? NSUB - 1 : 1) * GM * D * 8;
@@ -325,7 +324,7 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
     qbn_s[h][bb] = sqrtf(acc) * a.sm_scale;
   }
   __syncthreads();
-  const bool grouped = a.k_gexp != nullptr;
+  const bool grouped = a.group_scales != 0;
   if (tierb && tid < G) {
     float sq = 0.0f, l1 = 0.0f;
     for (int c = 0; c < D; ++c) {
@@ -363,8 +362,7 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
     float dq[GM], dx[GM], cq[GM];
 #pragma unroll
     for (int h = 0; h < GM; ++h) dq[h] = dx[h] = cq[h] = 0.0f;
-    float s = 0.0f;
-    uint32_t kgw = 0;
+    float ksg[4] = {0.0f, 0.0f, 0.0f, 0.0f};   // key step of each 32-channel group of the token
     if (valid) {
       uint32_t kb[CH / 4];
       const int64_t kpage = row / kBlockTokens;   // (block, KV head) page
@@ -383,12 +381,10 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
         xb[4 * w] = x.x; xb[4 * w + 1] = x.y; xb[4 * w + 2] = x.z; xb[4 * w + 3] = x.w;
       }
       const bool int8 = a.kind == WC_KIND_INT8_DITHER;
-      if (int8) s = f16_to_f32(a.k_scale[row]);
-      if (part == 0) {
-        vs_s[i] = int8 ? f16_to_f32(a.v_scale[row]) : 1.0f;
-        ve_s[i] = grouped ? a.v_gexp[row] : 0u;
-      }
-      kgw = grouped ? a.k_gexp[row] : 0u;
+      if (int8)
+        for (int gg = 0; gg < D / 32; ++gg) ksg[gg] = scale_of(a.k_scale, row, 32 * gg, D, grouped);
+      if (part == 0)
+        for (int gg = 0; gg < D / 32; ++gg) vs_s[i][gg] = int8 ? scale_of(a.v_scale, row, 32 * gg, D, grouped) : 1.0f;
 #pragma unroll
       for (int gi = 0; gi < NG; ++gi) {
         uint32_t rw[4] = {0, 0, 0, 0};
@@ -404,7 +400,7 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
           for (int e = 0; e < 4; ++e) {
             const int c = 16 * gi + 4 * w4 + e;
             const uint32_t byte = (kb[c >> 2] >> (8 * (c & 3))) & 0xFFu;
-            const float sg = s * group_step_factor(kgw, c0 + c);
+            const float sg = ksg[(c0 + c) >> 5];
             float kq = int8 ? sg * ((float)((int32_t)byte - 128) - dither_value((rw[w4] >> (8 * e)) & 0xFFu))
                             : e4m3_to_f32(byte);
             const int op = m2 > 0 ? opos_s[c0 + c] : -1;
@@ -423,7 +419,7 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
         }
       }
     } else if (part == 0) {
-      vs_s[i] = 0.0f;
+      for (int gg = 0; gg < 4; ++gg) vs_s[i][gg] = 0.0f;
     }
     // Tier A: witness bound; Tier B: radius from the key scale (+ rounding of bypassed values)
     float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -460,13 +456,13 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
         if (tierb && grouped) {
           float s2 = 0.0f, s1 = 0.0f;
           for (int gg = 0; gg < D / 32; ++gg) {
-            const float sg = s * group_step_factor(kgw, 32 * gg);
+            const float sg = ksg[gg];
             s2 = fmaf(sg * sg, qg_s[h][gg], s2);
             s1 = fmaf(sg, qg_s[h][4 + gg], s1);
           }
           cb_s[h][i] = a.sm_scale * (fmaf(rt, sqrtf(s2), s1 * (1.0f / 256.0f))) + cp;
         } else {
-          cb_s[h][i] = tierb ? fmaf(ab_s[h], s, cp) : cp;
+          cb_s[h][i] = tierb ? fmaf(ab_s[h], ksg[0], cp) : cp;
         }
       }
     }
@@ -540,8 +536,7 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
         float vq;
         if (a.kind == WC_KIND_INT8_DITHER) {
           const uint32_t xw = xi_s[i][c >> 2];
-          vq = vs_s[i] * group_step_factor(ve_s[i], c) *
-               ((float)((int32_t)byte - 128) - dither_value((xw >> (8 * (c & 3))) & 0xFFu));
+          vq = vs_s[i][c >> 5] * ((float)((int32_t)byte - 128) - dither_value((xw >> (8 * (c & 3))) & 0xFFu));
         } else {
           vq = e4m3_to_f32(byte);
         }

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "../../include/witcert.h"
+#include "wc_device.h"
 
 namespace wc {
 
@@ -28,8 +29,7 @@ struct WriteArgs {
   uint16_t* k_outlier;      // [blocks][n_kv][16][2 n_pairs] fp16
   uint16_t* v_resid;        // value side (or null): ||vhat - v|| fp16 up, [blocks][n_kv][16]
   uint16_t* v_norm;         // ||v|| fp16 down, same layout
-  uint16_t* k_gexp;         // group scales (or null): 4-bit exponent per 32-channel group,
-  uint16_t* v_gexp;         // [blocks][n_kv][16]
+  int group_scales;         // k_scale / v_scale hold one fp16 scale per 32-channel group
 };
 
 struct SelectArgs {
@@ -91,19 +91,19 @@ struct DecodeArgs {
   const uint16_t* v_norm;
   float* meter_v;           // [batch][n_q]
   float gate_tau_v;
-  // group scales (null: one scale per token): exponent e_g of channel group g in
-  // bits 4g..4g+3, the group's step s * 2^-e_g
-  const uint16_t* k_gexp;
-  const uint16_t* v_gexp;
+  // k_scale / v_scale hold one fp16 scale per 32-channel group ([..][16][D/32]),
+  // else one per token
+  int group_scales;
   // a decode step's new tokens (one per sequence, its last): written by the
   // matrix-core decode before it reads them (step_write != 0), else nothing
   WriteArgs sw;
   int step_write;
 };
 
-// 2^-e_g of channel c's group from a token's exponent word (exact).
-__device__ __forceinline__ float group_step_factor(uint32_t gexp, int c) {
-  return ldexpf(1.0f, -(int)((gexp >> (4 * (c >> 5))) & 15u));
+// Scale of channel c of the token in scale row `row` (page * 16 + offset): the
+// token's, or with group scales that of its 32-channel group.
+__device__ __forceinline__ float scale_of(const uint16_t* sc, int64_t row, int c, int D, bool grouped) {
+  return f16_to_f32(grouped ? sc[row * (D / 32) + (c >> 5)] : sc[row]);
 }
 
 // Channel of member `second` of RoPE pair j (pair index clamped into range).

@@ -116,33 +116,25 @@ __device__ __forceinline__ int64_t write_token_head(const WriteArgs& a, int64_t 
       if (((bmask >> i) & 1u) == 0) ak = fmaxf(ak, fabsf(k[i]));
       av = fmaxf(av, fabsf(v[i]));
     }
-    // group scales (Sec. 6.2 storage side): the 32-channel group of this lane is
-    // lanes g, g^1; its exponent is the largest e <= 14 with amax_g 2^e <= amax
-    // (2^-e and every code times 2^-e stay normal fp16 numbers)
-    const bool grouped = a.k_gexp != nullptr;
-    float akg = 0.0f, avg = 0.0f;
+    // group scales (Sec. 6.2 storage side, Table 4): the 32-channel group of this
+    // lane is lanes g, g^1, and its fp16 scale is formed from the group's amax as the
+    // token scale is from the token's
+    const bool grouped = a.group_scales != 0;
     if (grouped) {
-      akg = fmaxf(ak, __shfl_xor(ak, 1, LPT));
-      avg = fmaxf(av, __shfl_xor(av, 1, LPT));
-    }
+      ak = fmaxf(ak, __shfl_xor(ak, 1, LPT));
+      av = fmaxf(av, __shfl_xor(av, 1, LPT));
+    } else {
 #pragma unroll
-    for (int o = 1; o < LPT; o <<= 1) {
-      ak = fmaxf(ak, __shfl_xor(ak, o, LPT));
-      av = fmaxf(av, __shfl_xor(av, o, LPT));
-    }
-    int ek = 0, ev = 0;
-    if (grouped) {
-      while (ek < 14 && ldexpf(akg, ek + 1) <= ak) ++ek;
-      while (ev < 14 && ldexpf(avg, ev + 1) <= av) ++ev;
+      for (int o = 1; o < LPT; o <<= 1) {
+        ak = fmaxf(ak, __shfl_xor(ak, o, LPT));
+        av = fmaxf(av, __shfl_xor(av, o, LPT));
+      }
     }
     uint16_t skb, svb;
     float sk, ikk, sv, ivv;
     int8_scale(ak, skb, sk, ikk);
     int8_scale(av, svb, sv, ivv);
-    ikk = ldexpf(ikk, ek);                       // fl32(1/s) 2^e_g: exact
-    ivv = ldexpf(ivv, ev);
-    const double stk = ldexp((double)sk, -ek);   // the group's step s 2^-e_g
-    const double stv = ldexp((double)sv, -ev);
+    const double stk = (double)sk, stv = (double)sv;
 
     const U4 rnd = dither_block(g, slot, ((uint32_t)a.layer << 16) | (uint32_t)h, a.key0, a.key1);
     const uint32_t words[4] = {rnd.x, rnd.y, rnd.z, rnd.w};
@@ -155,7 +147,7 @@ __device__ __forceinline__ int64_t write_token_head(const WriteArgs& a, int64_t 
       const float ck = rintf(__fadd_rn(__fmul_rn(byp ? 0.0f : k[i], ikk), xi));
       const float cv = rintf(__fadd_rn(__fmul_rn(v[i], ivv), xi));
       const double rk = byp ? (double)(float)(_Float16)k[i] - (double)k[i]     // fp16(k) - k
-                            : stk * (double)(ck - xi) - (double)k[i];          // khat - k
+                            : stk * (double)(ck - xi) - (double)k[i];          // khat - k (step of the group)
       r2row[16 * g + i] = rk * rk;
       const double rv = stv * (double)(cv - xi) - (double)v[i];                // vhat - v
       vr2 = fma(rv, rv, vr2);
@@ -166,27 +158,17 @@ __device__ __forceinline__ int64_t write_token_head(const WriteArgs& a, int64_t 
         reinterpret_cast<uint8_t*>(a.v_data)[bh * (kBlockTokens * D) + vpage_off(off, 16 * g + i, D, 1)] =
             (uint8_t)((int32_t)cv + 128);
     }
-    // group exponents of the token-head: nibble g/2 from the first lane of each group
-    uint32_t ekw = 0, evw = 0;
-    if (grouped) {
-      ekw = (g & 1) ? 0u : (uint32_t)ek << (4 * (g >> 1));
-      evw = (g & 1) ? 0u : (uint32_t)ev << (4 * (g >> 1));
-#pragma unroll
-      for (int o = 1; o < LPT; o <<= 1) {
-        ekw |= __shfl_xor(ekw, o, LPT);
-        evw |= __shfl_xor(evw, o, LPT);
-      }
-    }
     if (active) {
       *reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(a.k_data) + bh * (kBlockTokens * D) +
                                 kpage_off(off, 16 * g, D, 1)) = make_uint4(kc[0], kc[1], kc[2], kc[3]);
-      if (g == 0) {
+      if (grouped) {   // the first lane of each group stores the group's scales
+        if ((g & 1) == 0) {
+          a.k_scale[(bh * kBlockTokens + off) * (D / 32) + (g >> 1)] = skb;
+          a.v_scale[(bh * kBlockTokens + off) * (D / 32) + (g >> 1)] = svb;
+        }
+      } else if (g == 0) {
         a.k_scale[bh * kBlockTokens + off] = skb;
         a.v_scale[bh * kBlockTokens + off] = svb;
-        if (grouped) {
-          a.k_gexp[bh * kBlockTokens + off] = (uint16_t)ekw;
-          a.v_gexp[bh * kBlockTokens + off] = (uint16_t)evw;
-        }
       }
       if (bmask != 0) {
         // fp16 (nearest-even) values of the bypassed channels, in pair order

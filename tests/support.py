@@ -52,7 +52,7 @@ def case_pairs(case, m):
 def gpu_cache(case, kind, seed=None, pairs=None, value_side=False, group_scales=False):
     """Write every sequence of the case into a fresh GPU cache through wc_quantize_write
     (pairs [n_kv, m]: bypassed RoPE pairs of the keys; value_side: store the value
-    residual and value norms; group_scales: per-32-channel group exponents)."""
+    residual and value norms; group_scales: one fp16 scale per 32-channel group)."""
     import torch
 
     import paper_2607_28699_amd as wc
@@ -134,7 +134,7 @@ def read_cache(cache, slots):
     if cache.kind == "int8_dither":   # stored excess-128
         out["k"] = out["k"].astype(np.int16) - 128
         out["v"] = out["v"].astype(np.int16) - 128
-    if t["k_scale"] is not None:
+    if t["k_scale"] is not None:   # [n, n_kv], or with group scales [n, n_kv, d/32]
         out["ks"] = ofp_f16(t["k_scale"].numpy()[blk, :, off])
         out["vs"] = ofp_f16(t["v_scale"].numpy()[blk, :, off])
     if t["k_witness"] is not None:
@@ -144,11 +144,6 @@ def read_cache(cache, slots):
     if t.get("v_resid") is not None:
         out["vr"] = ofp_f16(t["v_resid"].numpy()[blk, :, off])
         out["vn"] = ofp_f16(t["v_norm"].numpy()[blk, :, off])
-    if t.get("k_gexp") is not None:   # group exponents: 4 bits per 32-channel group
-        ng = cache.head_dim // 32
-        for name, key in (("k_gexp", "ke"), ("v_gexp", "ve")):
-            w = t[name].numpy().view(np.uint16)[blk, :, off].astype(np.int64)
-            out[key] = np.stack([(w >> (4 * g)) & 15 for g in range(ng)], axis=-1)
     return out
 
 

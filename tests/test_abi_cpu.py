@@ -39,11 +39,11 @@ def test_status_strings_and_version(L):
 
 
 def test_cache_byte_account(L):
-    sizes = (ctypes.c_size_t * 10)()
+    sizes = (ctypes.c_size_t * 8)()
     # one KV head, 32768 tokens, d = 128, B = 8: 128 + 128 + 2 + 2 + 16 = 276 B per token
     tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, 0, 0, sizes)
     assert tot == 32768 * 276
-    assert list(sizes) == [32768 * 128, 32768 * 128, 65536, 65536, 32768 * 16, 0, 0, 0, 0, 0]
+    assert list(sizes) == [32768 * 128, 32768 * 128, 65536, 65536, 32768 * 16, 0, 0, 0]
     assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, 0, 0, sizes) == 32768 * 272
     assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, 0, 0, 0, sizes) == 32768 * 512
     assert L.wc_cache_bytes(7, 1, 1, 128, 8, 0, 0, 0, sizes) == 0
@@ -59,10 +59,11 @@ def test_cache_byte_account(L):
     assert tot == 32768 * 280 and sizes[6] == sizes[7] == 65536
     assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, 1, 0, sizes) == 32768 * 276
     assert L.wc_cache_bytes(_lib.WC_KIND_BF16, 2048, 1, 128, 0, 0, 1, 0, sizes) == 0
-    # group scales: one 16-bit exponent word (4 bits per 32-channel group) per token-head
-    # and tensor, INT8 only (Table 4: the paper's fp16 group scales would be 8 + 8 bytes)
+    # group scales: one fp16 scale per 32-channel group and tensor, INT8 only: K + V
+    # take 272 bytes per token-head (Table 4), 288 with the 16-byte key witness
     tot = L.wc_cache_bytes(_lib.WC_KIND_INT8_DITHER, 2048, 1, 128, 8, 0, 0, 1, sizes)
-    assert tot == 32768 * 280 and sizes[8] == sizes[9] == 65536
+    assert tot == 32768 * 288 and sizes[2] == sizes[3] == 32768 * 8
+    assert sizes[0] + sizes[1] + sizes[2] + sizes[3] == 32768 * 272
     assert L.wc_cache_bytes(_lib.WC_KIND_FP8_RAW, 2048, 1, 128, 8, 0, 0, 1, sizes) == 0
 
 
@@ -142,17 +143,14 @@ def test_split_tokens_query(L):
 
 
 def test_group_scale_and_repair_argument_checks(L):
-    # group exponents: both arrays or neither, INT8 only, 16-byte aligned
-    c = _lib.WcCache(0, 128, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16, 0, 0, None, None, None, None, 16, None)
+    # group scales: a flag of 0 or 1, INT8 only
+    c = _lib.WcCache(0, 128, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16, 0, 2, None, None, None, None)
     assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
-    c.v_gexp = 24
-    assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
-    c.v_gexp, c.kind = 16, _lib.WC_KIND_FP8_RAW
+    c.group_scales, c.kind = 1, _lib.WC_KIND_FP8_RAW
     assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 1, None) == _lib.WC_EINVAL
     c.kind = _lib.WC_KIND_INT8_DITHER
     assert L.wc_quantize_write(ctypes.byref(c), 16, 16, 0, 16, 0, None) == _lib.WC_OK   # no tokens
     # repair workspace: a 1 KB header and one record of G (d + 2) doubles per
-    # (candidate block, 64-token tile) for every (sequence, KV head)
     # (candidate block, 64-token tile) for every (sequence, KV head); blocks are
     # fixed 256-token runs, so four tiles each
     unit = 1024 + 64 * 4 * 7 * 130 * 8
@@ -160,7 +158,7 @@ def test_group_scale_and_repair_argument_checks(L):
     assert L.wc_block_repair_workspace_size(4, 28, 4, 128, 65) == 0
     assert L.wc_block_repair_workspace_size(4, 27, 4, 128, 8) == 0
     ex = _lib.WcCache(_lib.WC_KIND_BF16, 128, 1, 0, 0, 0, 1, 0, 16, 16)
-    c.k_gexp = c.v_gexp = None
+    c.group_scales = 0
 
     def rep(max_rep, rws, rws_bytes):
         return L.wc_block_repair(ctypes.byref(c), ctypes.byref(ex), 16, 1, 1, 7, 16, 4, 16, 64, 0.1, 0, 0.0,

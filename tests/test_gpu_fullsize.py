@@ -205,11 +205,11 @@ def test_fullsize_bypass_group_scales():
         qb = q[b, h:h + 1].float().cpu().numpy().astype(np.float64)
         chans = obp.bypass_channels(ref_pairs[g], wl.d, wl.rope_layout)
         xi = oph.dither_values(sl, wl.d, layer, g, wl.philox_seed())
-        kc, ks, ke, ko, kh = ogs.quantize(kb, xi, chans)
-        vc, vs, ve, _, vh = ogs.quantize(vb, xi)
+        kc, ks, ko, kh = ogs.quantize(kb, xi, chans)
+        vc, vs, _, vh = ogs.quantize(vb, xi)
         kw = oq.witness(kb, kh, wl.bands, wl.rope_layout)
         ra = odec.metered_decode(qb, kh[:, None], vh[:, None], kw[:, None], sm, wl.bands, wl.rope_layout)
-        rb = ogs.tierb_decode(qb, kh[:, None], vh[:, None], ks[:, None], ke[:, None], sm, dloc, ko[:, None],
+        rb = ogs.tierb_decode(qb, kh[:, None], vh[:, None], ks[:, None], sm, dloc, ko[:, None],
                               chans[None])
         tv = odec.true_tv(qb, kb[:, None], kh[:, None], sm)
         j = ov.joint_decode(qb, kh[:, None], vh[:, None], ra["c"], ov.value_residual(vb[:, None], vh[:, None]),
@@ -223,5 +223,4 @@ def test_fullsize_bypass_group_scales():
         got = S.read_cache(cache, sl[pick])
         assert np.array_equal(got["k"][:, g].astype(np.int64), kc[pick])
         assert np.array_equal(got["v"][:, g].astype(np.int64), vc[pick])
-        assert np.array_equal(got["ke"][:, g], ke[pick]) and np.array_equal(got["ve"][:, g], ve[pick])
-        assert np.array_equal(got["ks"][:, g], ks[pick])
+        assert np.array_equal(got["ks"][:, g], ks[pick]) and np.array_equal(got["vs"][:, g], vs[pick])

@@ -1,10 +1,11 @@
 """GPU parity of the per-token 32-channel group scales (Sec. 6.2 storage side,
-Table 4 granularity) against the oracle.
+Table 4: one fp16 scale per token and group) against the oracle.
 
-* write path: codes, token scales, group exponents, witness, bypassed values and the
-  value side bit-exact, both RoPE layouts, d = 64 and 128;
-* decode: Tier A (witness), Tier B (radius over the group steps) and the joint
-  K + V gate: outputs within 1e-5 (fp32 workloads) / 2e-3 (bf16) of the oracle, raw
+* write path: codes, group scales, witness, bypassed values and the value side
+  bit-exact, both RoPE layouts, d = 64 and 128;
+* decode (a group-scaled cache runs on the vector ALUs): Tier A (witness), Tier B
+  (radius over the group steps) and the joint K + V gate: outputs within 1e-5 (fp32
+  workloads) / 2e-3 (bf16) of the oracle, raw
   relative, the meter never below the true TV, the gate bit-exact;
 * block repair over a group-scaled cache against the oracle's repaired state.
 """
@@ -59,12 +60,11 @@ def test_groupscale_write_bitexact(name, wl, lens, m, layout):
         assert np.array_equal(got["k"].astype(np.int64), r["kcode"])
         assert np.array_equal(got["v"].astype(np.int64), r["vcode"])
         assert np.array_equal(got["ks"], r["ks"]) and np.array_equal(got["vs"], r["vs"])
-        assert np.array_equal(got["ke"], r["ke"]) and np.array_equal(got["ve"], r["ve"])
         assert np.array_equal(got["kw"], r["kw"])
         assert np.array_equal(got["vr"], r["vr"]) and np.array_equal(got["vn"], r["vn"])
         if m:
             assert np.array_equal(got["ko"], r["ko"])
-        n_grouped += int(np.sum(r["ke"] > 0))
+        n_grouped += int(np.sum(r["ks"].max(axis=-1) != r["ks"].min(axis=-1)))   # groups differ
     assert n_grouped > 0
 
 
@@ -121,7 +121,7 @@ def test_groupscale_decode_parity(name, wl, lens, m, tier, path, joint):
             base = odec.metered_decode(q, c["khat"], c["vhat"], c["kw"], sm, wl.bands, wl.rope_layout)
             cb = base["c"]
         else:
-            base = ogs.tierb_decode(q, c["khat"], c["vhat"], c["ks"], c["ke"], sm, DLOC,
+            base = ogs.tierb_decode(q, c["khat"], c["vhat"], c["ks"], sm, DLOC,
                                     c.get("ko"), c.get("chans"))
             cb = base["u"]
         j = ov.joint_decode(q, c["khat"], c["vhat"], cb, c["vr"], c["vn"], sm)
