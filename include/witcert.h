@@ -25,6 +25,9 @@
  *                                   the routed heads (the fallback of the meter loop)
  *               wc_block_repair     repair of routed heads from the exact cache at block
  *                                   granularity (Sec. 6.3)
+ *               wc_repair_write_back
+ *                                   persistent repair: repaired pages are served from the
+ *                                   exact cache by every later decode (Sec. 6, Sec. 6.3)
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are DEVICE pointers owned by the caller; the library
@@ -133,6 +136,20 @@ extern "C" {
  * channels (bypassed channels leave amax_g), stored in k_scale / v_scale in place
  * of the token scale; codes use fl32(1/s_g).  The decode of a group-scaled cache
  * runs on the vector ALUs.
+ *
+ * Persistent repair (quantized kinds; the meter loop's gate, Sec. 6: page in,
+ * recompute, write back, zero the witness; Sec. 6.3 gated evaluation (c): repaired
+ * slots are paged in once and filtered out afterwards): repaired[blk * n_kv_heads +
+ * h] != 0 marks page blk of KV head h as served from the exact store, whose bf16
+ * pages (the k_data / v_data of a WC_KIND_BF16 cache with the same num_blocks,
+ * n_kv_heads and head_dim, written by wc_quantize_write_pair) are exact_k /
+ * exact_v.  Every decode of the cache reads a marked page's keys and values from
+ * the exact store with bound 0 (no witness, no radius, no value residual), for
+ * every token of the page, also tokens written after the mark; block repair ranks
+ * only blocks that hold an unmarked token.  wc_repair_write_back sets the marks
+ * (and zeroes the marked slots' witness); the caller allocates the array (one
+ * byte per page and KV head) and zeroes it with the cache.  With repaired NULL,
+ * exact_k and exact_v are ignored.
  */
 typedef struct wc_cache {
     int32_t  kind;          /* WC_KIND_*                                       */
@@ -149,6 +166,8 @@ typedef struct wc_cache {
     const int32_t* outlier_pairs;      /* [n_kv_heads][m] device, or NULL when m == 0  */
     void*    k_outlier;                /* see above, or NULL when m == 0               */
     void    *v_resid, *v_norm;          /* value side, or both NULL                     */
+    uint8_t* repaired;                 /* persistent repair marks, or NULL (see below)  */
+    const void *exact_k, *exact_v;     /* the exact store's k_data / v_data, with marks */
 } wc_cache;
 
 const char* wc_strerror(int status);
@@ -401,7 +420,8 @@ int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int 
  *   share_{h,i} = sum_{t in i} ptilde_{h,t} (e^{c_{h,t}} - 1) (they add up to A_h - 1),
  *   from the block segments the decode recorded in its workspace,
  *   taken in decreasing order of sum_h share_{h,i} (ties to the lower i), at most
- *   max_repair_blocks (1 .. 64) of them;
+ *   max_repair_blocks (1 .. 64) of them, among the blocks that hold a position not
+ *   yet marked as repaired (cache->repaired; all blocks without marks);
  *   a taken block contributes exact logits and values (from the bf16 cache `exact`)
  *   with bound 0; after each block A_h is recomputed, and the repair stops as soon
  *   as every query head h of the KV head passes: (tau < 1 ? meter : raw) <= tau.
@@ -431,6 +451,25 @@ int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q,
  */
 size_t wc_block_repair_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
                                       int max_repair_blocks);
+
+/*
+ * Write-back of a repair (the meter loop's gate, Sec. 6; incremental persistent
+ * repair, Sec. 6.3 gated evaluation (c)): marks pages of cache->repaired and zeroes
+ * the witness of their slots (when the cache has one), so that every later decode
+ * serves them from the exact store with bound 0.  For every (b, g) of the batch:
+ *   n_repaired[b][g] > 0: the pages holding positions 0 .. seq_lens[b]-1 of the
+ *     blocks repaired_blocks[b][g][0 .. n-1] (256-token blocks, block i = positions
+ *     256i .. 256i+255, as wc_block_repair reports them in `repaired`);
+ *   whole_kv != NULL and whole_kv[b][g] != 0 (a KV head served by the whole-head
+ *     fallback): every page holding positions 0 .. seq_lens[b]-1.
+ * Block ids outside [0, 4096), table entries outside the cache and positions past
+ * max_blocks_per_seq * 16 are skipped.  n_repaired may be NULL (then only
+ * whole_kv counts).  cache->repaired must be set.
+ */
+int wc_repair_write_back(const wc_cache* cache, int batch, const int32_t* block_table,
+                         int max_blocks_per_seq, const int32_t* seq_lens, const int32_t* repaired_blocks,
+                         const int32_t* n_repaired, int max_repair_blocks, const uint8_t* whole_kv,
+                         void* stream);
 
 /*
  * Gate (the meter loop's gate, Sec. 6; certified vs risk-ranked, Sec. 4.3):

@@ -22,6 +22,7 @@ from .api import (  # noqa: F401
     quantize_write,
     quantize_write_pair,
     repair_workspace,
+    repair_write_back,
     select_outlier_pairs,
     split_tokens_for,
     tierb_decode_attention,

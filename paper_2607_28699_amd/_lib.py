@@ -24,6 +24,7 @@ EXPORTS = (
     "wc_metered_decode_gate", "wc_step_metered_decode_gate", "wc_step_metered_decode_gate_noalloc",
     "wc_tierb_decode_attention", "wc_tierb_delta_loc", "wc_joint_decode_gate", "wc_gate",
     "wc_exact_decode_attention", "wc_block_repair", "wc_block_repair_workspace_size",
+    "wc_repair_write_back",
 )
 
 
@@ -37,6 +38,7 @@ class WcCache(ctypes.Structure):
         ("n_outlier_pairs", ctypes.c_int32), ("group_scales", ctypes.c_int32),
         ("outlier_pairs", ctypes.c_void_p), ("k_outlier", ctypes.c_void_p),
         ("v_resid", ctypes.c_void_p), ("v_norm", ctypes.c_void_p),
+        ("repaired", ctypes.c_void_p), ("exact_k", ctypes.c_void_p), ("exact_v", ctypes.c_void_p),
     ]
 
 
@@ -105,6 +107,8 @@ def lib() -> ctypes.CDLL:
                                            vp, sz, vp]),
         "wc_block_repair_workspace_size": (sz, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                                 ctypes.c_int]),
+        "wc_repair_write_back": (ctypes.c_int, [cp, ctypes.c_int, vp, ctypes.c_int, vp, vp, vp, ctypes.c_int,
+                                                vp, vp]),
         "wc_gate": (ctypes.c_int, [vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, f32, vp, vp,
                                    vp, vp]),
         "wc_exact_decode_attention": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int,

@@ -67,6 +67,7 @@ class PagedCache:
     value_side: bool = False
     group_scales: bool = False
     tensors: dict = field(default_factory=dict)
+    exact_store: object = None   # persistent repair: the bf16 PagedCache of marked pages
 
     def __post_init__(self):
         m = self.n_outlier_pairs
@@ -112,14 +113,28 @@ class PagedCache:
             raise _lib.WitCertError("outlier pairs do not match the cache")
         t.copy_(pairs.to(device=t.device, dtype=torch.int32))
 
+    def enable_repair(self, exact: "PagedCache") -> None:
+        """Persistent repair: repair marks (one byte per page and KV head, all 0) and
+        `exact` (the bf16 cache written by quantize_write_pair) as the exact store of
+        marked pages."""
+        if exact.kind != "bf16" or (exact.n_kv, exact.head_dim) != (self.n_kv, self.head_dim) or \
+                exact.num_blocks < self.num_blocks:
+            raise _lib.WitCertError("the exact store does not match the cache")
+        self.tensors["repaired"] = torch.zeros((self.num_blocks, self.n_kv), dtype=torch.uint8,
+                                               device=self.device)
+        self.exact_store = exact
+
     def struct(self) -> WcCache:
         t = self.tensors
+        ex = self.exact_store
         return WcCache(KINDS[self.kind], self.head_dim, self.n_kv, self.n_bands,
                        LAYOUTS[self.rope_layout], self.layer, self.num_blocks, self.seed,
                        _ptr(t["k_data"]), _ptr(t["v_data"]), _ptr(t["k_scale"]),
                        _ptr(t["v_scale"]), _ptr(t["k_witness"]), self.n_outlier_pairs,
                        1 if self.group_scales else 0, _ptr(t["outlier_pairs"]), _ptr(t["k_outlier"]),
-                       _ptr(t["v_resid"]), _ptr(t["v_norm"]))
+                       _ptr(t["v_resid"]), _ptr(t["v_norm"]), _ptr(t.get("repaired")),
+                       _ptr(ex.tensors["k_data"]) if ex is not None else None,
+                       _ptr(ex.tensors["v_data"]) if ex is not None else None)
 
 
 def quantize_write(cache: PagedCache, k: torch.Tensor, v: torch.Tensor, slots: torch.Tensor) -> None:
@@ -367,6 +382,21 @@ def block_repair(cache: PagedCache, exact: PagedCache, q: torch.Tensor, block_ta
         repair_ws.numel(), _stream()),
         "wc_block_repair")
     return n_repaired, repaired
+
+
+def repair_write_back(cache: PagedCache, block_table: torch.Tensor, seq_lens: torch.Tensor,
+                      repaired: torch.Tensor | None = None, n_repaired: torch.Tensor | None = None,
+                      whole_kv: torch.Tensor | None = None) -> None:
+    """Persistent repair: mark the pages of the blocks block_repair took (repaired
+    [batch, n_kv, max_blocks], n_repaired [batch, n_kv]) and of the KV heads served by
+    the whole-head fallback (whole_kv [batch, n_kv] uint8), zeroing their witness."""
+    _dev_check(block_table, seq_lens)
+    batch = seq_lens.shape[0]
+    c = cache.struct()
+    mb = repaired.shape[2] if repaired is not None else 0
+    check(lib().wc_repair_write_back(ctypes.byref(c), batch, _ptr(block_table), block_table.shape[1],
+                                     _ptr(seq_lens), _ptr(repaired), _ptr(n_repaired), mb, _ptr(whole_kv),
+                                     _stream()), "wc_repair_write_back")
 
 
 def repair_workspace(batch: int, n_q: int, n_kv: int, head_dim: int, max_blocks: int = 16,

@@ -43,6 +43,10 @@ int check_cache(const wc_cache* c, bool need_witness, bool witness_optional = fa
       (c->kind == WC_KIND_BF16 || !aligned16(c->v_resid) || !aligned16(c->v_norm)))
     return WC_EINVAL;
   if (c->group_scales != 0 && (c->group_scales != 1 || c->kind != WC_KIND_INT8_DITHER)) return WC_EINVAL;
+  // persistent repair marks: quantized kinds, with the exact store's pages
+  if (c->repaired != nullptr &&
+      (c->kind == WC_KIND_BF16 || !c->exact_k || !c->exact_v || !aligned16(c->exact_k) || !aligned16(c->exact_v)))
+    return WC_EINVAL;
   return WC_OK;
 }
 
@@ -87,7 +91,7 @@ const char* wc_strerror(int status) {
   }
 }
 
-int wc_version(void) { return 102; }   // 1.2: wc_step_metered_decode_gate_noalloc
+int wc_version(void) { return 103; }   // 1.3: persistent repair (marks, wc_repair_write_back)
 
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim, int n_bands,
                       int n_outlier_pairs, int value_side, int group_scales, size_t sizes[8]) {
@@ -304,6 +308,9 @@ static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int 
   a.v_resid = static_cast<const uint16_t*>(cache->v_resid);
   a.v_norm = static_cast<const uint16_t*>(cache->v_norm);
   a.group_scales = cache->group_scales;
+  a.repaired = cache->repaired;
+  a.x_k_data = cache->repaired ? cache->exact_k : nullptr;
+  a.x_v_data = cache->repaired ? cache->exact_v : nullptr;
   // WITCERT_FORCE_VALU=1 selects the vector-ALU kernels even where the
   // matrix-core ones apply (used to cross-check the two paths)
   const char* force = getenv("WITCERT_FORCE_VALU");
@@ -499,6 +506,9 @@ int wc_block_repair(const wc_cache* cache, const wc_cache* exact, const void* q,
     return WC_EINVAL;
   if (tierb && (cache->kind != WC_KIND_INT8_DITHER || !(delta_loc > 0.0f && delta_loc < 1.0f)))
     return WC_EINVAL;
+  // the marked pages were served from the cache's exact store: the same cache here
+  if (cache->repaired != nullptr && (cache->exact_k != exact->k_data || cache->exact_v != exact->v_data))
+    return WC_EINVAL;
   if (!(tau >= 0.0f) || max_repair_blocks < 1 || max_repair_blocks > 64) return WC_EINVAL;
   if (batch > 0 && (!meter || !mask_kv)) return WC_EINVAL;
   wc::DecodeArgs a{};
@@ -546,6 +556,35 @@ size_t wc_block_repair_workspace_size(int batch, int n_q_heads, int n_kv_heads, 
                                             wc::kRepairTiles);
   const size_t total = (size_t)batch * n_kv_heads * unit;
   return total > 0 ? total : 256;
+}
+
+int wc_repair_write_back(const wc_cache* cache, int batch, const int32_t* block_table,
+                         int max_blocks_per_seq, const int32_t* seq_lens, const int32_t* repaired_blocks,
+                         const int32_t* n_repaired, int max_repair_blocks, const uint8_t* whole_kv,
+                         void* stream) {
+  if (cache == nullptr || cache->repaired == nullptr) return WC_EINVAL;
+  const int s = check_cache(cache, false, true);
+  if (s != WC_OK) return s;
+  if (batch < 0 || max_blocks_per_seq < 1) return WC_EINVAL;
+  if (n_repaired != nullptr && (max_repair_blocks < 1 || max_repair_blocks > 64 || !repaired_blocks))
+    return WC_EINVAL;
+  if (batch == 0 || (n_repaired == nullptr && whole_kv == nullptr)) return WC_OK;
+  if (!block_table || !seq_lens) return WC_EINVAL;
+  wc::WriteBackArgs w{};
+  w.repaired = cache->repaired;
+  w.k_witness = static_cast<uint16_t*>(cache->k_witness);
+  w.num_blocks = cache->num_blocks;
+  w.n_kv = cache->n_kv_heads;
+  w.n_bands = cache->n_bands;
+  w.batch = batch;
+  w.max_blocks = max_blocks_per_seq;
+  w.max_rep = n_repaired != nullptr ? max_repair_blocks : 1;
+  w.table = block_table;
+  w.seq_lens = seq_lens;
+  w.list = repaired_blocks;
+  w.n_rep = n_repaired;
+  w.whole_kv = whole_kv;
+  return hip_status(wc::launch_write_back(w, static_cast<hipStream_t>(stream)));
 }
 
 int wc_gate(const float* meter, const float* raw, int batch, int n_q_heads, int group, float tau,

@@ -9,9 +9,10 @@
 //
 //   QK^T  S = K Q^T with v_mfma_f32_16x16x32_f16: A = 16 tokens x 32 channels of
 //         int8 codes (exact in fp16), B = the G (<= 16) queries in fp16.  The
-//         dither enters as a second product with D = 2048 + 2u (exact in fp16,
-//         built from the Philox byte u by a byte permute); since 512 xi = 2u - 255,
-//         q . khat = s (q . code - (q . D - 2303 sum(q)) / 512).
+//         dither enters as a second product into the same accumulator with
+//         E = -(4 + u/256) (exact in fp16: bits 0xC400 | u, one byte permute from
+//         the Philox byte u); since xi = (u - 127.5)/256 = -E - 4 - 127.5/256,
+//         q . khat = s (q . code + q . E + (4 + 127.5/256) sum(q)).
 //   bound c_t = sm_scale sum_b ||q_b|| w_{t,b}: one more MFMA, witness (fp16,
 //         exact) times band norms split into fp16 hi + lo parts.
 //   softmax online over the page; the running max is only raised when a page
@@ -20,9 +21,10 @@
 //   PV    O^T = V^T W with v_mfma_f32_16x16x16_f16: A = value codes + 1152 (the
 //         stored byte as fp16 1024 + u, one permute) of 16 channels x 4 tokens per
 //         lane group (the value pages are stored token-quad interleaved, so this is
-//         one 32-byte load), B = p_t s^v_t in fp16, and a second product with D,
-//         transposed through LDS; the 1152 and 2303 offsets are removed at the end
-//         with the running sum of the fp16 weights.
+//         one 32-byte load), B = p_t s^v_t in fp16, and a second product with E,
+//         transposed through LDS, into the same accumulators; the offset
+//         1152 - 4 - 127.5/256 is removed at the end with the running sum of the
+//         fp16 weights.
 //
 // Lane l: r = l % 16 (token in the QK operands, head in B and in the results,
 // channel row in the PV operands), g = l / 16 (k-group).  The channel order of
@@ -57,8 +59,8 @@ constexpr int kRow = 272;  // LDS bytes per token row of the dither transpose (2
 // page's largest value scale, with the accumulators rescaled by the exact power
 // of two), so it stays below e^2 2^8 < 65504 for any fp16 value scale.
 constexpr float kSlack = 2.0f;
-constexpr float kDOff = 2303.0f;   // 2048 + 255: D = 2u + 2048 = 512 xi + 2303
-constexpr float kCOff = 1152.0f;   // 1024 + 128: value operand 1024 + u = code + 1152
+constexpr float kQOff = 4.498046875f;    // 4 + 127.5/256: code - xi = code + E + kQOff
+constexpr float kVOff = 1147.501953125f; // 1152 - kQOff: (code + 1152) + E = code - xi + kVOff
 
 __device__ __forceinline__ uint32_t as_u32(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
 __device__ __forceinline__ h2_t as_h2(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
@@ -77,13 +79,13 @@ __device__ __forceinline__ uint32_t codes2(uint32_t xb, uint32_t sel) {
   return as_u32(as_h2(perm(0x64646464u, xb, sel)) - h2_t{(_Float16)1152.0f, (_Float16)1152.0f});
 }
 // Two stored bytes u -> fp16 1024 + u = code + 1152 (exact): the value operand of
-// PV, whose 1152 offset is removed once at the end with the weight sum.
+// PV, whose offset is removed once at the end with the weight sum.
 __device__ __forceinline__ uint32_t ucodes2(uint32_t xb, uint32_t sel) {
   return perm(0x64646464u, xb, sel);
 }
-// Two dither bytes u -> fp16 2048 + 2u (bits 0x6800 | u), exact, one permute.
-__device__ __forceinline__ uint32_t dith2(uint32_t u, uint32_t sel) {
-  return perm(0x68686868u, u, sel);
+// Two dither bytes u -> fp16 E = -(4 + u/256) (bits 0xC400 | u), exact, one permute.
+__device__ __forceinline__ uint32_t ndith2(uint32_t u, uint32_t sel) {
+  return perm(0xC4C4C4C4u, u, sel);
 }
 // Two E4M3 bytes (bytes 0, 1 of w, or 2, 3 with HI) -> fp16 pair, one gfx950
 // conversion instruction at scale 1: every E4M3 value, subnormals included, is
@@ -124,7 +126,7 @@ struct PageRegs {
   uint32_t kw[NW];   // keys of token r, channels 32g..32g+31
   uint32_t vw[NW];   // values of channels 8r..8r+7 for token quad g
   uint2 ks, vs;      // fp16 scales of tokens 4g..4g+3
-  uint4 wit;         // witness bands 8(g%2).. of token r (garbage where 8(g%2) >= n_bands)
+  uint4 wit;         // witness bands 8(g%2).. of token r (zeros where 8(g%2) >= n_bands)
   uint4 ov;          // fp16 keys of bypassed pairs: values 8g .. 8g+7 of token r (when 8g < 2m)
   uint2 vr, vn;      // value side: stored ||vhat - v|| and ||v|| of tokens 4g..4g+3
   int blk;           // cache block of the page (wave-uniform)
@@ -194,11 +196,37 @@ __device__ __forceinline__ void load_page(const DecodeArgs& a, int blk, bool val
   }
 }
 
+// A page marked as repaired (persistent repair, Sec. 6 gate): its bf16 keys and
+// values from the exact store, in the bf16 page layout, with the stored value
+// norm (value side) and no witness, scale or value residual, so that the page
+// enters with bound 0.
+template <bool VM>
+__device__ __forceinline__ void load_exact_page(const DecodeArgs& a, int blk, bool valid, int kv, int r, int g,
+                                                PageRegs<WC_KIND_BF16>& p) {
+  constexpr int PB = kBlockTokens * kD * 2;   // bytes per bf16 page and tensor
+  p.blk = blk;
+  valid = valid && (int64_t)(uint32_t)blk < a.num_blocks;
+  const int64_t page = valid ? (int64_t)blk * a.n_kv + kv : 0;
+  const auto kr = page_rsrc(reinterpret_cast<const uint8_t*>(a.x_k_data) + page * PB, valid ? PB : 0);
+  const auto vr = page_rsrc(reinterpret_cast<const uint8_t*>(a.x_v_data) + page * PB, valid ? PB : 0);
+  const int lane = 16 * g + r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint4 k4 = bload16(kr, (64 * i + lane) * 16), v4 = bload16(vr, (64 * i + lane) * 16);
+    p.kw[4 * i] = k4.x; p.kw[4 * i + 1] = k4.y; p.kw[4 * i + 2] = k4.z; p.kw[4 * i + 3] = k4.w;
+    p.vw[4 * i] = v4.x; p.vw[4 * i + 1] = v4.y; p.vw[4 * i + 2] = v4.z; p.vw[4 * i + 3] = v4.w;
+  }
+  p.ks = p.vs = p.vr = make_uint2(0, 0);
+  p.wit = p.ov = make_uint4(0, 0, 0, 0);
+  p.vn = VM ? bload8(page_rsrc(a.v_norm + page * kBlockTokens, valid ? 2 * kBlockTokens : 0), 8 * g)
+            : make_uint2(0, 0);
+}
+
 // Running state of one wave.  Logits are kept in log2 units; every weight carries
 // an extra factor 2^8 (the exponent is raised by 8), which keeps the fp16 PV
 // operand out of the subnormal range and cancels in out / l and n / l.
 struct WaveState {
-  f4_t o1[8], o2[8];
+  f4_t o1[8];            // PV accumulators (INT8: code and dither products together)
   float m, l, n, wsum;   // running max (log2 units), sum of weights, meter numerator, sum of fp16 weights
   float nb;              // meter numerator of the current block segment (block repair's shares)
   int ve;                // INT8 value exponent (wave-uniform, scalar): PV weights carry 2^-ve, and 2^ve
@@ -211,7 +239,7 @@ struct WaveConst {
   h8_t qop[4];     // fp16 queries, B operands of QK (channels 32g + 8kt ..)
   s8_t qbf[4];     // bf16 queries (bf16 cache)
   h8_t qnop;       // band norms * sm_scale * log2(e), hi (g < 2) / lo (g >= 2) parts
-  float s1_init;   // 2303 sum(q) / 512: the dither offset, preloaded into the code accumulator
+  float s1_init;   // (4 + 127.5/256) sum(q): the dither offset, preloaded into the code accumulator
   float lmul;      // logit multiplier: sm_scale * log2(e)
   float ab2;       // Tier B: (alpha_h + beta_h) * log2(e)
   h8_t qo;         // bypassed pairs: fp16 queries at the stored values 8g .. 8g+7
@@ -219,7 +247,6 @@ struct WaveConst {
   float gmul;      // Tier B: sm_scale * 2^-11 * log2(e)
   float gc;        // Tier B: sm_scale * 2^-25 * log2(e) * sum |q_c| over the bypassed channels
   uint32_t layer_head;
-  bool wit_ok;
   bool ov_lo, ov_hi;   // this lane's stored values 8g..8g+3, 8g+4..8g+7 exist (< 2m)
 };
 
@@ -262,18 +289,18 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
                                              uint8_t* my_dsh, WaveState& st) {
   // ---------------- QK^T and the bound ----------------
   const f4_t z4 = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
-  f4_t s1 = z4, s2 = z4;   // code products, dither products
+  f4_t s1 = z4;   // code and dither products
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
     s1 = f4_t{wc.s1_init, wc.s1_init, wc.s1_init, wc.s1_init};
     const int64_t slot = (int64_t)cur.blk * kBlockTokens + r;
     const U4 r0 = dither_block(2 * g, slot, wc.layer_head, a.key0, a.key1);
     const U4 r1 = dither_block(2 * g + 1, slot, wc.layer_head, a.key0, a.key1);
     const uint32_t u[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
-    uint32_t dq[16];   // 2048 + 2u of token r, channels 32g + 2i, 32g + 2i + 1
+    uint32_t dq[16];   // E of token r, channels 32g + 2i, 32g + 2i + 1
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      dq[2 * i] = dith2(u[i], kSelLo);
-      dq[2 * i + 1] = dith2(u[i], kSelHi);
+      dq[2 * i] = ndith2(u[i], kSelLo);
+      dq[2 * i + 1] = ndith2(u[i], kSelHi);
     }
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
@@ -281,7 +308,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       const h8_t ka = pack8(codes2(x0, kSelLo), codes2(x0, kSelHi), codes2(x1, kSelLo), codes2(x1, kSelHi));
       s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, wc.qop[kt], s1, 0, 0, 0);
       const h8_t kd = pack8(dq[4 * kt], dq[4 * kt + 1], dq[4 * kt + 2], dq[4 * kt + 3]);
-      s2 = __builtin_amdgcn_mfma_f32_16x16x32_f16(kd, wc.qop[kt], s2, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(kd, wc.qop[kt], s1, 0, 0, 0);
     }
     // dither of this page to LDS (row = token r, channels 32g..32g+31)
     uint4* dst = reinterpret_cast<uint4*>(my_dsh + r * kRow + 64 * g);
@@ -308,7 +335,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   }
   f4_t cb = z4;
   if constexpr (METER && !TB) {
-    const uint4 w = wc.wit_ok ? cur.wit : make_uint4(0, 0, 0, 0);
+    const uint4 w = cur.wit;
     cb = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, w),
                                                 wc.qnop, cb, 0, 0, 0);
   }
@@ -339,8 +366,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   float scv[4], cbv[4], sov[4], gov[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    scv[e] = s1[e];
-    if constexpr (KIND == WC_KIND_INT8_DITHER) scv[e] = fmaf(s2[e], -0.001953125f, scv[e]);   // q . (code + xi)
+    scv[e] = s1[e];   // INT8: q . (code - xi)
     cbv[e] = cb[e];
     sov[e] = so[e];
     gov[e] = go[e];
@@ -410,7 +436,6 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       st.o1[j] *= alpha;
-      st.o2[j] *= alpha;
     }
   }
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
@@ -423,9 +448,13 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       vsx &= tq >= 2 ? 0xFFFFFFFFu : (tq == 1 ? 0x0000FFFFu : 0u);
       vsy &= tq >= 4 ? 0xFFFFFFFFu : (tq == 3 ? 0x0000FFFFu : 0u);
     }
-    const h2_t pm2 = __builtin_elementwise_max(as_h2(vsx), as_h2(vsy));
-    const float pmax = fmaxf((float)pm2[0], (float)pm2[1]);
-    if (__ballot(pmax > __builtin_bit_cast(float, (uint32_t)(127 + st.ve) << 23)) != 0) {
+    // (scales are non-negative fp16: their bit patterns order like their values;
+    // 2^ve has the bits (15 + ve) << 10, +inf for ve = 16, above every fp16 scale)
+    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+    const u16x2 pm2 = __builtin_elementwise_max(__builtin_bit_cast(u16x2, vsx), __builtin_bit_cast(u16x2, vsy));
+    const uint32_t pbits = max((uint32_t)pm2[0], (uint32_t)pm2[1]);
+    if (__ballot(pbits > (uint32_t)(15 + st.ve) << 10) != 0) {
+      const float pmax = (float)__builtin_bit_cast(_Float16, (uint16_t)pbits);
       const float wmax = xor_max(xor_max(xor_max(xor_max(xor_max(xor_max(pmax, 1), 2), 4), 8), 16), 32);
       int e2;
       (void)frexpf(wmax, &e2);                    // wmax < 2^e2 (e2 <= 16 for fp16 scales)
@@ -436,7 +465,6 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
   #pragma unroll
       for (int j = 0; j < 8; ++j) {
         st.o1[j] *= alpha;
-        st.o2[j] *= alpha;
       }
     }
   }
@@ -505,10 +533,14 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       const uint32_t x = cur.vw[jt];     // codes (excess-128) of channel 8r+jt, tokens 4g..4g+3
       st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(ucodes2(x, kSelLo), ucodes2(x, kSelHi)), wop,
                                                         st.o1[jt], 0, 0, 0);
+    }
+    // (the dither products go to the same accumulators after all eight code products)
+#pragma unroll
+    for (int jt = 0; jt < 8; ++jt) {
       const uint32_t sel = (jt & 1) ? kSelH1 : kSelH0;
       const uint32_t d01 = perm(r1[jt >> 1], r0[jt >> 1], sel);
       const uint32_t d23 = perm(r3[jt >> 1], r2[jt >> 1], sel);
-      st.o2[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(d01, d23), wop, st.o2[jt], 0, 0, 0);
+      st.o1[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(pack4(d01, d23), wop, st.o1[jt], 0, 0, 0);
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);   // LDS reads done before the next page overwrites
     __builtin_amdgcn_wave_barrier();
@@ -552,6 +584,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       const int ve_new = __builtin_amdgcn_readfirstlane(max(st.ve, e2 - 15));
       const float alpha = __builtin_bit_cast(float, (uint32_t)(127 + st.ve - ve_new) << 23);
       st.ve = ve_new;
+      st.wsum *= alpha;   // (the INT8 weights of a mixed cache carry 2^-ve too)
 #pragma unroll
       for (int j = 0; j < 8; ++j) st.o1[j] *= alpha;
     }
@@ -615,7 +648,9 @@ __device__ __forceinline__ void step_write(const DecodeArgs& a, int b, int kv, i
   __syncthreads();
 }
 
-template <int KIND, bool METER, bool HALF, bool TB, bool BYP, bool VM>
+// REP: the cache carries repair marks (a.repaired set; a quantized kind), a
+// separate instantiation so that caches without marks run the loop unchanged.
+template <int KIND, bool METER, bool HALF, bool TB, bool BYP, bool VM, bool REP>
 __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
   __shared__ float qn_s[kWaves][16][16];
@@ -680,16 +715,28 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   // full pages go through the ring; a last page that reaches past t_end is done after it
   const int np = t_end > t_begin ? (t_end - t_begin) / kBlockTokens : 0;
   const int pg0 = t_begin / kBlockTokens;
-  const int wit_off = 8 * (g & 1) < B ? 2 * (r * B + 8 * (g & 1)) : 0;
+  // (a lane without bands -- 8 (g % 2) >= B -- reads past the page's witness
+  // bytes, which the buffer range check turns into zeros)
+  const int wit_off = 8 * (g & 1) < B ? 2 * (r * B + 8 * (g & 1)) : 1 << 30;
   PageRegs<KIND> p0, p1, p2;
   int nc = 0, tv = 0;
+  // persistent repair: the chunk's repair marks (lane j: page j), requested with
+  // the first two pages and read before the third is requested; a marked page is
+  // not read here (its loads get empty resources) and is served from the exact
+  // store after the loop
+  constexpr bool has_rep = REP && KIND != WC_KIND_BF16;   // (the exact cache has no marks)
+  int fl = 0;
+  uint64_t emask = 0;
   auto blk_at = [&](int j) { return __builtin_amdgcn_readlane(tv, min(j, nc - 1)); };
+  auto marked = [&](int j) { return j < 64 && ((emask >> j) & 1u) != 0; };
   // (scheduling barriers keep each page's loads together, so that waiting for
   // one page never waits for a later one)
   auto start_chunk = [&](int c0) {
     nc = min(64, np - c0);
     if (c0 == 0 && pg0 == pg_spec && nc <= nc_spec) tv = tv_spec;   // the early request holds them
     else tv = lane < nc ? trow[pg0 + c0 + lane] : 0;
+    if (has_rep)
+      fl = lane < nc && (int64_t)(uint32_t)tv < a.num_blocks ? a.repaired[(int64_t)tv * a.n_kv + kv] : 0;
     load_page<KIND, METER, TB, BYP, VM>(a, blk_at(0), true, kv, r, g, wit_off, p0);
     __builtin_amdgcn_sched_barrier(0);
     load_page<KIND, METER, TB, BYP, VM>(a, blk_at(1), 1 < nc, kv, r, g, wit_off, p1);
@@ -771,7 +818,6 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     }
   }
   wc.layer_head = ((uint32_t)a.layer << 16) | (uint32_t)kv;
-  wc.wit_ok = 8 * (g & 1) < B;
   wc.lmul = a.sm_scale * kLog2e;
   // B operands of QK: the kt-th MFMA uses channels 32g + 8kt .. 32g + 8kt + 7.
   float qsum = 0.0f;   // sum of the fp16 queries of head r over all channels
@@ -792,7 +838,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   }
   qsum += __shfl_xor(qsum, 16, 64);
   qsum += __shfl_xor(qsum, 32, 64);
-  wc.s1_init = kDOff * qsum * 0.001953125f;
+  wc.s1_init = kQOff * qsum;
   // band norms ||q_b|| * sm_scale * log2(e) -> witness-MFMA B operand (hi parts
   // for g < 2, lo for g >= 2); the bound then comes out in log2 units
   wc.qnop = pack8(0, 0, 0, 0);
@@ -870,7 +916,6 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     st.o1[j] = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
-    st.o2[j] = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
   }
   st.m = -INFINITY;
   st.l = st.n = st.wsum = st.nb = 0.0f;
@@ -900,27 +945,33 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     if (rec_shares && (t0 & (kRepairBlockTokens - 1)) == 0 && t0 / kBlockTokens > sg.first)
       flush_segment<HALF>(a, st, sg, t0 / kBlockTokens, my_slots, r, g);
   };
+  bool any_marked = false;
   for (int c0 = 0; c0 < np;) {
     const int tb = t_begin + c0 * kBlockTokens;
+    emask = has_rep ? (uint64_t)__ballot(fl != 0) : 0;
+    any_marked |= emask != 0;
     // No early exit from this loop: a break lets the compiler's load counting
     // assume the ring order may differ on the back edge and wait for every page.
     for (int j = 0; j < nc; j += 3) {
       set_priority(c0 + j);
-      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 2), j + 2 < nc, kv, r, g, wit_off, p2);
+      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 2), j + 2 < nc && !marked(j + 2), kv, r, g, wit_off, p2);
       __builtin_amdgcn_sched_barrier(0);
       seg_check(tb + j * kBlockTokens);
-      process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
-      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 3), j + 3 < nc, kv, r, g, wit_off, p0);
+      if (!marked(j))
+        process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p0, tb + j * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 3), j + 3 < nc && !marked(j + 3), kv, r, g, wit_off, p0);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 1 < nc) {
         seg_check(tb + (j + 1) * kBlockTokens);
-        process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+        if (!marked(j + 1))
+          process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p1, tb + (j + 1) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
       }
-      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 4), j + 4 < nc, kv, r, g, wit_off, p1);
+      load_page<KIND, METER, TB, BYP, VM>(a, blk_at(j + 4), j + 4 < nc && !marked(j + 4), kv, r, g, wit_off, p1);
       __builtin_amdgcn_sched_barrier(0);
       if (j + 2 < nc) {
         seg_check(tb + (j + 2) * kBlockTokens);
-        process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
+        if (!marked(j + 2))
+          process_page<KIND, METER, true, HALF, TB, BYP, VM>(a, p2, tb + (j + 2) * kBlockTokens, t_end, r, g, wc, my_dsh, st);
       }
     }
     c0 += 64;
@@ -929,15 +980,64 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __builtin_amdgcn_s_setprio(0);
   const int t_last = t_begin + np * kBlockTokens;
   if (t_last < t_end) {   // a partial last page: tokens from t_end on are masked
-    load_page<KIND, METER, TB, BYP, VM>(a, trow[t_last / kBlockTokens], true, kv, r, g, wit_off, p0);
+    const int blk = trow[t_last / kBlockTokens];
+    const bool last_marked =
+        has_rep && (int64_t)(uint32_t)blk < a.num_blocks && a.repaired[(int64_t)blk * a.n_kv + kv] != 0;
+    any_marked |= last_marked;
     seg_check(t_last);
-    process_page<KIND, METER, false, HALF, TB, BYP, VM>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
+    if (!last_marked) {
+      load_page<KIND, METER, TB, BYP, VM>(a, blk, true, kv, r, g, wit_off, p0);
+      process_page<KIND, METER, false, HALF, TB, BYP, VM>(a, p0, t_last, t_end, r, g, wc, my_dsh, st);
+    }
   }
   if (rec_shares) {
     // the last segment, then the wave's unused slots (0 pages)
     if (t_end > t_begin) flush_segment<HALF>(a, st, sg, (t_end + kBlockTokens - 1) / kBlockTokens, my_slots, r, g);
     for (int sl = sg.slot; sl < a.share_slots / kWaves; ++sl)
       if (g == 0 && r < G) my_slots[sl] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  }
+
+  // ---- pages served from the exact store (persistent repair), two in flight:
+  // exact logits against the whole bf16 query, exact values, bound 0 ----
+  if (has_rep && any_marked) {
+    WaveConst wx = wc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint4 v = hv ? q_lds[r][4 * g + i] : make_uint4(0, 0, 0, 0);
+      wx.qbf[i] = __builtin_bit_cast(s8_t, v);
+    }
+    const int np_all = np + (t_last < t_end ? 1 : 0);
+    auto process_exact = [&](const PageRegs<WC_KIND_BF16>& p, int jj) {
+      const int t0 = t_begin + jj * kBlockTokens;
+      if (t0 + kBlockTokens <= t_end)
+        process_page<WC_KIND_BF16, METER, true, HALF, false, false, VM>(a, p, t0, t_end, r, g, wx, my_dsh, st);
+      else
+        process_page<WC_KIND_BF16, METER, false, HALF, false, false, VM>(a, p, t0, t_end, r, g, wx, my_dsh, st);
+    };
+    for (int c0 = 0; c0 < np_all; c0 += 64) {
+      const int nc2 = min(64, np_all - c0);
+      const int tv2 = lane < nc2 ? trow[pg0 + c0 + lane] : 0;
+      const int fl2 = lane < nc2 && (int64_t)(uint32_t)tv2 < a.num_blocks ? a.repaired[(int64_t)tv2 * a.n_kv + kv] : 0;
+      uint64_t em = (uint64_t)__ballot(fl2 != 0);
+      auto next = [&]() {
+        if (em == 0) return -1;
+        const int j = __builtin_ctzll(em);
+        em &= em - 1;
+        return j;
+      };
+      PageRegs<WC_KIND_BF16> pa, pb;
+      int ja = next();
+      load_exact_page<VM>(a, __builtin_amdgcn_readlane(tv2, max(ja, 0)), ja >= 0, kv, r, g, pa);
+      while (ja >= 0) {
+        const int jb = next();
+        load_exact_page<VM>(a, __builtin_amdgcn_readlane(tv2, max(jb, 0)), jb >= 0, kv, r, g, pb);
+        process_exact(pa, c0 + ja);
+        if (jb < 0) break;
+        ja = next();
+        load_exact_page<VM>(a, __builtin_amdgcn_readlane(tv2, max(ja, 0)), ja >= 0, kv, r, g, pa);
+        process_exact(pb, c0 + jb);
+      }
+    }
   }
 
   // ---- merge the four waves of the workgroup, write one partial record ----
@@ -975,7 +1075,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     for (int jt = 0; jt < 8; ++jt) {
       v[jt] = st.o1[jt][e];
       if constexpr (KIND == WC_KIND_INT8_DITHER)
-        v[jt] = fmaf(st.o2[jt][e] - kDOff * wsum, -0.001953125f, v[jt] - kCOff * wsum);
+        v[jt] = fmaf(-kVOff, wsum, v[jt]);
     }
     float4* dst = reinterpret_cast<float4*>(&acc_s[wave][r][32 * g + 8 * e]);
     dst[0] = make_float4(v[0], v[1], v[2], v[3]);
@@ -1010,11 +1110,11 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
       }
     }
     if (isnan(nsum)) nsum = INFINITY;
-    // the output accumulators also carry each wave's 2^-ve (INT8 and bf16 values)
+    // the output accumulators also carry each wave's 2^-ve (INT8 and bf16 values; 0 for fp8
+    // values unless the wave read exact pages)
     float fo[kWaves];
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w)
-      fo[w] = KIND != WC_KIND_FP8_RAW ? f[w] * exp2_fast(ml_s[w][r][5]) : f[w];
+    for (int w = 0; w < kWaves; ++w) fo[w] = f[w] * exp2_fast(ml_s[w][r][5]);
     float* rec = a.part + (((int64_t)b * a.n_q + (int64_t)kv * G + r) * a.n_splits + split) * R;
 #pragma unroll
     for (int i = 0; i < 32; i += 4) {
@@ -1056,31 +1156,45 @@ bool mfma_decode_supported(const DecodeArgs& a) {
          (a.kind == WC_KIND_BF16 || a.n_bands == 8 || a.n_bands == 16);
 }
 
-template <bool HALF, bool VM>
+template <bool HALF, bool VM, bool REP>
 void launch_decode_mfma_int8(const DecodeArgs& a, bool tb, bool byp, const dim3& grid, const dim3& block,
                              hipStream_t st) {
   if (tb && byp) {
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, true, VM>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, true, VM, REP>), grid, block, 0, st,
+                       a);
   } else if (tb) {
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, false, VM>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, true, false, VM, REP>), grid, block, 0,
+                       st, a);
   } else if (byp) {
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, true, VM>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, true, VM, REP>), grid, block, 0,
+                       st, a);
   } else {
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, false, VM>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_INT8_DITHER, true, HALF, false, false, VM, REP>), grid, block, 0,
+                       st, a);
+  }
+}
+
+template <bool HALF, bool VM, bool REP>
+void launch_decode_mfma_g(const DecodeArgs& a, bool metered, bool tb, bool byp, const dim3& grid,
+                          const dim3& block, hipStream_t st) {
+  if (!metered) {
+    if constexpr (!VM && !REP)
+      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, HALF, false, false, false, false>), grid, block, 0,
+                         st, a);
+  } else if (a.kind == WC_KIND_FP8_RAW) {
+    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, HALF, false, false, VM, REP>), grid, block, 0, st,
+                       a);
+  } else {
+    launch_decode_mfma_int8<HALF, VM, REP>(a, tb, byp, grid, block, st);
   }
 }
 
 template <bool HALF, bool VM>
-void launch_decode_mfma_g(const DecodeArgs& a, bool metered, bool tb, bool byp, const dim3& grid,
+void launch_decode_mfma_r(const DecodeArgs& a, bool metered, bool tb, bool byp, const dim3& grid,
                           const dim3& block, hipStream_t st) {
-  if (!metered) {
-    if constexpr (!VM)
-      hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_BF16, false, HALF, false, false, false>), grid, block, 0, st, a);
-  } else if (a.kind == WC_KIND_FP8_RAW) {
-    hipLaunchKernelGGL((decode_mfma_kernel<WC_KIND_FP8_RAW, true, HALF, false, false, VM>), grid, block, 0, st, a);
-  } else {
-    launch_decode_mfma_int8<HALF, VM>(a, tb, byp, grid, block, st);
-  }
+  // repair marks apply to the quantized caches of the metered decodes
+  if (metered && a.repaired != nullptr) launch_decode_mfma_g<HALF, VM, true>(a, metered, tb, byp, grid, block, st);
+  else launch_decode_mfma_g<HALF, VM, false>(a, metered, tb, byp, grid, block, st);
 }
 
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st) {
@@ -1090,11 +1204,11 @@ hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st)
   const bool byp = metered && a.n_pairs > 0;        // bypassed pairs: INT8 keys only
   const bool vm = metered && a.meter_v != nullptr;    // value side
   if (a.group <= 8) {
-    if (vm) launch_decode_mfma_g<true, true>(a, metered, tb, byp, grid, block, st);
-    else launch_decode_mfma_g<true, false>(a, metered, tb, byp, grid, block, st);
+    if (vm) launch_decode_mfma_r<true, true>(a, metered, tb, byp, grid, block, st);
+    else launch_decode_mfma_r<true, false>(a, metered, tb, byp, grid, block, st);
   } else {
-    if (vm) launch_decode_mfma_g<false, true>(a, metered, tb, byp, grid, block, st);
-    else launch_decode_mfma_g<false, false>(a, metered, tb, byp, grid, block, st);
+    if (vm) launch_decode_mfma_r<false, true>(a, metered, tb, byp, grid, block, st);
+    else launch_decode_mfma_r<false, false>(a, metered, tb, byp, grid, block, st);
   }
   return hipGetLastError();
 }

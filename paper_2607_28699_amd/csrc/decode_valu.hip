@@ -51,6 +51,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   __shared__ float qg_s[kGMax][8];        // group scales, Tier B: ||q_g||^2 (0..3), ||q_g||_1 (4..7)
   __shared__ float alpha_s[kGMax];
   __shared__ int64_t slot_s[kT];
+  __shared__ uint8_t ex_s[kT];            // persistent repair: the token's page is served exactly
 
   const int split = decode_split(a.n_splits);
   const int unit = decode_unit();
@@ -187,10 +188,28 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
       const int c0 = part * CH;
       const int64_t page = valid ? (slot / kBlockTokens) * a.n_kv + kv : 0;
       const int off = valid ? (int)(slot % kBlockTokens) : 0;
+      // a page marked as repaired is read from the exact store with bound 0
+      const bool ex = KIND != WC_KIND_BF16 && valid && a.repaired != nullptr && a.repaired[page] != 0;
+      if (part == 0) ex_s[i] = ex ? 1 : 0;
       float kval[CH];
 #pragma unroll
       for (int c = 0; c < CH; ++c) kval[c] = 0.0f;
-      if (valid) {
+      if (ex) {
+        const uint8_t* kpg = reinterpret_cast<const uint8_t*>(a.x_k_data) + page * (kBlockTokens * D * 2);
+#pragma unroll
+        for (int v4 = 0; v4 < CH / 8; ++v4) {
+          const uint4 cw = *reinterpret_cast<const uint4*>(kpg + kpage_off(off, c0 + 8 * v4, D, 2));
+          const uint32_t wds[4] = {cw.x, cw.y, cw.z, cw.w};
+#pragma unroll
+          for (int w4 = 0; w4 < 4; ++w4) {
+            kval[8 * v4 + 2 * w4] = bf16_to_f32((uint16_t)(wds[w4] & 0xFFFFu));
+            kval[8 * v4 + 2 * w4 + 1] = bf16_to_f32((uint16_t)(wds[w4] >> 16));
+          }
+        }
+        if (part == 0) vs_s[i] = 1.0f;
+        if (grouped)
+          for (int gg = part; gg < D / 32; gg += 4) vg_s[i][gg] = 1.0f;
+      } else if (valid) {
         if constexpr (KIND == WC_KIND_INT8_DITHER) {
           const uint8_t* kpg = reinterpret_cast<const uint8_t*>(a.k_data) + page * (kBlockTokens * D);
           const int64_t srow = page * kBlockTokens + off;
@@ -248,15 +267,22 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
           for (int gg = 0; gg < D / 32; ++gg) vg_s[i][gg] = 0.0f;
       }
       if (vm && part == 0) {
-        vr_s[i] = valid ? f16_to_f32(a.v_resid[page * kBlockTokens + off]) : 0.0f;
+        vr_s[i] = valid && !ex ? f16_to_f32(a.v_resid[page * kBlockTokens + off]) : 0.0f;
         vn_s[i] = valid ? f16_to_f32(a.v_norm[page * kBlockTokens + off]) : 0.0f;
       }
       // stored fp16 values of the bypassed pairs: positions part, part + 4, ...
+      // (an exact token: its bf16 keys at those channels)
       float kov[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int pos = part + 4 * k;
-        kov[k] = (valid && pos < m2) ? f16_to_f32(a.k_outlier[(page * kBlockTokens + off) * m2 + pos]) : 0.0f;
+        if (ex && pos < m2) {
+          const int ch = pair_channel(plist[pos >> 1], pos & 1, D, a.interleaved);
+          kov[k] = bf16_to_f32(*reinterpret_cast<const uint16_t*>(
+              reinterpret_cast<const uint8_t*>(a.x_k_data) + page * (kBlockTokens * D * 2) + kpage_off(off, ch, D, 2)));
+        } else {
+          kov[k] = (valid && pos < m2) ? f16_to_f32(a.k_outlier[(page * kBlockTokens + off) * m2 + pos]) : 0.0f;
+        }
       }
       for (int h = 0; h < G; ++h) {
         float d = 0.0f;
@@ -270,7 +296,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         if (part == 0) logit_s[h][i] = valid ? d * a.sm_scale : -INFINITY;
       }
       if (METER && a.tierb_delta > 0.0f) {   // Tier B: u_t = (alpha_h + beta_h) s_t, no witness
-        const float s = valid && !grouped ? f16_to_f32(a.k_scale[page * kBlockTokens + off]) : 0.0f;
+        const float s = valid && !ex && !grouped ? f16_to_f32(a.k_scale[page * kBlockTokens + off]) : 0.0f;
         for (int h = 0; h < G; ++h) {
           // fp16 rounding bound of the bypassed channels: sm sum |q_c| (2^-11 |khat_c| + 2^-25)
           float gb = 0.0f;
@@ -280,11 +306,12 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
               gb = fmaf(fabsf(qo_s[h][part + 4 * k]), fmaf(fabsf(kov[k]), 0x1p-11f, 0x1p-25f), gb);
           gb += __shfl_xor(gb, 1, 4);
           gb += __shfl_xor(gb, 2, 4);
+          if (ex) gb = 0.0f;   // (exact keys: no rounding term)
           if (part == 0) {
             if (grouped) {
               float s2 = 0.0f, s1 = 0.0f;
               for (int gg = 0; gg < D / 32; ++gg) {
-                const float sg = valid ? scale_of(a.k_scale, page * kBlockTokens + off, 32 * gg, D, true) : 0.0f;
+                const float sg = valid && !ex ? scale_of(a.k_scale, page * kBlockTokens + off, 32 * gg, D, true) : 0.0f;
                 s2 = fmaf(sg * sg, qg_s[h][gg], s2);
                 s1 = fmaf(sg, qg_s[h][4 + gg], s1);
               }
@@ -296,7 +323,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         }
       } else if constexpr (METER) {
         float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        if (valid) {
+        if (valid && !ex) {
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
             const int bb = part + 4 * k;
@@ -365,8 +392,9 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
         const int64_t page = (slot / kBlockTokens) * a.n_kv + kv;
         const int off = (int)(slot % kBlockTokens);   // multiple of 4
         float vv[4];
-        if constexpr (KIND == WC_KIND_BF16) {
-          const uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint8_t*>(a.v_data) +
+        if (KIND == WC_KIND_BF16 || ex_s[i0]) {   // (a quad lies in one page: one mark)
+          const void* vd = KIND == WC_KIND_BF16 ? a.v_data : a.x_v_data;
+          const uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint8_t*>(vd) +
                                                           page * (kBlockTokens * D * 2) + vpage_off(off, c3, D, 2));
           vv[0] = bf16_to_f32((uint16_t)(w.x & 0xFFFFu));
           vv[1] = bf16_to_f32((uint16_t)(w.x >> 16));
@@ -560,18 +588,9 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
       vt = fmaxf(vt, st_s[w][4]);
     }
   }
-#pragma unroll
-  for (int c = 0; c < C; ++c) {
-    float o = 0.0f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) o = fmaf(f[w], acc_s[w][C * lane + c], o);
-    o = ns > 0 ? o / lt : 0.0f;
-    const int64_t oi = (int64_t)bh * D + C * lane + c;
-    if (a.out_dtype == WC_F32)
-      reinterpret_cast<float*>(a.out)[oi] = o;
-    else
-      reinterpret_cast<uint16_t*>(a.out)[oi] = f32_to_bf16_rne(o);
-  }
+  // The meter and the gate first: the gate's counter atomic is then in flight
+  // while the output row is formed and stored, and its result is used after.
+  int gate_unit = -1, gate_old = -1;
   if constexpr (METER) {
     if (lane == 0) {
       float raw = 0.0f;
@@ -598,16 +617,29 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
         const bool gated = (a.gate_tau >= 1.0f ? raw : meter) > a.gate_tau || (VM && mv > a.gate_tau_v);
         a.gate_mask_q[bh] = gated ? 1 : 0;
         if (gated) {
-          const int unit = b * a.n_kv + h / a.group;
-          a.gate_mask_kv[unit] = 1;
-          const int first = atomicAdd(a.gate_unit + unit, 1) == 0;
-          if (a.gate_count != nullptr) {
-            atomicAdd(a.gate_count, 1);
-            if (first) atomicAdd(a.gate_count + 1, 1);
-          }
+          gate_unit = b * a.n_kv + h / a.group;
+          a.gate_mask_kv[gate_unit] = 1;
+          gate_old = atomicAdd(a.gate_unit + gate_unit, 1);
         }
       }
     }
+  }
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    float o = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) o = fmaf(f[w], acc_s[w][C * lane + c], o);
+    o = ns > 0 ? o / lt : 0.0f;
+    const int64_t oi = (int64_t)bh * D + C * lane + c;
+    if (a.out_dtype == WC_F32)
+      reinterpret_cast<float*>(a.out)[oi] = o;
+    else
+      reinterpret_cast<uint16_t*>(a.out)[oi] = f32_to_bf16_rne(o);
+  }
+  if (METER && gate_unit >= 0 && a.gate_count != nullptr) {   // (lane 0 of a gated head)
+    asm volatile("" : "+v"(gate_old));   // (keeps the wait for the counter here)
+    atomicAdd(a.gate_count, 1);
+    if (gate_old == 0) atomicAdd(a.gate_count + 1, 1);
   }
 }
 

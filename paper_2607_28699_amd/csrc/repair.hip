@@ -50,7 +50,7 @@ enum : int32_t { kIdle = 0, kActive = 1, kRepaired = 2, kExhausted = 3 };
 
 // Per-(sequence, KV head) header at the start of its workspace slice.
 struct RepHeader {
-  int32_t status, K, round0_end, n_taken;
+  int32_t status, K, round0_end, n_taken, n_cand;
   int32_t order[kRMaxRep];
   double M[kRGMax], L[kRGMax], N[kRGMax];
 };
@@ -121,6 +121,7 @@ __global__ __launch_bounds__(kRThreads) void repair_rank_kernel(RepairArgs ra) {
   __shared__ uint64_t pass_s[kRGMax];
   __shared__ int order_s[kRMaxRep];
   __shared__ double M_s[kRGMax], L_s[kRGMax];
+  __shared__ int n_cand_s;
 
   const int unit = blockIdx.x;
   const int tid = threadIdx.x;
@@ -164,18 +165,35 @@ __global__ __launch_bounds__(kRThreads) void repair_rank_kernel(RepairArgs ra) {
     }
   }
   __syncthreads();
-  // block totals: sum over the heads of the block's share / L
+  // block totals: sum over the heads of the block's share / L; a block whose
+  // positions all lie in pages marked as repaired is no candidate (total -1)
   const float4* sh_unit = a.shares + ((int64_t)u.b * a.n_q + (int64_t)u.kv * G) * a.n_splits * a.share_slots;
+  if (tid == 0) n_cand_s = 0;
+  __syncthreads();
   for (int i = tid; i < u.nb; i += kRThreads) {
-    double t = 0.0;
-    for (int h = 0; h < G; ++h) t += block_share(a, sh_unit, i, h, u.ns, M_s[h]) / L_s[h];
+    bool done = a.repaired != nullptr;
+    if (done) {
+      int b0, b1;
+      block_range(i, u.Lc, b0, b1);
+      for (int pg = b0 / kBlockTokens; done && pg <= (b1 - 1) / kBlockTokens; ++pg) {
+        const int32_t e = a.table[(int64_t)u.b * a.max_blocks + pg];
+        done = (int64_t)(uint32_t)e < a.num_blocks && a.repaired[(int64_t)e * a.n_kv + u.kv] != 0;
+      }
+    }
+    double t = -1.0;
+    if (!done) {
+      t = 0.0;
+      for (int h = 0; h < G; ++h) t += block_share(a, sh_unit, i, h, u.ns, M_s[h]) / L_s[h];
+      atomicAdd(&n_cand_s, 1);
+    }
     T_s[i] = t;
   }
   __syncthreads();
+  const int n_cand = n_cand_s;
   // repair order: the budget's largest blocks, ties to the lower index.  Up to
   // 1024 blocks every block counts the blocks ahead of it; beyond, one wave takes
   // an arg-max per step.
-  const int K = min(ra.max_rep, u.nb);
+  const int K = min(ra.max_rep, n_cand);
   if (u.nb <= 1024) {
     for (int i = tid; i < u.nb; i += kRThreads) {
       const double ti = T_s[i];
@@ -233,6 +251,7 @@ __global__ __launch_bounds__(kRThreads) void repair_rank_kernel(RepairArgs ra) {
     for (int h = 0; h < G; ++h) all &= pass_s[h];
     const int pred = all ? __builtin_ctzll(all) + 1 : K;
     hd->K = K;
+    hd->n_cand = n_cand;
     hd->n_taken = 0;
     hd->round0_end = min(K, ra.round0_cap > 0 ? ra.round0_cap : pred + 1);
     hd->status = kActive;
@@ -347,8 +366,11 @@ __global__ __launch_bounds__(kRThreads, 4) void repair_block_kernel(RepairArgs r
     const int i = tid >> 2, part = tid & 3;
     const int t = t_lo + i;
     // a table entry outside the caches leaves the token out (no access outside them)
+    // (a token of a page marked as repaired is exact in the decode's records already:
+    // no correction)
     const int32_t e = i < nv ? a.table[(int64_t)b * a.max_blocks + t / kBlockTokens] : -1;
-    const bool valid = i < nv && (int64_t)(uint32_t)e < a.num_blocks;
+    const bool valid = i < nv && (int64_t)(uint32_t)e < a.num_blocks &&
+                       !(a.repaired != nullptr && a.repaired[(int64_t)e * a.n_kv + kv] != 0);
     int64_t slot = -1;
     if (valid) slot = (int64_t)e * kBlockTokens + t % kBlockTokens;
     if (part == 0) slot_s[i] = slot;
@@ -613,10 +635,10 @@ __global__ __launch_bounds__(kRThreads) void repair_scan_kernel(RepairArgs ra, i
     dN_s[jj][h] = dn;
   }
   __syncthreads();
-  // once every block of the sequence is taken no compressed token is left: the
+  // once every candidate block is taken no compressed token is left: the
   // numerator is 0 by definition (the corrections would leave the rounding of
   // the records' fp32 sums)
-  const int nb_all = unit_geom(a, unit).nb;
+  const int nb_all = hd->n_cand;
   if (tid < G) {
     double L = hd->L[tid], N = hd->N[tid];
     uint64_t bits = 0;
@@ -743,6 +765,38 @@ __global__ __launch_bounds__(kRThreads) void repair_final_kernel(RepairArgs ra) 
   }
 }
 
+// ---------------------------------------------------------------------------
+// write-back (persistent repair): one workgroup per (sequence, KV head); thread
+// (page, token) of the pages to mark zeroes the token's witness, token 0 marks
+// the page
+__global__ __launch_bounds__(kRThreads) void repair_write_back_kernel(WriteBackArgs w) {
+  const int unit = blockIdx.x;
+  const int b = unit / w.n_kv, kv = unit % w.n_kv;
+  const bool whole = w.whole_kv != nullptr && w.whole_kv[unit] != 0;
+  const int n = w.n_rep != nullptr ? min(w.n_rep[unit], w.max_rep) : 0;
+  if (!whole && n <= 0) return;
+  const int Lc = min(w.seq_lens[b], w.max_blocks * kBlockTokens);
+  const int npages = (Lc + kBlockTokens - 1) / kBlockTokens;
+  constexpr int kPPB = kRepairBlockTokens / kBlockTokens;   // pages per repair block
+  const int total = whole ? npages : n * kPPB;
+  for (int idx = threadIdx.x; idx < total * kBlockTokens; idx += kRThreads) {
+    const int pk = idx / kBlockTokens, tok = idx % kBlockTokens;
+    int pg = pk;
+    if (!whole) {
+      const int blk = w.list[(int64_t)unit * w.max_rep + pk / kPPB];
+      if (blk < 0 || blk >= kRMaxBlocks) continue;
+      pg = blk * kPPB + pk % kPPB;
+    }
+    if (pg >= npages) continue;
+    const int32_t e = w.table[(int64_t)b * w.max_blocks + pg];
+    if ((int64_t)(uint32_t)e >= w.num_blocks) continue;
+    const int64_t page = (int64_t)e * w.n_kv + kv;
+    if (w.k_witness != nullptr)
+      for (int bb = 0; bb < w.n_bands; ++bb) w.k_witness[(page * kBlockTokens + tok) * w.n_bands + bb] = 0;
+    if (tok == 0) w.repaired[page] = 1;
+  }
+}
+
 template <int D, int QT>
 void launch_repair_d(const RepairArgs& a, hipStream_t st) {
   const int units = a.d.batch * a.d.n_kv;
@@ -771,6 +825,12 @@ hipError_t launch_repair(const RepairArgs& a, hipStream_t st) {
 }
 
 int repair_max_blocks() { return kRMaxBlocks; }
+
+hipError_t launch_write_back(const WriteBackArgs& w, hipStream_t st) {
+  if (w.batch * w.n_kv == 0) return hipSuccess;
+  hipLaunchKernelGGL(repair_write_back_kernel, dim3(w.batch * w.n_kv), dim3(kRThreads), 0, st, w);
+  return hipGetLastError();
+}
 
 size_t repair_unit_bytes(int group, int head_dim, int max_rep, int tiles) {
   const size_t b = kRepHeaderBytes + (size_t)max_rep * tiles * group * (head_dim + 2) * sizeof(double);

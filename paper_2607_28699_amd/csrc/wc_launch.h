@@ -98,6 +98,11 @@ struct DecodeArgs {
   // matrix-core decode before it reads them (step_write != 0), else nothing
   WriteArgs sw;
   int step_write;
+  // persistent repair: pages marked in repaired[blk * n_kv + kv] are read from the
+  // exact store (bf16 pages x_k_data / x_v_data) with bound 0 (null: no marks)
+  const uint8_t* repaired;
+  const void* x_k_data;
+  const void* x_v_data;
 };
 
 // Scale of channel c of the token in scale row `row` (page * 16 + offset): the
@@ -161,6 +166,20 @@ struct RepairArgs {
   int round0_cap;           // > 0: blocks in the first correction round (else the predicted count + 1)
 };
 constexpr int kRepHeaderBytes = 1024;
+
+// Write-back of a repair (persistent repair): marks and zeroed witnesses.
+struct WriteBackArgs {
+  uint8_t* repaired;        // [num_blocks][n_kv]
+  uint16_t* k_witness;      // [num_blocks][n_kv][16][n_bands] or null
+  int64_t num_blocks;
+  int n_kv, n_bands, batch, max_blocks, max_rep;
+  const int32_t* table;
+  const int32_t* seq_lens;
+  const int32_t* list;      // [batch][n_kv][max_rep] repaired blocks
+  const int32_t* n_rep;     // [batch][n_kv] or null
+  const uint8_t* whole_kv;  // [batch][n_kv] or null
+};
+hipError_t launch_write_back(const WriteBackArgs& w, hipStream_t st);
 // Repair blocks: fixed runs of 256 tokens of the sequence (Sec. 6.3), corrected in
 // 64-token tiles.
 constexpr int kRepairBlockTokens = 256;
