@@ -630,21 +630,17 @@ __device__ __forceinline__ void flush_segment(const DecodeArgs& a, WaveState& st
 
 // The new token of sequence b, KV head kv (the step's token of that sequence, by
 // the workgroup that reads it): lanes 0 .. kD/16 - 1 of wave 0 quantize and store
-// it as the write kernel does (write_dev.h), then the witness bands; the barrier
-// after the stores comes before any wave of the workgroup requests a page.
+// it as the write kernel does (write_dev.h, witness included); the barrier after
+// the stores comes before any wave of the workgroup requests a page.
 template <int KIND>
-__device__ __forceinline__ void step_write(const DecodeArgs& a, int b, int kv, int wave, int lane, double* r2row,
-                                        int64_t* slot_sh) {
+__device__ __forceinline__ void step_write(const DecodeArgs& a, int b, int kv, int wave, int lane) {
   constexpr int LPT = kD / 16;
   if (wave == 0 && lane < LPT) {
-    const int64_t slot = write_token_head<kD, KIND, uint16_t>(a.sw, b, kv, true, lane, r2row);
-    if (lane == 0) *slot_sh = slot;
+    (void)write_token_head<kD, KIND, uint16_t, false>(a.sw, b, kv, true, lane);   // (no bypassed pairs)
+    // the stores are complete (acknowledged) before the barrier, not only ordered
+    // by it: no wave can then read the page before the new token is in it
+    __builtin_amdgcn_s_waitcnt(0);
   }
-  __syncthreads();
-  if (wave == 0 && lane < a.sw.n_bands) witness_band<kD>(a.sw, r2row, *slot_sh, kv, lane);
-  // wave 0's stores are complete (acknowledged) before the barrier, not only ordered
-  // by it: no wave can then read the page before the new token is in it
-  if (wave == 0) __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 }
 
@@ -657,11 +653,9 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) float acc_s[kWaves][16][kD];
   __shared__ float ml_s[kWaves][16][6];
   __shared__ uint4 q_lds[16][17];   // the workgroup's queries, bf16 rows of 256 bytes (+16 pad)
-  // a decode step's new token (plain Tier A caches, the variants the step call
-  // fuses; the others keep their registers): its squared key residuals
+  // a decode step's new token is written by the plain Tier A variants (the ones the
+  // step call fuses; the others keep their registers)
   constexpr bool kStep = METER && !TB && !BYP && !VM;
-  __shared__ double wr_s[kStep ? kD : 1];
-  __shared__ int64_t wslot_s;
 
   // the wave index is uniform: page addresses then live in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -698,7 +692,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   const bool unrouted = a.mask_kv != nullptr && a.mask_kv[unit] == 0;
   if (unrouted | (split >= a.n_splits) | (wg_begin >= L)) return;
   if constexpr (kStep) {
-    if (a.step_write && split == (L - 1) / a.split_tokens) step_write<KIND>(a, b, kv, wave, lane, wr_s, &wslot_s);
+    if (a.step_write && split == (L - 1) / a.split_tokens) step_write<KIND>(a, b, kv, wave, lane);
   }
   const int wg_end = min(min(L, wg_begin + a.split_tokens), a.max_blocks * kBlockTokens);
   // this wave's share: a quarter of the workgroup's pages (rounded up; a full

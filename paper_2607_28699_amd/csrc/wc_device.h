@@ -51,9 +51,9 @@ __device__ __forceinline__ U4 dither_block(int group, int64_t slot, uint32_t lay
                        (uint32_t)((uint64_t)slot >> 32), layer_head, key0, key1);
 }
 
-// xi = (u - 127.5) / 256 : exact in fp32.
+// xi = (u - 127.5) / 256 = u/256 - 127.5/256: exact in fp32 (one fma).
 __device__ __forceinline__ float dither_value(uint32_t u) {
-  return ((float)u - 127.5f) * 0.00390625f;
+  return fmaf((float)u, 0.00390625f, -0.498046875f);
 }
 
 // ---- format conversions -----------------------------------------------------
@@ -72,21 +72,24 @@ __device__ __forceinline__ uint16_t f16_round_up(float f) {
   return b;
 }
 
-// Smallest fp16 value >= d (d finite, >= 0): nearest-even conversion, then one
-// step up if that fell below d.
+// Smallest fp16 value >= d (d finite, >= 0).  Rounding up is monotone and every
+// fp16 value is an fp32 value, so it is the fp16 round-up of the fp32 round-up of
+// d: nearest fp32, one fp32 step up if that fell below d, then f16_round_up.
 __device__ __forceinline__ uint16_t f16_round_up_f64(double d) {
-  const _Float16 h = (_Float16)d;
-  uint16_t b = f16_bits(h);
-  if ((double)h < d) b += 1;
-  return b;
+  float f = (float)d;
+  if ((double)f < d) f = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f) + 1u);
+  return f16_round_up(f);
 }
 
-// Largest fp16 value <= d (d finite, >= 0; 65504 above the range): nearest-even
-// conversion, then one step down if that landed above d.
+// Largest fp16 value <= d (d finite, >= 0; 65504 above the range), the same way
+// down: nearest fp32, one step down if above d, nearest fp16, one step down if
+// above.
 __device__ __forceinline__ uint16_t f16_round_down_f64(double d) {
-  const _Float16 h = (_Float16)d;
+  float f = (float)d;
+  if ((double)f > d) f = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f) - 1u);
+  const _Float16 h = (_Float16)f;
   uint16_t b = f16_bits(h);
-  if ((double)h > d) b -= 1;
+  if ((float)h > f) b -= 1;
   return b;
 }
 

@@ -13,32 +13,106 @@ namespace {
 
 constexpr int kWriteThreads = 256;
 
-template <int D, int KIND, typename TIn>
+// Byte transpose of four words (rows t = tokens, bytes c = channels): word c of
+// the result holds byte c of w0, w1, w2, w3 -- one channel's codes of a token quad.
+__device__ __forceinline__ uint4 transpose_bytes(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {
+  const uint32_t lo01 = __builtin_amdgcn_perm(w1, w0, 0x05010400u);   // w0.b0 w1.b0 w0.b1 w1.b1
+  const uint32_t hi01 = __builtin_amdgcn_perm(w1, w0, 0x07030602u);   // w0.b2 w1.b2 w0.b3 w1.b3
+  const uint32_t lo23 = __builtin_amdgcn_perm(w3, w2, 0x05010400u);
+  const uint32_t hi23 = __builtin_amdgcn_perm(w3, w2, 0x07030602u);
+  return make_uint4(__builtin_amdgcn_perm(lo23, lo01, 0x05040100u), __builtin_amdgcn_perm(lo23, lo01, 0x07060302u),
+                    __builtin_amdgcn_perm(hi23, hi01, 0x05040100u), __builtin_amdgcn_perm(hi23, hi01, 0x07060302u));
+}
+
+// Workgroup: TH consecutive tokens of one KV head (grid: token blocks x KV heads),
+// D/16 lanes per token (codes, scales, witness and the exact copy's keys are
+// stored by the token's lanes).  Each token's value row (codes, and the exact
+// copy's bf16 values) is staged in LDS; after the barrier, a token quad of the
+// workgroup that fills one quad of a page (slots 4s .. 4s+3 in order, the common
+// case of a prefill) is stored as whole 16-byte pieces of the page's interleaved
+// quad row, any other token element by element.
+template <int D, int KIND, typename TIn, bool BYP>
 __global__ __launch_bounds__(kWriteThreads) void quantize_write_kernel(WriteArgs a) {
-  constexpr int LPT = D / 16;                 // lanes per token-head
-  constexpr int TH = kWriteThreads / LPT;     // token-heads per block
-  __shared__ double r2[TH][D];                // squared key residuals
+  constexpr int LPT = D / 16;                 // lanes per token
+  constexpr int TH = kWriteThreads / LPT;     // tokens per workgroup
+  constexpr int NQ = TH / 4;                  // token quads per workgroup
+  constexpr bool kCodes = KIND != WC_KIND_BF16;
+  __shared__ uint32_t vq_s[kCodes ? TH : 1][D / 4];   // value codes
+  __shared__ uint32_t vx_s[TH][D / 2];        // bf16 values of the exact copy (or of a bf16 cache)
   __shared__ int64_t slot_s[TH];
 
   const int tid = threadIdx.x;
   const int lth = tid / LPT;
   const int g = tid % LPT;
-  const int64_t th = (int64_t)blockIdx.x * TH + lth;
-  const int64_t total = a.n_tok * (int64_t)a.n_kv;
-  const bool in_range = th < total;
-  const int64_t slot = write_token_head<D, KIND, TIn>(a, in_range ? th / a.n_kv : 0,
-                                                      in_range ? (int)(th % a.n_kv) : 0, in_range, g, r2[lth]);
-  if constexpr (KIND == WC_KIND_BF16) return;   // an exact cache has no witness
+  const int h = blockIdx.y;
+  const int64_t tok = (int64_t)blockIdx.x * TH + lth;
+  const bool in_range = tok < a.n_tok;
+  const bool exact_copy = KIND == WC_KIND_BF16 || a.x_k_data != nullptr;
+  const VStage vst{kCodes ? vq_s[lth] : nullptr, exact_copy ? vx_s[lth] : nullptr};
+  const int64_t slot = write_token_head<D, KIND, TIn, BYP>(a, in_range ? tok : 0, h, in_range, g, vst);
   if (g == 0) slot_s[lth] = slot;
-
-  // ---- witness: band norms of the key residual, rounded up to fp16 ----
   __syncthreads();
-  const int B = a.n_bands;
-  for (int item = tid; item < TH * B; item += kWriteThreads) {
-    const int t = item / B;
-    const int64_t th2 = (int64_t)blockIdx.x * TH + t;
-    if (th2 >= total) continue;
-    witness_band<D>(a, r2[t], slot_s[t], (int)(th2 % a.n_kv), item % B);
+
+  // ---- value rows by token quads ----
+  {
+    // thread (quad q, piece p); a code quad row is D x 4 bytes (D/4 pieces), a bf16 one
+    // twice that
+    constexpr int PC = D / 4;                 // 16-byte pieces of a code quad row
+    static_assert(NQ * PC == kWriteThreads, "one code piece per thread");
+    const int q = tid / PC, p = tid % PC;
+    const int64_t s0 = slot_s[4 * q];
+    bool whole = s0 >= 0 && (s0 & 3) == 0;
+#pragma unroll
+    for (int t = 1; t < 4; ++t) whole = whole && slot_s[4 * q + t] == s0 + t;
+    const int64_t bh0 = whole ? (s0 / kBlockTokens) * a.n_kv + h : 0;
+    const int off0 = whole ? (int)(s0 % kBlockTokens) : 0;
+    if constexpr (kCodes) {
+      // piece p: channels 4p .. 4p+3 of the quad's four tokens
+      uint8_t* vpg = reinterpret_cast<uint8_t*>(a.v_data);
+      if (whole) {
+        const uint4 o = transpose_bytes(vq_s[4 * q][p], vq_s[4 * q + 1][p], vq_s[4 * q + 2][p], vq_s[4 * q + 3][p]);
+        *reinterpret_cast<uint4*>(vpg + bh0 * (kBlockTokens * D) + vpage_off(off0, 4 * p, D, 1)) = o;
+      } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int64_t st = slot_s[4 * q + t];
+          if (st < 0) continue;
+          const int64_t bh = (st / kBlockTokens) * a.n_kv + h;
+          const uint32_t w = vq_s[4 * q + t][p];
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            vpg[bh * (kBlockTokens * D) + vpage_off((int)(st % kBlockTokens), 4 * p + c, D, 1)] = (uint8_t)(w >> (8 * c));
+        }
+      }
+    }
+    if (exact_copy) {
+      // pieces p and p + D/4 of the bf16 quad row: channels 2p', 2p'+1 of the four tokens
+      uint8_t* xpg = reinterpret_cast<uint8_t*>(KIND == WC_KIND_BF16 ? a.v_data : a.x_v_data);
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int pp = p + half * PC;   // 0 .. D/2 - 1
+        if (whole) {
+          const uint32_t w0 = vx_s[4 * q][pp], w1 = vx_s[4 * q + 1][pp], w2 = vx_s[4 * q + 2][pp],
+                         w3 = vx_s[4 * q + 3][pp];
+          const uint4 o = make_uint4(__builtin_amdgcn_perm(w1, w0, 0x05040100u), __builtin_amdgcn_perm(w3, w2, 0x05040100u),
+                                     __builtin_amdgcn_perm(w1, w0, 0x07060302u), __builtin_amdgcn_perm(w3, w2, 0x07060302u));
+          *reinterpret_cast<uint4*>(xpg + bh0 * (kBlockTokens * D * 2) + vpage_off(off0, 2 * pp, D, 2)) = o;
+        } else {
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int64_t st = slot_s[4 * q + t];
+            if (st < 0) continue;
+            const int64_t bh = (st / kBlockTokens) * a.n_kv + h;
+            const uint32_t w = vx_s[4 * q + t][pp];
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+              *reinterpret_cast<uint16_t*>(xpg + bh * (kBlockTokens * D * 2) +
+                                           vpage_off((int)(st % kBlockTokens), 2 * pp + c, D, 2)) =
+                  (uint16_t)(w >> (16 * c));
+          }
+        }
+      }
+    }
   }
 }
 
@@ -65,16 +139,23 @@ __global__ __launch_bounds__(256) void witness_kernel(WitnessArgs a) {
   a.w_out[item] = f16_round_up_f64(sqrt(acc));
 }
 
+template <int D, int KIND, bool BYP>
+hipError_t launch_write_dtb(const WriteArgs& a, hipStream_t st) {
+  constexpr int TH = kWriteThreads / (D / 16);
+  const dim3 grid((unsigned)((a.n_tok + TH - 1) / TH), (unsigned)a.n_kv);
+  if (a.in_dtype == WC_F32)
+    hipLaunchKernelGGL((quantize_write_kernel<D, KIND, float, BYP>), grid, dim3(kWriteThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((quantize_write_kernel<D, KIND, uint16_t, BYP>), grid, dim3(kWriteThreads), 0, st, a);
+  return hipGetLastError();
+}
+
 template <int D, int KIND>
 hipError_t launch_write_dt(const WriteArgs& a, hipStream_t st) {
-  constexpr int TH = kWriteThreads / (D / 16);
-  const int64_t total = a.n_tok * (int64_t)a.n_kv;
-  const unsigned grid = (unsigned)((total + TH - 1) / TH);
-  if (a.in_dtype == WC_F32)
-    hipLaunchKernelGGL((quantize_write_kernel<D, KIND, float>), dim3(grid), dim3(kWriteThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL((quantize_write_kernel<D, KIND, uint16_t>), dim3(grid), dim3(kWriteThreads), 0, st, a);
-  return hipGetLastError();
+  // (bypassed pairs: INT8 keys only)
+  if constexpr (KIND == WC_KIND_INT8_DITHER)
+    if (a.n_pairs > 0) return launch_write_dtb<D, KIND, true>(a, st);
+  return launch_write_dtb<D, KIND, false>(a, st);
 }
 
 template <int D>
