@@ -653,6 +653,49 @@ def main():
                              "gate_fraction_q_heads": round(gq_ / (n_cells * wl.n_q), 4),
                              "gate_fraction_kv_heads": round(gkv_ / (n_cells * wl.n_kv), 4)}
             byp["group_scales"] = gsd
+
+        # incremental persistent repair (Sec. 6 gate; Sec. 6.3 gated evaluation (c)):
+        # each layer's Tier-A decode, gate and block repair once more, then the write-back
+        # (the taken blocks' pages, and every page of a KV head the budget left to the
+        # whole-head fallback, are served from the exact store from then on); timed: the
+        # next step's metered decode with the gate over the written-back caches, which
+        # reads the marked pages as bf16 with bound 0
+        for layer in range(wl.n_layers):
+            byp_caches[layer].enable_repair(exact[layer])
+        rws = wc.repair_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, REPAIR_BUDGET)
+        for layer in range(wl.n_layers):
+            q_l = last["layers"][layer]["q"]
+            wc.metered_decode_gate(byp_caches[layer], q_l, table, last["lens"], max_len_all, sm, args.tau,
+                                   ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mq_b, mask_kv=mkv_b)
+            wc.block_repair(byp_caches[layer], exact[layer], q_l, table, last["lens"], max_len_all, sm,
+                            args.tau, ws, out, meter, raw, mkv_b, max_blocks=REPAIR_BUDGET, split_tokens=ST,
+                            repaired=rlist, n_repaired=nrep, repair_ws=rws)
+            wc.repair_write_back(byp_caches[layer], table, last["lens"], rlist, nrep, whole_kv=mkv_b)
+        del rws
+        pr_ms = timed(lambda i: wc.metered_decode_gate(
+            byp_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],
+            max_len_all, sm, args.tau, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mq_b,
+            mask_kv=mkv_b), reps)
+        cnt_p = torch.zeros(2, dtype=torch.int32, device=dev)
+        marked, pages_used = 0, 0
+        used = torch.zeros(lay.nblocks, dtype=torch.bool, device=dev)
+        for b in range(lay.batch):
+            nb = (int(last["lens"][b].item()) + 15) // 16
+            used[table[b, :nb].long()] = True
+        for layer in range(wl.n_layers):
+            wc.metered_decode_gate(byp_caches[layer], last["layers"][layer]["q"], table, last["lens"], max_len_all,
+                                   sm, args.tau, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mq_b,
+                                   mask_kv=mkv_b, n_gated=cnt_p)
+            mk_ = byp_caches[layer].tensors["repaired"][used]
+            marked += int(mk_.sum().item())
+            pages_used += int(mk_.numel())
+        gqp, gkvp = cnt_p.cpu().tolist()
+        byp["persistent_repair"] = {
+            "tau": args.tau, "budget_blocks": REPAIR_BUDGET,
+            "marked_page_fraction": round(marked / max(pages_used, 1), 4),
+            "next_step_median_launch_ms": round(float(np.median(pr_ms)), 4),
+            "next_step_gate_fraction_q_heads": round(gqp / (n_cells * wl.n_q), 4),
+            "next_step_gate_fraction_kv_heads": round(gkvp / (n_cells * wl.n_kv), 4)}
     th_per_launch = float(last["tokens"] * wl.n_kv)
     tb_gbps = th_per_launch * TIERB_BYTES / (float(np.median(tb_ms)) * 1e-3) / 1e9
     dec_gbps = th_per_launch * INT8_BYTES / (float(np.median(dec_ms)) * 1e-3) / 1e9
