@@ -137,9 +137,9 @@ extern "C" {
  * of the token scale; codes use fl32(1/s_g).  The decode of a group-scaled cache
  * runs on the vector ALUs.
  *
- * Persistent repair (quantized kinds; the meter loop's gate, Sec. 6: page in,
- * recompute, write back, zero the witness; Sec. 6.3 gated evaluation (c): repaired
- * slots are paged in once and filtered out afterwards): repaired[blk * n_kv_heads +
+ * Persistent repair (quantized kinds; the meter loop's gate, Sec. 6: repaired slots
+ * keep their exact values and their witnesses are cleared; Sec. 6.3 gated evaluation
+ * (c): each slot is repaired once and skipped afterwards): repaired[blk * n_kv_heads +
  * h] != 0 marks page blk of KV head h as served from the exact store, whose bf16
  * pages (the k_data / v_data of a WC_KIND_BF16 cache with the same num_blocks,
  * n_kv_heads and head_dim, written by wc_quantize_write_pair) are exact_k /

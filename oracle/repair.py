@@ -31,8 +31,9 @@ Definitions followed, with our readings where the paper leaves a choice:
   or raw' when tau >= 1) is at most tau; at most max_blocks blocks, otherwise the
   KV head is left to the whole-head exact fallback.
 
-Incremental persistent repair (the meter loop's gate, Sec. 6: page in, recompute,
-write back, zero the witness; Sec. 6.3 gated evaluation (c): un-repaired slots are
+Incremental persistent repair (the meter loop's gate, Sec. 6: the flagged blocks or
+head come back from the exact store, the head is recomputed, the exact values are
+kept and their witnesses cleared; Sec. 6.3 gated evaluation (c): un-repaired slots are
 paged in once, and repaired slots are filtered out by their zero witness).
 Readings:
 

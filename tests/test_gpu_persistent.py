@@ -1,6 +1,6 @@
-"""GPU parity of persistent repair (the meter loop's gate, Sec. 6: page in,
-recompute, write back, zero the witness; Sec. 6.3 gated evaluation (c)) against
-the oracle.
+"""GPU parity of persistent repair (the meter loop's gate, Sec. 6: repaired
+slots keep their exact values and lose their witness; Sec. 6.3 gated evaluation
+(c)) against the oracle.
 
 * Decode over a cache whose pages carry repair marks (random marks, and every page
   marked): each decode variant serves the marked pages from the exact store with
