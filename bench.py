@@ -641,7 +641,7 @@ def main():
                                           ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw)
                 wc.gate(meter, raw, wl.group, args.tau, n_gated=cnt_g["B"], mask_q=mq_b, mask_kv=mkv_b)
                 raws_g["B"].append(raw.clone())
-            gsd = {"path": "vector ALUs (fp16 group scales)"}
+            gsd = {"path": "matrix cores (fp16 group scales)"}
             for tier, ms, nbytes in (("tier_a", ga_ms, INT8_BYTES + 4 * m_byp + 12),
                                      ("tier_b", gb_ms, TIERB_BYTES + 4 * m_byp + 12)):
                 key = "A" if tier == "tier_a" else "B"

@@ -135,7 +135,9 @@ extern "C" {
  * tensor, s_g = fp16_round_up(fl32(amax_g / 126.5)) over the group's quantized
  * channels (bypassed channels leave amax_g), stored in k_scale / v_scale in place
  * of the token scale; codes use fl32(1/s_g).  The decode of a group-scaled cache
- * runs on the vector ALUs.
+ * takes the same paths as a per-token one (matrix cores for head_dim 128 and bf16
+ * queries); its value operands carry one more fp16 rounding there (outputs within
+ * 2e-3 of the oracle, relative to the largest output; logits and meters exact).
  *
  * Persistent repair (quantized kinds; the meter loop's gate, Sec. 6: repaired slots
  * keep their exact values and their witnesses are cleared; Sec. 6.3 gated evaluation

@@ -3,9 +3,10 @@ Table 4: one fp16 scale per token and group) against the oracle.
 
 * write path: codes, group scales, witness, bypassed values and the value side
   bit-exact, both RoPE layouts, d = 64 and 128;
-* decode (a group-scaled cache runs on the vector ALUs): Tier A (witness), Tier B
-  (radius over the group steps) and the joint K + V gate: outputs within 1e-5 (fp32
-  workloads) / 2e-3 (bf16) of the oracle, raw
+* decode on both paths (matrix cores for head_dim 128 and bf16 queries, the
+  vector ALUs otherwise or when forced): Tier A (witness), Tier B (radius over the
+  group steps) and the joint K + V gate: outputs within 1e-5 (fp32 workloads) /
+  2e-3 (bf16) of the oracle, raw
   relative, the meter never below the true TV, the gate bit-exact;
 * block repair over a group-scaled cache against the oracle's repaired state.
 """

@@ -52,6 +52,8 @@ DEC_CASES = [
     ("gqa-bypass-tierb", W_GQA.replace(q_scale=1 / 4), [400], "int8_dither", "B", 4, False, False),
     ("gqa-value", W_GQA, [450, 70], "int8_dither", "A", 0, True, False),
     ("gqa-group-scales", W_GQA, [380, 21], "int8_dither", "A", 0, False, True),
+    ("gqa-group-scales-tierb", W_GQA.replace(q_scale=1 / 4), [420, 37], "int8_dither", "B", 0, False, True),
+    ("gqa-group-scales-value-bypass", W_GQA, [360, 45], "int8_dither", "A", 4, True, True),
     ("gqa-fp8", W_GQA, [480, 17], "fp8_raw", "A", 0, False, False),
     ("tiny-fp8", W_TINY, [200, 31], "fp8_raw", "A", 0, False, False),
 ]
@@ -95,7 +97,7 @@ def test_decode_with_repair_marks(name, wl, lens, kind, tier, m, vm, gs, path, d
     import torch
 
     import paper_2607_28699_amd as wc
-    if path == "vector" and (wl.d != 128 or gs):
+    if path == "vector" and wl.d != 128:
         pytest.skip("this case always takes the vector path")
     S.say(f"[persistent decode] {name} path={path} density={density}")
     case = S.make_case(wl, lens, permute=True, layer=3)
