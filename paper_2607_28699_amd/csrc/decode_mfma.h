@@ -844,9 +844,10 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   // the wave index is uniform: page addresses then live in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
-  const int unit = decode_unit(), split = decode_split(a.n_splits);
+  const DecodePos pos = decode_position(a.batch, a.n_kv, a.n_splits);
+  const int unit = __builtin_amdgcn_readfirstlane(pos.unit), split = __builtin_amdgcn_readfirstlane(pos.split);
   const int b = unit / a.n_kv, kv = unit % a.n_kv;
-  gate_clear(a, unit);
+  gate_clear(a, unit, split);
   const int G = a.group;
   const int B = a.n_bands;
   const int wg_begin = split * a.split_tokens;

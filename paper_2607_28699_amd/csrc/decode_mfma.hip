@@ -41,7 +41,7 @@ void launch_decode_mfma_r(const DecodeArgs& a, bool metered, bool tb, bool byp, 
 }
 
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st) {
-  const dim3 grid(a.n_splits, a.batch * a.n_kv);   // split index rotated by the unit: decode_split()
+  const dim3 grid(a.n_splits, a.batch * a.n_kv);   // workgroup order: decode_position()
   const dim3 block(64 * kWaves);
   const bool tb = metered && a.tierb_delta > 0.0f;   // Tier B: INT8 dithered cache only
   const bool byp = metered && a.n_pairs > 0;        // bypassed pairs: INT8 keys only

@@ -53,10 +53,10 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   __shared__ int64_t slot_s[kT];
   __shared__ uint8_t ex_s[kT];            // persistent repair: the token's page is served exactly
 
-  const int split = decode_split(a.n_splits);
-  const int unit = decode_unit();
+  const DecodePos pos = decode_position(a.batch, a.n_kv, a.n_splits);
+  const int split = pos.split, unit = pos.unit;
   const int b = unit / a.n_kv, kv = unit % a.n_kv;
-  gate_clear(a, unit);
+  gate_clear(a, unit, split);
   if (a.mask_kv != nullptr && a.mask_kv[unit] == 0) return;
   const int L = a.seq_lens[b];
   const int t_begin = split * a.split_tokens;

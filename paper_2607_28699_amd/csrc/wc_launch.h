@@ -127,21 +127,42 @@ __device__ __forceinline__ float tierb_factor(float q_sq, float q_l1, int n_toke
   return sm_scale * (sqrtf(q_sq) * sqrtf(2.0f * lg / 12.0f) + q_l1 * (1.0f / 256.0f));
 }
 
-// Decode grids are (splits, units).  Workgroups go to the eight XCDs round-robin in
-// linear order (x fastest), so with the split index equal to x a split count that
-// is a multiple of 8 would send every unit's split j to XCD j mod 8 -- and a
-// sequence's first split (always present, while later ones exist only for long
-// sequences) to the same XCD for every unit.  The split index is therefore
-// rotated by the unit: split = (x + unit) mod n_splits, which gives every XCD a
-// share of every unit's splits whatever the split count.
-__device__ __forceinline__ int decode_unit() { return blockIdx.y; }
-__device__ __forceinline__ int decode_split(int n_splits) {
-  return (int)(((uint32_t)blockIdx.x + (uint32_t)blockIdx.y) % (uint32_t)n_splits);
+// Decode grids hold n_splits x (batch x n_kv) workgroups, one per (sequence, KV
+// head, split).  Workgroups go to the eight XCDs round-robin in linear order, and
+// the KV heads of one block read the same 128-byte lines of the per-token arrays
+// (scales, value side: [block][kv][16] fp16, 32 bytes per KV head), so the linear
+// order puts the n_kv heads of one (sequence, split) 8 apart -- on one XCD, where
+// its L2 serves the line to all of them.  Positions P = (sequence, split) go in
+// groups of 8 (one per XCD; a last partial group fills the rest), and each
+// sequence's splits are rotated by the sequence index, so that the sequences'
+// first splits -- always present, while later ones exist only for long sequences
+// -- spread over the XCDs too.
+struct DecodePos {
+  int unit;    // sequence x n_kv + KV head
+  int split;
+};
+__device__ __forceinline__ DecodePos decode_position(int batch, int n_kv, int n_splits) {
+  const uint32_t K = (uint32_t)n_kv, NS = (uint32_t)n_splits;
+  const uint32_t L = blockIdx.x + gridDim.x * blockIdx.y;
+  const uint32_t nP = (uint32_t)batch * NS;
+  const uint32_t full = nP / 8u * 8u;   // positions in whole groups of 8
+  uint32_t P, kv;
+  if (L < full * K) {
+    const uint32_t grp = L / (8u * K), rem = L % (8u * K);
+    kv = rem / 8u;
+    P = 8u * grp + rem % 8u;
+  } else {
+    const uint32_t Lr = L - full * K, R = nP - full;
+    kv = Lr / R;
+    P = full + Lr % R;
+  }
+  const uint32_t b = P / NS, s = P % NS;
+  return DecodePos{(int)(b * K + kv), (int)((s + b) % NS)};
 }
 
 // Clears the gate outputs of one (sequence, KV head) ahead of the merge.
-__device__ __forceinline__ void gate_clear(const DecodeArgs& a, int unit) {
-  if (a.gate_mask_q != nullptr && decode_split(a.n_splits) == 0 && threadIdx.x == 0) {
+__device__ __forceinline__ void gate_clear(const DecodeArgs& a, int unit, int split) {
+  if (a.gate_mask_q != nullptr && split == 0 && threadIdx.x == 0) {
     a.gate_mask_kv[unit] = 0;
     a.gate_unit[unit] = 0;
   }
