@@ -374,6 +374,7 @@ def main():
     # knows the lengths; equal to the library default for equal lengths)
     ST = wc.split_tokens_for(lay.batch, wl.n_kv, max_len_all, total_tokens=int((lens0 + K + W).sum()))
     ws = wc.decode_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all, ST)
+    ws_step = wc.certified_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all, ST)
     out = torch.empty((lay.batch, wl.n_q, wl.d), dtype=torch.bfloat16, device=dev)
     meter = torch.empty((lay.batch, wl.n_q), dtype=torch.float32, device=dev)
     raw = torch.empty_like(meter)
@@ -389,14 +390,12 @@ def main():
             if wl.chunk:
                 wc.quantize_write_pair(caches[layer], exact[layer], it["ck"], it["cv"], it["cslots"])
             # the step's token of every sequence into the quantized cache and the exact
-            # copy, and the metered decode with the gate in its split merge, in one launch
-            wc.step_metered_decode_gate(caches[layer], exact[layer], it["k"], it["v"], st["slots"], it["q"],
-                                        table, st["lens"], max_len_all, sm, args.tau, ws=ws, split_tokens=ST,
-                                        out=out, meter=meter, raw=raw, mask_q=mask_q, mask_kv=mask_kv,
-                                        n_gated=counts)
-            # then the exact fallback
-            wc.exact_decode_attention(exact[layer], it["q"], table, st["lens"], max_len_all, sm,
-                                      mask_kv, out, ws=ws, split_tokens=ST)
+            # copy with the metered decode (one launch), the exact fallback whose
+            # workgroups decide their KV head's gate first, and one final merge
+            wc.step_certified_decode(caches[layer], exact[layer], it["k"], it["v"], st["slots"], it["q"],
+                                     table, st["lens"], max_len_all, sm, args.tau, ws=ws_step, split_tokens=ST,
+                                     out=out, meter=meter, raw=raw, mask_q=mask_q, mask_kv=mask_kv,
+                                     n_gated=counts)
 
     # one decode step per HIP graph (all layers), replayed back to back: the timed
     # region is GPU work only, as in a graph-captured serving loop

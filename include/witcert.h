@@ -23,6 +23,9 @@
  *               wc_exact_decode_attention
  *                                   exact attention from an uncompressed bf16 cache for
  *                                   the routed heads (the fallback of the meter loop)
+ *   step        wc_step_metered_decode_gate, wc_step_certified_decode
+ *                                   a decode step's token write with the read path and
+ *                                   gate (and, certified, the exact fallback) fused
  *               wc_block_repair     repair of routed heads from the exact cache at block
  *                                   granularity (Sec. 6.3)
  *               wc_repair_write_back
@@ -497,6 +500,40 @@ int wc_exact_decode_attention(const wc_cache* exact, const void* q, int q_dtype,
                               int64_t max_seq_len, float sm_scale, const uint8_t* mask_kv,
                               void* out, int out_dtype, int split_tokens, void* ws,
                               size_t ws_bytes, void* stream);
+
+/*
+ * Workspace bytes of wc_step_certified_decode: that of the metered decode plus one
+ * more region of split records (0 for invalid sizes).
+ */
+size_t wc_certified_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim,
+                                   int64_t max_seq_len, int split_tokens);
+
+/*
+ * One whole decode step of the meter loop (Sec. 6: write the step's token, the
+ * metered read path, the gate, the exact fallback for what the gate routes):
+ * results equal wc_step_metered_decode_gate(...) followed by
+ * wc_exact_decode_attention(exact, q, ..., mask_kv, out, ...) with the same
+ * arguments, bit for bit (out, meter, raw, mask_q, mask_kv, n_gated), in three
+ * launches instead of four: the metered decode writes its split records, the exact
+ * fallback's workgroups first decide their KV head's gate from those records
+ * (the split merge's own statistics, in the same bits; the workgroup of the first
+ * split stores mask_q and mask_kv) and only the routed ones read the exact cache,
+ * and one merge forms every output row (a routed KV head's query heads from the
+ * exact records) with meter and raw.  The gate is Tier A's (as
+ * wc_metered_decode_gate).
+ *   ws     at least wc_certified_workspace_size(batch, n_q_heads, cache->n_kv_heads,
+ *          cache->head_dim, max_seq_len, split_tokens) bytes
+ *   exact  the bf16 exact cache (kind WC_KIND_BF16, same n_kv_heads and head_dim,
+ *          addressed by the same block table)
+ * Other arguments and checks as wc_step_metered_decode_gate.
+ */
+int wc_step_certified_decode(const wc_cache* cache, const wc_cache* exact, const void* new_k,
+                             const void* new_v, int in_dtype, const int64_t* new_slots, const void* q,
+                             int q_dtype, int batch, int n_q_heads, const int32_t* block_table,
+                             int max_blocks_per_seq, const int32_t* seq_lens, int64_t max_seq_len,
+                             float sm_scale, void* out, int out_dtype, float* meter, float* raw,
+                             int split_tokens, float tau, uint8_t* mask_q, uint8_t* mask_kv,
+                             int32_t* n_gated, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * For callers that cannot allocate device memory (code under HIP graph capture,

@@ -18,6 +18,8 @@ from .api import (  # noqa: F401
     metered_decode_attention,
     metered_decode_gate,
     step_metered_decode_gate,
+    step_certified_decode,
+    certified_workspace,
     step_metered_decode_gate_noalloc,
     quantize_write,
     quantize_write_pair,

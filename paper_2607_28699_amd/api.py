@@ -306,6 +306,45 @@ def step_metered_decode_gate(cache: PagedCache, exact: PagedCache, new_k: torch.
     return out, meter, raw, mask_q, mask_kv
 
 
+def certified_workspace(batch: int, n_q: int, n_kv: int, head_dim: int, max_seq_len: int,
+                        split_tokens: int = 0, device="cuda") -> torch.Tensor:
+    """Workspace of step_certified_decode (two regions of split records)."""
+    n = lib().wc_certified_workspace_size(batch, n_q, n_kv, head_dim, max_seq_len, split_tokens)
+    if n == 0:
+        raise _lib.WitCertError("bad workspace geometry")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def step_certified_decode(cache: PagedCache, exact: PagedCache, new_k: torch.Tensor, new_v: torch.Tensor,
+                          new_slots: torch.Tensor, q: torch.Tensor, block_table: torch.Tensor,
+                          seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float, tau: float,
+                          out_dtype=torch.float32, split_tokens: int = 0, ws=None, out=None, meter=None,
+                          raw=None, mask_q=None, mask_kv=None, n_gated=None):
+    """One whole decode step: step_metered_decode_gate, then exact_decode_attention
+    of the routed KV heads, in three launches (the gate decided in the exact
+    fallback's prologue) -> (out, meter, raw, mask_q, mask_kv)."""
+    _dev_check(q, block_table, seq_lens, new_k, new_v, new_slots)
+    batch, n_q, d = q.shape
+    assert new_slots.dtype == torch.int64 and new_k.shape == new_v.shape == (batch, cache.n_kv, d)
+    assert new_k.dtype == new_v.dtype
+    if ws is None:
+        ws = certified_workspace(batch, n_q, cache.n_kv, d, max_seq_len, split_tokens, q.device)
+    out = torch.empty((batch, n_q, d), dtype=out_dtype, device=q.device) if out is None else out
+    meter = torch.empty((batch, n_q), dtype=torch.float32, device=q.device) if meter is None else meter
+    raw = torch.empty((batch, n_q), dtype=torch.float32, device=q.device) if raw is None else raw
+    mask_q = torch.empty((batch, n_q), dtype=torch.uint8, device=q.device) if mask_q is None else mask_q
+    mask_kv = (torch.empty((batch, cache.n_kv), dtype=torch.uint8, device=q.device)
+               if mask_kv is None else mask_kv)
+    c, e = cache.struct(), exact.struct()
+    check(lib().wc_step_certified_decode(
+        ctypes.byref(c), ctypes.byref(e), _ptr(new_k), _ptr(new_v), _dt(new_k), _ptr(new_slots), _ptr(q),
+        _dt(q), batch, n_q, _ptr(block_table), block_table.shape[1], _ptr(seq_lens), max_seq_len,
+        float(sm_scale), _ptr(out), _dt(out), _ptr(meter), _ptr(raw), split_tokens, float(tau),
+        _ptr(mask_q), _ptr(mask_kv), _ptr(n_gated), _ptr(ws), ws.numel(), _stream()),
+        "wc_step_certified_decode")
+    return out, meter, raw, mask_q, mask_kv
+
+
 def step_metered_decode_gate_noalloc(cache: PagedCache, exact: PagedCache, new_k: torch.Tensor,
                                      new_v: torch.Tensor, new_slots: torch.Tensor, q: torch.Tensor,
                                      block_table: torch.Tensor, seq_lens: torch.Tensor, max_seq_len: int,

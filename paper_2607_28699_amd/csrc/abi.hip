@@ -91,7 +91,7 @@ const char* wc_strerror(int status) {
   }
 }
 
-int wc_version(void) { return 103; }   // 1.3: persistent repair (marks, wc_repair_write_back)
+int wc_version(void) { return 104; }   // 1.4: certified step (wc_step_certified_decode)
 
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim, int n_bands,
                       int n_outlier_pairs, int value_side, int group_scales, size_t sizes[8]) {
@@ -457,6 +457,90 @@ int wc_step_metered_decode_gate_noalloc(const wc_cache* cache, const wc_cache* e
                      block_table, max_blocks_per_seq, seq_lens, max_seq_len, sm_scale, out, out_dtype, meter,
                      raw, split_tokens, tau, mask_q, mask_kv, n_gated, ws, (size_t)WC_NOALLOC_SCRATCH_BYTES,
                      stream);
+}
+
+size_t wc_certified_workspace_size(int batch, int n_q_heads, int n_kv_heads, int head_dim, int64_t max_seq_len,
+                                   int split_tokens) {
+  const size_t base = wc_decode_workspace_size(batch, n_q_heads, n_kv_heads, head_dim, max_seq_len, split_tokens);
+  if (base == 0) return 0;
+  const int st = wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens);
+  return base + wc::records_bytes(batch, n_q_heads, wc::n_splits_for(max_seq_len, st), head_dim);
+}
+
+// Certified step: the step write and the metered decode (records in the first
+// region of the workspace; no block segments: this call repairs nothing), the
+// exact fallback with the gate decided in its prologue from those records
+// (records in the second region), the final merge.
+int wc_step_certified_decode(const wc_cache* cache, const wc_cache* exact, const void* new_k, const void* new_v,
+                             int in_dtype, const int64_t* new_slots, const void* q, int q_dtype, int batch,
+                             int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                             const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out,
+                             int out_dtype, float* meter, float* raw, int split_tokens, float tau, uint8_t* mask_q,
+                             uint8_t* mask_kv, int32_t* n_gated, void* ws, size_t ws_bytes, void* stream) {
+  if (cache == nullptr || exact == nullptr) return WC_EINVAL;
+  wc::WriteArgs w;
+  int s = write_args(cache, exact, new_k, new_v, in_dtype, new_slots, batch, w);
+  if (s != WC_OK) return s;
+  s = check_cache(cache, true);
+  if (s != WC_OK) return s;
+  s = check_cache(exact, false);
+  if (s != WC_OK) return s;
+  if (cache->kind == WC_KIND_BF16 || exact->kind != WC_KIND_BF16) return WC_EINVAL;
+  if (exact->n_kv_heads != cache->n_kv_heads || exact->head_dim != cache->head_dim) return WC_EINVAL;
+  if (!(tau >= 0.0f)) return WC_EINVAL;
+  if (batch > 0 && (!meter || !mask_q || !mask_kv)) return WC_EINVAL;
+  if (n_q_heads < 1 || split_tokens < 0 || max_seq_len < 0 || batch < 0) return WC_EINVAL;
+  const size_t need = wc_certified_workspace_size(batch, n_q_heads, cache->n_kv_heads, cache->head_dim,
+                                                  max_seq_len, split_tokens);
+  if (need == 0) return WC_EINVAL;
+  if (ws_bytes < need) return WC_EWORKSPACE;
+  const int st = wc::choose_split_tokens(batch, cache->n_kv_heads, max_seq_len, split_tokens);
+  const size_t rb = wc::records_bytes(batch, n_q_heads, wc::n_splits_for(max_seq_len, st), cache->head_dim);
+  char* wsb = static_cast<char*>(ws);
+  wc::DecodeArgs am{}, ax{};
+  s = decode_common(cache, q, q_dtype, batch, n_q_heads, block_table, max_blocks_per_seq, seq_lens, max_seq_len,
+                    sm_scale, out, out_dtype, split_tokens, wsb, ws_bytes, am);
+  if (s != WC_OK) return s;
+  s = decode_common(exact, q, q_dtype, batch, n_q_heads, block_table, max_blocks_per_seq, seq_lens, max_seq_len,
+                    sm_scale, out, out_dtype, split_tokens, wsb + rb, ws_bytes - rb, ax);
+  if (s != WC_OK) return s;
+  // (the metered call's gate counters and block segments would overlap the second
+  // region: neither is used here)
+  am.shares = nullptr;
+  am.gate_unit = nullptr;
+  if (batch == 0) return WC_OK;
+  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  // 1. the metered decode (with the step's tokens written first), no merge
+  am.no_merge = 1;
+  hipError_t e = hipSuccess;
+  if (wc::step_write_fusable(am) && in_dtype == WC_BF16) {
+    am.sw = w;
+    am.step_write = 1;
+  } else {
+    e = wc::launch_quantize_write(w, hs);
+  }
+  if (e == hipSuccess) e = wc::launch_decode(am, true, hs);
+  // 2. the exact fallback: each unit's gate from the metered records, then the
+  //    routed units' exact records
+  ax.no_merge = 1;
+  ax.gate_part = am.part;
+  ax.gate_tau = tau;
+  ax.gate_mask_q = mask_q;
+  ax.gate_mask_kv = mask_kv;
+  if (e == hipSuccess) e = wc::launch_decode(ax, false, hs);
+  // 3. the final merge: routed heads from the exact records, the others from the
+  //    metered ones; meter and raw from the metered records
+  wc::DecodeArgs af = am;
+  af.no_merge = 0;
+  af.x_part = ax.part;
+  af.meter = meter;
+  af.raw = raw;
+  af.gate_mask_q = mask_q;
+  af.gate_mask_kv = mask_kv;
+  af.gate_count = n_gated;
+  af.gate_tau = tau;
+  if (e == hipSuccess) e = wc::launch_merge(af, true, hs);
+  return hip_status(e);
 }
 
 int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int batch,

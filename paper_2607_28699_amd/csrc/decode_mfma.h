@@ -52,6 +52,7 @@
 
 #include <type_traits>
 
+#include "merge_dev.h"
 #include "wc_device.h"
 #include "wc_launch.h"
 #include "write_dev.h"
@@ -837,6 +838,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) float acc_s[kWaves][16][kD];
   __shared__ float ml_s[kWaves][16][6];
   __shared__ uint4 q_lds[16][17];   // the workgroup's queries, bf16 rows of 256 bytes (+16 pad)
+  __shared__ int gate_flag_s;       // certified step: the unit's gate (exact fallback's prologue)
   // a decode step's new token is written by the plain Tier A variants (the ones the
   // step call fuses; the others keep their registers)
   constexpr bool kStep = METER && !TB && !BYP && !VM && !GS;
@@ -872,9 +874,14 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
   const int tv_spec = lane < nc_spec ? trow[pg_spec + lane] : 0;
   const bool hv = r < G;
 
+  // certified step: the exact fallback decides its unit's gate from the metered
+  // records first (split 0 always, for the masks; splits past the end skip it)
+  bool ungated = false;
+  if (KIND == WC_KIND_BF16 && a.gate_part != nullptr && (split == 0 || wg_begin < L))
+    ungated = !unit_gate(a, b, kv, split, wave, lane, &gate_flag_s);
   // whole workgroup: a KV head not routed here, or a split past the sequence end
   // (evaluated together, so that the length load is not held back behind the mask)
-  const bool unrouted = a.mask_kv != nullptr && a.mask_kv[unit] == 0;
+  const bool unrouted = ungated || (a.mask_kv != nullptr && a.mask_kv[unit] == 0);
   if (unrouted | (split >= a.n_splits) | (wg_begin >= L)) return;
   if constexpr (kStep) {
     if (a.step_write && split == (L - 1) / a.split_tokens) step_write<KIND>(a, b, kv, wave, lane);

@@ -20,6 +20,7 @@
 #include <float.h>
 
 #include "wc_device.h"
+#include "merge_dev.h"
 #include "wc_launch.h"
 
 namespace wc {
@@ -57,9 +58,17 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
   const int split = pos.split, unit = pos.unit;
   const int b = unit / a.n_kv, kv = unit % a.n_kv;
   gate_clear(a, unit, split);
-  if (a.mask_kv != nullptr && a.mask_kv[unit] == 0) return;
   const int L = a.seq_lens[b];
   const int t_begin = split * a.split_tokens;
+  // certified step: the exact fallback decides its unit's gate from the metered
+  // records first (split 0 always, for the masks; splits past the end skip it)
+  if (KIND == WC_KIND_BF16 && a.gate_part != nullptr && (split == 0 || t_begin < L)) {
+    __shared__ int gate_flag_s;
+    if (!unit_gate(a, b, kv, split, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), threadIdx.x & 63,
+                   &gate_flag_s))
+      return;
+  }
+  if (a.mask_kv != nullptr && a.mask_kv[unit] == 0) return;
   if (t_begin >= L) return;
   // clamp to what the block table can address (guards a seq_lens above max_seq_len)
   const int t_end = min(min(L, t_begin + a.split_tokens), a.max_blocks * kBlockTokens);
@@ -470,44 +479,76 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
 // Merge of the split records of one (sequence, query head) under the LSE
 // weights: out = sum_j e^{m_j - M} acc_j / L, A - 1 = sum_j e^{m_j - M} N_j / L with
 // L = sum_j e^{m_j - M} l_j; raw = (A-1)(A+1)/2 (+inf on overflow), meter = min(1, raw)
-// (Sec. 6.2: A merges exactly like the output).  256 threads: the split maxima and
-// weights are reduced in LDS, then thread (channel, half) sums every other split
-// with all its loads independent.
+// (Sec. 6.2: A merges exactly like the output).  The statistics (M, L, the
+// numerators) come from split_stats (merge_dev.h), in the same bits wherever they
+// are formed.
 constexpr int kMergeWaves = 4;   // waves per merge workgroup when a head has more than 32 splits
 
-// Split-KV merge (Sec. 6.2): one workgroup per (sequence, query head).  Splits
-// go 32 at a time to the four waves in turn.  In a chunk, lane j % 32 holds the
-// (max, weight sum, meter numerator) of split j and every lane holds its channels
-// of all 32 partial outputs; all of a chunk's loads are issued together, and the
-// split weights reach the channel lanes through readlane.  The waves' running
-// states are combined in LDS at the end.
+// The statistics a merge needs: of the output rows (so; the exact records of a
+// routed head in a certified step's final merge) and of the metered records for
+// the meter (sm).  Up to 64 splits both records' scalars are read in one round trip.
+template <bool METER, bool VM>
+__device__ __forceinline__ void merge_stats(const float* rec0, const float* src0, bool routed, int64_t R, int ns,
+                                            int n_avail, int lane, SplitStats& so, SplitStats& sm) {
+  const int D = (int)R - 8;
+  if (n_avail <= 64 && routed) {
+    const int jr = min(lane, n_avail - 1);
+    const float4 tx = *reinterpret_cast<const float4*>(src0 + (int64_t)jr * R + D);
+    const float4 tm = *reinterpret_cast<const float4*>(rec0 + (int64_t)jr * R + D);
+    const float tv = VM ? rec0[(int64_t)jr * R + D + 4] : 0.0f;
+    so = stats_of_lanes<false, false>(tx, 0.0f, ns, lane);
+    sm = stats_of_lanes<METER, VM>(tm, tv, ns, lane);
+    return;
+  }
+  if (routed) {
+    so = split_stats<false, false>(src0, R, D, ns, n_avail, lane);
+    sm = split_stats<METER, VM>(rec0, R, D, ns, n_avail, lane);
+  } else {
+    so = sm = split_stats<METER, VM>(rec0, R, D, ns, n_avail, lane);
+  }
+}
+
+// Split-KV merge (Sec. 6.2): one workgroup per (sequence, query head).  The
+// output rows go 32 splits at a time to the waves in turn: lane j % 32 weighs split
+// j, every lane holds its channels of all 32 partial outputs (all of a chunk's
+// loads are issued together, before the statistics), and the weights reach the
+// channel lanes through readlane.  The waves' sums are added in LDS in wave order.
+// Final merge of a certified step (a.x_part set): the heads of a routed KV head
+// (gate_mask_kv, stored by the exact fallback's prologue) take their output from
+// the exact records, the others from the metered ones; meter and raw always from
+// the metered records.
 template <int D, bool METER, bool VM, int NW>
 __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
   constexpr int C = D / 64;   // channels per lane
-  __shared__ float st_s[NW][5];
   __shared__ float acc_s[NW][D];
   const int bh = blockIdx.x;
   const int b = bh / a.n_q, h = bh % a.n_q;
-  if (a.mask_kv != nullptr && a.mask_kv[b * a.n_kv + h / a.group] == 0) return;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int unit = b * a.n_kv + h / a.group;
+  if (a.mask_kv != nullptr && a.mask_kv[unit] == 0) return;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t R = (int64_t)partial_record_floats(D);
+  const bool fin = a.x_part != nullptr;
+  const bool routed = fin && a.gate_mask_kv[unit] != 0;
   const float* rec0 = a.part + (int64_t)bh * a.n_splits * R;
+  const float* src0 = routed ? a.x_part + (int64_t)bh * a.n_splits * R : rec0;   // output rows
   const int jl = lane & 31;
+  const int L = a.seq_lens[b];
 
-  float M = -INFINITY, lsum = 0.0f, nsum = 0.0f, esum = 0.0f, vmax = 0.0f, acc[C];
+  float acc[C];
 #pragma unroll
   for (int c = 0; c < C; ++c) acc[c] = 0.0f;
-  // The records of a chunk are requested before the sequence length is known;
-  // records past the last active split are read but not used.
-  int ns = -1;
+  SplitStats so{}, sm{};   // the output rows' statistics; the meter's (the metered records)
+  bool have = false;
+  int ns = 0;
+  // The rows of a chunk are requested before the sequence length is known; rows
+  // past the last active split are read (they exist in the workspace) but not used.
   for (int j0 = 32 * wave; j0 < a.n_splits; j0 += 32 * NW) {
-    const int nr = min(32, a.n_splits - j0);    // records that exist in the workspace
-    const float4 t = *reinterpret_cast<const float4*>(rec0 + (int64_t)(j0 + min(jl, nr - 1)) * R + D);
-    const float tv = VM ? rec0[(int64_t)(j0 + min(jl, nr - 1)) * R + D + 4] : 0.0f;
+    const int nr = min(32, a.n_splits - j0);
     float ov[32][C];
+    const float mj_raw = src0[(int64_t)(j0 + min(jl, nr - 1)) * R + D];
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
-      const float* src = rec0 + (int64_t)(j0 + min(j, nr - 1)) * R + C * lane;
+      const float* src = src0 + (int64_t)(j0 + min(j, nr - 1)) * R + C * lane;
       if constexpr (C == 2) {
         const float2 v = *reinterpret_cast<const float2*>(src);
         ov[j][0] = v.x;
@@ -516,40 +557,15 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
         ov[j][0] = src[0];
       }
     }
-    if (ns < 0) {
-      const int L = a.seq_lens[b];
-      ns = min((L + a.split_tokens - 1) / a.split_tokens, a.n_splits);
-    }
+    ns = active_splits(L, a.split_tokens, a.n_splits);
     if (j0 >= ns) break;
     const int nj = min(32, ns - j0);
-    const float mj = jl < nj ? t.x : -INFINITY;
-    float mc = mj;
-#pragma unroll
-    for (int o = 1; o < 32; o <<= 1) mc = fmaxf(mc, __shfl_xor(mc, o, 64));
-    const float Mn = fmaxf(M, mc);
-    const float alpha = M == -INFINITY ? 0.0f : __expf(M - Mn);
-    const float ej = mj == -INFINITY ? 0.0f : __expf(mj - Mn);
-    float dl = jl < nj ? ej * t.y : 0.0f, dn = METER && jl < nj ? ej * t.z : 0.0f;
-    float de = VM && jl < nj ? ej * t.w : 0.0f, dv = VM && jl < nj ? tv : 0.0f;
-#pragma unroll
-    for (int o = 1; o < 32; o <<= 1) {
-      dl += __shfl_xor(dl, o, 64);
-      if constexpr (METER) dn += __shfl_xor(dn, o, 64);
-      if constexpr (VM) {
-        de += __shfl_xor(de, o, 64);
-        dv = fmaxf(dv, __shfl_xor(dv, o, 64));
-      }
+    if (!have) {   // the statistics (the first chunk's loads are in flight)
+      merge_stats<METER, VM>(rec0, src0, routed, R, ns, a.n_splits, lane, so, sm);
+      have = true;
     }
-    M = Mn;
-    lsum = fmaf(lsum, alpha, dl);
-    if constexpr (METER) nsum = fmaf(nsum, alpha, dn);
-    if constexpr (VM) {
-      esum = fmaf(esum, alpha, de);
-      vmax = fmaxf(vmax, dv);
-    }
-#pragma unroll
-    for (int c = 0; c < C; ++c) acc[c] *= alpha;
-    // (records past the last active split may hold anything, NaN included: skip them)
+    const float mj = jl < nj ? mj_raw : -INFINITY;
+    const float ej = mj == -INFINITY ? 0.0f : __expf(mj - so.M);
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
       if (j < nj) {
@@ -559,65 +575,36 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
       }
     }
   }
-  if (ns < 0) {
-    const int L = a.seq_lens[b];
-    ns = min((L + a.split_tokens - 1) / a.split_tokens, a.n_splits);
-  }
-  if (lane == 0) {
-    st_s[wave][0] = M;
-    st_s[wave][1] = lsum;
-    st_s[wave][2] = nsum;
-    st_s[wave][3] = esum;
-    st_s[wave][4] = vmax;
-  }
+  ns = active_splits(L, a.split_tokens, a.n_splits);
+  if (!have && wave == 0) merge_stats<METER, VM>(rec0, src0, routed, R, ns, a.n_splits, lane, so, sm);
 #pragma unroll
   for (int c = 0; c < C; ++c) acc_s[wave][C * lane + c] = acc[c];
-  __syncthreads();
+  if constexpr (NW > 1) __syncthreads();
   if (wave != 0) return;
-  float Mt = -INFINITY;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) Mt = fmaxf(Mt, st_s[w][0]);
-  float f[NW], lt = 0.0f, nt = 0.0f, et = 0.0f, vt = 0.0f;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    f[w] = st_s[w][0] == -INFINITY ? 0.0f : __expf(st_s[w][0] - Mt);
-    lt = fmaf(f[w], st_s[w][1], lt);
-    if constexpr (METER) nt = fmaf(f[w], st_s[w][2], nt);
-    if constexpr (VM) {
-      et = fmaf(f[w], st_s[w][3], et);
-      vt = fmaxf(vt, st_s[w][4]);
-    }
-  }
   // The meter and the gate first: the gate's counter atomic is then in flight
   // while the output row is formed and stored, and its result is used after.
   int gate_unit = -1, gate_old = -1;
   if constexpr (METER) {
     if (lane == 0) {
-      float raw = 0.0f;
-      if (ns > 0) {
-        if (isnan(nt)) nt = INFINITY;
-        const float am1 = nt / lt;
-        raw = 0.5f * am1 * (2.0f + am1);
-        if (!(raw <= FLT_MAX)) raw = INFINITY;
-      }
-      const float meter = fminf(1.0f, raw);
-      a.meter[bh] = meter;
+      const float raw = raw_of(sm, ns);
+      a.meter[bh] = fminf(1.0f, raw);
       if (a.raw != nullptr) a.raw[bh] = raw;
-      // value meter: sum_t ptilde_t rho_t over the largest stored value norm (0/0 = 0)
-      float mv = 0.0f;
-      if constexpr (VM) {
-        const float ev = ns > 0 ? et / lt : 0.0f;
-        mv = vt > 0.0f ? ev / vt : (ev > 0.0f ? INFINITY : 0.0f);
-        if (isnan(mv)) mv = INFINITY;
-        a.meter_v[bh] = mv;
-      }
-      if (a.gate_mask_q != nullptr) {
+      const float mv = VM ? meter_v_of(sm, ns) : 0.0f;
+      if constexpr (VM) a.meter_v[bh] = mv;
+      if (fin) {
+        // (the gate was decided and stored by the exact fallback's prologue): counts
+        // of gated query heads and, by each KV head's first query head, routed KV heads
+        if (a.gate_count != nullptr) {
+          if (a.gate_mask_q[bh] != 0) atomicAdd(a.gate_count, 1);
+          if (h % a.group == 0 && routed) atomicAdd(a.gate_count + 1, 1);
+        }
+      } else if (a.gate_mask_q != nullptr) {
         // the gate of this query head (the joint one: pass_K and pass_V); its KV
         // head is counted by the first gated head
-        const bool gated = (a.gate_tau >= 1.0f ? raw : meter) > a.gate_tau || (VM && mv > a.gate_tau_v);
+        const bool gated = gated_of(raw, mv, a.gate_tau, VM, a.gate_tau_v);
         a.gate_mask_q[bh] = gated ? 1 : 0;
         if (gated) {
-          gate_unit = b * a.n_kv + h / a.group;
+          gate_unit = unit;
           a.gate_mask_kv[gate_unit] = 1;
           gate_old = atomicAdd(a.gate_unit + gate_unit, 1);
         }
@@ -628,8 +615,8 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
   for (int c = 0; c < C; ++c) {
     float o = 0.0f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) o = fmaf(f[w], acc_s[w][C * lane + c], o);
-    o = ns > 0 ? o / lt : 0.0f;
+    for (int w = 0; w < NW; ++w) o += acc_s[w][C * lane + c];
+    o = ns > 0 ? o / so.l : 0.0f;
     const int64_t oi = (int64_t)bh * D + C * lane + c;
     if (a.out_dtype == WC_F32)
       reinterpret_cast<float*>(a.out)[oi] = o;
@@ -648,7 +635,7 @@ hipError_t launch_dq(const DecodeArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((decode_split_kernel<D, KIND, QT, METER>), dim3(a.n_splits, a.batch * a.n_kv),
                      dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || a.no_merge) return e;
   return launch_merge(a, METER, st);
 }
 
@@ -716,7 +703,7 @@ hipError_t launch_decode(const DecodeArgs& a, bool metered, hipStream_t st) {
   if (a.batch == 0 || a.n_q == 0) return hipSuccess;
   if (a.use_mfma && mfma_decode_supported(a)) {
     hipError_t e = launch_decode_mfma(a, metered, st);
-    return e != hipSuccess ? e : launch_merge(a, metered, st);
+    return e != hipSuccess || a.no_merge ? e : launch_merge(a, metered, st);
   }
   return a.head_dim == 64 ? launch_d<64>(a, metered, st) : launch_d<128>(a, metered, st);
 }

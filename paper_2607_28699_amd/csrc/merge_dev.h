@@ -1,0 +1,170 @@
+// Split-KV merge statistics and the gate (Sec. 6.2: the meter's numerator
+// merges across splits exactly like the output; Sec. 6 meter loop: the gate at
+// tau, any of a KV head's query heads).  One wave computes the statistics of one
+// (sequence, query head) from its split records in a fixed order -- split j at
+// lane j % 64, the largest split max first, then the LSE-weighted sums by one
+// shuffle tree per 64 splits -- so every kernel that forms them (the split merge,
+// the gate in the exact fallback's prologue, the final merge of a certified step)
+// gets the same bits, and the gate a kernel decides is the one the merged meter
+// shows.
+#pragma once
+
+#include <float.h>
+
+#include "wc_launch.h"
+
+namespace wc {
+
+struct SplitStats {
+  float M;      // largest split max (natural-log units); -inf without splits
+  float l, n;   // sum_j e^{m_j - M} l_j, and the meter numerators likewise
+  float e, v;   // value side: weighted residual sum, largest stored value norm
+};
+
+// Adds the weighted scalars of one record per lane (one shuffle tree over the wave).
+template <bool METER, bool VM>
+__device__ __forceinline__ void reduce_stats(SplitStats& s, float w, const float4& t, float tv) {
+  float dl = w * t.y, dn = METER ? w * t.z : 0.0f, de = VM ? w * t.w : 0.0f, dv = tv;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    dl += __shfl_xor(dl, o, 64);
+    if constexpr (METER) dn += __shfl_xor(dn, o, 64);
+    if constexpr (VM) {
+      de += __shfl_xor(de, o, 64);
+      dv = fmaxf(dv, __shfl_xor(dv, o, 64));
+    }
+  }
+  s.l += dl;
+  if constexpr (METER) s.n += dn;
+  if constexpr (VM) {
+    s.e += de;
+    s.v = fmaxf(s.v, dv);
+  }
+}
+
+// Statistics of at most 64 splits whose scalars (t: max, weight sum, meter
+// numerator, value residual sum; tv: value norm) lane j holds for split j (lanes
+// at or past ns are left out).
+template <bool METER, bool VM>
+__device__ __forceinline__ SplitStats stats_of_lanes(float4 t, float tv, int ns, int lane) {
+  SplitStats s{-INFINITY, 0.0f, 0.0f, 0.0f, 0.0f};
+  if (lane >= ns) {
+    t = make_float4(-INFINITY, 0.0f, 0.0f, 0.0f);
+    tv = 0.0f;
+  }
+  s.M = t.x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) s.M = fmaxf(s.M, __shfl_xor(s.M, o, 64));
+  const float w = t.x == -INFINITY ? 0.0f : __expf(t.x - s.M);
+  reduce_stats<METER, VM>(s, w, t, tv);
+  return s;
+}
+
+// Statistics of the first ns records at rec0 (record stride R floats, the
+// scalars at offset D: max, weight sum, meter numerator, value residual sum,
+// value norm) of the n_avail >= ns records the workspace holds.  Whole wave;
+// every lane returns the same values.  Up to 64 records are read in one round
+// trip (records past ns are read -- they exist -- but not used).
+template <bool METER, bool VM>
+__device__ __forceinline__ SplitStats split_stats(const float* rec0, int64_t R, int D, int ns, int n_avail,
+                                                  int lane) {
+  if (n_avail <= 64) {
+    const int jr = min(lane, n_avail - 1);
+    const float4 t = *reinterpret_cast<const float4*>(rec0 + (int64_t)jr * R + D);
+    const float tv = VM ? rec0[(int64_t)jr * R + D + 4] : 0.0f;
+    return stats_of_lanes<METER, VM>(t, tv, ns, lane);
+  }
+  SplitStats s{-INFINITY, 0.0f, 0.0f, 0.0f, 0.0f};
+  for (int j0 = 0; j0 < ns; j0 += 64) {
+    const int j = j0 + lane;
+    const float m = j < ns ? rec0[(int64_t)j * R + D] : -INFINITY;
+    s.M = fmaxf(s.M, m);
+  }
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) s.M = fmaxf(s.M, __shfl_xor(s.M, o, 64));
+  for (int j0 = 0; j0 < ns; j0 += 64) {
+    const int j = j0 + lane;
+    const bool ok = j < ns;
+    const float4 t = ok ? *reinterpret_cast<const float4*>(rec0 + (int64_t)j * R + D)
+                        : make_float4(-INFINITY, 0.0f, 0.0f, 0.0f);
+    const float w = t.x == -INFINITY ? 0.0f : __expf(t.x - s.M);
+    reduce_stats<METER, VM>(s, w, t, VM && ok ? rec0[(int64_t)j * R + D + 4] : 0.0f);
+  }
+  return s;
+}
+
+// raw = (A-1)(A+1)/2 with A - 1 = n / l (+inf on overflow or a NaN numerator),
+// 0 without splits.
+__device__ __forceinline__ float raw_of(const SplitStats& s, int ns) {
+  if (ns <= 0) return 0.0f;
+  const float nt = isnan(s.n) ? INFINITY : s.n;
+  const float am1 = nt / s.l;
+  float raw = 0.5f * am1 * (2.0f + am1);
+  if (!(raw <= FLT_MAX)) raw = INFINITY;
+  return raw;
+}
+
+// Value meter: sum_t ptilde_t rho_t over the largest stored value norm (0/0 = 0).
+__device__ __forceinline__ float meter_v_of(const SplitStats& s, int ns) {
+  const float ev = ns > 0 ? s.e / s.l : 0.0f;
+  float mv = s.v > 0.0f ? ev / s.v : (ev > 0.0f ? INFINITY : 0.0f);
+  if (isnan(mv)) mv = INFINITY;
+  return mv;
+}
+
+// The gate of one query head: meter (raw for tau >= 1) above tau, or (joint
+// gate) the value meter above tau_v.
+__device__ __forceinline__ bool gated_of(float raw, float mv, float tau, bool vm, float tau_v) {
+  const float meter = fminf(1.0f, raw);
+  return (tau >= 1.0f ? raw : meter) > tau || (vm && mv > tau_v);
+}
+
+// Active splits of a sequence of length L.
+__device__ __forceinline__ int active_splits(int L, int split_tokens, int n_splits) {
+  return min((L + split_tokens - 1) / split_tokens, n_splits);
+}
+
+// Gate of one (sequence b, KV head kv) from the metered decode's records
+// (a.gate_part, the same split layout), evaluated by a 4-wave workgroup of the
+// exact fallback before it reads anything: each wave takes query heads wave,
+// wave + 4, ...; the workgroup of split 0 stores mask_q of the unit's heads and
+// mask_kv of the unit.  Returns whether the unit is routed (uniform over the
+// workgroup; contains a barrier).
+__device__ __forceinline__ bool unit_gate(const DecodeArgs& a, int b, int kv, int split, int wave, int lane,
+                                          int* flag_s) {
+  if (threadIdx.x == 0) *flag_s = 0;
+  __syncthreads();
+  const int64_t R = (int64_t)partial_record_floats(a.head_dim);
+  const float* base = a.gate_part + (int64_t)(b * a.n_q + kv * a.group) * a.n_splits * R;
+  bool any = false;
+  auto decide = [&](const SplitStats& s, int hh, int ns) {
+    const bool g = gated_of(raw_of(s, ns), 0.0f, a.gate_tau, false, 0.0f);
+    any |= g;
+    if (lane == 0 && split == 0) a.gate_mask_q[b * a.n_q + kv * a.group + hh] = g ? 1 : 0;
+  };
+  if (a.n_splits <= 64) {
+    // every head of this wave in one round trip (up to 4: G <= 16), the length too
+    const int jr = min(lane, a.n_splits - 1);
+    float4 t[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (wave + 4 * i < a.group)
+        t[i] = *reinterpret_cast<const float4*>(base + ((int64_t)(wave + 4 * i) * a.n_splits + jr) * R + a.head_dim);
+    const int ns = active_splits(a.seq_lens[b], a.split_tokens, a.n_splits);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (wave + 4 * i < a.group) decide(stats_of_lanes<true, false>(t[i], 0.0f, ns, lane), wave + 4 * i, ns);
+  } else {
+    const int ns = active_splits(a.seq_lens[b], a.split_tokens, a.n_splits);
+    for (int hh = wave; hh < a.group; hh += 4)
+      decide(split_stats<true, false>(base + (int64_t)hh * a.n_splits * R, R, a.head_dim, ns, a.n_splits, lane), hh,
+             ns);
+  }
+  if (any && lane == 0) atomicOr(flag_s, 1);
+  __syncthreads();
+  const bool routed = *flag_s != 0;
+  if (split == 0 && threadIdx.x == 0) a.gate_mask_kv[b * a.n_kv + kv] = routed ? 1 : 0;
+  return routed;
+}
+
+}  // namespace wc

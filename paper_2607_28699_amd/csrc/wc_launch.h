@@ -103,6 +103,13 @@ struct DecodeArgs {
   const uint8_t* repaired;
   const void* x_k_data;
   const void* x_v_data;
+  // certified step (metered decode, exact fallback, final merge): the exact
+  // fallback decides each unit's gate from the metered records gate_part (same
+  // split layout) in its prologue; the final merge takes routed heads' outputs
+  // from the exact records x_part (null: not in use)
+  const float* gate_part;
+  const float* x_part;
+  int no_merge;             // launch_decode: the decode kernel only (the merge comes later)
 };
 
 // Scale of channel c of the token in scale row `row` (page * 16 + offset): the
@@ -162,7 +169,7 @@ __device__ __forceinline__ DecodePos decode_position(int batch, int n_kv, int n_
 
 // Clears the gate outputs of one (sequence, KV head) ahead of the merge.
 __device__ __forceinline__ void gate_clear(const DecodeArgs& a, int unit, int split) {
-  if (a.gate_mask_q != nullptr && split == 0 && threadIdx.x == 0) {
+  if (a.gate_mask_q != nullptr && a.gate_part == nullptr && split == 0 && threadIdx.x == 0) {
     a.gate_mask_kv[unit] = 0;
     a.gate_unit[unit] = 0;
   }

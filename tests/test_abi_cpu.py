@@ -189,6 +189,36 @@ def test_step_call_argument_checks(L):
     assert step(ctypes.byref(ex), ctypes.byref(ex)) == _lib.WC_EINVAL         # the metered cache is quantized
 
 
+def test_certified_step_checks_and_workspace(L):
+    """wc_step_certified_decode: workspace = the metered decode's plus one more region
+    of split records; host checks before anything is launched."""
+    for args in [(4, 28, 4, 128, 32768, 0), (4, 28, 4, 128, 32768, 512), (64, 28, 4, 128, 32832, 1088)]:
+        b, nq, nkv, d, L_, st = args
+        base = L.wc_decode_workspace_size(*args)
+        split = L.wc_decode_split_tokens(b, nkv, L_, 0, st)
+        ns = (L_ + split - 1) // split
+        rec = (b * nq * ns * (d + 8) * 4 + 255) // 256 * 256
+        assert L.wc_certified_workspace_size(*args) == base + rec
+    assert L.wc_certified_workspace_size(-1, 28, 4, 128, 100, 0) == 0
+    c = _lib.WcCache(_lib.WC_KIND_INT8_DITHER, 128, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16, 0, 0,
+                     None, None, None, None)
+    ex = _lib.WcCache(_lib.WC_KIND_BF16, 128, 1, 0, 0, 0, 1, 0, 16, 16)
+    ex64 = _lib.WcCache(_lib.WC_KIND_BF16, 64, 1, 0, 0, 0, 1, 0, 16, 16)
+
+    def step(cache, exact, ws_bytes=1 << 30, tau=0.2, meter=16):
+        return L.wc_step_certified_decode(
+            cache, exact, 16, 16, _lib.WC_BF16, 16, 16, _lib.WC_BF16, 1, 7, 16, 4, 16, 64, 0.1, 16, 0,
+            meter, 16, 0, tau, 16, 16, None, 256, ws_bytes, None)
+    assert step(ctypes.byref(c), None) == _lib.WC_EINVAL                       # no exact cache
+    assert step(ctypes.byref(c), ctypes.byref(c)) == _lib.WC_EINVAL            # exact must be bf16
+    assert step(ctypes.byref(c), ctypes.byref(ex64)) == _lib.WC_EINVAL         # same head size
+    assert step(ctypes.byref(ex), ctypes.byref(ex)) == _lib.WC_EINVAL          # the metered cache is quantized
+    assert step(ctypes.byref(c), ctypes.byref(ex), tau=-1.0) == _lib.WC_EINVAL
+    assert step(ctypes.byref(c), ctypes.byref(ex), meter=None) == _lib.WC_EINVAL
+    need = L.wc_certified_workspace_size(1, 7, 1, 128, 64, 0)
+    assert step(ctypes.byref(c), ctypes.byref(ex), ws_bytes=need - 1) == _lib.WC_EWORKSPACE
+
+
 def test_noalloc_step_call_checks(L):
     """wc_step_metered_decode_gate_noalloc refuses sizes beyond its static scratch
     before touching any device, and a missing cache."""
