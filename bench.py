@@ -615,10 +615,58 @@ def main():
                                                  if fixed.any() else None),
             "whole_head_bytes": round(whole)}
 
+        # the exact store in host memory, as the paper's CPU copy (Sec. 6.3): two layers'
+        # exact caches in pinned host memory, read by the kernels over the host link;
+        # timed like the repair above: the whole-head fallback of the routed KV heads,
+        # and block repair (each minus the metered decode + gate over the same caches)
+        far_n = min(2, wl.n_layers)
+        exact_h = [exact[layer].host_copy() for layer in range(far_n)]
+        rws = wc.repair_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, REPAIR_BUDGET)
+
+        def far_base(i):
+            layer = i % far_n
+            wc.metered_decode_gate(byp_caches[layer], last["layers"][layer]["q"], table, last["lens"], max_len_all,
+                                   sm, args.tau, ws=ws, split_tokens=ST, out=out, meter=meter, raw=raw, mask_q=mq_b,
+                                   mask_kv=mkv_b)
+
+        def far_fallback(i):
+            far_base(i)
+            layer = i % far_n
+            wc.exact_decode_attention(exact_h[layer], last["layers"][layer]["q"], table, last["lens"], max_len_all,
+                                      sm, mkv_b, out, ws=ws, split_tokens=ST)
+
+        def far_repair(i):
+            # block repair, then the whole-head fallback of the KV heads it left routed
+            far_base(i)
+            layer = i % far_n
+            wc.block_repair(byp_caches[layer], exact_h[layer], last["layers"][layer]["q"], table, last["lens"],
+                            max_len_all, sm, args.tau, ws, out, meter, raw, mkv_b, max_blocks=REPAIR_BUDGET,
+                            split_tokens=ST, repaired=rlist, n_repaired=nrep, repair_ws=rws)
+            wc.exact_decode_attention(exact_h[layer], last["layers"][layer]["q"], table, last["lens"], max_len_all,
+                                      sm, mkv_b, out, ws=ws, split_tokens=ST)
+        fr = 2 * far_n
+        fb0 = float(np.median(timed(far_base, fr)))
+        ffb = max(float(np.median(timed(far_fallback, fr))) - fb0, 0.0)
+        frp = max(float(np.median(timed(far_repair, fr))) - fb0, 0.0)
+        nr_f = []
+        for layer in range(far_n):
+            far_repair(layer)
+            nr_f.append(nrep.clone())
+        nr_f = torch.cat(nr_f).flatten().cpu().numpy()
+        fixed_f = nr_f > 0
+        n_units = len(nr_f)
+        byp["repair_host_store"] = {
+            "layers": far_n, "exact_store": "pinned host memory, read by the kernels over the host link",
+            "fallback_median_ms": round(ffb, 4), "repair_median_ms": round(frp, 4),
+            "routed_kv_fraction": round(float((nr_f != 0).mean()), 4),
+            "repaired_fraction_of_routed": round(float(fixed_f.sum() / max((nr_f != 0).sum(), 1)), 4),
+            "exact_bytes_fallback": round(float((nr_f != 0).sum()) / n_units * lay.batch * wl.n_kv * whole),
+            "exact_bytes_repair": round(float(nr_f[fixed_f].sum()) / n_units * lay.batch * wl.n_kv * bs * BF16_BYTES)}
+        del exact_h, rws
+
         # group scales (Sec. 6.2 storage side, Table 4): the same bypass caches with one
         # fp16 scale per token and 32-channel group (8 bytes per side instead of 2),
-        # both tiers with the fused gate, and their meters; these decodes run on the
-        # vector ALUs
+        # both tiers with the fused gate, and their meters, on the matrix cores
         if gs_caches:
             ga_ms = timed(lambda i: wc.metered_decode_gate(
                 gs_caches[i % wl.n_layers], last["layers"][i % wl.n_layers]["q"], table, last["lens"],

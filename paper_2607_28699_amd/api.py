@@ -53,7 +53,9 @@ def cache_bytes(kind: str, num_blocks: int, n_kv: int, head_dim: int, n_bands: i
 
 @dataclass
 class PagedCache:
-    """One layer's paged cache in device memory (layout: include/witcert.h)."""
+    """One layer's paged cache in device memory (layout: include/witcert.h); with
+    host=True in pinned host memory, which the kernels read over the host link
+    (an exact store kept off the GPU, as the paper's CPU copy)."""
     kind: str
     num_blocks: int
     n_kv: int
@@ -68,6 +70,7 @@ class PagedCache:
     group_scales: bool = False
     tensors: dict = field(default_factory=dict)
     exact_store: object = None   # persistent repair: the bf16 PagedCache of marked pages
+    host: bool = False            # pinned host memory instead of device memory
 
     def __post_init__(self):
         m = self.n_outlier_pairs
@@ -98,13 +101,29 @@ class PagedCache:
                 self.tensors[n] = None
                 continue
             dt = el if n in ("k_data", "v_data") else torch.uint16
-            t = torch.zeros(shapes[n], dtype=dt, device=self.device)
+            if self.host:
+                t = torch.empty(shapes[n], dtype=dt, pin_memory=True)
+                t.zero_()
+            else:
+                t = torch.zeros(shapes[n], dtype=dt, device=self.device)
             assert t.numel() * t.element_size() == s, (n, s, slots)
             self.tensors[n] = t
         self.total_bytes = total
         # bypassed RoPE pairs per KV head (set with set_outlier_pairs before writing)
         self.tensors["outlier_pairs"] = (
             torch.arange(m, dtype=torch.int32, device=self.device).repeat(self.n_kv, 1) if m else None)
+
+    def host_copy(self) -> "PagedCache":
+        """The same cache, contents included, in pinned host memory."""
+        c = PagedCache(self.kind, self.num_blocks, self.n_kv, self.head_dim, self.n_bands, self.layer, self.seed,
+                       self.rope_layout, self.device, self.n_outlier_pairs, self.value_side, self.group_scales,
+                       host=True)
+        for n, t in self.tensors.items():
+            if t is not None and n != "outlier_pairs":
+                c.tensors[n].copy_(t)
+        if self.tensors.get("outlier_pairs") is not None:
+            c.tensors["outlier_pairs"].copy_(self.tensors["outlier_pairs"])
+        return c
 
     def set_outlier_pairs(self, pairs: torch.Tensor) -> None:
         """pairs [n_kv, m] int32, ascending per row (e.g. from select_outlier_pairs)."""
