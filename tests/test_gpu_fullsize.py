@@ -2,8 +2,10 @@
 
 One layer of each long-context workload is prefilled through
 wc_quantize_write_pair (quantized cache and bf16 exact copy), then one decode step
-runs through wc_step_metered_decode_gate -- the call bench.py times, the step's
-token written by the decode kernel itself -- with bench.py's split choice
+runs through wc_step_metered_decode_gate -- the step's token written by the
+decode kernel itself -- and through wc_step_certified_decode, the call bench.py
+times (the same step with the exact fallback: meters and masks bit-identical, a
+routed head's output exact attention), with bench.py's split choice
 (max_seq_len = prefill + steps + warmup, the split balanced over the batch's
 total tokens; the serving mix with all 64 sequences).  Sampled (sequence, query
 head) cells, the shortest and the longest sequence among them, are recomputed by
@@ -126,6 +128,26 @@ def test_fullsize_sampled_cells(name):
         gx = S.read_cache(exact, sl[pick])
         kin = kv[b][0][:, g].float().cpu().numpy()[pick]
         assert np.array_equal(S.bf16_bits_to_f32(gx["k"][:, g]), kin)
+    # the certified step (what bench.py times) on the same caches: the step's token is
+    # written again with the same bytes; meters and masks as above, bit for bit; a
+    # routed KV head's rows are exact attention, the others the metered rows
+    ws = wc.certified_workspace(len(lens0), wl.n_q, wl.n_kv, wl.d, max_len, st)
+    c_out, c_meter, c_raw, c_mq, c_mk = wc.step_certified_decode(cache, exact, nk, nv, ns, q, tab, lens, max_len, sm,
+                                                                 tau, split_tokens=st, ws=ws)
+    torch.cuda.synchronize()
+    c_out = c_out.cpu().numpy()
+    assert np.array_equal(c_meter.cpu().numpy(), meter) and np.array_equal(c_raw.cpu().numpy(), raw)
+    assert np.array_equal(c_mq.cpu().numpy(), mask_q) and np.array_equal(c_mk.cpu().numpy(), mask_kv)
+    unrouted = np.repeat(mask_kv == 0, wl.group, axis=1)
+    assert np.array_equal(c_out[unrouted], out[unrouted])
+    for b, h in cells:
+        if mask_kv[b, h // wl.group]:
+            k, v, _ = kv[b]
+            g = h // wl.group
+            ex = odec.exact_decode(q[b, h:h + 1].float().cpu().numpy().astype(np.float64),
+                                   k[:, g:g + 1].float().cpu().numpy().astype(np.float64),
+                                   v[:, g:g + 1].float().cpu().numpy().astype(np.float64), sm)["out"]
+            assert S.rel_err(c_out[b, h], ex[0]) <= 2e-3, (b, h)
 
 
 def test_matrix_core_and_vector_paths_agree():
