@@ -1,8 +1,9 @@
 /*
  * witcert.h -- C-ABI of the WitCert hot path on MI355X (gfx950).
  *
- * WitCert meters, per (layer, head, decode step), a sound upper bound on the
- * total variation between exact and compressed softmax attention (paper:
+ * WitCert meters, per (layer, head, decode step), a provable bound on how far
+ * the softmax attention over the compressed cache can move, in total-variation
+ * distance, from the one over the uncompressed cache (paper:
  * "WitCert: Sound Runtime Risk Observability and Gating for KV-Cache
  * Quantization").  This library implements the meter loop of Sec. 6:
  *

@@ -2,8 +2,8 @@
 
 TEST INFRASTRUCTURE ONLY (see the package header).
 
-Definitions followed (Sec. 6.2, storage side: the serving store scales each
-token per group of G_c channels, G_c = 32 the default; Table 4 (granularity):
+Definitions followed (Sec. 6.2, storage side: the serving store keeps, for each
+token, one scale per run of G_c consecutive channels, G_c = 32 by default; Table 4 (granularity):
 272 bytes per token and KV head for K + V at G_c = 32, i.e. per side 128 codes
 and four 2-byte scales; Sec. 4.2 subtractive dither and Tier B, whose proxy sums
 q_c^2 s_c^2 over the channels):

@@ -4,7 +4,8 @@ Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3",
 SC'11, Sec. 3 (the Philox S-box family).  The paper draws its dither from this
 generator with a tuple counter so that the read side can regenerate exactly what
 the write side used (Sec. 6.2, research kernels: five-tuple counter; Sec. 6.2,
-storage side: the counter uses the slot, not the sequence position).
+storage side: the counter holds the cache slot rather than the token's position
+in its sequence).
 
 One round on a 4x32-bit counter (x0, x1, x2, x3) with 2x32-bit key (k0, k1):
     (hi0, lo0) = M0 * x0 as a 64-bit product,  (hi1, lo1) = M1 * x2
