@@ -120,3 +120,37 @@ def test_blackbox_witness(dts, layout):
     ref = oq.witness(x.double().numpy(), xh.double().numpy(), 16, layout)
     got = w.cpu().double().numpy()
     assert np.array_equal(got, ref)
+
+
+def test_witness_round_up_at_fp16_boundaries():
+    """Band norms at and next to fp16 values round up as in the oracle: norms that
+    are fp16 values, one part in 2^20 above and below them, norms within 2^-50 of a
+    square (where the kernels take the float64 root), zero, fp16 subnormals, tiny
+    residuals whose squares leave the float32 range, and norms past 65504."""
+    import torch
+
+    import paper_2607_28699_amd as wc
+    d, B = 128, 16
+    band = oq.band_index(d, B, "half")
+    chans = [np.flatnonzero(band == b) for b in range(B)]
+    rng = np.random.default_rng(11)
+    fp16 = np.unique(np.abs(rng.standard_normal(200).astype(np.float16)).astype(np.float64))
+    special = [1.0, 1.5, 2.0 ** -14, 2.0 ** -24, 3 * 2.0 ** -24, 2048.0, 65504.0]
+    cases = []   # the nonzero residuals of one band
+    for h in list(fp16[fp16 > 0][:60]) + special:
+        cases += [(h,), (h * (1 + 2.0 ** -20),), (h * (1 - 2.0 ** -20),)]
+    cases += [(1.0, 2.0 ** -25), (2.0, 2.0 ** -24), (1 - 2.0 ** -24,), (0.0,), (2.0 ** -30,), (2.0 ** -70,),
+              (2.0 ** -100,), (3.0, 4.0), (70000.0,), (65504.0, 256.0), (65504.0 * (1 + 2.0 ** -20),)]
+    rows = (len(cases) + B - 1) // B
+    xh = np.zeros((rows, d), np.float32)
+    for i, c in enumerate(cases):
+        r, b = divmod(i, B)
+        for j, val in enumerate(c):
+            xh[r, chans[b][j]] = np.float32(val)
+    x = np.zeros_like(xh)
+    S.say(f"[witness] fp16 boundaries: {len(cases)} bands")
+    w = wc.witness(torch.from_numpy(x).cuda(), torch.from_numpy(xh).cuda(), B, "half")
+    torch.cuda.synchronize()
+    ref = oq.witness(x.astype(np.float64), xh.astype(np.float64), B, "half")
+    got = w.cpu().double().numpy()
+    assert np.array_equal(got, ref), np.argwhere(got != ref)[:8]
