@@ -382,30 +382,37 @@ def main():
     mask_kv = torch.empty((lay.batch, wl.n_kv), dtype=torch.uint8, device=dev)
     counts = torch.zeros(2, dtype=torch.int32, device=dev)
 
-    def run_step(si):
+    def run_step(si, speculative):
         st = steps_in[si]
+        step_call = wc.step_certified_decode_speculative if speculative else wc.step_certified_decode
         for layer in range(wl.n_layers):
             it = st["layers"][layer]
             # new tokens into the quantized cache and the exact bf16 copy in one pass
             if wl.chunk:
                 wc.quantize_write_pair(caches[layer], exact[layer], it["ck"], it["cv"], it["cslots"])
             # the step's token of every sequence into the quantized cache and the exact
-            # copy with the metered decode (one launch), the exact fallback whose
-            # workgroups decide their KV head's gate first, and one final merge
-            wc.step_certified_decode(caches[layer], exact[layer], it["k"], it["v"], st["slots"], it["q"],
-                                     table, st["lens"], max_len_all, sm, args.tau, ws=ws_step, split_tokens=ST,
-                                     out=out, meter=meter, raw=raw, mask_q=mask_q, mask_kv=mask_kv,
-                                     n_gated=counts)
+            # copy with the metered decode, the exact fallback (gated: its workgroups
+            # decide their KV head's gate first; speculative: every KV head, beside the
+            # metered decode) and one final merge
+            step_call(caches[layer], exact[layer], it["k"], it["v"], st["slots"], it["q"],
+                      table, st["lens"], max_len_all, sm, args.tau, ws=ws_step, split_tokens=ST,
+                      out=out, meter=meter, raw=raw, mask_q=mask_q, mask_kv=mask_kv, n_gated=counts)
 
+    # The step form a serving loop would pick from what it observed: the speculative
+    # one when the previous step's gate routed at least half of the KV heads (here:
+    # the first step, run gated before the graphs are captured).
+    counts.zero_()
+    run_step(0, False)
+    torch.cuda.synchronize()
+    first_routed = float(counts[1].item()) / (wl.n_layers * lay.batch * wl.n_kv)
+    speculative = first_routed >= 0.5
     # one decode step per HIP graph (all layers), replayed back to back: the timed
     # region is GPU work only, as in a graph-captured serving loop
-    run_step(0)
-    torch.cuda.synchronize()
     graphs = []
     for s in range(K + W):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            run_step(s)
+            run_step(s, speculative)
         graphs.append(g)
     for s in range(W):
         graphs[s].replay()
@@ -787,7 +794,11 @@ def main():
                    "head_dim": wl.d, "bands": wl.bands, "batch": lay.batch,
                    "context": int(lens0.max()), "mean_context": float(lens0.mean()),
                    "tau": args.tau, "split_tokens": ST, "cache": "int8 dither + fp16 scales + fp16 key witness",
-                   "fallback": "bf16 exact cache in HBM"},
+                   "fallback": "bf16 exact cache in HBM",
+                   "step": ("certified, speculative (exact fallback of every KV head beside the metered decode, "
+                            "gate in the final merge)" if speculative else
+                            "certified, gated (exact fallback of the routed KV heads after the metered decode)"),
+                   "first_step_routed_kv_fraction": round(first_routed, 4)},
         "roofline": roof,
         "roofline_exact_fallback": roof_fb,
         "value_note": ("KV tokens attended per second over whole decode steps; each step includes the bf16 "

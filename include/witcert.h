@@ -24,7 +24,8 @@
  *               wc_exact_decode_attention
  *                                   exact attention from an uncompressed bf16 cache for
  *                                   the routed heads (the fallback of the meter loop)
- *   step        wc_step_metered_decode_gate, wc_step_certified_decode
+ *   step        wc_step_metered_decode_gate, wc_step_certified_decode,
+ *               wc_step_certified_decode_speculative
  *                                   a decode step's token write with the read path and
  *                                   gate (and, certified, the exact fallback) fused
  *               wc_block_repair     repair of routed heads from the exact cache at block
@@ -535,6 +536,31 @@ int wc_step_certified_decode(const wc_cache* cache, const wc_cache* exact, const
                              float sm_scale, void* out, int out_dtype, float* meter, float* raw,
                              int split_tokens, float tau, uint8_t* mask_q, uint8_t* mask_kv,
                              int32_t* n_gated, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * wc_step_certified_decode for steps where most KV heads are routed: the exact
+ * fallback of EVERY KV head runs beside the metered decode instead of after it, and
+ * the final merge decides the gate (Sec. 6 meter loop; the same gate, any of a KV
+ * head's query heads above tau, from the same statistics) and takes each routed KV
+ * head's rows from the exact records.  Results are bit for bit those of
+ * wc_step_certified_decode (out, meter, raw, mask_q, mask_kv, n_gated and both
+ * caches); only the work differs.  With a plain Tier A cache (INT8 dithered or raw
+ * fp8, no bypassed pairs, group scales, value side or repair marks), bf16 queries
+ * and head_dim 128 both decodes share one launch, their workgroups interleaved on
+ * every compute unit, and each writes the step's new tokens (bf16 inputs) into the
+ * cache it reads; otherwise the two decodes run one after the other.  It reads the
+ * whole exact cache of the active tokens (512 bytes per token and KV head at
+ * head_dim 128) whatever the gate decides: the caller picks it when the routed
+ * fraction it observes (n_gated) is high.  Arguments, workspace and checks as
+ * wc_step_certified_decode.
+ */
+int wc_step_certified_decode_speculative(const wc_cache* cache, const wc_cache* exact, const void* new_k,
+                                         const void* new_v, int in_dtype, const int64_t* new_slots, const void* q,
+                                         int q_dtype, int batch, int n_q_heads, const int32_t* block_table,
+                                         int max_blocks_per_seq, const int32_t* seq_lens, int64_t max_seq_len,
+                                         float sm_scale, void* out, int out_dtype, float* meter, float* raw,
+                                         int split_tokens, float tau, uint8_t* mask_q, uint8_t* mask_kv,
+                                         int32_t* n_gated, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * For callers that cannot allocate device memory (code under HIP graph capture,

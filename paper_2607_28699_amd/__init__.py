@@ -19,6 +19,7 @@ from .api import (  # noqa: F401
     metered_decode_gate,
     step_metered_decode_gate,
     step_certified_decode,
+    step_certified_decode_speculative,
     certified_workspace,
     step_metered_decode_gate_noalloc,
     quantize_write,

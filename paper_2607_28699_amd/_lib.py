@@ -25,6 +25,7 @@ EXPORTS = (
     "wc_tierb_decode_attention", "wc_tierb_delta_loc", "wc_joint_decode_gate", "wc_gate",
     "wc_exact_decode_attention", "wc_block_repair", "wc_block_repair_workspace_size",
     "wc_repair_write_back", "wc_certified_workspace_size", "wc_step_certified_decode",
+    "wc_step_certified_decode_speculative",
 )
 
 
@@ -94,6 +95,10 @@ def lib() -> ctypes.CDLL:
                                                     ctypes.c_int, ctypes.c_int, vp, ctypes.c_int, vp, i64,
                                                     f32, vp, ctypes.c_int, vp, vp, ctypes.c_int, f32, vp,
                                                     vp, vp, vp, sz, vp]),
+        "wc_step_certified_decode_speculative": (ctypes.c_int, [cp, cp, vp, vp, ctypes.c_int, vp, vp, ctypes.c_int,
+                                                                ctypes.c_int, ctypes.c_int, vp, ctypes.c_int, vp,
+                                                                i64, f32, vp, ctypes.c_int, vp, vp, ctypes.c_int,
+                                                                f32, vp, vp, vp, vp, sz, vp]),
         "wc_step_metered_decode_gate_noalloc": (ctypes.c_int, [cp, cp, vp, vp, ctypes.c_int, vp, vp,
                                                                ctypes.c_int, ctypes.c_int, ctypes.c_int, vp,
                                                                ctypes.c_int, vp, i64, f32, vp, ctypes.c_int, vp,

@@ -334,14 +334,8 @@ def certified_workspace(batch: int, n_q: int, n_kv: int, head_dim: int, max_seq_
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
-def step_certified_decode(cache: PagedCache, exact: PagedCache, new_k: torch.Tensor, new_v: torch.Tensor,
-                          new_slots: torch.Tensor, q: torch.Tensor, block_table: torch.Tensor,
-                          seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float, tau: float,
-                          out_dtype=torch.float32, split_tokens: int = 0, ws=None, out=None, meter=None,
-                          raw=None, mask_q=None, mask_kv=None, n_gated=None):
-    """One whole decode step: step_metered_decode_gate, then exact_decode_attention
-    of the routed KV heads, in three launches (the gate decided in the exact
-    fallback's prologue) -> (out, meter, raw, mask_q, mask_kv)."""
+def _certified(fn_name, cache, exact, new_k, new_v, new_slots, q, block_table, seq_lens, max_seq_len, sm_scale,
+               tau, out_dtype, split_tokens, ws, out, meter, raw, mask_q, mask_kv, n_gated):
     _dev_check(q, block_table, seq_lens, new_k, new_v, new_slots)
     batch, n_q, d = q.shape
     assert new_slots.dtype == torch.int64 and new_k.shape == new_v.shape == (batch, cache.n_kv, d)
@@ -355,13 +349,39 @@ def step_certified_decode(cache: PagedCache, exact: PagedCache, new_k: torch.Ten
     mask_kv = (torch.empty((batch, cache.n_kv), dtype=torch.uint8, device=q.device)
                if mask_kv is None else mask_kv)
     c, e = cache.struct(), exact.struct()
-    check(lib().wc_step_certified_decode(
+    check(getattr(lib(), fn_name)(
         ctypes.byref(c), ctypes.byref(e), _ptr(new_k), _ptr(new_v), _dt(new_k), _ptr(new_slots), _ptr(q),
         _dt(q), batch, n_q, _ptr(block_table), block_table.shape[1], _ptr(seq_lens), max_seq_len,
         float(sm_scale), _ptr(out), _dt(out), _ptr(meter), _ptr(raw), split_tokens, float(tau),
-        _ptr(mask_q), _ptr(mask_kv), _ptr(n_gated), _ptr(ws), ws.numel(), _stream()),
-        "wc_step_certified_decode")
+        _ptr(mask_q), _ptr(mask_kv), _ptr(n_gated), _ptr(ws), ws.numel(), _stream()), fn_name)
     return out, meter, raw, mask_q, mask_kv
+
+
+def step_certified_decode(cache: PagedCache, exact: PagedCache, new_k: torch.Tensor, new_v: torch.Tensor,
+                          new_slots: torch.Tensor, q: torch.Tensor, block_table: torch.Tensor,
+                          seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float, tau: float,
+                          out_dtype=torch.float32, split_tokens: int = 0, ws=None, out=None, meter=None,
+                          raw=None, mask_q=None, mask_kv=None, n_gated=None):
+    """One whole decode step: step_metered_decode_gate, then exact_decode_attention
+    of the routed KV heads, in three launches (the gate decided in the exact
+    fallback's prologue) -> (out, meter, raw, mask_q, mask_kv)."""
+    return _certified("wc_step_certified_decode", cache, exact, new_k, new_v, new_slots, q, block_table, seq_lens,
+                      max_seq_len, sm_scale, tau, out_dtype, split_tokens, ws, out, meter, raw, mask_q, mask_kv,
+                      n_gated)
+
+
+def step_certified_decode_speculative(cache: PagedCache, exact: PagedCache, new_k: torch.Tensor,
+                                      new_v: torch.Tensor, new_slots: torch.Tensor, q: torch.Tensor,
+                                      block_table: torch.Tensor, seq_lens: torch.Tensor, max_seq_len: int,
+                                      sm_scale: float, tau: float, out_dtype=torch.float32, split_tokens: int = 0,
+                                      ws=None, out=None, meter=None, raw=None, mask_q=None, mask_kv=None,
+                                      n_gated=None):
+    """step_certified_decode with the exact fallback of every KV head beside the
+    metered decode (one launch where the kernels allow it) and the gate decided in
+    the final merge: the same results, for steps where most KV heads are routed."""
+    return _certified("wc_step_certified_decode_speculative", cache, exact, new_k, new_v, new_slots, q,
+                      block_table, seq_lens, max_seq_len, sm_scale, tau, out_dtype, split_tokens, ws, out, meter,
+                      raw, mask_q, mask_kv, n_gated)
 
 
 def step_metered_decode_gate_noalloc(cache: PagedCache, exact: PagedCache, new_k: torch.Tensor,

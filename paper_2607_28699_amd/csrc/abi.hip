@@ -91,7 +91,7 @@ const char* wc_strerror(int status) {
   }
 }
 
-int wc_version(void) { return 104; }   // 1.4: certified step (wc_step_certified_decode)
+int wc_version(void) { return 105; }   // 1.5: speculative certified step
 
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim, int n_bands,
                       int n_outlier_pairs, int value_side, int group_scales, size_t sizes[8]) {
@@ -471,12 +471,16 @@ size_t wc_certified_workspace_size(int batch, int n_q_heads, int n_kv_heads, int
 // region of the workspace; no block segments: this call repairs nothing), the
 // exact fallback with the gate decided in its prologue from those records
 // (records in the second region), the final merge.
-int wc_step_certified_decode(const wc_cache* cache, const wc_cache* exact, const void* new_k, const void* new_v,
-                             int in_dtype, const int64_t* new_slots, const void* q, int q_dtype, int batch,
-                             int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
-                             const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out,
-                             int out_dtype, float* meter, float* raw, int split_tokens, float tau, uint8_t* mask_q,
-                             uint8_t* mask_kv, int32_t* n_gated, void* ws, size_t ws_bytes, void* stream) {
+// The certified step (spec = false: the exact fallback decides each unit's gate in
+// its prologue and reads the routed units) or its speculative form (spec = true:
+// the exact fallback of every unit runs beside the metered decode, in one launch
+// where the kernels allow it, and the final merge decides the gates).
+static int certified_step(const wc_cache* cache, const wc_cache* exact, const void* new_k, const void* new_v,
+                          int in_dtype, const int64_t* new_slots, const void* q, int q_dtype, int batch,
+                          int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                          const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out, int out_dtype,
+                          float* meter, float* raw, int split_tokens, float tau, uint8_t* mask_q, uint8_t* mask_kv,
+                          int32_t* n_gated, void* ws, size_t ws_bytes, void* stream, bool spec) {
   if (cache == nullptr || exact == nullptr) return WC_EINVAL;
   wc::WriteArgs w;
   int s = write_args(cache, exact, new_k, new_v, in_dtype, new_slots, batch, w);
@@ -510,27 +514,49 @@ int wc_step_certified_decode(const wc_cache* cache, const wc_cache* exact, const
   am.gate_unit = nullptr;
   if (batch == 0) return WC_OK;
   const hipStream_t hs = static_cast<hipStream_t>(stream);
-  // 1. the metered decode (with the step's tokens written first), no merge
   am.no_merge = 1;
-  hipError_t e = hipSuccess;
-  if (wc::step_write_fusable(am) && in_dtype == WC_BF16) {
-    am.sw = w;
-    am.step_write = 1;
-  } else {
-    e = wc::launch_quantize_write(w, hs);
-  }
-  if (e == hipSuccess) e = wc::launch_decode(am, true, hs);
-  // 2. the exact fallback: each unit's gate from the metered records, then the
-  //    routed units' exact records
   ax.no_merge = 1;
-  ax.gate_part = am.part;
-  ax.gate_tau = tau;
-  ax.gate_mask_q = mask_q;
-  ax.gate_mask_kv = mask_kv;
-  if (e == hipSuccess) e = wc::launch_decode(ax, false, hs);
+  hipError_t e = hipSuccess;
+  const bool fuse_write = wc::step_write_fusable(am) && in_dtype == WC_BF16;
+  if (spec && wc::spec_decode_fusable(am, ax)) {
+    // 1-2. one launch: the metered decode and the exact fallback of every unit, each
+    //      writing the step's tokens into the cache it reads first
+    if (fuse_write) {
+      wc::WriteArgs wx;
+      s = write_args(cache, nullptr, new_k, new_v, in_dtype, new_slots, batch, am.sw);
+      if (s == WC_OK) s = write_args(exact, nullptr, new_k, new_v, in_dtype, new_slots, batch, wx);
+      if (s != WC_OK) return s;
+      am.step_write = 1;
+      ax.sw = wx;
+      ax.step_write = 1;
+    } else {
+      e = wc::launch_quantize_write(w, hs);
+    }
+    if (e == hipSuccess) e = wc::launch_decode_spec(am, ax, hs);
+  } else {
+    // 1. the metered decode (with the step's tokens written first), no merge
+    if (fuse_write) {
+      am.sw = w;
+      am.step_write = 1;
+    } else {
+      e = wc::launch_quantize_write(w, hs);
+    }
+    if (e == hipSuccess) e = wc::launch_decode(am, true, hs);
+    // 2. the exact fallback: each unit's gate from the metered records, then the
+    //    routed units' exact records (speculative: every unit's, no gate)
+    if (!spec) {
+      ax.gate_part = am.part;
+      ax.gate_tau = tau;
+      ax.gate_mask_q = mask_q;
+      ax.gate_mask_kv = mask_kv;
+    }
+    if (e == hipSuccess) e = wc::launch_decode(ax, false, hs);
+  }
   // 3. the final merge: routed heads from the exact records, the others from the
-  //    metered ones; meter and raw from the metered records
+  //    metered ones; meter and raw from the metered records (speculative: the merge
+  //    decides the gates from the metered records)
   wc::DecodeArgs af = am;
+  af.step_write = 0;
   af.no_merge = 0;
   af.x_part = ax.part;
   af.meter = meter;
@@ -539,8 +565,35 @@ int wc_step_certified_decode(const wc_cache* cache, const wc_cache* exact, const
   af.gate_mask_kv = mask_kv;
   af.gate_count = n_gated;
   af.gate_tau = tau;
+  if (spec) {
+    af.gate_part = am.part;
+    af.merge_gate = 1;
+  }
   if (e == hipSuccess) e = wc::launch_merge(af, true, hs);
   return hip_status(e);
+}
+
+int wc_step_certified_decode(const wc_cache* cache, const wc_cache* exact, const void* new_k, const void* new_v,
+                             int in_dtype, const int64_t* new_slots, const void* q, int q_dtype, int batch,
+                             int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
+                             const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out,
+                             int out_dtype, float* meter, float* raw, int split_tokens, float tau, uint8_t* mask_q,
+                             uint8_t* mask_kv, int32_t* n_gated, void* ws, size_t ws_bytes, void* stream) {
+  return certified_step(cache, exact, new_k, new_v, in_dtype, new_slots, q, q_dtype, batch, n_q_heads, block_table,
+                        max_blocks_per_seq, seq_lens, max_seq_len, sm_scale, out, out_dtype, meter, raw,
+                        split_tokens, tau, mask_q, mask_kv, n_gated, ws, ws_bytes, stream, false);
+}
+
+int wc_step_certified_decode_speculative(const wc_cache* cache, const wc_cache* exact, const void* new_k,
+                                         const void* new_v, int in_dtype, const int64_t* new_slots, const void* q,
+                                         int q_dtype, int batch, int n_q_heads, const int32_t* block_table,
+                                         int max_blocks_per_seq, const int32_t* seq_lens, int64_t max_seq_len,
+                                         float sm_scale, void* out, int out_dtype, float* meter, float* raw,
+                                         int split_tokens, float tau, uint8_t* mask_q, uint8_t* mask_kv,
+                                         int32_t* n_gated, void* ws, size_t ws_bytes, void* stream) {
+  return certified_step(cache, exact, new_k, new_v, in_dtype, new_slots, q, q_dtype, batch, n_q_heads, block_table,
+                        max_blocks_per_seq, seq_lens, max_seq_len, sm_scale, out, out_dtype, meter, raw,
+                        split_tokens, tau, mask_q, mask_kv, n_gated, ws, ws_bytes, stream, true);
 }
 
 int wc_joint_decode_gate(const wc_cache* cache, const void* q, int q_dtype, int batch,

@@ -831,22 +831,37 @@ __device__ __forceinline__ void step_write(const DecodeArgs& a, int b, int kv, i
 
 // REP: the cache carries repair marks (a.repaired set; a quantized kind), a
 // separate instantiation so that caches without marks run the loop unchanged.
+// The workgroup's LDS: the dither rows of a page (INT8 caches), the query band
+// norms, the waves' output rows and scalars for the in-workgroup merge, the
+// queries (bf16 rows of 256 bytes, +16 pad) and the certified step's gate flag.
+template <int KIND>
+struct DecodeLds {
+  __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
+  float qn_s[kWaves][16][16];
+  __attribute__((aligned(16))) float acc_s[kWaves][16][kD];
+  float ml_s[kWaves][16][6];
+  uint4 q_lds[16][17];
+  int gate_flag_s;
+};
+
+// One workgroup of the decode: linear workgroup index lin (decode_position_at).
 template <int KIND, bool METER, bool HALF, bool TB, bool BYP, bool VM, bool REP, bool GS>
-__global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
-  __shared__ float qn_s[kWaves][16][16];
-  __shared__ __attribute__((aligned(16))) float acc_s[kWaves][16][kD];
-  __shared__ float ml_s[kWaves][16][6];
-  __shared__ uint4 q_lds[16][17];   // the workgroup's queries, bf16 rows of 256 bytes (+16 pad)
-  __shared__ int gate_flag_s;       // certified step: the unit's gate (exact fallback's prologue)
+__device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, DecodeLds<KIND>& lds) {
+  auto& dsh = lds.dsh;
+  auto& qn_s = lds.qn_s;
+  auto& acc_s = lds.acc_s;
+  auto& ml_s = lds.ml_s;
+  auto& q_lds = lds.q_lds;
+  int& gate_flag_s = lds.gate_flag_s;
   // a decode step's new token is written by the plain Tier A variants (the ones the
-  // step call fuses; the others keep their registers)
-  constexpr bool kStep = METER && !TB && !BYP && !VM && !GS;
+  // step call fuses; the others keep their registers) and, in the speculative
+  // certified step, into the exact cache by the exact fallback
+  constexpr bool kStep = (METER && !TB && !BYP && !VM && !GS) || (KIND == WC_KIND_BF16 && !REP);
 
   // the wave index is uniform: page addresses then live in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
-  const DecodePos pos = decode_position(a.batch, a.n_kv, a.n_splits);
+  const DecodePos pos = decode_position_at(lin, a.batch, a.n_kv, a.n_splits);
   const int unit = __builtin_amdgcn_readfirstlane(pos.unit), split = __builtin_amdgcn_readfirstlane(pos.split);
   const int b = unit / a.n_kv, kv = unit % a.n_kv;
   gate_clear(a, unit, split);
@@ -1389,6 +1404,41 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
     }
   }
 
+}
+
+template <int KIND, bool METER, bool HALF, bool TB, bool BYP, bool VM, bool REP, bool GS>
+__global__ __launch_bounds__(256, 2) void decode_mfma_kernel(DecodeArgs a) {
+  __shared__ DecodeLds<KIND> lds;
+  decode_block<KIND, METER, HALF, TB, BYP, VM, REP, GS>(a, blockIdx.x + gridDim.x * blockIdx.y, lds);
+}
+
+// Speculative certified step: the metered decode (KIND_M, Tier A) and the exact
+// fallback of every unit in one launch of 2 nb workgroups (nb = n_splits x batch x
+// n_kv each).  Linear index j: groups of eight alternate between the two decodes
+// (group 2i to the metered one, 2i + 1 to the exact one), each keeping its own
+// linear order within every XCD (j mod 8); the last partial group of each follows.
+// Every compute unit then holds both kinds, the metered decode's vector and matrix
+// work beside the exact fallback's memory streaming.
+template <int KIND_M, bool HALF>
+__global__ __launch_bounds__(256, 2) void decode_spec_kernel(DecodeArgs am, DecodeArgs ax, uint32_t nb) {
+  __shared__ DecodeLds<WC_KIND_INT8_DITHER> lds;   // (the largest layout)
+  const uint32_t j = blockIdx.x, full = nb / 8u * 8u;
+  bool metered;
+  uint32_t lin;
+  if (j < 2u * full) {
+    metered = ((j >> 3) & 1u) == 0;
+    lin = (j >> 4) * 8u + (j & 7u);
+  } else {
+    const uint32_t rest = nb - full, k = j - 2u * full;
+    metered = k < rest;
+    lin = full + (metered ? k : k - rest);
+  }
+  if (metered)
+    decode_block<KIND_M, true, HALF, false, false, false, false, false>(
+        am, lin, reinterpret_cast<DecodeLds<KIND_M>&>(lds));
+  else
+    decode_block<WC_KIND_BF16, false, HALF, false, false, false, false, false>(
+        ax, lin, reinterpret_cast<DecodeLds<WC_KIND_BF16>&>(lds));
 }
 
 }  // namespace

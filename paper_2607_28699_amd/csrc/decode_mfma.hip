@@ -40,6 +40,27 @@ void launch_decode_mfma_r(const DecodeArgs& a, bool metered, bool tb, bool byp, 
   else launch_decode_mfma_g<HALF, VM, false>(a, metered, tb, byp, grid, block, st);
 }
 
+bool spec_decode_fusable(const DecodeArgs& am, const DecodeArgs& ax) {
+  return am.use_mfma && ax.use_mfma && mfma_decode_supported(am) && mfma_decode_supported(ax) &&
+         (am.kind == WC_KIND_INT8_DITHER || am.kind == WC_KIND_FP8_RAW) && ax.kind == WC_KIND_BF16 &&
+         am.tierb_delta <= 0.0f && am.meter_v == nullptr && am.n_pairs == 0 && am.group_scales == 0 &&
+         am.repaired == nullptr && am.group == ax.group && am.n_splits == ax.n_splits;
+}
+
+hipError_t launch_decode_spec(const DecodeArgs& am, const DecodeArgs& ax, hipStream_t st) {
+  const uint32_t nb = (uint32_t)am.n_splits * (uint32_t)am.batch * (uint32_t)am.n_kv;
+  const dim3 grid(2 * nb), block(64 * kWaves);
+  const bool fp8 = am.kind == WC_KIND_FP8_RAW;
+  if (am.group <= 8) {
+    if (fp8) hipLaunchKernelGGL((decode_spec_kernel<WC_KIND_FP8_RAW, true>), grid, block, 0, st, am, ax, nb);
+    else hipLaunchKernelGGL((decode_spec_kernel<WC_KIND_INT8_DITHER, true>), grid, block, 0, st, am, ax, nb);
+  } else {
+    if (fp8) hipLaunchKernelGGL((decode_spec_kernel<WC_KIND_FP8_RAW, false>), grid, block, 0, st, am, ax, nb);
+    else hipLaunchKernelGGL((decode_spec_kernel<WC_KIND_INT8_DITHER, false>), grid, block, 0, st, am, ax, nb);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st) {
   const dim3 grid(a.n_splits, a.batch * a.n_kv);   // workgroup order: decode_position()
   const dim3 block(64 * kWaves);

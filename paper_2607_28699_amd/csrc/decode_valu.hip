@@ -483,6 +483,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
 // numerators) come from split_stats (merge_dev.h), in the same bits wherever they
 // are formed.
 constexpr int kMergeWaves = 4;   // waves per merge workgroup when a head has more than 32 splits
+static_assert(kMergeWaves == 4, "the merge that decides the gate runs unit_gate on four waves");
 
 // The statistics a merge needs: of the output rows (so; the exact records of a
 // routed head in a certified step's final merge) and of the metered records for
@@ -516,11 +517,15 @@ __device__ __forceinline__ void merge_stats(const float* rec0, const float* src0
 // Final merge of a certified step (a.x_part set): the heads of a routed KV head
 // (gate_mask_kv, stored by the exact fallback's prologue) take their output from
 // the exact records, the others from the metered ones; meter and raw always from
-// the metered records.
+// the metered records.  Speculative certified step (a.merge_gate, four waves):
+// the exact records cover every unit and the workgroup decides its unit's gate
+// itself, from the metered records, as the exact fallback's prologue does (each of
+// the unit's workgroups stores the same masks).
 template <int D, bool METER, bool VM, int NW>
 __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
   constexpr int C = D / 64;   // channels per lane
   __shared__ float acc_s[NW][D];
+  __shared__ int gate_flag_s;
   const int bh = blockIdx.x;
   const int b = bh / a.n_q, h = bh % a.n_q;
   const int unit = b * a.n_kv + h / a.group;
@@ -528,7 +533,10 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t R = (int64_t)partial_record_floats(D);
   const bool fin = a.x_part != nullptr;
-  const bool routed = fin && a.gate_mask_kv[unit] != 0;
+  bool routed = fin && !a.merge_gate && a.gate_mask_kv[unit] != 0;
+  if constexpr (NW == 4) {   // (unit_gate's heads go to four waves)
+    if (fin && a.merge_gate) routed = unit_gate(a, b, h / a.group, 0, wave, lane, &gate_flag_s);
+  }
   const float* rec0 = a.part + (int64_t)bh * a.n_splits * R;
   const float* src0 = routed ? a.x_part + (int64_t)bh * a.n_splits * R : rec0;   // output rows
   const int jl = lane & 31;
@@ -595,7 +603,9 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
         // (the gate was decided and stored by the exact fallback's prologue): counts
         // of gated query heads and, by each KV head's first query head, routed KV heads
         if (a.gate_count != nullptr) {
-          if (a.gate_mask_q[bh] != 0) atomicAdd(a.gate_count, 1);
+          // (the speculative merge's own head: the gate its unit_gate call stored)
+          const bool own = a.merge_gate ? gated_of(raw, 0.0f, a.gate_tau, false, 0.0f) : a.gate_mask_q[bh] != 0;
+          if (own) atomicAdd(a.gate_count, 1);
           if (h % a.group == 0 && routed) atomicAdd(a.gate_count + 1, 1);
         }
       } else if (a.gate_mask_q != nullptr) {
@@ -686,10 +696,11 @@ void launch_merge_w(const DecodeArgs& a, bool metered, hipStream_t st) {
   else hipLaunchKernelGGL((merge_kernel<D, true, false, NW>), grid, block, 0, st, a);
 }
 
-// One wave per head takes up to 32 records in one round trip; more splits get four.
+// One wave per head takes up to 32 records in one round trip; more splits, or a
+// merge that decides the gate, get four.
 template <int D>
 void launch_merge_d(const DecodeArgs& a, bool metered, hipStream_t st) {
-  if (a.n_splits <= 32) launch_merge_w<D, 1>(a, metered, st);
+  if (a.n_splits <= 32 && !a.merge_gate) launch_merge_w<D, 1>(a, metered, st);
   else launch_merge_w<D, kMergeWaves>(a, metered, st);
 }
 

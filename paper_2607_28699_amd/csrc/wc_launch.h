@@ -110,6 +110,10 @@ struct DecodeArgs {
   const float* gate_part;
   const float* x_part;
   int no_merge;             // launch_decode: the decode kernel only (the merge comes later)
+  // speculative certified step: the exact records x_part cover every unit, and the
+  // final merge decides each unit's gate itself from the metered records
+  // (gate_part), four waves per workgroup
+  int merge_gate;
 };
 
 // Scale of channel c of the token in scale row `row` (page * 16 + offset): the
@@ -148,9 +152,8 @@ struct DecodePos {
   int unit;    // sequence x n_kv + KV head
   int split;
 };
-__device__ __forceinline__ DecodePos decode_position(int batch, int n_kv, int n_splits) {
+__device__ __forceinline__ DecodePos decode_position_at(uint32_t L, int batch, int n_kv, int n_splits) {
   const uint32_t K = (uint32_t)n_kv, NS = (uint32_t)n_splits;
-  const uint32_t L = blockIdx.x + gridDim.x * blockIdx.y;
   const uint32_t nP = (uint32_t)batch * NS;
   const uint32_t full = nP / 8u * 8u;   // positions in whole groups of 8
   uint32_t P, kv;
@@ -165,6 +168,9 @@ __device__ __forceinline__ DecodePos decode_position(int batch, int n_kv, int n_
   }
   const uint32_t b = P / NS, s = P % NS;
   return DecodePos{(int)(b * K + kv), (int)((s + b) % NS)};
+}
+__device__ __forceinline__ DecodePos decode_position(int batch, int n_kv, int n_splits) {
+  return decode_position_at(blockIdx.x + gridDim.x * blockIdx.y, batch, n_kv, n_splits);
 }
 
 // Clears the gate outputs of one (sequence, KV head) ahead of the merge.
@@ -276,6 +282,10 @@ hipError_t launch_decode_mfma(const DecodeArgs& a, bool metered, hipStream_t st)
 // The decode call would run on the matrix cores (where a step's new tokens can be
 // written by the decode kernel itself).
 bool step_write_fusable(const DecodeArgs& a);
+// The speculative certified step's metered decode (am, plain Tier A) and exact
+// fallback of every unit (ax) can share one matrix-core launch.
+bool spec_decode_fusable(const DecodeArgs& am, const DecodeArgs& ax);
+hipError_t launch_decode_spec(const DecodeArgs& am, const DecodeArgs& ax, hipStream_t st);
 hipError_t launch_merge(const DecodeArgs& a, bool metered, hipStream_t st);
 hipError_t launch_gate(const GateArgs& a, hipStream_t st);
 hipError_t launch_repair(const RepairArgs& a, hipStream_t st);

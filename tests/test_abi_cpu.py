@@ -205,18 +205,19 @@ def test_certified_step_checks_and_workspace(L):
     ex = _lib.WcCache(_lib.WC_KIND_BF16, 128, 1, 0, 0, 0, 1, 0, 16, 16)
     ex64 = _lib.WcCache(_lib.WC_KIND_BF16, 64, 1, 0, 0, 0, 1, 0, 16, 16)
 
-    def step(cache, exact, ws_bytes=1 << 30, tau=0.2, meter=16):
-        return L.wc_step_certified_decode(
-            cache, exact, 16, 16, _lib.WC_BF16, 16, 16, _lib.WC_BF16, 1, 7, 16, 4, 16, 64, 0.1, 16, 0,
-            meter, 16, 0, tau, 16, 16, None, 256, ws_bytes, None)
-    assert step(ctypes.byref(c), None) == _lib.WC_EINVAL                       # no exact cache
-    assert step(ctypes.byref(c), ctypes.byref(c)) == _lib.WC_EINVAL            # exact must be bf16
-    assert step(ctypes.byref(c), ctypes.byref(ex64)) == _lib.WC_EINVAL         # same head size
-    assert step(ctypes.byref(ex), ctypes.byref(ex)) == _lib.WC_EINVAL          # the metered cache is quantized
-    assert step(ctypes.byref(c), ctypes.byref(ex), tau=-1.0) == _lib.WC_EINVAL
-    assert step(ctypes.byref(c), ctypes.byref(ex), meter=None) == _lib.WC_EINVAL
     need = L.wc_certified_workspace_size(1, 7, 1, 128, 64, 0)
-    assert step(ctypes.byref(c), ctypes.byref(ex), ws_bytes=need - 1) == _lib.WC_EWORKSPACE
+    # (the speculative form takes the same arguments and checks)
+    for fn in (L.wc_step_certified_decode, L.wc_step_certified_decode_speculative):
+        def step(cache, exact, ws_bytes=1 << 30, tau=0.2, meter=16):
+            return fn(cache, exact, 16, 16, _lib.WC_BF16, 16, 16, _lib.WC_BF16, 1, 7, 16, 4, 16, 64, 0.1, 16, 0,
+                      meter, 16, 0, tau, 16, 16, None, 256, ws_bytes, None)
+        assert step(ctypes.byref(c), None) == _lib.WC_EINVAL                   # no exact cache
+        assert step(ctypes.byref(c), ctypes.byref(c)) == _lib.WC_EINVAL        # exact must be bf16
+        assert step(ctypes.byref(c), ctypes.byref(ex64)) == _lib.WC_EINVAL     # same head size
+        assert step(ctypes.byref(ex), ctypes.byref(ex)) == _lib.WC_EINVAL      # the metered cache is quantized
+        assert step(ctypes.byref(c), ctypes.byref(ex), tau=-1.0) == _lib.WC_EINVAL
+        assert step(ctypes.byref(c), ctypes.byref(ex), meter=None) == _lib.WC_EINVAL
+        assert step(ctypes.byref(c), ctypes.byref(ex), ws_bytes=need - 1) == _lib.WC_EWORKSPACE
 
 
 def test_noalloc_step_call_checks(L):

@@ -220,3 +220,85 @@ def test_certified_graph_replay():
         torch.cuda.synchronize()
         for x, y in zip((out, meter, raw, mq, mk, cnt), eager):
             assert torch.equal(x, y)
+
+
+@pytest.mark.parametrize("tau_mode", TAUS)
+@pytest.mark.parametrize("name,wl,lens,split,kind,opts", CASES)
+def test_speculative_equals_certified(name, wl, lens, split, kind, opts, tau_mode):
+    """wc_step_certified_decode_speculative (the exact fallback of every KV head
+    beside the metered decode, the gate decided in the final merge) gives the
+    certified step's caches, outputs, meter, raw, masks and counts bit for bit: in
+    one launch for the plain Tier A caches with bf16 inputs, in two otherwise."""
+    import torch
+
+    import paper_2607_28699_amd as wc
+    S.say(f"[speculative] {name} tau={tau_mode} lens={lens} split={split}")
+    case, caches, (nk, nv, ns) = _setup(wl, lens, kind, opts)
+    q = torch.from_numpy(case["q"]).to("cuda", torch.float32 if wl.dtype == "f32" else torch.bfloat16)
+    table = torch.from_numpy(case["table"]).cuda()
+    sl = torch.from_numpy(case["seq_lens"].astype(np.int32)).cuda()
+    L = max(int(case["seq_lens"].max()), 1)
+    sm = 1 / np.sqrt(wl.d)
+    if opts.get("force_valu"):
+        os.environ["WITCERT_FORCE_VALU"] = "1"
+    try:
+        (c1, e1), (c2, e2) = caches
+        tau = _tau(tau_mode, case, caches, (nk, nv, ns), split)
+        n1 = torch.zeros(2, dtype=torch.int32, device="cuda")
+        got = wc.step_certified_decode_speculative(c1, e1, nk, nv, ns, q, table, sl, L, sm, tau,
+                                                   split_tokens=split, n_gated=n1)
+        n2 = torch.zeros(2, dtype=torch.int32, device="cuda")
+        ref = wc.step_certified_decode(c2, e2, nk, nv, ns, q, table, sl, L, sm, tau, split_tokens=split, n_gated=n2)
+        torch.cuda.synchronize()
+    finally:
+        os.environ.pop("WITCERT_FORCE_VALU", None)
+    for (x, y) in ((c1, c2), (e1, e2)):
+        for n, t in x.tensors.items():
+            if t is not None:
+                assert torch.equal(t, y.tensors[n]), (name, n)
+    for i, (x, y) in enumerate(zip(got, ref)):
+        assert torch.equal(x, y), (name, tau_mode, i)
+    assert torch.equal(n1, n2), (name, n1.tolist(), n2.tolist())
+
+
+def test_speculative_graph_replay():
+    import torch
+
+    import paper_2607_28699_amd as wc
+    S.say("[speculative] graph replay")
+    wl = W_GQA
+    lens = [900, 130, 1]
+    case, caches, (nk, nv, ns) = _setup(wl, lens, "int8_dither", {}, layer=5)
+    c, e = caches[0]
+    q = torch.from_numpy(case["q"]).to("cuda", torch.bfloat16)
+    table = torch.from_numpy(case["table"]).cuda()
+    sl = torch.from_numpy(case["seq_lens"].astype(np.int32)).cuda()
+    L, sm = max(lens), 1 / np.sqrt(wl.d)
+    tau = _tau("median", case, caches, (nk, nv, ns), 64)
+    ws = wc.certified_workspace(len(lens), wl.n_q, wl.n_kv, wl.d, L, 64)
+    out = torch.empty((len(lens), wl.n_q, wl.d), dtype=torch.float32, device="cuda")
+    meter = torch.empty((len(lens), wl.n_q), dtype=torch.float32, device="cuda")
+    raw, mq = torch.empty_like(meter), torch.empty((len(lens), wl.n_q), dtype=torch.uint8, device="cuda")
+    mk = torch.empty((len(lens), wl.n_kv), dtype=torch.uint8, device="cuda")
+    cnt = torch.zeros(2, dtype=torch.int32, device="cuda")
+    kw = dict(split_tokens=64, ws=ws, out=out, meter=meter, raw=raw, mask_q=mq, mask_kv=mk, n_gated=cnt)
+    args = (c, e, nk, nv, ns, q, table, sl, L, sm, tau)
+    wc.step_certified_decode_speculative(*args, **kw)
+    torch.cuda.synchronize()
+    eager = [x.clone() for x in (out, meter, raw, mq, mk, cnt)]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            wc.step_certified_decode_speculative(*args, **kw)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for x in (out, meter, raw, mq, mk):
+            x.zero_()
+        cnt.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for x, y in zip((out, meter, raw, mq, mk, cnt), eager):
+            assert torch.equal(x, y)

@@ -3,9 +3,10 @@
 One layer of each long-context workload is prefilled through
 wc_quantize_write_pair (quantized cache and bf16 exact copy), then one decode step
 runs through wc_step_metered_decode_gate -- the step's token written by the
-decode kernel itself -- and through wc_step_certified_decode, the call bench.py
-times (the same step with the exact fallback: meters and masks bit-identical, a
-routed head's output exact attention), with bench.py's split choice
+decode kernel itself -- and through wc_step_certified_decode and its speculative
+form, the calls bench.py times (the same step with the exact fallback: meters and
+masks bit-identical, a routed head's output exact attention; the speculative form
+bit-identical to the certified one), with bench.py's split choice
 (max_seq_len = prefill + steps + warmup, the split balanced over the batch's
 total tokens; the serving mix with all 64 sequences).  Sampled (sequence, query
 head) cells, the shortest and the longest sequence among them, are recomputed by
@@ -148,6 +149,15 @@ def test_fullsize_sampled_cells(name):
                                    k[:, g:g + 1].float().cpu().numpy().astype(np.float64),
                                    v[:, g:g + 1].float().cpu().numpy().astype(np.float64), sm)["out"]
             assert S.rel_err(c_out[b, h], ex[0]) <= 2e-3, (b, h)
+    # its speculative form (what bench.py times when the first step routes at least
+    # half of the KV heads): the certified step's results bit for bit
+    nq_ = torch.zeros(2, dtype=torch.int32, device="cuda")
+    s_res = wc.step_certified_decode_speculative(cache, exact, nk, nv, ns, q, tab, lens, max_len, sm, tau,
+                                                 split_tokens=st, ws=ws, n_gated=nq_)
+    torch.cuda.synchronize()
+    for x, y in zip(s_res, (c_out, c_meter, c_raw, c_mq, c_mk)):
+        y = y if isinstance(y, np.ndarray) else y.cpu().numpy()
+        assert np.array_equal(x.cpu().numpy(), y)
 
 
 def test_matrix_core_and_vector_paths_agree():
