@@ -483,7 +483,6 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeArgs a) {
 // numerators) come from split_stats (merge_dev.h), in the same bits wherever they
 // are formed.
 constexpr int kMergeWaves = 4;   // waves per merge workgroup when a head has more than 32 splits
-static_assert(kMergeWaves == 4, "the merge that decides the gate runs unit_gate on four waves");
 
 // The statistics a merge needs: of the output rows (so; the exact records of a
 // routed head in a certified step's final merge) and of the metered records for
@@ -517,15 +516,14 @@ __device__ __forceinline__ void merge_stats(const float* rec0, const float* src0
 // Final merge of a certified step (a.x_part set): the heads of a routed KV head
 // (gate_mask_kv, stored by the exact fallback's prologue) take their output from
 // the exact records, the others from the metered ones; meter and raw always from
-// the metered records.  Speculative certified step (a.merge_gate, four waves):
-// the exact records cover every unit and the workgroup decides its unit's gate
-// itself, from the metered records, as the exact fallback's prologue does (each of
-// the unit's workgroups stores the same masks).
+// the metered records.  Speculative certified step (a.merge_gate): the exact
+// records cover every unit and each wave decides its unit's gate itself from the
+// metered records, with the statistics the exact fallback's prologue uses (every
+// wave of the unit's workgroups stores the same masks).
 template <int D, bool METER, bool VM, int NW>
 __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
   constexpr int C = D / 64;   // channels per lane
   __shared__ float acc_s[NW][D];
-  __shared__ int gate_flag_s;
   const int bh = blockIdx.x;
   const int b = bh / a.n_q, h = bh % a.n_q;
   const int unit = b * a.n_kv + h / a.group;
@@ -534,29 +532,20 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
   const int64_t R = (int64_t)partial_record_floats(D);
   const bool fin = a.x_part != nullptr;
   bool routed = fin && !a.merge_gate && a.gate_mask_kv[unit] != 0;
-  if constexpr (NW == 4) {   // (unit_gate's heads go to four waves)
-    if (fin && a.merge_gate) routed = unit_gate(a, b, h / a.group, 0, wave, lane, &gate_flag_s);
-  }
   const float* rec0 = a.part + (int64_t)bh * a.n_splits * R;
-  const float* src0 = routed ? a.x_part + (int64_t)bh * a.n_splits * R : rec0;   // output rows
+  const float* xrec0 = fin ? a.x_part + (int64_t)bh * a.n_splits * R : rec0;
   const int jl = lane & 31;
   const int L = a.seq_lens[b];
-
-  float acc[C];
-#pragma unroll
-  for (int c = 0; c < C; ++c) acc[c] = 0.0f;
-  SplitStats so{}, sm{};   // the output rows' statistics; the meter's (the metered records)
-  bool have = false;
-  int ns = 0;
-  // The rows of a chunk are requested before the sequence length is known; rows
-  // past the last active split are read (they exist in the workspace) but not used.
-  for (int j0 = 32 * wave; j0 < a.n_splits; j0 += 32 * NW) {
+  // The rows of a chunk (32 splits from j0; rows past the last split repeat it) and
+  // lane jl's split max; the rows are requested before the sequence length is
+  // known, and rows past the last active split are read (they exist in the
+  // workspace) but not used.
+  auto load_chunk = [&](const float* s0, int j0, float (&ov)[32][C]) {
     const int nr = min(32, a.n_splits - j0);
-    float ov[32][C];
-    const float mj_raw = src0[(int64_t)(j0 + min(jl, nr - 1)) * R + D];
+    const float mj = s0[(int64_t)(j0 + min(jl, nr - 1)) * R + D];
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
-      const float* src = src0 + (int64_t)(j0 + min(j, nr - 1)) * R + C * lane;
+      const float* src = s0 + (int64_t)(j0 + min(j, nr - 1)) * R + C * lane;
       if constexpr (C == 2) {
         const float2 v = *reinterpret_cast<const float2*>(src);
         ov[j][0] = v.x;
@@ -565,11 +554,63 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
         ov[j][0] = src[0];
       }
     }
+    return mj;
+  };
+  // Speculative certified step: the exact rows of this wave's first chunk are
+  // requested before the unit's gate is decided, so that the gate's loads go out
+  // with them (the guess is the step's premise, a routed unit; a unit that is not
+  // reads its metered rows afterwards).
+  // Its own head's statistics come with the gate (the metered records' -- the same
+  // bits as merge_stats -- and, up to 64 splits, the exact records' from scalars
+  // fetched with the rows), so no further round trip precedes the merge.
+  float ovp[32][C];
+  float mjp = 0.0f;
+  bool pre = false, gstats = false;
+  float4 txp = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  SplitStats gsm{};
+  if (fin && a.merge_gate) {
+    if (32 * wave < a.n_splits) {
+      mjp = load_chunk(xrec0, 32 * wave, ovp);
+      pre = true;
+    }
+    gstats = !VM && a.n_splits <= 64;
+    if (gstats) txp = *reinterpret_cast<const float4*>(xrec0 + (int64_t)min(lane, a.n_splits - 1) * R + D);
+    routed = unit_gate_wave(a, b, h / a.group, lane, h % a.group, &gsm);
+    pre = pre && routed;
+  }
+  const float* src0 = routed ? xrec0 : rec0;   // output rows
+  auto stats = [&](int ns_, SplitStats& so_, SplitStats& sm_) {
+    if (gstats) {
+      sm_ = gsm;
+      so_ = routed ? stats_of_lanes<false, false>(txp, 0.0f, ns_, lane) : gsm;
+    } else {
+      merge_stats<METER, VM>(rec0, src0, routed, R, ns_, a.n_splits, lane, so_, sm_);
+    }
+  };
+
+  float acc[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) acc[c] = 0.0f;
+  SplitStats so{}, sm{};   // the output rows' statistics; the meter's (the metered records)
+  bool have = false;
+  int ns = 0;
+  for (int j0 = 32 * wave; j0 < a.n_splits; j0 += 32 * NW) {
+    float ov[32][C];
+    float mj_raw;
+    if (pre && j0 == 32 * wave) {
+#pragma unroll
+      for (int j = 0; j < 32; ++j)
+#pragma unroll
+        for (int c = 0; c < C; ++c) ov[j][c] = ovp[j][c];
+      mj_raw = mjp;
+    } else {
+      mj_raw = load_chunk(src0, j0, ov);
+    }
     ns = active_splits(L, a.split_tokens, a.n_splits);
     if (j0 >= ns) break;
     const int nj = min(32, ns - j0);
     if (!have) {   // the statistics (the first chunk's loads are in flight)
-      merge_stats<METER, VM>(rec0, src0, routed, R, ns, a.n_splits, lane, so, sm);
+      stats(ns, so, sm);
       have = true;
     }
     const float mj = jl < nj ? mj_raw : -INFINITY;
@@ -584,7 +625,7 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
     }
   }
   ns = active_splits(L, a.split_tokens, a.n_splits);
-  if (!have && wave == 0) merge_stats<METER, VM>(rec0, src0, routed, R, ns, a.n_splits, lane, so, sm);
+  if (!have && wave == 0) stats(ns, so, sm);
 #pragma unroll
   for (int c = 0; c < C; ++c) acc_s[wave][C * lane + c] = acc[c];
   if constexpr (NW > 1) __syncthreads();
@@ -603,7 +644,7 @@ __global__ __launch_bounds__(64 * NW) void merge_kernel(DecodeArgs a) {
         // (the gate was decided and stored by the exact fallback's prologue): counts
         // of gated query heads and, by each KV head's first query head, routed KV heads
         if (a.gate_count != nullptr) {
-          // (the speculative merge's own head: the gate its unit_gate call stored)
+          // (the speculative merge's own head: the gate unit_gate_wave stored)
           const bool own = a.merge_gate ? gated_of(raw, 0.0f, a.gate_tau, false, 0.0f) : a.gate_mask_q[bh] != 0;
           if (own) atomicAdd(a.gate_count, 1);
           if (h % a.group == 0 && routed) atomicAdd(a.gate_count + 1, 1);
@@ -696,11 +737,10 @@ void launch_merge_w(const DecodeArgs& a, bool metered, hipStream_t st) {
   else hipLaunchKernelGGL((merge_kernel<D, true, false, NW>), grid, block, 0, st, a);
 }
 
-// One wave per head takes up to 32 records in one round trip; more splits, or a
-// merge that decides the gate, get four.
+// One wave per head takes up to 32 records in one round trip; more splits get four.
 template <int D>
 void launch_merge_d(const DecodeArgs& a, bool metered, hipStream_t st) {
-  if (a.n_splits <= 32 && !a.merge_gate) launch_merge_w<D, 1>(a, metered, st);
+  if (a.n_splits <= 32) launch_merge_w<D, 1>(a, metered, st);
   else launch_merge_w<D, kMergeWaves>(a, metered, st);
 }
 

@@ -21,19 +21,74 @@ struct SplitStats {
   float e, v;   // value side: weighted residual sum, largest stored value norm
 };
 
-// Adds the weighted scalars of one record per lane (one shuffle tree over the wave).
+// One butterfly step over the wave: op(x, the value of lane i ^ O), in every lane.
+// O = 1, 2: quad permutes; O = 4: two row shifts by 4, one for each half of every
+// 8-lane group; O = 8: a row rotation by 8 (DPP); O = 16, 32: gfx950's lane-group
+// swaps, which leave a lane's own value and its partner's in the two results (in
+// that order in the lower lane group of each pair, reversed in the upper one: op
+// is commutative).  No step goes through LDS.
+template <int O, typename Op>
+__device__ __forceinline__ float butterfly(float x, Op op) {
+  const int v = __builtin_bit_cast(int, x);
+  if constexpr (O == 16 || O == 32) {
+    const auto p = O == 16 ? __builtin_amdgcn_permlane16_swap(v, v, false, false)
+                           : __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return op(__builtin_bit_cast(float, (int)p[0]), __builtin_bit_cast(float, (int)p[1]));
+  } else {
+    int r;
+    if constexpr (O == 1) {
+      r = __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);
+    } else if constexpr (O == 2) {
+      r = __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);
+    } else if constexpr (O == 4) {
+      r = __builtin_amdgcn_update_dpp(v, v, 0x104, 0xF, 0x5, false);   // banks 0, 2: lane + 4
+      r = __builtin_amdgcn_update_dpp(r, v, 0x114, 0xF, 0xA, false);   // banks 1, 3: lane - 4
+    } else {
+      static_assert(O == 8, "butterfly steps 1 .. 32");
+      r = __builtin_amdgcn_mov_dpp(v, 0x128, 0xF, 0xF, false);
+    }
+    return op(x, __builtin_bit_cast(float, r));
+  }
+}
+
+struct AddOp {
+  __device__ float operator()(float a, float b) const { return a + b; }
+};
+struct MaxOp {
+  __device__ float operator()(float a, float b) const { return fmaxf(a, b); }
+};
+
+// One butterfly step of the weighted scalars' sums (and the value norms' max).
+template <bool METER, bool VM, int O>
+__device__ __forceinline__ void reduce_step(float& dl, float& dn, float& de, float& dv) {
+  dl = butterfly<O>(dl, AddOp{});
+  if constexpr (METER) dn = butterfly<O>(dn, AddOp{});
+  if constexpr (VM) {
+    de = butterfly<O>(de, AddOp{});
+    dv = butterfly<O>(dv, MaxOp{});
+  }
+}
+
+// Max over the wave by the same butterfly.
+__device__ __forceinline__ float butterfly_max(float m) {
+  m = butterfly<1>(m, MaxOp{});
+  m = butterfly<2>(m, MaxOp{});
+  m = butterfly<4>(m, MaxOp{});
+  m = butterfly<8>(m, MaxOp{});
+  m = butterfly<16>(m, MaxOp{});
+  return butterfly<32>(m, MaxOp{});
+}
+
+// Adds the weighted scalars of one record per lane (one butterfly over the wave).
 template <bool METER, bool VM>
 __device__ __forceinline__ void reduce_stats(SplitStats& s, float w, const float4& t, float tv) {
   float dl = w * t.y, dn = METER ? w * t.z : 0.0f, de = VM ? w * t.w : 0.0f, dv = tv;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    dl += __shfl_xor(dl, o, 64);
-    if constexpr (METER) dn += __shfl_xor(dn, o, 64);
-    if constexpr (VM) {
-      de += __shfl_xor(de, o, 64);
-      dv = fmaxf(dv, __shfl_xor(dv, o, 64));
-    }
-  }
+  reduce_step<METER, VM, 1>(dl, dn, de, dv);
+  reduce_step<METER, VM, 2>(dl, dn, de, dv);
+  reduce_step<METER, VM, 4>(dl, dn, de, dv);
+  reduce_step<METER, VM, 8>(dl, dn, de, dv);
+  reduce_step<METER, VM, 16>(dl, dn, de, dv);
+  reduce_step<METER, VM, 32>(dl, dn, de, dv);
   s.l += dl;
   if constexpr (METER) s.n += dn;
   if constexpr (VM) {
@@ -52,9 +107,7 @@ __device__ __forceinline__ SplitStats stats_of_lanes(float4 t, float tv, int ns,
     t = make_float4(-INFINITY, 0.0f, 0.0f, 0.0f);
     tv = 0.0f;
   }
-  s.M = t.x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) s.M = fmaxf(s.M, __shfl_xor(s.M, o, 64));
+  s.M = butterfly_max(t.x);
   const float w = t.x == -INFINITY ? 0.0f : __expf(t.x - s.M);
   reduce_stats<METER, VM>(s, w, t, tv);
   return s;
@@ -80,8 +133,7 @@ __device__ __forceinline__ SplitStats split_stats(const float* rec0, int64_t R, 
     const float m = j < ns ? rec0[(int64_t)j * R + D] : -INFINITY;
     s.M = fmaxf(s.M, m);
   }
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) s.M = fmaxf(s.M, __shfl_xor(s.M, o, 64));
+  s.M = butterfly_max(s.M);
   for (int j0 = 0; j0 < ns; j0 += 64) {
     const int j = j0 + lane;
     const bool ok = j < ns;
@@ -143,13 +195,16 @@ __device__ __forceinline__ bool unit_gate(const DecodeArgs& a, int b, int kv, in
     if (lane == 0 && split == 0) a.gate_mask_q[b * a.n_q + kv * a.group + hh] = g ? 1 : 0;
   };
   if (a.n_splits <= 64) {
-    // every head of this wave in one round trip (up to 4: G <= 16), the length too
+    // every head of this wave in one round trip (up to 4: G <= 16), the length too;
+    // the loads are unconditional (past the last head: its record again), so that
+    // none waits for another
     const int jr = min(lane, a.n_splits - 1);
     float4 t[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (wave + 4 * i < a.group)
-        t[i] = *reinterpret_cast<const float4*>(base + ((int64_t)(wave + 4 * i) * a.n_splits + jr) * R + a.head_dim);
+    for (int i = 0; i < 4; ++i) {
+      const int hc = min(wave + 4 * i, a.group - 1);
+      t[i] = *reinterpret_cast<const float4*>(base + ((int64_t)hc * a.n_splits + jr) * R + a.head_dim);
+    }
     const int ns = active_splits(a.seq_lens[b], a.split_tokens, a.n_splits);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -165,6 +220,44 @@ __device__ __forceinline__ bool unit_gate(const DecodeArgs& a, int b, int kv, in
   const bool routed = *flag_s != 0;
   if (split == 0 && threadIdx.x == 0) a.gate_mask_kv[b * a.n_kv + kv] = routed ? 1 : 0;
   return routed;
+}
+
+// The same gate as unit_gate, decided by one wave without barriers (the final
+// merge of a speculative certified step): every query head of the unit from the
+// metered records a.gate_part, up to 64 splits of all heads in one load round
+// trip (more splits: split_stats per head); lane 0 stores mask_q of the unit's
+// heads and mask_kv (every wave that calls it stores the same values).  Returns
+// whether the unit is routed (uniform over the wave); own_stats receives head
+// own's statistics.
+__device__ __forceinline__ bool unit_gate_wave(const DecodeArgs& a, int b, int kv, int lane, int own,
+                                               SplitStats* own_stats) {
+  const int64_t R = (int64_t)partial_record_floats(a.head_dim);
+  const float* base = a.gate_part + (int64_t)(b * a.n_q + kv * a.group) * a.n_splits * R;
+  const int ns = active_splits(a.seq_lens[b], a.split_tokens, a.n_splits);
+  bool any = false;
+  auto decide = [&](const SplitStats& s, int hh) {
+    const bool g = gated_of(raw_of(s, ns), 0.0f, a.gate_tau, false, 0.0f);
+    any |= g;
+    if (hh == own) *own_stats = s;
+    if (lane == 0) a.gate_mask_q[b * a.n_q + kv * a.group + hh] = g ? 1 : 0;
+  };
+  if (a.n_splits <= 64) {
+    const int jr = min(lane, a.n_splits - 1);
+    float4 t[16];   // (G <= 16; unconditional loads, past the last head its record again)
+#pragma unroll
+    for (int hh = 0; hh < 16; ++hh) {
+      const int hc = min(hh, a.group - 1);
+      t[hh] = *reinterpret_cast<const float4*>(base + ((int64_t)hc * a.n_splits + jr) * R + a.head_dim);
+    }
+#pragma unroll
+    for (int hh = 0; hh < 16; ++hh)
+      if (hh < a.group) decide(stats_of_lanes<true, false>(t[hh], 0.0f, ns, lane), hh);
+  } else {
+    for (int hh = 0; hh < a.group; ++hh)
+      decide(split_stats<true, false>(base + (int64_t)hh * a.n_splits * R, R, a.head_dim, ns, a.n_splits, lane), hh);
+  }
+  if (lane == 0) a.gate_mask_kv[b * a.n_kv + kv] = any ? 1 : 0;
+  return any;
 }
 
 }  // namespace wc

@@ -111,8 +111,7 @@ struct DecodeArgs {
   const float* x_part;
   int no_merge;             // launch_decode: the decode kernel only (the merge comes later)
   // speculative certified step: the exact records x_part cover every unit, and the
-  // final merge decides each unit's gate itself from the metered records
-  // (gate_part), four waves per workgroup
+  // final merge decides each unit's gate itself from the metered records (gate_part)
   int merge_gate;
 };
 
