@@ -136,7 +136,9 @@ __device__ __forceinline__ h4_t pack4(uint32_t a, uint32_t b) {
   return __builtin_bit_cast(h4_t, make_uint2(a, b));
 }
 
-__device__ __forceinline__ float xor_max(float v, int m) { return fmaxf(v, __shfl_xor(v, m, 64)); }
+// (butterfly steps without LDS: merge_dev.h)
+template <int M>
+__device__ __forceinline__ float xor_max(float v) { return bfly_max<M>(v); }
 
 // Loaded bytes of one 16-token page for one lane.
 template <int KIND>
@@ -575,8 +577,8 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     loc = fmaxf(loc, lg[e]);
   }
   if (__ballot(loc > st.m + kSlack2) != 0) {
-    float full = HALF ? xor_max(loc, 8) : loc;     // lanes r and r + 8 share head r's max
-    full = xor_max(xor_max(full, 16), 32);
+    float full = HALF ? xor_max<8>(loc) : loc;     // lanes r and r + 8 share head r's max
+    full = xor_max<32>(xor_max<16>(full));
     const float m_new = fmaxf(st.m, full);
     const float alpha = exp2_fast(st.m - m_new);
     st.m = m_new;
@@ -609,7 +611,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
     const uint32_t pbits = max((uint32_t)pm2[0], (uint32_t)pm2[1]);
     if (__ballot(pbits > (uint32_t)(15 + st.ve) << 10) != 0) {
       const float pmax = (float)__builtin_bit_cast(_Float16, (uint16_t)pbits);
-      const float wmax = xor_max(xor_max(xor_max(xor_max(xor_max(xor_max(pmax, 1), 2), 4), 8), 16), 32);
+      const float wmax = xor_max<32>(xor_max<16>(xor_max<8>(xor_max<4>(xor_max<2>(xor_max<1>(pmax))))));
       int e2;
       (void)frexpf(wmax, &e2);                    // wmax < 2^e2 (e2 <= 16 for fp16 scales)
       const int ve_new = __builtin_amdgcn_readfirstlane(max(st.ve, e2));
@@ -762,7 +764,7 @@ __device__ __forceinline__ void process_page(const DecodeArgs& a, const PageRegs
       am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, vw[i] & 0x7FFF7FFFu));
     const float pmax = __builtin_bit_cast(float, (uint32_t)max(am[0], am[1]) << 16);
     if (__ballot(pmax > __builtin_bit_cast(float, (uint32_t)(142 + st.ve) << 23)) != 0) {
-      const float wmax = xor_max(xor_max(xor_max(xor_max(xor_max(xor_max(pmax, 1), 2), 4), 8), 16), 32);
+      const float wmax = xor_max<32>(xor_max<16>(xor_max<8>(xor_max<4>(xor_max<2>(xor_max<1>(pmax))))));
       int e2;
       (void)frexpf(wmax, &e2);                    // wmax < 2^e2
       const int ve_new = __builtin_amdgcn_readfirstlane(max(st.ve, e2 - 15));
@@ -802,9 +804,9 @@ template <bool HALF>
 __device__ __forceinline__ void flush_segment(const DecodeArgs& a, WaveState& st, Segment& sg, int last_page,
                                               float4* my_slots, int r, int g) {
   float t = st.nb;
-  if constexpr (HALF) t += __shfl_xor(t, 8, 64);   // lanes r and r + 8 hold tokens of head r
-  t += __shfl_xor(t, 16, 64);
-  t += __shfl_xor(t, 32, 64);
+  if constexpr (HALF) t = bfly_add<8>(t);   // lanes r and r + 8 hold tokens of head r
+  t = bfly_add<16>(t);
+  t = bfly_add<32>(t);
   if (g == 0 && r < a.group && sg.slot < a.share_slots / kWaves)
     my_slots[sg.slot] = make_float4(t, (st.m - kWExp) * kLn2, __builtin_bit_cast(float, sg.first),
                                     __builtin_bit_cast(float, last_page - sg.first));
@@ -1011,8 +1013,8 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
     wc.ov_lo = 8 * g < 2 * m;
     wc.ov_hi = 8 * g + 4 < 2 * m;
     if constexpr (TB) {
-      asum += __shfl_xor(asum, 16, 64);
-      asum += __shfl_xor(asum, 32, 64);
+      asum = bfly_add<16>(asum);
+      asum = bfly_add<32>(asum);
       wc.gmul = a.sm_scale * 0x1p-11f * kLog2e;
       wc.gc = a.sm_scale * 0x1p-25f * kLog2e * asum;
       if constexpr (HALF) wc.gc = dpp_from_lower8(wc.gc, wc.gc);
@@ -1037,8 +1039,8 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
       wc.qop[kt] = pack8(w[0], w[1], w[2], w[3]);
     }
   }
-  qsum += __shfl_xor(qsum, 16, 64);
-  qsum += __shfl_xor(qsum, 32, 64);
+  qsum = bfly_add<16>(qsum);
+  qsum = bfly_add<32>(qsum);
   wc.s1_init = kQOff * qsum;
 #pragma unroll
   for (int G = 0; G < 4; ++G) wc.qoff[G] = wc.ta2[G] = wc.tb1[G] = 0.0f;
@@ -1077,8 +1079,8 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
         w[i] = h;
       }
       wc.qop[G] = pack8(w[0], w[1], w[2], w[3]);
-      qs += __shfl_xor(qs, 16, 64);
-      qs += __shfl_xor(qs, 32, 64);
+      qs = bfly_add<16>(qs);
+      qs = bfly_add<32>(qs);
       wc.qoff[G] = kQOff * qs;
     }
     if constexpr (TB) {
@@ -1088,10 +1090,10 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
 #pragma unroll
       for (int G = 0; G < 4; ++G) {
         float x = n2[G], y = l1[G];
-        x += __shfl_xor(x, 16, 64);
-        x += __shfl_xor(x, 32, 64);
-        y += __shfl_xor(y, 16, 64);
-        y += __shfl_xor(y, 32, 64);
+        x = bfly_add<16>(x);
+        x = bfly_add<32>(x);
+        y = bfly_add<16>(y);
+        y = bfly_add<32>(y);
         wc.ta2[G] = (c * rt) * (c * rt) * x;   // (head r: the radii are formed before the HALF shift)
         wc.tb1[G] = c * y * (1.0f / 256.0f);
       }
@@ -1111,10 +1113,10 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
       sq = fmaf(x, x, sq);
       l1 += fabsf(x);
     }
-    sq += __shfl_xor(sq, 16, 64);
-    sq += __shfl_xor(sq, 32, 64);
-    l1 += __shfl_xor(l1, 16, 64);
-    l1 += __shfl_xor(l1, 32, 64);
+    sq = bfly_add<16>(sq);
+    sq = bfly_add<32>(sq);
+    l1 = bfly_add<16>(l1);
+    l1 = bfly_add<32>(l1);
     wc.ab2 = tierb_factor(sq, l1, L, a.tierb_delta, a.sm_scale) * kLog2e;
     // with two tokens per lane, lanes r + 8 hold tokens of head r
     if constexpr (HALF) wc.ab2 = dpp_from_lower8(wc.ab2, wc.ab2);
@@ -1146,7 +1148,7 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
     // rotate-half: lanes g and g ^ 2 hold the two halves of the same pairs
     if (!a.interleaved) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) pb[k] += __shfl_xor(pb[k], 32, 64);
+      for (int k = 0; k < 8; ++k) pb[k] = bfly_add<32>(pb[k]);
     }
     if (a.interleaved || g < 2) {
 #pragma unroll
@@ -1305,29 +1307,29 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
 
   // ---- merge the four waves of the workgroup, write one partial record ----
   if constexpr (HALF) {   // lanes r and r + 8 hold different tokens of head r
-    st.l += __shfl_xor(st.l, 8, 64);
-    if constexpr (METER) st.n += __shfl_xor(st.n, 8, 64);
-    if constexpr (KIND == WC_KIND_INT8_DITHER) st.wsum += __shfl_xor(st.wsum, 8, 64);
+    st.l = bfly_add<8>(st.l);
+    if constexpr (METER) st.n = bfly_add<8>(st.n);
+    if constexpr (KIND == WC_KIND_INT8_DITHER) st.wsum = bfly_add<8>(st.wsum);
     if constexpr (VM) {
-      st.ev += __shfl_xor(st.ev, 8, 64);
-      st.vmax = fmaxf(st.vmax, __shfl_xor(st.vmax, 8, 64));
+      st.ev = bfly_add<8>(st.ev);
+      st.vmax = bfly_max<8>(st.vmax);
     }
   }
   if constexpr (VM) {
-    st.ev += __shfl_xor(st.ev, 16, 64);
-    st.ev += __shfl_xor(st.ev, 32, 64);
-    st.vmax = fmaxf(st.vmax, __shfl_xor(st.vmax, 16, 64));
-    st.vmax = fmaxf(st.vmax, __shfl_xor(st.vmax, 32, 64));
+    st.ev = bfly_add<16>(st.ev);
+    st.ev = bfly_add<32>(st.ev);
+    st.vmax = bfly_max<16>(st.vmax);
+    st.vmax = bfly_max<32>(st.vmax);
   }
-  st.l += __shfl_xor(st.l, 16, 64);
-  st.l += __shfl_xor(st.l, 32, 64);
+  st.l = bfly_add<16>(st.l);
+  st.l = bfly_add<32>(st.l);
   if constexpr (METER) {
-    st.n += __shfl_xor(st.n, 16, 64);
-    st.n += __shfl_xor(st.n, 32, 64);
+    st.n = bfly_add<16>(st.n);
+    st.n = bfly_add<32>(st.n);
   }
   if constexpr (KIND == WC_KIND_INT8_DITHER) {
-    st.wsum += __shfl_xor(st.wsum, 16, 64);
-    st.wsum += __shfl_xor(st.wsum, 32, 64);
+    st.wsum = bfly_add<16>(st.wsum);
+    st.wsum = bfly_add<32>(st.wsum);
   }
   const float wsum = st.wsum;
   // rows 4g+e of tile jt hold channel 8(4g+e)+jt = 32g + 8e + jt

@@ -58,6 +58,16 @@ struct MaxOp {
   __device__ float operator()(float a, float b) const { return fmaxf(a, b); }
 };
 
+// x plus, or the max of x and, the value of lane i ^ O.
+template <int O>
+__device__ __forceinline__ float bfly_add(float x) {
+  return butterfly<O>(x, AddOp{});
+}
+template <int O>
+__device__ __forceinline__ float bfly_max(float x) {
+  return butterfly<O>(x, MaxOp{});
+}
+
 // One butterfly step of the weighted scalars' sums (and the value norms' max).
 template <bool METER, bool VM, int O>
 __device__ __forceinline__ void reduce_step(float& dl, float& dn, float& de, float& dv) {
