@@ -833,14 +833,23 @@ __device__ __forceinline__ void step_write(const DecodeArgs& a, int b, int kv, i
 
 // REP: the cache carries repair marks (a.repaired set; a quantized kind), a
 // separate instantiation so that caches without marks run the loop unchanged.
-// The workgroup's LDS: the dither rows of a page (INT8 caches), the query band
-// norms, the waves' output rows and scalars for the in-workgroup merge, the
-// queries (bf16 rows of 256 bytes, +16 pad) and the certified step's gate flag.
+// The workgroup's LDS.  Per wave, one region that holds in turn its query band
+// norms (prologue), a page's dither rows (INT8 caches, page loop) and its output
+// rows for the in-workgroup merge (epilogue): only that wave touches it, in that
+// order.  Then the waves' scalars for the merge, the queries (bf16 rows of 256
+// bytes, +16 pad) and the certified step's gate flag.
+struct DecodeWaveLds {
+  union {
+    struct {
+      __attribute__((aligned(16))) uint8_t dsh[16 * kRow];
+      float qn[16][16];
+    } loop;
+    __attribute__((aligned(16))) float acc[16][kD];
+  };
+};
 template <int KIND>
 struct DecodeLds {
-  __attribute__((aligned(16))) uint8_t dsh[KIND == WC_KIND_INT8_DITHER ? kWaves : 1][16 * kRow];
-  float qn_s[kWaves][16][16];
-  __attribute__((aligned(16))) float acc_s[kWaves][16][kD];
+  DecodeWaveLds w[kWaves];
   float ml_s[kWaves][16][6];
   uint4 q_lds[16][17];
   int gate_flag_s;
@@ -849,9 +858,6 @@ struct DecodeLds {
 // One workgroup of the decode: linear workgroup index lin (decode_position_at).
 template <int KIND, bool METER, bool HALF, bool TB, bool BYP, bool VM, bool REP, bool GS>
 __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, DecodeLds<KIND>& lds) {
-  auto& dsh = lds.dsh;
-  auto& qn_s = lds.qn_s;
-  auto& acc_s = lds.acc_s;
   auto& ml_s = lds.ml_s;
   auto& q_lds = lds.q_lds;
   int& gate_flag_s = lds.gate_flag_s;
@@ -1153,7 +1159,7 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
     if (a.interleaved || g < 2) {
 #pragma unroll
       for (int k = 0; k < 8; ++k)
-        if (k < nl) qn_s[wave][r][base + k] = pb[k];
+        if (k < nl) lds.w[wave].loop.qn[r][base + k] = pb[k];
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_wave_barrier();
@@ -1165,7 +1171,7 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int band = 8 * (g & 1) + 2 * e2 + j;
-        const float x = band < B ? __builtin_amdgcn_sqrtf(qn_s[wave][r][band]) * nmul : 0.0f;
+        const float x = band < B ? __builtin_amdgcn_sqrtf(lds.w[wave].loop.qn[r][band]) * nmul : 0.0f;
         const _Float16 hi = (_Float16)x;
         hv2[j] = (g < 2) ? hi : (_Float16)(x - (float)hi);
       }
@@ -1186,7 +1192,7 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
   // starting at 2^-14 keeps every fp16 scale's operand a normal number
   st.ve = GS ? -14 : 0;
   st.ev = st.vmax = 0.0f;
-  uint8_t* my_dsh = dsh[KIND == WC_KIND_INT8_DITHER ? wave : 0];
+  uint8_t* my_dsh = lds.w[wave].loop.dsh;
 
   // Two workgroups share each SIMD, and instruction issue favours the older
   // wave, so the later workgroup would finish long after the earlier one, alone
@@ -1344,7 +1350,7 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
       else if constexpr (KIND == WC_KIND_INT8_DITHER)
         v[jt] = fmaf(-kVOff, wsum, v[jt]);
     }
-    float4* dst = reinterpret_cast<float4*>(&acc_s[wave][r][32 * g + 8 * e]);
+    float4* dst = reinterpret_cast<float4*>(&lds.w[wave].acc[r][32 * g + 8 * e]);
     dst[0] = make_float4(v[0], v[1], v[2], v[3]);
     dst[1] = make_float4(v[4], v[5], v[6], v[7]);
   }
@@ -1388,7 +1394,7 @@ __device__ __forceinline__ void decode_block(const DecodeArgs& a, uint32_t lin, 
       float4 sum = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
-        const float4 x = *reinterpret_cast<const float4*>(&acc_s[w][r][32 * g + i]);
+        const float4 x = *reinterpret_cast<const float4*>(&lds.w[w].acc[r][32 * g + i]);
         sum.x = fmaf(fo[w], x.x, sum.x);
         sum.y = fmaf(fo[w], x.y, sum.y);
         sum.z = fmaf(fo[w], x.z, sum.z);
