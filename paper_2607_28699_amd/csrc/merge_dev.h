@@ -90,8 +90,12 @@ __device__ __forceinline__ float butterfly_max(float m) {
 }
 
 // Adds the weighted scalars of one record per lane (one butterfly over the wave).
+// The products are rounded before the butterfly: fused into its first add, lane i
+// would form fma(w_i, y_i, w_j y_j) and lane j fma(w_j, y_j, w_i y_i), and the two
+// halves of each pair would then hold sums one ulp apart.
 template <bool METER, bool VM>
 __device__ __forceinline__ void reduce_stats(SplitStats& s, float w, const float4& t, float tv) {
+#pragma clang fp contract(off)
   float dl = w * t.y, dn = METER ? w * t.z : 0.0f, de = VM ? w * t.w : 0.0f, dv = tv;
   reduce_step<METER, VM, 1>(dl, dn, de, dv);
   reduce_step<METER, VM, 2>(dl, dn, de, dv);
@@ -120,6 +124,32 @@ __device__ __forceinline__ SplitStats stats_of_lanes(float4 t, float tv, int ns,
   s.M = butterfly_max(t.x);
   const float w = t.x == -INFINITY ? 0.0f : __expf(t.x - s.M);
   reduce_stats<METER, VM>(s, w, t, tv);
+  return s;
+}
+
+// stats_of_lanes for up to 32 splits in each half of the wave (split j at lane j
+// of the half): the butterfly stops at step 16, so each half holds its own
+// records' statistics.  They are the bits stats_of_lanes gives for the same
+// records (its step 32 would only add the other half's zeros and -inf maxima).
+__device__ __forceinline__ SplitStats stats_of_half_lanes(float4 t, int ns, int hl) {
+#pragma clang fp contract(off)
+  SplitStats s{-INFINITY, 0.0f, 0.0f, 0.0f, 0.0f};
+  if (hl >= ns) t = make_float4(-INFINITY, 0.0f, 0.0f, 0.0f);
+  float m = t.x;
+  m = butterfly<1>(m, MaxOp{});
+  m = butterfly<2>(m, MaxOp{});
+  m = butterfly<4>(m, MaxOp{});
+  m = butterfly<8>(m, MaxOp{});
+  s.M = butterfly<16>(m, MaxOp{});
+  const float w = t.x == -INFINITY ? 0.0f : __expf(t.x - s.M);
+  float dl = w * t.y, dn = w * t.z, de = 0.0f, dv = 0.0f;
+  reduce_step<true, false, 1>(dl, dn, de, dv);
+  reduce_step<true, false, 2>(dl, dn, de, dv);
+  reduce_step<true, false, 4>(dl, dn, de, dv);
+  reduce_step<true, false, 8>(dl, dn, de, dv);
+  reduce_step<true, false, 16>(dl, dn, de, dv);
+  s.l += dl;
+  s.n += dn;
   return s;
 }
 
@@ -251,7 +281,32 @@ __device__ __forceinline__ bool unit_gate_wave(const DecodeArgs& a, int b, int k
     if (hh == own) *own_stats = s;
     if (lane == 0) a.gate_mask_q[b * a.n_q + kv * a.group + hh] = g ? 1 : 0;
   };
-  if (a.n_splits <= 64) {
+  if (a.n_splits <= 32) {
+    // two heads at a time, head 2p in lanes 0 .. 31 and head 2p + 1 in lanes 32 .. 63
+    // (split j at lane j of the half); each head's statistics are then read from the
+    // first lane of its half
+    const int hl = lane & 31, jr = min(hl, a.n_splits - 1);
+    float4 t[8];   // (G <= 16; unconditional loads, past the last head its record again)
+#pragma unroll
+    for (int p2 = 0; p2 < 8; ++p2) {
+      const int hc = min(2 * p2 + (lane >> 5), a.group - 1);
+      t[p2] = *reinterpret_cast<const float4*>(base + ((int64_t)hc * a.n_splits + jr) * R + a.head_dim);
+    }
+    auto from_lane = [](const SplitStats& s, int src) {
+      const auto rl = [src](float x) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), src));
+      };
+      return SplitStats{rl(s.M), rl(s.l), rl(s.n), 0.0f, 0.0f};
+    };
+#pragma unroll
+    for (int p2 = 0; p2 < 8; ++p2) {
+      if (2 * p2 < a.group) {
+        const SplitStats s = stats_of_half_lanes(t[p2], ns, hl);
+        decide(from_lane(s, 0), 2 * p2);
+        if (2 * p2 + 1 < a.group) decide(from_lane(s, 32), 2 * p2 + 1);
+      }
+    }
+  } else if (a.n_splits <= 64) {
     const int jr = min(lane, a.n_splits - 1);
     float4 t[16];   // (G <= 16; unconditional loads, past the last head its record again)
 #pragma unroll

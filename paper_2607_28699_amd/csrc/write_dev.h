@@ -50,6 +50,14 @@ __device__ __forceinline__ void int8_scale(float amax, uint16_t& s_bits, float& 
   inv = s > 0.0f ? __fdiv_rn(1.0f, s) : 0.0f;
 }
 
+// Dithered code round(x * inv + xi) (Sec. 4.2): the product is rounded to fp32
+// before the dither is added, never fused with the add into one fma, so that a
+// code next to a half-integer is decided as the quantizer defines it.
+__device__ __forceinline__ float dither_code(float x, float inv, float xi) {
+#pragma clang fp contract(off)
+  return rintf(x * inv + xi);
+}
+
 // Value rows of a token, staged in LDS by the write kernel: the codes (or bf16
 // values of an exact copy) in channel order, stored afterwards by token quads as
 // whole 16-byte pieces of the page (null pointers: stored here, element by element).
@@ -245,8 +253,8 @@ __device__ __forceinline__ int64_t write_token_head(const WriteArgs& a, int64_t 
       const bool byp = BYP && ((bmask >> i) & 1u);
       const float xi = dither_value((words[i >> 2] >> (8 * (i & 3))) & 0xFFu);
       // a bypassed channel quantizes 0 (|xi| < 1/2, so its code is 0)
-      const float ck = rintf(__fadd_rn(__fmul_rn(byp ? 0.0f : k[i], ikk), xi));
-      const float cv = rintf(__fadd_rn(__fmul_rn(v[i], ivv), xi));
+      const float ck = dither_code(byp ? 0.0f : k[i], ikk, xi);
+      const float cv = dither_code(v[i], ivv, xi);
       double rk = stk * (double)(ck - xi) - (double)k[i];                      // khat - k (step of the group)
       if constexpr (BYP)
         if (byp) rk = (double)(float)(_Float16)k[i] - (double)k[i];           // fp16(k) - k

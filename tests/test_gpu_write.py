@@ -154,3 +154,59 @@ def test_witness_round_up_at_fp16_boundaries():
     ref = oq.witness(x.astype(np.float64), xh.astype(np.float64), B, "half")
     got = w.cpu().double().numpy()
     assert np.array_equal(got, ref), np.argwhere(got != ref)[:8]
+
+
+
+def _codes_next_to_half(x, xi):
+    """Rows x [n, d] (float32) whose channels 1.. are moved, where possible, to the
+    float32 next to (sign(xi)/2 - xi) * s at which rounding x * inv to fp32 before
+    adding the dither xi gives code 0 and one fused multiply-add would give +-1
+    (the scaled value is then below 1/2 in magnitude, where its fp32 spacing is finer
+    than that of the sum); channel 0 holds the row's amax, so the scale is the
+    row's.  Returns the rows and the number of channels where the two roundings differ."""
+    x = np.array(x, dtype=np.float32)
+    n, d = x.shape
+    s = oq.int8_scale(x)
+    inv = (1.0 / s).astype(np.float32).astype(np.float64)
+    split = 0
+    steps = np.arange(-64, 65)
+    for r in range(n):
+        for c in range(1, d):
+            x0 = np.float32((np.sign(xi[r, c]) * 0.5 - xi[r, c]) / inv[r])
+            cand = (x0 + steps.astype(np.float32) * np.spacing(np.abs(x0))).astype(np.float32)
+            y = cand.astype(np.float64) * inv[r]                 # exact product
+            unfused = np.rint(np.float32(np.float32(y) + np.float32(xi[r, c])))
+            fused = np.rint(np.float32(y + xi[r, c]))            # y + xi is exact in float64
+            hit = np.flatnonzero(unfused != fused)
+            if len(hit):
+                x[r, c] = cand[hit[0]]
+                split += 1
+    return x, split
+
+
+def test_int8_code_decided_before_the_dither_is_added():
+    """The code 0 / +-1 of a channel whose scaled value x / s lies just off
+    +-1/2 - xi is decided as the quantizer defines it -- x / s rounded to fp32, then
+    the dither added -- not by one fused multiply-add, which there gives +-1 where
+    the definition gives 0: keys and values built so that the two roundings part in
+    about a third of the channels are written bit-exactly as in the oracle."""
+    from oracle.philox import dither_values
+
+    wl = synth.WORKLOADS["tiny-d64-s256"]
+    S.say("[write-int8] codes next to +-1/2")
+    case = S.make_case(wl, [48], permute=True, layer=3)
+    xi = dither_values(case["slots"][0], wl.d, 3, 0, wl.philox_seed())
+    split = 0
+    for name in ("k", "v"):
+        rows = np.clip(case[name][0][:, 0, :], -2.5, 2.5)
+        rows[:, 0] = 3.0
+        rows, n_split = _codes_next_to_half(rows, xi)
+        case[name][0][:, 0, :] = rows
+        split += n_split
+    assert split > 48 * wl.d // 2, split   # a third of the channels sit where the two roundings part
+    cache = S.gpu_cache(case, "int8_dither")
+    ref = S.oracle_write(case, "int8_dither")[0]
+    got = S.read_cache(cache, case["slots"][0])
+    assert np.array_equal(got["k"].astype(np.int64), ref["kcode"]), np.argwhere(got["k"] != ref["kcode"])[:8]
+    assert np.array_equal(got["v"].astype(np.int64), ref["vcode"]), np.argwhere(got["v"] != ref["vcode"])[:8]
+    assert np.array_equal(got["ks"], ref["ks"]) and np.array_equal(got["kw"], ref["kw"])
