@@ -373,6 +373,10 @@ def main():
     # split length of every decode call, balanced over the batch's tokens (the host
     # knows the lengths; equal to the library default for equal lengths)
     ST = wc.split_tokens_for(lay.batch, wl.n_kv, max_len_all, total_tokens=int((lens0 + K + W).sum()))
+    # the speculative step's split: its one launch holds the metered and the exact
+    # workgroups, so about half as many splits fill the GPU once (its workspace needs
+    # no more than the decode split's)
+    ST_SPEC = wc.speculative_split_tokens(lay.batch, wl.n_kv, max_len_all, total_tokens=int((lens0 + K + W).sum()))
     ws = wc.decode_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all, ST)
     ws_step = wc.certified_workspace(lay.batch, wl.n_q, wl.n_kv, wl.d, max_len_all, ST)
     out = torch.empty((lay.batch, wl.n_q, wl.d), dtype=torch.bfloat16, device=dev)
@@ -395,7 +399,8 @@ def main():
             # decide their KV head's gate first; speculative: every KV head, beside the
             # metered decode) and one final merge
             step_call(caches[layer], exact[layer], it["k"], it["v"], st["slots"], it["q"],
-                      table, st["lens"], max_len_all, sm, args.tau, ws=ws_step, split_tokens=ST,
+                      table, st["lens"], max_len_all, sm, args.tau, ws=ws_step,
+                      split_tokens=ST_SPEC if speculative else ST,
                       out=out, meter=meter, raw=raw, mask_q=mask_q, mask_kv=mask_kv, n_gated=counts)
 
     # The step form a serving loop would pick from what it observed: the speculative
@@ -793,7 +798,8 @@ def main():
         "config": {"workload": wl.name, "layers": wl.n_layers, "n_q": wl.n_q, "n_kv": wl.n_kv,
                    "head_dim": wl.d, "bands": wl.bands, "batch": lay.batch,
                    "context": int(lens0.max()), "mean_context": float(lens0.mean()),
-                   "tau": args.tau, "split_tokens": ST, "cache": "int8 dither + fp16 scales + fp16 key witness",
+                   "tau": args.tau, "split_tokens": ST, "step_split_tokens": ST_SPEC if speculative else ST,
+                   "cache": "int8 dither + fp16 scales + fp16 key witness",
                    "fallback": "bf16 exact cache in HBM",
                    "step": ("certified, speculative (exact fallback of every KV head beside the metered decode, "
                             "gate in the final merge)" if speculative else

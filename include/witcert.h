@@ -281,6 +281,20 @@ int wc_decode_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int64
                            int split_tokens);
 
 /*
+ * Tokens per KV split for wc_step_certified_decode_speculative, whose one launch
+ * holds the metered and the exact workgroups of every split (twice a decode's):
+ * as wc_decode_split_tokens with about 256 instead of 512 (sequence, KV head,
+ * split) workgroups, so that the launch fills the GPU's two workgroups per compute
+ * unit once rather than twice with a ragged second round (at 32k tokens x 4
+ * sequences: 2112 tokens, 16 splits, against 1088 for the decode calls).  A
+ * throughput choice only: any split gives results within rounding of any other.
+ * Pass the result as split_tokens to the speculative step and to
+ * wc_certified_workspace_size.  Returns 0 for invalid sizes.
+ */
+int wc_speculative_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int64_t total_tokens,
+                                int split_tokens);
+
+/*
  * Metered decode attention (the read path of the meter loop, Sec. 6).  For each
  * sequence b and query head h (KV head h / (n_q_heads / n_kv_heads)), over the
  * seq_lens[b] tokens whose slots are block_table[b][t/16]*16 + t%16:

@@ -27,6 +27,7 @@ from .api import (  # noqa: F401
     repair_workspace,
     repair_write_back,
     select_outlier_pairs,
+    speculative_split_tokens,
     split_tokens_for,
     tierb_decode_attention,
     tierb_delta_loc,

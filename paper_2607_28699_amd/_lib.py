@@ -20,7 +20,7 @@ WC_BLOCK_TOKENS = 16
 EXPORTS = (
     "wc_strerror", "wc_version", "wc_cache_bytes", "wc_quantize_write", "wc_quantize_write_pair",
     "wc_witness", "wc_select_workspace_size", "wc_select_outlier_pairs", "wc_decode_workspace_size",
-    "wc_decode_split_tokens", "wc_metered_decode_attention",
+    "wc_decode_split_tokens", "wc_speculative_split_tokens", "wc_metered_decode_attention",
     "wc_metered_decode_gate", "wc_step_metered_decode_gate", "wc_step_metered_decode_gate_noalloc",
     "wc_tierb_decode_attention", "wc_tierb_delta_loc", "wc_joint_decode_gate", "wc_gate",
     "wc_exact_decode_attention", "wc_block_repair", "wc_block_repair_workspace_size",
@@ -77,6 +77,7 @@ def lib() -> ctypes.CDLL:
         "wc_decode_workspace_size": (sz, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                           i64, ctypes.c_int]),
         "wc_decode_split_tokens": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, i64, i64, ctypes.c_int]),
+        "wc_speculative_split_tokens": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, i64, i64, ctypes.c_int]),
         "wc_metered_decode_attention": (ctypes.c_int, [cp, vp, ctypes.c_int, ctypes.c_int,
                                                        ctypes.c_int, vp, ctypes.c_int, vp, i64, f32,
                                                        vp, ctypes.c_int, vp, vp, ctypes.c_int, vp,

@@ -223,6 +223,16 @@ def split_tokens_for(batch: int, n_kv: int, max_seq_len: int, split_tokens: int 
     return n
 
 
+def speculative_split_tokens(batch: int, n_kv: int, max_seq_len: int, split_tokens: int = 0,
+                             total_tokens: int = 0) -> int:
+    """Tokens per KV split for step_certified_decode_speculative: about half the
+    decode calls' workgroups per split set, since its one launch holds both decodes'."""
+    n = lib().wc_speculative_split_tokens(batch, n_kv, max_seq_len, total_tokens, split_tokens)
+    if n <= 0:
+        raise _lib.WitCertError("bad split geometry")
+    return n
+
+
 def metered_decode_attention(cache: PagedCache, q: torch.Tensor, block_table: torch.Tensor,
                              seq_lens: torch.Tensor, max_seq_len: int, sm_scale: float,
                              out_dtype=torch.float32, split_tokens: int = 0,

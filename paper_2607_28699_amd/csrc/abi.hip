@@ -246,6 +246,15 @@ int wc_decode_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int64
   return wc::choose_split_tokens_total(n_kv_heads, max_seq_len, total_tokens);
 }
 
+int wc_speculative_split_tokens(int batch, int n_kv_heads, int64_t max_seq_len, int64_t total_tokens,
+                                int split_tokens) {
+  if (batch < 0 || n_kv_heads < 1 || max_seq_len < 0 || total_tokens < 0 || split_tokens < 0) return 0;
+  const int64_t target = wc::kDecodeWorkgroups / 2;
+  if (split_tokens > 0 || total_tokens == 0)
+    return wc::choose_split_tokens(batch, n_kv_heads, max_seq_len, split_tokens, target);
+  return wc::choose_split_tokens_total(n_kv_heads, max_seq_len, total_tokens, target);
+}
+
 static int decode_common(const wc_cache* cache, const void* q, int q_dtype, int batch,
                          int n_q_heads, const int32_t* block_table, int max_blocks_per_seq,
                          const int32_t* seq_lens, int64_t max_seq_len, float sm_scale, void* out,

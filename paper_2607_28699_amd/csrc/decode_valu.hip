@@ -705,10 +705,10 @@ hipError_t launch_d(const DecodeArgs& a, bool metered, hipStream_t st) {
 
 }  // namespace
 
-int choose_split_tokens_total(int n_kv, int64_t max_seq_len, int64_t total_tokens) {
-  // about 512 workgroups over all (sequence, KV head) token ranges: a long sequence
-  // gets many splits, a short one one
-  int64_t st = (total_tokens * n_kv + 511) / 512;
+int choose_split_tokens_total(int n_kv, int64_t max_seq_len, int64_t total_tokens, int64_t target) {
+  // about `target` workgroups over all (sequence, KV head) token ranges: a long
+  // sequence gets many splits, a short one one
+  int64_t st = (total_tokens * n_kv + target - 1) / target;
   st = (st + 63) / 64 * 64;
   if (st < 256) st = 256;
   const int64_t cap = (max_seq_len + 63) / 64 * 64;
@@ -716,11 +716,10 @@ int choose_split_tokens_total(int n_kv, int64_t max_seq_len, int64_t total_token
   return (int)st;
 }
 
-int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested) {
+int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested, int64_t target) {
   if (requested > 0) return (requested + 63) / 64 * 64;
-  // about two 256-thread workgroups per compute unit over the longest sequence
+  // about `target` workgroups over the longest sequence
   const int64_t units = (int64_t)batch * n_kv;
-  const int64_t target = 512;
   int64_t splits = target / (units > 0 ? units : 1);
   if (splits < 1) splits = 1;
   int64_t st = (max_seq_len + splits - 1) / splits;

@@ -230,10 +230,16 @@ struct GateArgs {
   float tau;
 };
 
-// Tokens per KV split chosen by the library (multiple of 64).
-int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested);
+// Tokens per KV split chosen by the library (multiple of 64): about `target`
+// (sequence, KV head, split) workgroups -- 512, two per compute unit, for the decode
+// calls; 256 for the speculative certified step, whose one launch holds twice the
+// workgroups of a decode.
+constexpr int64_t kDecodeWorkgroups = 512;
+int choose_split_tokens(int batch, int n_kv, int64_t max_seq_len, int requested,
+                        int64_t target = kDecodeWorkgroups);
 // The same, balanced over the batch's total tokens (ragged batches).
-int choose_split_tokens_total(int n_kv, int64_t max_seq_len, int64_t total_tokens);
+int choose_split_tokens_total(int n_kv, int64_t max_seq_len, int64_t total_tokens,
+                              int64_t target = kDecodeWorkgroups);
 inline int64_t n_splits_for(int64_t max_seq_len, int split_tokens) {
   return max_seq_len <= 0 ? 1 : (max_seq_len + split_tokens - 1) / split_tokens;
 }

@@ -142,6 +142,24 @@ def test_split_tokens_query(L):
     assert L.wc_decode_split_tokens(64, 4, 32768, 496384, 0) == 3904
 
 
+def test_speculative_split_tokens_query(L):
+    """The speculative step's split: about 256 workgroups per decode instead of 512
+    (its one launch holds both decodes' workgroups), so about twice the decode
+    calls' split where that split is not at its floor of 256 tokens; an explicit
+    request is rounded as for the decode calls."""
+    # 32k x 4 sequences, 4 KV heads: 16 splits of 2112 tokens (512 workgroups in
+    # the step's launch) against 31 of 1088
+    assert L.wc_decode_split_tokens(4, 4, 32770, 4 * 32770, 0) == 1088
+    assert L.wc_speculative_split_tokens(4, 4, 32770, 4 * 32770, 0) == 2112
+    assert L.wc_speculative_split_tokens(4, 4, 32770, 0, 0) == 2112
+    for batch, n_kv, s in ((4, 4, 32769), (1, 4, 131072), (8, 4, 4096), (64, 4, 32768), (1, 1, 10)):
+        st, sp = L.wc_decode_split_tokens(batch, n_kv, s, 0, 0), L.wc_speculative_split_tokens(batch, n_kv, s, 0, 0)
+        assert sp >= 256 and sp % 64 == 0 and st <= sp <= 2 * st + 64, (batch, n_kv, s, st, sp)
+    assert L.wc_speculative_split_tokens(4, 4, 32769, 0, 100) == 128
+    assert L.wc_speculative_split_tokens(4, 0, 100, 0, 0) == 0
+    assert L.wc_speculative_split_tokens(-1, 4, 100, 0, 0) == 0
+
+
 def test_group_scale_and_repair_argument_checks(L):
     # group scales: a flag of 0 or 1, INT8 only
     c = _lib.WcCache(0, 128, 1, 8, 0, 0, 1, 0, 16, 16, 16, 16, 16, 0, 2, None, None, None, None)

@@ -106,9 +106,11 @@ def test_fullsize_sampled_cells(name):
     rng = np.random.default_rng(17)
     seqs = sorted({int(np.argmin(lens0)), int(np.argmax(lens0)), int(rng.integers(len(lens0)))})
     cells = [(b, int(rng.integers(wl.n_q))) for b in seqs]
+    oracle_cells = {}
     for b, h in cells:
         S.say(f"  cell b={b} h={h} L={int(lens0[b]) + 1} split={st}")
         res, tv, kc, vc, ks = _cell_check(wl, kv, q, b, h, layer)
+        oracle_cells[(b, h)] = (res, tv)
         assert S.rel_err(out[b, h], res["out"][0]) <= 2e-3
         assert abs(raw[b, h] - res["raw"][0]) <= 2e-3 * res["raw"][0]
         assert meter[b, h] >= tv[0]
@@ -158,6 +160,27 @@ def test_fullsize_sampled_cells(name):
     for x, y in zip(s_res, (c_out, c_meter, c_raw, c_mq, c_mk)):
         y = y if isinstance(y, np.ndarray) else y.cpu().numpy()
         assert np.array_equal(x.cpu().numpy(), y)
+    # and at the split bench.py gives that form (about half the decode calls'
+    # workgroups per split set): the sampled cells against the oracle, the gate as a
+    # function of its own meter
+    st_s = wc.speculative_split_tokens(len(lens0), wl.n_kv, max_len, total_tokens=int((lens0 + max_len - lens0.max()).sum()))
+    S.say(f"  speculative split {st_s} (decode split {st})")
+    s_out, s_meter, s_raw, s_mq, s_mk = (x.cpu().numpy() for x in wc.step_certified_decode_speculative(
+        cache, exact, nk, nv, ns, q, tab, lens, max_len, sm, tau, split_tokens=st_s, ws=ws))
+    assert np.array_equal(s_mq, (s_meter > tau).astype(np.uint8))
+    assert np.array_equal(s_mk, s_mq.reshape(len(lens0), wl.n_kv, wl.group).max(-1))
+    for (b, h), (res, tv) in oracle_cells.items():
+        assert abs(s_raw[b, h] - res["raw"][0]) <= 2e-3 * res["raw"][0]
+        assert s_meter[b, h] >= tv[0]
+        if s_mk[b, h // wl.group]:
+            k, v, _ = kv[b]
+            g = h // wl.group
+            want = odec.exact_decode(q[b, h:h + 1].float().cpu().numpy().astype(np.float64),
+                                     k[:, g:g + 1].float().cpu().numpy().astype(np.float64),
+                                     v[:, g:g + 1].float().cpu().numpy().astype(np.float64), sm)["out"][0]
+        else:
+            want = res["out"][0]
+        assert S.rel_err(s_out[b, h], want) <= 2e-3, (b, h)
 
 
 def test_matrix_core_and_vector_paths_agree():
