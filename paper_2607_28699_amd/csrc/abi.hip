@@ -91,7 +91,7 @@ const char* wc_strerror(int status) {
   }
 }
 
-int wc_version(void) { return 105; }   // 1.5: speculative certified step
+int wc_version(void) { return 106; }   // 1.6: the speculative step's split query
 
 size_t wc_cache_bytes(int kind, int64_t num_blocks, int n_kv_heads, int head_dim, int n_bands,
                       int n_outlier_pairs, int value_side, int group_scales, size_t sizes[8]) {
